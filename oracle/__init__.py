@@ -1,0 +1,223 @@
+"""Double-precision CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Only `tests/`, `__graft_entry__.smoke()` and the CPU-baseline leg of
+`bench.py` may import this package.  The product path (the HIP library and its
+Python binding) never imports it, and it imports nothing from the product.
+
+Contents
+  forward(...)          plain complex128 statevector forward pass (C, OpenMP
+                        over samples): Sec. 3 and Algorithm 1.
+  vjp(...)              exact vector-Jacobian product by stored states and
+                        explicit derivative matrices (Sec. 3 "Gate Application
+                        and Differentiation").
+  param_shift_grad(...) gradients from forward passes only (two-term shift rule,
+                        exact for R_P(t) = exp(-i t P/2)); independent of vjp.
+  fd_grad(...)          central finite differences (the paper's FD policy,
+                        Sec. 4.2.3), independent of vjp.
+  loss_cotangent(...)   d loss / d E for the scalar objectives of the
+                        workloads (mean of <Z>, sum, MSE heads; Sec. 4.2.3).
+  dense                 a second, independent forward by dense 2^n x 2^n
+                        matrices built with matrix exponentials (n <= 8).
+
+Ops are any objects with `.kind`, `.wires`, `.angles` in the backend-neutral
+gate-list format of the workload generator.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "vqc_oracle.c")
+_BUILD = os.path.join(_HERE, "_build")
+_LIB_PATH = os.path.join(_BUILD, "liboracle.so")
+
+_KIND = {"RX": 0, "RY": 1, "RZ": 2, "ROT": 3, "CNOT": 4, "CZ": 5}
+_SRC_CODE = {"param": 0, "input": 1, "const": 2}
+_NANG = {"RX": 1, "RY": 1, "RZ": 1, "ROT": 3, "CNOT": 0, "CZ": 0}
+
+OP_DTYPE = np.dtype([("kind", np.int32), ("w0", np.int32), ("w1", np.int32),
+                     ("src", np.int32, 3), ("idx", np.int32, 3),
+                     ("pad", np.int32), ("val", np.float64, 3)], align=True)
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain C99, OpenMP, no fast-math)."""
+    os.makedirs(_BUILD, exist_ok=True)
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        cmd = ["gcc", "-std=c99", "-O2", "-fopenmp", "-fPIC", "-shared",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def open_library(path: str):
+    """Load an oracle build at `path` and declare its entry points."""
+    lib = ctypes.CDLL(path)
+    dp = ctypes.POINTER(ctypes.c_double)
+    lib.oracle_forward.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                   ctypes.c_int, dp, ctypes.c_int, dp,
+                                   ctypes.c_int, dp, dp, ctypes.c_int,
+                                   ctypes.c_int, ctypes.c_double, ctypes.c_int]
+    lib.oracle_forward.restype = ctypes.c_int
+    lib.oracle_vjp.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                               ctypes.c_int, dp, ctypes.c_int, dp, ctypes.c_int,
+                               dp, dp, dp, dp, ctypes.c_int]
+    lib.oracle_vjp.restype = ctypes.c_int
+    lib.oracle_op_size.restype = ctypes.c_int
+    assert lib.oracle_op_size() == OP_DTYPE.itemsize, "oracle_op layout mismatch"
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        _lib = open_library(_LIB_PATH)
+    return _lib
+
+
+def encode_ops(ops: Sequence) -> np.ndarray:
+    rec = np.zeros(max(1, len(ops)), dtype=OP_DTYPE)
+    for k, op in enumerate(ops):
+        rec[k]["kind"] = _KIND[op.kind]
+        w = list(op.wires) + [-1]
+        rec[k]["w0"], rec[k]["w1"] = w[0], w[1]
+        for s, (src, v) in enumerate(op.angles):
+            rec[k]["src"][s] = _SRC_CODE[src]
+            if src == "const":
+                rec[k]["val"][s] = float(v)
+            else:
+                rec[k]["idx"][s] = int(v)
+    return rec
+
+
+def _dptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _as2d(a, B, width):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float64).reshape(B, width))
+    if a.size == 0:
+        a = np.zeros((B, max(width, 1)), dtype=np.float64)
+    return a
+
+
+def forward(ops, n, params, inputs, want_state=False, shift=None, nthreads=0):
+    """E [B, n] (float64); with want_state also the final states [B, 2^n] c128.
+
+    params [B, P] and inputs [B, F] are taken as given (float32 values are
+    upcast exactly).  shift = (op_index, angle_slot, delta) offsets one angle
+    of one gate in every sample.
+    """
+    lib = _load()
+    params = np.asarray(params)
+    inputs = np.asarray(inputs)
+    B = params.shape[0]
+    P = params.shape[1] if params.ndim == 2 else 0
+    F = inputs.shape[1] if inputs.ndim == 2 else 0
+    p = _as2d(params, B, P)
+    x = _as2d(inputs, B, F)
+    rec = encode_ops(ops)
+    E = np.zeros((B, n), dtype=np.float64)
+    st = np.zeros((B, 1 << n), dtype=np.complex128) if want_state else None
+    so, ss, sd = shift if shift is not None else (-1, 0, 0.0)
+    rc = lib.oracle_forward(rec.ctypes.data, len(ops), n, B, _dptr(p), max(P, 1),
+                            _dptr(x), max(F, 1), _dptr(E),
+                            st.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+                            if st is not None else None,
+                            so, ss, sd, nthreads)
+    if rc != 0:
+        raise ValueError(f"oracle_forward failed ({rc})")
+    return (E, st) if want_state else E
+
+
+def vjp(ops, n, params, inputs, grad_out, nthreads=0):
+    """(dparams [B,P], dinputs [B,F], E [B,n]) in float64 for cotangent grad_out."""
+    lib = _load()
+    params = np.asarray(params)
+    inputs = np.asarray(inputs)
+    B = params.shape[0]
+    P = params.shape[1]
+    F = inputs.shape[1]
+    p = _as2d(params, B, P)
+    x = _as2d(inputs, B, F)
+    g = np.ascontiguousarray(np.asarray(grad_out, dtype=np.float64).reshape(B, n))
+    dp = np.zeros((B, max(P, 1)), dtype=np.float64)
+    dx = np.zeros((B, max(F, 1)), dtype=np.float64)
+    E = np.zeros((B, n), dtype=np.float64)
+    rec = encode_ops(ops)
+    rc = lib.oracle_vjp(rec.ctypes.data, len(ops), n, B, _dptr(p), max(P, 1), _dptr(x),
+                        max(F, 1), _dptr(g), _dptr(dp), _dptr(dx), _dptr(E), nthreads)
+    if rc != 0:
+        raise ValueError(f"oracle_vjp failed ({rc})")
+    return dp[:, :P], dx[:, :F], E
+
+
+def _occurrences(ops):
+    for k, op in enumerate(ops):
+        for s, (src, v) in enumerate(op.angles):
+            if src != "const":
+                yield k, s, src, int(v)
+
+
+def _shift_grad(ops, n, params, inputs, grad_out, delta, coef):
+    params = np.asarray(params)
+    inputs = np.asarray(inputs)
+    B = params.shape[0]
+    g = np.asarray(grad_out, dtype=np.float64).reshape(B, n)
+    dp = np.zeros((B, params.shape[1]))
+    dx = np.zeros((B, inputs.shape[1]))
+    for k, s, src, idx in _occurrences(ops):
+        ep = forward(ops, n, params, inputs, shift=(k, s, +delta))
+        em = forward(ops, n, params, inputs, shift=(k, s, -delta))
+        d = coef * np.sum(g * (ep - em), axis=1)
+        (dp if src == "param" else dx)[:, idx] += d
+    return dp, dx
+
+
+def param_shift_grad(ops, n, params, inputs, grad_out):
+    """Two-term parameter-shift rule per angle occurrence, summed per slot:
+    d f / d t = [f(t + pi/2) - f(t - pi/2)] / 2, exact for exp(-i t P/2)."""
+    return _shift_grad(ops, n, params, inputs, grad_out, np.pi / 2, 0.5)
+
+
+def fd_grad(ops, n, params, inputs, grad_out, h=1e-5):
+    """Central finite differences per angle occurrence, summed per slot."""
+    return _shift_grad(ops, n, params, inputs, grad_out, h, 0.5 / h)
+
+
+def loss_cotangent(kind: str, E: np.ndarray, y=None) -> np.ndarray:
+    """d loss / d E for the workload objectives (float64).
+
+    sum       : L = sum_b sum_i E[b,i]                   -> g = 1
+    mean      : L = sum_b mean_i E[b,i]                  -> g = 1/n
+                (the paper's shared objective, the mean of single-qubit <Z>,
+                 taken per sample)
+    mse_z0    : L = mean_b (E[b,0] - y_b)^2              -> g[b,0] = 2 (E[b,0]-y_b)/B
+    mse_meanz : L = mean_b (mean_i E[b,i] - y_b)^2       -> g[b,i] = 2 (s_b-y_b)/(n B)
+    """
+    E = np.asarray(E, dtype=np.float64)
+    B, n = E.shape
+    g = np.zeros_like(E)
+    if kind == "sum":
+        g[:] = 1.0
+    elif kind == "mean":
+        g[:] = 1.0 / n
+    elif kind == "mse_z0":
+        g[:, 0] = 2.0 * (E[:, 0] - np.asarray(y, dtype=np.float64)) / B
+    elif kind == "mse_meanz":
+        s = E.mean(axis=1)
+        g[:] = (2.0 * (s - np.asarray(y, dtype=np.float64)) / (n * B))[:, None]
+    else:
+        raise ValueError(kind)
+    return g

@@ -1,0 +1,339 @@
+"""Pins of the double-precision oracle against facts fixed by the mathematics.
+
+The paper prints no worked example values, so every pin here comes from a
+closed form, an independent construction or brute force:
+  * Bloch-sphere closed forms (SO(3) rotations, not SU(2) matrices) for
+    product circuits: fixes the rotation conventions, the half angle, the ROT
+    order and which wire a gate acts on (Sec. 3, Algorithm 1);
+  * a dense 2^n x 2^n construction from matrix exponentials (oracle.dense);
+  * classical (basis-state) circuits simulated on one integer: CNOT direction
+    and order;
+  * Heisenberg-picture Z-strings for one entangling layer;
+  * GHZ, norm, |E| <= 1, 2*pi periodicity up to global phase;
+  * gradients: two-term parameter shift and central differences (forward only,
+    the paper's FD policy, Sec. 4.2.3), exact zeros, linearity of the VJP.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2607_11985_amd import workloads as W
+
+TOL = 1e-13
+
+
+# ------------------------------------------------------------- Bloch helper
+
+def _so3(kind, t):
+    c, s = math.cos(t), math.sin(t)
+    if kind == "RX":
+        return np.array([[1, 0, 0], [0, c, -s], [0, s, c]])
+    if kind == "RY":
+        return np.array([[c, 0, s], [0, 1, 0], [-s, 0, c]])
+    return np.array([[c, -s, 0], [s, c, 0], [0, 0, 1]])
+
+
+def bloch_product_z(ops, n, prow, xrow):
+    """<Z_j> for a circuit of one-qubit gates only, by Bloch vectors."""
+    v = [np.array([0.0, 0.0, 1.0]) for _ in range(n)]
+
+    def ang(spec):
+        src, val = spec
+        return float(prow[val]) if src == "param" else float(xrow[val]) if src == "input" else float(val)
+
+    for op in ops:
+        q = op.wires[0]
+        if op.kind == "ROT":
+            phi, th, om = (ang(a) for a in op.angles)
+            v[q] = _so3("RZ", om) @ (_so3("RY", th) @ (_so3("RZ", phi) @ v[q]))
+        else:
+            v[q] = _so3(op.kind, ang(op.angles[0])) @ v[q]
+    return np.array([vq[2] for vq in v]), v
+
+
+def test_single_gate_closed_forms(oracle_mod):
+    ts = np.linspace(-7, 7, 29)
+    for kind in ("RX", "RY"):
+        ops = [W.Op(kind, (0,), (("param", 0),))]
+        E = oracle_mod.forward(ops, 1, ts[:, None], np.zeros((len(ts), 1)))
+        assert np.max(np.abs(E[:, 0] - np.cos(ts))) < TOL
+    ops = [W.Op("RZ", (0,), (("param", 0),))]
+    E = oracle_mod.forward(ops, 1, ts[:, None], np.zeros((len(ts), 1)))
+    assert np.max(np.abs(E[:, 0] - 1.0)) < TOL
+    ops = [W.Op("ROT", (0,), (("param", 0), ("param", 1), ("param", 2)))]
+    rng = np.random.default_rng(1)
+    p = rng.uniform(-7, 7, size=(20, 3))
+    E = oracle_mod.forward(ops, 1, p, np.zeros((20, 1)))
+    assert np.max(np.abs(E[:, 0] - np.cos(p[:, 1]))) < TOL
+
+
+def test_rx_rz_ry_bloch_formula(oracle_mod):
+    # RX(a), RZ(b), RY(c) on |0>: z = cos a cos c - sin a sin b sin c
+    rng = np.random.default_rng(2)
+    p = rng.uniform(-4, 4, size=(40, 3))
+    ops = [W.Op("RX", (0,), (("param", 0),)), W.Op("RZ", (0,), (("param", 1),)),
+           W.Op("RY", (0,), (("param", 2),))]
+    E = oracle_mod.forward(ops, 1, p, np.zeros((40, 1)))
+    a, b, c = p[:, 0], p[:, 1], p[:, 2]
+    ref = np.cos(a) * np.cos(c) - np.sin(a) * np.sin(b) * np.sin(c)
+    assert np.max(np.abs(E[:, 0] - ref)) < TOL
+
+
+@pytest.mark.parametrize("n", [1, 3, 6])
+def test_random_product_circuits_vs_bloch(oracle_mod, n):
+    ops, P, F = W.random_circuit(n, 12 * n, seed=10 + n, kinds=("RX", "RY", "RZ", "ROT"))
+    p, x = W.random_inputs(6, P, F, seed=20 + n)
+    E = oracle_mod.forward(ops, n, p, x)
+    for b in range(6):
+        z, _ = bloch_product_z(ops, n, p[b].astype(np.float64), x[b].astype(np.float64))
+        assert np.max(np.abs(E[b] - z)) < 1e-12
+
+
+# ----------------------------------------------------------- dense checker
+
+@pytest.mark.parametrize("n,seed", [(1, 0), (2, 1), (3, 2), (4, 3), (5, 4)])
+def test_random_circuits_vs_dense(oracle_mod, n, seed):
+    from oracle import dense
+    ops, P, F = W.random_circuit(n, 30, seed=seed)
+    p, x = W.random_inputs(5, P, F, seed=100 + seed)
+    E, st = oracle_mod.forward(ops, n, p, x, want_state=True)
+    Ed, std = dense.forward(ops, n, p, x, want_state=True)
+    assert np.max(np.abs(E - Ed)) < 1e-12
+    assert np.max(np.abs(st - std)) < 1e-12
+
+
+def test_config1_vs_dense(oracle_mod):
+    from oracle import dense
+    w = W.make_config(1)
+    E = oracle_mod.forward(w.ops, w.n_qubits, w.params, w.inputs)
+    Ed = dense.forward(w.ops, w.n_qubits, w.params, w.inputs)
+    assert np.max(np.abs(E - Ed)) < 1e-12
+
+
+@pytest.mark.parametrize("idx", [2, 3, 5])
+def test_small_variants_vs_dense(oracle_mod, idx):
+    """The layer structures of configs 2, 3, 5 at n = 4."""
+    from oracle import dense
+    c = W.CONFIGS[idx]
+    ops, P, F = c["builder"](4, 2)
+    p, x = W.random_inputs(4, P, F, seed=idx)
+    assert np.max(np.abs(oracle_mod.forward(ops, 4, p, x) - dense.forward(ops, 4, p, x))) < 1e-12
+
+
+def test_reupload_variant_vs_dense(oracle_mod):
+    from oracle import dense
+    ops, P, F = W.reupload_circuit(5, 2)
+    p, x = W.random_inputs(4, P, F, seed=44)
+    assert np.max(np.abs(oracle_mod.forward(ops, 5, p, x) - dense.forward(ops, 5, p, x))) < 1e-12
+
+
+# ----------------------------------------------------- classical circuits
+
+def _classical(ops_flip, ops_net, n):
+    x = 0
+    for q in ops_flip:
+        x ^= 1 << q
+    for op in ops_net:
+        c, t = op.wires
+        if (x >> c) & 1:
+            x ^= 1 << t
+    return np.array([1.0 - 2.0 * ((x >> j) & 1) for j in range(n)])
+
+
+@pytest.mark.parametrize("n", [2, 3, 5, 8])
+def test_classical_cnot_networks(oracle_mod, n):
+    rng = np.random.default_rng(n)
+    for trial in range(6):
+        flips = [q for q in range(n) if rng.random() < 0.5]
+        r = int(rng.integers(1, n)) if n > 1 else 0
+        net = W._ring(n, r) + [W.Op("CNOT", tuple(int(v) for v in rng.choice(n, 2, replace=False)))
+                               for _ in range(n)]
+        ops = [W.Op("RX", (q,), (("const", math.pi),)) for q in flips] + net
+        E = oracle_mod.forward(ops, n, np.zeros((1, 1)), np.zeros((1, 1)))
+        assert np.max(np.abs(E[0] - _classical(flips, net, n))) < TOL
+
+
+def test_ghz(oracle_mod):
+    for n in (2, 5, 9):
+        ops = [W.Op("RY", (0,), (("const", math.pi / 2),))] + \
+              [W.Op("CNOT", (i, i + 1)) for i in range(n - 1)]
+        E, st = oracle_mod.forward(ops, n, np.zeros((1, 1)), np.zeros((1, 1)), want_state=True)
+        assert np.max(np.abs(E)) < TOL
+        ref = np.zeros(1 << n, dtype=complex)
+        ref[0] = ref[-1] = 1 / math.sqrt(2)
+        assert np.max(np.abs(st[0] - ref)) < TOL
+
+
+# ------------------------------------------- Heisenberg Z-string closed forms
+
+def _zstrings(net, n):
+    """S_i with C^dagger Z_i C = Z_{S_i} for a CNOT/CZ network C."""
+    out = []
+    for i in range(n):
+        S = 1 << i
+        for op in reversed(net):
+            if op.kind == "CNOT":
+                c, t = op.wires
+                if (S >> t) & 1:
+                    S ^= 1 << c
+        out.append(S)
+    return out
+
+
+@pytest.mark.parametrize("idx,n", [(1, 4), (2, 8), (3, 12), (4, 9), (5, 10)])
+def test_one_layer_closed_forms(oracle_mod, idx, n):
+    c = W.CONFIGS[idx]
+    ops, P, F = c["builder"](n, 1)
+    one_q = [o for o in ops if o.kind not in ("CNOT", "CZ")]
+    net = [o for o in ops if o.kind in ("CNOT", "CZ")]
+    p, x = W.random_inputs(3, P, F, seed=7 * idx)
+    E = oracle_mod.forward(ops, n, p, x)
+    S = _zstrings(net, n)
+    for b in range(3):
+        z, _ = bloch_product_z(one_q, n, p[b].astype(np.float64), x[b].astype(np.float64))
+        ref = np.array([np.prod([z[j] for j in range(n) if (S[i] >> j) & 1]) for i in range(n)])
+        assert np.max(np.abs(E[b] - ref)) < 1e-13
+
+
+def test_hea_one_layer_cosine_product(oracle_mod):
+    """Config-1 structure, one layer: <Z_i> = prod_{j in S_i} cos(x_j + a_j)."""
+    n = 4
+    ops, P, F = W.hea_circuit(n, 1)
+    p, x = W.random_inputs(5, P, F, seed=3)
+    E = oracle_mod.forward(ops, n, p, x)
+    S = _zstrings([o for o in ops if o.kind == "CNOT"], n)
+    a = p[:, 0::2].astype(np.float64)
+    zz = np.cos(x.astype(np.float64) + a)
+    ref = np.array([[np.prod([zz[b, j] for j in range(n) if (S[i] >> j) & 1])
+                     for i in range(n)] for b in range(5)])
+    assert np.max(np.abs(E - ref)) < 1e-13
+
+
+# ----------------------------------------------------------- invariants
+
+def test_norm_and_bounds(oracle_mod):
+    ops, P, F = W.random_circuit(7, 80, seed=5)
+    p, x = W.random_inputs(4, P, F, seed=6)
+    E, st = oracle_mod.forward(ops, 7, p, x, want_state=True)
+    assert np.max(np.abs(np.sum(np.abs(st) ** 2, axis=1) - 1)) < 1e-12
+    assert np.all(np.abs(E) <= 1 + 1e-12)
+
+
+def test_periodicity(oracle_mod):
+    ops, P, F = W.random_circuit(5, 40, seed=8)
+    p, x = W.random_inputs(3, P, F, seed=9)
+    E0 = oracle_mod.forward(ops, 5, p, x)
+    E1 = oracle_mod.forward(ops, 5, p.astype(np.float64) + 2 * math.pi, x.astype(np.float64) - 2 * math.pi)
+    assert np.max(np.abs(E0 - E1)) < 1e-12
+
+
+# ----------------------------------------------------------- gradients
+
+def test_single_qubit_gradient_closed_form(oracle_mod):
+    ts = np.linspace(-3, 3, 13)[:, None]
+    for kind in ("RX", "RY"):
+        ops = [W.Op(kind, (0,), (("param", 0),))]
+        dp, dx, _ = oracle_mod.vjp(ops, 1, ts, np.zeros((13, 1)), np.ones((13, 1)))
+        assert np.max(np.abs(dp[:, 0] + np.sin(ts[:, 0]))) < TOL
+
+
+@pytest.mark.parametrize("n,seed", [(1, 11), (3, 12), (5, 13), (6, 14)])
+def test_vjp_vs_parameter_shift(oracle_mod, n, seed):
+    ops, P, F = W.random_circuit(n, 25, seed=seed, n_params=10, n_inputs=3)
+    p, x = W.random_inputs(4, P, F, seed=seed + 1)
+    g = W.random_cotangent(4, n, seed=seed + 2)
+    dp, dx, _ = oracle_mod.vjp(ops, n, p, x, g)
+    sp, sx = oracle_mod.param_shift_grad(ops, n, p, x, g)
+    assert np.max(np.abs(dp - sp)) < 1e-11
+    assert np.max(np.abs(dx - sx)) < 1e-11
+
+
+@pytest.mark.parametrize("idx", [1, 2])
+def test_config_vjp_vs_parameter_shift(oracle_mod, idx):
+    w = W.make_config(idx)
+    sel = slice(0, 4)
+    E = oracle_mod.forward(w.ops, w.n_qubits, w.params[sel], w.inputs[sel])
+    g = oracle_mod.loss_cotangent(w.loss, E, None)
+    dp, dx, _ = oracle_mod.vjp(w.ops, w.n_qubits, w.params[sel], w.inputs[sel], g)
+    sp, sx = oracle_mod.param_shift_grad(w.ops, w.n_qubits, w.params[sel], w.inputs[sel], g)
+    assert np.max(np.abs(dp - sp)) < 1e-11
+    assert np.max(np.abs(dx - sx)) < 1e-11
+
+
+def test_vjp_vs_central_differences(oracle_mod):
+    ops, P, F = W.random_circuit(4, 30, seed=21)
+    p, x = W.random_inputs(3, P, F, seed=22)
+    g = W.random_cotangent(3, 4, seed=23)
+    dp, dx, _ = oracle_mod.vjp(ops, 4, p, x, g)
+    fp, fx = oracle_mod.fd_grad(ops, 4, p, x, g, h=1e-5)
+    assert np.max(np.abs(dp - fp)) < 1e-7
+    assert np.max(np.abs(dx - fx)) < 1e-7
+
+
+@pytest.mark.parametrize("idx,n,layers", [(1, 4, 2), (2, 5, 3), (3, 5, 2), (4, 4, 3), (5, 5, 2)])
+def test_final_layer_exact_zeros(oracle_mod, idx, n, layers):
+    c = W.CONFIGS[idx]
+    ops, P, F = c["builder"](n, layers)
+    p, x = W.random_inputs(3, P, F, seed=idx)
+    g = W.random_cotangent(3, n, seed=idx)
+    dp, _, _ = oracle_mod.vjp(ops, n, p, x, g)
+    l = layers - 1
+    if c["builder"] in (W.hea_circuit, W.reupload_circuit):
+        zero = [(l * n + i) * 2 + 1 for i in range(n)]       # final-layer RZ
+    else:
+        zero = [(l * n + i) * 3 + 2 for i in range(n)]       # final-layer omega
+    assert np.max(np.abs(dp[:, zero])) < 1e-14
+    nz = [k for k in range(P) if k not in zero]
+    assert np.max(np.abs(dp[:, nz])) > 1e-3
+
+
+def test_vjp_linearity_and_unit_cotangents(oracle_mod):
+    n = 5
+    ops, P, F = W.random_circuit(n, 30, seed=31)
+    p, x = W.random_inputs(2, P, F, seed=32)
+    g1 = W.random_cotangent(2, n, seed=33)
+    g2 = W.random_cotangent(2, n, seed=34)
+    a = oracle_mod.vjp(ops, n, p, x, g1)
+    b = oracle_mod.vjp(ops, n, p, x, g2)
+    c = oracle_mod.vjp(ops, n, p, x, g1.astype(np.float64) + g2)
+    assert np.max(np.abs(a[0] + b[0] - c[0])) < 1e-13
+    assert np.max(np.abs(a[1] + b[1] - c[1])) < 1e-13
+    tot = sum(oracle_mod.vjp(ops, n, p, x, np.eye(n)[j][None].repeat(2, 0))[0] for j in range(n))
+    ones = oracle_mod.vjp(ops, n, p, x, np.ones((2, n)))[0]
+    assert np.max(np.abs(tot - ones)) < 1e-13
+
+
+def test_vjp_returns_forward_expectations(oracle_mod):
+    ops, P, F = W.random_circuit(4, 20, seed=41)
+    p, x = W.random_inputs(3, P, F, seed=42)
+    E = oracle_mod.forward(ops, 4, p, x)
+    _, _, E2 = oracle_mod.vjp(ops, 4, p, x, np.ones((3, 4)))
+    assert np.max(np.abs(E - E2)) == 0.0
+
+
+# ----------------------------------------------------------- loss heads
+
+@pytest.mark.parametrize("kind", ["sum", "mean", "mse_z0", "mse_meanz"])
+def test_loss_cotangent_vs_differences(oracle_mod, kind):
+    rng = np.random.default_rng(5)
+    B, n = 6, 5
+    E = rng.uniform(-1, 1, size=(B, n))
+    y = rng.uniform(-1, 1, size=B)
+
+    def L(E):
+        if kind == "sum":
+            return E.sum()
+        if kind == "mean":
+            return E.mean(axis=1).sum()
+        if kind == "mse_z0":
+            return np.mean((E[:, 0] - y) ** 2)
+        return np.mean((E.mean(axis=1) - y) ** 2)
+
+    g = oracle_mod.loss_cotangent(kind, E, y)
+    h = 1e-6
+    for b in range(B):
+        for i in range(n):
+            Ep = E.copy(); Ep[b, i] += h
+            Em = E.copy(); Em[b, i] -= h
+            assert abs((L(Ep) - L(Em)) / (2 * h) - g[b, i]) < 1e-8
