@@ -1,0 +1,192 @@
+/*
+ * vqc.h -- C ABI of the batched VQC statevector engine for MI355X (gfx950).
+ *
+ * The library runs the execute phase of compile-once VQC simulation on the GPU:
+ * a static parametrized circuit (one-qubit Pauli rotations RX/RY/RZ, ROT, and
+ * CNOT/CZ entanglers) is compiled once into a device schedule (Sec. 3
+ * "Compile-Once Lowering and Execution"; Algorithm 1, compile phase) and then
+ * applied to B independent 2^n-amplitude complex64 states, each starting in
+ * |0...0> (Algorithm 1, execute phase).  The forward pass returns the per-qubit
+ * Pauli-Z expectations E[b, j] = sum_x (-1)^{x_j} |psi_b[x]|^2 (Algorithm 1,
+ * return statement).  The backward pass returns the exact gradient of
+ * L_b = sum_j g[b, j] E[b, j] with respect to every per-sample parameter and
+ * encoded input (Sec. 3 "Gate Application and Differentiation"), computed by
+ * the adjoint method instead of a stored tape.
+ *
+ * Conventions shared by every entry point
+ *   - Rotations are R_P(t) = exp(-i t P / 2); ROT(phi, theta, omega) is
+ *     RZ(omega) RY(theta) RZ(phi) with phi applied first.  Qubit j is bit j of
+ *     the basis index.  CNOT(c, t) flips t when c is 1; CZ(a, b) negates the
+ *     amplitudes with both bits set.
+ *   - Device arrays are fp32, row-major, contiguous, device-resident and owned
+ *     by the caller; the library never allocates or frees them.  Outputs are
+ *     overwritten, never accumulated.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls only
+ *     enqueue work and return; launch failures return VQC_ERR_HIP, faults
+ *     inside kernels surface at the caller's next synchronisation.
+ *   - Every function returns VQC_OK (0) or a negative status; the message of
+ *     the last failure on the calling thread is vqc_last_error().
+ *   - A compiled circuit is immutable: it may be used from several threads
+ *     and streams at once.
+ */
+#ifndef VQC_H
+#define VQC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VQC_MAX_QUBITS 20
+
+/* status codes */
+#define VQC_OK 0
+#define VQC_ERR_INVALID_ARG -1 /* bad argument: null pointer, bad wire, bad index */
+#define VQC_ERR_UNSUPPORTED -2 /* valid request this build cannot run */
+#define VQC_ERR_TOO_LARGE -3   /* size limits exceeded (qubits, batch, schedule) */
+#define VQC_ERR_WORKSPACE -4   /* workspace missing or smaller than required */
+#define VQC_ERR_HIP -5         /* a HIP runtime call failed */
+#define VQC_ERR_OOM -6         /* the library's own (schedule) allocation failed */
+
+/* gate kinds */
+#define VQC_RX 0
+#define VQC_RY 1
+#define VQC_RZ 2
+#define VQC_ROT 3
+#define VQC_CNOT 4
+#define VQC_CZ 5
+
+/* angle sources */
+#define VQC_SRC_PARAM 0 /* params[b, idx] */
+#define VQC_SRC_INPUT 1 /* inputs[b, idx] */
+#define VQC_SRC_CONST 2 /* val, fixed at compile time (cached, Algorithm 1 compile phase) */
+
+/*
+ * One gate of the static sequence G = {(g_i, w_i, p_i)} (Algorithm 1, compile
+ * phase).  wires[0] is the target of a one-qubit gate, the control of CNOT,
+ * the first qubit of CZ; wires[1] is the CNOT target / second CZ qubit and is
+ * ignored for one-qubit gates.  Angle slot s (0 for RX/RY/RZ; phi, theta,
+ * omega = 0, 1, 2 for ROT) reads src[s]/idx[s]/val[s].
+ */
+typedef struct {
+    int32_t kind;
+    int32_t wires[2];
+    int32_t src[3];
+    int32_t idx[3];
+    float val[3];
+} vqc_op;
+
+typedef struct vqc_circuit vqc_circuit;
+
+/* compile options (pass NULL for the defaults) */
+#define VQC_PATH_AUTO 0     /* resident for n <= 14, streaming above */
+#define VQC_PATH_RESIDENT 1 /* one launch, state on chip; requires n <= 14 */
+#define VQC_PATH_STREAM 2   /* tiles of 2^14 amplitudes streamed through HBM */
+typedef struct {
+    int32_t device;      /* HIP device that receives the schedule; -1 = plan on
+                            the host only (validation and introspection; the
+                            handle cannot run) */
+    int32_t path;        /* VQC_PATH_* */
+    int32_t reserved[6]; /* must be zero */
+} vqc_compile_opts;
+
+/*
+ * vqc_compile -- validate a static gate list and build its device schedule
+ * (Algorithm 1, compile phase: parse, cache constant gates, classify static
+ * vs parametric).  ops: host array of n_ops gates (n_ops >= 0).  n_qubits in
+ * [1, VQC_MAX_QUBITS].  n_params, n_inputs >= 0 are the row widths P and F of
+ * the params/inputs arrays given at run time.  On success *out receives a
+ * handle that owns only the compiled schedule (host and device copies).
+ * Errors: VQC_ERR_INVALID_ARG (null pointer, wire out of range, CNOT/CZ on one
+ * wire, unknown kind or source, index out of range), VQC_ERR_TOO_LARGE
+ * (qubits or schedule beyond the limits), VQC_ERR_HIP, VQC_ERR_OOM.
+ */
+int vqc_compile(const vqc_op *ops, int32_t n_ops, int32_t n_qubits, int32_t n_params,
+                int32_t n_inputs, const vqc_compile_opts *opts, vqc_circuit **out);
+
+/* Frees the handle and its device schedule.  NULL is ignored. */
+void vqc_destroy(vqc_circuit *c);
+
+/*
+ * vqc_workspace_bytes -- device workspace a forward (training = 1: the saved
+ * final states for the backward pass, plus the backward's scratch) or an
+ * inference forward (training = 0) needs for `batch` samples.  0 means no
+ * workspace is needed.  Returns (size_t)-1 on invalid arguments.
+ */
+size_t vqc_workspace_bytes(const vqc_circuit *c, int64_t batch, int32_t training);
+
+/*
+ * vqc_forward -- E = expectations of the circuit for `batch` samples.
+ *   params   [batch, P] fp32 (may be NULL when P == 0)
+ *   inputs   [batch, F] fp32 (may be NULL when F == 0)
+ *   expvals  [batch, n] fp32, written
+ *   workspace / workspace_bytes: NULL/0 for inference when
+ *     vqc_workspace_bytes(c, batch, 0) == 0; for training pass at least
+ *     vqc_workspace_bytes(c, batch, 1) bytes, 256-byte aligned -- the final
+ *     states are saved there for vqc_backward.
+ * batch == 0 is a no-op.  Errors: VQC_ERR_INVALID_ARG, VQC_ERR_WORKSPACE,
+ * VQC_ERR_TOO_LARGE, VQC_ERR_HIP.
+ */
+int vqc_forward(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,
+                float *expvals, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * vqc_backward -- adjoint-method gradient (Sec. 3 "Gate Application and
+ * Differentiation"; exact, same result as reverse-mode AD over the tape).
+ *   grad_out [batch, n] fp32: cotangent g of E
+ *   workspace: the one a training forward with the same circuit, batch,
+ *     params and inputs filled, in stream order before this call.  The saved
+ *     states are left intact (the rest is scratch), so several cotangents may
+ *     be back-propagated from one forward.
+ *   dparams [batch, P], dinputs [batch, F] fp32: written (per-sample
+ *     gradients; a parameter used by several gates receives the sum).  Either
+ *     may be NULL to skip it.
+ * Errors: VQC_ERR_INVALID_ARG, VQC_ERR_WORKSPACE, VQC_ERR_HIP.
+ */
+int vqc_backward(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,
+                 const float *grad_out, void *workspace, size_t workspace_bytes, float *dparams,
+                 float *dinputs, void *stream);
+
+/*
+ * vqc_loss_grad -- cotangent g = dL/dE of a scalar objective over E
+ * (Sec. 4.2.3: the shared objective is the mean of single-qubit <Z>):
+ *   VQC_LOSS_SUM       L = sum_b sum_j E[b,j]                 g = 1
+ *   VQC_LOSS_MEAN      L = sum_b mean_j E[b,j]                g = 1/n
+ *   VQC_LOSS_MSE_Z0    L = mean_b (E[b,0] - y[b])^2           g[b,0] = 2(E[b,0]-y[b])/batch
+ *   VQC_LOSS_MSE_MEANZ L = mean_b (mean_j E[b,j] - y[b])^2    g[b,j] = 2(s_b-y[b])/(n batch)
+ * expvals [batch, n], target y [batch] (NULL for SUM/MEAN), grad_out
+ * [batch, n] written.  Errors: VQC_ERR_INVALID_ARG, VQC_ERR_HIP.
+ */
+#define VQC_LOSS_SUM 0
+#define VQC_LOSS_MEAN 1
+#define VQC_LOSS_MSE_Z0 2
+#define VQC_LOSS_MSE_MEANZ 3
+int vqc_loss_grad(int32_t kind, int64_t batch, int32_t n_qubits, const float *expvals,
+                  const float *target, float *grad_out, void *stream);
+
+/* Introspection of a compiled circuit (host-side values only). */
+typedef struct {
+    int32_t n_qubits, n_params, n_inputs, n_ops;
+    int32_t n_rotations;    /* primitive rotations (ROT counts 3) */
+    int32_t path;           /* VQC_PATH_RESIDENT or VQC_PATH_STREAM */
+    int32_t tile_qubits;    /* qubits held on chip by one workgroup */
+    int32_t threads;        /* workgroup size */
+    int32_t fwd_passes;     /* kernel passes of the forward (1 when resident) */
+    int32_t bwd_passes;     /* kernel passes of the backward */
+    int32_t fwd_exchanges;  /* on-chip layout exchanges in the forward */
+    int32_t bwd_exchanges;  /* on-chip layout exchanges in the backward */
+    int32_t fwd_instructions, bwd_instructions;
+    int32_t lds_bytes_fwd, lds_bytes_bwd;
+    int32_t reserved[8];
+} vqc_info;
+int vqc_circuit_info(const vqc_circuit *c, vqc_info *info);
+
+/* Message of the last failure on the calling thread ("" if none). */
+const char *vqc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VQC_H */

@@ -1,0 +1,126 @@
+"""Torch-facing wrapper of the C ABI: device memory and streams come from torch,
+every computation runs in libvqc.so.
+
+    circ = Circuit(ops, n_qubits, n_params, n_inputs)
+    E = VQCFunction.apply(circ, params, inputs)      # params/inputs: cuda fp32
+    E.sum().backward()                                # adjoint-method gradients
+"""
+from __future__ import annotations
+
+import torch
+
+from . import _lib
+
+_PATHS = {"auto": _lib.VQC_PATH_AUTO, "resident": _lib.VQC_PATH_RESIDENT,
+          "stream": _lib.VQC_PATH_STREAM}
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device):
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _as_rows(x, batch, width, device, name):
+    if width == 0:
+        return None
+    if x is None:
+        raise ValueError(f"{name} is required (width {width})")
+    if x.dtype != torch.float32 or x.device != device or not x.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 tensor on {device}")
+    if tuple(x.shape) != (batch, width):
+        raise ValueError(f"{name} must have shape {(batch, width)}, got {tuple(x.shape)}")
+    return x
+
+
+class Circuit:
+    """A compiled static circuit (compile once, execute many: Sec. 3)."""
+
+    def __init__(self, ops, n_qubits: int, n_params: int, n_inputs: int, device: int = 0,
+                 path: str = "auto"):
+        self.ops = list(ops)
+        self.n = int(n_qubits)
+        self.P = int(n_params)
+        self.F = int(n_inputs)
+        self.device = torch.device("cuda", device)
+        self.handle = _lib.vqc_compile(self.ops, self.n, self.P, self.F, device=device,
+                                       path=_PATHS[path])
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and _lib._lib is not None:
+            _lib.vqc_destroy(h)
+            self.handle = None
+
+    def info(self) -> dict:
+        return _lib.vqc_circuit_info(self.handle)
+
+    def workspace_bytes(self, batch: int, training: bool = True) -> int:
+        return _lib.vqc_workspace_bytes(self.handle, batch, int(training))
+
+    def new_workspace(self, batch: int, training: bool = True):
+        nb = self.workspace_bytes(batch, training)
+        return torch.empty(max(nb, 1), dtype=torch.uint8, device=self.device), nb
+
+    def forward(self, params, inputs, training: bool = False, workspace=None, out=None):
+        """E [B, n]; with training=True also the workspace for backward()."""
+        B = int(params.shape[0]) if params is not None else int(inputs.shape[0])
+        params = _as_rows(params, B, self.P, self.device, "params")
+        inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
+        E = out if out is not None else torch.empty((B, self.n), dtype=torch.float32,
+                                                   device=self.device)
+        ws, nb = None, 0
+        if training or self.workspace_bytes(B, False) > 0:
+            if workspace is None:
+                workspace, nb = self.new_workspace(B, training)
+            else:
+                nb = workspace.numel()
+            ws = workspace
+        _lib.vqc_forward(self.handle, B, _ptr(params), _ptr(inputs), E.data_ptr(), _ptr(ws),
+                         nb, _stream(self.device))
+        return (E, ws) if training else E
+
+    def backward(self, params, inputs, grad_out, workspace, dparams=None, dinputs=None):
+        """Per-sample gradients (dparams [B,P], dinputs [B,F]) of sum(grad_out * E)."""
+        B = int(grad_out.shape[0])
+        params = _as_rows(params, B, self.P, self.device, "params")
+        inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
+        grad_out = _as_rows(grad_out, B, self.n, self.device, "grad_out")
+        if dparams is None:
+            dparams = torch.empty((B, self.P), dtype=torch.float32, device=self.device)
+        if dinputs is None:
+            dinputs = torch.empty((B, self.F), dtype=torch.float32, device=self.device)
+        _lib.vqc_backward(self.handle, B, _ptr(params), _ptr(inputs), grad_out.data_ptr(),
+                          workspace.data_ptr(), workspace.numel(),
+                          dparams.data_ptr() if self.P else None,
+                          dinputs.data_ptr() if self.F else None, _stream(self.device))
+        return dparams, dinputs
+
+
+def loss_grad(kind: str, E, y=None, out=None):
+    """Cotangent dL/dE of a scalar objective, computed on the GPU."""
+    B, n = E.shape
+    g = out if out is not None else torch.empty_like(E)
+    _lib.vqc_loss_grad(_lib.LOSS[kind], B, n, E.data_ptr(), _ptr(y), g.data_ptr(),
+                       _stream(E.device))
+    return g
+
+
+class VQCFunction(torch.autograd.Function):
+    """E = circuit(params, inputs) with adjoint-method backward."""
+
+    @staticmethod
+    def forward(ctx, circuit: Circuit, params, inputs):
+        E, ws = circuit.forward(params, inputs, training=True)
+        ctx.circuit = circuit
+        ctx.ws = ws
+        ctx.save_for_backward(params, inputs)
+        return E
+
+    @staticmethod
+    def backward(ctx, gE):
+        params, inputs = ctx.saved_tensors
+        dp, dx = ctx.circuit.backward(params, inputs, gE.contiguous(), ctx.ws)
+        return None, dp, dx

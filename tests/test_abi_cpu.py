@@ -1,0 +1,172 @@
+"""C ABI checks that need no GPU: exports, validation and host-only plans.
+
+vqc_compile with device = -1 plans on the host only and makes no HIP call,
+so every validation path of the compile phase is exercised here.
+"""
+import ctypes
+import math
+import re
+
+import pytest
+
+from paper_2607_11985_amd import _lib
+from paper_2607_11985_amd import workloads as W
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def host_compile(ops, n, P, F, path=0, reserved=None, raw=None):
+    arr = raw if raw is not None else _lib.encode_ops(ops)
+    opts = _lib.vqc_compile_opts(device=-1, path=path)
+    if reserved is not None:
+        opts.reserved[0] = reserved
+    return _lib.vqc_compile_raw(arr, len(ops) if raw is None else raw._n, n, P, F, opts)
+
+
+def test_exports_every_declared_function(lib):
+    names = _lib.header_functions()
+    assert {"vqc_compile", "vqc_forward", "vqc_backward", "vqc_destroy",
+            "vqc_workspace_bytes", "vqc_loss_grad", "vqc_last_error",
+            "vqc_circuit_info"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_header_constants_match_binding():
+    text = open(_lib.HEADER).read()
+    defs = dict(re.findall(r"#define\s+(VQC_\w+)\s+(-?\d+)", text))
+    for name in ("VQC_OK", "VQC_ERR_INVALID_ARG", "VQC_ERR_UNSUPPORTED", "VQC_ERR_TOO_LARGE",
+                 "VQC_ERR_WORKSPACE", "VQC_ERR_HIP", "VQC_ERR_OOM"):
+        assert int(defs[name]) == getattr(_lib, name)
+    for k, v in _lib.KIND.items():
+        assert int(defs["VQC_" + k]) == v
+    assert int(defs["VQC_SRC_PARAM"]) == 0 and int(defs["VQC_SRC_CONST"]) == 2
+    assert int(defs["VQC_LOSS_MSE_MEANZ"]) == _lib.LOSS["mse_meanz"]
+    assert ctypes.sizeof(_lib.vqc_op) == 48
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+def test_configs_plan_on_host(idx):
+    w = W.make_config(idx, batch=2)
+    rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    assert rc == 0, _lib.vqc_last_error()
+    info = _lib.vqc_circuit_info(h)
+    rot, ent, nops = W.count_ops(w.ops)
+    assert info["n_rotations"] == rot and info["n_ops"] == nops
+    assert info["path"] == _lib.VQC_PATH_RESIDENT
+    assert info["tile_qubits"] == max(4, w.n_qubits)
+    assert info["lds_bytes_bwd"] <= 160 * 1024
+    # forward and backward sweep each hold one instruction per primitive plus exchanges
+    n_prims = sum(3 if o.kind == "ROT" else 1 for o in w.ops)
+    assert info["fwd_instructions"] == n_prims + info["fwd_exchanges"]
+    assert info["bwd_instructions"] == n_prims + info["bwd_exchanges"]
+    assert _lib.vqc_workspace_bytes(h, 0, 1) == 0
+    assert _lib.vqc_workspace_bytes(h, 10, 0) == 0
+    assert _lib.vqc_workspace_bytes(h, 10, 1) >= 10 * (1 << w.n_qubits) * 8
+    _lib.vqc_destroy(h)
+
+
+def test_host_only_handle_cannot_run(lib):
+    w = W.make_config(1, batch=2)
+    rc, h = host_compile(w.ops, 4, w.n_params, w.n_inputs)
+    assert rc == 0
+    rc = lib.vqc_forward(h, 2, 1, 1, 1, None, 0, None)
+    assert rc == _lib.VQC_ERR_INVALID_ARG and "host-only" in _lib.vqc_last_error()
+    rc = lib.vqc_backward(h, 2, 1, 1, 1, 1, 1 << 20, 1, 1, None)
+    assert rc == _lib.VQC_ERR_INVALID_ARG
+    _lib.vqc_destroy(h)
+
+
+def test_null_handle_and_out(lib):
+    assert lib.vqc_forward(None, 1, None, None, None, None, 0, None) == _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_backward(None, 1, None, None, None, None, 0, None, None, None) == \
+        _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_circuit_info(None, None) == _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_workspace_bytes(None, 1, 1) == ctypes.c_size_t(-1).value
+    lib.vqc_destroy(None)
+    arr = _lib.encode_ops([])
+    opts = _lib.vqc_compile_opts(device=-1)
+    assert lib.vqc_compile(arr, 0, 2, 0, 0, ctypes.byref(opts), None) == _lib.VQC_ERR_INVALID_ARG
+
+
+def _one(kind, wires, angles=()):
+    return [W.Op(kind, wires, angles)]
+
+
+BAD = [
+    ("wire_high", _one("RY", (3,), (("param", 0),)), 3, 1, 0, _lib.VQC_ERR_INVALID_ARG, "wire"),
+    ("wire_negative", _one("RX", (-1,), (("param", 0),)), 3, 1, 0, _lib.VQC_ERR_INVALID_ARG, "wire"),
+    ("cnot_same", _one("CNOT", (1, 1)), 3, 0, 0, _lib.VQC_ERR_INVALID_ARG, "single wire"),
+    ("cz_high", _one("CZ", (0, 5)), 3, 0, 0, _lib.VQC_ERR_INVALID_ARG, "wire"),
+    ("param_range", _one("RZ", (0,), (("param", 4),)), 2, 4, 0, _lib.VQC_ERR_INVALID_ARG, "param"),
+    ("input_range", _one("RZ", (0,), (("input", 1),)), 2, 0, 1, _lib.VQC_ERR_INVALID_ARG, "input"),
+    ("input_negative", _one("RZ", (0,), (("input", -1),)), 2, 0, 1, _lib.VQC_ERR_INVALID_ARG, "input"),
+    ("nan_const", _one("RX", (0,), (("const", math.nan),)), 2, 0, 0, _lib.VQC_ERR_INVALID_ARG, "finite"),
+    ("zero_qubits", [], 0, 0, 0, _lib.VQC_ERR_INVALID_ARG, "n_qubits"),
+    ("too_many_qubits", [], 21, 0, 0, _lib.VQC_ERR_TOO_LARGE, "n_qubits"),
+    ("negative_params", [], 2, -1, 0, _lib.VQC_ERR_INVALID_ARG, "n_params"),
+]
+
+
+@pytest.mark.parametrize("case", BAD, ids=[b[0] for b in BAD])
+def test_compile_rejects(case):
+    _, ops, n, P, F, code, text = case
+    rc, h = host_compile(ops, n, P, F)
+    assert rc == code
+    assert text in _lib.vqc_last_error()
+    assert not h.value
+
+
+def test_compile_rejects_unknown_kind_and_source():
+    arr = _lib.encode_ops(_one("RX", (0,), (("param", 0),)))
+    arr[0].kind = 9
+    rc, _ = _lib.vqc_compile_raw(arr, 1, 2, 1, 0, _lib.vqc_compile_opts(device=-1))
+    assert rc == _lib.VQC_ERR_INVALID_ARG and "kind" in _lib.vqc_last_error()
+    arr = _lib.encode_ops(_one("RX", (0,), (("param", 0),)))
+    arr[0].src[0] = 7
+    rc, _ = _lib.vqc_compile_raw(arr, 1, 2, 1, 0, _lib.vqc_compile_opts(device=-1))
+    assert rc == _lib.VQC_ERR_INVALID_ARG and "source" in _lib.vqc_last_error()
+
+
+def test_compile_rejects_options():
+    rc, _ = host_compile([], 2, 0, 0, reserved=1)
+    assert rc == _lib.VQC_ERR_INVALID_ARG and "reserved" in _lib.vqc_last_error()
+    rc, _ = host_compile([], 2, 0, 0, path=7)
+    assert rc == _lib.VQC_ERR_INVALID_ARG
+    rc, _ = host_compile([], 15, 0, 0, path=_lib.VQC_PATH_RESIDENT)
+    assert rc == _lib.VQC_ERR_UNSUPPORTED
+    arr = _lib.encode_ops([])
+    rc, _ = _lib.vqc_compile_raw(arr, -1, 2, 0, 0, _lib.vqc_compile_opts(device=-1))
+    assert rc == _lib.VQC_ERR_INVALID_ARG
+    rc = _lib.load().vqc_compile(None, 3, 2, 0, 0, ctypes.byref(_lib.vqc_compile_opts(device=-1)),
+                                 ctypes.byref(ctypes.c_void_p()))
+    assert rc == _lib.VQC_ERR_INVALID_ARG
+
+
+def test_loss_grad_validation(lib):
+    assert lib.vqc_loss_grad(9, 4, 2, 1, 1, 1, None) == _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_loss_grad(0, -1, 2, 1, 1, 1, None) == _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_loss_grad(2, 4, 2, 1, None, 1, None) == _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_loss_grad(0, 4, 2, None, None, 1, None) == _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_loss_grad(0, 0, 2, None, None, None, None) == _lib.VQC_OK
+
+
+@pytest.mark.parametrize("n", [1, 2, 4, 5, 8, 11, 14])
+def test_random_circuits_plan(n):
+    ops, P, F = W.random_circuit(n, 60, seed=n)
+    rc, h = host_compile(ops, n, P, F)
+    assert rc == 0, _lib.vqc_last_error()
+    info = _lib.vqc_circuit_info(h)
+    assert info["threads"] == max(64, 1 << (max(n, 4) - 4))
+    _lib.vqc_destroy(h)
+
+
+def test_empty_circuit_plans():
+    rc, h = host_compile([], 3, 0, 0)
+    assert rc == 0
+    info = _lib.vqc_circuit_info(h)
+    assert info["fwd_instructions"] == 0 and info["n_rotations"] == 0
+    _lib.vqc_destroy(h)

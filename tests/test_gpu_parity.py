@@ -1,0 +1,215 @@
+"""GPU parity: the HIP path (through the C ABI) against the double-precision oracle.
+
+Bars (complex64 on the GPU, complex128 in the oracle):
+  E      : max |E - E_ref| <= 1e-5 (absolute)
+  grads  : per sample row, max_p |g - g_ref| <= 1e-4 * max_p |g_ref| + 1e-6 * sum_j |cot_j|
+           (row max-norm relative error; the floor, scaled by the cotangent, only
+           matters for rows whose gradient is all but zero)
+Every input and cotangent is seeded and synthetic and reaches both sides as the
+same float32 values; nothing the oracle sees comes from the GPU.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_11985_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+E_TOL = 1e-5
+G_REL = 1e-4
+G_FLOOR = 1e-6
+
+
+@pytest.fixture(scope="module")
+def torch_mod():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2607_11985_amd import _lib
+    _lib.load()  # fails loudly if the HIP library is not built
+    return torch
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def gpu_run(torch, ops, n, P, F, params, inputs, cot=None, path="auto"):
+    from paper_2607_11985_amd.api import Circuit
+    circ = Circuit(ops, n, P, F, path=path)
+    p = torch.from_numpy(np.ascontiguousarray(params)).cuda()
+    x = torch.from_numpy(np.ascontiguousarray(inputs)).cuda()
+    E, ws = circ.forward(p, x, training=True)
+    out = {"E": None, "dp": None, "dx": None, "circ": circ}
+    if cot is not None:
+        g = torch.from_numpy(np.ascontiguousarray(cot, dtype=np.float32)).cuda()
+        dp, dx = circ.backward(p, x, g, ws)
+        torch.cuda.synchronize()
+        out["dp"], out["dx"] = dp.cpu().numpy(), dx.cpu().numpy()
+    torch.cuda.synchronize()
+    out["E"] = E.cpu().numpy()
+    return out
+
+
+def check_E(E, Eref):
+    err = float(np.max(np.abs(E.astype(np.float64) - Eref))) if E.size else 0.0
+    assert err <= E_TOL, f"E max abs err {err:.3e}"
+    return err
+
+
+def check_grad(g, gref, cot, what):
+    if g.size == 0:
+        return 0.0
+    g = g.astype(np.float64)
+    err = np.max(np.abs(g - gref), axis=1)
+    scale = np.max(np.abs(gref), axis=1)
+    floor = G_FLOOR * np.sum(np.abs(np.asarray(cot, dtype=np.float64)), axis=1)
+    bad = err > G_REL * scale + floor
+    assert not np.any(bad), (f"{what}: rows {np.nonzero(bad)[0][:8]} err {err[bad][:4]} "
+                             f"scale {scale[bad][:4]}")
+    return float(np.max(err / np.maximum(scale, 1e-30)))
+
+
+def samples_per_wg(n):
+    nq = max(n, 4)
+    T = 1 << (nq - 4)
+    return max(1, 64 // T)
+
+
+@pytest.mark.parametrize("n", list(range(1, 15)))
+def test_random_circuit_parity(torch_mod, n):
+    S = samples_per_wg(n)
+    B = 2 * S + 1 if S > 1 else 3
+    n_ops = 40 + 6 * n
+    ops, P, F = W.random_circuit(n, n_ops, seed=1000 + n)
+    params, inputs = W.random_inputs(B, P, F, seed=2000 + n)
+    cot = W.random_cotangent(B, n, seed=3000 + n)
+    note(f"random circuit n={n} B={B} ops={n_ops}")
+    r = gpu_run(torch_mod, ops, n, P, F, params, inputs, cot)
+    dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
+    check_E(r["E"], Er)
+    check_grad(r["dp"], dpr, cot, "dparams")
+    check_grad(r["dx"], dxr, cot, "dinputs")
+
+
+@pytest.mark.parametrize("n", [5, 9, 13])
+def test_entangler_heavy_parity(torch_mod, n):
+    """Dense CNOT/CZ networks between rotations: exercises every exchange layout."""
+    ops, P, F = W.random_circuit(n, 150, seed=77 + n, kinds=("RY", "CNOT", "CZ", "RX", "CNOT"))
+    B = 5
+    params, inputs = W.random_inputs(B, P, F, seed=88 + n)
+    cot = W.random_cotangent(B, n, seed=99 + n)
+    note(f"entangler-heavy n={n}")
+    r = gpu_run(torch_mod, ops, n, P, F, params, inputs, cot)
+    dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
+    check_E(r["E"], Er)
+    check_grad(r["dp"], dpr, cot, "dparams")
+    check_grad(r["dx"], dxr, cot, "dinputs")
+
+
+@pytest.mark.parametrize("idx", [1, 2])
+def test_config_full_batch(torch_mod, idx):
+    w = W.make_config(idx)
+    note(f"config {w.name} full batch {w.batch}")
+    Er = oracle.forward(w.ops, w.n_qubits, w.params, w.inputs)
+    cot = oracle.loss_cotangent(w.loss, Er, w.y).astype(np.float32)
+    r = gpu_run(torch_mod, w.ops, w.n_qubits, w.n_params, w.n_inputs, w.params, w.inputs, cot)
+    dpr, dxr, _ = oracle.vjp(w.ops, w.n_qubits, w.params, w.inputs, cot)
+    check_E(r["E"], Er)
+    check_grad(r["dp"], dpr, cot, "dparams")
+    check_grad(r["dx"], dxr, cot, "dinputs")
+
+
+@pytest.mark.parametrize("idx,rows", [(3, [0, 1, 2047, 4095]), (4, [0, 4097, 8191])])
+def test_config_full_batch_sampled(torch_mod, idx, rows):
+    """Full batch on the GPU in the benchmark's launch configuration; the oracle
+    checks sampled rows (rows are independent).  The MSE cotangent of a sampled
+    row comes from the oracle's own E; other rows get a seeded random cotangent."""
+    w = W.make_config(idx)
+    note(f"config {w.name} full batch {w.batch}, oracle rows {rows}")
+    Er = oracle.forward(w.ops, w.n_qubits, w.params[rows], w.inputs[rows])
+    cot = W.random_cotangent(w.batch, w.n_qubits, seed=5 + idx)
+    g_rows = np.zeros((len(rows), w.n_qubits))
+    for i, b in enumerate(rows):
+        if w.loss == "mse_z0":
+            g_rows[i, 0] = 2.0 * (Er[i, 0] - w.y[b]) / w.batch
+        else:
+            g_rows[i, :] = 2.0 * (Er[i].mean() - w.y[b]) / (w.n_qubits * w.batch)
+    cot[rows] = g_rows.astype(np.float32)
+    r = gpu_run(torch_mod, w.ops, w.n_qubits, w.n_params, w.n_inputs, w.params, w.inputs, cot)
+    assert np.all(np.isfinite(r["E"])) and np.all(np.abs(r["E"]) <= 1 + 1e-5)
+    dpr, dxr, _ = oracle.vjp(w.ops, w.n_qubits, w.params[rows], w.inputs[rows], cot[rows])
+    check_E(r["E"][rows], Er)
+    check_grad(r["dp"][rows], dpr, cot[rows], "dparams")
+    check_grad(r["dx"][rows], dxr, cot[rows], "dinputs")
+
+
+def test_loss_grad_kernel(torch_mod):
+    from paper_2607_11985_amd.api import loss_grad
+    rng = np.random.default_rng(4)
+    for B, n in ((1, 3), (300, 14), (8192, 14), (37, 1)):
+        E = rng.uniform(-1, 1, size=(B, n)).astype(np.float32)
+        y = rng.uniform(-1, 1, size=B).astype(np.float32)
+        for kind in ("sum", "mean", "mse_z0", "mse_meanz"):
+            g = loss_grad(kind, torch_mod.from_numpy(E).cuda(), torch_mod.from_numpy(y).cuda())
+            ref = oracle.loss_cotangent(kind, E.astype(np.float64), y.astype(np.float64))
+            err = np.max(np.abs(g.cpu().numpy() - ref))
+            assert err <= 1e-6 * max(1.0, np.max(np.abs(ref))), (kind, B, n, err)
+
+
+def test_edge_cases(torch_mod):
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit
+    # empty circuit: E = 1, gradients are zero
+    c = Circuit([], 5, 2, 3)
+    p = torch.zeros((4, 2), device="cuda")
+    x = torch.zeros((4, 3), device="cuda")
+    E, ws = c.forward(p, x, training=True)
+    dp, dx = c.backward(p, x, torch.ones((4, 5), device="cuda"), ws)
+    assert torch.all(E == 1) and torch.all(dp == 0) and torch.all(dx == 0)
+    # batch 0 is a no-op
+    E0 = c.forward(torch.zeros((0, 2), device="cuda"), torch.zeros((0, 3), device="cuda"))
+    assert E0.shape == (0, 5)
+    # constants only (P = F = 0)
+    ops = [W.Op("RY", (0,), (("const", 0.7),)), W.Op("CNOT", (0, 2))]
+    c = Circuit(ops, 3, 0, 0)
+    E = c.forward(None, torch.zeros((2, 0), device="cuda"))
+    Er = oracle.forward(ops, 3, np.zeros((2, 1)), np.zeros((2, 1)))
+    check_E(E.cpu().numpy(), Er)
+
+
+def test_backward_twice_and_determinism(torch_mod):
+    torch = torch_mod
+    w = W.make_config(2)
+    cot = W.random_cotangent(w.batch, w.n_qubits, seed=12)
+    a = gpu_run(torch, w.ops, w.n_qubits, w.n_params, w.n_inputs, w.params, w.inputs, cot)
+    b = gpu_run(torch, w.ops, w.n_qubits, w.n_params, w.n_inputs, w.params, w.inputs, cot)
+    assert np.array_equal(a["E"], b["E"])
+    assert np.array_equal(a["dp"], b["dp"]) and np.array_equal(a["dx"], b["dx"])
+    from paper_2607_11985_amd.api import Circuit
+    c = Circuit(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    p = torch.from_numpy(w.params).cuda()
+    x = torch.from_numpy(w.inputs).cuda()
+    g = torch.from_numpy(cot).cuda()
+    E, ws = c.forward(p, x, training=True)
+    d1 = c.backward(p, x, g, ws)
+    d2 = c.backward(p, x, g, ws)
+    assert torch.equal(d1[0], d2[0]) and torch.equal(d1[1], d2[1])
+
+
+def test_autograd_function(torch_mod):
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit, VQCFunction
+    w = W.make_config(1)
+    c = Circuit(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    p = torch.from_numpy(w.params).cuda().requires_grad_(True)
+    x = torch.from_numpy(w.inputs).cuda().requires_grad_(True)
+    E = VQCFunction.apply(c, p, x)
+    E.sum().backward()
+    dpr, dxr, Er = oracle.vjp(w.ops, 4, w.params, w.inputs, np.ones((w.batch, 4)))
+    check_E(E.detach().cpu().numpy(), Er)
+    check_grad(p.grad.cpu().numpy(), dpr, np.ones((w.batch, 4)), "dparams")
+    check_grad(x.grad.cpu().numpy(), dxr, np.ones((w.batch, 4)), "dinputs")
