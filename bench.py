@@ -1,0 +1,210 @@
+"""Throughput of the batched VQC hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+vqc_forward (training: saves the final states) -> vqc_loss_grad (cotangent of
+the workload's objective) -> vqc_backward (adjoint gradients for every
+parameter and input), all on one HIP stream with inputs resident in HBM.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5]
+
+Prints one JSON line.  value = circuit evaluations (forward E + full
+gradient) per second = B * K / timed seconds.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import subprocess
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "circuit evals/sec (fwd+adjoint grad) at n=4..16; % of LDS/HBM BW peak"
+PEAK_FP32_TFLOPS = 157.3     # MI355X fp32 vector peak (packed FMA, 256 CU x 2.4 GHz)
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+DEFAULT_CONFIG = 2
+
+
+def algorithmic_flops(w):
+    """Per-sample flops of the method (gate by gate), forward and backward.
+
+    forward : every rotation updates each amplitude with a 2x2 whose entries are
+              c, s or c +- i s: 6 flops per amplitude; <Z_j> needs |a|^2 (3) and
+              one signed add per qubit (n) per amplitude.
+    backward: lambda = H psi costs n + 2 per amplitude; every rotation costs
+              4 per amplitude for Im<lambda|P|psi> plus 6 on each of psi and
+              lambda to un-apply it (16).  CNOT and CZ are data movement (0).
+    """
+    from paper_2607_11985_amd import workloads as W
+    R, _, _ = W.count_ops(w.ops)
+    N = float(1 << w.n_qubits)
+    n = w.n_qubits
+    return N * (6 * R + 3 + n), N * (16 * R + n + 2)
+
+
+def cpu_baseline(w, budget_s=12.0):
+    """The oracle as it stands (forward, loss cotangent, VJP) on host cores,
+    on a bounded sample of the same workload."""
+    import oracle
+    rows_total = w.batch
+    chunk = max(1, min(rows_total, 64 if w.n_qubits <= 10 else 8 if w.n_qubits <= 12 else 2))
+    done, t0, start = 0, time.perf_counter(), 0
+    while time.perf_counter() - t0 < budget_s:
+        sel = slice(start, start + chunk)
+        E = oracle.forward(w.ops, w.n_qubits, w.params[sel], w.inputs[sel])
+        ycut = w.y[sel] if w.y is not None else None
+        g = oracle.loss_cotangent(w.loss, E, ycut)
+        if w.loss in ("mse_z0", "mse_meanz"):
+            g *= E.shape[0] / w.batch  # the objective averages over the whole batch
+        oracle.vjp(w.ops, w.n_qubits, w.params[sel], w.inputs[sel], g)
+        done += E.shape[0]
+        start = (start + chunk) % rows_total
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": done / dt, "unit": "circuit evals/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} samples of {w.name} (rows taken cyclically in chunks of {chunk}), "
+                      f"{dt:.1f} s, forward + loss cotangent + VJP in complex128"}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=DEFAULT_CONFIG, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this engine runs on one GPU: samples are independent, so a "
+                          "multi-GPU run would shard the batch with no communication; "
+                          "run with --gpus 1"}))
+        sys.exit(2)
+
+    import torch
+    from paper_2607_11985_amd import _lib, workloads as W
+    from paper_2607_11985_amd.api import Circuit
+
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2607_11985_amd.build import build_library
+        build_library()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = W.make_config(args.config)
+    B, n = w.batch, w.n_qubits
+    circ = Circuit(w.ops, n, w.n_params, w.n_inputs, device=0)
+    info = circ.info()
+    p = torch.from_numpy(w.params).to(dev)
+    x = torch.from_numpy(w.inputs).to(dev)
+    y = torch.from_numpy(w.y).to(dev) if w.y is not None else None
+    E = torch.empty((B, n), dtype=torch.float32, device=dev)
+    g = torch.empty_like(E)
+    dp = torch.empty((B, w.n_params), dtype=torch.float32, device=dev)
+    dx = torch.empty((B, w.n_inputs), dtype=torch.float32, device=dev)
+    ws, nb = circ.new_workspace(B, training=True)
+    stream = torch.cuda.current_stream(dev)
+    s = stream.cuda_stream
+    h = circ.handle
+    loss_kind = _lib.LOSS[w.loss]
+    pp, xp, yp = p.data_ptr(), x.data_ptr(), (y.data_ptr() if y is not None else None)
+
+    def fwd():
+        _lib.vqc_forward(h, B, pp, xp, E.data_ptr(), ws.data_ptr(), nb, s)
+
+    def loss():
+        _lib.vqc_loss_grad(loss_kind, B, n, E.data_ptr(), yp, g.data_ptr(), s)
+
+    def bwd():
+        _lib.vqc_backward(h, B, pp, xp, g.data_ptr(), ws.data_ptr(), nb, dp.data_ptr(),
+                          dx.data_ptr(), s)
+
+    for _ in range(args.warmup):
+        fwd(); loss(); bwd()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(K):
+        e = ev[k]
+        e[0].record(stream); fwd()
+        e[1].record(stream); loss()
+        e[2].record(stream); bwd()
+        e[3].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    loss_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+    ms_per_step = total_ms / K
+    value = B * K / (total_ms / 1e3)
+
+    # forward-only rate (inference, no state saved), outside the timed region
+    for _ in range(3):
+        circ.forward(p, x, out=E)
+    torch.cuda.synchronize()
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record(stream)
+    for _ in range(K):
+        circ.forward(p, x, out=E)
+    a1.record(stream)
+    torch.cuda.synchronize()
+    inf_ms = a0.elapsed_time(a1) / K
+
+    f_fwd, f_bwd = algorithmic_flops(w)
+    dominant = "backward" if bwd_ms >= fwd_ms else "forward"
+    dom_ms = bwd_ms if dominant == "backward" else fwd_ms
+    flops = (f_bwd if dominant == "backward" else f_fwd) * B
+    achieved = flops / (dom_ms / 1e3) / 1e12
+    roofline = {"bound": "alu", "kernel": f"resident_kernel ({dominant})", "achieved": achieved,
+                "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS,
+                "traffic": None,
+                "flops_per_launch": flops, "avg_launch_ms": dom_ms}
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "circuit evals/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "c64",
+        "data": "synthetic (seeded draws of the configuration; no dataset)",
+        "config": {"workload": w.name, "description": w.description, "n_qubits": n, "batch": B,
+                   "n_params": w.n_params, "n_inputs": w.n_inputs, "ops": len(w.ops),
+                   "loss": w.loss, "path": "resident" if info["path"] == 1 else "stream",
+                   "threads_per_workgroup": info["threads"],
+                   "exchanges_fwd_bwd": [info["fwd_exchanges"], info["bwd_exchanges"]]},
+        "kernel_ms": {"forward_train": fwd_ms, "loss_grad": loss_ms, "backward": bwd_ms,
+                      "forward_inference": inf_ms},
+        "forward_only_evals_per_s": B / (inf_ms / 1e3),
+        "roofline": roofline,
+        "env": {"torch": torch.__version__, "hip": getattr(torch.version, "hip", None),
+                "gpu": torch.cuda.get_device_name(dev), "host_cpu": cpu_model(),
+                "host_cores": os.cpu_count()},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+        out["gpu_over_cpu"] = value / out["cpu_baseline"]["value"]
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -18,8 +18,13 @@ SOURCES = ["api.cpp", "planner.cpp", "kernels.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed-FP32 instructions are disabled for every device compilation.
+# SimplifyCFG must not sink / hoist the near-identical cases of the register-
+# position switches into one block: the merged block selects between the
+# amplitude variables through pointers, which pins the whole register tile in
+# scratch memory.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
-                "-packed-fp32-ops"]
+                "-packed-fp32-ops", "-mllvm", "-simplifycfg-sink-common=false",
+                "-mllvm", "-simplifycfg-hoist-common=false"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
 
 

@@ -24,80 +24,95 @@
 namespace vqc {
 namespace {
 
-typedef float2 Amp;
+// A thread's 16 amplitudes as plain scalars (real and imaginary parts kept in
+// separate arrays so every access has a constant index and stays in VGPRs).
+struct St {
+  float r[kRegAmps];
+  float i[kRegAmps];
+};
 
 // ------------------------------------------------------------------ gates
 // R_P(t) = exp(-i t P / 2) with c = cos(t/2), s = sin(t/2); the adjoint uses -s.
 
 template <int P>
-__device__ __forceinline__ void rx_reg(Amp (&a)[kRegAmps], float c, float s) {
+__device__ __forceinline__ void rx_reg(St& a, float c, float s) {
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    if (i & (1 << P)) continue;
-    const int j = i | (1 << P);
-    const Amp x = a[i], y = a[j];
+  for (int u = 0; u < kRegAmps; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
     // [c, -is; -is, c]
-    a[i] = make_float2(c * x.x + s * y.y, c * x.y - s * y.x);
-    a[j] = make_float2(s * x.y + c * y.x, c * y.y - s * x.x);
+    a.r[u] = c * xr + s * yi;
+    a.i[u] = c * xi - s * yr;
+    a.r[v] = c * yr + s * xi;
+    a.i[v] = c * yi - s * xr;
   }
 }
 
 template <int P>
-__device__ __forceinline__ void ry_reg(Amp (&a)[kRegAmps], float c, float s) {
+__device__ __forceinline__ void ry_reg(St& a, float c, float s) {
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    if (i & (1 << P)) continue;
-    const int j = i | (1 << P);
-    const Amp x = a[i], y = a[j];
+  for (int u = 0; u < kRegAmps; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
     // [c, -s; s, c]
-    a[i] = make_float2(c * x.x - s * y.x, c * x.y - s * y.y);
-    a[j] = make_float2(s * x.x + c * y.x, s * x.y + c * y.y);
+    a.r[u] = c * xr - s * yr;
+    a.i[u] = c * xi - s * yi;
+    a.r[v] = s * xr + c * yr;
+    a.i[v] = s * xi + c * yi;
   }
 }
 
 // diag(c - is, c + is) on register bit P
 template <int P>
-__device__ __forceinline__ void rz_reg(Amp (&a)[kRegAmps], float c, float s) {
+__device__ __forceinline__ void rz_reg(St& a, float c, float s) {
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    const float ss = (i & (1 << P)) ? s : -s;
-    const Amp x = a[i];
-    a[i] = make_float2(c * x.x - ss * x.y, c * x.y + ss * x.x);
+  for (int u = 0; u < kRegAmps; ++u) {
+    const float ss = (u & (1 << P)) ? s : -s;
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = c * xr - ss * xi;
+    a.i[u] = c * xi + ss * xr;
   }
 }
 
 // multiply every amplitude by (c + i ss)
-__device__ __forceinline__ void phase_all(Amp (&a)[kRegAmps], float c, float ss) {
+__device__ __forceinline__ void phase_all(St& a, float c, float ss) {
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    const Amp x = a[i];
-    a[i] = make_float2(c * x.x - ss * x.y, c * x.y + ss * x.x);
+  for (int u = 0; u < kRegAmps; ++u) {
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = c * xr - ss * xi;
+    a.i[u] = c * xi + ss * xr;
   }
 }
 
-// CNOT with control and target on register bits
+// CNOT with control and target on register bits: a register permutation
 template <int C, int T>
-__device__ __forceinline__ void cnot_rr(Amp (&a)[kRegAmps]) {
+__device__ __forceinline__ void cnot_rr(St& a) {
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    if (!(i & (1 << C)) || (i & (1 << T))) continue;
-    const int j = i | (1 << T);
-    const Amp x = a[i];
-    a[i] = a[j];
-    a[j] = x;
+  for (int u = 0; u < kRegAmps; ++u) {
+    if (!(u & (1 << C)) || (u & (1 << T))) continue;
+    const int v = u | (1 << T);
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = a.r[v];
+    a.i[u] = a.i[v];
+    a.r[v] = xr;
+    a.i[v] = xi;
   }
 }
 
 // CNOT with the control on a thread bit (flag) and the target on register bit T
 template <int T>
-__device__ __forceinline__ void cnot_tr(Amp (&a)[kRegAmps], bool flag) {
+__device__ __forceinline__ void cnot_tr(St& a, bool flag) {
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    if (i & (1 << T)) continue;
-    const int j = i | (1 << T);
-    const Amp x = a[i], y = a[j];
-    a[i] = flag ? y : x;
-    a[j] = flag ? x : y;
+  for (int u = 0; u < kRegAmps; ++u) {
+    if (u & (1 << T)) continue;
+    const int v = u | (1 << T);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
+    a.r[u] = flag ? yr : xr;
+    a.i[u] = flag ? yi : xi;
+    a.r[v] = flag ? xr : yr;
+    a.i[v] = flag ? xi : yi;
   }
 }
 
@@ -105,16 +120,17 @@ __device__ __forceinline__ uint32_t reg_pattern(int p) {
   return p == 0 ? 0xAAAAu : p == 1 ? 0xCCCCu : p == 2 ? 0xF0F0u : 0xFF00u;
 }
 
-// amplitudes whose register index j has bit j of `m` set are negated
-__device__ __forceinline__ void negate_mask(Amp (&a)[kRegAmps], uint32_t m) {
+// amplitudes whose register index u has bit u of `m` set are negated
+__device__ __forceinline__ void negate_mask(St& a, uint32_t m) {
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    const bool f = (m >> i) & 1u;
-    a[i] = f ? make_float2(-a[i].x, -a[i].y) : a[i];
+  for (int u = 0; u < kRegAmps; ++u) {
+    const float sg = ((m >> u) & 1u) ? -1.f : 1.f;
+    a.r[u] *= sg;
+    a.i[u] *= sg;
   }
 }
 
-__device__ __forceinline__ void apply_rx(Amp (&a)[kRegAmps], int p, float c, float s) {
+__device__ __forceinline__ void apply_rx(St& a, int p, float c, float s) {
   switch (p) {
     case 0: rx_reg<0>(a, c, s); break;
     case 1: rx_reg<1>(a, c, s); break;
@@ -123,7 +139,7 @@ __device__ __forceinline__ void apply_rx(Amp (&a)[kRegAmps], int p, float c, flo
   }
 }
 
-__device__ __forceinline__ void apply_ry(Amp (&a)[kRegAmps], int p, float c, float s) {
+__device__ __forceinline__ void apply_ry(St& a, int p, float c, float s) {
   switch (p) {
     case 0: ry_reg<0>(a, c, s); break;
     case 1: ry_reg<1>(a, c, s); break;
@@ -133,7 +149,7 @@ __device__ __forceinline__ void apply_ry(Amp (&a)[kRegAmps], int p, float c, flo
 }
 
 // RZ on physical bit p: register bit, or a thread bit (uniform phase per thread)
-__device__ __forceinline__ void apply_rz(Amp (&a)[kRegAmps], int p, float c, float s, int stid) {
+__device__ __forceinline__ void apply_rz(St& a, int p, float c, float s, int stid) {
   switch (p) {
     case 0: rz_reg<0>(a, c, s); break;
     case 1: rz_reg<1>(a, c, s); break;
@@ -143,7 +159,7 @@ __device__ __forceinline__ void apply_rz(Amp (&a)[kRegAmps], int p, float c, flo
   }
 }
 
-__device__ __forceinline__ void apply_cnot(Amp (&a)[kRegAmps], int pc, int pt, int stid) {
+__device__ __forceinline__ void apply_cnot(St& a, int pc, int pt, int stid) {
   if (pc >= kRegBits) {
     const bool f = (stid >> (pc - kRegBits)) & 1;
     switch (pt) {
@@ -177,56 +193,56 @@ __device__ __forceinline__ uint32_t bit_mask(int p, int stid) {
 }
 
 // ------------------------------------------------------- gradient partials
-// Im(conj(l) p) = l.x p.y - l.y p.x ; Re(conj(l) p) = l.x p.x + l.y p.y
+// Im(conj(l) p) = l.r p.i - l.i p.r ; Re(conj(l) p) = l.r p.r + l.i p.i
 
 template <int P>
-__device__ __forceinline__ float gx_reg(const Amp (&l)[kRegAmps], const Amp (&p)[kRegAmps]) {
+__device__ __forceinline__ float gx_reg(const St& l, const St& p) {
   float acc = 0.f;
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    if (i & (1 << P)) continue;
-    const int j = i | (1 << P);
+  for (int u = 0; u < kRegAmps; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
     // X: <l|X|p> = conj(l0) p1 + conj(l1) p0
-    acc += l[i].x * p[j].y - l[i].y * p[j].x;
-    acc += l[j].x * p[i].y - l[j].y * p[i].x;
+    acc += l.r[u] * p.i[v] - l.i[u] * p.r[v];
+    acc += l.r[v] * p.i[u] - l.i[v] * p.r[u];
   }
   return acc;
 }
 
 template <int P>
-__device__ __forceinline__ float gy_reg(const Amp (&l)[kRegAmps], const Amp (&p)[kRegAmps]) {
+__device__ __forceinline__ float gy_reg(const St& l, const St& p) {
   float acc = 0.f;
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    if (i & (1 << P)) continue;
-    const int j = i | (1 << P);
+  for (int u = 0; u < kRegAmps; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
     // Y p = (-i p1, i p0): Im<l|Y|p> = -Re(conj(l0) p1) + Re(conj(l1) p0)
-    acc -= l[i].x * p[j].x + l[i].y * p[j].y;
-    acc += l[j].x * p[i].x + l[j].y * p[i].y;
+    acc -= l.r[u] * p.r[v] + l.i[u] * p.i[v];
+    acc += l.r[v] * p.r[u] + l.i[v] * p.i[u];
   }
   return acc;
 }
 
 // Z on register bit P: sum over amplitudes of sign * Im(conj(l) p)
 template <int P>
-__device__ __forceinline__ float gz_reg(const Amp (&l)[kRegAmps], const Amp (&p)[kRegAmps]) {
+__device__ __forceinline__ float gz_reg(const St& l, const St& p) {
   float a0 = 0.f, a1 = 0.f;
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) {
-    const float v = l[i].x * p[i].y - l[i].y * p[i].x;
-    if (i & (1 << P)) a1 += v; else a0 += v;
+  for (int u = 0; u < kRegAmps; ++u) {
+    const float v = l.r[u] * p.i[u] - l.i[u] * p.r[u];
+    if (u & (1 << P)) a1 += v; else a0 += v;
   }
   return a0 - a1;
 }
 
-__device__ __forceinline__ float gz_all(const Amp (&l)[kRegAmps], const Amp (&p)[kRegAmps]) {
+__device__ __forceinline__ float gz_all(const St& l, const St& p) {
   float a = 0.f;
 #pragma unroll
-  for (int i = 0; i < kRegAmps; ++i) a += l[i].x * p[i].y - l[i].y * p[i].x;
+  for (int u = 0; u < kRegAmps; ++u) a += l.r[u] * p.i[u] - l.i[u] * p.r[u];
   return a;
 }
 
-__device__ __forceinline__ float grad_x(const Amp (&l)[kRegAmps], const Amp (&p)[kRegAmps], int r) {
+__device__ __forceinline__ float grad_x(const St& l, const St& p, int r) {
   switch (r) {
     case 0: return gx_reg<0>(l, p);
     case 1: return gx_reg<1>(l, p);
@@ -235,7 +251,7 @@ __device__ __forceinline__ float grad_x(const Amp (&l)[kRegAmps], const Amp (&p)
   }
 }
 
-__device__ __forceinline__ float grad_y(const Amp (&l)[kRegAmps], const Amp (&p)[kRegAmps], int r) {
+__device__ __forceinline__ float grad_y(const St& l, const St& p, int r) {
   switch (r) {
     case 0: return gy_reg<0>(l, p);
     case 1: return gy_reg<1>(l, p);
@@ -244,8 +260,7 @@ __device__ __forceinline__ float grad_y(const Amp (&l)[kRegAmps], const Amp (&p)
   }
 }
 
-__device__ __forceinline__ float grad_z(const Amp (&l)[kRegAmps], const Amp (&p)[kRegAmps], int ph,
-                                        int stid) {
+__device__ __forceinline__ float grad_z(const St& l, const St& p, int ph, int stid) {
   switch (ph) {
     case 0: return gz_reg<0>(l, p);
     case 1: return gz_reg<1>(l, p);
@@ -269,8 +284,8 @@ __device__ __forceinline__ float seg_sum(float v, int width) {
 
 // LDS exchange: write the 16 amplitudes at lam(old index), read lam(new index).
 // col[0..k) are the write-side columns, col[k..2k) the read-side columns.
-__device__ __forceinline__ void exchange(Amp (&a)[kRegAmps], Amp* xbuf, const uint32_t* col,
-                                         int k, int t, int stid, int sl) {
+__device__ __forceinline__ void exchange(St& a, float2* xbuf, const uint32_t* col, int k, int t,
+                                         int stid, int sl) {
   uint32_t bw = 0, br = 0;
   for (int i = 0; i < t; ++i) {
     if ((stid >> i) & 1) {
@@ -287,17 +302,19 @@ __device__ __forceinline__ void exchange(Amp (&a)[kRegAmps], Amp* xbuf, const ui
   const uint32_t w0 = col[0], w1 = col[1], w2 = col[2], w3 = col[3];
   const uint32_t r0 = col[k], r1 = col[k + 1], r2 = col[k + 2], r3 = col[k + 3];
 #pragma unroll
-  for (int j = 0; j < kRegAmps; ++j) {
-    const uint32_t o = ((j & 1) ? w0 : 0u) ^ ((j & 2) ? w1 : 0u) ^ ((j & 4) ? w2 : 0u) ^
-                       ((j & 8) ? w3 : 0u);
-    xbuf[bw ^ o] = a[j];
+  for (int u = 0; u < kRegAmps; ++u) {
+    const uint32_t o = ((u & 1) ? w0 : 0u) ^ ((u & 2) ? w1 : 0u) ^ ((u & 4) ? w2 : 0u) ^
+                       ((u & 8) ? w3 : 0u);
+    xbuf[bw ^ o] = make_float2(a.r[u], a.i[u]);
   }
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < kRegAmps; ++j) {
-    const uint32_t o = ((j & 1) ? r0 : 0u) ^ ((j & 2) ? r1 : 0u) ^ ((j & 4) ? r2 : 0u) ^
-                       ((j & 8) ? r3 : 0u);
-    a[j] = xbuf[br ^ o];
+  for (int u = 0; u < kRegAmps; ++u) {
+    const uint32_t o = ((u & 1) ? r0 : 0u) ^ ((u & 2) ? r1 : 0u) ^ ((u & 4) ? r2 : 0u) ^
+                       ((u & 8) ? r3 : 0u);
+    const float2 v = xbuf[br ^ o];
+    a.r[u] = v.x;
+    a.i[u] = v.y;
   }
   __syncthreads();
 }
@@ -307,8 +324,8 @@ __device__ __forceinline__ void exchange(Amp (&a)[kRegAmps], Amp* xbuf, const ui
 template <int WG, bool BWD>
 __global__ void __launch_bounds__(WG) resident_kernel(const TileArgs A) {
   extern __shared__ __align__(16) unsigned char smem[];
-  Amp* xbuf = reinterpret_cast<Amp*>(smem);
-  Amp* tab = reinterpret_cast<Amp*>(smem + A.lds_tab);
+  float2* xbuf = reinterpret_cast<float2*>(smem);
+  float2* tab = reinterpret_cast<float2*>(smem + A.lds_tab);
   float* acc = reinterpret_cast<float*>(smem + A.lds_acc);
 
   const int tid = threadIdx.x;
@@ -347,16 +364,22 @@ __global__ void __launch_bounds__(WG) resident_kernel(const TileArgs A) {
   __syncthreads();
 
   // 2. state
-  Amp a[kRegAmps];
-  Amp l[kRegAmps];
+  St a, l;
   if (!BWD) {
 #pragma unroll
-    for (int j = 0; j < kRegAmps; ++j) a[j] = make_float2(0.f, 0.f);
-    if (stid == 0) a[0].x = 1.f;
+    for (int j = 0; j < kRegAmps; ++j) {
+      a.r[j] = 0.f;
+      a.i[j] = 0.f;
+    }
+    if (stid == 0) a.r[0] = 1.f;
   } else {
-    const Amp* ws = reinterpret_cast<const Amp*>(A.ws);
+    const float2* ws = reinterpret_cast<const float2*>(A.ws);
 #pragma unroll
-    for (int j = 0; j < kRegAmps; ++j) a[j] = ws[((size_t)blockIdx.x * kRegAmps + j) * WG + tid];
+    for (int j = 0; j < kRegAmps; ++j) {
+      const float2 v = ws[((size_t)blockIdx.x * kRegAmps + j) * WG + tid];
+      a.r[j] = v.x;
+      a.i[j] = v.y;
+    }
     // lambda = H psi_G, H = sum_q g_q Z_q
     float gt = 0.f, g0 = 0.f, g1 = 0.f, g2 = 0.f, g3 = 0.f;
     if (valid) {
@@ -374,7 +397,8 @@ __global__ void __launch_bounds__(WG) resident_kernel(const TileArgs A) {
     for (int j = 0; j < kRegAmps; ++j) {
       const float h = gt + ((j & 1) ? -g0 : g0) + ((j & 2) ? -g1 : g1) + ((j & 4) ? -g2 : g2) +
                       ((j & 8) ? -g3 : g3);
-      l[j] = make_float2(h * a[j].x, h * a[j].y);
+      l.r[j] = h * a.r[j];
+      l.i[j] = h * a.i[j];
     }
   }
 
@@ -401,7 +425,7 @@ __global__ void __launch_bounds__(WG) resident_kernel(const TileArgs A) {
       if (BWD) negate_mask(l, m);
       continue;
     }
-    const Amp cs = tab[arg * S + sl];
+    const float2 cs = tab[arg * S + sl];
     if (!BWD) {
       if (op == OP_RX) apply_rx(a, pa, cs.x, cs.y);
       else if (op == OP_RY) apply_ry(a, pa, cs.x, cs.y);
@@ -430,14 +454,15 @@ __global__ void __launch_bounds__(WG) resident_kernel(const TileArgs A) {
   // 4. epilogue
   if (!BWD) {
     if (A.ws) {
-      Amp* ws = reinterpret_cast<Amp*>(A.ws);
+      float2* ws = reinterpret_cast<float2*>(A.ws);
 #pragma unroll
-      for (int j = 0; j < kRegAmps; ++j) ws[((size_t)blockIdx.x * kRegAmps + j) * WG + tid] = a[j];
+      for (int j = 0; j < kRegAmps; ++j)
+        ws[((size_t)blockIdx.x * kRegAmps + j) * WG + tid] = make_float2(a.r[j], a.i[j]);
     }
     float tot = 0.f, s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
     for (int j = 0; j < kRegAmps; ++j) {
-      const float pj = a[j].x * a[j].x + a[j].y * a[j].y;
+      const float pj = a.r[j] * a.r[j] + a.i[j] * a.i[j];
       tot += pj;
       s0 += (j & 1) ? -pj : pj;
       s1 += (j & 2) ? -pj : pj;
