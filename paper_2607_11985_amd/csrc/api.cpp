@@ -15,8 +15,8 @@ struct vqc_circuit {
   Plan plan;
   int device = -1;   // -1: host-only plan
   void* blob = nullptr;
-  size_t off_fwd = 0, off_bwd = 0, off_cols = 0, off_src = 0, off_idx = 0, off_slot = 0,
-         off_cs = 0, off_end = 0;
+  size_t off_fwd = 0, off_bwd = 0, off_cols = 0, off_src = 0, off_idx = 0, off_cs = 0,
+         off_maps = 0, off_pslots = 0;
 };
 
 namespace {
@@ -63,6 +63,34 @@ size_t resident_state_bytes(const Plan& p, int64_t batch) {
   return (size_t)resident_blocks(p, batch) * (size_t)p.WG * vqc::kRegAmps * 8;
 }
 
+// Streaming workspace: [psi | E partials | psi work | lambda work | grad partials]
+struct StreamLayout {
+  size_t psi = 0, epart = 0, psiw = 0, lamw = 0, gpart = 0, end_inference = 0, end_training = 0;
+};
+
+StreamLayout stream_layout(const Plan& p, int64_t batch) {
+  StreamLayout L;
+  const size_t state = (size_t)batch * ((size_t)1 << p.nq) * 8;
+  const size_t tiles = (size_t)batch << p.ng;
+  L.psi = 0;
+  L.epart = align_up(L.psi + state, 256);
+  L.end_inference = align_up(L.epart + tiles * (size_t)p.n * 4, 256);
+  L.psiw = L.end_inference;
+  L.lamw = align_up(L.psiw + state, 256);
+  L.gpart = align_up(L.lamw + state, 256);
+  L.end_training = align_up(L.gpart + tiles * (size_t)(p.P + p.F) * 4, 256);
+  return L;
+}
+
+size_t required_bytes(const Plan& p, int64_t batch, bool training) {
+  if (batch == 0) return 0;
+  if (p.path == VQC_PATH_STREAM) {
+    const StreamLayout L = stream_layout(p, batch);
+    return training ? L.end_training : L.end_inference;
+  }
+  return training ? resident_state_bytes(p, batch) : 0;
+}
+
 template <typename T>
 const T* at(const vqc_circuit* c, size_t off) {
   return reinterpret_cast<const T*>(static_cast<const unsigned char*>(c->blob) + off);
@@ -78,8 +106,7 @@ vqc::TileArgs tile_args(const vqc_circuit* c, bool bwd, int64_t batch) {
   a.occ_src = at<int32_t>(c, c->off_src);
   a.occ_idx = at<int32_t>(c, c->off_idx);
   a.occ_cs = at<float>(c, c->off_cs);
-  a.occ_slot = at<int32_t>(c, c->off_slot);
-  a.end_phys = at<uint8_t>(c, c->off_end);
+  a.end_phys = at<uint8_t>(c, c->off_maps) + p.end_off;
   a.n_occ = (int32_t)p.occ_src.size();
   a.n_slots = p.P + p.F;
   a.P = p.P;
@@ -104,9 +131,44 @@ int check_runnable(const vqc_circuit* c) {
 
 int check_batch(const vqc_circuit* c, int64_t batch) {
   if (batch < 0) return fail(VQC_ERR_INVALID_ARG, "batch must be >= 0");
-  if (resident_blocks(c->plan, batch) > (int64_t)INT_MAX)
+  const int64_t blocks = c->plan.path == VQC_PATH_STREAM ? (batch << c->plan.ng)
+                                                         : resident_blocks(c->plan, batch);
+  if (blocks > (int64_t)INT_MAX || batch > ((int64_t)1 << 40))
     return fail(VQC_ERR_TOO_LARGE, "batch too large for one launch");
   return VQC_OK;
+}
+
+vqc::PassArgs pass_args(const vqc_circuit* c, const vqc::PassPlan& pp, bool bwd, int64_t batch) {
+  const Plan& p = c->plan;
+  vqc::PassArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.ins = at<uint32_t>(c, bwd ? c->off_bwd : c->off_fwd) + 2 * (size_t)pp.ins_off;
+  a.n_ins = pp.n_ins;
+  a.cols = at<uint32_t>(c, c->off_cols);
+  a.io = a.cols + pp.io_off;
+  a.start_phys = at<uint8_t>(c, c->off_maps) + pp.start_off;
+  a.end_phys = at<uint8_t>(c, c->off_maps) + pp.end_off;
+  a.pslots = at<int32_t>(c, c->off_pslots) + pp.slots_off;
+  a.n_pslots = pp.n_slots;
+  a.flags = pp.flags;
+  a.occ_src = at<int32_t>(c, c->off_src);
+  a.occ_idx = at<int32_t>(c, c->off_idx);
+  a.occ_cs = at<float>(c, c->off_cs);
+  a.n_occ = (int32_t)p.occ_src.size();
+  a.n_slots = p.P + p.F;
+  a.P = p.P;
+  a.F = p.F;
+  a.n = p.n;
+  a.k = p.k;
+  a.ng = p.ng;
+  a.B = batch;
+  a.lds_tab = (uint32_t)p.lds_tab;
+  a.lds_acc = (uint32_t)p.lds_acc;
+  return a;
+}
+
+int hip_fail(const char* what, int rc) {
+  return fail(VQC_ERR_HIP, std::string(what) + " failed: " + hipGetErrorString((hipError_t)rc));
 }
 
 int check_rows(const vqc_circuit* c, const float* params, const float* inputs) {
@@ -174,9 +236,9 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
     c->off_cols = append(blob, p.cols);
     c->off_src = append(blob, p.occ_src);
     c->off_idx = append(blob, p.occ_idx);
-    c->off_slot = append(blob, p.occ_slot);
     c->off_cs = append(blob, p.occ_cs);
-    c->off_end = append(blob, p.end_phys);
+    c->off_maps = append(blob, p.maps);
+    c->off_pslots = append(blob, p.pslots);
     DeviceGuard g(device);
     if (!g.ok()) {
       delete c;
@@ -191,7 +253,8 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
       delete c;
       return fail(VQC_ERR_HIP, "copy of the schedule failed");
     }
-    rc = vqc::prepare_kernels(p.WG, p.lds_fwd, p.lds_bwd);
+    rc = p.path == VQC_PATH_STREAM ? vqc::prepare_stream_kernels(p.lds_fwd, p.lds_bwd)
+                                   : vqc::prepare_kernels(p.WG, p.lds_fwd, p.lds_bwd);
     if (rc != 0) {
       (void)hipFree(c->blob);
       delete c;
@@ -214,8 +277,7 @@ void vqc_destroy(vqc_circuit* c) {
 
 size_t vqc_workspace_bytes(const vqc_circuit* c, int64_t batch, int32_t training) {
   if (!c || batch < 0) return (size_t)-1;
-  if (!training || batch == 0) return 0;
-  return resident_state_bytes(c->plan, batch);
+  return required_bytes(c->plan, batch, training != 0);
 }
 
 int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
@@ -226,22 +288,44 @@ int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const 
   if (batch == 0) return VQC_OK;
   if ((rc = check_rows(c, params, inputs))) return rc;
   if (!expvals) return fail(VQC_ERR_INVALID_ARG, "expvals is NULL");
+  const Plan& p = c->plan;
+  if (p.path == VQC_PATH_STREAM && !workspace)
+    return fail(VQC_ERR_WORKSPACE, "the streaming path needs a workspace (states live in HBM)");
   if (workspace) {
-    if (workspace_bytes < resident_state_bytes(c->plan, batch))
-      return fail(VQC_ERR_WORKSPACE, "workspace smaller than vqc_workspace_bytes(c, batch, 1)");
-    if (reinterpret_cast<uintptr_t>(workspace) % 16)
-      return fail(VQC_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+    if (workspace_bytes < required_bytes(p, batch, p.path == VQC_PATH_RESIDENT))
+      return fail(VQC_ERR_WORKSPACE, "workspace smaller than vqc_workspace_bytes(c, batch, " +
+                                         std::string(p.path == VQC_PATH_RESIDENT ? "1" : "0") +
+                                         ")");
+    if (reinterpret_cast<uintptr_t>(workspace) % 256)
+      return fail(VQC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   }
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
+  if (p.path == VQC_PATH_STREAM) {
+    const StreamLayout L = stream_layout(p, batch);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    for (const vqc::PassPlan& pp : p.fpass) {
+      vqc::PassArgs a = pass_args(c, pp, false, batch);
+      a.params = params;
+      a.inputs = inputs;
+      a.psi_src = ws + L.psi;
+      a.psi_dst = ws + L.psi;
+      a.epart = reinterpret_cast<float*>(ws + L.epart);
+      rc = vqc::launch_stream_pass(false, a, batch << p.ng, p.lds_fwd, stream);
+      if (rc) return hip_fail("forward pass launch", rc);
+    }
+    rc = vqc::launch_reduce_e(batch, p.ng, p.n, reinterpret_cast<const float*>(ws + L.epart),
+                              expvals, stream);
+    if (rc) return hip_fail("expectation reduction launch", rc);
+    return VQC_OK;
+  }
   vqc::TileArgs a = tile_args(c, false, batch);
   a.params = params;
   a.inputs = inputs;
   a.expvals = expvals;
   a.ws = workspace;
-  rc = vqc::launch_resident_forward(c->plan, a, resident_blocks(c->plan, batch), stream);
-  if (rc) return fail(VQC_ERR_HIP, std::string("forward launch failed: ") +
-                                       hipGetErrorString((hipError_t)rc));
+  rc = vqc::launch_resident_forward(p, a, resident_blocks(p, batch), stream);
+  if (rc) return hip_fail("forward launch", rc);
   return VQC_OK;
 }
 
@@ -254,22 +338,49 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
   if (batch == 0) return VQC_OK;
   if ((rc = check_rows(c, params, inputs))) return rc;
   if (!grad_out) return fail(VQC_ERR_INVALID_ARG, "grad_out is NULL");
-  if (!workspace || workspace_bytes < resident_state_bytes(c->plan, batch))
+  const Plan& p = c->plan;
+  if (!workspace || workspace_bytes < required_bytes(p, batch, true))
     return fail(VQC_ERR_WORKSPACE, "backward needs the workspace of a training forward");
-  if (reinterpret_cast<uintptr_t>(workspace) % 16)
-    return fail(VQC_ERR_WORKSPACE, "workspace must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(VQC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
+  float* dp = p.P > 0 ? dparams : nullptr;
+  float* dx = p.F > 0 ? dinputs : nullptr;
+  if (p.path == VQC_PATH_STREAM) {
+    const StreamLayout L = stream_layout(p, batch);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    float* gpart = reinterpret_cast<float*>(ws + L.gpart);
+    rc = vqc::launch_fill_zero(gpart, (batch << p.ng) * (int64_t)(p.P + p.F), stream);
+    if (rc) return hip_fail("gradient partial clear", rc);
+    bool first = true;
+    for (const vqc::PassPlan& pp : p.bpass) {
+      vqc::PassArgs a = pass_args(c, pp, true, batch);
+      a.params = params;
+      a.inputs = inputs;
+      a.grad_out = grad_out;
+      a.psi_src = ws + (first ? L.psi : L.psiw);  // the saved psi_G is only read
+      a.psi_dst = ws + L.psiw;
+      a.lam_src = ws + L.lamw;
+      a.lam_dst = ws + L.lamw;
+      a.gpart = gpart;
+      rc = vqc::launch_stream_pass(true, a, batch << p.ng, p.lds_bwd, stream);
+      if (rc) return hip_fail("backward pass launch", rc);
+      first = false;
+    }
+    rc = vqc::launch_reduce_grad(batch, p.ng, p.P + p.F, p.P, p.F, gpart, dp, dx, stream);
+    if (rc) return hip_fail("gradient reduction launch", rc);
+    return VQC_OK;
+  }
   vqc::TileArgs a = tile_args(c, true, batch);
   a.params = params;
   a.inputs = inputs;
   a.ws = workspace;
   a.grad_out = grad_out;
-  a.dparams = c->plan.P > 0 ? dparams : nullptr;
-  a.dinputs = c->plan.F > 0 ? dinputs : nullptr;
-  rc = vqc::launch_resident_backward(c->plan, a, resident_blocks(c->plan, batch), stream);
-  if (rc) return fail(VQC_ERR_HIP, std::string("backward launch failed: ") +
-                                       hipGetErrorString((hipError_t)rc));
+  a.dparams = dp;
+  a.dinputs = dx;
+  rc = vqc::launch_resident_backward(p, a, resident_blocks(p, batch), stream);
+  if (rc) return hip_fail("backward launch", rc);
   return VQC_OK;
 }
 
@@ -302,8 +413,8 @@ int vqc_circuit_info(const vqc_circuit* c, vqc_info* info) {
   info->path = p.path;
   info->tile_qubits = p.k;
   info->threads = p.WG;
-  info->fwd_passes = 1;
-  info->bwd_passes = 1;
+  info->fwd_passes = p.path == VQC_PATH_STREAM ? (int32_t)p.fpass.size() : 1;
+  info->bwd_passes = p.path == VQC_PATH_STREAM ? (int32_t)p.bpass.size() : 1;
   info->fwd_exchanges = p.fwd_exchanges;
   info->bwd_exchanges = p.bwd_exchanges;
   info->fwd_instructions = (int32_t)(p.fwd.size() / 2);

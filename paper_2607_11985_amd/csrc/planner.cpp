@@ -1,13 +1,22 @@
 // planner.cpp -- compile phase (Algorithm 1, compile phase): validate the
 // static gate list, lower it to primitives, classify every angle as parametric
 // (param / input slot) or constant (cached cos/sin), and plan the register-tile
-// schedule of the forward sweep and of the adjoint (reverse) sweep.
+// schedules of the forward sweep and of the adjoint (reverse) sweep.
+//
+// Resident path (n <= 14): one pass holds every qubit on chip.
+// Streaming path (n > 14): a pass holds 14 "local" qubits of one sample in a
+// workgroup; the other ng = n - 14 "global" qubits are fixed per workgroup (its
+// tile index).  A pass runs every gate whose qubit lines are ready and whose
+// register-bit qubit is local -- gates on disjoint qubits commute, so a gate
+// that must wait blocks only its own lines.  Diagonal gates and CNOT controls
+// may sit on global qubits (their value is uniform over the tile).
 //
 // Host-only code: no device calls, so it can run (and be tested) without a GPU.
 #include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <map>
 
 #include "vqc.h"
 #include "vqc_internal.h"
@@ -16,9 +25,13 @@ namespace vqc {
 namespace {
 
 struct Mapping {
-  int k = 0;
-  int p2q[kMaxTileQubits];
-  int q2p[kMaxQubits];
+  int k = 0, nq = 0;
+  int p2q[kMaxTileQubits];  // local physical bit -> logical qubit
+  int q2p[kMaxQubits];      // logical qubit -> physical bit (>= k: global bit + k)
+  bool operator==(const Mapping& o) const {
+    return k == o.k && nq == o.nq && std::memcmp(p2q, o.p2q, sizeof(int) * k) == 0 &&
+           std::memcmp(q2p, o.q2p, sizeof(int) * nq) == 0;
+  }
 };
 
 // Qubit a primitive needs on a register bit, or -1 (diagonal gates and CNOT
@@ -35,6 +48,8 @@ int register_need(const Prim& p) {
   }
 }
 
+bool two_qubit(const Prim& p) { return p.kind == P_CNOT || p.kind == P_CZ; }
+
 // next_need[i * nq + q]: first index >= i of `seq` that needs q on a register.
 std::vector<int> next_need_table(const std::vector<Prim>& seq, int nq) {
   const int G = (int)seq.size();
@@ -48,15 +63,15 @@ std::vector<int> next_need_table(const std::vector<Prim>& seq, int nq) {
 }
 
 // Exchange tables.  The LDS slot of an amplitude is a GF(2)-linear function
-// lam(x) of its logical tile index; lam is chosen per exchange so that the
-// lanes of a 32-lane group hit 32 distinct 8-byte slots modulo 256 bytes both
-// when writing in the old layout and when reading in the new one:
-// slot bit i (i < bank bits) = x[old lane-i qubit] xor x[new lane-i qubit]
-// (the second term only when the qubit changes), the other qubits get one
-// high bit each.  Exchanges only swap register bits with thread bits, so a
-// qubit never moves between two lane positions, which keeps lam bijective.
-int emit_exchange(const Mapping& a, const Mapping& b, int k, int t, std::vector<uint32_t>& cols,
-                  std::string& msg) {
+// lam(x) of its tile position.  When the exchange only swaps register bits with
+// thread bits (every exchange the register planner makes), lam is chosen so
+// that the lanes of a 32-lane group hit 32 distinct 8-byte slots modulo 256
+// bytes both when writing in the old layout and when reading in the new one:
+// slot bit i (i < bank bits) = x[old lane-i qubit] xor x[new lane-i qubit] (the
+// second term only when that lane position changes hands), every other qubit
+// gets one high bit.  A general permutation falls back to a layout whose reads
+// are conflict free.
+int emit_exchange(const Mapping& a, const Mapping& b, int k, int t, std::vector<uint32_t>& cols) {
   const int lb = std::min(kBankBits, t);
   uint32_t lam[kMaxQubits];
   bool in_a[kMaxQubits], in_b[kMaxQubits];
@@ -67,25 +82,28 @@ int emit_exchange(const Mapping& a, const Mapping& b, int k, int t, std::vector<
     in_a[a.p2q[kRegBits + i]] = true;
     in_b[b.p2q[kRegBits + i]] = true;
   }
+  bool swap_only = true;
   for (int i = 0; i < lb; ++i) {
     const int qa = a.p2q[kRegBits + i], qb = b.p2q[kRegBits + i];
-    lam[qa] |= 1u << i;
-    if (qb != qa) {
-      if (in_a[qb] || in_b[qa]) {
-        msg = "internal: exchange moves a qubit between lane positions";
-        return VQC_ERR_UNSUPPORTED;
-      }
-      lam[qb] |= 1u << i;
+    if (qa != qb && (in_a[qb] || in_b[qa])) swap_only = false;
+  }
+  if (swap_only) {
+    for (int i = 0; i < lb; ++i) {
+      const int qa = a.p2q[kRegBits + i], qb = b.p2q[kRegBits + i];
+      lam[qa] |= 1u << i;
+      if (qb != qa) lam[qb] |= 1u << i;
     }
-  }
-  int nb = lb;
-  for (int p = 0; p < k; ++p) {
-    const int q = a.p2q[p];
-    if (!in_a[q]) lam[q] |= 1u << nb++;
-  }
-  if (nb != k) {
-    msg = "internal: exchange layout is not a bijection";
-    return VQC_ERR_UNSUPPORTED;
+    int nb = lb;
+    for (int p = 0; p < k; ++p) {
+      const int q = a.p2q[p];
+      if (!in_a[q]) lam[q] |= 1u << nb++;
+    }
+  } else {
+    // slot = thread bits of the new layout in the low bits, register bits on top
+    for (int p = 0; p < k; ++p) {
+      const int q = b.p2q[p];
+      lam[q] = 1u << (p >= kRegBits ? p - kRegBits : t + p);
+    }
   }
   const int off = (int)cols.size();
   for (int p = 0; p < k; ++p) cols.push_back(lam[a.p2q[p]]);
@@ -93,24 +111,30 @@ int emit_exchange(const Mapping& a, const Mapping& b, int k, int t, std::vector<
   return off;
 }
 
-void emit(std::vector<uint32_t>& out, uint32_t op, int a, int b, uint32_t arg) {
-  out.push_back(ins_word0(op, (uint32_t)a, (uint32_t)b));
+void emit(std::vector<uint32_t>& out, uint32_t op, int a, int b, int slot, uint32_t arg) {
+  out.push_back(ins_word0(op, (uint32_t)a, (uint32_t)b, slot));
   out.push_back(arg);
 }
 
-// One sweep over `seq` starting from mapping `m` (updated to the end mapping).
+// One register-level sweep over `seq` (already in execution order) starting
+// from mapping `m` (updated to the end mapping).  slot_of(occ) gives the
+// gradient accumulator written into rotation instructions.
+template <typename SlotFn>
 int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int t, Mapping& m,
                std::vector<uint32_t>& out, std::vector<uint32_t>& cols, int& exchanges,
-               std::string& msg) {
+               SlotFn slot_of, std::string& msg) {
   const std::vector<int> nn = next_need_table(seq, nq);
   for (size_t i = 0; i < seq.size(); ++i) {
     const Prim& pr = seq[i];
     const int need = register_need(pr);
+    if (need >= 0 && m.q2p[need] >= k) {
+      msg = "internal: register-bit gate on a global qubit";
+      return VQC_ERR_UNSUPPORTED;
+    }
     if (need >= 0 && m.q2p[need] >= kRegBits) {
-      // Belady: the register bits get the kRegBits qubits needed soonest.
+      // Belady: the register bits get the kRegBits local qubits needed soonest.
       std::vector<int> qs;
-      for (int q = 0; q < nq; ++q)
-        if (m.q2p[q] >= 0) qs.push_back(q);
+      for (int p = 0; p < k; ++p) qs.push_back(m.p2q[p]);
       const int* row = &nn[i * (size_t)nq];
       std::stable_sort(qs.begin(), qs.end(), [&](int x, int y) {
         if (row[x] != row[y]) return row[x] < row[y];
@@ -136,21 +160,142 @@ int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int t, Mapping& m,
         nm.p2q[pin] = qout;
         nm.q2p[qout] = pin;
       }
-      const int off = emit_exchange(m, nm, k, t, cols, msg);
-      if (off < 0) return off;
-      emit(out, OP_EXCHANGE, 0, 0, (uint32_t)off);
+      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, nm, k, t, cols));
       ++exchanges;
       m = nm;
     }
     switch (pr.kind) {
-      case P_RX: emit(out, OP_RX, m.q2p[pr.q0], 0, (uint32_t)pr.occ); break;
-      case P_RY: emit(out, OP_RY, m.q2p[pr.q0], 0, (uint32_t)pr.occ); break;
-      case P_RZ: emit(out, OP_RZ, m.q2p[pr.q0], 0, (uint32_t)pr.occ); break;
-      case P_CNOT: emit(out, OP_CNOT, m.q2p[pr.q0], m.q2p[pr.q1], 0); break;
-      case P_CZ: emit(out, OP_CZ, m.q2p[pr.q0], m.q2p[pr.q1], 0); break;
+      case P_RX: emit(out, OP_RX, m.q2p[pr.q0], 0, slot_of(pr.occ), (uint32_t)pr.occ); break;
+      case P_RY: emit(out, OP_RY, m.q2p[pr.q0], 0, slot_of(pr.occ), (uint32_t)pr.occ); break;
+      case P_RZ: emit(out, OP_RZ, m.q2p[pr.q0], 0, slot_of(pr.occ), (uint32_t)pr.occ); break;
+      case P_CNOT: emit(out, OP_CNOT, m.q2p[pr.q0], m.q2p[pr.q1], -1, 0); break;
+      case P_CZ: emit(out, OP_CZ, m.q2p[pr.q0], m.q2p[pr.q1], -1, 0); break;
       default: msg = "internal: unknown primitive"; return VQC_ERR_UNSUPPORTED;
     }
   }
+  return 0;
+}
+
+int append_map(const Mapping& m, std::vector<uint8_t>& maps) {
+  const int off = (int)maps.size();
+  for (int q = 0; q < m.nq; ++q) maps.push_back((uint8_t)m.q2p[q]);
+  return off;
+}
+
+// Tile I/O layout of a streaming pass: the 14 local qubits in ascending order
+// are the tile ranks; ranks 0..9 sit on the thread bits, 10..13 on the
+// register bits, so consecutive lanes touch consecutive low qubits in HBM.
+Mapping io_mapping(const std::vector<int>& local, const std::vector<int>& glob, int k, int nq) {
+  Mapping m;
+  m.k = k;
+  m.nq = nq;
+  for (int q = 0; q < kMaxQubits; ++q) m.q2p[q] = -1;
+  const int nt = k - kRegBits;
+  for (int r = 0; r < k; ++r) {
+    const int p = r < nt ? kRegBits + r : r - nt;
+    m.p2q[p] = local[r];
+    m.q2p[local[r]] = p;
+  }
+  for (size_t i = 0; i < glob.size(); ++i) m.q2p[glob[i]] = k + (int)i;
+  return m;
+}
+
+int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, std::vector<uint32_t>& out,
+                std::vector<PassPlan>& passes, int& exchanges, std::string& msg) {
+  const int nq = plan.nq, k = plan.k, t = plan.t, ng = plan.ng;
+  std::vector<char> done(seq.size(), 0);
+  size_t remaining = seq.size();
+  do {
+    // rank the qubits by their first pending register need
+    std::vector<int> order;
+    std::vector<char> seen(nq, 0);
+    for (size_t i = 0; i < seq.size(); ++i) {
+      if (done[i]) continue;
+      const int q = register_need(seq[i]);
+      if (q >= 0 && !seen[q]) {
+        seen[q] = 1;
+        order.push_back(q);
+      }
+    }
+    for (int q = 0; q < nq; ++q)
+      if (!seen[q]) order.push_back(q);
+    // global qubits: needed last, preferring qubits >= 6 so that the low qubits
+    // stay on the lanes and tile I/O stays contiguous
+    const int lowlim = std::min(6, nq - ng);
+    std::vector<char> is_glob(nq, 0);
+    std::vector<int> glob;
+    for (auto it = order.rbegin(); it != order.rend() && (int)glob.size() < ng; ++it)
+      if (*it >= lowlim) {
+        glob.push_back(*it);
+        is_glob[*it] = 1;
+      }
+    for (auto it = order.rbegin(); it != order.rend() && (int)glob.size() < ng; ++it)
+      if (!is_glob[*it]) {
+        glob.push_back(*it);
+        is_glob[*it] = 1;
+      }
+    std::sort(glob.begin(), glob.end());
+    std::vector<int> local;
+    for (int q = 0; q < nq; ++q)
+      if (!is_glob[q]) local.push_back(q);
+    // the pass: every ready gate whose register qubit is local
+    std::vector<char> blocked(nq, 0);
+    std::vector<Prim> pass_prims;
+    for (size_t i = 0; i < seq.size(); ++i) {
+      if (done[i]) continue;
+      const Prim& pr = seq[i];
+      const bool two = two_qubit(pr);
+      const bool ready = !blocked[pr.q0] && !(two && blocked[pr.q1]);
+      const int need = register_need(pr);
+      if (ready && (need < 0 || !is_glob[need])) {
+        pass_prims.push_back(pr);
+        done[i] = 1;
+        --remaining;
+      } else {
+        blocked[pr.q0] = 1;
+        if (two) blocked[pr.q1] = 1;
+      }
+    }
+    if (pass_prims.empty() && remaining > 0) {
+      msg = "internal: streaming pass made no progress";
+      return VQC_ERR_UNSUPPORTED;
+    }
+    const Mapping io = io_mapping(local, glob, k, nq);
+    Mapping m = io;
+    PassPlan pp;
+    pp.ins_off = (int)out.size() / 2;
+    pp.start_off = append_map(io, plan.maps);
+    pp.end_off = pp.start_off;
+    std::map<int, int> local_slot;
+    std::vector<int32_t> slots;
+    auto slot_of = [&](int occ) -> int {
+      const int s = plan.occ_slot[occ];
+      if (s < 0) return -1;
+      auto it = local_slot.find(s);
+      if (it != local_slot.end()) return it->second;
+      const int id = (int)slots.size();
+      local_slot[s] = id;
+      slots.push_back(s);
+      return id;
+    };
+    int rc = plan_sweep(pass_prims, nq, k, t, m, out, plan.cols, exchanges, slot_of, msg);
+    if (rc < 0) return rc;
+    if (!(m == io)) {
+      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, io, k, t, plan.cols));
+      ++exchanges;
+    }
+    pp.n_ins = (int)out.size() / 2 - pp.ins_off;
+    pp.io_off = (int)plan.cols.size();
+    for (int r = 0; r < k; ++r) plan.cols.push_back(1u << local[r]);
+    for (int i = 0; i < ng; ++i) plan.cols.push_back(1u << glob[i]);
+    pp.slots_off = (int)plan.pslots.size();
+    pp.n_slots = (int)slots.size();
+    plan.pslots.insert(plan.pslots.end(), slots.begin(), slots.end());
+    plan.max_pass_slots = std::max(plan.max_pass_slots, pp.n_slots);
+    if (passes.empty()) pp.flags |= bwd ? PF_MAKE_LAMBDA : PF_INIT;
+    passes.push_back(pp);
+  } while (remaining > 0);
+  if (!bwd) passes.back().flags |= PF_ZPART;
   return 0;
 }
 
@@ -247,63 +392,84 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, Pl
   const int nq = std::max(n, kRegBits);  // qubits >= n stay |0> and are never read
   plan.nq = nq;
   if (path == VQC_PATH_AUTO) path = nq <= kMaxTileQubits ? VQC_PATH_RESIDENT : VQC_PATH_STREAM;
-  if (path == VQC_PATH_STREAM) {
-    msg = "the streaming path (n > 14) is not available in this build";
-    return VQC_ERR_UNSUPPORTED;
-  }
-  if (path != VQC_PATH_RESIDENT) {
+  if (path != VQC_PATH_RESIDENT && path != VQC_PATH_STREAM) {
     msg = "unknown path option";
     return VQC_ERR_INVALID_ARG;
   }
-  if (nq > kMaxTileQubits) {
+  if (path == VQC_PATH_RESIDENT && nq > kMaxTileQubits) {
     msg = "the resident path holds at most 14 qubits";
     return VQC_ERR_UNSUPPORTED;
   }
-  plan.path = VQC_PATH_RESIDENT;
-  plan.k = nq;
-  plan.t = nq - kRegBits;
-  const int T = 1 << plan.t;
-  plan.WG = std::max(64, T);
-  plan.S = plan.WG / T;
-  plan.G = T >= 64 ? plan.WG / 64 : plan.S;
-
-  // initial mapping: registers get the first qubits the sweep needs there
-  Mapping m;
-  m.k = plan.k;
-  for (int q = 0; q < kMaxQubits; ++q) m.q2p[q] = -1;
-  {
-    const std::vector<int> nn = next_need_table(plan.prims, nq);
-    std::vector<int> qs(nq);
-    for (int q = 0; q < nq; ++q) qs[q] = q;
-    std::stable_sort(qs.begin(), qs.end(), [&](int x, int y) { return nn[x] < nn[y]; });
-    std::vector<int> rest(qs.begin() + kRegBits, qs.end());
-    std::sort(rest.begin(), rest.end());
-    for (int r = 0; r < kRegBits; ++r) {
-      m.p2q[r] = qs[r];
-      m.q2p[qs[r]] = r;
-    }
-    for (size_t j = 0; j < rest.size(); ++j) {
-      m.p2q[kRegBits + j] = rest[j];
-      m.q2p[rest[j]] = kRegBits + (int)j;
-    }
+  if (path == VQC_PATH_STREAM && nq < kMaxTileQubits) {
+    msg = "the streaming path needs at least 14 qubits (its tiles hold 14)";
+    return VQC_ERR_UNSUPPORTED;
   }
-  int rc = plan_sweep(plan.prims, nq, plan.k, plan.t, m, plan.fwd, plan.cols, plan.fwd_exchanges,
-                      msg);
-  if (rc < 0) return rc;
-  plan.end_phys.assign(nq, 0);
-  for (int q = 0; q < nq; ++q) plan.end_phys[q] = (uint8_t)m.q2p[q];
-  std::vector<Prim> rev(plan.prims.rbegin(), plan.prims.rend());
-  rc = plan_sweep(rev, nq, plan.k, plan.t, m, plan.bwd, plan.cols, plan.bwd_exchanges, msg);
-  if (rc < 0) return rc;
-
-  // LDS: exchange buffer | angle table [occ][S] | gradient accumulators [slot][G]
-  const size_t xbuf = (size_t)plan.WG * kRegAmps * 8;
-  plan.lds_tab = xbuf;
-  const size_t tab = align_up((size_t)n_occ * plan.S * 8, 16);
-  plan.lds_acc = xbuf + tab;
-  const size_t acc = align_up((size_t)(P + F) * plan.G * 4, 16);
-  plan.lds_fwd = std::max<size_t>(xbuf + tab, 16);
-  plan.lds_bwd = xbuf + tab + acc;
+  plan.path = path;
+  const std::vector<Prim> rev(plan.prims.rbegin(), plan.prims.rend());
+  int rc = 0;
+  if (path == VQC_PATH_RESIDENT) {
+    plan.k = nq;
+    plan.t = nq - kRegBits;
+    const int T = 1 << plan.t;
+    plan.WG = std::max(64, T);
+    plan.S = plan.WG / T;
+    plan.G = T >= 64 ? plan.WG / 64 : plan.S;
+    // initial mapping: registers get the first qubits the sweep needs there
+    Mapping m;
+    m.k = plan.k;
+    m.nq = nq;
+    for (int q = 0; q < kMaxQubits; ++q) m.q2p[q] = -1;
+    {
+      const std::vector<int> nn = next_need_table(plan.prims, nq);
+      std::vector<int> qs(nq);
+      for (int q = 0; q < nq; ++q) qs[q] = q;
+      std::stable_sort(qs.begin(), qs.end(), [&](int x, int y) { return nn[x] < nn[y]; });
+      std::vector<int> rest(qs.begin() + kRegBits, qs.end());
+      std::sort(rest.begin(), rest.end());
+      for (int r = 0; r < kRegBits; ++r) {
+        m.p2q[r] = qs[r];
+        m.q2p[qs[r]] = r;
+      }
+      for (size_t j = 0; j < rest.size(); ++j) {
+        m.p2q[kRegBits + j] = rest[j];
+        m.q2p[rest[j]] = kRegBits + (int)j;
+      }
+    }
+    auto global_slot = [&](int occ) { return plan.occ_slot[occ]; };
+    rc = plan_sweep(plan.prims, nq, plan.k, plan.t, m, plan.fwd, plan.cols, plan.fwd_exchanges,
+                    global_slot, msg);
+    if (rc < 0) return rc;
+    plan.end_off = append_map(m, plan.maps);
+    rc = plan_sweep(rev, nq, plan.k, plan.t, m, plan.bwd, plan.cols, plan.bwd_exchanges,
+                    global_slot, msg);
+    if (rc < 0) return rc;
+    // LDS: exchange buffer | angle table [occ][S] | gradient accumulators [slot][G]
+    const size_t xbuf = (size_t)plan.WG * kRegAmps * 8;
+    plan.lds_tab = xbuf;
+    const size_t tab = align_up((size_t)n_occ * plan.S * 8, 16);
+    plan.lds_acc = xbuf + tab;
+    const size_t acc = align_up((size_t)(P + F) * plan.G * 4, 16);
+    plan.lds_fwd = std::max<size_t>(xbuf + tab, 16);
+    plan.lds_bwd = xbuf + tab + acc;
+  } else {
+    plan.k = kMaxTileQubits;
+    plan.t = plan.k - kRegBits;
+    plan.ng = nq - plan.k;
+    plan.WG = 1 << plan.t;
+    plan.S = 1;
+    plan.G = plan.WG / 64;
+    rc = plan_stream(plan, plan.prims, false, plan.fwd, plan.fpass, plan.fwd_exchanges, msg);
+    if (rc < 0) return rc;
+    rc = plan_stream(plan, rev, true, plan.bwd, plan.bpass, plan.bwd_exchanges, msg);
+    if (rc < 0) return rc;
+    const size_t xbuf = (size_t)plan.WG * kRegAmps * 8;
+    plan.lds_tab = xbuf;
+    const size_t tab = align_up((size_t)n_occ * 8, 16);
+    plan.lds_acc = xbuf + tab;
+    const size_t acc = align_up((size_t)plan.max_pass_slots * plan.G * 4, 16);
+    plan.lds_fwd = xbuf + tab;
+    plan.lds_bwd = xbuf + tab + acc;
+  }
   if (plan.lds_bwd > (size_t)kLdsBytes) {
     msg = "circuit too large for on-chip tables: " + std::to_string(plan.lds_bwd) +
           " bytes of LDS needed (limit " + std::to_string(kLdsBytes) + ")";

@@ -30,7 +30,8 @@ constexpr int kBankBits = 5;                 // lane bits kept bank-conflict fre
 // primitive kinds after lowering (ROT -> RZ, RY, RZ)
 enum PrimKind : int { P_RX = 0, P_RY = 1, P_RZ = 2, P_CNOT = 4, P_CZ = 5 };
 
-// instruction opcodes
+// instruction opcodes.  Physical bits p >= k name global qubits of a
+// streamed tile (bit p - k of the tile index within the sample).
 enum Opcode : uint32_t {
   OP_RX = 1,      // a = register position, arg = occurrence
   OP_RY = 2,      // a = register position, arg = occurrence
@@ -40,7 +41,27 @@ enum Opcode : uint32_t {
   OP_EXCHANGE = 6 // arg = offset of 2k column words (write side, read side)
 };
 
-inline uint32_t ins_word0(uint32_t op, uint32_t a, uint32_t b) { return op | (a << 8) | (b << 16); }
+// word0 = op | a << 5 | b << 10 | (slot + 1) << 16; word1 = arg.  `slot` is the
+// gradient accumulator of a rotation (-1: constant angle, no gradient).
+inline uint32_t ins_word0(uint32_t op, uint32_t a, uint32_t b, int slot) {
+  return op | (a << 5) | (b << 10) | ((uint32_t)(slot + 1) << 16);
+}
+
+// pass flags of the streaming kernels
+enum PassFlag : int32_t {
+  PF_INIT = 1,        // start from |0...0> instead of loading psi
+  PF_MAKE_LAMBDA = 2, // (adjoint) lambda = H psi after loading psi_G
+  PF_ZPART = 4,       // (forward) per-tile <Z> partial sums
+};
+
+struct PassPlan {
+  int ins_off = 0, n_ins = 0;   // instruction pairs (offset in pairs)
+  int io_off = 0;               // k + ng words: x offset of each tile rank bit, then
+                                // of each global bit
+  int start_off = 0, end_off = 0;  // nq bytes each: logical qubit -> physical bit
+  int slots_off = 0, n_slots = 0;  // pass-local gradient slot -> global slot
+  int flags = 0;
+};
 
 struct Prim {
   int kind;
@@ -56,7 +77,6 @@ struct TileArgs {
   const int32_t* occ_src;   // per occurrence: 0 param, 1 input, 2 const
   const int32_t* occ_idx;
   const float* occ_cs;      // per occurrence (cos, sin) of const angles / 2
-  const int32_t* occ_slot;  // per occurrence: gradient slot in [0, P+F) or -1
   const uint8_t* end_phys;  // per logical qubit: physical bit at forward end
   int32_t n_occ, n_slots, P, F;
   int32_t n;                // real qubits (E and g have n columns)
@@ -78,14 +98,19 @@ struct TileArgs {
 
 struct Plan {
   int n = 0, nq = 0, k = 0, t = 0, WG = 0, S = 0, G = 0;
+  int ng = 0;                             // global (streamed) qubits
   int P = 0, F = 0, n_ops = 0, path = 1;
   std::vector<Prim> prims;
   std::vector<int32_t> occ_src, occ_idx, occ_slot;
   std::vector<float> occ_cs;              // 2 per occurrence
   std::vector<uint32_t> fwd, bwd;         // instruction pairs
-  std::vector<uint32_t> cols;             // exchange column tables
-  std::vector<uint8_t> end_phys;          // logical -> phys at forward end (nq)
+  std::vector<uint32_t> cols;             // exchange / tile I/O column tables
+  std::vector<uint8_t> maps;              // logical -> phys tables (nq bytes each)
+  std::vector<int32_t> pslots;            // pass-local -> global gradient slots
+  std::vector<PassPlan> fpass, bpass;     // streaming passes
+  int end_off = 0;                        // resident: forward end mapping in `maps`
   int fwd_exchanges = 0, bwd_exchanges = 0;
+  int max_pass_slots = 0;
   size_t lds_fwd = 0, lds_bwd = 0, lds_tab = 0, lds_acc = 0;
 };
 
@@ -101,6 +126,40 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, Pl
 // Kernel launchers (kernels.hip).  Return 0 or a hipError_t value.
 int launch_resident_forward(const Plan& plan, const TileArgs& a, int64_t blocks, void* stream);
 int launch_resident_backward(const Plan& plan, const TileArgs& a, int64_t blocks, void* stream);
+
+// Arguments of one streaming pass (1024 threads, one 2^14 tile per workgroup).
+struct PassArgs {
+  const uint32_t* ins;
+  int32_t n_ins;
+  const uint32_t* cols;
+  const uint32_t* io;          // tile I/O columns (k + ng)
+  const uint8_t* start_phys;   // logical -> phys at pass start
+  const uint8_t* end_phys;     // logical -> phys at pass end
+  const int32_t* pslots;       // pass-local -> global gradient slot
+  int32_t n_pslots;
+  int32_t flags;
+  const int32_t* occ_src;
+  const int32_t* occ_idx;
+  const float* occ_cs;
+  int32_t n_occ, n_slots, P, F, n, k, ng;
+  int64_t B;
+  const float* params;
+  const float* inputs;
+  const void* psi_src;        // float2 states, logical order [B][2^n]
+  void* psi_dst;
+  const void* lam_src;
+  void* lam_dst;
+  float* epart;                // [B * 2^ng, n] <Z> partial sums
+  float* gpart;                // [B * 2^ng, n_slots] gradient partial sums
+  const float* grad_out;
+  uint32_t lds_tab, lds_acc;
+};
+int launch_stream_pass(bool bwd, const PassArgs& a, int64_t blocks, size_t lds, void* stream);
+int launch_reduce_e(int64_t batch, int ng, int n, const float* epart, float* e, void* stream);
+int launch_reduce_grad(int64_t batch, int ng, int n_slots, int P, int F, const float* gpart,
+                       float* dparams, float* dinputs, void* stream);
+int launch_fill_zero(float* p, int64_t count, void* stream);
+int prepare_stream_kernels(size_t lds_fwd, size_t lds_bwd);
 int launch_loss_grad(int kind, int64_t batch, int n, const float* e, const float* y, float* g,
                      void* stream);
 int prepare_kernels(int wg, size_t lds_fwd, size_t lds_bwd);

@@ -117,6 +117,23 @@ def test_entangler_heavy_parity(torch_mod, n):
     check_grads(r, dpr, dxr, cot)
 
 
+@pytest.mark.parametrize("n,path,B", [(14, "stream", 3), (15, "auto", 3), (16, "auto", 2),
+                                      (17, "auto", 1)])
+def test_streaming_parity(torch_mod, n, path, B):
+    """HBM-streamed tiles of 14 qubits (n = 14 forced onto the streaming path is a
+    cross-path check of the same circuit family the resident path runs)."""
+    ops, P, F = W.random_circuit(n, 120, seed=4000 + n)
+    params, inputs = W.random_inputs(B, P, F, seed=5000 + n)
+    cot = W.random_cotangent(B, n, seed=6000 + n)
+    note(f"streaming n={n} path={path} B={B}")
+    r = gpu_run(torch_mod, ops, n, P, F, params, inputs, cot, path=path)
+    info = r["circ"].info()
+    assert info["path"] == 2 and (n == 14 or info["fwd_passes"] > 1)
+    dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
+    check_E(r["E"], Er)
+    check_grads(r, dpr, dxr, cot)
+
+
 @pytest.mark.parametrize("idx", [1, 2])
 def test_config_full_batch(torch_mod, idx):
     w = W.make_config(idx)
@@ -129,7 +146,8 @@ def test_config_full_batch(torch_mod, idx):
     check_grads(r, dpr, dxr, cot)
 
 
-@pytest.mark.parametrize("idx,rows", [(3, [0, 1, 2047, 4095]), (4, [0, 4097, 8191])])
+@pytest.mark.parametrize("idx,rows", [(3, [0, 1, 2047, 4095]), (4, [0, 4097, 8191]),
+                                      (5, [0, 255])])
 def test_config_full_batch_sampled(torch_mod, idx, rows):
     """Full batch on the GPU in the benchmark's launch configuration; the oracle
     checks sampled rows (rows are independent).  The MSE cotangent of a sampled
@@ -142,8 +160,10 @@ def test_config_full_batch_sampled(torch_mod, idx, rows):
     for i, b in enumerate(rows):
         if w.loss == "mse_z0":
             g_rows[i, 0] = 2.0 * (Er[i, 0] - w.y[b]) / w.batch
-        else:
+        elif w.loss == "mse_meanz":
             g_rows[i, :] = 2.0 * (Er[i].mean() - w.y[b]) / (w.n_qubits * w.batch)
+        else:
+            g_rows[i] = oracle.loss_cotangent(w.loss, Er[i:i + 1])[0]
     cot[rows] = g_rows.astype(np.float32)
     r = gpu_run(torch_mod, w.ops, w.n_qubits, w.n_params, w.n_inputs, w.params, w.inputs, cot)
     assert np.all(np.isfinite(r["E"])) and np.all(np.abs(r["E"]) <= 1 + 1e-5)
