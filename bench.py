@@ -26,6 +26,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "circuit evals/sec (fwd+adjoint grad) at n=4..16; % of LDS/HBM BW peak"
+CSRC = os.path.join(ROOT, "paper_2607_11985_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
 PEAK_FP32_TFLOPS = 157.3     # MI355X fp32 vector peak (packed FMA, 256 CU x 2.4 GHz)
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 DEFAULT_CONFIG = 2
@@ -72,6 +74,46 @@ def cpu_baseline(w, budget_s=12.0):
                       f"{dt:.1f} s, forward + loss cotangent + VJP in complex128"}
 
 
+def kernel_source_hash():
+    """Hash of the HIP/C++ sources; traffic counters taken on other sources are stale."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".cpp", ".h")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch from the committed counter record, or None when the
+    record is missing or was taken on different kernel sources."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != kernel_source_hash():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("bytes_per_launch")
+
+
+def copy_calibration(size_mib=1024, reps=10):
+    """A plain device-to-device copy of known size, for scaling the HBM counters."""
+    import torch
+    n = size_mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}), flush=True)
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -90,7 +132,12 @@ def main():
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this engine runs on one GPU: samples are independent, so a "
                           "multi-GPU run would shard the batch with no communication; "
@@ -177,10 +224,12 @@ def main():
     dom_ms = bwd_ms if dominant == "backward" else fwd_ms
     flops = (f_bwd if dominant == "backward" else f_fwd) * B
     achieved = flops / (dom_ms / 1e3) / 1e12
-    roofline = {"bound": "alu", "kernel": f"resident_kernel ({dominant})", "achieved": achieved,
+    kname = ("stream_kernel" if info["path"] == 2 else "resident_kernel") + f" ({dominant})"
+    roofline = {"bound": "alu", "kernel": kname, "achieved": achieved,
                 "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS,
-                "traffic": None,
-                "flops_per_launch": flops, "avg_launch_ms": dom_ms}
+                "traffic": measured_traffic(w.name, dominant),
+                "flops_per_launch": flops, "avg_launch_ms": dom_ms,
+                "source_hash": kernel_source_hash()}
 
     out = {
         "metric": METRIC, "value": value, "unit": "circuit evals/s", "n_gpus": 1,
