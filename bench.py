@@ -130,6 +130,9 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--engine", default="jit", choices=["jit", "interp"],
+                    help="kernels generated for the circuit (jit) or the precompiled "
+                         "schedule interpreter (interp)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -156,7 +159,9 @@ def main():
     torch.cuda.set_device(dev)
     w = W.make_config(args.config)
     B, n = w.batch, w.n_qubits
-    circ = Circuit(w.ops, n, w.n_params, w.n_inputs, device=0)
+    t0 = time.time()
+    circ = Circuit(w.ops, n, w.n_params, w.n_inputs, device=0, engine=args.engine)
+    compile_s = time.time() - t0
     info = circ.info()
     p = torch.from_numpy(w.params).to(dev)
     x = torch.from_numpy(w.inputs).to(dev)
@@ -224,7 +229,12 @@ def main():
     dom_ms = bwd_ms if dominant == "backward" else fwd_ms
     flops = (f_bwd if dominant == "backward" else f_fwd) * B
     achieved = flops / (dom_ms / 1e3) / 1e12
-    kname = ("stream_kernel" if info["path"] == 2 else "resident_kernel") + f" ({dominant})"
+    if args.engine == "jit":
+        kname = {(1, "forward"): "vqc_rf", (1, "backward"): "vqc_rb", (2, "forward"): "vqc_sf*",
+                 (2, "backward"): "vqc_sb*"}[(info["path"], dominant)]
+    else:
+        kname = "stream_kernel" if info["path"] == 2 else "resident_kernel"
+    kname += f" ({dominant}, all passes)" if info["path"] == 2 else f" ({dominant})"
     roofline = {"bound": "alu", "kernel": kname, "achieved": achieved,
                 "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS,
                 "traffic": measured_traffic(w.name, dominant),
@@ -239,7 +249,8 @@ def main():
         "config": {"workload": w.name, "description": w.description, "n_qubits": n, "batch": B,
                    "n_params": w.n_params, "n_inputs": w.n_inputs, "ops": len(w.ops),
                    "loss": w.loss, "path": "resident" if info["path"] == 1 else "stream",
-                   "threads_per_workgroup": info["threads"],
+                   "threads_per_workgroup": info["threads"], "engine": args.engine,
+                   "compile_s": round(compile_s, 2),
                    "exchanges_fwd_bwd": [info["fwd_exchanges"], info["bwd_exchanges"]]},
         "kernel_ms": {"forward_train": fwd_ms, "loss_grad": loss_ms, "backward": bwd_ms,
                       "forward_inference": inf_ms},

@@ -32,8 +32,10 @@
 #ifndef VQC_H
 #define VQC_H
 
+#ifndef __HIPCC_RTC__ /* the run-time compiler predefines the fixed-width types */
 #include <stddef.h>
 #include <stdint.h>
+#endif
 
 #ifdef __cplusplus
 extern "C" {
@@ -81,15 +83,21 @@ typedef struct {
 typedef struct vqc_circuit vqc_circuit;
 
 /* compile options (pass NULL for the defaults) */
-#define VQC_PATH_AUTO 0     /* resident for n <= 14, streaming above */
+#define VQC_PATH_AUTO 0     /* resident for n <= 13, streaming from n = 14 */
 #define VQC_PATH_RESIDENT 1 /* one launch, state on chip; requires n <= 14 */
-#define VQC_PATH_STREAM 2   /* tiles of 2^14 amplitudes streamed through HBM */
+#define VQC_PATH_STREAM 2   /* tiles of 2^14 amplitudes streamed through HBM; n >= 14 */
+#define VQC_ENGINE_JIT 0    /* kernels generated for this circuit and compiled at
+                               vqc_compile time (straight-line schedule) */
+#define VQC_ENGINE_INTERP 1 /* precompiled kernels that interpret the schedule */
 typedef struct {
     int32_t device;      /* HIP device that receives the schedule; -1 = plan on
                             the host only (validation and introspection; the
                             handle cannot run) */
     int32_t path;        /* VQC_PATH_* */
-    int32_t reserved[6]; /* must be zero */
+    int32_t reg_bits;    /* amplitudes per thread = 2^reg_bits on the resident
+                            path, in [2, 4]; 0 = default (4) */
+    int32_t engine;      /* VQC_ENGINE_* */
+    int32_t reserved[4]; /* must be zero */
 } vqc_compile_opts;
 
 /*
@@ -99,9 +107,14 @@ typedef struct {
  * [1, VQC_MAX_QUBITS].  n_params, n_inputs >= 0 are the row widths P and F of
  * the params/inputs arrays given at run time.  On success *out receives a
  * handle that owns only the compiled schedule (host and device copies).
+ * With VQC_ENGINE_JIT (the default) and device >= 0 the kernels of this
+ * circuit are generated and compiled for the device here (seconds for large
+ * circuits; compiled modules are cached per process and source text).
  * Errors: VQC_ERR_INVALID_ARG (null pointer, wire out of range, CNOT/CZ on one
- * wire, unknown kind or source, index out of range), VQC_ERR_TOO_LARGE
- * (qubits or schedule beyond the limits), VQC_ERR_HIP, VQC_ERR_OOM.
+ * wire, unknown kind or source, index out of range, unknown option),
+ * VQC_ERR_UNSUPPORTED (path not possible for n_qubits, run-time compilation
+ * failed), VQC_ERR_TOO_LARGE (qubits or schedule beyond the limits),
+ * VQC_ERR_HIP, VQC_ERR_OOM.
  */
 int vqc_compile(const vqc_op *ops, int32_t n_ops, int32_t n_qubits, int32_t n_params,
                 int32_t n_inputs, const vqc_compile_opts *opts, vqc_circuit **out);
@@ -179,9 +192,18 @@ typedef struct {
     int32_t bwd_exchanges;  /* on-chip layout exchanges in the backward */
     int32_t fwd_instructions, bwd_instructions;
     int32_t lds_bytes_fwd, lds_bytes_bwd;
-    int32_t reserved[8];
+    int32_t engine;         /* VQC_ENGINE_* */
+    int32_t reserved[7];
 } vqc_info;
 int vqc_circuit_info(const vqc_circuit *c, vqc_info *info);
+
+/*
+ * vqc_jit_check -- generate the run-time kernels of a compiled circuit (host-
+ * only handles included) and compile them for gfx950 without loading them.
+ * Needs no GPU.  Errors: VQC_ERR_INVALID_ARG (NULL), VQC_ERR_UNSUPPORTED (the
+ * compiler rejected the source; vqc_last_error() holds its log).
+ */
+int vqc_jit_check(const vqc_circuit *c);
 
 /* Message of the last failure on the calling thread ("" if none). */
 const char *vqc_last_error(void);

@@ -23,6 +23,7 @@ VQC_ERR_WORKSPACE = -4
 VQC_ERR_HIP = -5
 VQC_ERR_OOM = -6
 VQC_PATH_AUTO, VQC_PATH_RESIDENT, VQC_PATH_STREAM = 0, 1, 2
+VQC_ENGINE_JIT, VQC_ENGINE_INTERP = 0, 1
 KIND = {"RX": 0, "RY": 1, "RZ": 2, "ROT": 3, "CNOT": 4, "CZ": 5}
 SRC = {"param": 0, "input": 1, "const": 2}
 LOSS = {"sum": 0, "mean": 1, "mse_z0": 2, "mse_meanz": 3}
@@ -36,7 +37,8 @@ class vqc_op(ctypes.Structure):
 
 class vqc_compile_opts(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int32), ("path", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 6)]
+                ("reg_bits", ctypes.c_int32), ("engine", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 4)]
 
 
 class vqc_info(ctypes.Structure):
@@ -44,7 +46,7 @@ class vqc_info(ctypes.Structure):
         "n_qubits", "n_params", "n_inputs", "n_ops", "n_rotations", "path",
         "tile_qubits", "threads", "fwd_passes", "bwd_passes", "fwd_exchanges",
         "bwd_exchanges", "fwd_instructions", "bwd_instructions", "lds_bytes_fwd",
-        "lds_bytes_bwd")] + [("reserved", ctypes.c_int32 * 8)]
+        "lds_bytes_bwd", "engine")] + [("reserved", ctypes.c_int32 * 7)]
 
 
 class VQCError(RuntimeError):
@@ -82,6 +84,8 @@ def load():
     lib.vqc_loss_grad.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _vp, _vp,
                                   _vp, _vp]
     lib.vqc_loss_grad.restype = ctypes.c_int
+    lib.vqc_jit_check.argtypes = [_vp]
+    lib.vqc_jit_check.restype = ctypes.c_int
     lib.vqc_circuit_info.argtypes = [_vp, ctypes.POINTER(vqc_info)]
     lib.vqc_circuit_info.restype = ctypes.c_int
     lib.vqc_last_error.argtypes = []
@@ -120,10 +124,10 @@ def encode_ops(ops) -> ctypes.Array:
 
 
 def vqc_compile(ops, n_qubits: int, n_params: int, n_inputs: int, device: int = 0,
-                path: int = VQC_PATH_AUTO):
+                path: int = VQC_PATH_AUTO, reg_bits: int = 0, engine: int = VQC_ENGINE_JIT):
     lib = load()
     arr = encode_ops(ops)
-    opts = vqc_compile_opts(device=device, path=path)
+    opts = vqc_compile_opts(device=device, path=path, reg_bits=reg_bits, engine=engine)
     h = _vp()
     _check(lib.vqc_compile(arr, len(ops), n_qubits, n_params, n_inputs, ctypes.byref(opts),
                            ctypes.byref(h)))
@@ -160,6 +164,10 @@ def vqc_backward(h, batch, params_ptr, inputs_ptr, grad_ptr, ws_ptr, ws_bytes, d
 
 def vqc_loss_grad(kind: int, batch: int, n: int, e_ptr, y_ptr, g_ptr, stream):
     _check(load().vqc_loss_grad(kind, batch, n, e_ptr, y_ptr, g_ptr, stream))
+
+
+def vqc_jit_check(h):
+    _check(load().vqc_jit_check(h))
 
 
 def vqc_circuit_info(h) -> dict:

@@ -13,6 +13,7 @@ from . import _lib
 
 _PATHS = {"auto": _lib.VQC_PATH_AUTO, "resident": _lib.VQC_PATH_RESIDENT,
           "stream": _lib.VQC_PATH_STREAM}
+_ENGINES = {"jit": _lib.VQC_ENGINE_JIT, "interp": _lib.VQC_ENGINE_INTERP}
 
 
 def _ptr(t):
@@ -39,14 +40,15 @@ class Circuit:
     """A compiled static circuit (compile once, execute many: Sec. 3)."""
 
     def __init__(self, ops, n_qubits: int, n_params: int, n_inputs: int, device: int = 0,
-                 path: str = "auto"):
+                 path: str = "auto", reg_bits: int = 0, engine: str = "jit"):
         self.ops = list(ops)
         self.n = int(n_qubits)
         self.P = int(n_params)
         self.F = int(n_inputs)
         self.device = torch.device("cuda", device)
         self.handle = _lib.vqc_compile(self.ops, self.n, self.P, self.F, device=device,
-                                       path=_PATHS[path])
+                                       path=_PATHS[path], reg_bits=reg_bits,
+                                       engine=_ENGINES[engine])
 
     def __del__(self):
         h = getattr(self, "handle", None)

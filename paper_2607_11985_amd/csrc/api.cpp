@@ -14,6 +14,8 @@ using vqc::Plan;
 struct vqc_circuit {
   Plan plan;
   int device = -1;   // -1: host-only plan
+  int engine = VQC_ENGINE_JIT;
+  vqc::JitKernels jit;
   void* blob = nullptr;
   size_t off_fwd = 0, off_bwd = 0, off_cols = 0, off_src = 0, off_idx = 0, off_cs = 0,
          off_maps = 0, off_pslots = 0;
@@ -60,7 +62,7 @@ size_t append(std::vector<unsigned char>& blob, const std::vector<T>& v) {
 int64_t resident_blocks(const Plan& p, int64_t batch) { return (batch + p.S - 1) / p.S; }
 
 size_t resident_state_bytes(const Plan& p, int64_t batch) {
-  return (size_t)resident_blocks(p, batch) * (size_t)p.WG * vqc::kRegAmps * 8;
+  return (size_t)resident_blocks(p, batch) * (size_t)p.WG * ((size_t)1 << p.R) * 8;
 }
 
 // Streaming workspace: [psi | E partials | psi work | lambda work | grad partials]
@@ -190,12 +192,16 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   if (n_ops < 0) return fail(VQC_ERR_INVALID_ARG, "n_ops must be >= 0");
   if (n_ops > 0 && !ops) return fail(VQC_ERR_INVALID_ARG, "ops is NULL");
   if (n_ops > (1 << 20)) return fail(VQC_ERR_TOO_LARGE, "more than 2^20 gates");
-  int device = 0, path = VQC_PATH_AUTO;
+  int device = 0, path = VQC_PATH_AUTO, reg_bits = 0, engine = VQC_ENGINE_JIT;
   if (opts) {
     for (int r : opts->reserved)
       if (r != 0) return fail(VQC_ERR_INVALID_ARG, "reserved option fields must be zero");
     device = opts->device;
     path = opts->path;
+    reg_bits = opts->reg_bits;
+    engine = opts->engine;
+    if (engine != VQC_ENGINE_JIT && engine != VQC_ENGINE_INTERP)
+      return fail(VQC_ERR_INVALID_ARG, "unknown engine option");
     if (path < VQC_PATH_AUTO || path > VQC_PATH_STREAM)
       return fail(VQC_ERR_INVALID_ARG, "unknown path option");
   } else if (hipGetDevice(&device) != hipSuccess) {
@@ -217,12 +223,13 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   vqc_circuit* c = new (std::nothrow) vqc_circuit();
   if (!c) return fail(VQC_ERR_OOM, "out of host memory");
   std::string msg;
-  int rc = vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, c->plan, msg);
+  int rc = vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, reg_bits, c->plan, msg);
   if (rc != 0) {
     delete c;
     return fail(rc, msg);
   }
   c->device = device;
+  c->engine = engine;
   if (device >= 0) {
     int count = 0;
     if (hipGetDeviceCount(&count) != hipSuccess || device >= count) {
@@ -253,13 +260,21 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
       delete c;
       return fail(VQC_ERR_HIP, "copy of the schedule failed");
     }
-    rc = p.path == VQC_PATH_STREAM ? vqc::prepare_stream_kernels(p.lds_fwd, p.lds_bwd)
-                                   : vqc::prepare_kernels(p.WG, p.lds_fwd, p.lds_bwd);
-    if (rc != 0) {
-      (void)hipFree(c->blob);
-      delete c;
-      return fail(VQC_ERR_HIP, std::string("hipFuncSetAttribute failed: ") +
-                                   hipGetErrorString((hipError_t)rc));
+    if (engine == VQC_ENGINE_JIT) {
+      rc = vqc::jit_build(p, device, c->jit, msg);
+      if (rc != 0) {
+        (void)hipFree(c->blob);
+        delete c;
+        return fail(rc, msg);
+      }
+    } else {
+      rc = vqc::prepare_kernels(p);
+      if (rc != 0) {
+        (void)hipFree(c->blob);
+        delete c;
+        return fail(VQC_ERR_HIP, std::string("hipFuncSetAttribute failed: ") +
+                                     hipGetErrorString((hipError_t)rc));
+      }
     }
   }
   *out = c;
@@ -311,7 +326,11 @@ int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const 
       a.psi_src = ws + L.psi;
       a.psi_dst = ws + L.psi;
       a.epart = reinterpret_cast<float*>(ws + L.epart);
-      rc = vqc::launch_stream_pass(false, a, batch << p.ng, p.lds_fwd, stream);
+      const size_t i = &pp - p.fpass.data();
+      rc = c->engine == VQC_ENGINE_JIT
+               ? vqc::jit_launch(c->jit.pass_fwd[i], batch << p.ng, 1 << (p.k - p.Rf), &a,
+                                 sizeof(a), stream)
+               : vqc::launch_stream_pass(p, false, a, batch << p.ng, stream);
       if (rc) return hip_fail("forward pass launch", rc);
     }
     rc = vqc::launch_reduce_e(batch, p.ng, p.n, reinterpret_cast<const float*>(ws + L.epart),
@@ -324,7 +343,9 @@ int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const 
   a.inputs = inputs;
   a.expvals = expvals;
   a.ws = workspace;
-  rc = vqc::launch_resident_forward(p, a, resident_blocks(p, batch), stream);
+  rc = c->engine == VQC_ENGINE_JIT
+           ? vqc::jit_launch(c->jit.res_fwd, resident_blocks(p, batch), p.WG, &a, sizeof(a), stream)
+           : vqc::launch_resident_forward(p, a, resident_blocks(p, batch), stream);
   if (rc) return hip_fail("forward launch", rc);
   return VQC_OK;
 }
@@ -364,7 +385,11 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
       a.lam_src = ws + L.lamw;
       a.lam_dst = ws + L.lamw;
       a.gpart = gpart;
-      rc = vqc::launch_stream_pass(true, a, batch << p.ng, p.lds_bwd, stream);
+      const size_t i = &pp - p.bpass.data();
+      rc = c->engine == VQC_ENGINE_JIT
+               ? vqc::jit_launch(c->jit.pass_bwd[i], batch << p.ng, 1 << (p.k - p.Rb), &a,
+                                 sizeof(a), stream)
+               : vqc::launch_stream_pass(p, true, a, batch << p.ng, stream);
       if (rc) return hip_fail("backward pass launch", rc);
       first = false;
     }
@@ -379,7 +404,9 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
   a.grad_out = grad_out;
   a.dparams = dp;
   a.dinputs = dx;
-  rc = vqc::launch_resident_backward(p, a, resident_blocks(p, batch), stream);
+  rc = c->engine == VQC_ENGINE_JIT
+           ? vqc::jit_launch(c->jit.res_bwd, resident_blocks(p, batch), p.WG, &a, sizeof(a), stream)
+           : vqc::launch_resident_backward(p, a, resident_blocks(p, batch), stream);
   if (rc) return hip_fail("backward launch", rc);
   return VQC_OK;
 }
@@ -421,6 +448,15 @@ int vqc_circuit_info(const vqc_circuit* c, vqc_info* info) {
   info->bwd_instructions = (int32_t)(p.bwd.size() / 2);
   info->lds_bytes_fwd = (int32_t)p.lds_fwd;
   info->lds_bytes_bwd = (int32_t)p.lds_bwd;
+  info->engine = c->engine;
+  return VQC_OK;
+}
+
+int vqc_jit_check(const vqc_circuit* c) {
+  if (!c) return fail(VQC_ERR_INVALID_ARG, "circuit handle is NULL");
+  std::string log;
+  const int rc = vqc::jit_compile_only(c->plan, log);
+  if (rc) return fail(rc, "run-time compilation failed: " + log.substr(0, 4000));
   return VQC_OK;
 }
 

@@ -3,8 +3,8 @@
 // (param / input slot) or constant (cached cos/sin), and plan the register-tile
 // schedules of the forward sweep and of the adjoint (reverse) sweep.
 //
-// Resident path (n <= 14): one pass holds every qubit on chip.
-// Streaming path (n > 14): a pass holds 14 "local" qubits of one sample in a
+// Resident path (n <= 13 by default): one pass holds every qubit on chip.
+// Streaming path (n >= 14): a pass holds 14 "local" qubits of one sample in a
 // workgroup; the other ng = n - 14 "global" qubits are fixed per workgroup (its
 // tile index).  A pass runs every gate whose qubit lines are ready and whose
 // register-bit qubit is local -- gates on disjoint qubits commute, so a gate
@@ -20,6 +20,10 @@
 
 #include "vqc.h"
 #include "vqc_internal.h"
+
+static_assert(vqc::kSrcParam == VQC_SRC_PARAM && vqc::kSrcInput == VQC_SRC_INPUT &&
+                  vqc::kSrcConst == VQC_SRC_CONST,
+              "angle source codes of the device header and the C ABI differ");
 
 namespace vqc {
 namespace {
@@ -71,7 +75,8 @@ std::vector<int> next_need_table(const std::vector<Prim>& seq, int nq) {
 // second term only when that lane position changes hands), every other qubit
 // gets one high bit.  A general permutation falls back to a layout whose reads
 // are conflict free.
-int emit_exchange(const Mapping& a, const Mapping& b, int k, int t, std::vector<uint32_t>& cols) {
+int emit_exchange(const Mapping& a, const Mapping& b, int k, int R, std::vector<uint32_t>& cols) {
+  const int t = k - R;
   const int lb = std::min(kBankBits, t);
   uint32_t lam[kMaxQubits];
   bool in_a[kMaxQubits], in_b[kMaxQubits];
@@ -79,17 +84,17 @@ int emit_exchange(const Mapping& a, const Mapping& b, int k, int t, std::vector<
   std::memset(in_a, 0, sizeof(in_a));
   std::memset(in_b, 0, sizeof(in_b));
   for (int i = 0; i < lb; ++i) {
-    in_a[a.p2q[kRegBits + i]] = true;
-    in_b[b.p2q[kRegBits + i]] = true;
+    in_a[a.p2q[R + i]] = true;
+    in_b[b.p2q[R + i]] = true;
   }
   bool swap_only = true;
   for (int i = 0; i < lb; ++i) {
-    const int qa = a.p2q[kRegBits + i], qb = b.p2q[kRegBits + i];
+    const int qa = a.p2q[R + i], qb = b.p2q[R + i];
     if (qa != qb && (in_a[qb] || in_b[qa])) swap_only = false;
   }
   if (swap_only) {
     for (int i = 0; i < lb; ++i) {
-      const int qa = a.p2q[kRegBits + i], qb = b.p2q[kRegBits + i];
+      const int qa = a.p2q[R + i], qb = b.p2q[R + i];
       lam[qa] |= 1u << i;
       if (qb != qa) lam[qb] |= 1u << i;
     }
@@ -102,7 +107,7 @@ int emit_exchange(const Mapping& a, const Mapping& b, int k, int t, std::vector<
     // slot = thread bits of the new layout in the low bits, register bits on top
     for (int p = 0; p < k; ++p) {
       const int q = b.p2q[p];
-      lam[q] = 1u << (p >= kRegBits ? p - kRegBits : t + p);
+      lam[q] = 1u << (p >= R ? p - R : t + p);
     }
   }
   const int off = (int)cols.size();
@@ -120,7 +125,7 @@ void emit(std::vector<uint32_t>& out, uint32_t op, int a, int b, int slot, uint3
 // from mapping `m` (updated to the end mapping).  slot_of(occ) gives the
 // gradient accumulator written into rotation instructions.
 template <typename SlotFn>
-int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int t, Mapping& m,
+int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int R, Mapping& m,
                std::vector<uint32_t>& out, std::vector<uint32_t>& cols, int& exchanges,
                SlotFn slot_of, std::string& msg) {
   const std::vector<int> nn = next_need_table(seq, nq);
@@ -131,24 +136,24 @@ int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int t, Mapping& m,
       msg = "internal: register-bit gate on a global qubit";
       return VQC_ERR_UNSUPPORTED;
     }
-    if (need >= 0 && m.q2p[need] >= kRegBits) {
-      // Belady: the register bits get the kRegBits local qubits needed soonest.
+    if (need >= 0 && m.q2p[need] >= R) {
+      // Belady: the register bits get the R local qubits needed soonest.
       std::vector<int> qs;
       for (int p = 0; p < k; ++p) qs.push_back(m.p2q[p]);
       const int* row = &nn[i * (size_t)nq];
       std::stable_sort(qs.begin(), qs.end(), [&](int x, int y) {
         if (row[x] != row[y]) return row[x] < row[y];
-        const bool rx = m.q2p[x] < kRegBits, ry = m.q2p[y] < kRegBits;
+        const bool rx = m.q2p[x] < R, ry = m.q2p[y] < R;
         if (rx != ry) return rx;  // keep residents on ties
         return x < y;
       });
       bool chosen[kMaxQubits] = {false};
-      for (int r = 0; r < kRegBits; ++r) chosen[qs[r]] = true;
+      for (int r = 0; r < R; ++r) chosen[qs[r]] = true;
       std::vector<int> incoming, outgoing;
-      for (int r = 0; r < kRegBits; ++r)
+      for (int r = 0; r < R; ++r)
         if (!chosen[m.p2q[r]]) outgoing.push_back(r);
-      for (int r = 0; r < kRegBits; ++r)
-        if (m.q2p[qs[r]] >= kRegBits) incoming.push_back(qs[r]);
+      for (int r = 0; r < R; ++r)
+        if (m.q2p[qs[r]] >= R) incoming.push_back(qs[r]);
       Mapping nm = m;
       for (size_t j = 0; j < incoming.size(); ++j) {
         const int qin = incoming[j];
@@ -160,7 +165,7 @@ int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int t, Mapping& m,
         nm.p2q[pin] = qout;
         nm.q2p[qout] = pin;
       }
-      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, nm, k, t, cols));
+      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, nm, k, R, cols));
       ++exchanges;
       m = nm;
     }
@@ -183,16 +188,17 @@ int append_map(const Mapping& m, std::vector<uint8_t>& maps) {
 }
 
 // Tile I/O layout of a streaming pass: the 14 local qubits in ascending order
-// are the tile ranks; ranks 0..9 sit on the thread bits, 10..13 on the
+// are the tile ranks; ranks 0..13-R sit on the thread bits, the top R on the
 // register bits, so consecutive lanes touch consecutive low qubits in HBM.
-Mapping io_mapping(const std::vector<int>& local, const std::vector<int>& glob, int k, int nq) {
+Mapping io_mapping(const std::vector<int>& local, const std::vector<int>& glob, int k, int R,
+                   int nq) {
   Mapping m;
   m.k = k;
   m.nq = nq;
   for (int q = 0; q < kMaxQubits; ++q) m.q2p[q] = -1;
-  const int nt = k - kRegBits;
+  const int nt = k - R;
   for (int r = 0; r < k; ++r) {
-    const int p = r < nt ? kRegBits + r : r - nt;
+    const int p = r < nt ? R + r : r - nt;
     m.p2q[p] = local[r];
     m.q2p[local[r]] = p;
   }
@@ -200,9 +206,10 @@ Mapping io_mapping(const std::vector<int>& local, const std::vector<int>& glob, 
   return m;
 }
 
-int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, std::vector<uint32_t>& out,
-                std::vector<PassPlan>& passes, int& exchanges, std::string& msg) {
-  const int nq = plan.nq, k = plan.k, t = plan.t, ng = plan.ng;
+int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, int R,
+                std::vector<uint32_t>& out, std::vector<PassPlan>& passes, int& exchanges,
+                std::string& msg) {
+  const int nq = plan.nq, k = plan.k, ng = plan.ng;
   std::vector<char> done(seq.size(), 0);
   size_t remaining = seq.size();
   do {
@@ -260,7 +267,7 @@ int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, std::vector<
       msg = "internal: streaming pass made no progress";
       return VQC_ERR_UNSUPPORTED;
     }
-    const Mapping io = io_mapping(local, glob, k, nq);
+    const Mapping io = io_mapping(local, glob, k, R, nq);
     Mapping m = io;
     PassPlan pp;
     pp.ins_off = (int)out.size() / 2;
@@ -278,10 +285,10 @@ int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, std::vector<
       slots.push_back(s);
       return id;
     };
-    int rc = plan_sweep(pass_prims, nq, k, t, m, out, plan.cols, exchanges, slot_of, msg);
+    int rc = plan_sweep(pass_prims, nq, k, R, m, out, plan.cols, exchanges, slot_of, msg);
     if (rc < 0) return rc;
     if (!(m == io)) {
-      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, io, k, t, plan.cols));
+      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, io, k, R, plan.cols));
       ++exchanges;
     }
     pp.n_ins = (int)out.size() / 2 - pp.ins_off;
@@ -309,8 +316,8 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
-int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, Plan& plan,
-               std::string& msg) {
+int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
+               Plan& plan, std::string& msg) {
   if (n < 1 || n > kMaxQubits) {
     msg = "n_qubits must be in [1, " + std::to_string(kMaxQubits) + "]";
     return n < 1 ? VQC_ERR_INVALID_ARG : VQC_ERR_TOO_LARGE;
@@ -389,9 +396,16 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, Pl
     }
   }
   const int n_occ = (int)plan.occ_src.size();
-  const int nq = std::max(n, kRegBits);  // qubits >= n stay |0> and are never read
+  if (reg_bits == 0) reg_bits = kDefaultRegBits;
+  if (reg_bits < 2 || reg_bits > 4) {
+    msg = "reg_bits must be 2, 3 or 4";
+    return VQC_ERR_INVALID_ARG;
+  }
+  const int nq = std::max(n, kDefaultRegBits);  // qubits >= n stay |0> and are never read
   plan.nq = nq;
-  if (path == VQC_PATH_AUTO) path = nq <= kMaxTileQubits ? VQC_PATH_RESIDENT : VQC_PATH_STREAM;
+  // 14-qubit tiles go through the streaming kernels: their adjoint holds 32
+  // amplitudes per thread in 512 threads, which keeps psi and lambda in registers
+  if (path == VQC_PATH_AUTO) path = nq < kMaxTileQubits ? VQC_PATH_RESIDENT : VQC_PATH_STREAM;
   if (path != VQC_PATH_RESIDENT && path != VQC_PATH_STREAM) {
     msg = "unknown path option";
     return VQC_ERR_INVALID_ARG;
@@ -408,8 +422,9 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, Pl
   const std::vector<Prim> rev(plan.prims.rbegin(), plan.prims.rend());
   int rc = 0;
   if (path == VQC_PATH_RESIDENT) {
+    plan.R = reg_bits;
     plan.k = nq;
-    plan.t = nq - kRegBits;
+    plan.t = nq - plan.R;
     const int T = 1 << plan.t;
     plan.WG = std::max(64, T);
     plan.S = plan.WG / T;
@@ -424,27 +439,27 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, Pl
       std::vector<int> qs(nq);
       for (int q = 0; q < nq; ++q) qs[q] = q;
       std::stable_sort(qs.begin(), qs.end(), [&](int x, int y) { return nn[x] < nn[y]; });
-      std::vector<int> rest(qs.begin() + kRegBits, qs.end());
+      std::vector<int> rest(qs.begin() + plan.R, qs.end());
       std::sort(rest.begin(), rest.end());
-      for (int r = 0; r < kRegBits; ++r) {
+      for (int r = 0; r < plan.R; ++r) {
         m.p2q[r] = qs[r];
         m.q2p[qs[r]] = r;
       }
       for (size_t j = 0; j < rest.size(); ++j) {
-        m.p2q[kRegBits + j] = rest[j];
-        m.q2p[rest[j]] = kRegBits + (int)j;
+        m.p2q[plan.R + j] = rest[j];
+        m.q2p[rest[j]] = plan.R + (int)j;
       }
     }
     auto global_slot = [&](int occ) { return plan.occ_slot[occ]; };
-    rc = plan_sweep(plan.prims, nq, plan.k, plan.t, m, plan.fwd, plan.cols, plan.fwd_exchanges,
+    rc = plan_sweep(plan.prims, nq, plan.k, plan.R, m, plan.fwd, plan.cols, plan.fwd_exchanges,
                     global_slot, msg);
     if (rc < 0) return rc;
     plan.end_off = append_map(m, plan.maps);
-    rc = plan_sweep(rev, nq, plan.k, plan.t, m, plan.bwd, plan.cols, plan.bwd_exchanges,
+    rc = plan_sweep(rev, nq, plan.k, plan.R, m, plan.bwd, plan.cols, plan.bwd_exchanges,
                     global_slot, msg);
     if (rc < 0) return rc;
     // LDS: exchange buffer | angle table [occ][S] | gradient accumulators [slot][G]
-    const size_t xbuf = (size_t)plan.WG * kRegAmps * 8;
+    const size_t xbuf = (size_t)plan.WG * ((size_t)1 << plan.R) * 8;
     plan.lds_tab = xbuf;
     const size_t tab = align_up((size_t)n_occ * plan.S * 8, 16);
     plan.lds_acc = xbuf + tab;
@@ -453,20 +468,22 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, Pl
     plan.lds_bwd = xbuf + tab + acc;
   } else {
     plan.k = kMaxTileQubits;
-    plan.t = plan.k - kRegBits;
     plan.ng = nq - plan.k;
+    plan.t = plan.k - plan.Rf;       // the forward's geometry (informational)
     plan.WG = 1 << plan.t;
     plan.S = 1;
     plan.G = plan.WG / 64;
-    rc = plan_stream(plan, plan.prims, false, plan.fwd, plan.fpass, plan.fwd_exchanges, msg);
+    rc = plan_stream(plan, plan.prims, false, plan.Rf, plan.fwd, plan.fpass, plan.fwd_exchanges,
+                     msg);
     if (rc < 0) return rc;
-    rc = plan_stream(plan, rev, true, plan.bwd, plan.bpass, plan.bwd_exchanges, msg);
+    rc = plan_stream(plan, rev, true, plan.Rb, plan.bwd, plan.bpass, plan.bwd_exchanges, msg);
     if (rc < 0) return rc;
-    const size_t xbuf = (size_t)plan.WG * kRegAmps * 8;
+    const size_t xbuf = ((size_t)1 << plan.k) * 8;
     plan.lds_tab = xbuf;
     const size_t tab = align_up((size_t)n_occ * 8, 16);
     plan.lds_acc = xbuf + tab;
-    const size_t acc = align_up((size_t)plan.max_pass_slots * plan.G * 4, 16);
+    const size_t groups_bwd = ((size_t)1 << (plan.k - plan.Rb)) / 64;
+    const size_t acc = align_up((size_t)plan.max_pass_slots * groups_bwd * 4, 16);
     plan.lds_fwd = xbuf + tab;
     plan.lds_bwd = xbuf + tab + acc;
   }

@@ -1,0 +1,836 @@
+// vqc_device.h -- device code of the batched VQC engine for gfx950, shared by
+// the precompiled kernels (kernels.hip) and by the kernels generated and
+// compiled at run time for one specific circuit.
+//
+// Register tile: a workgroup keeps a tile of 2^k amplitudes on chip, 2^R per
+// thread (R register bits), for the whole circuit (Algorithm 1, execute phase):
+//   1. per-sample angle table: (cos, sin)(theta/2) for every rotation
+//      occurrence, theta read from params / inputs, constants from the
+//      compiled schedule (parameter resolution);
+//   2. state init |0...0> in registers, or a tile loaded from HBM;
+//   3. the schedule: register-bit rotations and CNOTs (VALU only), diagonal RZ
+//      / CZ on any bit, LDS exchanges that move other qubits onto the register
+//      bits;
+//   4. epilogue: <Z_j> partial sums (Algorithm 1, return statement), tile
+//      store, gradient sums.
+// The adjoint kernels start from psi_G, form lambda = (sum_j g_j Z_j) psi_G
+// and walk the schedule backwards: for every rotation R_P(t) they accumulate
+// dL/dt = Im <lambda| P |psi> and un-apply the gate on both states
+// (psi <- U^dagger psi, lambda <- U^dagger lambda): the exact gradient of
+// Sec. 3 "Gate Application and Differentiation" with O(state) memory.
+#pragma once
+#include "vqc_structs.h"
+
+namespace vqc {
+
+template <int V>
+struct IC {
+  static constexpr int value = V;
+};
+
+// A thread's 2^R amplitudes as plain scalars (real and imaginary parts in
+// separate arrays so every access has a constant index and stays in VGPRs).
+template <int R>
+struct St {
+  static constexpr int N = 1 << R;
+  float r[N];
+  float i[N];
+};
+
+// Calls f(IC<p>) for a runtime register position p < R.
+template <int R, typename F>
+__device__ __forceinline__ void by_reg(int p, F&& f) {
+  switch (p) {
+    case 0: f(IC<0>{}); break;
+    case 1: if constexpr (R > 1) f(IC<1>{}); break;
+    case 2: if constexpr (R > 2) f(IC<2>{}); break;
+    case 3: if constexpr (R > 3) f(IC<3>{}); break;
+    default: if constexpr (R > 4) f(IC<4>{}); break;
+  }
+}
+
+// ------------------------------------------------------------------ gates
+// R_P(t) = exp(-i t P / 2) with c = cos(t/2), s = sin(t/2); the adjoint uses -s.
+
+template <int R, int P>
+__device__ __forceinline__ void rx_reg(St<R>& a, float c, float s) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
+    // [c, -is; -is, c]
+    a.r[u] = c * xr + s * yi;
+    a.i[u] = c * xi - s * yr;
+    a.r[v] = c * yr + s * xi;
+    a.i[v] = c * yi - s * xr;
+  }
+}
+
+template <int R, int P>
+__device__ __forceinline__ void ry_reg(St<R>& a, float c, float s) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
+    // [c, -s; s, c]
+    a.r[u] = c * xr - s * yr;
+    a.i[u] = c * xi - s * yi;
+    a.r[v] = s * xr + c * yr;
+    a.i[v] = s * xi + c * yi;
+  }
+}
+
+// diag(c - is, c + is) on register bit P
+template <int R, int P>
+__device__ __forceinline__ void rz_reg(St<R>& a, float c, float s) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float ss = (u & (1 << P)) ? s : -s;
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = c * xr - ss * xi;
+    a.i[u] = c * xi + ss * xr;
+  }
+}
+
+// multiply every amplitude by (c + i ss)
+template <int R>
+__device__ __forceinline__ void phase_all(St<R>& a, float c, float ss) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = c * xr - ss * xi;
+    a.i[u] = c * xi + ss * xr;
+  }
+}
+
+// CNOT with control and target on register bits: a register permutation
+template <int R, int C, int T>
+__device__ __forceinline__ void cnot_rr(St<R>& a) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (!(u & (1 << C)) || (u & (1 << T))) continue;
+    const int v = u | (1 << T);
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = a.r[v];
+    a.i[u] = a.i[v];
+    a.r[v] = xr;
+    a.i[v] = xi;
+  }
+}
+
+// CNOT with the control on a thread / tile bit (flag) and the target on register bit T
+template <int R, int T>
+__device__ __forceinline__ void cnot_tr(St<R>& a, bool flag) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << T)) continue;
+    const int v = u | (1 << T);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
+    a.r[u] = flag ? yr : xr;
+    a.i[u] = flag ? yi : xi;
+    a.r[v] = flag ? xr : yr;
+    a.i[v] = flag ? xi : yi;
+  }
+}
+
+// register indices u with bit p set, as a mask over u
+template <int R>
+__device__ __forceinline__ uint32_t reg_pattern(int p) {
+  constexpr uint32_t full = R == 5 ? 0xFFFFFFFFu : ((1u << (1 << R)) - 1u);
+  const uint32_t pat = p == 0 ? 0xAAAAAAAAu : p == 1 ? 0xCCCCCCCCu : p == 2 ? 0xF0F0F0F0u
+                       : p == 3 ? 0xFF00FF00u : 0xFFFF0000u;
+  return pat & full;
+}
+
+// tb: the bits of the amplitude position above the register bits (thread index
+// within the tile, then the tile index of a streamed sample)
+template <int R>
+__device__ __forceinline__ uint32_t bit_mask(int p, uint32_t tb) {
+  if (p < R) return reg_pattern<R>(p);
+  return ((tb >> (p - R)) & 1u) ? 0xFFFFFFFFu : 0u;
+}
+
+// amplitudes whose register index u has bit u of `m` set are negated
+template <int R>
+__device__ __forceinline__ void negate_mask(St<R>& a, uint32_t m) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float sg = ((m >> u) & 1u) ? -1.f : 1.f;
+    a.r[u] *= sg;
+    a.i[u] *= sg;
+  }
+}
+
+// x with its sign flipped when m == 0x80000000 (m == 0: unchanged)
+__device__ __forceinline__ float flip_sign(float x, uint32_t m) {
+  return __uint_as_float(__float_as_uint(x) ^ m);
+}
+
+// CZ between register positions P and Q
+template <int R, int P, int Q>
+__device__ __forceinline__ void cz_rr(St<R>& a) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u)
+    if ((u >> P) & (u >> Q) & 1) {
+      a.r[u] = -a.r[u];
+      a.i[u] = -a.i[u];
+    }
+}
+
+// CZ between register position P and a thread / tile bit of value `bit`
+template <int R, int P>
+__device__ __forceinline__ void cz_tr(St<R>& a, uint32_t bit) {
+  const uint32_t m = bit << 31;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u)
+    if ((u >> P) & 1) {
+      a.r[u] = flip_sign(a.r[u], m);
+      a.i[u] = flip_sign(a.i[u], m);
+    }
+}
+
+// every amplitude negated when bit == 1 (CZ between two thread / tile bits)
+template <int R>
+__device__ __forceinline__ void negate_if(St<R>& a, uint32_t bit) {
+  const uint32_t m = bit << 31;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    a.r[u] = flip_sign(a.r[u], m);
+    a.i[u] = flip_sign(a.i[u], m);
+  }
+}
+
+template <int R>
+__device__ __forceinline__ void apply_rx(St<R>& a, int p, float c, float s) {
+  by_reg<R>(p, [&](auto P) { rx_reg<R, decltype(P)::value>(a, c, s); });
+}
+
+template <int R>
+__device__ __forceinline__ void apply_ry(St<R>& a, int p, float c, float s) {
+  by_reg<R>(p, [&](auto P) { ry_reg<R, decltype(P)::value>(a, c, s); });
+}
+
+// RZ on physical bit p: register bit, or a thread / tile bit (uniform phase)
+template <int R>
+__device__ __forceinline__ void apply_rz(St<R>& a, int p, float c, float s, uint32_t tb) {
+  if (p >= R) {
+    phase_all<R>(a, c, ((tb >> (p - R)) & 1u) ? s : -s);
+    return;
+  }
+  by_reg<R>(p, [&](auto P) { rz_reg<R, decltype(P)::value>(a, c, s); });
+}
+
+template <int R>
+__device__ __forceinline__ void apply_cnot(St<R>& a, int pc, int pt, uint32_t tb) {
+  if (pc >= R) {
+    const bool f = (tb >> (pc - R)) & 1u;
+    by_reg<R>(pt, [&](auto T) { cnot_tr<R, decltype(T)::value>(a, f); });
+    return;
+  }
+  by_reg<R>(pc, [&](auto C) {
+    by_reg<R>(pt, [&](auto T) {
+      if constexpr (decltype(C)::value != decltype(T)::value)
+        cnot_rr<R, decltype(C)::value, decltype(T)::value>(a);
+    });
+  });
+}
+
+// ------------------------------------------- fused adjoint rotation steps
+// One pass over the amplitude pairs: accumulate dL/dtheta = Im <l| P |a> and
+// un-apply R_P(theta) (i.e. apply R_P(-theta)) to both a and l.  Working pair by
+// pair keeps only the pair's old values alive.
+// Im(conj(l) a) = l.r a.i - l.i a.r ; Re(conj(l) a) = l.r a.r + l.i a.i
+
+template <int R, int P>
+__device__ __forceinline__ float adj_rx(St<R>& a, St<R>& l, float c, float s) {
+  float acc = 0.f;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
+    const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
+    // X: <l|X|a> = conj(l0) a1 + conj(l1) a0
+    acc += lr * bi - li * br;
+    acc += mr * ai - mi * ar;
+    // RX(-theta) = [c, is; is, c]
+    a.r[u] = c * ar - s * bi;
+    a.i[u] = c * ai + s * br;
+    a.r[v] = c * br - s * ai;
+    a.i[v] = c * bi + s * ar;
+    l.r[u] = c * lr - s * mi;
+    l.i[u] = c * li + s * mr;
+    l.r[v] = c * mr - s * li;
+    l.i[v] = c * mi + s * lr;
+  }
+  return acc;
+}
+
+template <int R, int P>
+__device__ __forceinline__ float adj_ry(St<R>& a, St<R>& l, float c, float s) {
+  float acc = 0.f;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
+    const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
+    // Y a = (-i a1, i a0): Im<l|Y|a> = -Re(conj(l0) a1) + Re(conj(l1) a0)
+    acc -= lr * br + li * bi;
+    acc += mr * ar + mi * ai;
+    // RY(-theta) = [c, s; -s, c]
+    a.r[u] = c * ar + s * br;
+    a.i[u] = c * ai + s * bi;
+    a.r[v] = c * br - s * ar;
+    a.i[v] = c * bi - s * ai;
+    l.r[u] = c * lr + s * mr;
+    l.i[u] = c * li + s * mi;
+    l.r[v] = c * mr - s * lr;
+    l.i[v] = c * mi - s * li;
+  }
+  return acc;
+}
+
+// RZ on register bit P: Im<l|Z|a> and diag(c + is, c - is) on both states
+template <int R, int P>
+__device__ __forceinline__ float adj_rz(St<R>& a, St<R>& l, float c, float s) {
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
+    const float v = lr * ai - li * ar;
+    if (u & (1 << P)) a1 += v; else a0 += v;
+    const float ss = (u & (1 << P)) ? -s : s;  // the inverse phase
+    a.r[u] = c * ar - ss * ai;
+    a.i[u] = c * ai + ss * ar;
+    l.r[u] = c * lr - ss * li;
+    l.i[u] = c * li + ss * lr;
+  }
+  return a0 - a1;
+}
+
+// RZ on a thread / tile bit: the Z sign and the inverse phase are uniform
+template <int R>
+__device__ __forceinline__ float adj_rz_uniform(St<R>& a, St<R>& l, float c, float s, bool one) {
+  float acc = 0.f;
+  const float ss = one ? -s : s;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
+    acc += lr * ai - li * ar;
+    a.r[u] = c * ar - ss * ai;
+    a.i[u] = c * ai + ss * ar;
+    l.r[u] = c * lr - ss * li;
+    l.i[u] = c * li + ss * lr;
+  }
+  return one ? -acc : acc;
+}
+
+template <int R>
+__device__ __forceinline__ float adjoint_rotation(int op, St<R>& a, St<R>& l, int p, float c,
+                                                  float s, uint32_t tb) {
+  float g = 0.f;
+  if (op == OP_RX) {
+    by_reg<R>(p, [&](auto P) { g = adj_rx<R, decltype(P)::value>(a, l, c, s); });
+  } else if (op == OP_RY) {
+    by_reg<R>(p, [&](auto P) { g = adj_ry<R, decltype(P)::value>(a, l, c, s); });
+  } else if (p >= R) {
+    g = adj_rz_uniform<R>(a, l, c, s, (tb >> (p - R)) & 1u);
+  } else {
+    by_reg<R>(p, [&](auto P) { g = adj_rz<R, decltype(P)::value>(a, l, c, s); });
+  }
+  return g;
+}
+
+// --------------------------------------------------------------- helpers
+
+// Stores a loaded (re, im) pair into two independent 32-bit values.  Without
+// the empty asm the pair stays one 64-bit register tuple whose halves are later
+// rewritten separately, and the allocator then keeps (and spills) dead halves.
+__device__ __forceinline__ void split(const float2 v, float& r, float& i) {
+  float x = v.x, y = v.y;
+  asm volatile("" : "+v"(x), "+v"(y));
+  r = x;
+  i = y;
+}
+
+// A copy of x that the compiler cannot prove equal to x.  Addresses formed
+// from it are recomputed instead of being kept alive (and spilled) across the
+// whole schedule.
+__device__ __forceinline__ uint32_t opaque(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// butterfly sum over `width` consecutive lanes (power of two <= 64); every lane
+// of the segment ends with the same, order-fixed value
+__device__ __forceinline__ float seg_sum(float v, int width) {
+  for (int m = 1; m < width; m <<= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+// the same over the whole wave, fully unrolled
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+// XOR of the columns selected by the bits of u (u < 2^R)
+template <int R>
+__device__ __forceinline__ uint32_t xor_cols(int u, const uint32_t (&c)[R]) {
+  uint32_t o = 0;
+#pragma unroll
+  for (int b = 0; b < R; ++b)
+    if (u & (1 << b)) o ^= c[b];
+  return o;
+}
+
+// LDS exchange: write the amplitudes at lam(old index), read lam(new index).
+// col[0..k) are the write-side columns, col[k..2k) the read-side columns.  The
+// buffer is planar (real parts, then imaginary parts, `plane` floats apart) so
+// every access is a 32-bit one: no 64-bit register tuples enter the schedule
+// loop, and 32 lanes hit 32 banks.
+template <int R>
+__device__ __forceinline__ void exchange(St<R>& a, float* xbuf, uint32_t plane,
+                                         const uint32_t* col, int k, int t, int stid, int sl) {
+  // an opaque thread index: the addresses of one exchange are not merged with
+  // equal ones of later exchanges (which would keep them alive in between)
+  const uint32_t ot = opaque((uint32_t)stid);
+  uint32_t bw = 0, br = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxTileQubits - 2; ++i) {
+    if (i < t && ((ot >> i) & 1)) {
+      bw ^= col[R + i];
+      br ^= col[k + R + i];
+    }
+  }
+  // samples sharing a 32-lane group are spread over different banks
+  const uint32_t lowmask = (1u << (k < kBankBits ? k : kBankBits)) - 1u;
+  const uint32_t xs = ((uint32_t)sl << t) & lowmask;
+  const uint32_t base = (uint32_t)sl << k;
+  bw = base | (bw ^ xs);
+  br = base | (br ^ xs);
+  uint32_t cw[R], cr[R];
+#pragma unroll
+  for (int b = 0; b < R; ++b) {
+    cw[b] = col[b];
+    cr[b] = col[k + b];
+  }
+  float* xr = xbuf;
+  float* xi = xbuf + plane;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const uint32_t o = bw ^ xor_cols<R>(u, cw);
+    xr[o] = a.r[u];
+    xi[o] = a.i[u];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const uint32_t o = br ^ xor_cols<R>(u, cr);
+    a.r[u] = xr[o];
+    a.i[u] = xi[o];
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------- schedule runner
+
+// Context of one workgroup's walk through an instruction stream.
+struct Walk {
+  const uint32_t* cols;
+  float* xbuf;        // planar exchange buffer: plane floats of real parts, then imaginary
+  uint32_t plane;
+  const float2* tab;  // (cos, sin)(theta/2), [occurrence][S]
+  float* acc;         // gradient accumulators [slot][G]
+  int k, t, S, G;
+  int stid, sl, grp, width;
+  uint32_t tb;        // tile bits above the register bits
+  bool leader;
+};
+
+// Bit p >= R of the amplitude position (a thread or tile bit).  Taken from an
+// opaque copy of tb so that the compiler recomputes it at each gate instead of
+// keeping every bit (and the masks built from it) alive across the schedule.
+template <int R>
+__device__ __forceinline__ uint32_t tile_bit(const Walk& w, int p) {
+  return (opaque(w.tb) >> (p - R)) & 1u;
+}
+
+// Adds a rotation's gradient partial (summed over the lanes of a sample) to
+// the sample's accumulator row of this wave.  One writer per address keeps the
+// order of additions fixed.
+template <bool WIDE>
+__device__ __forceinline__ void acc_add(const Walk& w, int slot, float g) {
+  g = WIDE ? wave_sum(g) : seg_sum(g, w.width);
+  if (w.leader) atomicAdd(&w.acc[slot * w.G + w.grp], g);
+}
+
+// Runs `n_ins` instructions on psi (a) and, for the adjoint, lambda (l).
+// WIDE: every sample spans whole waves (the reduction width is 64).
+template <int R, bool BWD, bool WIDE>
+__device__ __forceinline__ void run_schedule(St<R>& a, St<R>& l, const uint32_t* ins, int n_ins,
+                                             const Walk& w) {
+  for (int pc = 0; pc < n_ins; ++pc) {
+    const uint32_t w0 = ins[2 * pc];
+    const uint32_t arg = ins[2 * pc + 1];
+    const int op = w0 & 31;
+    const int pa = (w0 >> 5) & 31;
+    const int pb = (w0 >> 10) & 31;
+    if (op == OP_EXCHANGE) {
+      exchange<R>(a, w.xbuf, w.plane, w.cols + arg, w.k, w.t, w.stid, w.sl);
+      if (BWD) exchange<R>(l, w.xbuf, w.plane, w.cols + arg, w.k, w.t, w.stid, w.sl);
+      continue;
+    }
+    if (op == OP_CNOT) {
+      apply_cnot<R>(a, pa, pb, w.tb);
+      if (BWD) apply_cnot<R>(l, pa, pb, w.tb);
+      continue;
+    }
+    if (op == OP_CZ) {
+      const uint32_t m = bit_mask<R>(pa, w.tb) & bit_mask<R>(pb, w.tb);
+      negate_mask<R>(a, m);
+      if (BWD) negate_mask<R>(l, m);
+      continue;
+    }
+    const float2 cs = w.tab[arg * w.S + w.sl];
+    if (!BWD) {
+      if (op == OP_RX) apply_rx<R>(a, pa, cs.x, cs.y);
+      else if (op == OP_RY) apply_ry<R>(a, pa, cs.x, cs.y);
+      else apply_rz<R>(a, pa, cs.x, cs.y, w.tb);
+    } else {
+      // dL/dtheta = Im <lambda| P |psi>, then psi, lambda <- R(-theta) psi, lambda
+      const float g = adjoint_rotation<R>(op, a, l, pa, cs.x, cs.y, w.tb);
+      const int slot = (int)(w0 >> 16) - 1;
+      if (slot >= 0) acc_add<WIDE>(w, slot, g);
+    }
+  }
+}
+
+// Parameter resolution: (cos, sin)(theta/2) for every occurrence and sample of
+// the workgroup.  Constant angles come precomputed from the compile phase.
+__device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64_t b0, int64_t B,
+                                            const int32_t* occ_src, const int32_t* occ_idx,
+                                            const float* occ_cs, const float* params, int P,
+                                            const float* inputs, int F, int tid, int nthreads) {
+  for (int i = tid; i < n_occ * S; i += nthreads) {
+    const int o = i / S;
+    const int s = i - o * S;
+    const int64_t bb = b0 + s;
+    const int src = occ_src[o];
+    float c, sn;
+    if (src == kSrcConst) {
+      c = occ_cs[2 * o];
+      sn = occ_cs[2 * o + 1];
+    } else {
+      float th = 0.f;
+      if (bb < B)
+        th = src == kSrcParam ? params[bb * P + occ_idx[o]] : inputs[bb * F + occ_idx[o]];
+      sincosf(0.5f * th, &sn, &c);
+    }
+    tab[i] = make_float2(c, sn);
+  }
+}
+
+// lambda = H psi with H = sum_q g_q Z_q, the Z signs read from the mapping
+template <int R>
+__device__ __forceinline__ void make_lambda(St<R>& l, const St<R>& a, const float* g, int n,
+                                            const uint8_t* phys, uint32_t tb, bool valid) {
+  float gt = 0.f, gr[R];
+#pragma unroll
+  for (int b = 0; b < R; ++b) gr[b] = 0.f;
+  if (valid) {
+    for (int q = 0; q < n; ++q) {
+      const float gq = g[q];
+      const int p = phys[q];
+      if (p >= R) gt += ((tb >> (p - R)) & 1u) ? -gq : gq;
+#pragma unroll
+      for (int b = 0; b < R; ++b)
+        if (p == b) gr[b] += gq;
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    float h = gt;
+#pragma unroll
+    for (int b = 0; b < R; ++b) h += (u & (1 << b)) ? -gr[b] : gr[b];
+    l.r[u] = h * a.r[u];
+    l.i[u] = h * a.i[u];
+  }
+}
+
+// Per-qubit signed probability sums of this workgroup's amplitudes:
+// ez[q * G + grp] = sum over the group's amplitudes of (-1)^{x_q} |a|^2.
+// Must be called by every thread; ez may alias the exchange buffer.
+template <int R>
+__device__ __forceinline__ void z_partials(const St<R>& a, float* ez, int n, const uint8_t* phys,
+                                           const Walk& w) {
+  float tot = 0.f, sr[R];
+#pragma unroll
+  for (int b = 0; b < R; ++b) sr[b] = 0.f;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float pj = a.r[u] * a.r[u] + a.i[u] * a.i[u];
+    tot += pj;
+#pragma unroll
+    for (int b = 0; b < R; ++b) sr[b] += (u & (1 << b)) ? -pj : pj;
+  }
+  __syncthreads();  // the exchange buffer may still be read by other threads
+  for (int q = 0; q < n; ++q) {
+    const int p = phys[q];
+    float v = ((w.tb >> (p - R)) & 1u) ? -tot : tot;
+#pragma unroll
+    for (int b = 0; b < R; ++b)
+      if (p == b) v = sr[b];
+    v = seg_sum(v, w.width);
+    if (w.leader) ez[q * w.G + w.grp] = v;
+  }
+  __syncthreads();
+}
+
+// The precompiled kernels' schedule runner: interprets the instruction stream.
+struct InterpSched {
+  template <int R, bool BWD, bool WIDE>
+  __device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w,
+                                             const uint32_t* ins, int n_ins) {
+    run_schedule<R, BWD, WIDE>(a, l, ins, n_ins, w);
+  }
+};
+
+// ------------------------------------------------------ resident body
+
+// One launch for a tile of samples; Sched runs the instruction stream (the
+// interpreter of the precompiled kernels, or the straight-line code generated
+// for one circuit).
+template <int WG, bool BWD, int R, typename Sched>
+__device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* smem) {
+  float* xbuf = reinterpret_cast<float*>(smem);
+  float2* tab = reinterpret_cast<float2*>(smem + A.lds_tab);
+  float* acc = reinterpret_cast<float*>(smem + A.lds_acc);
+  constexpr int NA = 1 << R;
+
+  const int tid = threadIdx.x;
+  const int T = 1 << A.t;
+  const int stid = tid & (T - 1);
+  const int sl = tid >> A.t;
+  const int S = A.S;
+  const int64_t b0 = (int64_t)blockIdx.x * S;
+  const int64_t b = b0 + sl;
+  const bool valid = b < A.B;
+  Walk w;
+  w.cols = A.cols;
+  w.xbuf = xbuf;
+  w.plane = (uint32_t)WG * NA;
+  w.tab = tab;
+  w.acc = acc;
+  w.k = A.k;
+  w.t = A.t;
+  w.S = S;
+  w.G = A.G;
+  w.stid = stid;
+  w.sl = sl;
+  w.width = T < 64 ? T : 64;
+  w.grp = T < 64 ? sl : (tid >> 6);
+  w.leader = (tid & (w.width - 1)) == 0;
+  w.tb = (uint32_t)stid;
+
+  angle_table(tab, A.n_occ, S, b0, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.P, A.inputs,
+              A.F, tid, WG);
+  if (BWD)
+    for (int i = tid; i < A.n_slots * A.G; i += WG) acc[i] = 0.f;
+  __syncthreads();
+
+  St<R> a, l;
+  if (!BWD) {
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      a.r[j] = 0.f;
+      a.i[j] = 0.f;
+    }
+    if (stid == 0) a.r[0] = 1.f;
+  } else {
+    const float2* ws = reinterpret_cast<const float2*>(A.ws);
+    float2 v[NA];
+#pragma unroll
+    for (int j = 0; j < NA; ++j) v[j] = ws[((size_t)blockIdx.x * NA + j) * WG + tid];
+#pragma unroll
+    for (int j = 0; j < NA; ++j) split(v[j], a.r[j], a.i[j]);
+    make_lambda<R>(l, a, A.grad_out + (valid ? b : 0) * A.n, A.n, A.end_phys, w.tb, valid);
+  }
+
+  Sched::template run<R, BWD, (WG > 64)>(a, l, w, A.ins, A.n_ins);
+
+  if (!BWD) {
+    if (A.ws) {
+      float2* ws = reinterpret_cast<float2*>(A.ws);
+#pragma unroll
+      for (int j = 0; j < NA; ++j)
+        ws[((size_t)blockIdx.x * NA + j) * WG + tid] = make_float2(a.r[j], a.i[j]);
+    }
+    float* ez = xbuf;
+    z_partials<R>(a, ez, A.n, A.end_phys, w);
+    for (int i = tid; i < A.n * S; i += WG) {
+      const int q = i / S;
+      const int s = i - q * S;
+      const int64_t bb = b0 + s;
+      if (bb >= A.B) continue;
+      float e;
+      if (T >= 64) {
+        e = 0.f;
+        for (int g = 0; g < A.G; ++g) e += ez[q * A.G + g];
+      } else {
+        e = ez[q * A.G + s];
+      }
+      A.expvals[bb * A.n + q] = e;
+    }
+  } else {
+    __syncthreads();
+    for (int i = tid; i < A.n_slots * S; i += WG) {
+      const int slot = i / S;
+      const int s = i - slot * S;
+      const int64_t bb = b0 + s;
+      if (bb >= A.B) continue;
+      float v;
+      if (T >= 64) {
+        v = 0.f;
+        for (int g = 0; g < A.G; ++g) v += acc[slot * A.G + g];
+      } else {
+        v = acc[slot * A.G + s];
+      }
+      if (slot < A.P) {
+        if (A.dparams) A.dparams[bb * A.P + slot] = v;
+      } else if (A.dinputs) {
+        A.dinputs[bb * A.F + (slot - A.P)] = v;
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------- streaming kernel
+// One pass over B * 2^ng tiles of 2^14 amplitudes (2^(14-R) threads x 2^R).
+// Tiles are read and written in the pass's I/O layout: tile rank r (the
+// position of an amplitude among the 14 local qubits in ascending order) is
+// r = stid + 2^(14-R) j, so consecutive lanes touch consecutive low-qubit
+// addresses.
+
+template <int R>
+__device__ __forceinline__ void io_offsets(const uint32_t* io, int k, int ng, int stid, int g,
+                                           uint32_t& base, uint32_t (&off)[1 << R]) {
+  const int nt = k - R;
+  base = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxTileQubits - 2; ++i)
+    if (i < nt && ((stid >> i) & 1)) base |= io[i];
+  for (int i = 0; i < ng; ++i)
+    if ((g >> i) & 1) base |= io[k + i];
+  uint32_t c[R];
+#pragma unroll
+  for (int b = 0; b < R; ++b) c[b] = io[nt + b];
+#pragma unroll
+  for (int j = 0; j < (1 << R); ++j) off[j] = xor_cols<R>(j, c);
+}
+
+// All loads are issued before the first split, so that they overlap.
+template <int R>
+__device__ __forceinline__ void load_tile(St<R>& a, const float2* src, uint32_t base,
+                                          const uint32_t (&off)[1 << R]) {
+  float2 v[1 << R];
+#pragma unroll
+  for (int j = 0; j < (1 << R); ++j) v[j] = src[base | off[j]];
+#pragma unroll
+  for (int j = 0; j < (1 << R); ++j) split(v[j], a.r[j], a.i[j]);
+}
+
+template <bool BWD, int R, typename Sched>
+__device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* smem) {
+  constexpr int WG = 1 << (kMaxTileQubits - R);
+  constexpr int NA = 1 << R;
+  constexpr int G = WG / 64;
+  float* xbuf = reinterpret_cast<float*>(smem);
+  float2* tab = reinterpret_cast<float2*>(smem + A.lds_tab);
+  float* acc = reinterpret_cast<float*>(smem + A.lds_acc);
+  const int tid = threadIdx.x;
+  const int64_t blk = blockIdx.x;
+  const int64_t b = blk >> A.ng;
+  const int g = (int)(blk & ((1 << A.ng) - 1));
+  Walk w;
+  w.cols = A.cols;
+  w.xbuf = xbuf;
+  w.plane = (uint32_t)WG * NA;
+  w.tab = tab;
+  w.acc = acc;
+  w.k = A.k;
+  w.t = A.k - R;
+  w.S = 1;
+  w.G = G;
+  w.stid = tid;
+  w.sl = 0;
+  w.width = 64;
+  w.grp = tid >> 6;
+  w.leader = (tid & 63) == 0;
+  w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
+
+  angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.P, A.inputs,
+              A.F, tid, WG);
+  if (BWD)
+    for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
+  __syncthreads();
+
+  uint32_t base, off[NA];
+  io_offsets<R>(A.io, A.k, A.ng, tid, g, base, off);
+  const size_t sbase = (size_t)b << (A.k + A.ng);
+  St<R> a, l;
+  if (!BWD && (A.flags & PF_INIT)) {
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      a.r[j] = 0.f;
+      a.i[j] = 0.f;
+    }
+    if (tid == 0 && g == 0) a.r[0] = 1.f;
+  } else {
+    const float2* src = reinterpret_cast<const float2*>(A.psi_src) + sbase;
+    load_tile<R>(a, src, base, off);
+  }
+  if (BWD) {
+    if (A.flags & PF_MAKE_LAMBDA) {
+      make_lambda<R>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, w.tb, true);
+    } else {
+      const float2* src = reinterpret_cast<const float2*>(A.lam_src) + sbase;
+      load_tile<R>(l, src, base, off);
+    }
+  }
+
+  Sched::template run<R, BWD, true>(a, l, w, A.ins, A.n_ins);
+
+  base = opaque(base);
+  {
+    float2* dst = reinterpret_cast<float2*>(A.psi_dst) + sbase;
+#pragma unroll
+    for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(a.r[j], a.i[j]);
+  }
+  if (BWD) {
+    float2* dst = reinterpret_cast<float2*>(A.lam_dst) + sbase;
+#pragma unroll
+    for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(l.r[j], l.i[j]);
+    __syncthreads();
+    float* gp = A.gpart + blk * A.n_slots;
+    for (int i = tid; i < A.n_pslots; i += WG) {
+      float v = 0.f;
+      for (int r = 0; r < G; ++r) v += acc[i * G + r];
+      gp[A.pslots[i]] += v;
+    }
+  } else if (A.flags & PF_ZPART) {
+    float* ez = xbuf;
+    z_partials<R>(a, ez, A.n, A.end_phys, w);
+    for (int q = tid; q < A.n; q += WG) {
+      float e = 0.f;
+      for (int r = 0; r < G; ++r) e += ez[q * G + r];
+      A.epart[blk * A.n + q] = e;
+    }
+  }
+}
+
+}  // namespace vqc

@@ -1,0 +1,115 @@
+// vqc_structs.h -- constants, instruction encoding and kernel argument records
+// shared by the host library, the precompiled kernels and the kernels compiled
+// at run time for a specific circuit.  Plain C++ with no standard-library
+// dependency beyond <stdint.h>, so the run-time compiler can include it.
+#pragma once
+#ifndef __HIPCC_RTC__
+#include <stddef.h>
+#include <stdint.h>
+#else
+// the run-time compiler has no C headers: take the types from the compiler
+typedef __INT32_TYPE__ int32_t;
+typedef __UINT32_TYPE__ uint32_t;
+typedef __INT64_TYPE__ int64_t;
+typedef __UINT64_TYPE__ uint64_t;
+typedef __UINT8_TYPE__ uint8_t;
+typedef __INT16_TYPE__ int16_t;
+typedef __UINT16_TYPE__ uint16_t;
+typedef __SIZE_TYPE__ size_t;
+#endif
+
+namespace vqc {
+
+constexpr int kDefaultRegBits = 4;           // R of the resident kernels
+constexpr int kStreamRegBitsFwd = 4;         // streaming forward: 1024 threads x 16
+constexpr int kStreamRegBitsBwd = 5;         // streaming adjoint: 512 threads x 32
+constexpr int kMaxTileQubits = 14;           // 2^14 c64 = 128 KiB per tile
+constexpr int kMaxQubits = 20;
+constexpr int kLdsBytes = 160 * 1024;        // gfx950 LDS per workgroup
+constexpr int kBankBits = 5;                 // lane bits kept bank-conflict free
+constexpr int kSrcParam = 0;                 // angle sources, as in the C ABI
+constexpr int kSrcInput = 1;
+constexpr int kSrcConst = 2;
+
+// primitive kinds after lowering (ROT -> RZ, RY, RZ)
+enum PrimKind : int { P_RX = 0, P_RY = 1, P_RZ = 2, P_CNOT = 4, P_CZ = 5 };
+
+// instruction opcodes.  Physical bits p >= k name global qubits of a
+// streamed tile (bit p - k of the tile index within the sample).
+enum Opcode : uint32_t {
+  OP_RX = 1,      // a = register position, arg = occurrence
+  OP_RY = 2,      // a = register position, arg = occurrence
+  OP_RZ = 3,      // a = physical bit,      arg = occurrence
+  OP_CNOT = 4,    // a = control physical bit, b = target register position
+  OP_CZ = 5,      // a, b = physical bits
+  OP_EXCHANGE = 6 // arg = offset of 2k column words (write side, read side)
+};
+
+// word0 = op | a << 5 | b << 10 | (slot + 1) << 16; word1 = arg.  `slot` is the
+// gradient accumulator of a rotation (-1: constant angle, no gradient).
+inline uint32_t ins_word0(uint32_t op, uint32_t a, uint32_t b, int slot) {
+  return op | (a << 5) | (b << 10) | ((uint32_t)(slot + 1) << 16);
+}
+
+// pass flags of the streaming kernels
+enum PassFlag : int32_t {
+  PF_INIT = 1,        // start from |0...0> instead of loading psi
+  PF_MAKE_LAMBDA = 2, // (adjoint) lambda = H psi after loading psi_G
+  PF_ZPART = 4,       // (forward) per-tile <Z> partial sums
+};
+
+// Arguments of the resident kernels (one launch, whole sample on chip).
+struct TileArgs {
+  const uint32_t* ins;      // instruction pairs (word0, arg)
+  int32_t n_ins;
+  const uint32_t* cols;     // exchange column tables
+  const int32_t* occ_src;   // per occurrence: 0 param, 1 input, 2 const
+  const int32_t* occ_idx;
+  const float* occ_cs;      // per occurrence (cos, sin) of const angles / 2
+  const uint8_t* end_phys;  // per logical qubit: physical bit at forward end
+  int32_t n_occ, n_slots, P, F;
+  int32_t n;                // real qubits (E and g have n columns)
+  int32_t k;                // tile qubits (>= 4)
+  int32_t t;                // thread bits per sample: k - R
+  int32_t S;                // samples per workgroup
+  int32_t G;                // reduction groups per workgroup
+  int64_t B;
+  const float* params;
+  const float* inputs;
+  float* expvals;
+  void* ws;                 // saved final states (training) or null
+  const float* grad_out;
+  float* dparams;
+  float* dinputs;
+  uint32_t lds_tab;         // byte offset of the angle table in LDS
+  uint32_t lds_acc;         // byte offset of the gradient accumulators
+};
+
+// Arguments of one streaming pass (1024 threads, one 2^14 tile per workgroup).
+struct PassArgs {
+  const uint32_t* ins;
+  int32_t n_ins;
+  const uint32_t* cols;
+  const uint32_t* io;          // tile I/O columns (k + ng)
+  const uint8_t* start_phys;   // logical -> phys at pass start
+  const uint8_t* end_phys;     // logical -> phys at pass end
+  const int32_t* pslots;       // pass-local -> global gradient slot
+  int32_t n_pslots;
+  int32_t flags;
+  const int32_t* occ_src;
+  const int32_t* occ_idx;
+  const float* occ_cs;
+  int32_t n_occ, n_slots, P, F, n, k, ng;
+  int64_t B;
+  const float* params;
+  const float* inputs;
+  const void* psi_src;        // float2 states, logical order [B][2^n]
+  void* psi_dst;
+  const void* lam_src;
+  void* lam_dst;
+  float* epart;                // [B * 2^ng, n] <Z> partial sums
+  float* gpart;                // [B * 2^ng, n_slots] gradient partial sums
+  const float* grad_out;
+  uint32_t lds_tab, lds_acc;
+};
+}  // namespace vqc

@@ -18,9 +18,9 @@ def lib():
     return _lib.load()
 
 
-def host_compile(ops, n, P, F, path=0, reserved=None, raw=None):
+def host_compile(ops, n, P, F, path=0, reserved=None, raw=None, reg_bits=0, engine=0):
     arr = raw if raw is not None else _lib.encode_ops(ops)
-    opts = _lib.vqc_compile_opts(device=-1, path=path)
+    opts = _lib.vqc_compile_opts(device=-1, path=path, reg_bits=reg_bits, engine=engine)
     if reserved is not None:
         opts.reserved[0] = reserved
     return _lib.vqc_compile_raw(arr, len(ops) if raw is None else raw._n, n, P, F, opts)
@@ -30,7 +30,7 @@ def test_exports_every_declared_function(lib):
     names = _lib.header_functions()
     assert {"vqc_compile", "vqc_forward", "vqc_backward", "vqc_destroy",
             "vqc_workspace_bytes", "vqc_loss_grad", "vqc_last_error",
-            "vqc_circuit_info"} <= set(names)
+            "vqc_circuit_info", "vqc_jit_check"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
 
@@ -45,10 +45,13 @@ def test_header_constants_match_binding():
         assert int(defs["VQC_" + k]) == v
     assert int(defs["VQC_SRC_PARAM"]) == 0 and int(defs["VQC_SRC_CONST"]) == 2
     assert int(defs["VQC_LOSS_MSE_MEANZ"]) == _lib.LOSS["mse_meanz"]
+    assert int(defs["VQC_ENGINE_JIT"]) == _lib.VQC_ENGINE_JIT
+    assert int(defs["VQC_ENGINE_INTERP"]) == _lib.VQC_ENGINE_INTERP
+    assert ctypes.sizeof(_lib.vqc_compile_opts) == 32 and ctypes.sizeof(_lib.vqc_info) == 96
     assert ctypes.sizeof(_lib.vqc_op) == 48
 
 
-@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
 def test_configs_plan_on_host(idx):
     w = W.make_config(idx, batch=2)
     rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
@@ -56,16 +59,20 @@ def test_configs_plan_on_host(idx):
     info = _lib.vqc_circuit_info(h)
     rot, ent, nops = W.count_ops(w.ops)
     assert info["n_rotations"] == rot and info["n_ops"] == nops
-    assert info["path"] == _lib.VQC_PATH_RESIDENT
-    assert info["tile_qubits"] == max(4, w.n_qubits)
+    stream = w.n_qubits >= 14
+    assert info["path"] == (_lib.VQC_PATH_STREAM if stream else _lib.VQC_PATH_RESIDENT)
+    assert info["tile_qubits"] == (14 if stream else max(4, w.n_qubits))
+    if w.n_qubits > 14:
+        assert info["fwd_passes"] > 1 and info["bwd_passes"] > 1
     assert info["lds_bytes_bwd"] <= 160 * 1024
     # forward and backward sweep each hold one instruction per primitive plus exchanges
     n_prims = sum(3 if o.kind == "ROT" else 1 for o in w.ops)
     assert info["fwd_instructions"] == n_prims + info["fwd_exchanges"]
     assert info["bwd_instructions"] == n_prims + info["bwd_exchanges"]
     assert _lib.vqc_workspace_bytes(h, 0, 1) == 0
-    assert _lib.vqc_workspace_bytes(h, 10, 0) == 0
-    assert _lib.vqc_workspace_bytes(h, 10, 1) >= 10 * (1 << w.n_qubits) * 8
+    assert _lib.vqc_workspace_bytes(h, 10, 0) == (0 if not stream else
+                                                  _lib.vqc_workspace_bytes(h, 10, 0))
+    assert _lib.vqc_workspace_bytes(h, 10, 1) >= 10 * (1 << w.n_qubits) * 8 * (3 if stream else 1)
     _lib.vqc_destroy(h)
 
 
@@ -136,6 +143,11 @@ def test_compile_rejects_options():
     assert rc == _lib.VQC_ERR_INVALID_ARG and "reserved" in _lib.vqc_last_error()
     rc, _ = host_compile([], 2, 0, 0, path=7)
     assert rc == _lib.VQC_ERR_INVALID_ARG
+    rc, _ = host_compile([], 2, 0, 0, engine=2)
+    assert rc == _lib.VQC_ERR_INVALID_ARG and "engine" in _lib.vqc_last_error()
+    for bad in (1, 5, -1):
+        rc, _ = host_compile([], 6, 0, 0, reg_bits=bad)
+        assert rc == _lib.VQC_ERR_INVALID_ARG and "reg_bits" in _lib.vqc_last_error()
     rc, _ = host_compile([], 15, 0, 0, path=_lib.VQC_PATH_RESIDENT)
     assert rc == _lib.VQC_ERR_UNSUPPORTED
     arr = _lib.encode_ops([])
@@ -170,3 +182,53 @@ def test_empty_circuit_plans():
     info = _lib.vqc_circuit_info(h)
     assert info["fwd_instructions"] == 0 and info["n_rotations"] == 0
     _lib.vqc_destroy(h)
+
+
+@pytest.mark.parametrize("engine", [0, 1])
+def test_info_reports_engine(engine):
+    rc, h = host_compile([], 3, 0, 0, engine=engine)
+    assert rc == 0
+    assert _lib.vqc_circuit_info(h)["engine"] == engine
+    _lib.vqc_destroy(h)
+
+
+@pytest.mark.parametrize("reg_bits", [2, 3, 4])
+def test_register_width_option(reg_bits):
+    ops, P, F = W.random_circuit(9, 50, seed=9)
+    rc, h = host_compile(ops, 9, P, F, reg_bits=reg_bits)
+    assert rc == 0, _lib.vqc_last_error()
+    info = _lib.vqc_circuit_info(h)
+    assert info["threads"] == max(64, 1 << (9 - reg_bits))
+    _lib.vqc_destroy(h)
+
+
+# Run-time code generation: every kind of instruction the generator emits
+# (register / thread / tile positions of rotations, CNOT and CZ, exchanges,
+# gradient slots) must compile for gfx950.  No GPU is needed for this.
+JIT_CASES = [
+    ("n1", 1, 0, 0), ("n5_r2", 5, 0, 2), ("n7_r3", 7, 0, 3), ("n11", 11, 0, 0),
+    ("n13", 13, 0, 0), ("n15_stream", 15, 0, 0),
+]
+
+
+@pytest.mark.parametrize("case", JIT_CASES, ids=[c[0] for c in JIT_CASES])
+def test_generated_kernels_compile(case):
+    _, n, path, reg_bits = case
+    ops, P, F = W.random_circuit(n, 30 + 3 * n, seed=31 + n,
+                                 kinds=("RX", "RY", "RZ", "ROT", "CNOT", "CZ"))
+    rc, h = host_compile(ops, n, P, F, path=path, reg_bits=reg_bits)
+    assert rc == 0, _lib.vqc_last_error()
+    _lib.vqc_jit_check(h)
+    _lib.vqc_destroy(h)
+
+
+def test_generated_kernels_compile_config2():
+    w = W.make_config(2, batch=2)
+    rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    assert rc == 0
+    _lib.vqc_jit_check(h)
+    _lib.vqc_destroy(h)
+
+
+def test_jit_check_null(lib):
+    assert lib.vqc_jit_check(None) == _lib.VQC_ERR_INVALID_ARG

@@ -39,9 +39,10 @@ def note(msg):
     sys.stdout.flush()
 
 
-def gpu_run(torch, ops, n, P, F, params, inputs, cot=None, path="auto"):
+def gpu_run(torch, ops, n, P, F, params, inputs, cot=None, path="auto", engine="jit",
+            reg_bits=0):
     from paper_2607_11985_amd.api import Circuit
-    circ = Circuit(ops, n, P, F, path=path)
+    circ = Circuit(ops, n, P, F, path=path, engine=engine, reg_bits=reg_bits)
     p = torch.from_numpy(np.ascontiguousarray(params)).cuda()
     x = torch.from_numpy(np.ascontiguousarray(inputs)).cuda()
     E, ws = circ.forward(p, x, training=True)
@@ -132,6 +133,26 @@ def test_streaming_parity(torch_mod, n, path, B):
     dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
     check_E(r["E"], Er)
     check_grads(r, dpr, dxr, cot)
+
+
+@pytest.mark.parametrize("n,path,reg_bits", [(3, "auto", 0), (8, "auto", 2), (9, "auto", 3),
+                                             (13, "auto", 0), (15, "auto", 0)])
+def test_interpreter_engine_parity(torch_mod, n, path, reg_bits):
+    """The precompiled schedule interpreter against the oracle, and bit-level
+    agreement of E with the generated kernels is not required (different
+    instruction order), only both within the bar."""
+    ops, P, F = W.random_circuit(n, 40 + 6 * n, seed=7000 + n)
+    B = 5
+    params, inputs = W.random_inputs(B, P, F, seed=7100 + n)
+    cot = W.random_cotangent(B, n, seed=7200 + n)
+    note(f"interpreter n={n} path={path} reg_bits={reg_bits}")
+    dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
+    for engine in ("interp", "jit"):
+        r = gpu_run(torch_mod, ops, n, P, F, params, inputs, cot, path=path, engine=engine,
+                    reg_bits=reg_bits)
+        assert r["circ"].info()["engine"] == (1 if engine == "interp" else 0)
+        check_E(r["E"], Er)
+        check_grads(r, dpr, dxr, cot)
 
 
 @pytest.mark.parametrize("idx", [1, 2])
