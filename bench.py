@@ -9,6 +9,13 @@ parameter and input), all on one HIP stream with inputs resident in HBM.
 
 Prints one JSON line.  value = circuit evaluations (forward E + full
 gradient) per second = B * K / timed seconds.
+
+The timed region replays a HIP graph that holds one whole step (the three
+calls' kernels, captured once on the step's stream), bracketed by events; a
+fixed-shape training loop runs this way.  Eager timings (per call, each
+bracketed by events) are reported next to it, and the dominant call is timed
+separately as K back-to-back launches for the roofline.  Every replay's
+outputs are checked bit for bit against an eager step.
 """
 from __future__ import annotations
 
@@ -133,6 +140,10 @@ def main():
     ap.add_argument("--engine", default="jit", choices=["jit", "interp"],
                     help="kernels generated for the circuit (jit) or the precompiled "
                          "schedule interpreter (interp)")
+    ap.add_argument("--reg-bits", type=int, default=0,
+                    help="amplitudes per thread = 2^reg_bits (0: the library's default)")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time eager launches instead of graph replays of the step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -160,7 +171,8 @@ def main():
     w = W.make_config(args.config)
     B, n = w.batch, w.n_qubits
     t0 = time.time()
-    circ = Circuit(w.ops, n, w.n_params, w.n_inputs, device=0, engine=args.engine)
+    circ = Circuit(w.ops, n, w.n_params, w.n_inputs, device=0, engine=args.engine,
+                   reg_bits=args.reg_bits)
     compile_s = time.time() - t0
     info = circ.info()
     p = torch.from_numpy(w.params).to(dev)
@@ -177,46 +189,90 @@ def main():
     loss_kind = _lib.LOSS[w.loss]
     pp, xp, yp = p.data_ptr(), x.data_ptr(), (y.data_ptr() if y is not None else None)
 
-    def fwd():
-        _lib.vqc_forward(h, B, pp, xp, E.data_ptr(), ws.data_ptr(), nb, s)
+    def fwd(st):
+        _lib.vqc_forward(h, B, pp, xp, E.data_ptr(), ws.data_ptr(), nb, st)
 
-    def loss():
-        _lib.vqc_loss_grad(loss_kind, B, n, E.data_ptr(), yp, g.data_ptr(), s)
+    def loss(st):
+        _lib.vqc_loss_grad(loss_kind, B, n, E.data_ptr(), yp, g.data_ptr(), st)
 
-    def bwd():
+    def bwd(st):
         _lib.vqc_backward(h, B, pp, xp, g.data_ptr(), ws.data_ptr(), nb, dp.data_ptr(),
-                          dx.data_ptr(), s)
+                          dx.data_ptr(), st)
+
+    def step(st):
+        fwd(st); loss(st); bwd(st)
 
     for _ in range(args.warmup):
-        fwd(); loss(); bwd()
+        step(s)
     torch.cuda.synchronize()
+    ref = [t.clone() for t in (E, g, dp, dx)]
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    # eager: every call bracketed by events (includes host launch gaps)
+    evs = [[ev() for _ in range(4)] for _ in range(K)]
+    t0e, t1e = ev(), ev()
+    torch.cuda.synchronize()
+    t0e.record(stream)
+    for k in range(K):
+        e = evs[k]
+        e[0].record(stream); fwd(s)
+        e[1].record(stream); loss(s)
+        e[2].record(stream); bwd(s)
+        e[3].record(stream)
+    t1e.record(stream)
+    torch.cuda.synchronize()
+    eager_step_ms = t0e.elapsed_time(t1e) / K
+    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    loss_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+
+    # the timed region: K replays of the captured step
+    use_graph = not args.no_graph
+    if use_graph:
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream(device=dev)  # default priority
+        cap.wait_stream(stream)
+        with torch.cuda.graph(graph, stream=cap):
+            step(cap.cuda_stream)
+        stream.wait_stream(cap)
+        torch.cuda.synchronize()
+    t_start, t_end = ev(), ev()
     torch.cuda.synchronize()
     t_start.record(stream)
-    for k in range(K):
-        e = ev[k]
-        e[0].record(stream); fwd()
-        e[1].record(stream); loss()
-        e[2].record(stream); bwd()
-        e[3].record(stream)
+    for _ in range(K):
+        if use_graph:
+            graph.replay()
+        else:
+            step(s)
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
-    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    loss_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
     ms_per_step = total_ms / K
     value = B * K / (total_ms / 1e3)
+    for t, r in zip((E, g, dp, dx), ref):
+        if not torch.equal(t, r):
+            raise SystemExit("replayed step differs from the eager step")
+
+    # dominant call, K back-to-back launches on the same stream
+    f_fwd, f_bwd = algorithmic_flops(w)
+    dominant = "backward" if bwd_ms >= fwd_ms else "forward"
+    dom_call = bwd if dominant == "backward" else fwd
+    d0, d1 = ev(), ev()
+    d0.record(stream)
+    for _ in range(K):
+        dom_call(s)
+    d1.record(stream)
+    torch.cuda.synchronize()
+    dom_ms = d0.elapsed_time(d1) / K
 
     # forward-only rate (inference, no state saved), outside the timed region
     for _ in range(3):
         circ.forward(p, x, out=E)
     torch.cuda.synchronize()
-    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0, a1 = ev(), ev()
     a0.record(stream)
     for _ in range(K):
         circ.forward(p, x, out=E)
@@ -224,9 +280,6 @@ def main():
     torch.cuda.synchronize()
     inf_ms = a0.elapsed_time(a1) / K
 
-    f_fwd, f_bwd = algorithmic_flops(w)
-    dominant = "backward" if bwd_ms >= fwd_ms else "forward"
-    dom_ms = bwd_ms if dominant == "backward" else fwd_ms
     flops = (f_bwd if dominant == "backward" else f_fwd) * B
     achieved = flops / (dom_ms / 1e3) / 1e12
     if args.engine == "jit":
@@ -250,10 +303,13 @@ def main():
                    "n_params": w.n_params, "n_inputs": w.n_inputs, "ops": len(w.ops),
                    "loss": w.loss, "path": "resident" if info["path"] == 1 else "stream",
                    "threads_per_workgroup": info["threads"], "engine": args.engine,
+                   "reg_bits": args.reg_bits or "default",
                    "compile_s": round(compile_s, 2),
                    "exchanges_fwd_bwd": [info["fwd_exchanges"], info["bwd_exchanges"]]},
+        "timing": "hip graph replay of the step" if use_graph else "eager launches",
+        "eager_ms_per_step": eager_step_ms,
         "kernel_ms": {"forward_train": fwd_ms, "loss_grad": loss_ms, "backward": bwd_ms,
-                      "forward_inference": inf_ms},
+                      "forward_inference": inf_ms, f"{dominant}_back_to_back": dom_ms},
         "forward_only_evals_per_s": B / (inf_ms / 1e3),
         "roofline": roofline,
         "env": {"torch": torch.__version__, "hip": getattr(torch.version, "hip", None),

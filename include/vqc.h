@@ -94,8 +94,9 @@ typedef struct {
                             the host only (validation and introspection; the
                             handle cannot run) */
     int32_t path;        /* VQC_PATH_* */
-    int32_t reg_bits;    /* amplitudes per thread = 2^reg_bits on the resident
-                            path, in [2, 4]; 0 = default (4) */
+    int32_t reg_bits;    /* amplitudes per thread = 2^reg_bits: resident path
+                            2, 3 or 4 (default 4); streaming path 4 or 5 for both
+                            sweeps (default: forward 4, adjoint 5); 0 = default */
     int32_t engine;      /* VQC_ENGINE_* */
     int32_t reserved[4]; /* must be zero */
 } vqc_compile_opts;

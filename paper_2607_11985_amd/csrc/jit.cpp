@@ -42,9 +42,29 @@ std::string hex(uint32_t v) {
   return b;
 }
 
+// How the adjoint kernels collect gradient partials.  Lanes are grouped by
+// sample (tm lanes: the sample's threads, at most one wave).  With `regs`, lane
+// j of a group keeps slots j, j + tm, ... in registers (nr of them) and adds
+// the group sum of each rotation's partial to the owning lane: no branch and no
+// LDS access per rotation.  Otherwise one lane adds it to the LDS accumulator.
+struct GradMode {
+  int tm = 64, ns = 0, nr = 0;
+  bool regs = false;
+};
+constexpr int kMaxGradRegs = 16;
+
+GradMode grad_mode(int lanes_per_sample, int n_slots) {
+  GradMode g;
+  g.tm = lanes_per_sample < 64 ? lanes_per_sample : 64;
+  g.ns = n_slots;
+  g.nr = (n_slots + g.tm - 1) / g.tm;
+  g.regs = g.nr <= kMaxGradRegs;
+  return g;
+}
+
 // Statements of one instruction stream for register width R.
 void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, int n_ins, bool bwd,
-                   int R, int k, int S) {
+                   int R, int k, int S, const GradMode& gm) {
   const int t = k - R;
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
@@ -102,24 +122,45 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           else
             o << "const float g = adj_rz_uniform<R>(a, l, cs.x, cs.y, tile_bit<R>(w, " << pa
               << "));";
-          if (slot >= 0) o << " acc_add<WIDE>(w, " << slot << ", g);";
-          else o << " (void)g;";
+          if (slot < 0)
+            o << " (void)g;";
+          else if (gm.regs)
+            // the empty asm keeps the update here: left free, the additions drift
+            // to the end of the kernel and every partial stays alive until then
+            o << " const float gs = group_sum<" << gm.tm << ">(g); ga[" << slot / gm.tm
+              << "] += (opaque(ln) == " << slot % gm.tm << "u) ? gs : 0.f; asm volatile(\"\" : \"+v\"(ga["
+              << slot / gm.tm << "]));";
+          else
+            o << " { const float gs = group_sum<" << gm.tm << ">(g); if (w.leader) atomicAdd(&w.acc["
+              << slot << " * w.G + w.grp], gs); }";
         }
-        o << " }\n";
+        o << " gate_boundary(w); }\n";
       }
     }
   }
 }
 
 void emit_sched_struct(std::ostringstream& o, const std::string& name, const Plan& p,
-                       const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S) {
+                       const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S,
+                       const GradMode& gm) {
   o << "struct " << name << " {\n"
     << "template <int R, bool BWD, bool WIDE>\n"
     << "__device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w, "
        "const uint32_t*, int) {\n"
     << "  (void)l;\n";
-  emit_schedule(o, p, ins, n_ins, bwd, R, k, S);
-  o << "}\n};\n";
+  const bool regs = bwd && gm.regs && gm.nr > 0;
+  if (regs)
+    o << "  const uint32_t ln = (uint32_t)w.stid & " << gm.tm - 1 << "u;\n"
+      << "  float ga[" << gm.nr << "];\n"
+      << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) ga[j] = 0.f;\n";
+  emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm);
+  if (regs)  // every (slot, group) accumulator is written by exactly one lane
+    o << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) {\n"
+      << "    const uint32_t slot = j * " << gm.tm << "u + ln;\n"
+      << "    if (slot < " << gm.ns << "u) w.acc[slot * w.G + w.grp] = ga[j];\n  }\n";
+  o << "}\n"
+    << "__device__ __forceinline__ static float lane_sum(float v, const Walk&) {\n"
+    << "  return group_sum<" << gm.tm << ">(v);\n}\n};\n";
 }
 
 size_t lds_size(size_t b) { return b < 16 ? 16 : b; }
@@ -127,10 +168,12 @@ size_t lds_size(size_t b) { return b < 16 ? 16 : b; }
 // One kernel in a program of its own, so that the kernels of a circuit compile
 // in parallel.
 std::string kernel_unit(const Plan& p, const std::string& name, const uint32_t* ins, int n_ins,
-                        bool bwd, bool stream, int R, int S, int threads, size_t lds) {
+                        bool bwd, bool stream, int R, int S, int threads, size_t lds,
+                        int n_slots) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
-  emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S);
+  const int lanes = stream ? threads : 1 << (p.k - R);
+  emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots));
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << name
     << (stream ? "(const vqc::PassArgs A) {\n" : "(const vqc::TileArgs A) {\n")
@@ -150,22 +193,22 @@ std::vector<JitUnit> jit_units(const Plan& p) {
   std::vector<JitUnit> u;
   if (p.path == VQC_PATH_RESIDENT) {
     u.push_back({"vqc_rf", kernel_unit(p, "vqc_rf", p.fwd.data(), (int)p.fwd.size() / 2, false,
-                                       false, p.R, p.S, p.WG, p.lds_fwd)});
+                                       false, p.R, p.S, p.WG, p.lds_fwd, p.P + p.F)});
     u.push_back({"vqc_rb", kernel_unit(p, "vqc_rb", p.bwd.data(), (int)p.bwd.size() / 2, true,
-                                       false, p.R, p.S, p.WG, p.lds_bwd)});
+                                       false, p.R, p.S, p.WG, p.lds_bwd, p.P + p.F)});
     return u;
   }
   for (size_t i = 0; i < p.fpass.size(); ++i) {
     const std::string name = "vqc_sf" + std::to_string(i);
     u.push_back({name, kernel_unit(p, name, p.fwd.data() + 2 * p.fpass[i].ins_off,
                                    p.fpass[i].n_ins, false, true, p.Rf, 1, 1 << (p.k - p.Rf),
-                                   p.lds_fwd)});
+                                   p.lds_fwd, p.fpass[i].n_slots)});
   }
   for (size_t i = 0; i < p.bpass.size(); ++i) {
     const std::string name = "vqc_sb" + std::to_string(i);
     u.push_back({name, kernel_unit(p, name, p.bwd.data() + 2 * p.bpass[i].ins_off,
                                    p.bpass[i].n_ins, true, true, p.Rb, 1, 1 << (p.k - p.Rb),
-                                   p.lds_bwd)});
+                                   p.lds_bwd, p.bpass[i].n_slots)});
   }
   return u;
 }

@@ -396,9 +396,8 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     }
   }
   const int n_occ = (int)plan.occ_src.size();
-  if (reg_bits == 0) reg_bits = kDefaultRegBits;
-  if (reg_bits < 2 || reg_bits > 4) {
-    msg = "reg_bits must be 2, 3 or 4";
+  if (reg_bits != 0 && (reg_bits < 2 || reg_bits > 5)) {
+    msg = "reg_bits must be 0 (default) or in [2, 5]";
     return VQC_ERR_INVALID_ARG;
   }
   const int nq = std::max(n, kDefaultRegBits);  // qubits >= n stay |0> and are never read
@@ -418,11 +417,22 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     msg = "the streaming path needs at least 14 qubits (its tiles hold 14)";
     return VQC_ERR_UNSUPPORTED;
   }
+  if (path == VQC_PATH_RESIDENT && reg_bits > 4) {
+    msg = "reg_bits on the resident path must be 2, 3 or 4";
+    return VQC_ERR_INVALID_ARG;
+  }
+  if (path == VQC_PATH_STREAM && reg_bits != 0 && reg_bits < 4) {
+    msg = "reg_bits on the streaming path must be 4 or 5";
+    return VQC_ERR_INVALID_ARG;
+  }
   plan.path = path;
   const std::vector<Prim> rev(plan.prims.rbegin(), plan.prims.rend());
   int rc = 0;
   if (path == VQC_PATH_RESIDENT) {
-    plan.R = reg_bits;
+    // default width: at least 64 threads per sample up to 8 qubits, 2^(n-3) from
+    // 9 to 10, 16 amplitudes per thread from 11 on (measured on configurations
+    // of 4, 8 and 12 qubits: small states are latency bound, so more threads win)
+    plan.R = reg_bits ? reg_bits : nq <= 8 ? 2 : nq <= 10 ? 3 : kDefaultRegBits;
     plan.k = nq;
     plan.t = nq - plan.R;
     const int T = 1 << plan.t;
@@ -469,6 +479,8 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
   } else {
     plan.k = kMaxTileQubits;
     plan.ng = nq - plan.k;
+    plan.Rf = reg_bits ? reg_bits : kStreamRegBitsFwd;
+    plan.Rb = reg_bits ? reg_bits : kStreamRegBitsBwd;
     plan.t = plan.k - plan.Rf;       // the forward's geometry (informational)
     plan.WG = 1 << plan.t;
     plan.S = 1;

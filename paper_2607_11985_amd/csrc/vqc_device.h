@@ -365,16 +365,56 @@ __device__ __forceinline__ uint32_t opaque(uint32_t x) {
 }
 
 // butterfly sum over `width` consecutive lanes (power of two <= 64); every lane
-// of the segment ends with the same, order-fixed value
+// of the segment ends with the same, order-fixed value.  The empty asm keeps
+// the shuffles where all lanes are active (see group_sum).
 __device__ __forceinline__ float seg_sum(float v, int width) {
+  asm volatile("" : "+v"(v));
   for (int m = 1; m < width; m <<= 1) v += __shfl_xor(v, m, 64);
+  asm volatile("" : "+v"(v));
   return v;
 }
 
 // the same over the whole wave, fully unrolled
 __device__ __forceinline__ float wave_sum(float v) {
+  asm volatile("" : "+v"(v));
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) v += __shfl_xor(v, m, 64);
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// v from another lane through a DPP lane pattern (every lane reads a valid lane)
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over aligned groups of W lanes (W a power of two <= 64).  Every lane of a
+// group ends with the group's sum; the pairing order is fixed, so the result is
+// deterministic.  Pairs, quads, 8- and 16-lane rows use DPP (quad_perm 1032 and
+// 2301, row_half_mirror, row_mirror), 32 lanes a swizzle (xor 16), 64 lanes the
+// four row sums read as scalars.
+template <int W>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(W >= 1 && W <= 64 && (W & (W - 1)) == 0, "group width");
+  // The empty asm statements pin the cross-lane steps to this point of the
+  // program: without them the compiler may sink the whole sum into a branch
+  // taken by one lane only (the lane that consumes it), where the lanes it reads
+  // from are inactive.
+  asm volatile("" : "+v"(v));
+  if (W >= 2) v += dpp_f<0xB1>(v);
+  if (W >= 4) v += dpp_f<0x4E>(v);
+  if (W >= 8) v += dpp_f<0x141>(v);
+  if (W >= 16) v += dpp_f<0x140>(v);
+  if (W == 32) v += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));
+  if (W == 64) {
+    const int x = __float_as_int(v);
+    v = (__int_as_float(__builtin_amdgcn_readlane(x, 0)) +
+         __int_as_float(__builtin_amdgcn_readlane(x, 16))) +
+        (__int_as_float(__builtin_amdgcn_readlane(x, 32)) +
+         __int_as_float(__builtin_amdgcn_readlane(x, 48)));
+  }
+  asm volatile("" : "+v"(v));
   return v;
 }
 
@@ -450,7 +490,16 @@ struct Walk {
   int stid, sl, grp, width;
   uint32_t tb;        // tile bits above the register bits
   bool leader;
+  bool never;         // false, but not provably so (see gate_boundary)
 };
+
+// Ends the current basic block with a uniform branch that is never taken.  The
+// generated kernels put one after every rotation, so that instruction
+// selection and scheduling work gate by gate: one block for a whole circuit
+// makes them keep values alive across it (and compile slowly).
+__device__ __forceinline__ void gate_boundary(const Walk& w) {
+  if (w.never) asm volatile("");
+}
 
 // Bit p >= R of the amplitude position (a thread or tile bit).  Taken from an
 // opaque copy of tb so that the compiler recomputes it at each gate instead of
@@ -565,7 +614,7 @@ __device__ __forceinline__ void make_lambda(St<R>& l, const St<R>& a, const floa
 // Per-qubit signed probability sums of this workgroup's amplitudes:
 // ez[q * G + grp] = sum over the group's amplitudes of (-1)^{x_q} |a|^2.
 // Must be called by every thread; ez may alias the exchange buffer.
-template <int R>
+template <int R, typename Sched>
 __device__ __forceinline__ void z_partials(const St<R>& a, float* ez, int n, const uint8_t* phys,
                                            const Walk& w) {
   float tot = 0.f, sr[R];
@@ -585,7 +634,7 @@ __device__ __forceinline__ void z_partials(const St<R>& a, float* ez, int n, con
 #pragma unroll
     for (int b = 0; b < R; ++b)
       if (p == b) v = sr[b];
-    v = seg_sum(v, w.width);
+    v = Sched::lane_sum(v, w);
     if (w.leader) ez[q * w.G + w.grp] = v;
   }
   __syncthreads();
@@ -597,6 +646,10 @@ struct InterpSched {
   __device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w,
                                              const uint32_t* ins, int n_ins) {
     run_schedule<R, BWD, WIDE>(a, l, ins, n_ins, w);
+  }
+  // sum over the lanes of one sample within the wave
+  __device__ __forceinline__ static float lane_sum(float v, const Walk& w) {
+    return seg_sum(v, w.width);
   }
 };
 
@@ -635,6 +688,7 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
   w.width = T < 64 ? T : 64;
   w.grp = T < 64 ? sl : (tid >> 6);
   w.leader = (tid & (w.width - 1)) == 0;
+  w.never = A.B < 0;
   w.tb = (uint32_t)stid;
 
   angle_table(tab, A.n_occ, S, b0, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.P, A.inputs,
@@ -671,7 +725,7 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
         ws[((size_t)blockIdx.x * NA + j) * WG + tid] = make_float2(a.r[j], a.i[j]);
     }
     float* ez = xbuf;
-    z_partials<R>(a, ez, A.n, A.end_phys, w);
+    z_partials<R, Sched>(a, ez, A.n, A.end_phys, w);
     for (int i = tid; i < A.n * S; i += WG) {
       const int q = i / S;
       const int s = i - q * S;
@@ -771,6 +825,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.width = 64;
   w.grp = tid >> 6;
   w.leader = (tid & 63) == 0;
+  w.never = A.B < 0;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
   angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.P, A.inputs,
@@ -824,7 +879,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
     }
   } else if (A.flags & PF_ZPART) {
     float* ez = xbuf;
-    z_partials<R>(a, ez, A.n, A.end_phys, w);
+    z_partials<R, Sched>(a, ez, A.n, A.end_phys, w);
     for (int q = tid; q < A.n; q += WG) {
       float e = 0.f;
       for (int r = 0; r < G; ++r) e += ez[q * G + r];

@@ -22,7 +22,7 @@ namespace vqc {
 
 constexpr int kDefaultRegBits = 4;           // R of the resident kernels
 constexpr int kStreamRegBitsFwd = 4;         // streaming forward: 1024 threads x 16
-constexpr int kStreamRegBitsBwd = 5;         // streaming adjoint: 512 threads x 32
+constexpr int kStreamRegBitsBwd = 4;         // streaming adjoint: 1024 threads x 16
 constexpr int kMaxTileQubits = 14;           // 2^14 c64 = 128 KiB per tile
 constexpr int kMaxQubits = 20;
 constexpr int kLdsBytes = 160 * 1024;        // gfx950 LDS per workgroup

@@ -145,8 +145,8 @@ def test_compile_rejects_options():
     assert rc == _lib.VQC_ERR_INVALID_ARG
     rc, _ = host_compile([], 2, 0, 0, engine=2)
     assert rc == _lib.VQC_ERR_INVALID_ARG and "engine" in _lib.vqc_last_error()
-    for bad in (1, 5, -1):
-        rc, _ = host_compile([], 6, 0, 0, reg_bits=bad)
+    for n, bad in ((6, 1), (6, 5), (6, -1), (6, 6), (15, 3), (15, 6)):
+        rc, _ = host_compile([], n, 0, 0, reg_bits=bad)
         assert rc == _lib.VQC_ERR_INVALID_ARG and "reg_bits" in _lib.vqc_last_error()
     rc, _ = host_compile([], 15, 0, 0, path=_lib.VQC_PATH_RESIDENT)
     assert rc == _lib.VQC_ERR_UNSUPPORTED
@@ -172,7 +172,9 @@ def test_random_circuits_plan(n):
     rc, h = host_compile(ops, n, P, F)
     assert rc == 0, _lib.vqc_last_error()
     info = _lib.vqc_circuit_info(h)
-    assert info["threads"] == max(64, 1 << (max(n, 4) - 4))
+    nq = max(n, 4)
+    R = 2 if nq <= 8 else 3 if nq <= 10 else 4
+    assert info["threads"] == max(64, 1 << (nq - R))
     _lib.vqc_destroy(h)
 
 

@@ -84,8 +84,10 @@ def check_grad(g, gref, cot, what):
 
 
 def samples_per_wg(n):
+    """Samples per workgroup of the resident kernels at the default width."""
     nq = max(n, 4)
-    T = 1 << (nq - 4)
+    R = 2 if nq <= 8 else 3 if nq <= 10 else 4
+    T = 1 << (nq - R)
     return max(1, 64 // T)
 
 
