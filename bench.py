@@ -1,21 +1,20 @@
 """Throughput of the batched VQC hot path on one MI355X.
 
 One step = one pass of the whole hot path over one batch of synthetic input:
-vqc_forward (training: saves the final states) -> vqc_loss_grad (cotangent of
-the workload's objective) -> vqc_backward (adjoint gradients for every
-parameter and input), all on one HIP stream with inputs resident in HBM.
+forward (every gate, <Z>), the workload's loss-head cotangent, and the adjoint
+sweep (gradients for every parameter and input), on one HIP stream with the
+inputs resident in HBM.  By default a step is one vqc_train_step call (a single
+launch on the resident path: the state never leaves the chip); --separate
+times vqc_forward + vqc_loss_grad + vqc_backward instead, and those calls'
+timings are reported beside the step either way.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5]
 
 Prints one JSON line.  value = circuit evaluations (forward E + full
-gradient) per second = B * K / timed seconds.
-
-The timed region replays a HIP graph that holds one whole step (the three
-calls' kernels, captured once on the step's stream), bracketed by events; a
-fixed-shape training loop runs this way.  Eager timings (per call, each
-bracketed by events) are reported next to it, and the dominant call is timed
-separately as K back-to-back launches for the roofline.  Every replay's
-outputs are checked bit for bit against an eager step.
+gradient) per second = B * K / timed seconds, the K steps bracketed by events.
+The dominant kernel is timed again as K back-to-back launches for the
+roofline.  Every timed step's outputs are checked bit for bit against the
+first one, and the fused step against the separate calls.
 """
 from __future__ import annotations
 
@@ -142,8 +141,11 @@ def main():
                          "schedule interpreter (interp)")
     ap.add_argument("--reg-bits", type=int, default=0,
                     help="amplitudes per thread = 2^reg_bits (0: the library's default)")
-    ap.add_argument("--no-graph", action="store_true",
-                    help="time eager launches instead of graph replays of the step")
+    ap.add_argument("--graph", action="store_true",
+                    help="time HIP graph replays of the step instead of its launches")
+    ap.add_argument("--separate", action="store_true",
+                    help="time vqc_forward + vqc_loss_grad + vqc_backward instead of "
+                         "vqc_train_step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -183,11 +185,15 @@ def main():
     dp = torch.empty((B, w.n_params), dtype=torch.float32, device=dev)
     dx = torch.empty((B, w.n_inputs), dtype=torch.float32, device=dev)
     ws, nb = circ.new_workspace(B, training=True)
+    nb_step = circ.workspace_bytes(B, 2)
+    ws_step = torch.empty(max(nb_step, 1), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     s = stream.cuda_stream
     h = circ.handle
     loss_kind = _lib.LOSS[w.loss]
     pp, xp, yp = p.data_ptr(), x.data_ptr(), (y.data_ptr() if y is not None else None)
+    dpp = dp.data_ptr() if w.n_params else None
+    dxp = dx.data_ptr() if w.n_inputs else None
 
     def fwd(st):
         _lib.vqc_forward(h, B, pp, xp, E.data_ptr(), ws.data_ptr(), nb, st)
@@ -196,41 +202,61 @@ def main():
         _lib.vqc_loss_grad(loss_kind, B, n, E.data_ptr(), yp, g.data_ptr(), st)
 
     def bwd(st):
-        _lib.vqc_backward(h, B, pp, xp, g.data_ptr(), ws.data_ptr(), nb, dp.data_ptr(),
-                          dx.data_ptr(), st)
+        _lib.vqc_backward(h, B, pp, xp, g.data_ptr(), ws.data_ptr(), nb, dpp, dxp, st)
 
-    def step(st):
+    def separate(st):
         fwd(st); loss(st); bwd(st)
 
-    for _ in range(args.warmup):
-        step(s)
-    torch.cuda.synchronize()
-    ref = [t.clone() for t in (E, g, dp, dx)]
+    def fused(st):
+        _lib.vqc_train_step(h, B, pp, xp, loss_kind, yp, E.data_ptr(), g.data_ptr(), dpp, dxp,
+                            ws_step.data_ptr() if nb_step else None, nb_step, st)
+
+    step = separate if args.separate else fused
 
     def ev():
         return torch.cuda.Event(enable_timing=True)
 
+    def back_to_back(call, K):
+        """Average duration of K launches of `call` issued back to back."""
+        e0, e1 = ev(), ev()
+        e0.record(stream)
+        for _ in range(K):
+            call(s)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
     K = args.steps
-    # eager: every call bracketed by events (includes host launch gaps)
-    evs = [[ev() for _ in range(4)] for _ in range(K)]
-    t0e, t1e = ev(), ev()
+    for _ in range(args.warmup):
+        separate(s)
     torch.cuda.synchronize()
-    t0e.record(stream)
+    ref = [t.clone() for t in (E, g, dp, dx)]
+    for _ in range(args.warmup):
+        fused(s)
+    torch.cuda.synchronize()
+    # the fused step reproduces the separate calls (up to the compiler's rounding)
+    dev_max = max(float((t - r).abs().max()) if t.numel() else 0.0
+                  for t, r in zip((E, g, dp, dx), ref))
+    if dev_max > 1e-4:
+        raise SystemExit(f"training step differs from the separate calls by {dev_max}")
+
+    # separate calls, each bracketed by events (includes host launch gaps)
+    evs = [[ev() for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
     for k in range(K):
         e = evs[k]
         e[0].record(stream); fwd(s)
         e[1].record(stream); loss(s)
         e[2].record(stream); bwd(s)
         e[3].record(stream)
-    t1e.record(stream)
     torch.cuda.synchronize()
-    eager_step_ms = t0e.elapsed_time(t1e) / K
     fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     loss_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    separate_ms = back_to_back(separate, K)
 
-    # the timed region: K replays of the captured step
-    use_graph = not args.no_graph
+    # the timed region: K steps
+    use_graph = args.graph
     if use_graph:
         graph = torch.cuda.CUDAGraph()
         cap = torch.cuda.Stream(device=dev)  # default priority
@@ -239,6 +265,9 @@ def main():
             step(cap.cuda_stream)
         stream.wait_stream(cap)
         torch.cuda.synchronize()
+    step(s)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (E, g, dp, dx)]
     t_start, t_end = ev(), ev()
     torch.cuda.synchronize()
     t_start.record(stream)
@@ -254,39 +283,30 @@ def main():
     value = B * K / (total_ms / 1e3)
     for t, r in zip((E, g, dp, dx), ref):
         if not torch.equal(t, r):
-            raise SystemExit("replayed step differs from the eager step")
+            raise SystemExit("a timed step differs from the first one")
 
-    # dominant call, K back-to-back launches on the same stream
+    # the dominant kernel: the one-launch training step on the resident path,
+    # else the adjoint (all of its passes), timed as K back-to-back launches
     f_fwd, f_bwd = algorithmic_flops(w)
-    dominant = "backward" if bwd_ms >= fwd_ms else "forward"
-    dom_call = bwd if dominant == "backward" else fwd
-    d0, d1 = ev(), ev()
-    d0.record(stream)
-    for _ in range(K):
-        dom_call(s)
-    d1.record(stream)
-    torch.cuda.synchronize()
-    dom_ms = d0.elapsed_time(d1) / K
+    resident = info["path"] == 1
+    if resident and not args.separate:
+        dominant, dom_ms, flops_sample = "train_step", back_to_back(fused, K), f_fwd + f_bwd
+    elif bwd_ms >= fwd_ms:
+        dominant, dom_ms, flops_sample = "backward", back_to_back(bwd, K), f_bwd
+    else:
+        dominant, dom_ms, flops_sample = "forward", back_to_back(fwd, K), f_fwd
 
     # forward-only rate (inference, no state saved), outside the timed region
-    for _ in range(3):
-        circ.forward(p, x, out=E)
-    torch.cuda.synchronize()
-    a0, a1 = ev(), ev()
-    a0.record(stream)
-    for _ in range(K):
-        circ.forward(p, x, out=E)
-    a1.record(stream)
-    torch.cuda.synchronize()
-    inf_ms = a0.elapsed_time(a1) / K
+    inf_ms = back_to_back(lambda st: circ.forward(p, x, out=E), K)
 
-    flops = (f_bwd if dominant == "backward" else f_fwd) * B
+    flops = flops_sample * B
     achieved = flops / (dom_ms / 1e3) / 1e12
     if args.engine == "jit":
-        kname = {(1, "forward"): "vqc_rf", (1, "backward"): "vqc_rb", (2, "forward"): "vqc_sf*",
-                 (2, "backward"): "vqc_sb*"}[(info["path"], dominant)]
+        kname = {(1, "train_step"): "vqc_rs", (1, "forward"): "vqc_rf", (1, "backward"): "vqc_rb",
+                 (2, "forward"): "vqc_sf*", (2, "backward"): "vqc_sb*"}[(info["path"], dominant)]
     else:
-        kname = "stream_kernel" if info["path"] == 2 else "resident_kernel"
+        kname = ("stream_kernel" if info["path"] == 2 else
+                 "resident_step_kernel" if dominant == "train_step" else "resident_kernel")
     kname += f" ({dominant}, all passes)" if info["path"] == 2 else f" ({dominant})"
     roofline = {"bound": "alu", "kernel": kname, "achieved": achieved,
                 "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS,
@@ -306,8 +326,10 @@ def main():
                    "reg_bits": args.reg_bits or "default",
                    "compile_s": round(compile_s, 2),
                    "exchanges_fwd_bwd": [info["fwd_exchanges"], info["bwd_exchanges"]]},
-        "timing": "hip graph replay of the step" if use_graph else "eager launches",
-        "eager_ms_per_step": eager_step_ms,
+        "step": ("vqc_forward + vqc_loss_grad + vqc_backward" if args.separate else
+                 "vqc_train_step"),
+        "timing": "hip graph replays of the step" if use_graph else "launches on one stream",
+        "separate_calls_ms_per_step": separate_ms,
         "kernel_ms": {"forward_train": fwd_ms, "loss_grad": loss_ms, "backward": bwd_ms,
                       "forward_inference": inf_ms, f"{dominant}_back_to_back": dom_ms},
         "forward_only_evals_per_s": B / (inf_ms / 1e3),

@@ -124,10 +124,12 @@ int vqc_compile(const vqc_op *ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
 void vqc_destroy(vqc_circuit *c);
 
 /*
- * vqc_workspace_bytes -- device workspace a forward (training = 1: the saved
- * final states for the backward pass, plus the backward's scratch) or an
- * inference forward (training = 0) needs for `batch` samples.  0 means no
- * workspace is needed.  Returns (size_t)-1 on invalid arguments.
+ * vqc_workspace_bytes -- device workspace for `batch` samples of
+ *   training = 0: an inference vqc_forward;
+ *   training = 1: a training vqc_forward (the saved final states) and the
+ *                 vqc_backward calls that use it (plus their scratch);
+ *   training = 2: vqc_train_step.
+ * 0 means no workspace is needed.  Returns (size_t)-1 on invalid arguments.
  */
 size_t vqc_workspace_bytes(const vqc_circuit *c, int64_t batch, int32_t training);
 
@@ -179,6 +181,24 @@ int vqc_backward(const vqc_circuit *c, int64_t batch, const float *params, const
 #define VQC_LOSS_MSE_MEANZ 3
 int vqc_loss_grad(int32_t kind, int64_t batch, int32_t n_qubits, const float *expvals,
                   const float *target, float *grad_out, void *stream);
+
+/*
+ * vqc_train_step -- one training evaluation: vqc_forward, vqc_loss_grad with
+ * `loss_kind` and `target`, and vqc_backward with that cotangent, in one call
+ * (Sec. 3 "Gate Application and Differentiation"; Sec. 4.2.3 objective).  On
+ * the resident path this is a single launch: the final state stays on chip
+ * between the forward and the adjoint sweep and is never written to HBM.
+ *   expvals [batch, n] written; grad_out [batch, n] receives the cotangent
+ *   when not NULL; dparams [batch, P] / dinputs [batch, F] written (either
+ *   may be NULL); workspace: vqc_workspace_bytes(c, batch, 2) bytes, 256-byte
+ *   aligned (0 bytes / NULL on the resident path).
+ * Results equal those of the three separate calls.  Errors: those of the
+ * three calls.
+ */
+int vqc_train_step(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,
+                   int32_t loss_kind, const float *target, float *expvals, float *grad_out,
+                   float *dparams, float *dinputs, void *workspace, size_t workspace_bytes,
+                   void *stream);
 
 /* Introspection of a compiled circuit (host-side values only). */
 typedef struct {

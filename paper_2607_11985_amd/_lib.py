@@ -84,6 +84,9 @@ def load():
     lib.vqc_loss_grad.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _vp, _vp,
                                   _vp, _vp]
     lib.vqc_loss_grad.restype = ctypes.c_int
+    lib.vqc_train_step.argtypes = [_vp, ctypes.c_int64, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp,
+                                   _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.vqc_train_step.restype = ctypes.c_int
     lib.vqc_jit_check.argtypes = [_vp]
     lib.vqc_jit_check.restype = ctypes.c_int
     lib.vqc_circuit_info.argtypes = [_vp, ctypes.POINTER(vqc_info)]
@@ -160,6 +163,12 @@ def vqc_backward(h, batch, params_ptr, inputs_ptr, grad_ptr, ws_ptr, ws_bytes, d
                  dinputs_ptr, stream):
     _check(load().vqc_backward(h, batch, params_ptr, inputs_ptr, grad_ptr, ws_ptr, ws_bytes,
                                dparams_ptr, dinputs_ptr, stream))
+
+
+def vqc_train_step(h, batch, params_ptr, inputs_ptr, loss_kind, y_ptr, expvals_ptr, grad_ptr,
+                   dparams_ptr, dinputs_ptr, ws_ptr, ws_bytes, stream):
+    _check(load().vqc_train_step(h, batch, params_ptr, inputs_ptr, loss_kind, y_ptr, expvals_ptr,
+                                 grad_ptr, dparams_ptr, dinputs_ptr, ws_ptr, ws_bytes, stream))
 
 
 def vqc_loss_grad(kind: int, batch: int, n: int, e_ptr, y_ptr, g_ptr, stream):

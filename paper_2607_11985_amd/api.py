@@ -101,6 +101,30 @@ class Circuit:
         return dparams, dinputs
 
 
+    def train_step(self, params, inputs, loss: str, y=None, workspace=None, want_cot=False):
+        """Forward, loss cotangent and adjoint gradients in one call.
+
+        Returns (E, dparams, dinputs), plus the cotangent g when want_cot."""
+        B = int(params.shape[0]) if params is not None else int(inputs.shape[0])
+        params = _as_rows(params, B, self.P, self.device, "params")
+        inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
+        if y is not None:
+            y = _as_rows(y.reshape(B, 1), B, 1, self.device, "y")
+        E = torch.empty((B, self.n), dtype=torch.float32, device=self.device)
+        g = torch.empty_like(E) if want_cot else None
+        dparams = torch.empty((B, self.P), dtype=torch.float32, device=self.device)
+        dinputs = torch.empty((B, self.F), dtype=torch.float32, device=self.device)
+        nb = _lib.vqc_workspace_bytes(self.handle, B, 2)
+        if workspace is None and nb > 0:
+            workspace = torch.empty(nb, dtype=torch.uint8, device=self.device)
+        _lib.vqc_train_step(self.handle, B, _ptr(params), _ptr(inputs), _lib.LOSS[loss], _ptr(y),
+                            E.data_ptr(), _ptr(g), dparams.data_ptr() if self.P else None,
+                            dinputs.data_ptr() if self.F else None, _ptr(workspace),
+                            workspace.numel() if workspace is not None else 0,
+                            _stream(self.device))
+        return (E, dparams, dinputs, g) if want_cot else (E, dparams, dinputs)
+
+
 def loss_grad(kind: str, E, y=None, out=None):
     """Cotangent dL/dE of a scalar objective, computed on the GPU."""
     B, n = E.shape

@@ -68,6 +68,7 @@ size_t resident_state_bytes(const Plan& p, int64_t batch) {
 // Streaming workspace: [psi | E partials | psi work | lambda work | grad partials]
 struct StreamLayout {
   size_t psi = 0, epart = 0, psiw = 0, lamw = 0, gpart = 0, end_inference = 0, end_training = 0;
+  size_t cot = 0, end_step = 0;  // the training step's cotangent rows [B, n]
 };
 
 StreamLayout stream_layout(const Plan& p, int64_t batch) {
@@ -81,16 +82,19 @@ StreamLayout stream_layout(const Plan& p, int64_t batch) {
   L.lamw = align_up(L.psiw + state, 256);
   L.gpart = align_up(L.lamw + state, 256);
   L.end_training = align_up(L.gpart + tiles * (size_t)(p.P + p.F) * 4, 256);
+  L.cot = L.end_training;
+  L.end_step = align_up(L.cot + (size_t)batch * (size_t)p.n * 4, 256);
   return L;
 }
 
-size_t required_bytes(const Plan& p, int64_t batch, bool training) {
+// mode: 0 inference forward, 1 training forward (+ backward), 2 training step
+size_t required_bytes(const Plan& p, int64_t batch, int mode) {
   if (batch == 0) return 0;
   if (p.path == VQC_PATH_STREAM) {
     const StreamLayout L = stream_layout(p, batch);
-    return training ? L.end_training : L.end_inference;
+    return mode == 0 ? L.end_inference : mode == 1 ? L.end_training : L.end_step;
   }
-  return training ? resident_state_bytes(p, batch) : 0;
+  return mode == 1 ? resident_state_bytes(p, batch) : 0;
 }
 
 template <typename T>
@@ -176,6 +180,73 @@ int hip_fail(const char* what, int rc) {
 int check_rows(const vqc_circuit* c, const float* params, const float* inputs) {
   if (c->plan.P > 0 && !params) return fail(VQC_ERR_INVALID_ARG, "params is NULL but P > 0");
   if (c->plan.F > 0 && !inputs) return fail(VQC_ERR_INVALID_ARG, "inputs is NULL but F > 0");
+  return VQC_OK;
+}
+
+int check_workspace(const void* workspace, size_t bytes, size_t need, const char* what) {
+  if (need == 0) return VQC_OK;
+  if (!workspace || bytes < need) return fail(VQC_ERR_WORKSPACE, what);
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(VQC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return VQC_OK;
+}
+
+// Streaming forward: every pass, then the <Z> reduction into expvals.
+int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
+                   float* expvals, unsigned char* ws, void* stream) {
+  const Plan& p = c->plan;
+  const StreamLayout L = stream_layout(p, batch);
+  int rc = 0;
+  for (const vqc::PassPlan& pp : p.fpass) {
+    vqc::PassArgs a = pass_args(c, pp, false, batch);
+    a.params = params;
+    a.inputs = inputs;
+    a.psi_src = ws + L.psi;
+    a.psi_dst = ws + L.psi;
+    a.epart = reinterpret_cast<float*>(ws + L.epart);
+    const size_t i = &pp - p.fpass.data();
+    rc = c->engine == VQC_ENGINE_JIT
+             ? vqc::jit_launch(c->jit.pass_fwd[i], batch << p.ng, 1 << (p.k - p.Rf), &a, sizeof(a),
+                               stream)
+             : vqc::launch_stream_pass(p, false, a, batch << p.ng, stream);
+    if (rc) return hip_fail("forward pass launch", rc);
+  }
+  rc = vqc::launch_reduce_e(batch, p.ng, p.n, reinterpret_cast<const float*>(ws + L.epart),
+                            expvals, stream);
+  if (rc) return hip_fail("expectation reduction launch", rc);
+  return VQC_OK;
+}
+
+// Streaming adjoint: clear the partials, every pass (the first reads the saved
+// psi_G and leaves it intact), then the reduction into dparams / dinputs.
+int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
+                    const float* grad_out, unsigned char* ws, float* dp, float* dx, void* stream) {
+  const Plan& p = c->plan;
+  const StreamLayout L = stream_layout(p, batch);
+  float* gpart = reinterpret_cast<float*>(ws + L.gpart);
+  int rc = vqc::launch_fill_zero(gpart, (batch << p.ng) * (int64_t)(p.P + p.F), stream);
+  if (rc) return hip_fail("gradient partial clear", rc);
+  bool first = true;
+  for (const vqc::PassPlan& pp : p.bpass) {
+    vqc::PassArgs a = pass_args(c, pp, true, batch);
+    a.params = params;
+    a.inputs = inputs;
+    a.grad_out = grad_out;
+    a.psi_src = ws + (first ? L.psi : L.psiw);
+    a.psi_dst = ws + L.psiw;
+    a.lam_src = ws + L.lamw;
+    a.lam_dst = ws + L.lamw;
+    a.gpart = gpart;
+    const size_t i = &pp - p.bpass.data();
+    rc = c->engine == VQC_ENGINE_JIT
+             ? vqc::jit_launch(c->jit.pass_bwd[i], batch << p.ng, 1 << (p.k - p.Rb), &a, sizeof(a),
+                               stream)
+             : vqc::launch_stream_pass(p, true, a, batch << p.ng, stream);
+    if (rc) return hip_fail("backward pass launch", rc);
+    first = false;
+  }
+  rc = vqc::launch_reduce_grad(batch, p.ng, p.P + p.F, p.P, p.F, gpart, dp, dx, stream);
+  if (rc) return hip_fail("gradient reduction launch", rc);
   return VQC_OK;
 }
 
@@ -291,8 +362,8 @@ void vqc_destroy(vqc_circuit* c) {
 }
 
 size_t vqc_workspace_bytes(const vqc_circuit* c, int64_t batch, int32_t training) {
-  if (!c || batch < 0) return (size_t)-1;
-  return required_bytes(c->plan, batch, training != 0);
+  if (!c || batch < 0 || training < 0 || training > 2) return (size_t)-1;
+  return required_bytes(c->plan, batch, training);
 }
 
 int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
@@ -307,37 +378,17 @@ int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const 
   if (p.path == VQC_PATH_STREAM && !workspace)
     return fail(VQC_ERR_WORKSPACE, "the streaming path needs a workspace (states live in HBM)");
   if (workspace) {
-    if (workspace_bytes < required_bytes(p, batch, p.path == VQC_PATH_RESIDENT))
-      return fail(VQC_ERR_WORKSPACE, "workspace smaller than vqc_workspace_bytes(c, batch, " +
-                                         std::string(p.path == VQC_PATH_RESIDENT ? "1" : "0") +
-                                         ")");
-    if (reinterpret_cast<uintptr_t>(workspace) % 256)
-      return fail(VQC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+    const int mode = p.path == VQC_PATH_RESIDENT ? 1 : 0;
+    if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(p, batch, mode),
+                              mode ? "workspace smaller than vqc_workspace_bytes(c, batch, 1)"
+                                   : "workspace smaller than vqc_workspace_bytes(c, batch, 0)")))
+      return rc;
   }
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
-  if (p.path == VQC_PATH_STREAM) {
-    const StreamLayout L = stream_layout(p, batch);
-    unsigned char* ws = static_cast<unsigned char*>(workspace);
-    for (const vqc::PassPlan& pp : p.fpass) {
-      vqc::PassArgs a = pass_args(c, pp, false, batch);
-      a.params = params;
-      a.inputs = inputs;
-      a.psi_src = ws + L.psi;
-      a.psi_dst = ws + L.psi;
-      a.epart = reinterpret_cast<float*>(ws + L.epart);
-      const size_t i = &pp - p.fpass.data();
-      rc = c->engine == VQC_ENGINE_JIT
-               ? vqc::jit_launch(c->jit.pass_fwd[i], batch << p.ng, 1 << (p.k - p.Rf), &a,
-                                 sizeof(a), stream)
-               : vqc::launch_stream_pass(p, false, a, batch << p.ng, stream);
-      if (rc) return hip_fail("forward pass launch", rc);
-    }
-    rc = vqc::launch_reduce_e(batch, p.ng, p.n, reinterpret_cast<const float*>(ws + L.epart),
-                              expvals, stream);
-    if (rc) return hip_fail("expectation reduction launch", rc);
-    return VQC_OK;
-  }
+  if (p.path == VQC_PATH_STREAM)
+    return stream_forward(c, batch, params, inputs, expvals,
+                          static_cast<unsigned char*>(workspace), stream);
   vqc::TileArgs a = tile_args(c, false, batch);
   a.params = params;
   a.inputs = inputs;
@@ -360,43 +411,16 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
   if ((rc = check_rows(c, params, inputs))) return rc;
   if (!grad_out) return fail(VQC_ERR_INVALID_ARG, "grad_out is NULL");
   const Plan& p = c->plan;
-  if (!workspace || workspace_bytes < required_bytes(p, batch, true))
-    return fail(VQC_ERR_WORKSPACE, "backward needs the workspace of a training forward");
-  if (reinterpret_cast<uintptr_t>(workspace) % 256)
-    return fail(VQC_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(p, batch, 1),
+                            "backward needs the workspace of a training forward")))
+    return rc;
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
   float* dp = p.P > 0 ? dparams : nullptr;
   float* dx = p.F > 0 ? dinputs : nullptr;
-  if (p.path == VQC_PATH_STREAM) {
-    const StreamLayout L = stream_layout(p, batch);
-    unsigned char* ws = static_cast<unsigned char*>(workspace);
-    float* gpart = reinterpret_cast<float*>(ws + L.gpart);
-    rc = vqc::launch_fill_zero(gpart, (batch << p.ng) * (int64_t)(p.P + p.F), stream);
-    if (rc) return hip_fail("gradient partial clear", rc);
-    bool first = true;
-    for (const vqc::PassPlan& pp : p.bpass) {
-      vqc::PassArgs a = pass_args(c, pp, true, batch);
-      a.params = params;
-      a.inputs = inputs;
-      a.grad_out = grad_out;
-      a.psi_src = ws + (first ? L.psi : L.psiw);  // the saved psi_G is only read
-      a.psi_dst = ws + L.psiw;
-      a.lam_src = ws + L.lamw;
-      a.lam_dst = ws + L.lamw;
-      a.gpart = gpart;
-      const size_t i = &pp - p.bpass.data();
-      rc = c->engine == VQC_ENGINE_JIT
-               ? vqc::jit_launch(c->jit.pass_bwd[i], batch << p.ng, 1 << (p.k - p.Rb), &a,
-                                 sizeof(a), stream)
-               : vqc::launch_stream_pass(p, true, a, batch << p.ng, stream);
-      if (rc) return hip_fail("backward pass launch", rc);
-      first = false;
-    }
-    rc = vqc::launch_reduce_grad(batch, p.ng, p.P + p.F, p.P, p.F, gpart, dp, dx, stream);
-    if (rc) return hip_fail("gradient reduction launch", rc);
-    return VQC_OK;
-  }
+  if (p.path == VQC_PATH_STREAM)
+    return stream_backward(c, batch, params, inputs, grad_out,
+                           static_cast<unsigned char*>(workspace), dp, dx, stream);
   vqc::TileArgs a = tile_args(c, true, batch);
   a.params = params;
   a.inputs = inputs;
@@ -408,6 +432,57 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
            ? vqc::jit_launch(c->jit.res_bwd, resident_blocks(p, batch), p.WG, &a, sizeof(a), stream)
            : vqc::launch_resident_backward(p, a, resident_blocks(p, batch), stream);
   if (rc) return hip_fail("backward launch", rc);
+  return VQC_OK;
+}
+
+int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
+                   int32_t loss_kind, const float* target, float* expvals, float* grad_out,
+                   float* dparams, float* dinputs, void* workspace, size_t workspace_bytes,
+                   void* stream) {
+  int rc = check_runnable(c);
+  if (rc) return rc;
+  if (loss_kind < VQC_LOSS_SUM || loss_kind > VQC_LOSS_MSE_MEANZ)
+    return fail(VQC_ERR_INVALID_ARG, "unknown loss kind");
+  if ((rc = check_batch(c, batch))) return rc;
+  if (batch == 0) return VQC_OK;
+  if ((rc = check_rows(c, params, inputs))) return rc;
+  if (!expvals) return fail(VQC_ERR_INVALID_ARG, "expvals is NULL");
+  if ((loss_kind == VQC_LOSS_MSE_Z0 || loss_kind == VQC_LOSS_MSE_MEANZ) && !target)
+    return fail(VQC_ERR_INVALID_ARG, "MSE losses need a target");
+  const Plan& p = c->plan;
+  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(p, batch, 2),
+                            "workspace smaller than vqc_workspace_bytes(c, batch, 2)")))
+    return rc;
+  DeviceGuard g(c->device);
+  if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
+  float* dp = p.P > 0 ? dparams : nullptr;
+  float* dx = p.F > 0 ? dinputs : nullptr;
+  if (p.path == VQC_PATH_STREAM) {
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    float* cot = grad_out ? grad_out
+                          : reinterpret_cast<float*>(ws + stream_layout(p, batch).cot);
+    if ((rc = stream_forward(c, batch, params, inputs, expvals, ws, stream))) return rc;
+    rc = vqc::launch_loss_grad(loss_kind, batch, p.n, expvals, target, cot, stream);
+    if (rc) return hip_fail("loss launch", rc);
+    return stream_backward(c, batch, params, inputs, cot, ws, dp, dx, stream);
+  }
+  vqc::TileArgs a = tile_args(c, false, batch);
+  a.ins_b = at<uint32_t>(c, c->off_bwd);
+  a.n_ins_b = (int32_t)(p.bwd.size() / 2);
+  a.params = params;
+  a.inputs = inputs;
+  a.expvals = expvals;
+  a.loss = loss_kind;
+  a.target = target;
+  a.cot_out = grad_out;
+  a.dparams = dp;
+  a.dinputs = dx;
+  a.lds_e = (uint32_t)p.lds_e;
+  rc = c->engine == VQC_ENGINE_JIT
+           ? vqc::jit_launch(c->jit.res_step, resident_blocks(p, batch), p.WG, &a, sizeof(a),
+                             stream)
+           : vqc::launch_resident_step(p, a, resident_blocks(p, batch), stream);
+  if (rc) return hip_fail("training step launch", rc);
   return VQC_OK;
 }
 

@@ -6,11 +6,15 @@
 // call of the register-tile template for its position, a CNOT between register
 // bits is a renaming, and exchanges use constant column tables.  The text plus
 // the shared device code (vqc_device.h) is compiled with hiprtc for gfx950, one
-// program per kernel on a pool of host threads, and loaded as modules; launches
-// go through hipModuleLaunchKernel.  Identical kernels are compiled once per
-// process.
+// program per kernel, several at a time in helper processes, and loaded as
+// modules; launches go through hipModuleLaunchKernel.  Identical kernels are
+// compiled once per process.
+#include <dlfcn.h>
+#include <fcntl.h>
 #include <hip/hip_runtime_api.h>
-#include <hip/hiprtc.h>
+#include <spawn.h>
+#include <sys/wait.h>
+#include <unistd.h>
 
 #include <algorithm>
 #include <atomic>
@@ -26,13 +30,9 @@
 #include "vqc.h"
 #include "vqc_internal.h"
 
-namespace vqc {
+extern char** environ;
 
-// Shared headers embedded at build time (generated from vqc.h, vqc_structs.h,
-// vqc_device.h).
-extern const int kJitHeaderCount;
-extern const char* const kJitHeaderNames[];
-extern const char* const kJitHeaderSources[];
+namespace vqc {
 
 namespace {
 
@@ -189,6 +189,22 @@ std::string kernel_unit(const Plan& p, const std::string& name, const uint32_t* 
 
 }  // namespace
 
+// The training step: forward and adjoint sweeps in one kernel.
+std::string step_unit(const Plan& p) {
+  std::ostringstream o;
+  o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
+  const int lanes = 1 << (p.k - p.R);
+  const GradMode gm = grad_mode(lanes, p.P + p.F);
+  emit_sched_struct(o, "SchedF", p, p.fwd.data(), (int)p.fwd.size() / 2, false, p.R, p.k, p.S, gm);
+  emit_sched_struct(o, "SchedB", p, p.bwd.data(), (int)p.bwd.size() / 2, true, p.R, p.k, p.S, gm);
+  o << "}  // namespace vqc\n"
+    << "extern \"C\" __global__ void __launch_bounds__(" << p.WG << ") vqc_rs(const vqc::TileArgs A) {\n"
+    << "  __shared__ __align__(16) unsigned char smem[" << lds_size(p.lds_step) << "];\n"
+    << "  vqc::resident_step_body<" << p.WG << ", " << p.R
+    << ", vqc::SchedF, vqc::SchedB>(A, smem);\n}\n";
+  return o.str();
+}
+
 std::vector<JitUnit> jit_units(const Plan& p) {
   std::vector<JitUnit> u;
   if (p.path == VQC_PATH_RESIDENT) {
@@ -196,6 +212,7 @@ std::vector<JitUnit> jit_units(const Plan& p) {
                                        false, p.R, p.S, p.WG, p.lds_fwd, p.P + p.F)});
     u.push_back({"vqc_rb", kernel_unit(p, "vqc_rb", p.bwd.data(), (int)p.bwd.size() / 2, true,
                                        false, p.R, p.S, p.WG, p.lds_bwd, p.P + p.F)});
+    u.push_back({"vqc_rs", step_unit(p)});
     return u;
   }
   for (size_t i = 0; i < p.fpass.size(); ++i) {
@@ -215,60 +232,142 @@ std::vector<JitUnit> jit_units(const Plan& p) {
 
 namespace {
 
-const char* const kJitOptions[] = {
-    "--offload-arch=gfx950", "-O3", "-std=c++17",
-    // no packed FP32 instructions in any device code
-    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    // keep the near-identical register cases apart (see build.py)
-    "-mllvm", "-simplifycfg-sink-common=false", "-mllvm", "-simplifycfg-hoist-common=false"};
-
-int compile_source(const std::string& src, std::vector<char>& code, std::string& log) {
-  hiprtcProgram prog;
-  if (hiprtcCreateProgram(&prog, src.c_str(), "vqc_jit.hip", kJitHeaderCount, kJitHeaderSources,
-                          kJitHeaderNames) != HIPRTC_SUCCESS) {
-    log = "hiprtcCreateProgram failed";
-    return VQC_ERR_UNSUPPORTED;
-  }
-  const int nopt = (int)(sizeof(kJitOptions) / sizeof(kJitOptions[0]));
-  const hiprtcResult rc = hiprtcCompileProgram(prog, nopt, kJitOptions);
-  size_t n = 0;
-  hiprtcGetProgramLogSize(prog, &n);
-  log.assign(n, '\0');
-  if (n) hiprtcGetProgramLog(prog, &log[0]);
-  if (rc != HIPRTC_SUCCESS) {
-    hiprtcDestroyProgram(&prog);
-    return VQC_ERR_UNSUPPORTED;
-  }
-  size_t sz = 0;
-  hiprtcGetCodeSize(prog, &sz);
-  code.resize(sz);
-  hiprtcGetCode(prog, code.data());
-  hiprtcDestroyProgram(&prog);
-  return VQC_OK;
+// The helper next to this library (vqc_jitc), or "" when it is missing.
+const std::string& helper_path() {
+  static const std::string path = [] {
+    Dl_info info;
+    if (dladdr(reinterpret_cast<void*>(&compile_source), &info) && info.dli_fname) {
+      const std::string lib = info.dli_fname;
+      const size_t slash = lib.rfind('/');
+      const std::string h = (slash == std::string::npos ? std::string(".") : lib.substr(0, slash)) +
+                            "/vqc_jitc";
+      if (access(h.c_str(), X_OK) == 0) return h;
+    }
+    return std::string();
+  }();
+  return path;
 }
 
-// Compiles every source on a pool of host threads; returns the first failure.
+bool read_file(const std::string& path, std::vector<char>& out) {
+  FILE* f = std::fopen(path.c_str(), "rb");
+  if (!f) return false;
+  out.clear();
+  char buf[1 << 16];
+  size_t n;
+  while ((n = std::fread(buf, 1, sizeof buf, f)) > 0) out.insert(out.end(), buf, buf + n);
+  std::fclose(f);
+  return true;
+}
+
+bool write_file(const std::string& path, const std::string& text) {
+  FILE* f = std::fopen(path.c_str(), "wb");
+  if (!f) return false;
+  const bool ok = std::fwrite(text.data(), 1, text.size(), f) == text.size();
+  return std::fclose(f) == 0 && ok;
+}
+
+// Compiles the sources in child processes of the helper, at most `slots` at a
+// time.  Returns false when the helper could not be run (the caller then
+// compiles in this process); a failed compilation returns true with rc set.
+bool compile_in_children(const std::vector<const std::string*>& srcs, size_t slots,
+                         std::vector<std::vector<char>>& codes, int& rc, std::string& log) {
+  const std::string& helper = helper_path();
+  if (helper.empty()) return false;
+  const char* tmp = std::getenv("TMPDIR");
+  std::string dir = std::string(tmp && *tmp ? tmp : "/tmp") + "/vqcjit.XXXXXX";
+  if (!mkdtemp(&dir[0])) return false;
+  const size_t n = srcs.size();
+  std::vector<std::string> in(n), out(n), err(n);
+  bool ok = true;
+  for (size_t i = 0; i < n && ok; ++i) {
+    in[i] = dir + "/k" + std::to_string(i) + ".hip";
+    out[i] = dir + "/k" + std::to_string(i) + ".co";
+    err[i] = dir + "/k" + std::to_string(i) + ".log";
+    ok = write_file(in[i], *srcs[i]);
+  }
+  std::vector<int> status(n, -1);
+  std::vector<pid_t> pid(n, -1);
+  size_t next = 0, running = 0, done = 0;
+  while (ok && done < n) {
+    while (next < n && running < slots) {
+      posix_spawn_file_actions_t fa;
+      posix_spawn_file_actions_init(&fa);
+      posix_spawn_file_actions_addopen(&fa, 2, err[next].c_str(), O_WRONLY | O_CREAT | O_TRUNC,
+                                       0644);
+      char* argv[] = {const_cast<char*>(helper.c_str()), const_cast<char*>(in[next].c_str()),
+                      const_cast<char*>(out[next].c_str()), nullptr};
+      const int e = posix_spawn(&pid[next], helper.c_str(), &fa, nullptr, argv, environ);
+      posix_spawn_file_actions_destroy(&fa);
+      if (e != 0) {
+        ok = false;
+        break;
+      }
+      ++next;
+      ++running;
+    }
+    bool reaped = false;
+    for (size_t i = 0; i < next; ++i) {
+      if (pid[i] <= 0 || status[i] != -1) continue;
+      int st = 0;
+      const pid_t r = waitpid(pid[i], &st, WNOHANG);
+      if (r == pid[i] || r < 0) {
+        status[i] = (r == pid[i] && WIFEXITED(st)) ? WEXITSTATUS(st) : 255;
+        --running;
+        ++done;
+        reaped = true;
+      }
+    }
+    if (!reaped && ok) usleep(2000);
+  }
+  // children still running after a spawn failure are waited for
+  for (size_t i = 0; i < next; ++i)
+    if (pid[i] > 0 && status[i] == -1) {
+      int st = 0;
+      (void)waitpid(pid[i], &st, 0);
+      status[i] = 255;
+    }
+  rc = VQC_OK;
+  if (ok) {
+    codes.assign(n, {});
+    for (size_t i = 0; i < n; ++i) {
+      if (status[i] == 0 && read_file(out[i], codes[i])) continue;
+      if (status[i] == 1) {  // the compiler rejected the source
+        std::vector<char> text;
+        read_file(err[i], text);
+        log.assign(text.begin(), text.end());
+        rc = VQC_ERR_UNSUPPORTED;
+      } else {
+        ok = false;  // the helper itself failed: compile here instead
+      }
+      break;
+    }
+  }
+  for (size_t i = 0; i < n; ++i) {
+    unlink(in[i].c_str());
+    unlink(out[i].c_str());
+    unlink(err[i].c_str());
+  }
+  rmdir(dir.c_str());
+  return ok;
+}
+
+// Compiles every source; returns the first failure.  Several kernels go to
+// helper processes in parallel (VQC_JIT_INPROC=1 keeps everything in this
+// process, where compilations run one at a time).
 int compile_all(const std::vector<const std::string*>& srcs, std::vector<std::vector<char>>& codes,
                 std::string& log) {
+  const unsigned hw = std::thread::hardware_concurrency();
+  const size_t slots = std::min<size_t>(srcs.size(), hw ? std::min(hw, 16u) : 4u);
+  const char* inproc = std::getenv("VQC_JIT_INPROC");
+  if (slots > 1 && !(inproc && *inproc == '1')) {
+    int rc = VQC_OK;
+    if (compile_in_children(srcs, slots, codes, rc, log)) return rc;
+  }
   codes.assign(srcs.size(), {});
-  std::vector<int> rcs(srcs.size(), VQC_OK);
-  std::vector<std::string> logs(srcs.size());
-  unsigned hw = std::thread::hardware_concurrency();
-  const size_t nthreads = std::min<size_t>(srcs.size(), hw ? std::min(hw, 16u) : 4u);
-  std::atomic<size_t> next{0};
-  auto work = [&]() {
-    for (size_t i; (i = next.fetch_add(1)) < srcs.size();)
-      rcs[i] = compile_source(*srcs[i], codes[i], logs[i]);
-  };
-  std::vector<std::thread> pool;
-  for (size_t t = 1; t < nthreads; ++t) pool.emplace_back(work);
-  work();
-  for (auto& th : pool) th.join();
-  for (size_t i = 0; i < srcs.size(); ++i)
-    if (rcs[i] != VQC_OK) {
-      log = logs[i];
-      return rcs[i];
-    }
+  for (size_t i = 0; i < srcs.size(); ++i) {
+    const int rc = compile_source(*srcs[i], codes[i], log);
+    if (rc != VQC_OK) return rc;
+  }
   return VQC_OK;
 }
 
@@ -348,6 +447,7 @@ int jit_build(const Plan& p, int device, JitKernels& out, std::string& msg) {
   if (p.path == VQC_PATH_RESIDENT) {
     out.res_fwd = fns[0];
     out.res_bwd = fns[1];
+    out.res_step = fns[2];
   } else {
     out.pass_fwd.assign(fns.begin(), fns.begin() + p.fpass.size());
     out.pass_bwd.assign(fns.begin() + p.fpass.size(), fns.end());

@@ -16,6 +16,12 @@ __global__ void __launch_bounds__(WG) resident_kernel(const TileArgs A) {
   resident_body<WG, BWD, R, InterpSched>(A, smem);
 }
 
+template <int WG, int R>
+__global__ void __launch_bounds__(WG) resident_step_kernel(const TileArgs A) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  resident_step_body<WG, R, InterpSched, InterpSched>(A, smem);
+}
+
 template <bool BWD, int R>
 __global__ void __launch_bounds__(1 << (kMaxTileQubits - R)) stream_kernel(const PassArgs A) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -60,25 +66,8 @@ __global__ void loss_grad_kernel(int kind, int64_t B, int n, const float* __rest
   if (b >= B) return;
   const float* eb = e + b * n;
   float* gb = g + b * n;
-  switch (kind) {
-    case VQC_LOSS_SUM:
-      for (int j = 0; j < n; ++j) gb[j] = 1.f;
-      break;
-    case VQC_LOSS_MEAN:
-      for (int j = 0; j < n; ++j) gb[j] = 1.f / (float)n;
-      break;
-    case VQC_LOSS_MSE_Z0:
-      gb[0] = 2.f * (eb[0] - y[b]) / (float)B;
-      for (int j = 1; j < n; ++j) gb[j] = 0.f;
-      break;
-    default: {
-      float s = 0.f;
-      for (int j = 0; j < n; ++j) s += eb[j];
-      s /= (float)n;
-      const float v = 2.f * (s - y[b]) / ((float)n * (float)B);
-      for (int j = 0; j < n; ++j) gb[j] = v;
-    }
-  }
+  const float yb = y ? y[b] : 0.f;
+  for (int j = 0; j < n; ++j) gb[j] = loss_cot(kind, eb, yb, n, j, B);
 }
 
 // ------------------------------------------------------------ launchers
@@ -142,6 +131,8 @@ int prepare_kernels(const Plan& p) {
       constexpr int WG = decltype(Wc)::value;
       int e = set_attr((const void*)resident_kernel<WG, false, R>, p.lds_fwd);
       if (e) return e;
+      e = set_attr((const void*)resident_step_kernel<WG, R>, p.lds_step);
+      if (e) return e;
       return set_attr((const void*)resident_kernel<WG, true, R>, p.lds_bwd);
     });
   });
@@ -153,6 +144,18 @@ int launch_resident_forward(const Plan& plan, const TileArgs& a, int64_t blocks,
 
 int launch_resident_backward(const Plan& plan, const TileArgs& a, int64_t blocks, void* stream) {
   return launch_resident<true>(plan, a, blocks, stream);
+}
+
+int launch_resident_step(const Plan& p, const TileArgs& a, int64_t blocks, void* stream) {
+  return by_res_r(p.R, [&](auto Rc) {
+    constexpr int R = decltype(Rc)::value;
+    return by_wg(p.WG, [&](auto Wc) {
+      constexpr int WG = decltype(Wc)::value;
+      hipLaunchKernelGGL((resident_step_kernel<WG, R>), dim3((unsigned)blocks), dim3(WG),
+                         p.lds_step, (hipStream_t)stream, a);
+      return (int)hipGetLastError();
+    });
+  });
 }
 
 int launch_stream_pass(const Plan& p, bool bwd, const PassArgs& a, int64_t blocks,

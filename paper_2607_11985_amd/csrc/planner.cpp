@@ -24,6 +24,9 @@
 static_assert(vqc::kSrcParam == VQC_SRC_PARAM && vqc::kSrcInput == VQC_SRC_INPUT &&
                   vqc::kSrcConst == VQC_SRC_CONST,
               "angle source codes of the device header and the C ABI differ");
+static_assert(vqc::kLossSum == VQC_LOSS_SUM && vqc::kLossMean == VQC_LOSS_MEAN &&
+                  vqc::kLossMseZ0 == VQC_LOSS_MSE_Z0 && vqc::kLossMseMeanZ == VQC_LOSS_MSE_MEANZ,
+              "loss head codes of the device header and the C ABI differ");
 
 namespace vqc {
 namespace {
@@ -476,6 +479,10 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     const size_t acc = align_up((size_t)(P + F) * plan.G * 4, 16);
     plan.lds_fwd = std::max<size_t>(xbuf + tab, 16);
     plan.lds_bwd = xbuf + tab + acc;
+    // training step: E and g rows of the workgroup's samples after the adjoint's
+    // tables
+    plan.lds_e = align_up(plan.lds_bwd, 16);
+    plan.lds_step = plan.lds_e + 2 * (size_t)plan.S * n * 4;
   } else {
     plan.k = kMaxTileQubits;
     plan.ng = nq - plan.k;
@@ -499,8 +506,9 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     plan.lds_fwd = xbuf + tab;
     plan.lds_bwd = xbuf + tab + acc;
   }
-  if (plan.lds_bwd > (size_t)kLdsBytes) {
-    msg = "circuit too large for on-chip tables: " + std::to_string(plan.lds_bwd) +
+  if (std::max(plan.lds_bwd, plan.lds_step) > (size_t)kLdsBytes) {
+    msg = "circuit too large for on-chip tables: " +
+          std::to_string(std::max(plan.lds_bwd, plan.lds_step)) +
           " bytes of LDS needed (limit " + std::to_string(kLdsBytes) + ")";
     return VQC_ERR_TOO_LARGE;
   }

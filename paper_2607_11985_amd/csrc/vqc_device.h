@@ -653,58 +653,123 @@ struct InterpSched {
   }
 };
 
+// Cotangent g_j = dL/dE_j of one sample's row e[0..n) for the loss heads of the
+// C ABI (y: the sample's target, B: the batch the mean runs over).
+__device__ __forceinline__ float loss_cot(int kind, const float* e, float y, int n, int j,
+                                          int64_t B) {
+  if (kind == kLossSum) return 1.f;
+  if (kind == kLossMean) return 1.f / (float)n;
+  if (kind == kLossMseZ0) return j == 0 ? 2.f * (e[0] - y) / (float)B : 0.f;
+  float s = 0.f;
+  for (int q = 0; q < n; ++q) s += e[q];
+  s /= (float)n;
+  return 2.f * (s - y) / ((float)n * (float)B);
+}
+
 // ------------------------------------------------------ resident body
 
-// One launch for a tile of samples; Sched runs the instruction stream (the
-// interpreter of the precompiled kernels, or the straight-line code generated
-// for one circuit).
-template <int WG, bool BWD, int R, typename Sched>
-__device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* smem) {
-  float* xbuf = reinterpret_cast<float*>(smem);
-  float2* tab = reinterpret_cast<float2*>(smem + A.lds_tab);
-  float* acc = reinterpret_cast<float*>(smem + A.lds_acc);
-  constexpr int NA = 1 << R;
+// One launch for a tile of S samples (T = 2^t threads each); Sched runs the
+// instruction stream (the interpreter of the precompiled kernels, or the
+// straight-line code generated for one circuit).
 
+template <int WG, int R>
+__device__ __forceinline__ Walk resident_walk(const TileArgs& A, unsigned char* smem) {
+  Walk w;
   const int tid = threadIdx.x;
   const int T = 1 << A.t;
-  const int stid = tid & (T - 1);
-  const int sl = tid >> A.t;
-  const int S = A.S;
-  const int64_t b0 = (int64_t)blockIdx.x * S;
-  const int64_t b = b0 + sl;
-  const bool valid = b < A.B;
-  Walk w;
   w.cols = A.cols;
-  w.xbuf = xbuf;
-  w.plane = (uint32_t)WG * NA;
-  w.tab = tab;
-  w.acc = acc;
+  w.xbuf = reinterpret_cast<float*>(smem);
+  w.plane = (uint32_t)WG << R;
+  w.tab = reinterpret_cast<float2*>(smem + A.lds_tab);
+  w.acc = reinterpret_cast<float*>(smem + A.lds_acc);
   w.k = A.k;
   w.t = A.t;
-  w.S = S;
+  w.S = A.S;
   w.G = A.G;
-  w.stid = stid;
-  w.sl = sl;
+  w.stid = tid & (T - 1);
+  w.sl = tid >> A.t;
   w.width = T < 64 ? T : 64;
-  w.grp = T < 64 ? sl : (tid >> 6);
+  w.grp = T < 64 ? w.sl : (tid >> 6);
   w.leader = (tid & (w.width - 1)) == 0;
   w.never = A.B < 0;
-  w.tb = (uint32_t)stid;
+  w.tb = (uint32_t)w.stid;
+  return w;
+}
 
-  angle_table(tab, A.n_occ, S, b0, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.P, A.inputs,
-              A.F, tid, WG);
+// <Z_q> of the workgroup's samples from the ez partials: e[s * n + q] (when e
+// is not null) and expvals rows.  Every thread must call it.
+__device__ __forceinline__ void resident_expvals(const TileArgs& A, const float* ez, float* e,
+                                                 int WG) {
+  const int S = A.S;
+  const int64_t b0 = (int64_t)blockIdx.x * S;
+  for (int i = threadIdx.x; i < A.n * S; i += WG) {
+    const int q = i / S;
+    const int s = i - q * S;
+    const int64_t bb = b0 + s;
+    float v;
+    if (A.t >= 6) {
+      v = 0.f;
+      for (int g = 0; g < A.G; ++g) v += ez[q * A.G + g];
+    } else {
+      v = ez[q * A.G + s];
+    }
+    if (e) e[s * A.n + q] = v;
+    if (bb < A.B) A.expvals[bb * A.n + q] = v;
+  }
+}
+
+// dparams / dinputs rows from the per-group accumulators (after a barrier).
+__device__ __forceinline__ void resident_grads(const TileArgs& A, const float* acc, int WG) {
+  const int S = A.S;
+  const int64_t b0 = (int64_t)blockIdx.x * S;
+  for (int i = threadIdx.x; i < A.n_slots * S; i += WG) {
+    const int slot = i / S;
+    const int s = i - slot * S;
+    const int64_t bb = b0 + s;
+    if (bb >= A.B) continue;
+    float v;
+    if (A.t >= 6) {
+      v = 0.f;
+      for (int g = 0; g < A.G; ++g) v += acc[slot * A.G + g];
+    } else {
+      v = acc[slot * A.G + s];
+    }
+    if (slot < A.P) {
+      if (A.dparams) A.dparams[bb * A.P + slot] = v;
+    } else if (A.dinputs) {
+      A.dinputs[bb * A.F + (slot - A.P)] = v;
+    }
+  }
+}
+
+template <int R>
+__device__ __forceinline__ void zero_state(St<R>& a, int stid) {
+#pragma unroll
+  for (int j = 0; j < St<R>::N; ++j) {
+    a.r[j] = 0.f;
+    a.i[j] = 0.f;
+  }
+  if (stid == 0) a.r[0] = 1.f;
+}
+
+template <int WG, bool BWD, int R, typename Sched>
+__device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* smem) {
+  constexpr int NA = 1 << R;
+  const int tid = threadIdx.x;
+  const Walk w = resident_walk<WG, R>(A, smem);
+  const int64_t b0 = (int64_t)blockIdx.x * A.S;
+  const int64_t b = b0 + w.sl;
+  const bool valid = b < A.B;
+
+  angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
+              A.occ_idx, A.occ_cs, A.params, A.P, A.inputs, A.F, tid, WG);
   if (BWD)
-    for (int i = tid; i < A.n_slots * A.G; i += WG) acc[i] = 0.f;
+    for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
 
   St<R> a, l;
   if (!BWD) {
-#pragma unroll
-    for (int j = 0; j < NA; ++j) {
-      a.r[j] = 0.f;
-      a.i[j] = 0.f;
-    }
-    if (stid == 0) a.r[0] = 1.f;
+    zero_state<R>(a, w.stid);
   } else {
     const float2* ws = reinterpret_cast<const float2*>(A.ws);
     float2 v[NA];
@@ -724,43 +789,51 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
       for (int j = 0; j < NA; ++j)
         ws[((size_t)blockIdx.x * NA + j) * WG + tid] = make_float2(a.r[j], a.i[j]);
     }
-    float* ez = xbuf;
-    z_partials<R, Sched>(a, ez, A.n, A.end_phys, w);
-    for (int i = tid; i < A.n * S; i += WG) {
-      const int q = i / S;
-      const int s = i - q * S;
-      const int64_t bb = b0 + s;
-      if (bb >= A.B) continue;
-      float e;
-      if (T >= 64) {
-        e = 0.f;
-        for (int g = 0; g < A.G; ++g) e += ez[q * A.G + g];
-      } else {
-        e = ez[q * A.G + s];
-      }
-      A.expvals[bb * A.n + q] = e;
-    }
+    z_partials<R, Sched>(a, w.xbuf, A.n, A.end_phys, w);
+    resident_expvals(A, w.xbuf, nullptr, WG);
   } else {
     __syncthreads();
-    for (int i = tid; i < A.n_slots * S; i += WG) {
-      const int slot = i / S;
-      const int s = i - slot * S;
-      const int64_t bb = b0 + s;
-      if (bb >= A.B) continue;
-      float v;
-      if (T >= 64) {
-        v = 0.f;
-        for (int g = 0; g < A.G; ++g) v += acc[slot * A.G + g];
-      } else {
-        v = acc[slot * A.G + s];
-      }
-      if (slot < A.P) {
-        if (A.dparams) A.dparams[bb * A.P + slot] = v;
-      } else if (A.dinputs) {
-        A.dinputs[bb * A.F + (slot - A.P)] = v;
-      }
-    }
+    resident_grads(A, w.acc, WG);
   }
+}
+
+// Training step in one launch: forward (FS), <Z>, the loss head's cotangent,
+// lambda = (sum_j g_j Z_j) psi and the adjoint sweep (BS).  The state stays on
+// chip between the two sweeps; nothing is saved to HBM.
+template <int WG, int R, typename FS, typename BS>
+__device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned char* smem) {
+  const int tid = threadIdx.x;
+  const Walk w = resident_walk<WG, R>(A, smem);
+  const int64_t b0 = (int64_t)blockIdx.x * A.S;
+  const bool valid = b0 + w.sl < A.B;
+  float* e = reinterpret_cast<float*>(smem + A.lds_e);  // [S][n]
+  float* g = e + A.S * A.n;                             // [S][n]
+
+  angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
+              A.occ_idx, A.occ_cs, A.params, A.P, A.inputs, A.F, tid, WG);
+  for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
+  __syncthreads();
+
+  St<R> a, l;
+  zero_state<R>(a, w.stid);
+  FS::template run<R, false, (WG > 64)>(a, l, w, A.ins, A.n_ins);
+  z_partials<R, FS>(a, w.xbuf, A.n, A.end_phys, w);
+  resident_expvals(A, w.xbuf, e, WG);
+  __syncthreads();
+  for (int i = tid; i < A.S * A.n; i += WG) {
+    const int s = i / A.n;
+    const int q = i - s * A.n;
+    const int64_t bb = b0 + s;
+    const float y = (A.target && bb < A.B) ? A.target[bb] : 0.f;
+    const float v = loss_cot(A.loss, e + s * A.n, y, A.n, q, A.B);
+    g[i] = v;
+    if (A.cot_out && bb < A.B) A.cot_out[bb * A.n + q] = v;
+  }
+  __syncthreads();
+  make_lambda<R>(l, a, g + w.sl * A.n, A.n, A.end_phys, w.tb, valid);
+  BS::template run<R, true, (WG > 64)>(a, l, w, A.ins_b, A.n_ins_b);
+  __syncthreads();
+  resident_grads(A, w.acc, WG);
 }
 
 // ----------------------------------------------------- streaming kernel

@@ -55,6 +55,7 @@ struct Plan {
   int fwd_exchanges = 0, bwd_exchanges = 0;
   int max_pass_slots = 0;
   size_t lds_fwd = 0, lds_bwd = 0, lds_tab = 0, lds_acc = 0;
+  size_t lds_e = 0, lds_step = 0;  // resident training step (0 when streaming)
 };
 
 // Host planning (no device calls).  Returns 0 or a VQC_ERR_* code with msg.
@@ -69,6 +70,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
 // Kernel launchers (kernels.hip).  Return 0 or a hipError_t value.
 int launch_resident_forward(const Plan& plan, const TileArgs& a, int64_t blocks, void* stream);
 int launch_resident_backward(const Plan& plan, const TileArgs& a, int64_t blocks, void* stream);
+int launch_resident_step(const Plan& plan, const TileArgs& a, int64_t blocks, void* stream);
 
 int launch_stream_pass(const Plan& plan, bool bwd, const PassArgs& a, int64_t blocks,
                        void* stream);
@@ -84,6 +86,7 @@ int prepare_kernels(const Plan& plan);
 struct JitKernels {
   void* res_fwd = nullptr;            // hipFunction_t
   void* res_bwd = nullptr;
+  void* res_step = nullptr;           // forward, loss head and adjoint in one launch
   std::vector<void*> pass_fwd, pass_bwd;
 };
 struct JitUnit {
@@ -91,6 +94,8 @@ struct JitUnit {
 };
 std::vector<JitUnit> jit_units(const Plan& plan);
 int jit_compile_only(const Plan& plan, std::string& log);
+// hiprtc compilation of one generated kernel (jit_compile.cpp)
+int compile_source(const std::string& src, std::vector<char>& code, std::string& log);
 int jit_build(const Plan& plan, int device, JitKernels& out, std::string& msg);
 int jit_launch(void* fn, int64_t blocks, int threads, const void* args, size_t args_size,
                void* stream);

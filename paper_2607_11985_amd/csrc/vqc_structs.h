@@ -30,6 +30,10 @@ constexpr int kBankBits = 5;                 // lane bits kept bank-conflict fre
 constexpr int kSrcParam = 0;                 // angle sources, as in the C ABI
 constexpr int kSrcInput = 1;
 constexpr int kSrcConst = 2;
+constexpr int kLossSum = 0;                  // loss heads, as in the C ABI
+constexpr int kLossMean = 1;
+constexpr int kLossMseZ0 = 2;
+constexpr int kLossMseMeanZ = 3;
 
 // primitive kinds after lowering (ROT -> RZ, RY, RZ)
 enum PrimKind : int { P_RX = 0, P_RY = 1, P_RZ = 2, P_CNOT = 4, P_CZ = 5 };
@@ -83,6 +87,13 @@ struct TileArgs {
   float* dinputs;
   uint32_t lds_tab;         // byte offset of the angle table in LDS
   uint32_t lds_acc;         // byte offset of the gradient accumulators
+  // training step only (forward, loss head and adjoint in one launch)
+  const uint32_t* ins_b;    // the adjoint's instruction pairs
+  int32_t n_ins_b;
+  int32_t loss;             // loss head kLoss*
+  const float* target;      // [B] (MSE heads)
+  float* cot_out;           // [B, n] cotangent written here when not null
+  uint32_t lds_e;           // byte offset of E and g rows [S][n] each
 };
 
 // Arguments of one streaming pass (1024 threads, one 2^14 tile per workgroup).

@@ -70,6 +70,12 @@ def test_configs_plan_on_host(idx):
     assert info["fwd_instructions"] == n_prims + info["fwd_exchanges"]
     assert info["bwd_instructions"] == n_prims + info["bwd_exchanges"]
     assert _lib.vqc_workspace_bytes(h, 0, 1) == 0
+    assert _lib.vqc_workspace_bytes(h, 10, 3) == ctypes.c_size_t(-1).value
+    step = _lib.vqc_workspace_bytes(h, 10, 2)
+    if stream:  # training workspace plus the cotangent rows
+        assert step >= _lib.vqc_workspace_bytes(h, 10, 1) + 10 * w.n_qubits * 4
+    else:       # the resident step keeps every state on chip
+        assert step == 0
     assert _lib.vqc_workspace_bytes(h, 10, 0) == (0 if not stream else
                                                   _lib.vqc_workspace_bytes(h, 10, 0))
     assert _lib.vqc_workspace_bytes(h, 10, 1) >= 10 * (1 << w.n_qubits) * 8 * (3 if stream else 1)
@@ -84,6 +90,8 @@ def test_host_only_handle_cannot_run(lib):
     assert rc == _lib.VQC_ERR_INVALID_ARG and "host-only" in _lib.vqc_last_error()
     rc = lib.vqc_backward(h, 2, 1, 1, 1, 1, 1 << 20, 1, 1, None)
     assert rc == _lib.VQC_ERR_INVALID_ARG
+    rc = lib.vqc_train_step(h, 2, 1, 1, 0, None, 1, None, 1, 1, None, 0, None)
+    assert rc == _lib.VQC_ERR_INVALID_ARG and "host-only" in _lib.vqc_last_error()
     _lib.vqc_destroy(h)
 
 
@@ -92,6 +100,8 @@ def test_null_handle_and_out(lib):
     assert lib.vqc_backward(None, 1, None, None, None, None, 0, None, None, None) == \
         _lib.VQC_ERR_INVALID_ARG
     assert lib.vqc_circuit_info(None, None) == _lib.VQC_ERR_INVALID_ARG
+    assert lib.vqc_train_step(None, 1, None, None, 0, None, None, None, None, None, None, 0,
+                              None) == _lib.VQC_ERR_INVALID_ARG
     assert lib.vqc_workspace_bytes(None, 1, 1) == ctypes.c_size_t(-1).value
     lib.vqc_destroy(None)
     arr = _lib.encode_ops([])

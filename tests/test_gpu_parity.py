@@ -195,6 +195,63 @@ def test_config_full_batch_sampled(torch_mod, idx, rows):
     check_grads({"dp": r["dp"][rows], "dx": r["dx"][rows]}, dpr, dxr, cot[rows])
 
 
+def check_cot(g, E_ref, y, loss, batch):
+    """The step's cotangent against the loss head evaluated on the oracle's E
+    (batch: the batch size the MSE mean runs over)."""
+    n = E_ref.shape[1]
+    if loss == "sum":
+        ref = np.ones_like(E_ref)
+    elif loss == "mean":
+        ref = np.full_like(E_ref, 1.0 / n)
+    elif loss == "mse_z0":
+        ref = np.zeros_like(E_ref)
+        ref[:, 0] = 2.0 * (E_ref[:, 0] - y) / batch
+    else:
+        ref = np.repeat((2.0 * (E_ref.mean(axis=1) - y) / (n * batch))[:, None], n, axis=1)
+    # E is within E_TOL, so the cotangent is within 2 E_TOL / batch (+ rounding)
+    err = float(np.max(np.abs(g.astype(np.float64) - ref)))
+    assert err <= 2 * E_TOL / batch + 1e-6 * max(1.0, float(np.max(np.abs(ref)))), err
+
+
+@pytest.mark.parametrize("n,loss,path,engine", [
+    (1, "sum", "auto", "jit"), (3, "mean", "auto", "jit"), (6, "mse_z0", "auto", "jit"),
+    (9, "mse_meanz", "auto", "jit"), (12, "mse_z0", "auto", "jit"),
+    (13, "mse_meanz", "auto", "jit"), (14, "mean", "stream", "jit"),
+    (15, "mse_meanz", "auto", "jit"), (7, "mse_meanz", "auto", "interp"),
+    (14, "mse_z0", "resident", "interp")])
+def test_train_step_parity(torch_mod, n, loss, path, engine):
+    """vqc_train_step (forward, loss head and adjoint in one call; one launch on
+    the resident path) against the oracle, and against the three separate calls."""
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit, loss_grad
+    S = samples_per_wg(n)
+    B = 2 * S + 1 if S > 1 else 5
+    ops, P, F = W.random_circuit(n, 40 + 5 * n, seed=8000 + n)
+    params, inputs = W.random_inputs(B, P, F, seed=8100 + n)
+    y = np.random.default_rng(8200 + n).uniform(-1, 1, size=B).astype(np.float32)
+    note(f"train step n={n} loss={loss} path={path} engine={engine} B={B}")
+    c = Circuit(ops, n, P, F, path=path, engine=engine)
+    p = torch.from_numpy(params).cuda()
+    x = torch.from_numpy(inputs).cuda()
+    yt = torch.from_numpy(y).cuda()
+    E, dp, dx, g = c.train_step(p, x, loss, yt, want_cot=True)
+    torch.cuda.synchronize()
+    E, dp, dx, g = (t.cpu().numpy() for t in (E, dp, dx, g))
+    Er = oracle.forward(ops, n, params, inputs)
+    check_E(E, Er)
+    check_cot(g, Er, y.astype(np.float64), loss, B)
+    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, g.astype(np.float64))
+    check_grads({"dp": dp, "dx": dx}, dpr, dxr, g)
+    # the separate calls give the same results (up to the compiler's rounding)
+    E2, ws = c.forward(p, x, training=True)
+    g2 = loss_grad(loss, E2, yt)
+    dp2, dx2 = c.backward(p, x, g2, ws)
+    torch.cuda.synchronize()
+    assert np.max(np.abs(E2.cpu().numpy() - E)) <= 1e-6
+    assert np.max(np.abs(g2.cpu().numpy() - g)) <= 1e-6
+    check_grads({"dp": dp2.cpu().numpy(), "dx": dx2.cpu().numpy()}, dp, dx, g)
+
+
 def test_loss_grad_kernel(torch_mod):
     from paper_2607_11985_amd.api import loss_grad
     rng = np.random.default_rng(4)
