@@ -199,12 +199,12 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
   int rc = 0;
   for (const vqc::PassPlan& pp : p.fpass) {
     vqc::PassArgs a = pass_args(c, pp, false, batch);
+    const size_t i = &pp - p.fpass.data();
     a.params = params;
     a.inputs = inputs;
     a.psi_src = ws + L.psi;
     a.psi_dst = ws + L.psi;
     a.epart = reinterpret_cast<float*>(ws + L.epart);
-    const size_t i = &pp - p.fpass.data();
     rc = c->engine == VQC_ENGINE_JIT
              ? vqc::jit_launch(c->jit.pass_fwd[i], batch << p.ng, 1 << (p.k - p.Rf), &a, sizeof(a),
                                stream)
@@ -229,6 +229,7 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
   bool first = true;
   for (const vqc::PassPlan& pp : p.bpass) {
     vqc::PassArgs a = pass_args(c, pp, true, batch);
+    const size_t j = &pp - p.bpass.data();
     a.params = params;
     a.inputs = inputs;
     a.grad_out = grad_out;
@@ -237,9 +238,8 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     a.lam_src = ws + L.lamw;
     a.lam_dst = ws + L.lamw;
     a.gpart = gpart;
-    const size_t i = &pp - p.bpass.data();
     rc = c->engine == VQC_ENGINE_JIT
-             ? vqc::jit_launch(c->jit.pass_bwd[i], batch << p.ng, 1 << (p.k - p.Rb), &a, sizeof(a),
+             ? vqc::jit_launch(c->jit.pass_bwd[j], batch << p.ng, 1 << (p.k - p.Rb), &a, sizeof(a),
                                stream)
              : vqc::launch_stream_pass(p, true, a, batch << p.ng, stream);
     if (rc) return hip_fail("backward pass launch", rc);

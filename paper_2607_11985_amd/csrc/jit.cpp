@@ -62,10 +62,223 @@ GradMode grad_mode(int lanes_per_sample, int n_slots) {
   return g;
 }
 
-// Statements of one instruction stream for register width R.
+// ------------------------------------------------------------ tangent form
+// With one sample per workgroup the generated kernels apply every rotation as
+// I - i t P with |t| <= 1 (vqc_device.h, "tangent form"): the Pauli P^m that
+// brings the half angle into [-pi/4, pi/4] is moved aside.  The moved Paulis
+// form a frame F, one Pauli string per sample, which changes where a rotation's
+// m is odd (its parity bit) and where an entangler conjugates it.  That is
+// GF(2)-linear, so for rotation j, "F anticommutes with P_j on j's qubit" (then
+// t_j and the gradient of j change sign) is the parity of (parities AND
+// arow[j]), and "<Z_q> changes sign" that of (parities AND erow[q]); the rows
+// are compile-time constants over all occurrences in circuit order.  Gates that
+// the streaming planner reorders commute, and a Pauli carried through a
+// commuting gate is unchanged, so the rows hold for every execution order.
+// The factors cos(phi') are applied to the state after every kBlock rotations
+// of a stream (each unscaled gate grows the state by at most sqrt 2), and the
+// adjoint scales each gradient by the square of the factors not yet applied.
+constexpr int kBlock = 24;
+
+struct Frame {
+  int words = 0;
+  std::vector<uint32_t> arow;  // [occ][words]
+  std::vector<uint32_t> erow;  // [qubit][words]
+};
+
+void pauli_bits(int kind, uint32_t& x, uint32_t& z) {
+  x = kind == P_RX || kind == P_RY;
+  z = kind == P_RY || kind == P_RZ;
+}
+
+Frame frame_rows(const Plan& p) {
+  Frame f;
+  const int nocc = (int)p.occ_src.size();
+  f.words = (nocc + 31) / 32;
+  const int W = f.words;
+  f.arow.assign((size_t)nocc * W, 0u);
+  f.erow.assign((size_t)p.n * W, 0u);
+  for (size_t i = 0; i < p.prims.size(); ++i) {
+    const Prim& src = p.prims[i];
+    if (src.occ < 0) continue;
+    const int k = src.occ;
+    uint32_t px, pz;
+    pauli_bits(src.kind, px, pz);
+    uint32_t x = px << src.q0, z = pz << src.q0;
+    for (size_t j = i + 1; j < p.prims.size(); ++j) {
+      const Prim& g = p.prims[j];
+      if (g.kind == P_CNOT) {  // X_c -> X_c X_t, Z_t -> Z_c Z_t
+        const uint32_t xc = (x >> g.q0) & 1u, zt = (z >> g.q1) & 1u;
+        x ^= xc << g.q1;
+        z ^= zt << g.q0;
+      } else if (g.kind == P_CZ) {  // X_a -> X_a Z_b
+        const uint32_t xa = (x >> g.q0) & 1u, xb = (x >> g.q1) & 1u;
+        z ^= (xa << g.q1) | (xb << g.q0);
+      } else {
+        uint32_t gx, gz;
+        pauli_bits(g.kind, gx, gz);
+        const uint32_t anti = (((x >> g.q0) & 1u) & gz) ^ (((z >> g.q0) & 1u) & gx);
+        if (anti) f.arow[(size_t)g.occ * W + (k >> 5)] |= 1u << (k & 31);
+      }
+    }
+    for (int q = 0; q < p.n; ++q)
+      if ((x >> q) & 1u) f.erow[(size_t)q * W + (k >> 5)] |= 1u << (k & 31);
+  }
+  return f;
+}
+
+std::vector<int> stream_rotations(const uint32_t* ins, int n_ins) {
+  std::vector<int> occ;
+  for (int pc = 0; pc < n_ins; ++pc) {
+    const int op = ins[2 * pc] & 31;
+    if (op == OP_RX || op == OP_RY || op == OP_RZ) occ.push_back((int)ins[2 * pc + 1]);
+  }
+  return occ;
+}
+
+int n_blocks(size_t rotations) { return (int)((rotations + kBlock - 1) / kBlock); }
+
+// Tables of one kernel, in LDS after the kernel's own layout.
+struct TanMode {
+  bool on = false;
+  int W = 0;
+  std::vector<int> focc, bocc;  // rotations of the forward / adjoint stream, in stream order
+  bool esign = false;
+  size_t off_bits = 0, off_gm = 0, off_es = 0, off_fs = 0, off_bs = 0, end = 0;
+};
+
+size_t align16(size_t v) { return (v + 15) / 16 * 16; }
+
+TanMode tan_mode(const Plan& p, const uint32_t* fins, int fn, const uint32_t* bins, int bn, int S,
+                 bool esign, size_t base) {
+  TanMode t;
+  const int nocc = (int)p.occ_src.size();
+  t.W = std::max(1, (nocc + 31) / 32);
+  if (fins) t.focc = stream_rotations(fins, fn);
+  if (bins) t.bocc = stream_rotations(bins, bn);
+  t.esign = esign;
+  size_t off = align16(base);
+  t.off_bits = off;
+  off = align16(off + (size_t)(t.W + 1) * 4);  // + 1: the ballot writes word pairs
+  t.off_gm = off;
+  if (bins) off = align16(off + (size_t)nocc * 4);
+  t.off_es = off;
+  if (esign) off = align16(off + (size_t)p.n * 4);
+  t.off_fs = off;
+  off = align16(off + (size_t)n_blocks(t.focc.size()) * 4);
+  t.off_bs = off;
+  off = align16(off + (size_t)n_blocks(t.bocc.size()) * 4);
+  t.end = off;
+  t.on = S == 1 && t.end <= (size_t)kLdsBytes;
+  return t;
+}
+
+template <typename T>
+void emit_array(std::ostringstream& o, const char* type, const char* name, const std::vector<T>& v) {
+  o << "  static constexpr " << type << " " << name << "[] = {";
+  if (v.empty()) o << "0";
+  for (size_t i = 0; i < v.size(); ++i) o << (i ? "," : "") << (uint64_t)v[i];
+  o << "};\n";
+}
+
+// prepare(): (cos, sin)(theta/2) -> (t, cos phi') in place with the parity bits
+// (one ballot per 64 occurrences), then in one round over the streams'
+// rotations: the frame sign of each (t negated in place, once), the adjoint's
+// gradient factor (sign x square of the block's factors before it) and the
+// block factors; and the <Z> signs.  esigns(): those signs.
+void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const Frame& fr) {
+  const int nocc = (int)p.occ_src.size(), W = t.W;
+  o << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt) {\n";
+  if (!t.on) {
+    o << "  (void)w; (void)tid; (void)nt;\n}\n"
+      << "__device__ __forceinline__ static const float* esigns(const Walk&) { return nullptr; }\n";
+    return;
+  }
+  o << "  float2* tab = const_cast<float2*>(w.tab);\n"
+    << "  float* tx = reinterpret_cast<float*>(tab);  // tab[k].x = tx[2 k]\n"
+    << "  uint32_t* bits = reinterpret_cast<uint32_t*>(w.smem + " << t.off_bits << "u);\n"
+    << "  for (int i0 = 0; i0 < " << nocc << "; i0 += nt) {\n"
+    << "    const int i = i0 + tid;\n"
+    << "    bool odd = false;\n"
+    << "    if (i < " << nocc << ") {\n"
+    << "      const float2 cs = tab[i];\n"
+    << "      odd = fabsf(cs.y) > fabsf(cs.x);\n"
+    << "      tab[i] = make_float2(odd ? -cs.x / cs.y : cs.y / cs.x, odd ? fabsf(cs.y) : fabsf(cs.x));\n"
+    << "    }\n"
+    << "    const uint64_t m = __ballot(odd);\n"
+    << "    if ((tid & 63) == 0 && i < " << nocc << ") {\n"
+    << "      bits[i >> 5] = (uint32_t)m;\n"
+    << "      bits[(i >> 5) + 1] = (uint32_t)(m >> 32);\n"
+    << "    }\n"
+    << "  }\n"
+    << "  __syncthreads();\n";
+  // instances: the forward stream's rotations, then the adjoint's
+  std::vector<int> inst = t.focc;
+  inst.insert(inst.end(), t.bocc.begin(), t.bocc.end());
+  std::vector<uint32_t> rows;
+  for (int k : inst)
+    for (int j = 0; j < W; ++j) rows.push_back(j < fr.words ? fr.arow[(size_t)k * fr.words + j] : 0u);
+  const int nf = (int)t.focc.size(), ni = (int)inst.size();
+  emit_array(o, "uint16_t", "kOcc", inst);
+  emit_array(o, "uint32_t", "kArow", rows);
+  o << "  float* gm = reinterpret_cast<float*>(w.smem + " << t.off_gm << "u);\n"
+    << "  float* fs = reinterpret_cast<float*>(w.smem + " << t.off_fs << "u);\n"
+    << "  float* bs = reinterpret_cast<float*>(w.smem + " << t.off_bs << "u);\n"
+    << "  (void)gm; (void)fs; (void)bs;\n"
+    << "  for (int i = tid; i < " << ni << "; i += nt) {\n"
+    << "    const bool f = i < " << nf << ";\n"
+    << "    const int m = f ? i : i - " << nf << ", base = f ? 0 : " << nf << ";\n"
+    << "    const int k = kOcc[i], b0 = m - m % " << kBlock << ";\n"
+    << "    uint32_t par = 0u;\n"
+    << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & kArow[i * " << W
+    << " + j]);\n"
+    << "    float pr = 1.f;\n"
+    << "#pragma unroll 8\n"
+    << "    for (int j = b0; j < m; ++j) pr *= tab[kOcc[base + j]].y;\n"
+    << "    const bool last = m % " << kBlock << " == " << kBlock - 1 << " || m == (f ? "
+    << nf << " : " << ni - nf << ") - 1;\n"
+    << "    if (f) {\n"
+    << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n"
+    << "      if (last) fs[m / " << kBlock << "] = pr * tab[k].y;\n"
+    << "    } else {\n";
+  if (nf == 0)  // a lone adjoint stream applies the signs itself
+    o << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n";
+  o << "      gm[k] = (par & 1u) ? -pr * pr : pr * pr;\n"
+    << "      if (last) bs[m / " << kBlock << "] = pr * tab[k].y;\n"
+    << "    }\n"
+    << "  }\n";
+  if (t.esign) {
+    std::vector<uint32_t> erows;
+    for (int q = 0; q < p.n; ++q)
+      for (int j = 0; j < W; ++j) erows.push_back(j < fr.words ? fr.erow[(size_t)q * fr.words + j] : 0u);
+    emit_array(o, "uint32_t", "kErow", erows);
+    o << "  for (int q = tid; q < " << p.n << "; q += nt) {\n"
+      << "    uint32_t par = 0u;\n"
+      << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & kErow[q * "
+      << W << " + j]);\n"
+      << "    reinterpret_cast<float*>(w.smem + " << t.off_es << "u)[q] = (par & 1u) ? -1.f : 1.f;\n"
+      << "  }\n";
+  }
+  o << "  __syncthreads();\n}\n";
+  if (t.esign)
+    o << "__device__ __forceinline__ static const float* esigns(const Walk& w) {\n"
+      << "  return reinterpret_cast<const float*>(w.smem + " << t.off_es << "u);\n}\n";
+  else
+    o << "__device__ __forceinline__ static const float* esigns(const Walk&) { return nullptr; }\n";
+}
+
+// Statements of one instruction stream for register width R.  With tangent
+// tables (tm.on) rotations use the tangent form and blocks are rescaled.
 void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, int n_ins, bool bwd,
-                   int R, int k, int S, const GradMode& gm) {
+                   int R, int k, int S, const GradMode& gm, const TanMode& tm) {
   const int t = k - R;
+  const bool tan = tm.on;
+  const int nrot = (int)(bwd ? tm.bocc.size() : tm.focc.size());
+  int m = 0;  // rotation index in the stream
+  if (tan && bwd)
+    o << "  const float* gmul = reinterpret_cast<const float*>(w.smem + " << tm.off_gm << "u);\n";
+  if (tan)
+    o << "  const float* bscale = reinterpret_cast<const float*>(w.smem + "
+      << (bwd ? tm.off_bs : tm.off_fs) << "u);\n";
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
     const int op = w0 & 31, pa = (w0 >> 5) & 31, pb = (w0 >> 10) & 31;
@@ -107,21 +320,40 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         break;
       }
       default: {
-        o << "  { const float2 cs = w.tab[" << arg << " * " << S << " + w.sl]; ";
         const bool reg = pa < R;
         const char* kind = op == OP_RX ? "rx" : op == OP_RY ? "ry" : "rz";
-        if (!bwd) {
-          if (reg)
-            o << kind << "_reg<R, " << pa << ">(a, cs.x, cs.y);";
-          else  // RZ on a thread / tile bit
-            o << "phase_all<R>(a, cs.x, flip_sign(cs.y, (tile_bit<R>(w, " << pa
-              << ") ^ 1u) << 31));";
+        const std::string at = std::to_string(arg) + " * " + std::to_string(S) + " + w.sl";
+        if (tan) {
+          o << "  { const float t = w.tab[" << arg << "].x; ";
+          if (!bwd) {
+            if (reg)
+              o << kind << "_t<R, " << pa << ">(a, t);";
+            else
+              o << "phase_t<R>(a, flip_sign(t, tile_bit<R>(w, " << pa << ") << 31));";
+          } else {
+            if (reg)
+              o << "float g = adj_" << kind << "_t<R, " << pa << ">(a, l, t);";
+            else
+              o << "float g = adj_phase_t<R>(a, l, t, tile_bit<R>(w, " << pa << "));";
+            o << " g *= gmul[" << arg << "];";
+          }
         } else {
-          if (reg)
-            o << "const float g = adj_" << kind << "<R, " << pa << ">(a, l, cs.x, cs.y);";
-          else
-            o << "const float g = adj_rz_uniform<R>(a, l, cs.x, cs.y, tile_bit<R>(w, " << pa
-              << "));";
+          o << "  { const float2 cs = w.tab[" << at << "]; ";
+          if (!bwd) {
+            if (reg)
+              o << kind << "_reg<R, " << pa << ">(a, cs.x, cs.y);";
+            else  // RZ on a thread / tile bit
+              o << "phase_all<R>(a, cs.x, flip_sign(cs.y, (tile_bit<R>(w, " << pa
+                << ") ^ 1u) << 31));";
+          } else {
+            if (reg)
+              o << "const float g = adj_" << kind << "<R, " << pa << ">(a, l, cs.x, cs.y);";
+            else
+              o << "const float g = adj_rz_uniform<R>(a, l, cs.x, cs.y, tile_bit<R>(w, " << pa
+                << "));";
+          }
+        }
+        if (bwd) {
           if (slot < 0)
             o << " (void)g;";
           else if (gm.regs)
@@ -134,15 +366,23 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
             o << " { const float gs = group_sum<" << gm.tm << ">(g); if (w.leader) atomicAdd(&w.acc["
               << slot << " * w.G + w.grp], gs); }";
         }
+        if (tan && (m % kBlock == kBlock - 1 || m == nrot - 1)) {
+          o << " { const float f = bscale[" << m / kBlock << "]; rescale<R>(a, f);";
+          if (bwd) o << " rescale<R>(l, f);";
+          o << " }";
+        }
+        ++m;
         o << " gate_boundary(w); }\n";
       }
     }
   }
 }
 
+// A schedule struct: run() for one stream, the group sum used for <Z>, and
+// (when `tables`) the kernel's tangent-form tables.
 void emit_sched_struct(std::ostringstream& o, const std::string& name, const Plan& p,
                        const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S,
-                       const GradMode& gm) {
+                       const GradMode& gm, const TanMode& tm, const Frame* tables) {
   o << "struct " << name << " {\n"
     << "template <int R, bool BWD, bool WIDE>\n"
     << "__device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w, "
@@ -153,31 +393,41 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
     o << "  const uint32_t ln = (uint32_t)w.stid & " << gm.tm - 1 << "u;\n"
       << "  float ga[" << gm.nr << "];\n"
       << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) ga[j] = 0.f;\n";
-  emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm);
+  emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm, tm);
   if (regs)  // every (slot, group) accumulator is written by exactly one lane
     o << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) {\n"
       << "    const uint32_t slot = j * " << gm.tm << "u + ln;\n"
       << "    if (slot < " << gm.ns << "u) w.acc[slot * w.G + w.grp] = ga[j];\n  }\n";
   o << "}\n"
     << "__device__ __forceinline__ static float lane_sum(float v, const Walk&) {\n"
-    << "  return group_sum<" << gm.tm << ">(v);\n}\n};\n";
+    << "  return group_sum<" << gm.tm << ">(v);\n}\n";
+  if (tables) emit_tables(o, p, tm, *tables);
+  o << "};\n";
 }
 
 size_t lds_size(size_t b) { return b < 16 ? 16 : b; }
 
+// Whether a kernel uses the tangent form: one sample per workgroup, and enough
+// work per launch that the tables' set-up latency pays off (the 4-amplitude
+// kernels of small states are latency-bound and keep the (cos, sin) form).
+bool tangent_wanted(int S, int R) { return S == 1 && R >= 3; }
+
 // One kernel in a program of its own, so that the kernels of a circuit compile
-// in parallel.
-std::string kernel_unit(const Plan& p, const std::string& name, const uint32_t* ins, int n_ins,
-                        bool bwd, bool stream, int R, int S, int threads, size_t lds,
-                        int n_slots) {
+// in parallel.  esign: the kernel computes <Z> (forward) or forms lambda
+// (adjoint).
+std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
+                        const uint32_t* ins, int n_ins, bool bwd, bool stream, int R, int S,
+                        int threads, size_t lds, int n_slots, bool esign) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
   const int lanes = stream ? threads : 1 << (p.k - R);
-  emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots));
+  TanMode tm = tan_mode(p, bwd ? nullptr : ins, n_ins, bwd ? ins : nullptr, n_ins, S, esign, lds);
+  tm.on = tm.on && tangent_wanted(S, R);
+  emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << name
     << (stream ? "(const vqc::PassArgs A) {\n" : "(const vqc::TileArgs A) {\n")
-    << "  __shared__ __align__(16) unsigned char smem[" << lds_size(lds) << "];\n";
+    << "  __shared__ __align__(16) unsigned char smem[" << lds_size(tm.on ? tm.end : lds) << "];\n";
   if (stream)
     o << "  vqc::stream_body<" << (bwd ? "true" : "false") << ", " << R
       << ", vqc::Sched>(A, smem);\n}\n";
@@ -187,45 +437,52 @@ std::string kernel_unit(const Plan& p, const std::string& name, const uint32_t* 
   return o.str();
 }
 
-}  // namespace
-
 // The training step: forward and adjoint sweeps in one kernel.
-std::string step_unit(const Plan& p) {
+std::string step_unit(const Plan& p, const Frame& fr) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
   const int lanes = 1 << (p.k - p.R);
   const GradMode gm = grad_mode(lanes, p.P + p.F);
-  emit_sched_struct(o, "SchedF", p, p.fwd.data(), (int)p.fwd.size() / 2, false, p.R, p.k, p.S, gm);
-  emit_sched_struct(o, "SchedB", p, p.bwd.data(), (int)p.bwd.size() / 2, true, p.R, p.k, p.S, gm);
+  const int nf = (int)p.fwd.size() / 2, nb = (int)p.bwd.size() / 2;
+  TanMode tm = tan_mode(p, p.fwd.data(), nf, p.bwd.data(), nb, p.S, true, p.lds_step);
+  tm.on = tm.on && tangent_wanted(p.S, p.R);
+  emit_sched_struct(o, "SchedF", p, p.fwd.data(), nf, false, p.R, p.k, p.S, gm, tm, &fr);
+  emit_sched_struct(o, "SchedB", p, p.bwd.data(), nb, true, p.R, p.k, p.S, gm, tm, nullptr);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << p.WG << ") vqc_rs(const vqc::TileArgs A) {\n"
-    << "  __shared__ __align__(16) unsigned char smem[" << lds_size(p.lds_step) << "];\n"
+    << "  __shared__ __align__(16) unsigned char smem["
+    << lds_size(tm.on ? tm.end : p.lds_step) << "];\n"
     << "  vqc::resident_step_body<" << p.WG << ", " << p.R
     << ", vqc::SchedF, vqc::SchedB>(A, smem);\n}\n";
   return o.str();
 }
 
+}  // namespace
+
 std::vector<JitUnit> jit_units(const Plan& p) {
   std::vector<JitUnit> u;
+  const Frame fr = frame_rows(p);
   if (p.path == VQC_PATH_RESIDENT) {
-    u.push_back({"vqc_rf", kernel_unit(p, "vqc_rf", p.fwd.data(), (int)p.fwd.size() / 2, false,
-                                       false, p.R, p.S, p.WG, p.lds_fwd, p.P + p.F)});
-    u.push_back({"vqc_rb", kernel_unit(p, "vqc_rb", p.bwd.data(), (int)p.bwd.size() / 2, true,
-                                       false, p.R, p.S, p.WG, p.lds_bwd, p.P + p.F)});
-    u.push_back({"vqc_rs", step_unit(p)});
+    u.push_back({"vqc_rf", kernel_unit(p, fr, "vqc_rf", p.fwd.data(), (int)p.fwd.size() / 2,
+                                       false, false, p.R, p.S, p.WG, p.lds_fwd, p.P + p.F, true)});
+    u.push_back({"vqc_rb", kernel_unit(p, fr, "vqc_rb", p.bwd.data(), (int)p.bwd.size() / 2,
+                                       true, false, p.R, p.S, p.WG, p.lds_bwd, p.P + p.F, true)});
+    u.push_back({"vqc_rs", step_unit(p, fr)});
     return u;
   }
   for (size_t i = 0; i < p.fpass.size(); ++i) {
     const std::string name = "vqc_sf" + std::to_string(i);
-    u.push_back({name, kernel_unit(p, name, p.fwd.data() + 2 * p.fpass[i].ins_off,
-                                   p.fpass[i].n_ins, false, true, p.Rf, 1, 1 << (p.k - p.Rf),
-                                   p.lds_fwd, p.fpass[i].n_slots)});
+    const PassPlan& pp = p.fpass[i];
+    u.push_back({name, kernel_unit(p, fr, name, p.fwd.data() + 2 * pp.ins_off, pp.n_ins, false,
+                                   true, p.Rf, 1, 1 << (p.k - p.Rf), p.lds_fwd, pp.n_slots,
+                                   (pp.flags & PF_ZPART) != 0)});
   }
   for (size_t i = 0; i < p.bpass.size(); ++i) {
     const std::string name = "vqc_sb" + std::to_string(i);
-    u.push_back({name, kernel_unit(p, name, p.bwd.data() + 2 * p.bpass[i].ins_off,
-                                   p.bpass[i].n_ins, true, true, p.Rb, 1, 1 << (p.k - p.Rb),
-                                   p.lds_bwd, p.bpass[i].n_slots)});
+    const PassPlan& pp = p.bpass[i];
+    u.push_back({name, kernel_unit(p, fr, name, p.bwd.data() + 2 * pp.ins_off, pp.n_ins, true,
+                                   true, p.Rb, 1, 1 << (p.k - p.Rb), p.lds_bwd, pp.n_slots,
+                                   (pp.flags & PF_MAKE_LAMBDA) != 0)});
   }
   return u;
 }

@@ -328,6 +328,157 @@ __device__ __forceinline__ float adj_rz_uniform(St<R>& a, St<R>& l, float c, flo
   return one ? -acc : acc;
 }
 
+// ------------------------------------------------ tangent form (generated kernels)
+// R_P(theta) is written as R_P(2 phi') P^m (up to a global phase) with
+// phi' = theta/2 - m pi/2 in [-pi/4, pi/4], and R_P(2 phi') = cos(phi') (I - i t P)
+// with t = tan(phi').  The generated kernels apply only I - i t P, one FMA per
+// real component, keep the per-sample factors cos(phi') aside (applied in blocks
+// by rescale) and carry the Paulis P^m as a frame that only flips signs of t,
+// of <Z_q> and of gradients (tables built per sample before the schedule).
+
+// (I - i t X) on the pair (u, u + 2^P)
+template <int R, int P>
+__device__ __forceinline__ void rx_t(St<R>& a, float t) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
+    a.r[u] = fmaf(t, yi, xr);
+    a.i[u] = fmaf(-t, yr, xi);
+    a.r[v] = fmaf(t, xi, yr);
+    a.i[v] = fmaf(-t, xr, yi);
+  }
+}
+
+// (I - i t Y) = [1, -t; t, 1]
+template <int R, int P>
+__device__ __forceinline__ void ry_t(St<R>& a, float t) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float xr = a.r[u], xi = a.i[u], yr = a.r[v], yi = a.i[v];
+    a.r[u] = fmaf(-t, yr, xr);
+    a.i[u] = fmaf(-t, yi, xi);
+    a.r[v] = fmaf(t, xr, yr);
+    a.i[v] = fmaf(t, xi, yi);
+  }
+}
+
+// (I - i t Z) on register bit P: amplitude times (1 - i t z), z = +-1
+template <int R, int P>
+__device__ __forceinline__ void rz_t(St<R>& a, float t) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float tz = (u & (1 << P)) ? -t : t;
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = fmaf(tz, xi, xr);
+    a.i[u] = fmaf(-tz, xr, xi);
+  }
+}
+
+// every amplitude times (1 - i tz) (RZ on a thread / tile bit, tz = t z)
+template <int R>
+__device__ __forceinline__ void phase_t(St<R>& a, float tz) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float xr = a.r[u], xi = a.i[u];
+    a.r[u] = fmaf(tz, xi, xr);
+    a.i[u] = fmaf(-tz, xr, xi);
+  }
+}
+
+template <int R>
+__device__ __forceinline__ void rescale(St<R>& a, float f) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    a.r[u] *= f;
+    a.i[u] *= f;
+  }
+}
+
+// Adjoint steps: Im<l| P |a> at the gate's output, then (I + i t P) on both.
+template <int R, int P>
+__device__ __forceinline__ float adj_rx_t(St<R>& a, St<R>& l, float t) {
+  float acc = 0.f;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
+    const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
+    acc += lr * bi - li * br;
+    acc += mr * ai - mi * ar;
+    a.r[u] = fmaf(-t, bi, ar);
+    a.i[u] = fmaf(t, br, ai);
+    a.r[v] = fmaf(-t, ai, br);
+    a.i[v] = fmaf(t, ar, bi);
+    l.r[u] = fmaf(-t, mi, lr);
+    l.i[u] = fmaf(t, mr, li);
+    l.r[v] = fmaf(-t, li, mr);
+    l.i[v] = fmaf(t, lr, mi);
+  }
+  return acc;
+}
+
+template <int R, int P>
+__device__ __forceinline__ float adj_ry_t(St<R>& a, St<R>& l, float t) {
+  float acc = 0.f;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (u & (1 << P)) continue;
+    const int v = u | (1 << P);
+    const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
+    const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
+    acc -= lr * br + li * bi;
+    acc += mr * ar + mi * ai;
+    a.r[u] = fmaf(t, br, ar);
+    a.i[u] = fmaf(t, bi, ai);
+    a.r[v] = fmaf(-t, ar, br);
+    a.i[v] = fmaf(-t, ai, bi);
+    l.r[u] = fmaf(t, mr, lr);
+    l.i[u] = fmaf(t, mi, li);
+    l.r[v] = fmaf(-t, lr, mr);
+    l.i[v] = fmaf(-t, li, mi);
+  }
+  return acc;
+}
+
+template <int R, int P>
+__device__ __forceinline__ float adj_rz_t(St<R>& a, St<R>& l, float t) {
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
+    const float v = lr * ai - li * ar;
+    if (u & (1 << P)) a1 += v; else a0 += v;
+    const float tz = (u & (1 << P)) ? t : -t;  // the inverse: (1 + i t z)
+    a.r[u] = fmaf(tz, ai, ar);
+    a.i[u] = fmaf(-tz, ar, ai);
+    l.r[u] = fmaf(tz, li, lr);
+    l.i[u] = fmaf(-tz, lr, li);
+  }
+  return a0 - a1;
+}
+
+// RZ on a thread / tile bit of value `one`: uniform z
+template <int R>
+__device__ __forceinline__ float adj_phase_t(St<R>& a, St<R>& l, float t, uint32_t one) {
+  float acc = 0.f;
+  const float tz = one ? t : -t;  // the inverse phase (1 + i t z)
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
+    acc += lr * ai - li * ar;
+    a.r[u] = fmaf(tz, ai, ar);
+    a.i[u] = fmaf(-tz, ar, ai);
+    l.r[u] = fmaf(tz, li, lr);
+    l.i[u] = fmaf(-tz, lr, li);
+  }
+  return one ? -acc : acc;
+}
+
 template <int R>
 __device__ __forceinline__ float adjoint_rotation(int op, St<R>& a, St<R>& l, int p, float c,
                                                   float s, uint32_t tb) {
@@ -491,6 +642,7 @@ struct Walk {
   uint32_t tb;        // tile bits above the register bits
   bool leader;
   bool never;         // false, but not provably so (see gate_boundary)
+  unsigned char* smem;  // the workgroup's LDS (tables of the generated kernels)
 };
 
 // Ends the current basic block with a uniform branch that is never taken.  The
@@ -587,13 +739,14 @@ __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64
 // lambda = H psi with H = sum_q g_q Z_q, the Z signs read from the mapping
 template <int R>
 __device__ __forceinline__ void make_lambda(St<R>& l, const St<R>& a, const float* g, int n,
-                                            const uint8_t* phys, uint32_t tb, bool valid) {
+                                            const uint8_t* phys, uint32_t tb, bool valid,
+                                            const float* esign = nullptr) {
   float gt = 0.f, gr[R];
 #pragma unroll
   for (int b = 0; b < R; ++b) gr[b] = 0.f;
   if (valid) {
     for (int q = 0; q < n; ++q) {
-      const float gq = g[q];
+      const float gq = esign ? g[q] * esign[q] : g[q];
       const int p = phys[q];
       if (p >= R) gt += ((tb >> (p - R)) & 1u) ? -gq : gq;
 #pragma unroll
@@ -635,6 +788,7 @@ __device__ __forceinline__ void z_partials(const St<R>& a, float* ez, int n, con
     for (int b = 0; b < R; ++b)
       if (p == b) v = sr[b];
     v = Sched::lane_sum(v, w);
+    if (const float* es = Sched::esigns(w)) v *= es[q];
     if (w.leader) ez[q * w.G + w.grp] = v;
   }
   __syncthreads();
@@ -651,6 +805,10 @@ struct InterpSched {
   __device__ __forceinline__ static float lane_sum(float v, const Walk& w) {
     return seg_sum(v, w.width);
   }
+  // per-sample tables built before the schedule (none here)
+  __device__ __forceinline__ static void prepare(const Walk&, int, int) {}
+  // signs of <Z_q> of the thread's sample (none: the state is the true state)
+  __device__ __forceinline__ static const float* esigns(const Walk&) { return nullptr; }
 };
 
 // Cotangent g_j = dL/dE_j of one sample's row e[0..n) for the loss heads of the
@@ -692,6 +850,7 @@ __device__ __forceinline__ Walk resident_walk(const TileArgs& A, unsigned char* 
   w.grp = T < 64 ? w.sl : (tid >> 6);
   w.leader = (tid & (w.width - 1)) == 0;
   w.never = A.B < 0;
+  w.smem = smem;
   w.tb = (uint32_t)w.stid;
   return w;
 }
@@ -766,6 +925,7 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
   if (BWD)
     for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
+  Sched::prepare(w, tid, WG);
 
   St<R> a, l;
   if (!BWD) {
@@ -777,7 +937,8 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
     for (int j = 0; j < NA; ++j) v[j] = ws[((size_t)blockIdx.x * NA + j) * WG + tid];
 #pragma unroll
     for (int j = 0; j < NA; ++j) split(v[j], a.r[j], a.i[j]);
-    make_lambda<R>(l, a, A.grad_out + (valid ? b : 0) * A.n, A.n, A.end_phys, w.tb, valid);
+    make_lambda<R>(l, a, A.grad_out + (valid ? b : 0) * A.n, A.n, A.end_phys, w.tb, valid,
+                   Sched::esigns(w));
   }
 
   Sched::template run<R, BWD, (WG > 64)>(a, l, w, A.ins, A.n_ins);
@@ -813,6 +974,7 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
               A.occ_idx, A.occ_cs, A.params, A.P, A.inputs, A.F, tid, WG);
   for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
+  FS::prepare(w, tid, WG);  // the tables of both sweeps
 
   St<R> a, l;
   zero_state<R>(a, w.stid);
@@ -830,7 +992,7 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
     if (A.cot_out && bb < A.B) A.cot_out[bb * A.n + q] = v;
   }
   __syncthreads();
-  make_lambda<R>(l, a, g + w.sl * A.n, A.n, A.end_phys, w.tb, valid);
+  make_lambda<R>(l, a, g + w.sl * A.n, A.n, A.end_phys, w.tb, valid, FS::esigns(w));
   BS::template run<R, true, (WG > 64)>(a, l, w, A.ins_b, A.n_ins_b);
   __syncthreads();
   resident_grads(A, w.acc, WG);
@@ -899,6 +1061,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.grp = tid >> 6;
   w.leader = (tid & 63) == 0;
   w.never = A.B < 0;
+  w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
   angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.P, A.inputs,
@@ -906,6 +1069,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   if (BWD)
     for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
   __syncthreads();
+  Sched::prepare(w, tid, WG);
 
   uint32_t base, off[NA];
   io_offsets<R>(A.io, A.k, A.ng, tid, g, base, off);
@@ -924,7 +1088,8 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   }
   if (BWD) {
     if (A.flags & PF_MAKE_LAMBDA) {
-      make_lambda<R>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, w.tb, true);
+      make_lambda<R>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, w.tb, true,
+                     Sched::esigns(w));
     } else {
       const float2* src = reinterpret_cast<const float2*>(A.lam_src) + sbase;
       load_tile<R>(l, src, base, off);
