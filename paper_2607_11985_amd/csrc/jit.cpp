@@ -306,17 +306,50 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         break;
       }
       case OP_CZ: {
-        const int lo = pa < pb ? pa : pb, hi = pa < pb ? pb : pa;
+        // A run of consecutive CZs is one diagonal of signs: amplitude u of the
+        // thread is negated when c[u] ^ t0 ^ (XOR of m[r] over the register bits
+        // r set in u) is 1.  c: the register/register pairs (compile time); m[r]:
+        // the thread / tile bits paired with register bit r; t0: the products
+        // of the thread / tile pairs.  One sign flip per value instead of one
+        // per gate.
+        int end = pc;
+        while (end < n_ins && (ins[2 * end] & 31) == OP_CZ) ++end;
+        const int N = 1 << R;
+        std::vector<int> cu(N, 0);
+        std::vector<std::string> mr(R);
+        std::string t0;
+        for (int q = pc; q < end; ++q) {
+          const int x = (ins[2 * q] >> 5) & 31, y = (ins[2 * q] >> 10) & 31;
+          const int lo = x < y ? x : y, hi = x < y ? y : x;
+          if (hi < R) {
+            for (int u = 0; u < N; ++u) cu[u] ^= (u >> lo) & (u >> hi) & 1;
+          } else if (lo < R) {
+            mr[lo] += (mr[lo].empty() ? "" : " ^ ") + std::string("(tb >> ") +
+                      std::to_string(hi - R) + ")";
+          } else {
+            t0 += (t0.empty() ? "" : " ^ ") + std::string("((tb >> ") + std::to_string(lo - R) +
+                  ") & (tb >> " + std::to_string(hi - R) + "))";
+          }
+        }
+        o << "  { const uint32_t tb = opaque(w.tb); (void)tb;\n"
+          << "    const uint32_t s0 = " << (t0.empty() ? "0u" : "(" + t0 + ") & 1u") << ";\n";
+        for (int r = 0; r < R; ++r)
+          o << "    const uint32_t m" << r << " = "
+            << (mr[r].empty() ? "0u" : "(" + mr[r] + ") & 1u") << ";\n";
+        for (int u = 1; u < N; ++u) {
+          int low = 0;
+          while (!((u >> low) & 1)) ++low;
+          o << "    const uint32_t s" << u << " = s" << (u & (u - 1)) << " ^ m" << low << ";\n";
+        }
         for (const char* st : {"a", "l"}) {
           if (st[0] == 'l' && !bwd) break;
-          if (hi < R)
-            o << "  cz_rr<R, " << lo << ", " << hi << ">(" << st << ");\n";
-          else if (lo < R)
-            o << "  cz_tr<R, " << lo << ">(" << st << ", tile_bit<R>(w, " << hi << "));\n";
-          else
-            o << "  negate_if<R>(" << st << ", tile_bit<R>(w, " << lo << ") & tile_bit<R>(w, "
-              << hi << "));\n";
+          for (int u = 0; u < N; ++u)
+            o << "    " << st << ".r[" << u << "] = flip_sign(" << st << ".r[" << u << "], (s" << u
+              << " ^ " << cu[u] << "u) << 31); " << st << ".i[" << u << "] = flip_sign(" << st
+              << ".i[" << u << "], (s" << u << " ^ " << cu[u] << "u) << 31);\n";
         }
+        o << "  }\n";
+        pc = end - 1;
         break;
       }
       default: {
