@@ -98,7 +98,12 @@ typedef struct {
                             2, 3 or 4 (default 4); streaming path 4 or 5 for both
                             sweeps (default: forward 4, adjoint 5); 0 = default */
     int32_t engine;      /* VQC_ENGINE_* */
-    int32_t reserved[4]; /* must be zero */
+    int32_t shared_params; /* 1: one parameter vector for the whole batch
+                              (Algorithm 1's shared theta): params is [P] in
+                              every call and dparams is [P], the sum over the
+                              samples.  Inputs stay per sample.  0: per-sample
+                              rows [B, P] */
+    int32_t reserved[3]; /* must be zero */
 } vqc_compile_opts;
 
 /*
@@ -135,7 +140,7 @@ size_t vqc_workspace_bytes(const vqc_circuit *c, int64_t batch, int32_t training
 
 /*
  * vqc_forward -- E = expectations of the circuit for `batch` samples.
- *   params   [batch, P] fp32 (may be NULL when P == 0)
+ *   params   [batch, P] fp32, or [P] with shared_params (may be NULL when P == 0)
  *   inputs   [batch, F] fp32 (may be NULL when F == 0)
  *   expvals  [batch, n] fp32, written
  *   workspace / workspace_bytes: NULL/0 for inference when
@@ -158,7 +163,8 @@ int vqc_forward(const vqc_circuit *c, int64_t batch, const float *params, const 
  *     be back-propagated from one forward.
  *   dparams [batch, P], dinputs [batch, F] fp32: written (per-sample
  *     gradients; a parameter used by several gates receives the sum).  Either
- *     may be NULL to skip it.
+ *     may be NULL to skip it.  With shared_params, dparams is [P]: the sum of
+ *     the samples' gradients, in a fixed order.
  * Errors: VQC_ERR_INVALID_ARG, VQC_ERR_WORKSPACE, VQC_ERR_HIP.
  */
 int vqc_backward(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,
@@ -189,9 +195,10 @@ int vqc_loss_grad(int32_t kind, int64_t batch, int32_t n_qubits, const float *ex
  * the resident path this is a single launch: the final state stays on chip
  * between the forward and the adjoint sweep and is never written to HBM.
  *   expvals [batch, n] written; grad_out [batch, n] receives the cotangent
- *   when not NULL; dparams [batch, P] / dinputs [batch, F] written (either
- *   may be NULL); workspace: vqc_workspace_bytes(c, batch, 2) bytes, 256-byte
- *   aligned (0 bytes / NULL on the resident path).
+ *   when not NULL; dparams [batch, P] ([P] with shared_params) / dinputs
+ *   [batch, F] written (either may be NULL); workspace:
+ *   vqc_workspace_bytes(c, batch, 2) bytes, 256-byte aligned (on the resident
+ *   path 0 bytes / NULL unless shared_params).
  * Results equal those of the three separate calls.  Errors: those of the
  * three calls.
  */
@@ -214,7 +221,8 @@ typedef struct {
     int32_t fwd_instructions, bwd_instructions;
     int32_t lds_bytes_fwd, lds_bytes_bwd;
     int32_t engine;         /* VQC_ENGINE_* */
-    int32_t reserved[7];
+    int32_t shared_params;  /* the compile option */
+    int32_t reserved[6];
 } vqc_info;
 int vqc_circuit_info(const vqc_circuit *c, vqc_info *info);
 

@@ -38,7 +38,7 @@ class vqc_op(ctypes.Structure):
 class vqc_compile_opts(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int32), ("path", ctypes.c_int32),
                 ("reg_bits", ctypes.c_int32), ("engine", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 4)]
+                ("shared_params", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
 
 
 class vqc_info(ctypes.Structure):
@@ -46,7 +46,7 @@ class vqc_info(ctypes.Structure):
         "n_qubits", "n_params", "n_inputs", "n_ops", "n_rotations", "path",
         "tile_qubits", "threads", "fwd_passes", "bwd_passes", "fwd_exchanges",
         "bwd_exchanges", "fwd_instructions", "bwd_instructions", "lds_bytes_fwd",
-        "lds_bytes_bwd", "engine")] + [("reserved", ctypes.c_int32 * 7)]
+        "lds_bytes_bwd", "engine", "shared_params")] + [("reserved", ctypes.c_int32 * 6)]
 
 
 class VQCError(RuntimeError):
@@ -127,10 +127,12 @@ def encode_ops(ops) -> ctypes.Array:
 
 
 def vqc_compile(ops, n_qubits: int, n_params: int, n_inputs: int, device: int = 0,
-                path: int = VQC_PATH_AUTO, reg_bits: int = 0, engine: int = VQC_ENGINE_JIT):
+                path: int = VQC_PATH_AUTO, reg_bits: int = 0, engine: int = VQC_ENGINE_JIT,
+                shared_params: int = 0):
     lib = load()
     arr = encode_ops(ops)
-    opts = vqc_compile_opts(device=device, path=path, reg_bits=reg_bits, engine=engine)
+    opts = vqc_compile_opts(device=device, path=path, reg_bits=reg_bits, engine=engine,
+                            shared_params=shared_params)
     h = _vp()
     _check(lib.vqc_compile(arr, len(ops), n_qubits, n_params, n_inputs, ctypes.byref(opts),
                            ctypes.byref(h)))

@@ -40,15 +40,30 @@ class Circuit:
     """A compiled static circuit (compile once, execute many: Sec. 3)."""
 
     def __init__(self, ops, n_qubits: int, n_params: int, n_inputs: int, device: int = 0,
-                 path: str = "auto", reg_bits: int = 0, engine: str = "jit"):
+                 path: str = "auto", reg_bits: int = 0, engine: str = "jit",
+                 shared_params: bool = False):
         self.ops = list(ops)
         self.n = int(n_qubits)
         self.P = int(n_params)
         self.F = int(n_inputs)
+        self.shared = bool(shared_params)
         self.device = torch.device("cuda", device)
         self.handle = _lib.vqc_compile(self.ops, self.n, self.P, self.F, device=device,
                                        path=_PATHS[path], reg_bits=reg_bits,
-                                       engine=_ENGINES[engine])
+                                       engine=_ENGINES[engine], shared_params=int(self.shared))
+
+    def _params(self, params, B):
+        """Per-sample rows [B, P], or the shared vector [P]."""
+        if not self.shared:
+            return _as_rows(params, B, self.P, self.device, "params")
+        if self.P == 0:
+            return None
+        return _as_rows(params.reshape(1, -1), 1, self.P, self.device, "params").reshape(-1)
+
+    def _batch(self, params, inputs):
+        if inputs is not None and (self.shared or params is None):
+            return int(inputs.shape[0])
+        return int(params.shape[0])
 
     def __del__(self):
         h = getattr(self, "handle", None)
@@ -68,8 +83,8 @@ class Circuit:
 
     def forward(self, params, inputs, training: bool = False, workspace=None, out=None):
         """E [B, n]; with training=True also the workspace for backward()."""
-        B = int(params.shape[0]) if params is not None else int(inputs.shape[0])
-        params = _as_rows(params, B, self.P, self.device, "params")
+        B = self._batch(params, inputs)
+        params = self._params(params, B)
         inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
         E = out if out is not None else torch.empty((B, self.n), dtype=torch.float32,
                                                    device=self.device)
@@ -87,11 +102,12 @@ class Circuit:
     def backward(self, params, inputs, grad_out, workspace, dparams=None, dinputs=None):
         """Per-sample gradients (dparams [B,P], dinputs [B,F]) of sum(grad_out * E)."""
         B = int(grad_out.shape[0])
-        params = _as_rows(params, B, self.P, self.device, "params")
+        params = self._params(params, B)
         inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
         grad_out = _as_rows(grad_out, B, self.n, self.device, "grad_out")
         if dparams is None:
-            dparams = torch.empty((B, self.P), dtype=torch.float32, device=self.device)
+            shape = (self.P,) if self.shared else (B, self.P)
+            dparams = torch.empty(shape, dtype=torch.float32, device=self.device)
         if dinputs is None:
             dinputs = torch.empty((B, self.F), dtype=torch.float32, device=self.device)
         _lib.vqc_backward(self.handle, B, _ptr(params), _ptr(inputs), grad_out.data_ptr(),
@@ -105,14 +121,15 @@ class Circuit:
         """Forward, loss cotangent and adjoint gradients in one call.
 
         Returns (E, dparams, dinputs), plus the cotangent g when want_cot."""
-        B = int(params.shape[0]) if params is not None else int(inputs.shape[0])
-        params = _as_rows(params, B, self.P, self.device, "params")
+        B = self._batch(params, inputs)
+        params = self._params(params, B)
         inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
         if y is not None:
             y = _as_rows(y.reshape(B, 1), B, 1, self.device, "y")
         E = torch.empty((B, self.n), dtype=torch.float32, device=self.device)
         g = torch.empty_like(E) if want_cot else None
-        dparams = torch.empty((B, self.P), dtype=torch.float32, device=self.device)
+        dparams = torch.empty((self.P,) if self.shared else (B, self.P), dtype=torch.float32,
+                              device=self.device)
         dinputs = torch.empty((B, self.F), dtype=torch.float32, device=self.device)
         nb = _lib.vqc_workspace_bytes(self.handle, B, 2)
         if workspace is None and nb > 0:

@@ -15,6 +15,7 @@ struct vqc_circuit {
   Plan plan;
   int device = -1;   // -1: host-only plan
   int engine = VQC_ENGINE_JIT;
+  bool shared = false;  // one parameter vector for the batch
   vqc::JitKernels jit;
   void* blob = nullptr;
   size_t off_fwd = 0, off_bwd = 0, off_cols = 0, off_src = 0, off_idx = 0, off_cs = 0,
@@ -88,13 +89,26 @@ StreamLayout stream_layout(const Plan& p, int64_t batch) {
 }
 
 // mode: 0 inference forward, 1 training forward (+ backward), 2 training step
-size_t required_bytes(const Plan& p, int64_t batch, int mode) {
+size_t required_bytes_core(const Plan& p, int64_t batch, int mode) {
   if (batch == 0) return 0;
   if (p.path == VQC_PATH_STREAM) {
     const StreamLayout L = stream_layout(p, batch);
     return mode == 0 ? L.end_inference : mode == 1 ? L.end_training : L.end_step;
   }
   return mode == 1 ? resident_state_bytes(p, batch) : 0;
+}
+
+// With shared parameters the gradient passes through per-sample rows [B, P]
+// placed after the rest of the workspace.
+size_t shared_rows_offset(const Plan& p, int64_t batch, int mode) {
+  return align_up(required_bytes_core(p, batch, mode), 256);
+}
+
+size_t required_bytes(const vqc_circuit* c, int64_t batch, int mode) {
+  const Plan& p = c->plan;
+  if (batch == 0) return 0;
+  if (!c->shared || mode == 0 || p.P == 0) return required_bytes_core(p, batch, mode);
+  return shared_rows_offset(p, batch, mode) + (size_t)batch * p.P * 4;
 }
 
 template <typename T>
@@ -117,6 +131,7 @@ vqc::TileArgs tile_args(const vqc_circuit* c, bool bwd, int64_t batch) {
   a.n_slots = p.P + p.F;
   a.P = p.P;
   a.F = p.F;
+  a.pstride = c->shared ? 0 : p.P;
   a.n = p.n;
   a.k = p.k;
   a.t = p.t;
@@ -164,6 +179,7 @@ vqc::PassArgs pass_args(const vqc_circuit* c, const vqc::PassPlan& pp, bool bwd,
   a.n_slots = p.P + p.F;
   a.P = p.P;
   a.F = p.F;
+  a.pstride = c->shared ? 0 : p.P;
   a.n = p.n;
   a.k = p.k;
   a.ng = p.ng;
@@ -264,6 +280,7 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   if (n_ops > 0 && !ops) return fail(VQC_ERR_INVALID_ARG, "ops is NULL");
   if (n_ops > (1 << 20)) return fail(VQC_ERR_TOO_LARGE, "more than 2^20 gates");
   int device = 0, path = VQC_PATH_AUTO, reg_bits = 0, engine = VQC_ENGINE_JIT;
+  bool shared = false;
   if (opts) {
     for (int r : opts->reserved)
       if (r != 0) return fail(VQC_ERR_INVALID_ARG, "reserved option fields must be zero");
@@ -273,6 +290,9 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
     engine = opts->engine;
     if (engine != VQC_ENGINE_JIT && engine != VQC_ENGINE_INTERP)
       return fail(VQC_ERR_INVALID_ARG, "unknown engine option");
+    if (opts->shared_params != 0 && opts->shared_params != 1)
+      return fail(VQC_ERR_INVALID_ARG, "shared_params must be 0 or 1");
+    shared = opts->shared_params == 1;
     if (path < VQC_PATH_AUTO || path > VQC_PATH_STREAM)
       return fail(VQC_ERR_INVALID_ARG, "unknown path option");
   } else if (hipGetDevice(&device) != hipSuccess) {
@@ -301,6 +321,7 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   }
   c->device = device;
   c->engine = engine;
+  c->shared = shared;
   if (device >= 0) {
     int count = 0;
     if (hipGetDeviceCount(&count) != hipSuccess || device >= count) {
@@ -363,7 +384,7 @@ void vqc_destroy(vqc_circuit* c) {
 
 size_t vqc_workspace_bytes(const vqc_circuit* c, int64_t batch, int32_t training) {
   if (!c || batch < 0 || training < 0 || training > 2) return (size_t)-1;
-  return required_bytes(c->plan, batch, training);
+  return required_bytes(c, batch, training);
 }
 
 int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
@@ -379,7 +400,7 @@ int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const 
     return fail(VQC_ERR_WORKSPACE, "the streaming path needs a workspace (states live in HBM)");
   if (workspace) {
     const int mode = p.path == VQC_PATH_RESIDENT ? 1 : 0;
-    if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(p, batch, mode),
+    if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(c, batch, mode),
                               mode ? "workspace smaller than vqc_workspace_bytes(c, batch, 1)"
                                    : "workspace smaller than vqc_workspace_bytes(c, batch, 0)")))
       return rc;
@@ -411,27 +432,37 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
   if ((rc = check_rows(c, params, inputs))) return rc;
   if (!grad_out) return fail(VQC_ERR_INVALID_ARG, "grad_out is NULL");
   const Plan& p = c->plan;
-  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(p, batch, 1),
+  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(c, batch, 1),
                             "backward needs the workspace of a training forward")))
     return rc;
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
   float* dp = p.P > 0 ? dparams : nullptr;
   float* dx = p.F > 0 ? dinputs : nullptr;
-  if (p.path == VQC_PATH_STREAM)
-    return stream_backward(c, batch, params, inputs, grad_out,
-                           static_cast<unsigned char*>(workspace), dp, dx, stream);
+  // shared parameters: per-sample rows first, summed over the batch after
+  float* rows = (c->shared && dp) ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
+                                                             shared_rows_offset(p, batch, 1))
+                                  : nullptr;
+  if (p.path == VQC_PATH_STREAM) {
+    rc = stream_backward(c, batch, params, inputs, grad_out,
+                         static_cast<unsigned char*>(workspace), rows ? rows : dp, dx, stream);
+    if (rc || !rows) return rc;
+    rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream);
+    return rc ? hip_fail("parameter gradient sum", rc) : VQC_OK;
+  }
   vqc::TileArgs a = tile_args(c, true, batch);
   a.params = params;
   a.inputs = inputs;
   a.ws = workspace;
   a.grad_out = grad_out;
-  a.dparams = dp;
+  a.dparams = rows ? rows : dp;
   a.dinputs = dx;
   rc = c->engine == VQC_ENGINE_JIT
            ? vqc::jit_launch(c->jit.res_bwd, resident_blocks(p, batch), p.WG, &a, sizeof(a), stream)
            : vqc::launch_resident_backward(p, a, resident_blocks(p, batch), stream);
   if (rc) return hip_fail("backward launch", rc);
+  if (rows && (rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream)))
+    return hip_fail("parameter gradient sum", rc);
   return VQC_OK;
 }
 
@@ -450,13 +481,16 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
   if ((loss_kind == VQC_LOSS_MSE_Z0 || loss_kind == VQC_LOSS_MSE_MEANZ) && !target)
     return fail(VQC_ERR_INVALID_ARG, "MSE losses need a target");
   const Plan& p = c->plan;
-  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(p, batch, 2),
+  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(c, batch, 2),
                             "workspace smaller than vqc_workspace_bytes(c, batch, 2)")))
     return rc;
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
   float* dp = p.P > 0 ? dparams : nullptr;
   float* dx = p.F > 0 ? dinputs : nullptr;
+  float* rows = (c->shared && dp) ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
+                                                             shared_rows_offset(p, batch, 2))
+                                  : nullptr;
   if (p.path == VQC_PATH_STREAM) {
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     float* cot = grad_out ? grad_out
@@ -464,7 +498,10 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
     if ((rc = stream_forward(c, batch, params, inputs, expvals, ws, stream))) return rc;
     rc = vqc::launch_loss_grad(loss_kind, batch, p.n, expvals, target, cot, stream);
     if (rc) return hip_fail("loss launch", rc);
-    return stream_backward(c, batch, params, inputs, cot, ws, dp, dx, stream);
+    rc = stream_backward(c, batch, params, inputs, cot, ws, rows ? rows : dp, dx, stream);
+    if (rc || !rows) return rc;
+    rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream);
+    return rc ? hip_fail("parameter gradient sum", rc) : VQC_OK;
   }
   vqc::TileArgs a = tile_args(c, false, batch);
   a.ins_b = at<uint32_t>(c, c->off_bwd);
@@ -475,7 +512,7 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
   a.loss = loss_kind;
   a.target = target;
   a.cot_out = grad_out;
-  a.dparams = dp;
+  a.dparams = rows ? rows : dp;
   a.dinputs = dx;
   a.lds_e = (uint32_t)p.lds_e;
   rc = c->engine == VQC_ENGINE_JIT
@@ -483,6 +520,8 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
                              stream)
            : vqc::launch_resident_step(p, a, resident_blocks(p, batch), stream);
   if (rc) return hip_fail("training step launch", rc);
+  if (rows && (rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream)))
+    return hip_fail("parameter gradient sum", rc);
   return VQC_OK;
 }
 
@@ -524,6 +563,7 @@ int vqc_circuit_info(const vqc_circuit* c, vqc_info* info) {
   info->lds_bytes_fwd = (int32_t)p.lds_fwd;
   info->lds_bytes_bwd = (int32_t)p.lds_bwd;
   info->engine = c->engine;
+  info->shared_params = c->shared ? 1 : 0;
   return VQC_OK;
 }
 

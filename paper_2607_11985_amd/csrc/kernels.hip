@@ -55,6 +55,24 @@ __global__ void reduce_grad_kernel(int64_t B, int ng, int n_slots, int P, int F,
   }
 }
 
+// One workgroup per column: thread t adds rows t, t + 256, ... in order, then a
+// fixed tree over the threads.  Deterministic for a given batch size.
+__global__ void __launch_bounds__(256) sum_rows_kernel(int64_t B, int P,
+                                                       const float* __restrict__ rows,
+                                                       float* __restrict__ out) {
+  __shared__ float part[256];
+  const int p = blockIdx.x;
+  float v = 0.f;
+  for (int64_t b = threadIdx.x; b < B; b += 256) v += rows[b * P + p];
+  part[threadIdx.x] = v;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[p] = part[0];
+}
+
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) p[i] = 0.f;
@@ -185,6 +203,13 @@ int launch_reduce_grad(int64_t batch, int ng, int n_slots, int P, int F, const f
   if (batch * n_slots == 0) return 0;
   hipLaunchKernelGGL(reduce_grad_kernel, dim3(grid_1d(batch * n_slots, 256)), dim3(256), 0,
                      (hipStream_t)stream, batch, ng, n_slots, P, F, gpart, dparams, dinputs);
+  return (int)hipGetLastError();
+}
+
+int launch_sum_rows(int64_t batch, int P, const float* rows, float* out, void* stream) {
+  if (P == 0) return 0;
+  hipLaunchKernelGGL(sum_rows_kernel, dim3((unsigned)P), dim3(256), 0, (hipStream_t)stream, batch,
+                     P, rows, out);
   return (int)hipGetLastError();
 }
 

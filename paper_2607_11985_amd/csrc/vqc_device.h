@@ -921,7 +921,7 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
   const bool valid = b < A.B;
 
   angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
-              A.occ_idx, A.occ_cs, A.params, A.P, A.inputs, A.F, tid, WG);
+              A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs, A.F, tid, WG);
   if (BWD)
     for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
@@ -971,7 +971,7 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
   float* g = e + A.S * A.n;                             // [S][n]
 
   angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
-              A.occ_idx, A.occ_cs, A.params, A.P, A.inputs, A.F, tid, WG);
+              A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs, A.F, tid, WG);
   for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
   FS::prepare(w, tid, WG);  // the tables of both sweeps
@@ -1064,7 +1064,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
-  angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.P, A.inputs,
+  angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs,
               A.F, tid, WG);
   if (BWD)
     for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;

@@ -72,6 +72,7 @@ struct TileArgs {
   const float* occ_cs;      // per occurrence (cos, sin) of const angles / 2
   const uint8_t* end_phys;  // per logical qubit: physical bit at forward end
   int32_t n_occ, n_slots, P, F;
+  int32_t pstride;          // row stride of params: P, or 0 when shared by the batch
   int32_t n;                // real qubits (E and g have n columns)
   int32_t k;                // tile qubits (>= 4)
   int32_t t;                // thread bits per sample: k - R
@@ -111,6 +112,7 @@ struct PassArgs {
   const int32_t* occ_idx;
   const float* occ_cs;
   int32_t n_occ, n_slots, P, F, n, k, ng;
+  int32_t pstride;             // row stride of params: P, or 0 when shared by the batch
   int64_t B;
   const float* params;
   const float* inputs;

@@ -155,6 +155,9 @@ def test_compile_rejects_options():
     assert rc == _lib.VQC_ERR_INVALID_ARG
     rc, _ = host_compile([], 2, 0, 0, engine=2)
     assert rc == _lib.VQC_ERR_INVALID_ARG and "engine" in _lib.vqc_last_error()
+    arr = _lib.encode_ops([])
+    rc, _ = _lib.vqc_compile_raw(arr, 0, 2, 0, 0, _lib.vqc_compile_opts(device=-1, shared_params=2))
+    assert rc == _lib.VQC_ERR_INVALID_ARG and "shared_params" in _lib.vqc_last_error()
     for n, bad in ((6, 1), (6, 5), (6, -1), (6, 6), (15, 3), (15, 6)):
         rc, _ = host_compile([], n, 0, 0, reg_bits=bad)
         assert rc == _lib.VQC_ERR_INVALID_ARG and "reg_bits" in _lib.vqc_last_error()
@@ -244,3 +247,22 @@ def test_generated_kernels_compile_config2():
 
 def test_jit_check_null(lib):
     assert lib.vqc_jit_check(None) == _lib.VQC_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("idx", [2, 5])
+def test_shared_params_workspace(idx):
+    """Shared parameters add the per-sample gradient rows [B, P] to the
+    training workspaces and change nothing else."""
+    w = W.make_config(idx, batch=2)
+    arr = _lib.encode_ops(w.ops)
+    sizes = {}
+    for shared in (0, 1):
+        rc, h = _lib.vqc_compile_raw(arr, len(w.ops), w.n_qubits, w.n_params, w.n_inputs,
+                                     _lib.vqc_compile_opts(device=-1, shared_params=shared))
+        assert rc == 0, _lib.vqc_last_error()
+        assert _lib.vqc_circuit_info(h)["shared_params"] == shared
+        sizes[shared] = [_lib.vqc_workspace_bytes(h, 10, m) for m in (0, 1, 2)]
+        _lib.vqc_destroy(h)
+    assert sizes[1][0] == sizes[0][0]
+    for m in (1, 2):
+        assert sizes[1][m] >= sizes[0][m] + 10 * w.n_params * 4

@@ -252,6 +252,46 @@ def test_train_step_parity(torch_mod, n, loss, path, engine):
     check_grads({"dp": dp2.cpu().numpy(), "dx": dx2.cpu().numpy()}, dp, dx, g)
 
 
+@pytest.mark.parametrize("n,path,engine", [(6, "auto", "jit"), (9, "auto", "jit"),
+                                           (12, "auto", "jit"), (15, "auto", "jit"),
+                                           (9, "auto", "interp"), (15, "auto", "interp")])
+def test_shared_params_parity(torch_mod, n, path, engine):
+    """One parameter vector for the whole batch (Algorithm 1's shared theta):
+    dparams is the sum of the samples' gradients; the inputs stay per sample."""
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit
+    ops, P, F = W.random_circuit(n, 40 + 5 * n, seed=9000 + n)
+    B = 2 * samples_per_wg(n) + 3
+    theta, inputs = W.random_inputs(B, P, F, seed=9100 + n)
+    theta = theta[0]
+    params = np.repeat(theta[None, :], B, axis=0)  # the oracle sees the shared row per sample
+    cot = W.random_cotangent(B, n, seed=9200 + n)
+    note(f"shared params n={n} path={path} engine={engine} B={B}")
+    c = Circuit(ops, n, P, F, path=path, engine=engine, shared_params=True)
+    assert c.info()["shared_params"] == 1
+    p = torch.from_numpy(np.ascontiguousarray(theta)).cuda()
+    x = torch.from_numpy(inputs).cuda()
+    g = torch.from_numpy(cot.astype(np.float32)).cuda()
+    E, ws = c.forward(p, x, training=True)
+    dp, dx = c.backward(p, x, g, ws)
+    Es, dps, dxs = c.train_step(p, x, "sum")
+    torch.cuda.synchronize()
+    dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
+    check_E(E.cpu().numpy(), Er)
+    check_grad(dx.cpu().numpy(), dxr, cot, "dinputs")
+    dp_sum = dpr.sum(axis=0)
+    err = np.max(np.abs(dp.cpu().numpy() - dp_sum))
+    assert err <= G_REL * np.max(np.abs(dp_sum)) + G_FLOOR * np.sum(np.abs(cot)), err
+    # the training step with the summed objective: the cotangent is all ones
+    ones = np.ones((B, n))
+    dpr1, dxr1, _ = oracle.vjp(ops, n, params, inputs, ones)
+    check_E(Es.cpu().numpy(), Er)
+    check_grad(dxs.cpu().numpy(), dxr1, ones, "dinputs (step)")
+    ref1 = dpr1.sum(axis=0)
+    err = np.max(np.abs(dps.cpu().numpy() - ref1))
+    assert err <= G_REL * np.max(np.abs(ref1)) + G_FLOOR * np.sum(np.abs(ones)), err
+
+
 def test_loss_grad_kernel(torch_mod):
     from paper_2607_11985_amd.api import loss_grad
     rng = np.random.default_rng(4)
