@@ -266,6 +266,82 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
     o << "__device__ __forceinline__ static const float* esigns(const Walk&) { return nullptr; }\n";
 }
 
+// Batched gradient reduction for samples spanning whole waves.  A rotation's
+// per-lane partial waits in pending register pd[slot % 16]; a batch is flushed
+// when a position is needed by another slot, and at the end of the stream.
+// The flush is a reduce-scatter over the 64 lanes: four halving steps pair
+// lane bit b with value-index bit b (lane bit 2 through row_half_mirror, a
+// lane ^ 7 pairing taken first while every lane still holds all values; then
+// quad_perm 1032 and 2301 for bits 0 and 1, row_ror 8 for bit 3), leaving in
+// each lane the partial of value lane % 16 over its 16-lane row; two more
+// additions (a swizzle across 16 lanes, a shuffle across 32) complete it.
+// The lane that owns the slot (lane = slot % 64) adds it to its register.
+// About 4 instructions per rotation instead of a full DPP sum per rotation.
+struct Pending {
+  int tag[16];
+  Pending() { clear(); }
+  void clear() {
+    for (int& t : tag) t = -1;
+  }
+  bool empty() const {
+    for (int t : tag)
+      if (t >= 0) return false;
+    return true;
+  }
+};
+
+void emit_flush(std::ostringstream& o, Pending& pd) {
+  if (pd.empty()) return;
+  static const int kSteps[4][2] = {{2, 0x141}, {0, 0xB1}, {1, 0x4E}, {3, 0x128}};
+  o << "  { float v[16];\n";
+  for (int j = 0; j < 16; ++j)
+    o << "    v[" << j << "] = " << (pd.tag[j] >= 0 ? "pd" + std::to_string(j) : "0.f") << ";\n";
+  o << "    const uint32_t lo = opaque(ln);\n";
+  int live = 16;  // values left, at indices 0..live-1 after compaction
+  std::vector<int> bits_left = {0, 1, 2, 3};
+  // value index -> position: keep a map from the remaining value-index bits
+  std::vector<int> order;  // value-index bits still present, low to high in position
+  order = {0, 1, 2, 3};
+  for (const auto& st : kSteps) {
+    const int b = st[0], ctrl = st[1];
+    // position bit of value-index bit b among the remaining bits
+    int pos = 0;
+    while (order[pos] != b) ++pos;
+    const int half = live / 2;
+    o << "    { const bool hb = (lo >> " << b << ") & 1u;\n";
+    for (int q = 0; q < half; ++q) {
+      // positions with bit `pos` 0 / 1
+      const int lowmask = (1 << pos) - 1;
+      const int p0 = ((q & ~lowmask) << 1) | (q & lowmask);
+      const int p1 = p0 | (1 << pos);
+      o << "      const float k" << q << " = hb ? v[" << p1 << "] : v[" << p0 << "];\n"
+        << "      const float s" << q << " = hb ? v[" << p0 << "] : v[" << p1 << "];\n";
+    }
+    for (int q = 0; q < half; ++q)
+      o << "      v[" << q << "] = k" << q << " + dpp_f<" << ctrl << ">(s" << q << ");\n";
+    o << "    }\n";
+    order.erase(order.begin() + pos);
+    live = half;
+  }
+  o << "    float tot = v[0] + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v[0]), 0x401F));\n"
+    << "    tot += __shfl_xor(tot, 32, 64);\n";
+  // lane L holds the total of value index L % 16 (identity map of bits)
+  std::map<int, std::pair<uint32_t, uint32_t>> byreg;  // register -> (position mask, row table)
+  for (int j = 0; j < 16; ++j) {
+    if (pd.tag[j] < 0) continue;
+    const int slot = pd.tag[j];
+    auto& e = byreg[slot / 64];
+    e.first |= 1u << j;
+    e.second |= (uint32_t)((slot % 64) >> 4) << (2 * j);
+  }
+  o << "    const uint32_t j = lo & 15u, row = lo >> 4;\n";
+  for (const auto& kv : byreg)
+    o << "    ga[" << kv.first << "] += ((" << hex(kv.second.first) << " >> j) & 1u) && row == (("
+      << hex(kv.second.second) << " >> (2u * j)) & 3u) ? tot : 0.f;\n";
+  o << "  }\n";
+  pd.clear();
+}
+
 // Statements of one instruction stream for register width R.  With tangent
 // tables (tm.on) rotations use the tangent form and blocks are rescaled.
 void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, int n_ins, bool bwd,
@@ -274,6 +350,15 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   const bool tan = tm.on;
   const int nrot = (int)(bwd ? tm.bocc.size() : tm.focc.size());
   int m = 0;  // rotation index in the stream
+  // batched only with up to 8 amplitudes per thread: with 16 the sixteen
+  // pending partials no longer fit beside psi and lambda, and the per-rotation
+  // group sum is a small part of a rotation's work there anyway
+  const bool batched = bwd && gm.regs && gm.tm == 64 && R <= 3;
+  Pending pend;
+  if (batched)
+    o << "  float pd0 = 0.f, pd1 = 0.f, pd2 = 0.f, pd3 = 0.f, pd4 = 0.f, pd5 = 0.f, pd6 = 0.f, "
+         "pd7 = 0.f, pd8 = 0.f, pd9 = 0.f, pd10 = 0.f, pd11 = 0.f, pd12 = 0.f, pd13 = 0.f, "
+         "pd14 = 0.f, pd15 = 0.f;\n";
   if (tan && bwd)
     o << "  const float* gmul = reinterpret_cast<const float*>(w.smem + " << tm.off_gm << "u);\n";
   if (tan)
@@ -355,6 +440,10 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       default: {
         const bool reg = pa < R;
         const char* kind = op == OP_RX ? "rx" : op == OP_RY ? "ry" : "rz";
+        if (batched && slot >= 0) {  // the slot's position is taken by another slot
+          const int pos = slot & 15;
+          if (pend.tag[pos] >= 0 && pend.tag[pos] != slot) emit_flush(o, pend);
+        }
         const std::string at = std::to_string(arg) + " * " + std::to_string(S) + " + w.sl";
         if (tan) {
           o << "  { const float t = w.tab[" << arg << "].x; ";
@@ -387,9 +476,16 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           }
         }
         if (bwd) {
-          if (slot < 0)
+          if (slot < 0) {
             o << " (void)g;";
-          else if (gm.regs)
+          } else if (batched) {
+            const int pos = slot & 15;
+            // the empty asm keeps the partial's computation here: left free, the
+            // compiler sinks it into the flush and keeps the old states alive
+            o << " pd" << pos << (pend.tag[pos] == slot ? " += g;" : " = g;")
+              << " asm volatile(\"\" : \"+v\"(pd" << pos << "));";
+            pend.tag[pos] = slot;
+          } else if (gm.regs)
             // the empty asm keeps the update here: left free, the additions drift
             // to the end of the kernel and every partial stays alive until then
             o << " const float gs = group_sum<" << gm.tm << ">(g); ga[" << slot / gm.tm
@@ -409,6 +505,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       }
     }
   }
+  if (batched) emit_flush(o, pend);
 }
 
 // A schedule struct: run() for one stream, the group sum used for <Z>, and
