@@ -87,6 +87,9 @@ def load():
     lib.vqc_train_step.argtypes = [_vp, ctypes.c_int64, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp,
                                    _vp, _vp, _vp, ctypes.c_size_t, _vp]
     lib.vqc_train_step.restype = ctypes.c_int
+    lib.vqc_fd_backward.argtypes = [_vp, ctypes.c_int64, _vp, _vp, _vp, ctypes.c_float, _vp,
+                                    ctypes.c_size_t, _vp, _vp, _vp]
+    lib.vqc_fd_backward.restype = ctypes.c_int
     lib.vqc_jit_check.argtypes = [_vp]
     lib.vqc_jit_check.restype = ctypes.c_int
     lib.vqc_circuit_info.argtypes = [_vp, ctypes.POINTER(vqc_info)]
@@ -175,6 +178,12 @@ def vqc_train_step(h, batch, params_ptr, inputs_ptr, loss_kind, y_ptr, expvals_p
 
 def vqc_loss_grad(kind: int, batch: int, n: int, e_ptr, y_ptr, g_ptr, stream):
     _check(load().vqc_loss_grad(kind, batch, n, e_ptr, y_ptr, g_ptr, stream))
+
+
+def vqc_fd_backward(h, batch, params_ptr, inputs_ptr, grad_ptr, step, ws_ptr, ws_bytes,
+                    dparams_ptr, dinputs_ptr, stream):
+    _check(load().vqc_fd_backward(h, batch, params_ptr, inputs_ptr, grad_ptr, step, ws_ptr,
+                                  ws_bytes, dparams_ptr, dinputs_ptr, stream))
 
 
 def vqc_jit_check(h):

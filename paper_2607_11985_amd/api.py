@@ -142,6 +142,23 @@ class Circuit:
         return (E, dparams, dinputs, g) if want_cot else (E, dparams, dinputs)
 
 
+    def fd_backward(self, params, inputs, grad_out, h: float = 1e-2):
+        """Central-difference gradients (the paper's FD mode), resident path only."""
+        B = int(grad_out.shape[0])
+        params = self._params(params, B)
+        inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
+        grad_out = _as_rows(grad_out, B, self.n, self.device, "grad_out")
+        dparams = torch.empty((self.P,) if self.shared else (B, self.P), dtype=torch.float32,
+                              device=self.device)
+        dinputs = torch.empty((B, self.F), dtype=torch.float32, device=self.device)
+        nb = _lib.vqc_workspace_bytes(self.handle, B, 3)
+        ws = torch.empty(max(nb, 1), dtype=torch.uint8, device=self.device)
+        _lib.vqc_fd_backward(self.handle, B, _ptr(params), _ptr(inputs), grad_out.data_ptr(),
+                             float(h), ws.data_ptr(), nb, dparams.data_ptr() if self.P else None,
+                             dinputs.data_ptr() if self.F else None, _stream(self.device))
+        return dparams, dinputs
+
+
 def loss_grad(kind: str, E, y=None, out=None):
     """Cotangent dL/dE of a scalar objective, computed on the GPU."""
     B, n = E.shape

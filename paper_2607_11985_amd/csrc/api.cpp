@@ -2,6 +2,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <climits>
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <string>
@@ -104,9 +105,19 @@ size_t shared_rows_offset(const Plan& p, int64_t batch, int mode) {
   return align_up(required_bytes_core(p, batch, mode), 256);
 }
 
+// Central differences (mode 3, resident path): the shifted copies' E rows
+// [B * 2 (P + F), n], then (shared parameters) the per-sample rows.
+size_t fd_rows_bytes(const Plan& p, int64_t batch) {
+  return align_up((size_t)batch * 2 * (p.P + p.F) * p.n * 4, 256);
+}
+
 size_t required_bytes(const vqc_circuit* c, int64_t batch, int mode) {
   const Plan& p = c->plan;
   if (batch == 0) return 0;
+  if (mode == 3) {
+    if (p.path != VQC_PATH_RESIDENT) return 0;
+    return fd_rows_bytes(p, batch) + (c->shared ? (size_t)batch * p.P * 4 : 0);
+  }
   if (!c->shared || mode == 0 || p.P == 0) return required_bytes_core(p, batch, mode);
   return shared_rows_offset(p, batch, mode) + (size_t)batch * p.P * 4;
 }
@@ -383,7 +394,7 @@ void vqc_destroy(vqc_circuit* c) {
 }
 
 size_t vqc_workspace_bytes(const vqc_circuit* c, int64_t batch, int32_t training) {
-  if (!c || batch < 0 || training < 0 || training > 2) return (size_t)-1;
+  if (!c || batch < 0 || training < 0 || training > 3) return (size_t)-1;
   return required_bytes(c, batch, training);
 }
 
@@ -520,6 +531,49 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
                              stream)
            : vqc::launch_resident_step(p, a, resident_blocks(p, batch), stream);
   if (rc) return hip_fail("training step launch", rc);
+  if (rows && (rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream)))
+    return hip_fail("parameter gradient sum", rc);
+  return VQC_OK;
+}
+
+int vqc_fd_backward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
+                    const float* grad_out, float h, void* workspace, size_t workspace_bytes,
+                    float* dparams, float* dinputs, void* stream) {
+  int rc = check_runnable(c);
+  if (rc) return rc;
+  const Plan& p = c->plan;
+  if (!(h > 0.f) || !std::isfinite(h)) return fail(VQC_ERR_INVALID_ARG, "h must be finite and > 0");
+  if (p.path != VQC_PATH_RESIDENT)
+    return fail(VQC_ERR_UNSUPPORTED, "central differences run on the resident path only");
+  if ((rc = check_batch(c, batch))) return rc;
+  const int NS = p.P + p.F;
+  if (batch == 0 || NS == 0) return VQC_OK;
+  if ((rc = check_rows(c, params, inputs))) return rc;
+  if (!grad_out) return fail(VQC_ERR_INVALID_ARG, "grad_out is NULL");
+  const int64_t virt = batch * 2 * NS;
+  if ((rc = check_batch(c, virt))) return rc;
+  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(c, batch, 3),
+                            "workspace smaller than vqc_workspace_bytes(c, batch, 3)")))
+    return rc;
+  DeviceGuard g(c->device);
+  if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  float* ev = reinterpret_cast<float*>(ws);
+  float* dp = p.P > 0 ? dparams : nullptr;
+  float* dx = p.F > 0 ? dinputs : nullptr;
+  float* rows = (c->shared && dp) ? reinterpret_cast<float*>(ws + fd_rows_bytes(p, batch)) : nullptr;
+  vqc::TileArgs a = tile_args(c, false, virt);
+  a.params = params;
+  a.inputs = inputs;
+  a.expvals = ev;
+  a.fd_slots = NS;
+  a.fd_h = h;
+  rc = c->engine == VQC_ENGINE_JIT
+           ? vqc::jit_launch(c->jit.res_fwd, resident_blocks(p, virt), p.WG, &a, sizeof(a), stream)
+           : vqc::launch_resident_forward(p, a, resident_blocks(p, virt), stream);
+  if (rc) return hip_fail("shifted forward launch", rc);
+  rc = vqc::launch_fd_combine(batch, NS, p.P, p.n, h, ev, grad_out, rows ? rows : dp, dx, stream);
+  if (rc) return hip_fail("difference launch", rc);
   if (rows && (rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream)))
     return hip_fail("parameter gradient sum", rc);
   return VQC_OK;

@@ -73,6 +73,28 @@ __global__ void __launch_bounds__(256) sum_rows_kernel(int64_t B, int P,
   if (threadIdx.x == 0) out[p] = part[0];
 }
 
+// Central differences: d L / d slot s of row b = sum_q g[b,q] (E(+h) - E(-h)) / 2h,
+// with the shifted copies laid out as the forward's fd_slots mode writes them.
+__global__ void fd_combine_kernel(int64_t B, int NS, int P, int n, float h,
+                                  const float* __restrict__ ev, const float* __restrict__ g,
+                                  float* __restrict__ dparams, float* __restrict__ dinputs) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * NS) return;
+  const int64_t b = i / NS;
+  const int s = (int)(i - b * NS);
+  const float* ep = ev + ((b * NS + s) * 2) * n;
+  const float* em = ep + n;
+  const float* gb = g + b * n;
+  float v = 0.f;
+  for (int q = 0; q < n; ++q) v += gb[q] * (ep[q] - em[q]);
+  v /= 2.f * h;
+  if (s < P) {
+    if (dparams) dparams[b * P + s] = v;
+  } else if (dinputs) {
+    dinputs[b * (NS - P) + (s - P)] = v;
+  }
+}
+
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) p[i] = 0.f;
@@ -210,6 +232,14 @@ int launch_sum_rows(int64_t batch, int P, const float* rows, float* out, void* s
   if (P == 0) return 0;
   hipLaunchKernelGGL(sum_rows_kernel, dim3((unsigned)P), dim3(256), 0, (hipStream_t)stream, batch,
                      P, rows, out);
+  return (int)hipGetLastError();
+}
+
+int launch_fd_combine(int64_t batch, int NS, int P, int n, float h, const float* ev,
+                      const float* g, float* dparams, float* dinputs, void* stream) {
+  if (batch * NS == 0) return 0;
+  hipLaunchKernelGGL(fd_combine_kernel, dim3(grid_1d(batch * NS, 256)), dim3(256), 0,
+                     (hipStream_t)stream, batch, NS, P, n, h, ev, g, dparams, dinputs);
   return (int)hipGetLastError();
 }
 

@@ -713,10 +713,15 @@ __device__ __forceinline__ void run_schedule(St<R>& a, St<R>& l, const uint32_t*
 
 // Parameter resolution: (cos, sin)(theta/2) for every occurrence and sample of
 // the workgroup.  Constant angles come precomputed from the compile phase.
+// fd_slots > 0 (central differences): sample bb of the launch is the shifted
+// copy r = bb mod (2 fd_slots) of input row bb / (2 fd_slots), in which slot
+// r / 2 (a parameter, then an input) is moved by +fd_h (r even) or -fd_h.
 __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64_t b0, int64_t B,
                                             const int32_t* occ_src, const int32_t* occ_idx,
                                             const float* occ_cs, const float* params, int P,
-                                            const float* inputs, int F, int tid, int nthreads) {
+                                            const float* inputs, int F, int tid, int nthreads,
+                                            int n_params = 0, int fd_slots = 0,
+                                            float fd_h = 0.f) {
   for (int i = tid; i < n_occ * S; i += nthreads) {
     const int o = i / S;
     const int s = i - o * S;
@@ -728,8 +733,19 @@ __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64
       sn = occ_cs[2 * o + 1];
     } else {
       float th = 0.f;
-      if (bb < B)
-        th = src == kSrcParam ? params[bb * P + occ_idx[o]] : inputs[bb * F + occ_idx[o]];
+      if (bb < B) {
+        int64_t row = bb;
+        float shift = 0.f;
+        if (fd_slots > 0) {
+          const int64_t per = 2 * (int64_t)fd_slots;
+          row = bb / per;
+          const int r = (int)(bb - row * per);
+          const int slot = src == kSrcParam ? occ_idx[o] : n_params + occ_idx[o];
+          if (slot == (r >> 1)) shift = (r & 1) ? -fd_h : fd_h;
+        }
+        th = (src == kSrcParam ? params[row * P + occ_idx[o]] : inputs[row * F + occ_idx[o]]) +
+             shift;
+      }
       sincosf(0.5f * th, &sn, &c);
     }
     tab[i] = make_float2(c, sn);
@@ -921,7 +937,8 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
   const bool valid = b < A.B;
 
   angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
-              A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs, A.F, tid, WG);
+              A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots,
+              A.fd_h);
   if (BWD)
     for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();

@@ -95,6 +95,9 @@ struct TileArgs {
   const float* target;      // [B] (MSE heads)
   float* cot_out;           // [B, n] cotangent written here when not null
   uint32_t lds_e;           // byte offset of E and g rows [S][n] each
+  // central differences (forward only): B counts shifted copies, 2 per slot
+  int32_t fd_slots;         // P + F, or 0
+  float fd_h;
 };
 
 // Arguments of one streaming pass (1024 threads, one 2^14 tile per workgroup).

@@ -70,7 +70,7 @@ def test_configs_plan_on_host(idx):
     assert info["fwd_instructions"] == n_prims + info["fwd_exchanges"]
     assert info["bwd_instructions"] == n_prims + info["bwd_exchanges"]
     assert _lib.vqc_workspace_bytes(h, 0, 1) == 0
-    assert _lib.vqc_workspace_bytes(h, 10, 3) == ctypes.c_size_t(-1).value
+    assert _lib.vqc_workspace_bytes(h, 10, 4) == ctypes.c_size_t(-1).value
     step = _lib.vqc_workspace_bytes(h, 10, 2)
     if stream:  # training workspace plus the cotangent rows
         assert step >= _lib.vqc_workspace_bytes(h, 10, 1) + 10 * w.n_qubits * 4
@@ -242,6 +242,20 @@ def test_generated_kernels_compile_config2():
     rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
     assert rc == 0
     _lib.vqc_jit_check(h)
+    _lib.vqc_destroy(h)
+
+
+def test_fd_backward_validation(lib):
+    assert lib.vqc_fd_backward(None, 1, None, None, None, 1e-2, None, 0, None, None,
+                               None) == _lib.VQC_ERR_INVALID_ARG
+    w = W.make_config(5, batch=2)
+    rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    assert rc == 0
+    assert _lib.vqc_workspace_bytes(h, 4, 3) == 0  # streaming: not offered
+    _lib.vqc_destroy(h)
+    w = W.make_config(2, batch=2)
+    rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    assert _lib.vqc_workspace_bytes(h, 4, 3) >= 4 * 2 * (w.n_params + w.n_inputs) * 8 * 4
     _lib.vqc_destroy(h)
 
 

@@ -292,6 +292,47 @@ def test_shared_params_parity(torch_mod, n, path, engine):
     assert err <= G_REL * np.max(np.abs(ref1)) + G_FLOOR * np.sum(np.abs(ones)), err
 
 
+@pytest.mark.parametrize("n,engine,shared", [(4, "jit", False), (9, "jit", False),
+                                             (12, "jit", False), (7, "interp", False),
+                                             (10, "jit", True)])
+def test_fd_backward(torch_mod, n, engine, shared):
+    """Central differences through the shifted-batch forward, against the
+    oracle's exact gradient.  Bound: truncation h^2/6 times the third
+    derivative (at most k^3 sum|g| for a slot used by k gates), plus the
+    float32 rounding of E (2e-5 per evaluation, twice the tested bar) over h."""
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit
+    ops, P, F = W.random_circuit(n, 30 + 4 * n, seed=9300 + n)
+    B = 3
+    params, inputs = W.random_inputs(B, P, F, seed=9400 + n)
+    if shared:
+        params = np.repeat(params[:1], B, axis=0)
+    cot = W.random_cotangent(B, n, seed=9500 + n)
+    note(f"fd backward n={n} engine={engine} shared={shared}")
+    c = Circuit(ops, n, P, F, engine=engine, shared_params=shared)
+    h = 1e-2
+    p = torch.from_numpy(np.ascontiguousarray(params[0] if shared else params)).cuda()
+    dp, dx = c.fd_backward(p, torch.from_numpy(inputs).cuda(),
+                           torch.from_numpy(cot.astype(np.float32)).cuda(), h=h)
+    torch.cuda.synchronize()
+    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, cot)
+    if shared:
+        dpr = dpr.sum(axis=0, keepdims=True)
+    uses = {}
+    for o in ops:
+        for src, v in o.angles:
+            if src != "const":
+                uses[(src, v)] = uses.get((src, v), 0) + 1
+    k = max(uses.values())
+    gsum = np.sum(np.abs(cot), axis=1, keepdims=True)
+    if shared:
+        gsum = gsum.sum(keepdims=True)
+    bound = (h * h / 6 * k ** 3 + 2e-5 / h) * gsum
+    assert np.all(np.abs(dp.cpu().numpy().reshape(dpr.shape) - dpr) <= bound)
+    gsx = np.sum(np.abs(cot), axis=1, keepdims=True)
+    assert np.all(np.abs(dx.cpu().numpy() - dxr) <= (h * h / 6 * k ** 3 + 2e-5 / h) * gsx)
+
+
 def test_loss_grad_kernel(torch_mod):
     from paper_2607_11985_amd.api import loss_grad
     rng = np.random.default_rng(4)
