@@ -14,6 +14,7 @@ Contents
                         exact for R_P(t) = exp(-i t P/2)); independent of vjp.
   fd_grad(...)          central finite differences (the paper's FD policy,
                         Sec. 4.2.3), independent of vjp.
+  probabilities(...)    basis-state probabilities |Psi_k|^2 of the final state.
   loss_cotangent(...)   d loss / d E for the scalar objectives of the
                         workloads (mean of <Z>, sum, MSE heads; Sec. 4.2.3).
   dense                 a second, independent forward by dense 2^n x 2^n
@@ -66,11 +67,11 @@ def open_library(path: str):
     lib.oracle_forward.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                    ctypes.c_int, dp, ctypes.c_int, dp,
                                    ctypes.c_int, dp, dp, ctypes.c_int,
-                                   ctypes.c_int, ctypes.c_double, ctypes.c_int]
+                                   ctypes.c_int, ctypes.c_double, ctypes.c_int, dp]
     lib.oracle_forward.restype = ctypes.c_int
     lib.oracle_vjp.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                ctypes.c_int, dp, ctypes.c_int, dp, ctypes.c_int,
-                               dp, dp, dp, dp, ctypes.c_int]
+                               dp, dp, dp, dp, ctypes.c_int, dp]
     lib.oracle_vjp.restype = ctypes.c_int
     lib.oracle_op_size.restype = ctypes.c_int
     assert lib.oracle_op_size() == OP_DTYPE.itemsize, "oracle_op layout mismatch"
@@ -112,12 +113,20 @@ def _as2d(a, B, width):
     return a
 
 
-def forward(ops, n, params, inputs, want_state=False, shift=None, nthreads=0):
+def _psi0(psi0, B, n):
+    if psi0 is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(psi0, dtype=np.complex128).reshape(B, 1 << n))
+    return a
+
+
+def forward(ops, n, params, inputs, want_state=False, shift=None, nthreads=0, psi0=None):
     """E [B, n] (float64); with want_state also the final states [B, 2^n] c128.
 
     params [B, P] and inputs [B, F] are taken as given (float32 values are
     upcast exactly).  shift = (op_index, angle_slot, delta) offsets one angle
-    of one gate in every sample.
+    of one gate in every sample.  psi0 [B, 2^n]: initial states (default
+    |0...0>), Algorithm 1's optional input.
     """
     lib = _load()
     params = np.asarray(params)
@@ -131,18 +140,22 @@ def forward(ops, n, params, inputs, want_state=False, shift=None, nthreads=0):
     E = np.zeros((B, n), dtype=np.float64)
     st = np.zeros((B, 1 << n), dtype=np.complex128) if want_state else None
     so, ss, sd = shift if shift is not None else (-1, 0, 0.0)
+    s0 = _psi0(psi0, B, n)
     rc = lib.oracle_forward(rec.ctypes.data, len(ops), n, B, _dptr(p), max(P, 1),
                             _dptr(x), max(F, 1), _dptr(E),
                             st.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
                             if st is not None else None,
-                            so, ss, sd, nthreads)
+                            so, ss, sd, nthreads,
+                            s0.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+                            if s0 is not None else None)
     if rc != 0:
         raise ValueError(f"oracle_forward failed ({rc})")
     return (E, st) if want_state else E
 
 
-def vjp(ops, n, params, inputs, grad_out, nthreads=0):
-    """(dparams [B,P], dinputs [B,F], E [B,n]) in float64 for cotangent grad_out."""
+def vjp(ops, n, params, inputs, grad_out, nthreads=0, psi0=None):
+    """(dparams [B,P], dinputs [B,F], E [B,n]) in float64 for cotangent grad_out
+    (psi0: initial states as in forward)."""
     lib = _load()
     params = np.asarray(params)
     inputs = np.asarray(inputs)
@@ -156,8 +169,11 @@ def vjp(ops, n, params, inputs, grad_out, nthreads=0):
     dx = np.zeros((B, max(F, 1)), dtype=np.float64)
     E = np.zeros((B, n), dtype=np.float64)
     rec = encode_ops(ops)
+    s0 = _psi0(psi0, B, n)
     rc = lib.oracle_vjp(rec.ctypes.data, len(ops), n, B, _dptr(p), max(P, 1), _dptr(x),
-                        max(F, 1), _dptr(g), _dptr(dp), _dptr(dx), _dptr(E), nthreads)
+                        max(F, 1), _dptr(g), _dptr(dp), _dptr(dx), _dptr(E), nthreads,
+                        s0.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+                        if s0 is not None else None)
     if rc != 0:
         raise ValueError(f"oracle_vjp failed ({rc})")
     return dp[:, :P], dx[:, :F], E
@@ -170,7 +186,14 @@ def _occurrences(ops):
                 yield k, s, src, int(v)
 
 
-def _shift_grad(ops, n, params, inputs, grad_out, delta, coef):
+def probabilities(ops, n, params, inputs, psi0=None, nthreads=0):
+    """Basis-state probabilities |Psi_k|^2 [B, 2^n] of the final state: the
+    other output the execute phase offers besides <Z> (Sec. 3)."""
+    _, st = forward(ops, n, params, inputs, want_state=True, nthreads=nthreads, psi0=psi0)
+    return np.abs(st) ** 2
+
+
+def _shift_grad(ops, n, params, inputs, grad_out, delta, coef, psi0=None):
     params = np.asarray(params)
     inputs = np.asarray(inputs)
     B = params.shape[0]
@@ -178,22 +201,22 @@ def _shift_grad(ops, n, params, inputs, grad_out, delta, coef):
     dp = np.zeros((B, params.shape[1]))
     dx = np.zeros((B, inputs.shape[1]))
     for k, s, src, idx in _occurrences(ops):
-        ep = forward(ops, n, params, inputs, shift=(k, s, +delta))
-        em = forward(ops, n, params, inputs, shift=(k, s, -delta))
+        ep = forward(ops, n, params, inputs, shift=(k, s, +delta), psi0=psi0)
+        em = forward(ops, n, params, inputs, shift=(k, s, -delta), psi0=psi0)
         d = coef * np.sum(g * (ep - em), axis=1)
         (dp if src == "param" else dx)[:, idx] += d
     return dp, dx
 
 
-def param_shift_grad(ops, n, params, inputs, grad_out):
+def param_shift_grad(ops, n, params, inputs, grad_out, psi0=None):
     """Two-term parameter-shift rule per angle occurrence, summed per slot:
     d f / d t = [f(t + pi/2) - f(t - pi/2)] / 2, exact for exp(-i t P/2)."""
-    return _shift_grad(ops, n, params, inputs, grad_out, np.pi / 2, 0.5)
+    return _shift_grad(ops, n, params, inputs, grad_out, np.pi / 2, 0.5, psi0)
 
 
-def fd_grad(ops, n, params, inputs, grad_out, h=1e-5):
+def fd_grad(ops, n, params, inputs, grad_out, h=1e-5, psi0=None):
     """Central finite differences per angle occurrence, summed per slot."""
-    return _shift_grad(ops, n, params, inputs, grad_out, h, 0.5 / h)
+    return _shift_grad(ops, n, params, inputs, grad_out, h, 0.5 / h, psi0)
 
 
 def loss_cotangent(kind: str, E: np.ndarray, y=None) -> np.ndarray:

@@ -6,7 +6,7 @@ matrices (scipy.linalg.expm), lifted to n qubits with Kronecker products
 (qubit j = bit j of the basis index, so qubit 0 is the right-most factor);
 CNOT and CZ are written as permutation / diagonal matrices from their action
 on basis states.  The whole circuit is the ordered matrix product applied to
-|0...0>, and <Z_j> is read off the probabilities (Algorithm 1, return
+|0...0> (or a given initial state), and <Z_j> is read off the probabilities (Algorithm 1, return
 statement).  Meant for n <= 8.
 """
 from __future__ import annotations
@@ -74,7 +74,7 @@ def circuit_unitary(ops, n: int, params_row, inputs_row) -> np.ndarray:
     return U
 
 
-def forward(ops, n: int, params, inputs, want_state: bool = False):
+def forward(ops, n: int, params, inputs, want_state: bool = False, psi0=None):
     params = np.asarray(params, dtype=np.float64)
     inputs = np.asarray(inputs, dtype=np.float64)
     B = params.shape[0]
@@ -83,7 +83,8 @@ def forward(ops, n: int, params, inputs, want_state: bool = False):
     states = np.zeros((B, N), dtype=np.complex128)
     signs = np.array([[1.0 - 2.0 * ((x >> j) & 1) for j in range(n)] for x in range(N)])
     for b in range(B):
-        psi = circuit_unitary(ops, n, params[b], inputs[b])[:, 0]
+        U = circuit_unitary(ops, n, params[b], inputs[b])
+        psi = U[:, 0] if psi0 is None else U @ np.asarray(psi0[b], dtype=np.complex128)
         states[b] = psi
         E[b] = (np.abs(psi) ** 2) @ signs
     return (E, states) if want_state else E

@@ -10,8 +10,10 @@
  *
  * What it follows:
  *   - Sec. 3 "Compile-Once Lowering and Execution" and Algorithm 1 (execute
- *     phase): the state starts as |0...0>, every gate of the fixed sequence is
- *     applied in order with its angle resolved from the current parameters.
+ *     phase): the state starts as |0...0> (or the caller's Psi_0, which
+ *     Algorithm 1 accepts as an optional input), every gate of the fixed
+ *     sequence is applied in order with its angle resolved from the current
+ *     parameters.
  *   - Algorithm 1, return statement: E[:,j] = sum_k (-1)^{k_j} |Psi[:,k]|^2.
  *   - Sec. 3 "Gate Application and Differentiation": exact gradients of the
  *     trainable parameters.  Here they are obtained by the chain rule over
@@ -212,10 +214,12 @@ static void set_threads(int nthreads) {
  * and finite-difference checks of the tests).  Returns 0, or -1 on invalid
  * input, -2 on allocation failure.
  */
+/* psi0: NULL for |0...0>, else [B][2^n] complex128 initial states. */
 int oracle_forward(const oracle_op *ops, int n_ops, int n, int B,
                    const double *params, int P, const double *inputs, int F,
                    double *expvals, double *states,
-                   int shift_op, int shift_slot, double delta, int nthreads) {
+                   int shift_op, int shift_slot, double delta, int nthreads,
+                   const double *psi0) {
     if (validate(ops, n_ops, n, P, F) != 0 || B < 0) return -1;
     set_threads(nthreads);
     size_t N = (size_t)1 << n;
@@ -224,7 +228,8 @@ int oracle_forward(const oracle_op *ops, int n_ops, int n, int B,
     for (int b = 0; b < B; ++b) {
         cplx *psi = (cplx *)calloc(N, sizeof(cplx));
         if (!psi) { err = -2; continue; }
-        psi[0] = 1.0;
+        if (psi0) memcpy(psi, psi0 + (size_t)b * N * 2, N * sizeof(cplx));
+        else psi[0] = 1.0;
         for (int k = 0; k < n_ops; ++k) {
             double ang[3] = {0, 0, 0};
             resolve_angles(&ops[k], b, params, P, inputs, F, ang);
@@ -252,7 +257,7 @@ int oracle_forward(const oracle_op *ops, int n_ops, int n, int B,
 int oracle_vjp(const oracle_op *ops, int n_ops, int n, int B,
                const double *params, int P, const double *inputs, int F,
                const double *grad_out, double *dparams, double *dinputs,
-               double *expvals, int nthreads) {
+               double *expvals, int nthreads, const double *psi0) {
     if (validate(ops, n_ops, n, P, F) != 0 || B < 0) return -1;
     set_threads(nthreads);
     size_t N = (size_t)1 << n;
@@ -266,8 +271,12 @@ int oracle_vjp(const oracle_op *ops, int n_ops, int n, int B,
         cplx *tmp = (cplx *)malloc(sizeof(cplx) * N);
         if (!st || !lam || !tmp) { free(st); free(lam); free(tmp); err = -2; continue; }
         /* forward, keeping psi_0 .. psi_G */
-        memset(st, 0, sizeof(cplx) * N);
-        st[0] = 1.0;
+        if (psi0) {
+            memcpy(st, psi0 + (size_t)b * N * 2, sizeof(cplx) * N);
+        } else {
+            memset(st, 0, sizeof(cplx) * N);
+            st[0] = 1.0;
+        }
         for (int k = 0; k < n_ops; ++k) {
             double ang[3] = {0, 0, 0};
             resolve_angles(&ops[k], b, params, P, inputs, F, ang);

@@ -337,3 +337,160 @@ def test_loss_cotangent_vs_differences(oracle_mod, kind):
             Ep = E.copy(); Ep[b, i] += h
             Em = E.copy(); Em[b, i] -= h
             assert abs((L(Ep) - L(Em)) / (2 * h) - g[b, i]) < 1e-8
+
+
+# ------------------------------------- initial state Psi_0 and probabilities
+# Algorithm 1 takes an optional initial state Psi_0 in place of |0...0>, and
+# Sec. 3 returns either <Z> or the basis-state probabilities of the final state.
+
+def _random_states(rng, B, n, normalize=True):
+    s = rng.normal(size=(B, 1 << n)) + 1j * rng.normal(size=(B, 1 << n))
+    if normalize:
+        s /= np.linalg.norm(s, axis=1, keepdims=True)
+    return s
+
+
+def test_psi0_zero_state_is_default(oracle_mod):
+    ops, P, F = W.random_circuit(5, 40, seed=61)
+    p, x = W.random_inputs(4, P, F, seed=62)
+    psi0 = np.zeros((4, 32), dtype=complex)
+    psi0[:, 0] = 1.0
+    E, st = oracle_mod.forward(ops, 5, p, x, want_state=True)
+    E0, st0 = oracle_mod.forward(ops, 5, p, x, want_state=True, psi0=psi0)
+    assert np.array_equal(E, E0) and np.array_equal(st, st0)
+    g = np.random.default_rng(63).normal(size=(4, 5))
+    a = oracle_mod.vjp(ops, 5, p, x, g)
+    b = oracle_mod.vjp(ops, 5, p, x, g, psi0=psi0)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+@pytest.mark.parametrize("n", [1, 3, 6])
+def test_psi0_basis_state_vs_x_prefix(oracle_mod, n):
+    """|k> as Psi_0 equals RX(pi) on the set bits of k prepended to the circuit,
+    up to the global phase (-i)^popcount(k)."""
+    rng = np.random.default_rng(70 + n)
+    ops, P, F = W.random_circuit(n, 25, seed=71 + n)
+    B = 6
+    p, x = W.random_inputs(B, P, F, seed=72 + n)
+    ks = rng.integers(0, 1 << n, size=B)
+    psi0 = np.zeros((B, 1 << n), dtype=complex)
+    psi0[np.arange(B), ks] = 1.0
+    E, st = oracle_mod.forward(ops, n, p, x, want_state=True, psi0=psi0)
+    for b in range(B):
+        k = int(ks[b])
+        pre = [W.Op("RX", (q,), (("const", math.pi),)) for q in range(n) if (k >> q) & 1]
+        Eb, sb = oracle_mod.forward(pre + ops, n, p[b:b + 1], x[b:b + 1], want_state=True)
+        phase = (-1j) ** bin(k).count("1")
+        assert np.max(np.abs(E[b] - Eb[0])) < 1e-13
+        assert np.max(np.abs(st[b] - sb[0] / phase)) < 1e-13
+
+
+def test_psi0_linearity(oracle_mod):
+    """The evolution is linear in Psi_0 (unnormalized inputs are evolved as given)."""
+    rng = np.random.default_rng(80)
+    ops, P, F = W.random_circuit(5, 40, seed=81)
+    p, x = W.random_inputs(3, P, F, seed=82)
+    a = _random_states(rng, 3, 5, normalize=False)
+    c = _random_states(rng, 3, 5, normalize=False)
+    al, be = 0.7 - 0.3j, -1.1 + 0.4j
+    _, sa = oracle_mod.forward(ops, 5, p, x, want_state=True, psi0=a)
+    _, sc = oracle_mod.forward(ops, 5, p, x, want_state=True, psi0=c)
+    _, s = oracle_mod.forward(ops, 5, p, x, want_state=True, psi0=al * a + be * c)
+    assert np.max(np.abs(s - (al * sa + be * sc))) < 1e-12
+    # the norm is preserved, whatever it was
+    assert np.max(np.abs(np.linalg.norm(s, axis=1) - np.linalg.norm(al * a + be * c, axis=1))) < 1e-12
+
+
+@pytest.mark.parametrize("n,seed", [(1, 0), (3, 1), (5, 2)])
+def test_psi0_vs_dense(oracle_mod, n, seed):
+    from oracle import dense
+    rng = np.random.default_rng(90 + seed)
+    ops, P, F = W.random_circuit(n, 30, seed=91 + seed)
+    p, x = W.random_inputs(4, P, F, seed=92 + seed)
+    psi0 = _random_states(rng, 4, n)
+    E, st = oracle_mod.forward(ops, n, p, x, want_state=True, psi0=psi0)
+    Ed, sd = dense.forward(ops, n, p, x, want_state=True, psi0=psi0)
+    assert np.max(np.abs(E - Ed)) < 1e-12
+    assert np.max(np.abs(st - sd)) < 1e-12
+
+
+@pytest.mark.parametrize("n", [1, 2, 4])
+def test_psi0_product_states_vs_bloch(oracle_mod, n):
+    """Product Psi_0 = (x)_q (cos a_q/2, e^{i b_q} sin a_q/2) under one-qubit gates:
+    each Bloch vector (sin a cos b, sin a sin b, cos a) turns by SO(3)."""
+    rng = np.random.default_rng(100 + n)
+    ops, P, F = W.random_circuit(n, 10 * n, seed=101 + n, kinds=("RX", "RY", "RZ", "ROT"))
+    B = 4
+    p, x = W.random_inputs(B, P, F, seed=102 + n)
+    a = rng.uniform(0, math.pi, size=(B, n))
+    bb = rng.uniform(-math.pi, math.pi, size=(B, n))
+    psi0 = np.ones((B, 1), dtype=complex)
+    for q in range(n):               # qubit q is bit q: kron puts it on the left
+        v = np.stack([np.cos(a[:, q] / 2), np.exp(1j * bb[:, q]) * np.sin(a[:, q] / 2)], axis=1)
+        psi0 = np.einsum("bi,bj->bij", v, psi0).reshape(B, -1)
+    E = oracle_mod.forward(ops, n, p, x, psi0=psi0)
+    for b in range(B):
+        v = [np.array([math.sin(a[b, q]) * math.cos(bb[b, q]),
+                       math.sin(a[b, q]) * math.sin(bb[b, q]), math.cos(a[b, q])])
+             for q in range(n)]
+
+        def ang(spec):
+            src, val = spec
+            return float(p[b, val]) if src == "param" else float(x[b, val]) if src == "input" else float(val)
+
+        for op in ops:
+            q = op.wires[0]
+            if op.kind == "ROT":
+                phi, th, om = (ang(s) for s in op.angles)
+                v[q] = _so3("RZ", om) @ (_so3("RY", th) @ (_so3("RZ", phi) @ v[q]))
+            else:
+                v[q] = _so3(op.kind, ang(op.angles[0])) @ v[q]
+        assert np.max(np.abs(E[b] - np.array([vq[2] for vq in v]))) < 1e-12
+
+
+@pytest.mark.parametrize("n,seed", [(2, 0), (4, 1)])
+def test_psi0_vjp_vs_parameter_shift(oracle_mod, n, seed):
+    rng = np.random.default_rng(110 + seed)
+    ops, P, F = W.random_circuit(n, 20, seed=111 + seed)
+    p, x = W.random_inputs(3, P, F, seed=112 + seed)
+    psi0 = _random_states(rng, 3, n)
+    g = rng.normal(size=(3, n))
+    dp, dx, _ = oracle_mod.vjp(ops, n, p, x, g, psi0=psi0)
+    sp, sx = oracle_mod.param_shift_grad(ops, n, p, x, g, psi0=psi0)
+    assert np.max(np.abs(dp - sp)) < 1e-12 and np.max(np.abs(dx - sx)) < 1e-12
+
+
+@pytest.mark.parametrize("n", [1, 3, 5])
+def test_probabilities_product_circuits(oracle_mod, n):
+    """One-qubit gates from |0...0>: p_k = prod_j (1 + (-1)^{k_j} z_j) / 2 with z_j
+    the Bloch z components; the probabilities sum to one."""
+    ops, P, F = W.random_circuit(n, 8 * n, seed=120 + n, kinds=("RX", "RY", "RZ", "ROT"))
+    p, x = W.random_inputs(4, P, F, seed=121 + n)
+    pr = oracle_mod.probabilities(ops, n, p, x)
+    for b in range(4):
+        z, _ = bloch_product_z(ops, n, p[b].astype(np.float64), x[b].astype(np.float64))
+        ref = np.array([np.prod([(1 + (1 - 2 * ((k >> j) & 1)) * z[j]) / 2 for j in range(n)])
+                        for k in range(1 << n)])
+        assert np.max(np.abs(pr[b] - ref)) < 1e-13
+    assert np.max(np.abs(pr.sum(axis=1) - 1)) < 1e-13
+
+
+def test_probabilities_ghz_and_marginals(oracle_mod):
+    rng = np.random.default_rng(130)
+    n = 4
+    ops = [W.Op("RY", (0,), (("const", math.pi / 2),))] + \
+          [W.Op("CNOT", (i, i + 1)) for i in range(n - 1)]
+    pr = oracle_mod.probabilities(ops, n, np.zeros((1, 1)), np.zeros((1, 1)))
+    ref = np.zeros(1 << n)
+    ref[0] = ref[-1] = 0.5
+    assert np.max(np.abs(pr[0] - ref)) < 1e-15
+    # random entangled circuit with Psi_0: <Z_j> is the signed marginal of the probabilities
+    ops, P, F = W.random_circuit(n, 30, seed=131)
+    p, x = W.random_inputs(3, P, F, seed=132)
+    psi0 = _random_states(rng, 3, n)
+    E = oracle_mod.forward(ops, n, p, x, psi0=psi0)
+    pr = oracle_mod.probabilities(ops, n, p, x, psi0=psi0)
+    for j in range(n):
+        sgn = np.array([1 - 2 * ((k >> j) & 1) for k in range(1 << n)])
+        assert np.max(np.abs(pr @ sgn - E[:, j])) < 1e-13
