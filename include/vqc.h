@@ -155,6 +155,28 @@ int vqc_forward(const vqc_circuit *c, int64_t batch, const float *params, const 
                 float *expvals, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * vqc_forward_ex -- vqc_forward with the execute phase's optional input and
+ * its other output (Algorithm 1: the state starts from Psi_0 when one is
+ * given, else |0...0>; Sec. 3: the final state yields basis-state
+ * probabilities or Pauli-Z expectations).
+ *   psi0    [batch, 2^n] complex64 (interleaved re, im), device, 8-byte
+ *           aligned, or NULL for |0...0>.  Basis index x holds qubit q in bit
+ *           q.  Used as given: it is not normalized, and the evolution is
+ *           linear in it.  Read only.
+ *   expvals [batch, n] fp32 written, or NULL
+ *   probs   [batch, 2^n] fp32 written, or NULL: |Psi_x|^2 of the final state
+ *           (they sum to |Psi_0|^2 per sample)
+ * At least one of expvals, probs must be non-NULL.  params, inputs and the
+ * workspace are as in vqc_forward: with a training workspace the final states
+ * are saved, and vqc_backward then gives the gradients of this forward
+ * (Psi_0 held fixed).  Errors: VQC_ERR_INVALID_ARG (also a misaligned psi0 or
+ * probs), VQC_ERR_WORKSPACE, VQC_ERR_TOO_LARGE, VQC_ERR_HIP.
+ */
+int vqc_forward_ex(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,
+                   const void *psi0, float *expvals, float *probs, void *workspace,
+                   size_t workspace_bytes, void *stream);
+
+/*
  * vqc_backward -- adjoint-method gradient (Sec. 3 "Gate Application and
  * Differentiation"; exact, same result as reverse-mode AD over the tape).
  *   grad_out [batch, n] fp32: cotangent g of E

@@ -78,6 +78,9 @@ def load():
     lib.vqc_workspace_bytes.restype = ctypes.c_size_t
     lib.vqc_forward.argtypes = [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
     lib.vqc_forward.restype = ctypes.c_int
+    lib.vqc_forward_ex.argtypes = [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, _vp, _vp,
+                                   ctypes.c_size_t, _vp]
+    lib.vqc_forward_ex.restype = ctypes.c_int
     lib.vqc_backward.argtypes = [_vp, ctypes.c_int64, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                  _vp, _vp, _vp]
     lib.vqc_backward.restype = ctypes.c_int
@@ -162,6 +165,12 @@ def vqc_workspace_bytes(h, batch: int, training: int) -> int:
 def vqc_forward(h, batch, params_ptr, inputs_ptr, expvals_ptr, ws_ptr, ws_bytes, stream):
     _check(load().vqc_forward(h, batch, params_ptr, inputs_ptr, expvals_ptr, ws_ptr, ws_bytes,
                               stream))
+
+
+def vqc_forward_ex(h, batch, params_ptr, inputs_ptr, psi0_ptr, expvals_ptr, probs_ptr, ws_ptr,
+                   ws_bytes, stream):
+    _check(load().vqc_forward_ex(h, batch, params_ptr, inputs_ptr, psi0_ptr, expvals_ptr,
+                                 probs_ptr, ws_ptr, ws_bytes, stream))
 
 
 def vqc_backward(h, batch, params_ptr, inputs_ptr, grad_ptr, ws_ptr, ws_bytes, dparams_ptr,

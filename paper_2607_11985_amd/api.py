@@ -99,6 +99,33 @@ class Circuit:
                          nb, _stream(self.device))
         return (E, ws) if training else E
 
+    def forward_ex(self, params, inputs, psi0=None, expvals: bool = True, probs: bool = False,
+                   training: bool = False, workspace=None):
+        """(E or None, probabilities or None[, workspace]) from the initial states
+        psi0 [B, 2^n] complex64 (default |0...0>)."""
+        B = self._batch(params, inputs) if (params is not None or inputs is not None) \
+            else int(psi0.shape[0])
+        params = self._params(params, B)
+        inputs = _as_rows(inputs, B, self.F, self.device, "inputs")
+        if psi0 is not None:
+            if psi0.dtype != torch.complex64 or psi0.device != self.device or \
+                    not psi0.is_contiguous() or tuple(psi0.shape) != (B, 1 << self.n):
+                raise ValueError(f"psi0 must be a contiguous complex64 tensor of shape "
+                                 f"{(B, 1 << self.n)} on {self.device}")
+        E = torch.empty((B, self.n), dtype=torch.float32, device=self.device) if expvals else None
+        pr = torch.empty((B, 1 << self.n), dtype=torch.float32, device=self.device) \
+            if probs else None
+        ws, nb = None, 0
+        if training or self.workspace_bytes(B, False) > 0:
+            if workspace is None:
+                workspace, nb = self.new_workspace(B, training)
+            else:
+                nb = workspace.numel()
+            ws = workspace
+        _lib.vqc_forward_ex(self.handle, B, _ptr(params), _ptr(inputs), _ptr(psi0), _ptr(E),
+                            _ptr(pr), _ptr(ws), nb, _stream(self.device))
+        return (E, pr, ws) if training else (E, pr)
+
     def backward(self, params, inputs, grad_out, workspace, dparams=None, dinputs=None):
         """Per-sample gradients (dparams [B,P], dinputs [B,F]) of sum(grad_out * E)."""
         B = int(grad_out.shape[0])

@@ -138,6 +138,7 @@ vqc::TileArgs tile_args(const vqc_circuit* c, bool bwd, int64_t batch) {
   a.occ_idx = at<int32_t>(c, c->off_idx);
   a.occ_cs = at<float>(c, c->off_cs);
   a.end_phys = at<uint8_t>(c, c->off_maps) + p.end_off;
+  a.start_phys = at<uint8_t>(c, c->off_maps) + p.start_off;
   a.n_occ = (int32_t)p.occ_src.size();
   a.n_slots = p.P + p.F;
   a.P = p.P;
@@ -218,9 +219,11 @@ int check_workspace(const void* workspace, size_t bytes, size_t need, const char
   return VQC_OK;
 }
 
-// Streaming forward: every pass, then the <Z> reduction into expvals.
+// Streaming forward: every pass (the first starts from |0...0> or reads psi0),
+// then the <Z> reduction into expvals; the last pass writes probs.
 int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
-                   float* expvals, unsigned char* ws, void* stream) {
+                   float* expvals, unsigned char* ws, void* stream, const void* psi0 = nullptr,
+                   float* probs = nullptr) {
   const Plan& p = c->plan;
   const StreamLayout L = stream_layout(p, batch);
   int rc = 0;
@@ -231,6 +234,11 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     a.inputs = inputs;
     a.psi_src = ws + L.psi;
     a.psi_dst = ws + L.psi;
+    if (psi0 && (a.flags & vqc::PF_INIT)) {
+      a.flags &= ~vqc::PF_INIT;
+      a.psi_src = psi0;
+    }
+    if (a.flags & vqc::PF_ZPART) a.probs = probs;
     a.epart = reinterpret_cast<float*>(ws + L.epart);
     rc = c->engine == VQC_ENGINE_JIT
              ? vqc::jit_launch(c->jit.pass_fwd[i], batch << p.ng, 1 << (p.k - p.Rf), &a, sizeof(a),
@@ -238,6 +246,7 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
              : vqc::launch_stream_pass(p, false, a, batch << p.ng, stream);
     if (rc) return hip_fail("forward pass launch", rc);
   }
+  if (!expvals) return VQC_OK;
   rc = vqc::launch_reduce_e(batch, p.ng, p.n, reinterpret_cast<const float*>(ws + L.epart),
                             expvals, stream);
   if (rc) return hip_fail("expectation reduction launch", rc);
@@ -400,12 +409,24 @@ size_t vqc_workspace_bytes(const vqc_circuit* c, int64_t batch, int32_t training
 
 int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
                 float* expvals, void* workspace, size_t workspace_bytes, void* stream) {
+  if (c && batch > 0 && !expvals) return fail(VQC_ERR_INVALID_ARG, "expvals is NULL");
+  return vqc_forward_ex(c, batch, params, inputs, nullptr, expvals, nullptr, workspace,
+                        workspace_bytes, stream);
+}
+
+int vqc_forward_ex(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
+                   const void* psi0, float* expvals, float* probs, void* workspace,
+                   size_t workspace_bytes, void* stream) {
   int rc = check_runnable(c);
   if (rc) return rc;
   if ((rc = check_batch(c, batch))) return rc;
   if (batch == 0) return VQC_OK;
   if ((rc = check_rows(c, params, inputs))) return rc;
-  if (!expvals) return fail(VQC_ERR_INVALID_ARG, "expvals is NULL");
+  if (!expvals && !probs) return fail(VQC_ERR_INVALID_ARG, "expvals and probs are both NULL");
+  if (psi0 && reinterpret_cast<uintptr_t>(psi0) % 8)
+    return fail(VQC_ERR_INVALID_ARG, "psi0 must be 8-byte aligned (complex64)");
+  if (probs && reinterpret_cast<uintptr_t>(probs) % 4)
+    return fail(VQC_ERR_INVALID_ARG, "probs must be 4-byte aligned");
   const Plan& p = c->plan;
   if (p.path == VQC_PATH_STREAM && !workspace)
     return fail(VQC_ERR_WORKSPACE, "the streaming path needs a workspace (states live in HBM)");
@@ -420,12 +441,14 @@ int vqc_forward(const vqc_circuit* c, int64_t batch, const float* params, const 
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
   if (p.path == VQC_PATH_STREAM)
     return stream_forward(c, batch, params, inputs, expvals,
-                          static_cast<unsigned char*>(workspace), stream);
+                          static_cast<unsigned char*>(workspace), stream, psi0, probs);
   vqc::TileArgs a = tile_args(c, false, batch);
   a.params = params;
   a.inputs = inputs;
   a.expvals = expvals;
   a.ws = workspace;
+  a.psi0 = psi0;
+  a.probs = probs;
   rc = c->engine == VQC_ENGINE_JIT
            ? vqc::jit_launch(c->jit.res_fwd, resident_blocks(p, batch), p.WG, &a, sizeof(a), stream)
            : vqc::launch_resident_forward(p, a, resident_blocks(p, batch), stream);

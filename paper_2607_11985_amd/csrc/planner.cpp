@@ -464,6 +464,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
       }
     }
     auto global_slot = [&](int occ) { return plan.occ_slot[occ]; };
+    plan.start_off = append_map(m, plan.maps);
     rc = plan_sweep(plan.prims, nq, plan.k, plan.R, m, plan.fwd, plan.cols, plan.fwd_exchanges,
                     global_slot, msg);
     if (rc < 0) return rc;

@@ -889,7 +889,7 @@ __device__ __forceinline__ void resident_expvals(const TileArgs& A, const float*
       v = ez[q * A.G + s];
     }
     if (e) e[s * A.n + q] = v;
-    if (bb < A.B) A.expvals[bb * A.n + q] = v;
+    if (bb < A.B && A.expvals) A.expvals[bb * A.n + q] = v;
   }
 }
 
@@ -915,6 +915,114 @@ __device__ __forceinline__ void resident_grads(const TileArgs& A, const float* a
       A.dinputs[bb * A.F + (slot - A.P)] = v;
     }
   }
+}
+
+// Logical basis index of a thread's amplitudes under a mapping phys[q] (logical
+// qubit -> physical bit): x(u) = xt ^ (XOR of rq[b] over the set bits b of u).
+// Qubits n..k-1 pad small circuits to the tile; amplitudes with a padding bit
+// set (thread bits: pt, register bits: pr) are identically zero.
+template <int R>
+struct LogicalIndex {
+  uint32_t xt, pr, rq[R];
+  bool pt;
+  __device__ __forceinline__ uint32_t at(int u) const {
+    uint32_t x = xt;
+#pragma unroll
+    for (int b = 0; b < R; ++b)
+      if (u & (1 << b)) x ^= rq[b];
+    return x;
+  }
+};
+
+template <int R>
+__device__ __forceinline__ LogicalIndex<R> logical_index(const uint8_t* phys, int n, int k,
+                                                         uint32_t tb) {
+  LogicalIndex<R> li;
+  li.xt = 0u;
+  li.pr = 0u;
+  li.pt = false;
+#pragma unroll
+  for (int b = 0; b < R; ++b) li.rq[b] = 0u;
+  for (int q = 0; q < k; ++q) {
+    const int p = phys[q];
+    if (p >= R) {
+      const uint32_t bit = (tb >> (p - R)) & 1u;
+      if (q < n) li.xt |= bit << q;
+      else li.pt = li.pt || bit;
+    } else {
+#pragma unroll
+      for (int b = 0; b < R; ++b)
+        if (p == b) {
+          if (q < n) li.rq[b] = 1u << q;
+          else li.pr |= 1u << b;
+        }
+    }
+  }
+  return li;
+}
+
+// X part of the Pauli frame the tangent form leaves on the state: bit q is set
+// where the frame anticommutes with Z_q (its <Z_q> sign is -1).  Basis state
+// x of the register state is basis state x ^ mask of the true state.
+__device__ __forceinline__ uint32_t frame_xmask(const float* es, int n) {
+  uint32_t m = 0u;
+  if (es)
+    for (int q = 0; q < n; ++q)
+      if (es[q] < 0.f) m |= 1u << q;
+  return m;
+}
+
+// Resident forward from the caller's initial states (Algorithm 1, optional
+// Psi_0): the workgroup's rows are staged in LDS with coalesced loads, then
+// every thread picks its amplitudes by logical index under the start mapping.
+template <int WG, int R>
+__device__ __forceinline__ void load_initial(St<R>& a, const TileArgs& A, const Walk& w) {
+  const int N = 1 << A.n;
+  const int64_t b0 = (int64_t)blockIdx.x * A.S;
+  const int64_t have = (A.B - b0) * N;  // amplitudes of the workgroup's real samples
+  float* re = w.xbuf;
+  float* im = w.xbuf + A.S * N;
+  const float2* src = reinterpret_cast<const float2*>(A.psi0) + b0 * N;
+  for (int i = threadIdx.x; i < A.S * N; i += WG) {
+    const float2 v = i < have ? src[i] : make_float2(0.f, 0.f);
+    re[i] = v.x;
+    im[i] = v.y;
+  }
+  __syncthreads();
+  const LogicalIndex<R> li = logical_index<R>(A.start_phys, A.n, A.k, w.tb);
+  const int row = w.sl * N;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const bool live = !li.pt && !(u & li.pr);
+    const uint32_t x = li.at(u);
+    a.r[u] = live ? re[row + x] : 0.f;
+    a.i[u] = live ? im[row + x] : 0.f;
+  }
+  __syncthreads();  // the exchange buffer is reused by the sweep
+}
+
+// Basis-state probabilities of the workgroup's final states (Sec. 3: the other
+// output of the execute phase), permuted to logical order through LDS and
+// written with coalesced stores.  Every thread must call it.
+template <int WG, int R, typename Sched>
+__device__ __forceinline__ void resident_probs(const St<R>& a, const TileArgs& A, const Walk& w) {
+  const int N = 1 << A.n;
+  const uint32_t xm = frame_xmask(Sched::esigns(w), A.n);
+  const LogicalIndex<R> li = logical_index<R>(A.end_phys, A.n, A.k, w.tb);
+  float* pb = w.xbuf;
+  __syncthreads();  // the exchange buffer may still be read
+  if (!li.pt) {
+    const int row = w.sl * N;
+#pragma unroll
+    for (int u = 0; u < St<R>::N; ++u)
+      if (!(u & li.pr)) pb[row + (li.at(u) ^ xm)] = a.r[u] * a.r[u] + a.i[u] * a.i[u];
+  }
+  __syncthreads();
+  const int64_t b0 = (int64_t)blockIdx.x * A.S;
+  const int64_t have = (A.B - b0) * N;
+  float* dst = A.probs + b0 * N;
+  for (int i = threadIdx.x; i < A.S * N; i += WG)
+    if (i < have) dst[i] = pb[i];
 }
 
 template <int R>
@@ -946,7 +1054,8 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
 
   St<R> a, l;
   if (!BWD) {
-    zero_state<R>(a, w.stid);
+    if (A.psi0) load_initial<WG, R>(a, A, w);
+    else zero_state<R>(a, w.stid);
   } else {
     const float2* ws = reinterpret_cast<const float2*>(A.ws);
     float2 v[NA];
@@ -969,6 +1078,7 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
     }
     z_partials<R, Sched>(a, w.xbuf, A.n, A.end_phys, w);
     resident_expvals(A, w.xbuf, nullptr, WG);
+    if (A.probs) resident_probs<WG, R, Sched>(a, A, w);
   } else {
     __syncthreads();
     resident_grads(A, w.acc, WG);
@@ -1133,6 +1243,14 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
       gp[A.pslots[i]] += v;
     }
   } else if (A.flags & PF_ZPART) {
+    if (A.probs) {
+      // the tile's rows are in logical order: a permutation of the stored
+      // state's addresses, so the stores stay coalesced
+      const uint32_t xm = frame_xmask(Sched::esigns(w), A.n);
+      float* pd = A.probs + sbase;
+#pragma unroll
+      for (int j = 0; j < NA; ++j) pd[(base | off[j]) ^ xm] = a.r[j] * a.r[j] + a.i[j] * a.i[j];
+    }
     float* ez = xbuf;
     z_partials<R, Sched>(a, ez, A.n, A.end_phys, w);
     for (int q = tid; q < A.n; q += WG) {

@@ -51,7 +51,7 @@ struct Plan {
   std::vector<uint8_t> maps;              // logical -> phys tables (nq bytes each)
   std::vector<int32_t> pslots;            // pass-local -> global gradient slots
   std::vector<PassPlan> fpass, bpass;     // streaming passes
-  int end_off = 0;                        // resident: forward end mapping in `maps`
+  int start_off = 0, end_off = 0;         // resident: forward start / end mapping in `maps`
   int fwd_exchanges = 0, bwd_exchanges = 0;
   int max_pass_slots = 0;
   size_t lds_fwd = 0, lds_bwd = 0, lds_tab = 0, lds_acc = 0;

@@ -98,6 +98,10 @@ struct TileArgs {
   // central differences (forward only): B counts shifted copies, 2 per slot
   int32_t fd_slots;         // P + F, or 0
   float fd_h;
+  // forward only: initial states and basis-state probabilities (logical order)
+  const void* psi0;         // float2 [B][2^n] initial states, or null for |0...0>
+  const uint8_t* start_phys;  // per logical qubit: physical bit at forward start
+  float* probs;             // [B][2^n] |psi_x|^2 of the final states, or null
 };
 
 // Arguments of one streaming pass (1024 threads, one 2^14 tile per workgroup).
@@ -127,5 +131,6 @@ struct PassArgs {
   float* gpart;                // [B * 2^ng, n_slots] gradient partial sums
   const float* grad_out;
   uint32_t lds_tab, lds_acc;
+  float* probs;                // (last forward pass) [B][2^n] probabilities, or null
 };
 }  // namespace vqc

@@ -243,6 +243,31 @@ def random_inputs(batch: int, n_params: int, n_inputs: int, seed: int):
     return p, x
 
 
+def random_states(batch: int, n: int, seed: int, kind: str = "haar") -> np.ndarray:
+    """Seeded initial states [B, 2^n] complex64 (the optional Psi_0).
+
+    haar   : complex Gaussian amplitudes scaled to unit norm (Haar-random pure
+             states), norm taken in float64 before rounding to complex64
+    basis  : |k_b> with k_b uniform in [0, 2^n)
+    sparse : a unit-norm state on 4 random basis states (peaked probabilities)
+    """
+    rng = np.random.default_rng(seed)
+    N = 1 << n
+    if kind == "basis":
+        s = np.zeros((batch, N), dtype=np.complex128)
+        s[np.arange(batch), rng.integers(0, N, size=batch)] = 1.0
+    elif kind == "sparse":
+        s = np.zeros((batch, N), dtype=np.complex128)
+        for b in range(batch):
+            idx = rng.choice(N, size=min(4, N), replace=False)
+            s[b, idx] = rng.normal(size=len(idx)) + 1j * rng.normal(size=len(idx))
+        s /= np.linalg.norm(s, axis=1, keepdims=True)
+    else:
+        s = rng.normal(size=(batch, N)) + 1j * rng.normal(size=(batch, N))
+        s /= np.linalg.norm(s, axis=1, keepdims=True)
+    return s.astype(np.complex64)
+
+
 def count_ops(ops: Sequence[Op]):
     """(rotation primitives, entanglers, ops) -- ROT counts as 3 primitives."""
     rot = sum(N_ANGLES[o.kind] for o in ops)

@@ -30,7 +30,8 @@ def test_exports_every_declared_function(lib):
     names = _lib.header_functions()
     assert {"vqc_compile", "vqc_forward", "vqc_backward", "vqc_destroy",
             "vqc_workspace_bytes", "vqc_loss_grad", "vqc_last_error",
-            "vqc_circuit_info", "vqc_jit_check"} <= set(names)
+            "vqc_circuit_info", "vqc_jit_check", "vqc_forward_ex", "vqc_train_step",
+            "vqc_fd_backward"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
 
@@ -242,6 +243,19 @@ def test_generated_kernels_compile_config2():
     rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
     assert rc == 0
     _lib.vqc_jit_check(h)
+    _lib.vqc_destroy(h)
+
+
+def test_forward_ex_validation(lib):
+    assert lib.vqc_forward_ex(None, 1, None, None, None, None, None, None, 0,
+                              None) == _lib.VQC_ERR_INVALID_ARG
+    ops, P, F = W.random_circuit(3, 10, seed=3)
+    rc, h = host_compile(ops, 3, P, F)
+    assert rc == 0
+    # a host-only handle cannot run
+    assert lib.vqc_forward_ex(h, 1, None, None, None, None, None, None, 0,
+                              None) == _lib.VQC_ERR_INVALID_ARG
+    assert "host-only" in _lib.vqc_last_error()
     _lib.vqc_destroy(h)
 
 
