@@ -21,7 +21,9 @@ Contents
                         matrices built with matrix exponentials (n <= 8).
 
 Ops are any objects with `.kind`, `.wires`, `.angles` in the backend-neutral
-gate-list format of the workload generator.
+gate-list format of the workload generator.  Kinds: RX RY RZ ROT CNOT(CX) CZ,
+ID X Y Z H S SDG T TDG SX SXDG, P(U1) U2 U3(U), CY CH SWAP CRX CRY CRZ CP RXX
+RYY RZZ, CCX CSWAP (wire 0 is the control of controlled gates).
 """
 from __future__ import annotations
 
@@ -37,13 +39,18 @@ _SRC = os.path.join(_HERE, "vqc_oracle.c")
 _BUILD = os.path.join(_HERE, "_build")
 _LIB_PATH = os.path.join(_BUILD, "liboracle.so")
 
-_KIND = {"RX": 0, "RY": 1, "RZ": 2, "ROT": 3, "CNOT": 4, "CZ": 5}
+_GATES = ("RX", "RY", "RZ", "ROT", "CNOT", "CZ",
+          "ID", "X", "Y", "Z", "H", "S", "SDG", "T", "TDG", "SX", "SXDG",
+          "P", "U2", "U3",
+          "CY", "CH", "SWAP", "CRX", "CRY", "CRZ", "CP", "RXX", "RYY", "RZZ",
+          "CCX", "CSWAP")
+_KIND = {g: i for i, g in enumerate(_GATES)}
+_KIND.update({"CX": _KIND["CNOT"], "U1": _KIND["P"], "U": _KIND["U3"]})
 _SRC_CODE = {"param": 0, "input": 1, "const": 2}
-_NANG = {"RX": 1, "RY": 1, "RZ": 1, "ROT": 3, "CNOT": 0, "CZ": 0}
 
-OP_DTYPE = np.dtype([("kind", np.int32), ("w0", np.int32), ("w1", np.int32),
-                     ("src", np.int32, 3), ("idx", np.int32, 3),
-                     ("pad", np.int32), ("val", np.float64, 3)], align=True)
+OP_DTYPE = np.dtype([("kind", np.int32), ("w", np.int32, 3), ("src", np.int32, 3),
+                     ("idx", np.int32, 3), ("mul", np.float64, 3), ("add", np.float64, 3)],
+                    align=True)
 
 _lib = None
 
@@ -88,17 +95,22 @@ def _load():
 
 
 def encode_ops(ops: Sequence) -> np.ndarray:
+    """Gate records.  An angle is ("const", value), or (src, index) or
+    (src, index, mul, add) for src in {"param", "input"}: mul * value + add."""
     rec = np.zeros(max(1, len(ops)), dtype=OP_DTYPE)
     for k, op in enumerate(ops):
         rec[k]["kind"] = _KIND[op.kind]
-        w = list(op.wires) + [-1]
-        rec[k]["w0"], rec[k]["w1"] = w[0], w[1]
-        for s, (src, v) in enumerate(op.angles):
+        w = list(op.wires) + [-1] * (3 - len(op.wires))
+        rec[k]["w"] = w[:3]
+        for s, spec in enumerate(op.angles):
+            src, v = spec[0], spec[1]
             rec[k]["src"][s] = _SRC_CODE[src]
             if src == "const":
-                rec[k]["val"][s] = float(v)
+                rec[k]["add"][s] = float(v)
             else:
                 rec[k]["idx"][s] = int(v)
+                rec[k]["mul"][s] = float(spec[2]) if len(spec) > 2 else 1.0
+                rec[k]["add"][s] = float(spec[3]) if len(spec) > 3 else 0.0
     return rec
 
 
@@ -180,10 +192,11 @@ def vjp(ops, n, params, inputs, grad_out, nthreads=0, psi0=None):
 
 
 def _occurrences(ops):
+    """(gate, slot, source, index, mul) of every non-constant angle."""
     for k, op in enumerate(ops):
-        for s, (src, v) in enumerate(op.angles):
-            if src != "const":
-                yield k, s, src, int(v)
+        for s, spec in enumerate(op.angles):
+            if spec[0] != "const":
+                yield k, s, spec[0], int(spec[1]), float(spec[2]) if len(spec) > 2 else 1.0
 
 
 def probabilities(ops, n, params, inputs, psi0=None, nthreads=0):
@@ -200,17 +213,20 @@ def _shift_grad(ops, n, params, inputs, grad_out, delta, coef, psi0=None):
     g = np.asarray(grad_out, dtype=np.float64).reshape(B, n)
     dp = np.zeros((B, params.shape[1]))
     dx = np.zeros((B, inputs.shape[1]))
-    for k, s, src, idx in _occurrences(ops):
+    for k, s, src, idx, mul in _occurrences(ops):
         ep = forward(ops, n, params, inputs, shift=(k, s, +delta), psi0=psi0)
         em = forward(ops, n, params, inputs, shift=(k, s, -delta), psi0=psi0)
-        d = coef * np.sum(g * (ep - em), axis=1)
+        d = mul * coef * np.sum(g * (ep - em), axis=1)  # chain rule through the affine angle
         (dp if src == "param" else dx)[:, idx] += d
     return dp, dx
 
 
 def param_shift_grad(ops, n, params, inputs, grad_out, psi0=None):
     """Two-term parameter-shift rule per angle occurrence, summed per slot:
-    d f / d t = [f(t + pi/2) - f(t - pi/2)] / 2, exact for exp(-i t P/2)."""
+    d f / d t = [f(t + pi/2) - f(t - pi/2)] / 2, exact when the angle enters as
+    exp(-i t G) with G of two eigenvalues 1/2 apart up to a shared offset (the
+    Pauli rotations, R_PP, P, CP, and the Euler angles of U3 / U2 / ROT) -- not
+    for the controlled rotations, whose generator has three eigenvalues."""
     return _shift_grad(ops, n, params, inputs, grad_out, np.pi / 2, 0.5, psi0)
 
 

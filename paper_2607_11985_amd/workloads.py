@@ -38,14 +38,29 @@ import numpy as np
 SEED_BASE = 260711985
 
 KINDS = ("RX", "RY", "RZ", "ROT", "CNOT", "CZ")
-N_ANGLES = {"RX": 1, "RY": 1, "RZ": 1, "ROT": 3, "CNOT": 0, "CZ": 0}
+# the general static gate set: kind -> (wires, angles).  Structure only (the
+# generators draw circuits over it); what each gate computes is not here.
+GATE_SHAPES = {
+    "RX": (1, 1), "RY": (1, 1), "RZ": (1, 1), "ROT": (1, 3), "CNOT": (2, 0), "CZ": (2, 0),
+    "ID": (1, 0), "X": (1, 0), "Y": (1, 0), "Z": (1, 0), "H": (1, 0), "S": (1, 0),
+    "SDG": (1, 0), "T": (1, 0), "TDG": (1, 0), "SX": (1, 0), "SXDG": (1, 0),
+    "P": (1, 1), "U2": (1, 2), "U3": (1, 3),
+    "CY": (2, 0), "CH": (2, 0), "SWAP": (2, 0), "CRX": (2, 1), "CRY": (2, 1), "CRZ": (2, 1),
+    "CP": (2, 1), "RXX": (2, 1), "RYY": (2, 1), "RZZ": (2, 1),
+    "CCX": (3, 0), "CSWAP": (3, 0),
+}
+GENERAL_KINDS = tuple(GATE_SHAPES)
+N_ANGLES = {k: v[1] for k, v in GATE_SHAPES.items()}
 
 
 @dataclass(frozen=True)
 class Op:
+    """One gate: kind, wires (controls first), angle specs.  An angle spec is
+    ("const", value), or (src, index) / (src, index, mul, add) with src in
+    {"param", "input"}, meaning mul * value + add."""
     kind: str
     wires: Tuple[int, ...]
-    angles: Tuple[Tuple[str, float], ...] = ()
+    angles: Tuple[tuple, ...] = ()
 
 
 @dataclass
@@ -203,35 +218,42 @@ def random_cotangent(batch: int, n: int, seed: int) -> np.ndarray:
 
 def random_circuit(n: int, n_ops: int, seed: int, n_params: int = 0,
                    n_inputs: int = 0, kinds: Sequence[str] = KINDS,
-                   p_const: float = 0.1) -> Tuple[List[Op], int, int]:
+                   p_const: float = 0.1, p_affine: float = 0.0) -> Tuple[List[Op], int, int]:
     """A seeded random static circuit over `kinds` (structure only).
 
     Angle sources are drawn among params, inputs and constants; parameters
-    and inputs may be re-used by several gates.  Returns (ops, P, F) with
-    P, F at least 1 so that every array is non-empty.
+    and inputs may be re-used by several gates.  With p_affine > 0 that share
+    of the non-constant angles gets a random (mul, add) (float32 values, mul
+    in +-[0.25, 2]).  Returns (ops, P, F) with P, F at least 1 so that every
+    array is non-empty.
     """
     rng = np.random.default_rng(seed)
     P = max(1, n_params or n_ops)
     F = max(1, n_inputs or n)
     ops: List[Op] = []
-    kinds = [k for k in kinds if (k not in ("CNOT", "CZ")) or n >= 2]
+    kinds = [k for k in kinds if GATE_SHAPES[k][0] <= n]
     for _ in range(n_ops):
         k = kinds[int(rng.integers(len(kinds)))]
-        if k in ("CNOT", "CZ"):
-            a, b = rng.choice(n, size=2, replace=False)
-            ops.append(Op(k, (int(a), int(b))))
-            continue
-        q = int(rng.integers(n))
+        nw, na = GATE_SHAPES[k]
+        if nw == 1:
+            wires = (int(rng.integers(n)),)
+        else:
+            wires = tuple(int(v) for v in rng.choice(n, size=nw, replace=False))
         ang = []
-        for _s in range(N_ANGLES[k]):
+        for _s in range(na):
             u = rng.random()
             if u < p_const:
                 ang.append(("const", float(np.float32(rng.uniform(-4, 4)))))
-            elif u < 0.5:
-                ang.append(("input", int(rng.integers(F))))
+                continue
+            src = "input" if u < 0.5 else "param"
+            idx = int(rng.integers(F if src == "input" else P))
+            if p_affine > 0 and rng.random() < p_affine:
+                mul = float(np.float32(rng.choice([-1.0, 1.0]) * rng.uniform(0.25, 2.0)))
+                add = float(np.float32(rng.uniform(-3.0, 3.0)))
+                ang.append((src, idx, mul, add))
             else:
-                ang.append(("param", int(rng.integers(P))))
-        ops.append(Op(k, (q,), tuple(ang)))
+                ang.append((src, idx))
+        ops.append(Op(k, wires, tuple(ang)))
     return ops, P, F
 
 
@@ -271,5 +293,5 @@ def random_states(batch: int, n: int, seed: int, kind: str = "haar") -> np.ndarr
 def count_ops(ops: Sequence[Op]):
     """(rotation primitives, entanglers, ops) -- ROT counts as 3 primitives."""
     rot = sum(N_ANGLES[o.kind] for o in ops)
-    ent = sum(1 for o in ops if o.kind in ("CNOT", "CZ"))
+    ent = sum(1 for o in ops if GATE_SHAPES[o.kind][0] > 1)
     return rot, ent, len(ops)
