@@ -2,11 +2,13 @@
  * vqc.h -- C ABI of the batched VQC statevector engine for MI355X (gfx950).
  *
  * The library runs the execute phase of compile-once VQC simulation on the GPU:
- * a static parametrized circuit (one-qubit Pauli rotations RX/RY/RZ, ROT, and
- * CNOT/CZ entanglers) is compiled once into a device schedule (Sec. 3
+ * a static parametrized circuit over the standard gate library (Pauli
+ * rotations, ROT, U3, the fixed Clifford+T gates, controlled and two-qubit
+ * rotations, SWAP, CCX, CSWAP) is compiled once into a device schedule (Sec. 3
  * "Compile-Once Lowering and Execution"; Algorithm 1, compile phase) and then
  * applied to B independent 2^n-amplitude complex64 states, each starting in
- * |0...0> (Algorithm 1, execute phase).  The forward pass returns the per-qubit
+ * |0...0> or a given Psi_0 (Algorithm 1, execute phase).  vqc_compile_qasm
+ * takes the circuit as OpenQASM text.  The forward pass returns the per-qubit
  * Pauli-Z expectations E[b, j] = sum_x (-1)^{x_j} |psi_b[x]|^2 (Algorithm 1,
  * return statement).  The backward pass returns the exact gradient of
  * L_b = sum_j g[b, j] E[b, j] with respect to every per-sample parameter and
@@ -17,7 +19,13 @@
  *   - Rotations are R_P(t) = exp(-i t P / 2); ROT(phi, theta, omega) is
  *     RZ(omega) RY(theta) RZ(phi) with phi applied first.  Qubit j is bit j of
  *     the basis index.  CNOT(c, t) flips t when c is 1; CZ(a, b) negates the
- *     amplitudes with both bits set.
+ *     amplitudes with both bits set.  The other gates are the OpenQASM standard
+ *     library's: P(l) = diag(1, e^{il}); U3(t, p, l) = [[c, -e^{il} s],
+ *     [e^{ip} s, e^{i(p+l)} c]] (c, s of t/2); U2(p, l) = U3(pi/2, p, l); H, S,
+ *     SDG, T, TDG, SX = sqrt(X), SXDG, X, Y, Z, ID; controlled gates (control =
+ *     wires[0]) act on the target when the control is 1; R_PP(t) =
+ *     exp(-i t P(x)P / 2); CCX(c0, c1, t); CSWAP(c, a, b).  Every gate is
+ *     applied up to a global phase, which no output depends on.
  *   - Device arrays are fp32, row-major, contiguous, device-resident and owned
  *     by the caller; the library never allocates or frees them.  Outputs are
  *     overwritten, never accumulated.
@@ -59,6 +67,32 @@ extern "C" {
 #define VQC_ROT 3
 #define VQC_CNOT 4
 #define VQC_CZ 5
+#define VQC_ID 6
+#define VQC_X 7
+#define VQC_Y 8
+#define VQC_Z 9
+#define VQC_H 10
+#define VQC_S 11
+#define VQC_SDG 12
+#define VQC_T 13
+#define VQC_TDG 14
+#define VQC_SX 15
+#define VQC_SXDG 16
+#define VQC_P 17     /* also OpenQASM u1 */
+#define VQC_U2 18    /* (phi, lambda) */
+#define VQC_U3 19    /* (theta, phi, lambda); also OpenQASM u */
+#define VQC_CY 20
+#define VQC_CH 21
+#define VQC_SWAP 22
+#define VQC_CRX 23
+#define VQC_CRY 24
+#define VQC_CRZ 25
+#define VQC_CP 26    /* also OpenQASM cu1 */
+#define VQC_RXX 27
+#define VQC_RYY 28
+#define VQC_RZZ 29
+#define VQC_CCX 30   /* controls wires[0], wires[1]; target wires[2] */
+#define VQC_CSWAP 31 /* control wires[0]; swaps wires[1], wires[2] */
 
 /* angle sources */
 #define VQC_SRC_PARAM 0 /* params[b, idx] */
@@ -67,17 +101,24 @@ extern "C" {
 
 /*
  * One gate of the static sequence G = {(g_i, w_i, p_i)} (Algorithm 1, compile
- * phase).  wires[0] is the target of a one-qubit gate, the control of CNOT,
- * the first qubit of CZ; wires[1] is the CNOT target / second CZ qubit and is
- * ignored for one-qubit gates.  Angle slot s (0 for RX/RY/RZ; phi, theta,
- * omega = 0, 1, 2 for ROT) reads src[s]/idx[s]/val[s].
+ * phase).  wires[0..k) are the gate's k qubits in the order of its definition
+ * (one-qubit gates: the target; CNOT / controlled gates: control, target; CZ,
+ * SWAP, R_PP: the two qubits; CCX: two controls, target; CSWAP: control, the
+ * two swapped qubits); unused wires are ignored.  Angle slot s (RX/RY/RZ/P and
+ * the controlled and two-qubit rotations: 0; ROT: phi, theta, omega; U3:
+ * theta, phi, lambda; U2: phi, lambda) is
+ *   src[s] == VQC_SRC_CONST:          angle = val[s]
+ *   src[s] == VQC_SRC_PARAM / INPUT:  angle = mul[s] * value + val[s]
+ * with value = params[b, idx[s]] or inputs[b, idx[s]]; mul[s] must be finite
+ * and nonzero, and gradients carry the factor mul[s] (chain rule).
  */
 typedef struct {
     int32_t kind;
-    int32_t wires[2];
+    int32_t wires[3];
     int32_t src[3];
     int32_t idx[3];
     float val[3];
+    float mul[3];
 } vqc_op;
 
 typedef struct vqc_circuit vqc_circuit;
@@ -116,8 +157,9 @@ typedef struct {
  * With VQC_ENGINE_JIT (the default) and device >= 0 the kernels of this
  * circuit are generated and compiled for the device here (seconds for large
  * circuits; compiled modules are cached per process and source text).
- * Errors: VQC_ERR_INVALID_ARG (null pointer, wire out of range, CNOT/CZ on one
- * wire, unknown kind or source, index out of range, unknown option),
+ * Errors: VQC_ERR_INVALID_ARG (null pointer, wire out of range, a wire twice
+ * in one gate, unknown kind or source, index out of range, a zero or
+ * non-finite mul, a non-finite val, unknown option),
  * VQC_ERR_UNSUPPORTED (path not possible for n_qubits, run-time compilation
  * failed), VQC_ERR_TOO_LARGE (qubits or schedule beyond the limits),
  * VQC_ERR_HIP, VQC_ERR_OOM.

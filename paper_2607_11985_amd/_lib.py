@@ -24,15 +24,19 @@ VQC_ERR_HIP = -5
 VQC_ERR_OOM = -6
 VQC_PATH_AUTO, VQC_PATH_RESIDENT, VQC_PATH_STREAM = 0, 1, 2
 VQC_ENGINE_JIT, VQC_ENGINE_INTERP = 0, 1
-KIND = {"RX": 0, "RY": 1, "RZ": 2, "ROT": 3, "CNOT": 4, "CZ": 5}
+KIND = {name: code for code, name in enumerate((
+    "RX", "RY", "RZ", "ROT", "CNOT", "CZ", "ID", "X", "Y", "Z", "H", "S", "SDG", "T", "TDG",
+    "SX", "SXDG", "P", "U2", "U3", "CY", "CH", "SWAP", "CRX", "CRY", "CRZ", "CP", "RXX", "RYY",
+    "RZZ", "CCX", "CSWAP"))}
+KIND_ALIASES = {"CX": "CNOT", "U1": "P", "U": "U3"}
 SRC = {"param": 0, "input": 1, "const": 2}
 LOSS = {"sum": 0, "mean": 1, "mse_z0": 2, "mse_meanz": 3}
 
 
 class vqc_op(ctypes.Structure):
-    _fields_ = [("kind", ctypes.c_int32), ("wires", ctypes.c_int32 * 2),
+    _fields_ = [("kind", ctypes.c_int32), ("wires", ctypes.c_int32 * 3),
                 ("src", ctypes.c_int32 * 3), ("idx", ctypes.c_int32 * 3),
-                ("val", ctypes.c_float * 3)]
+                ("val", ctypes.c_float * 3), ("mul", ctypes.c_float * 3)]
 
 
 class vqc_compile_opts(ctypes.Structure):
@@ -116,19 +120,26 @@ def _check(rc: int):
 
 
 def encode_ops(ops) -> ctypes.Array:
-    """Gate list (kind, wires, angles) -> vqc_op array."""
+    """Gate list (kind, wires, angles) -> vqc_op array.  An angle is
+    ("const", value), (src, index) or (src, index, mul, add)."""
     arr = (vqc_op * max(1, len(ops)))()
     for k, op in enumerate(ops):
         r = arr[k]
-        r.kind = KIND[op.kind]
-        w = list(op.wires) + [-1, -1]
-        r.wires[0], r.wires[1] = w[0], w[1]
-        for s, (src, v) in enumerate(op.angles):
+        r.kind = KIND[KIND_ALIASES.get(op.kind, op.kind)]
+        w = list(op.wires) + [-1, -1, -1]
+        r.wires[0], r.wires[1], r.wires[2] = w[0], w[1], w[2]
+        for s, spec in enumerate(op.angles):
+            src, v = spec[0], spec[1]
             r.src[s] = SRC[src]
+            r.mul[s] = 1.0
             if src == "const":
                 r.val[s] = float(v)
             else:
                 r.idx[s] = int(v)
+                if len(spec) > 2:
+                    r.mul[s] = float(spec[2])
+                if len(spec) > 3:
+                    r.val[s] = float(spec[3])
     return arr
 
 

@@ -20,7 +20,7 @@ struct vqc_circuit {
   vqc::JitKernels jit;
   void* blob = nullptr;
   size_t off_fwd = 0, off_bwd = 0, off_cols = 0, off_src = 0, off_idx = 0, off_cs = 0,
-         off_maps = 0, off_pslots = 0;
+         off_maps = 0, off_pslots = 0, off_ma = 0;
 };
 
 namespace {
@@ -137,6 +137,7 @@ vqc::TileArgs tile_args(const vqc_circuit* c, bool bwd, int64_t batch) {
   a.occ_src = at<int32_t>(c, c->off_src);
   a.occ_idx = at<int32_t>(c, c->off_idx);
   a.occ_cs = at<float>(c, c->off_cs);
+  a.occ_ma = p.affine ? at<float>(c, c->off_ma) : nullptr;
   a.end_phys = at<uint8_t>(c, c->off_maps) + p.end_off;
   a.start_phys = at<uint8_t>(c, c->off_maps) + p.start_off;
   a.n_occ = (int32_t)p.occ_src.size();
@@ -187,6 +188,7 @@ vqc::PassArgs pass_args(const vqc_circuit* c, const vqc::PassPlan& pp, bool bwd,
   a.occ_src = at<int32_t>(c, c->off_src);
   a.occ_idx = at<int32_t>(c, c->off_idx);
   a.occ_cs = at<float>(c, c->off_cs);
+  a.occ_ma = p.affine ? at<float>(c, c->off_ma) : nullptr;
   a.n_occ = (int32_t)p.occ_src.size();
   a.n_slots = p.P + p.F;
   a.P = p.P;
@@ -323,12 +325,12 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
     const vqc_op& o = ops[k];
     vqc::HostOp& h = hops[k];
     h.kind = o.kind;
-    h.w0 = o.wires[0];
-    h.w1 = o.wires[1];
     for (int s = 0; s < 3; ++s) {
+      h.w[s] = o.wires[s];
       h.src[s] = o.src[s];
       h.idx[s] = o.idx[s];
       h.val[s] = o.val[s];
+      h.mul[s] = o.mul[s];
     }
   }
   vqc_circuit* c = new (std::nothrow) vqc_circuit();
@@ -356,6 +358,7 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
     c->off_src = append(blob, p.occ_src);
     c->off_idx = append(blob, p.occ_idx);
     c->off_cs = append(blob, p.occ_cs);
+    c->off_ma = append(blob, p.occ_ma);
     c->off_maps = append(blob, p.maps);
     c->off_pslots = append(blob, p.pslots);
     DeviceGuard g(device);

@@ -342,6 +342,15 @@ void emit_flush(std::ostringstream& o, Pending& pd) {
   pd.clear();
 }
 
+// The chain-rule factor of an occurrence whose angle is mul * value + add, as
+// a statement on the gradient partial g (nothing when mul is 1).
+std::string occ_scale(const Plan& p, uint32_t occ) {
+  if (!p.affine || p.occ_ma[2 * occ] == 1.f) return "";
+  std::ostringstream o;
+  o << " g *= " << std::hexfloat << (double)p.occ_ma[2 * occ] << "f;";
+  return o.str();
+}
+
 // Statements of one instruction stream for register width R.  With tangent
 // tables (tm.on) rotations use the tangent form and blocks are rescaled.
 void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, int n_ins, bool bwd,
@@ -458,6 +467,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
             else
               o << "float g = adj_phase_t<R>(a, l, t, tile_bit<R>(w, " << pa << "));";
             o << " g *= gmul[" << arg << "];";
+            o << occ_scale(p, arg);
           }
         } else {
           o << "  { const float2 cs = w.tab[" << at << "]; ";
@@ -469,10 +479,11 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
                 << ") ^ 1u) << 31));";
           } else {
             if (reg)
-              o << "const float g = adj_" << kind << "<R, " << pa << ">(a, l, cs.x, cs.y);";
+              o << "float g = adj_" << kind << "<R, " << pa << ">(a, l, cs.x, cs.y);";
             else
-              o << "const float g = adj_rz_uniform<R>(a, l, cs.x, cs.y, tile_bit<R>(w, " << pa
+              o << "float g = adj_rz_uniform<R>(a, l, cs.x, cs.y, tile_bit<R>(w, " << pa
                 << "));";
+            o << occ_scale(p, arg);
           }
         }
         if (bwd) {

@@ -309,10 +309,200 @@ int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, int R,
   return 0;
 }
 
-int n_angles(int kind) {
-  if (kind == VQC_RX || kind == VQC_RY || kind == VQC_RZ) return 1;
-  if (kind == VQC_ROT) return 3;
-  return 0;
+// ------------------------------------------------------------- lowering
+// Every gate of the static set becomes primitives the kernels run: Pauli
+// rotations R_P(t) = exp(-i t P / 2) on one qubit, CNOT and CZ.  The products
+// equal the gate up to a global phase (which no output depends on); each is a
+// standard identity: H ~ RY(pi/2) RZ(pi); S, T, P ~ RZ; SX ~ RX(pi/2);
+// U3(t, p, l) ~ RZ(p) RY(t) RZ(l); controlled rotations split into half-angle
+// rotations around two CNOTs; R_ZZ is a CNOT-conjugated RZ and R_XX, R_YY add
+// basis changes; CY, CH conjugate CNOT / CZ by target rotations; SWAP is three
+// CNOTs; CCX is the six-CNOT Toffoli circuit of Nielsen and Chuang (Fig. 4.9);
+// CSWAP is a Toffoli between two CNOTs.
+
+struct GateShape {
+  int wires, angles;
+};
+
+GateShape gate_shape(int kind) {
+  switch (kind) {
+    case VQC_RX: case VQC_RY: case VQC_RZ: case VQC_P: return {1, 1};
+    case VQC_ROT: case VQC_U3: return {1, 3};
+    case VQC_U2: return {1, 2};
+    case VQC_CNOT: case VQC_CZ: case VQC_CY: case VQC_CH: case VQC_SWAP: return {2, 0};
+    case VQC_CRX: case VQC_CRY: case VQC_CRZ: case VQC_CP: case VQC_RXX: case VQC_RYY:
+    case VQC_RZZ: return {2, 1};
+    case VQC_CCX: case VQC_CSWAP: return {3, 0};
+    default: return {1, 0};  // ID and the fixed one-qubit gates
+  }
+}
+
+constexpr double kPi = 3.14159265358979323846;
+
+// Emits the primitives of one (validated) gate into plan.prims, with one
+// angle occurrence per rotation: m * (the gate's angle slot s) + a, or the
+// constant a when s < 0.
+class Lowering {
+ public:
+  Lowering(const HostOp& o, Plan& p) : o_(o), p_(p) {}
+
+  void rot(int kind, int q, int s, double m = 1.0, double a = 0.0) {
+    const int occ = (int)p_.occ_src.size();
+    const int src = s < 0 ? VQC_SRC_CONST : o_.src[s];
+    if (src == VQC_SRC_CONST) {
+      // constant gates are cached at compile time (Algorithm 1, compile phase)
+      const double th = s < 0 ? a : m * (double)o_.val[s] + a;
+      p_.occ_src.push_back(VQC_SRC_CONST);
+      p_.occ_idx.push_back(0);
+      p_.occ_slot.push_back(-1);
+      p_.occ_cs.push_back((float)std::cos(0.5 * th));
+      p_.occ_cs.push_back((float)std::sin(0.5 * th));
+      p_.occ_ma.push_back(1.f);
+      p_.occ_ma.push_back(0.f);
+    } else {
+      const int idx = o_.idx[s];
+      const float mul = (float)(m * (double)o_.mul[s]);
+      const float add = (float)(m * (double)o_.val[s] + a);
+      p_.occ_src.push_back(src);
+      p_.occ_idx.push_back(idx);
+      p_.occ_slot.push_back(src == VQC_SRC_PARAM ? idx : p_.P + idx);
+      p_.occ_cs.push_back(0.f);
+      p_.occ_cs.push_back(0.f);
+      p_.occ_ma.push_back(mul);
+      p_.occ_ma.push_back(add);
+      if (mul != 1.f || add != 0.f) p_.affine = true;
+    }
+    p_.prims.push_back({kind, q, -1, occ});
+  }
+  void cnot(int c, int t) { p_.prims.push_back({P_CNOT, c, t, -1}); }
+  void cz(int a, int b) { p_.prims.push_back({P_CZ, a, b, -1}); }
+  void c_rz(int q, double a) { rot(P_RZ, q, -1, 1.0, a); }
+  void c_ry(int q, double a) { rot(P_RY, q, -1, 1.0, a); }
+  void c_rx(int q, double a) { rot(P_RX, q, -1, 1.0, a); }
+  void h(int q) {
+    c_rz(q, kPi);
+    c_ry(q, kPi / 2);
+  }
+  void toffoli(int a, int b, int c) {
+    h(c);
+    cnot(b, c);
+    c_rz(c, -kPi / 4);
+    cnot(a, c);
+    c_rz(c, kPi / 4);
+    cnot(b, c);
+    c_rz(c, -kPi / 4);
+    cnot(a, c);
+    c_rz(b, kPi / 4);
+    c_rz(c, kPi / 4);
+    h(c);
+    cnot(a, b);
+    c_rz(a, kPi / 4);
+    c_rz(b, -kPi / 4);
+    cnot(a, b);
+  }
+
+ private:
+  const HostOp& o_;
+  Plan& p_;
+};
+
+void lower_gate(const HostOp& o, Plan& plan) {
+  Lowering L(o, plan);
+  const int a = o.w[0], b = o.w[1], c = o.w[2];
+  switch (o.kind) {
+    case VQC_RX: L.rot(P_RX, a, 0); break;
+    case VQC_RY: L.rot(P_RY, a, 0); break;
+    case VQC_RZ: L.rot(P_RZ, a, 0); break;
+    case VQC_ROT:  // RZ(omega) RY(theta) RZ(phi): phi first
+      L.rot(P_RZ, a, 0);
+      L.rot(P_RY, a, 1);
+      L.rot(P_RZ, a, 2);
+      break;
+    case VQC_CNOT: L.cnot(a, b); break;
+    case VQC_CZ: L.cz(a, b); break;
+    case VQC_ID: break;
+    case VQC_X: L.c_rx(a, kPi); break;
+    case VQC_Y: L.c_ry(a, kPi); break;
+    case VQC_Z: L.c_rz(a, kPi); break;
+    case VQC_H: L.h(a); break;
+    case VQC_S: L.c_rz(a, kPi / 2); break;
+    case VQC_SDG: L.c_rz(a, -kPi / 2); break;
+    case VQC_T: L.c_rz(a, kPi / 4); break;
+    case VQC_TDG: L.c_rz(a, -kPi / 4); break;
+    case VQC_SX: L.c_rx(a, kPi / 2); break;
+    case VQC_SXDG: L.c_rx(a, -kPi / 2); break;
+    case VQC_P: L.rot(P_RZ, a, 0); break;
+    case VQC_U2:  // U3(pi/2, phi, lambda)
+      L.rot(P_RZ, a, 1);
+      L.c_ry(a, kPi / 2);
+      L.rot(P_RZ, a, 0);
+      break;
+    case VQC_U3:  // RZ(phi) RY(theta) RZ(lambda): lambda first
+      L.rot(P_RZ, a, 2);
+      L.rot(P_RY, a, 0);
+      L.rot(P_RZ, a, 1);
+      break;
+    case VQC_CY:
+      L.c_rz(b, -kPi / 2);
+      L.cnot(a, b);
+      L.c_rz(b, kPi / 2);
+      break;
+    case VQC_CH:
+      L.c_ry(b, -kPi / 4);
+      L.cz(a, b);
+      L.c_ry(b, kPi / 4);
+      break;
+    case VQC_SWAP:
+      L.cnot(a, b);
+      L.cnot(b, a);
+      L.cnot(a, b);
+      break;
+    case VQC_CRX:
+      L.c_rz(b, kPi / 2);
+      L.rot(P_RY, b, 0, 0.5);
+      L.cnot(a, b);
+      L.rot(P_RY, b, 0, -0.5);
+      L.cnot(a, b);
+      L.c_rz(b, -kPi / 2);
+      break;
+    case VQC_CRY:
+    case VQC_CRZ: {
+      const int pk = o.kind == VQC_CRY ? P_RY : P_RZ;
+      L.rot(pk, b, 0, 0.5);
+      L.cnot(a, b);
+      L.rot(pk, b, 0, -0.5);
+      L.cnot(a, b);
+      break;
+    }
+    case VQC_CP:
+      L.rot(P_RZ, a, 0, 0.5);
+      L.rot(P_RZ, b, 0, 0.5);
+      L.cnot(a, b);
+      L.rot(P_RZ, b, 0, -0.5);
+      L.cnot(a, b);
+      break;
+    case VQC_RXX:
+    case VQC_RYY:
+    case VQC_RZZ: {
+      // basis change B with B Z B^dagger = X (RY(pi/2)) or Y (RX(-pi/2))
+      const bool xx = o.kind == VQC_RXX, yy = o.kind == VQC_RYY;
+      if (xx) { L.c_ry(a, -kPi / 2); L.c_ry(b, -kPi / 2); }
+      if (yy) { L.c_rx(a, kPi / 2); L.c_rx(b, kPi / 2); }
+      L.cnot(a, b);
+      L.rot(P_RZ, b, 0);
+      L.cnot(a, b);
+      if (xx) { L.c_ry(a, kPi / 2); L.c_ry(b, kPi / 2); }
+      if (yy) { L.c_rx(a, -kPi / 2); L.c_rx(b, -kPi / 2); }
+      break;
+    }
+    case VQC_CCX: L.toffoli(a, b, c); break;
+    case VQC_CSWAP:
+      L.cnot(c, b);
+      L.toffoli(a, b, c);
+      L.cnot(c, b);
+      break;
+    default: break;
+  }
 }
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -339,29 +529,23 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
   for (size_t k = 0; k < ops.size(); ++k) {
     const HostOp& o = ops[k];
     const std::string at = "op " + std::to_string(k) + ": ";
-    if (o.kind < VQC_RX || o.kind > VQC_CZ) {
+    if (o.kind < 0 || o.kind >= kNumGateKinds) {
       msg = at + "unknown kind " + std::to_string(o.kind);
       return VQC_ERR_INVALID_ARG;
     }
-    if (o.w0 < 0 || o.w0 >= n) {
-      msg = at + "wire " + std::to_string(o.w0) + " out of range";
-      return VQC_ERR_INVALID_ARG;
-    }
-    if (o.kind == VQC_CNOT || o.kind == VQC_CZ) {
-      if (o.w1 < 0 || o.w1 >= n) {
-        msg = at + "second wire " + std::to_string(o.w1) + " out of range";
+    const GateShape sh = gate_shape(o.kind);
+    for (int i = 0; i < sh.wires; ++i) {
+      if (o.w[i] < 0 || o.w[i] >= n) {
+        msg = at + "wire " + std::to_string(o.w[i]) + " out of range";
         return VQC_ERR_INVALID_ARG;
       }
-      if (o.w1 == o.w0) {
-        msg = at + "two-qubit gate on a single wire";
-        return VQC_ERR_INVALID_ARG;
-      }
-      plan.prims.push_back({o.kind == VQC_CNOT ? P_CNOT : P_CZ, o.w0, o.w1, -1});
-      continue;
+      for (int j = 0; j < i; ++j)
+        if (o.w[j] == o.w[i]) {
+          msg = at + "a wire appears twice in one gate";
+          return VQC_ERR_INVALID_ARG;
+        }
     }
-    const int na = n_angles(o.kind);
-    int occ0 = (int)plan.occ_src.size();
-    for (int s = 0; s < na; ++s) {
+    for (int s = 0; s < sh.angles; ++s) {
       const int src = o.src[s], idx = o.idx[s];
       if (src == VQC_SRC_PARAM) {
         if (idx < 0 || idx >= P) {
@@ -376,27 +560,17 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
       } else if (src != VQC_SRC_CONST) {
         msg = at + "unknown angle source " + std::to_string(src);
         return VQC_ERR_INVALID_ARG;
-      } else if (!std::isfinite(o.val[s])) {
-        msg = at + "constant angle is not finite";
+      }
+      if (!std::isfinite(o.val[s])) {
+        msg = at + (src == VQC_SRC_CONST ? "constant angle" : "angle offset") + " is not finite";
         return VQC_ERR_INVALID_ARG;
       }
-      plan.occ_src.push_back(src);
-      plan.occ_idx.push_back(src == VQC_SRC_CONST ? 0 : idx);
-      plan.occ_slot.push_back(src == VQC_SRC_PARAM ? idx : src == VQC_SRC_INPUT ? P + idx : -1);
-      // constant gates are cached at compile time (Algorithm 1, compile phase)
-      const double half = 0.5 * (double)o.val[s];
-      plan.occ_cs.push_back(src == VQC_SRC_CONST ? (float)std::cos(half) : 0.f);
-      plan.occ_cs.push_back(src == VQC_SRC_CONST ? (float)std::sin(half) : 0.f);
+      if (src != VQC_SRC_CONST && (!std::isfinite(o.mul[s]) || o.mul[s] == 0.f)) {
+        msg = at + "angle scale (mul) must be finite and nonzero";
+        return VQC_ERR_INVALID_ARG;
+      }
     }
-    if (o.kind == VQC_ROT) {
-      // ROT(phi, theta, omega) = RZ(omega) RY(theta) RZ(phi): phi first
-      plan.prims.push_back({P_RZ, o.w0, -1, occ0 + 0});
-      plan.prims.push_back({P_RY, o.w0, -1, occ0 + 1});
-      plan.prims.push_back({P_RZ, o.w0, -1, occ0 + 2});
-    } else {
-      const int pk = o.kind == VQC_RX ? P_RX : o.kind == VQC_RY ? P_RY : P_RZ;
-      plan.prims.push_back({pk, o.w0, -1, occ0});
-    }
+    lower_gate(o, plan);
   }
   const int n_occ = (int)plan.occ_src.size();
   if (reg_bits != 0 && (reg_bits < 2 || reg_bits > 5)) {

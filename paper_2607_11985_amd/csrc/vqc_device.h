@@ -636,6 +636,7 @@ struct Walk {
   float* xbuf;        // planar exchange buffer: plane floats of real parts, then imaginary
   uint32_t plane;
   const float2* tab;  // (cos, sin)(theta/2), [occurrence][S]
+  const float* ma;    // (mul, add) per occurrence, or null: gradients carry mul
   float* acc;         // gradient accumulators [slot][G]
   int k, t, S, G;
   int stid, sl, grp, width;
@@ -706,19 +707,21 @@ __device__ __forceinline__ void run_schedule(St<R>& a, St<R>& l, const uint32_t*
       // dL/dtheta = Im <lambda| P |psi>, then psi, lambda <- R(-theta) psi, lambda
       const float g = adjoint_rotation<R>(op, a, l, pa, cs.x, cs.y, w.tb);
       const int slot = (int)(w0 >> 16) - 1;
-      if (slot >= 0) acc_add<WIDE>(w, slot, g);
+      if (slot >= 0) acc_add<WIDE>(w, slot, w.ma ? g * w.ma[2 * arg] : g);
     }
   }
 }
 
 // Parameter resolution: (cos, sin)(theta/2) for every occurrence and sample of
-// the workgroup.  Constant angles come precomputed from the compile phase.
+// the workgroup, theta = mul * value + add (occ_ma, or the value itself when
+// occ_ma is null).  Constant angles come precomputed from the compile phase.
 // fd_slots > 0 (central differences): sample bb of the launch is the shifted
 // copy r = bb mod (2 fd_slots) of input row bb / (2 fd_slots), in which slot
 // r / 2 (a parameter, then an input) is moved by +fd_h (r even) or -fd_h.
 __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64_t b0, int64_t B,
                                             const int32_t* occ_src, const int32_t* occ_idx,
-                                            const float* occ_cs, const float* params, int P,
+                                            const float* occ_cs, const float* occ_ma,
+                                            const float* params, int P,
                                             const float* inputs, int F, int tid, int nthreads,
                                             int n_params = 0, int fd_slots = 0,
                                             float fd_h = 0.f) {
@@ -745,6 +748,7 @@ __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64
         }
         th = (src == kSrcParam ? params[row * P + occ_idx[o]] : inputs[row * F + occ_idx[o]]) +
              shift;
+        if (occ_ma) th = fmaf(occ_ma[2 * o], th, occ_ma[2 * o + 1]);
       }
       sincosf(0.5f * th, &sn, &c);
     }
@@ -855,6 +859,7 @@ __device__ __forceinline__ Walk resident_walk(const TileArgs& A, unsigned char* 
   w.xbuf = reinterpret_cast<float*>(smem);
   w.plane = (uint32_t)WG << R;
   w.tab = reinterpret_cast<float2*>(smem + A.lds_tab);
+  w.ma = A.occ_ma;
   w.acc = reinterpret_cast<float*>(smem + A.lds_acc);
   w.k = A.k;
   w.t = A.t;
@@ -1045,8 +1050,8 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
   const bool valid = b < A.B;
 
   angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
-              A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots,
-              A.fd_h);
+              A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F, tid, WG, A.P,
+              A.fd_slots, A.fd_h);
   if (BWD)
     for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
@@ -1098,7 +1103,7 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
   float* g = e + A.S * A.n;                             // [S][n]
 
   angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
-              A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs, A.F, tid, WG);
+              A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F, tid, WG);
   for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
   FS::prepare(w, tid, WG);  // the tables of both sweeps
@@ -1177,6 +1182,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.xbuf = xbuf;
   w.plane = (uint32_t)WG * NA;
   w.tab = tab;
+  w.ma = A.occ_ma;
   w.acc = acc;
   w.k = A.k;
   w.t = A.k - R;
@@ -1191,7 +1197,8 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
-  angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.params, A.pstride, A.inputs,
+  angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params,
+              A.pstride, A.inputs,
               A.F, tid, WG);
   if (BWD)
     for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;

@@ -46,6 +46,8 @@ struct Plan {
   std::vector<Prim> prims;
   std::vector<int32_t> occ_src, occ_idx, occ_slot;
   std::vector<float> occ_cs;              // 2 per occurrence
+  std::vector<float> occ_ma;              // 2 per occurrence: angle = mul * value + add
+  bool affine = false;                    // some occurrence has (mul, add) != (1, 0)
   std::vector<uint32_t> fwd, bwd;         // instruction pairs
   std::vector<uint32_t> cols;             // exchange / tile I/O column tables
   std::vector<uint8_t> maps;              // logical -> phys tables (nq bytes each)
@@ -60,10 +62,11 @@ struct Plan {
 
 // Host planning (no device calls).  Returns 0 or a VQC_ERR_* code with msg.
 struct HostOp {
-  int32_t kind, w0, w1;
+  int32_t kind, w[3];
   int32_t src[3], idx[3];
-  float val[3];
+  float val[3], mul[3];
 };
+constexpr int kNumGateKinds = 32;  // VQC_RX .. VQC_CSWAP
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
                Plan& plan, std::string& msg);
 

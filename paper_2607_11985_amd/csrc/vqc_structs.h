@@ -70,6 +70,8 @@ struct TileArgs {
   const int32_t* occ_src;   // per occurrence: 0 param, 1 input, 2 const
   const int32_t* occ_idx;
   const float* occ_cs;      // per occurrence (cos, sin) of const angles / 2
+  const float* occ_ma;      // per occurrence (mul, add): angle = mul * value + add;
+                            // null when every occurrence is (1, 0)
   const uint8_t* end_phys;  // per logical qubit: physical bit at forward end
   int32_t n_occ, n_slots, P, F;
   int32_t pstride;          // row stride of params: P, or 0 when shared by the batch
@@ -118,6 +120,7 @@ struct PassArgs {
   const int32_t* occ_src;
   const int32_t* occ_idx;
   const float* occ_cs;
+  const float* occ_ma;         // (mul, add) per occurrence, or null
   int32_t n_occ, n_slots, P, F, n, k, ng;
   int32_t pstride;             // row stride of params: P, or 0 when shared by the batch
   int64_t B;

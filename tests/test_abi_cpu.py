@@ -49,7 +49,7 @@ def test_header_constants_match_binding():
     assert int(defs["VQC_ENGINE_JIT"]) == _lib.VQC_ENGINE_JIT
     assert int(defs["VQC_ENGINE_INTERP"]) == _lib.VQC_ENGINE_INTERP
     assert ctypes.sizeof(_lib.vqc_compile_opts) == 32 and ctypes.sizeof(_lib.vqc_info) == 96
-    assert ctypes.sizeof(_lib.vqc_op) == 48
+    assert ctypes.sizeof(_lib.vqc_op) == 64
 
 
 @pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
@@ -117,7 +117,16 @@ def _one(kind, wires, angles=()):
 BAD = [
     ("wire_high", _one("RY", (3,), (("param", 0),)), 3, 1, 0, _lib.VQC_ERR_INVALID_ARG, "wire"),
     ("wire_negative", _one("RX", (-1,), (("param", 0),)), 3, 1, 0, _lib.VQC_ERR_INVALID_ARG, "wire"),
-    ("cnot_same", _one("CNOT", (1, 1)), 3, 0, 0, _lib.VQC_ERR_INVALID_ARG, "single wire"),
+    ("cnot_same", _one("CNOT", (1, 1)), 3, 0, 0, _lib.VQC_ERR_INVALID_ARG, "twice"),
+    ("ccx_same", _one("CCX", (0, 2, 0)), 3, 0, 0, _lib.VQC_ERR_INVALID_ARG, "twice"),
+    ("cswap_high", _one("CSWAP", (0, 1, 3)), 3, 0, 0, _lib.VQC_ERR_INVALID_ARG, "wire"),
+    ("zero_mul", _one("RY", (0,), (("param", 0, 0.0, 0.1),)), 2, 1, 0, _lib.VQC_ERR_INVALID_ARG,
+     "mul"),
+    ("inf_mul", _one("CRX", (0, 1), (("input", 0, math.inf, 0.0),)), 2, 0, 1,
+     _lib.VQC_ERR_INVALID_ARG, "mul"),
+    ("nan_offset", _one("U3", (0,), (("param", 0, 1.0, math.nan), ("const", 0.0),
+                                     ("const", 0.0))), 2, 1, 0, _lib.VQC_ERR_INVALID_ARG,
+     "finite"),
     ("cz_high", _one("CZ", (0, 5)), 3, 0, 0, _lib.VQC_ERR_INVALID_ARG, "wire"),
     ("param_range", _one("RZ", (0,), (("param", 4),)), 2, 4, 0, _lib.VQC_ERR_INVALID_ARG, "param"),
     ("input_range", _one("RZ", (0,), (("input", 1),)), 2, 0, 1, _lib.VQC_ERR_INVALID_ARG, "input"),
@@ -140,7 +149,7 @@ def test_compile_rejects(case):
 
 def test_compile_rejects_unknown_kind_and_source():
     arr = _lib.encode_ops(_one("RX", (0,), (("param", 0),)))
-    arr[0].kind = 9
+    arr[0].kind = 32
     rc, _ = _lib.vqc_compile_raw(arr, 1, 2, 1, 0, _lib.vqc_compile_opts(device=-1))
     assert rc == _lib.VQC_ERR_INVALID_ARG and "kind" in _lib.vqc_last_error()
     arr = _lib.encode_ops(_one("RX", (0,), (("param", 0),)))
