@@ -167,6 +167,45 @@ typedef struct {
 int vqc_compile(const vqc_op *ops, int32_t n_ops, int32_t n_qubits, int32_t n_params,
                 int32_t n_inputs, const vqc_compile_opts *opts, vqc_circuit **out);
 
+/*
+ * vqc_parse_qasm -- the OpenQASM front end alone (Sec. 3: a normalized
+ * OpenQASM circuit is lowered once; Algorithm 1, compile phase: parse C into
+ * the gate sequence).  Host only, no device.
+ *   source       NUL-terminated OpenQASM 2.0, or the static subset of
+ *                OpenQASM 3: qreg/qubit and creg/bit registers (qubits
+ *                numbered across registers in declaration order), the
+ *                standard gate library (qelib1.inc / stdgates.inc names,
+ *                plus u, U, CX, cnot, phase, cphase, toffoli, fredkin),
+ *                user gate definitions, register broadcasting, barrier,
+ *                gphase, and terminal measurement.
+ *   input_names  comma-separated names of declared inputs that are data
+ *                features (inputs[b, .]); every other declared input
+ *                (`input float theta;`, `input array[float[64], 8] w;`) is a
+ *                trainable parameter.  Slots follow declaration order, an
+ *                array taking consecutive slots.  NULL: no data inputs.
+ *   Angles are expressions in numbers, pi, tau, euler, declared inputs,
+ *   + - * / ^ and sin cos tan exp ln sqrt arcsin arccos arctan; each must be
+ *   constant or affine in one input (then it becomes mul * value + val).
+ *   ops/capacity receive the gate list (ops may be NULL with capacity 0 to
+ *   query the count); *n_ops, *n_qubits, *n_params, *n_inputs are written on
+ *   success even when the capacity is too small (then VQC_ERR_TOO_LARGE).
+ * Errors: VQC_ERR_INVALID_ARG (syntax, unknown names, out-of-range indices,
+ * non-affine angles; the message gives line:column), VQC_ERR_UNSUPPORTED
+ * (reset, mid-circuit measurement, classical control, loops, subroutines,
+ * gate modifiers, opaque gates, other includes, gates outside the library),
+ * VQC_ERR_TOO_LARGE, VQC_ERR_OOM.
+ */
+int vqc_parse_qasm(const char *source, const char *input_names, vqc_op *ops, int32_t capacity,
+                   int32_t *n_ops, int32_t *n_qubits, int32_t *n_params, int32_t *n_inputs);
+
+/*
+ * vqc_compile_qasm -- vqc_parse_qasm followed by vqc_compile of its gate list
+ * with n_qubits, n_params and n_inputs from the program (vqc_circuit_info
+ * reports them).  Errors: those of both.
+ */
+int vqc_compile_qasm(const char *source, const char *input_names, const vqc_compile_opts *opts,
+                     vqc_circuit **out);
+
 /* Frees the handle and its device schedule.  NULL is ignored. */
 void vqc_destroy(vqc_circuit *c);
 

@@ -76,6 +76,12 @@ def load():
                                 ctypes.c_int32, ctypes.c_int32,
                                 ctypes.POINTER(vqc_compile_opts), ctypes.POINTER(_vp)]
     lib.vqc_compile.restype = ctypes.c_int
+    lib.vqc_parse_qasm.argtypes = [ctypes.c_char_p, ctypes.c_char_p, ctypes.POINTER(vqc_op),
+                                   ctypes.c_int32] + [ctypes.POINTER(ctypes.c_int32)] * 4
+    lib.vqc_parse_qasm.restype = ctypes.c_int
+    lib.vqc_compile_qasm.argtypes = [ctypes.c_char_p, ctypes.c_char_p,
+                                     ctypes.POINTER(vqc_compile_opts), ctypes.POINTER(_vp)]
+    lib.vqc_compile_qasm.restype = ctypes.c_int
     lib.vqc_destroy.argtypes = [_vp]
     lib.vqc_destroy.restype = None
     lib.vqc_workspace_bytes.argtypes = [_vp, ctypes.c_int64, ctypes.c_int32]
@@ -163,6 +169,31 @@ def vqc_compile_raw(arr, n_ops, n_qubits, n_params, n_inputs, opts):
     rc = lib.vqc_compile(arr, n_ops, n_qubits, n_params, n_inputs,
                          ctypes.byref(opts) if opts is not None else None, ctypes.byref(h))
     return rc, h
+
+
+def vqc_parse_qasm(source: str, input_names: str | None = None):
+    """(vqc_op array, n_ops, n_qubits, n_params, n_inputs) of an OpenQASM program."""
+    lib = load()
+    counts = [ctypes.c_int32() for _ in range(4)]
+    src = source.encode()
+    names = input_names.encode() if input_names else None
+    _check(lib.vqc_parse_qasm(src, names, None, 0, *[ctypes.byref(c) for c in counts]))
+    n = counts[0].value
+    arr = (vqc_op * max(1, n))()
+    _check(lib.vqc_parse_qasm(src, names, arr, n, *[ctypes.byref(c) for c in counts]))
+    return arr, n, counts[1].value, counts[2].value, counts[3].value
+
+
+def vqc_compile_qasm(source: str, input_names: str | None = None, device: int = 0,
+                     path: int = VQC_PATH_AUTO, reg_bits: int = 0, engine: int = VQC_ENGINE_JIT,
+                     shared_params: int = 0):
+    lib = load()
+    opts = vqc_compile_opts(device=device, path=path, reg_bits=reg_bits, engine=engine,
+                            shared_params=shared_params)
+    h = _vp()
+    _check(lib.vqc_compile_qasm(source.encode(), input_names.encode() if input_names else None,
+                                ctypes.byref(opts), ctypes.byref(h)))
+    return h
 
 
 def vqc_destroy(h):

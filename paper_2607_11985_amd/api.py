@@ -52,6 +52,26 @@ class Circuit:
                                        path=_PATHS[path], reg_bits=reg_bits,
                                        engine=_ENGINES[engine], shared_params=int(self.shared))
 
+    @classmethod
+    def from_qasm(cls, source: str, inputs=(), device: int = 0, path: str = "auto",
+                  reg_bits: int = 0, engine: str = "jit", shared_params: bool = False):
+        """Compile an OpenQASM program (vqc_compile_qasm).  `inputs`: names of the
+        declared inputs that are data features; the other declared inputs are
+        trainable parameters, in declaration order."""
+        self = cls.__new__(cls)
+        names = ",".join(inputs) if inputs else None
+        self.handle = _lib.vqc_compile_qasm(source, names, device=device, path=_PATHS[path],
+                                            reg_bits=reg_bits, engine=_ENGINES[engine],
+                                            shared_params=int(bool(shared_params)))
+        info = _lib.vqc_circuit_info(self.handle)
+        self.ops = None
+        self.n = info["n_qubits"]
+        self.P = info["n_params"]
+        self.F = info["n_inputs"]
+        self.shared = bool(shared_params)
+        self.device = torch.device("cuda", device)
+        return self
+
     def _params(self, params, B):
         """Per-sample rows [B, P], or the shared vector [P]."""
         if not self.shared:

@@ -396,6 +396,40 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   return VQC_OK;
 }
 
+int vqc_parse_qasm(const char* source, const char* input_names, vqc_op* ops, int32_t capacity,
+                   int32_t* n_ops, int32_t* n_qubits, int32_t* n_params, int32_t* n_inputs) {
+  if (!n_ops || !n_qubits || !n_params || !n_inputs)
+    return fail(VQC_ERR_INVALID_ARG, "an output count pointer is NULL");
+  if (capacity < 0 || (capacity > 0 && !ops))
+    return fail(VQC_ERR_INVALID_ARG, "ops is NULL or capacity is negative");
+  std::vector<vqc_op> v;
+  int nq = 0, np = 0, ni = 0;
+  std::string msg;
+  const int rc = vqc::parse_qasm(source, input_names, v, nq, np, ni, msg);
+  if (rc) return fail(rc, msg);
+  *n_ops = (int32_t)v.size();
+  *n_qubits = nq;
+  *n_params = np;
+  *n_inputs = ni;
+  if (ops && (int64_t)v.size() > capacity)
+    return fail(VQC_ERR_TOO_LARGE, "ops capacity " + std::to_string(capacity) + " < " +
+                                       std::to_string(v.size()) + " gates");
+  if (ops && !v.empty()) std::memcpy(ops, v.data(), v.size() * sizeof(vqc_op));
+  return VQC_OK;
+}
+
+int vqc_compile_qasm(const char* source, const char* input_names, const vqc_compile_opts* opts,
+                     vqc_circuit** out) {
+  if (!out) return fail(VQC_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  std::vector<vqc_op> v;
+  int nq = 0, np = 0, ni = 0;
+  std::string msg;
+  const int rc = vqc::parse_qasm(source, input_names, v, nq, np, ni, msg);
+  if (rc) return fail(rc, msg);
+  return vqc_compile(v.data(), (int32_t)v.size(), nq, np, ni, opts, out);
+}
+
 void vqc_destroy(vqc_circuit* c) {
   if (!c) return;
   if (c->blob) {

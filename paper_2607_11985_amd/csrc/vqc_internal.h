@@ -69,6 +69,9 @@ struct HostOp {
 constexpr int kNumGateKinds = 32;  // VQC_RX .. VQC_CSWAP
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
                Plan& plan, std::string& msg);
+// OpenQASM front end (qasm.cpp).  Returns 0 or a VQC_ERR_* code with msg.
+int parse_qasm(const char* source, const char* input_names, std::vector<vqc_op>& ops,
+               int& n_qubits, int& n_params, int& n_inputs, std::string& msg);
 
 // Kernel launchers (kernels.hip).  Return 0 or a hipError_t value.
 int launch_resident_forward(const Plan& plan, const TileArgs& a, int64_t blocks, void* stream);

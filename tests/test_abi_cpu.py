@@ -31,7 +31,7 @@ def test_exports_every_declared_function(lib):
     assert {"vqc_compile", "vqc_forward", "vqc_backward", "vqc_destroy",
             "vqc_workspace_bytes", "vqc_loss_grad", "vqc_last_error",
             "vqc_circuit_info", "vqc_jit_check", "vqc_forward_ex", "vqc_train_step",
-            "vqc_fd_backward"} <= set(names)
+            "vqc_fd_backward", "vqc_parse_qasm", "vqc_compile_qasm"} <= set(names)
     for name in names:
         assert hasattr(lib, name), name
 
