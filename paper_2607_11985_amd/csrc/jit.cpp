@@ -342,6 +342,35 @@ void emit_flush(std::ostringstream& o, Pending& pd) {
   pd.clear();
 }
 
+// Whether exchange `arg` only swaps register bits with lane bits of the sample
+// (bits the 64 lanes of one wave hold), and the (register bit, lane bit) pairs.
+// The planner stores, after the exchange's 2k columns, where each physical
+// bit's qubit goes.
+bool lane_exchange(const Plan& p, uint32_t arg, int k, int R, int t,
+                   std::vector<std::pair<int, int>>& swaps) {
+  const int lanes = std::min(t, 6);
+  const uint32_t* dest = p.cols.data() + arg + 2 * k;
+  for (int q = 0; q < k; ++q) {
+    const int d = (int)dest[q];
+    if (d == q) continue;
+    if (d < 0 || d >= k || (int)dest[d] != q) return false;  // not a transposition
+    const int lo = std::min(q, d), hi = std::max(q, d);
+    if (lo >= R || hi < R || hi - R >= lanes) return false;
+    if (q == lo) swaps.push_back({lo, hi - R});
+  }
+  if (swaps.empty()) return false;
+  // Lane bits 4 and 5 cost one permlane swap per two values.  Below that a
+  // swap costs a DPP move (two for lane bit 2) and a select per value, more
+  // VALU work than an LDS exchange of 8 or 16 amplitudes per thread: it pays
+  // only where latency, not issue, bounds the kernel (4 amplitudes per thread;
+  // measured: 35 % faster on the 8-qubit training step, 10 % slower on the
+  // 12-qubit one).
+  if (R <= 2) return true;
+  for (const auto& sw : swaps)
+    if (sw.second < 4) return false;
+  return true;
+}
+
 // The chain-rule factor of an occurrence whose angle is mul * value + add, as
 // a statement on the gradient partial g (nothing when mul is 1).
 std::string occ_scale(const Plan& p, uint32_t occ) {
@@ -379,6 +408,17 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
     const int slot = (int)(w0 >> 16) - 1;
     switch (op) {
       case OP_EXCHANGE: {
+        std::vector<std::pair<int, int>> swaps;
+        if (lane_exchange(p, arg, k, R, t, swaps)) {
+          // register bits swapped with lane bits: cross-lane moves, no LDS
+          o << "  { const uint32_t ln = opaque(__lane_id());\n";
+          for (const auto& sw : swaps) {
+            o << "    lane_swap<R, " << sw.first << ", " << sw.second << ">(a, ln);\n";
+            if (bwd) o << "    lane_swap<R, " << sw.first << ", " << sw.second << ">(l, ln);\n";
+          }
+          o << "  }\n";
+          break;
+        }
         o << "  { static constexpr uint32_t col[] = {";
         for (int i = 0; i < 2 * k; ++i) o << (i ? "," : "") << hex(p.cols[arg + i]);
         o << "};\n    exchange<R>(a, w.xbuf, w.plane, col, " << k << ", " << t

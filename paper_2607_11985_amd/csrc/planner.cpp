@@ -116,6 +116,9 @@ int emit_exchange(const Mapping& a, const Mapping& b, int k, int R, std::vector<
   const int off = (int)cols.size();
   for (int p = 0; p < k; ++p) cols.push_back(lam[a.p2q[p]]);
   for (int p = 0; p < k; ++p) cols.push_back(lam[b.p2q[p]]);
+  // then where each physical bit's qubit goes (the generated kernels do
+  // exchanges that only swap register bits with lane bits without LDS)
+  for (int p = 0; p < k; ++p) cols.push_back((uint32_t)b.q2p[a.p2q[p]]);
   return off;
 }
 

@@ -540,6 +540,75 @@ __device__ __forceinline__ float dpp_f(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 
+// The value lane (lane ^ 2^J) of the wave holds, for J < 4: lanes 1, 2 and 8
+// apart are one DPP move (quad_perm 1032, quad_perm 2301, row_ror 8), 4 apart
+// two (row_half_mirror, then quad_perm 3210: (i ^ 7) ^ 3 = i ^ 4).  Every lane
+// is a valid source, so no old value is needed.
+template <int CTRL>
+__device__ __forceinline__ float mov_dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+template <int J>
+__device__ __forceinline__ float xlane(float v) {
+  static_assert(J >= 0 && J < 4, "lane bit");
+  if constexpr (J == 0) return mov_dpp_f<0xB1>(v);
+  else if constexpr (J == 1) return mov_dpp_f<0x4E>(v);
+  else if constexpr (J == 2) return mov_dpp_f<0x1B>(mov_dpp_f<0x141>(v));
+  else return mov_dpp_f<0x128>(v);
+}
+
+// Exchange of register bit RB with lane bit J without LDS: the qubit on
+// register bit RB moves to lane bit J and back.  The amplitude at register u,
+// lane L stays where bit RB of u equals bit J of L, and otherwise comes from
+// lane L ^ 2^J, register u ^ 2^RB.  For J = 4 and 5 this is exactly what
+// gfx950's permlane16 / permlane32 swaps do to the pair (a[u0], a[u1]): the
+// odd 16-lane rows (upper 32 lanes) of the first operand trade places with the
+// even rows (lower 32 lanes) of the second.  Below that, a DPP move and a
+// select per value.
+// x where the mask is set, y elsewhere
+__device__ __forceinline__ float bit_select(uint32_t m, float x, float y) {
+  return __uint_as_float((__float_as_uint(x) & m) | (__float_as_uint(y) & ~m));
+}
+
+__device__ __forceinline__ void swap_pair16(float& x0, float& x1) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x0), __float_as_uint(x1), false,
+                                                  false);
+  x0 = __uint_as_float(r[0]);
+  x1 = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void swap_pair32(float& x0, float& x1) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x1), false,
+                                                  false);
+  x0 = __uint_as_float(r[0]);
+  x1 = __uint_as_float(r[1]);
+}
+
+template <int R, int RB, int J>
+__device__ __forceinline__ void lane_swap(St<R>& a, uint32_t lane) {
+#pragma unroll
+  for (int u0 = 0; u0 < St<R>::N; ++u0) {
+    if (u0 & (1 << RB)) continue;
+    const int u1 = u0 | (1 << RB);
+    if constexpr (J == 4) {
+      swap_pair16(a.r[u0], a.r[u1]);
+      swap_pair16(a.i[u0], a.i[u1]);
+    } else if constexpr (J == 5) {
+      swap_pair32(a.r[u0], a.r[u1]);
+      swap_pair32(a.i[u0], a.i[u1]);
+    } else {
+      // a bit-select (one bitfield insert per value): written as a select the
+      // compiler turns the four choices into a divergent branch
+      const uint32_t m = 0u - ((lane >> J) & 1u);
+      const float r0 = xlane<J>(a.r[u1]), i0 = xlane<J>(a.i[u1]);
+      const float r1 = xlane<J>(a.r[u0]), i1 = xlane<J>(a.i[u0]);
+      a.r[u0] = bit_select(m, r0, a.r[u0]);
+      a.i[u0] = bit_select(m, i0, a.i[u0]);
+      a.r[u1] = bit_select(m, a.r[u1], r1);
+      a.i[u1] = bit_select(m, a.i[u1], i1);
+    }
+  }
+}
+
 // Sum over aligned groups of W lanes (W a power of two <= 64).  Every lane of a
 // group ends with the group's sum; the pairing order is fixed, so the result is
 // deterministic.  Pairs, quads, 8- and 16-lane rows use DPP (quad_perm 1032 and
