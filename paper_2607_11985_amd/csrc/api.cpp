@@ -336,7 +336,8 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   vqc_circuit* c = new (std::nothrow) vqc_circuit();
   if (!c) return fail(VQC_ERR_OOM, "out of host memory");
   std::string msg;
-  int rc = vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, reg_bits, c->plan, msg);
+  int rc = vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, reg_bits, c->plan, msg,
+                           engine == VQC_ENGINE_JIT);
   if (rc != 0) {
     delete c;
     return fail(rc, msg);

@@ -432,7 +432,12 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       case OP_CNOT: {
         const char* sts[2] = {"a", "l"};
         for (int s = 0; s < (bwd ? 2 : 1); ++s) {
-          if (pa < R)
+          if (pb >= R)  // target on a lane bit
+            o << (pa < R ? "  cnot_rl<R, " + std::to_string(pa) + ", " + std::to_string(pb - R) +
+                               ">(" + sts[s] + ");\n"
+                         : "  cnot_tl<R, " + std::to_string(pb - R) + ">(" + sts[s] +
+                               ", tile_bit<R>(w, " + std::to_string(pa) + "));\n");
+          else if (pa < R)
             o << "  cnot_rr<R, " << pa << ", " << pb << ">(" << sts[s] << ");\n";
           else
             o << "  cnot_tr<R, " << pb << ">(" << sts[s] << ", tile_bit<R>(w, " << pa << "));\n";
@@ -511,18 +516,27 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           }
         } else {
           o << "  { const float2 cs = w.tab[" << at << "]; ";
+          // RX / RY off the register bits sit on a lane bit (planner option)
+          const std::string lane = std::to_string(pa - R);
+          const std::string hi = "tile_bit<R>(w, " + std::to_string(pa) + ")";
           if (!bwd) {
             if (reg)
               o << kind << "_reg<R, " << pa << ">(a, cs.x, cs.y);";
-            else  // RZ on a thread / tile bit
-              o << "phase_all<R>(a, cs.x, flip_sign(cs.y, (tile_bit<R>(w, " << pa
-                << ") ^ 1u) << 31));";
+            else if (op == OP_RZ)  // RZ on a thread / tile bit
+              o << "phase_all<R>(a, cs.x, flip_sign(cs.y, (" << hi << " ^ 1u) << 31));";
+            else if (op == OP_RX)
+              o << "rx_lane<R, " << lane << ">(a, cs.x, cs.y);";
+            else
+              o << "ry_lane<R, " << lane << ">(a, cs.x, cs.y, " << hi << ");";
           } else {
             if (reg)
               o << "float g = adj_" << kind << "<R, " << pa << ">(a, l, cs.x, cs.y);";
+            else if (op == OP_RZ)
+              o << "float g = adj_rz_uniform<R>(a, l, cs.x, cs.y, " << hi << ");";
+            else if (op == OP_RX)
+              o << "float g = adj_rx_lane<R, " << lane << ">(a, l, cs.x, cs.y);";
             else
-              o << "float g = adj_rz_uniform<R>(a, l, cs.x, cs.y, tile_bit<R>(w, " << pa
-                << "));";
+              o << "float g = adj_ry_lane<R, " << lane << ">(a, l, cs.x, cs.y, " << hi << ");";
             o << occ_scale(p, arg);
           }
         }
@@ -552,7 +566,10 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           o << " }";
         }
         ++m;
-        o << " gate_boundary(w); }\n";
+        // gate by gate instruction selection (see gate_boundary); the small
+        // kernels with gates on lane bits leave the scheduler free instead, so
+        // that the DPP moves fold into the multiplies that use them
+        o << (p.lanes > 0 ? " }\n" : " gate_boundary(w); }\n");
       }
     }
   }

@@ -130,10 +130,12 @@ void emit(std::vector<uint32_t>& out, uint32_t op, int a, int b, int slot, uint3
 // One register-level sweep over `seq` (already in execution order) starting
 // from mapping `m` (updated to the end mapping).  slot_of(occ) gives the
 // gradient accumulator written into rotation instructions.
+// `lanes` > 0: RX / RY and CNOT targets may also act on the first `lanes`
+// thread bits (lane bits of the sample; generated kernels only).
 template <typename SlotFn>
 int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int R, Mapping& m,
                std::vector<uint32_t>& out, std::vector<uint32_t>& cols, int& exchanges,
-               SlotFn slot_of, std::string& msg) {
+               SlotFn slot_of, std::string& msg, int lanes = 0) {
   const std::vector<int> nn = next_need_table(seq, nq);
   for (size_t i = 0; i < seq.size(); ++i) {
     const Prim& pr = seq[i];
@@ -142,13 +144,19 @@ int plan_sweep(const std::vector<Prim>& seq, int nq, int k, int R, Mapping& m,
       msg = "internal: register-bit gate on a global qubit";
       return VQC_ERR_UNSUPPORTED;
     }
-    if (need >= 0 && m.q2p[need] >= R) {
-      // Belady: the register bits get the R local qubits needed soonest.
+    if (need >= 0 && m.q2p[need] >= R + lanes) {
+      // Belady: the register bits get the R local qubits needed soonest.  A
+      // qubit on a lane bit that takes gates needs no register.
       std::vector<int> qs;
       for (int p = 0; p < k; ++p) qs.push_back(m.p2q[p]);
-      const int* row = &nn[i * (size_t)nq];
+      const int* nrow = &nn[i * (size_t)nq];
+      auto row_of = [&](int q) {
+        const int p = m.q2p[q];
+        return (p >= R && p < R + lanes) ? INT_MAX : nrow[q];
+      };
       std::stable_sort(qs.begin(), qs.end(), [&](int x, int y) {
-        if (row[x] != row[y]) return row[x] < row[y];
+        const int rx_need = row_of(x), ry_need = row_of(y);
+        if (rx_need != ry_need) return rx_need < ry_need;
         const bool rx = m.q2p[x] < R, ry = m.q2p[y] < R;
         if (rx != ry) return rx;  // keep residents on ties
         return x < y;
@@ -513,7 +521,7 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 }  // namespace
 
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
-               Plan& plan, std::string& msg) {
+               Plan& plan, std::string& msg, bool lane_gates) {
   if (n < 1 || n > kMaxQubits) {
     msg = "n_qubits must be in [1, " + std::to_string(kMaxQubits) + "]";
     return n < 1 ? VQC_ERR_INVALID_ARG : VQC_ERR_TOO_LARGE;
@@ -642,12 +650,17 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     }
     auto global_slot = [&](int occ) { return plan.occ_slot[occ]; };
     plan.start_off = append_map(m, plan.maps);
+    // gates on lane bits 0..3 (one or two DPP moves per value): generated
+    // kernels with 4 amplitudes per thread, where exchanges are not hidden.
+    // Qubits on lane bits 4 and 5 still come to a register bit, by a permlane
+    // swap (one instruction per two values).
+    plan.lanes = (lane_gates && plan.R <= 2) ? std::min(plan.t, 4) : 0;
     rc = plan_sweep(plan.prims, nq, plan.k, plan.R, m, plan.fwd, plan.cols, plan.fwd_exchanges,
-                    global_slot, msg);
+                    global_slot, msg, plan.lanes);
     if (rc < 0) return rc;
     plan.end_off = append_map(m, plan.maps);
     rc = plan_sweep(rev, nq, plan.k, plan.R, m, plan.bwd, plan.cols, plan.bwd_exchanges,
-                    global_slot, msg);
+                    global_slot, msg, plan.lanes);
     if (rc < 0) return rc;
     // LDS: exchange buffer | angle table [occ][S] | gradient accumulators [slot][G]
     const size_t xbuf = (size_t)plan.WG * ((size_t)1 << plan.R) * 8;

@@ -609,6 +609,107 @@ __device__ __forceinline__ void lane_swap(St<R>& a, uint32_t lane) {
   }
 }
 
+// ------------------------------------------------------- gates on lane bits
+// With 4 amplitudes per thread and every other qubit on a lane bit of the
+// sample, the generated kernels apply RX, RY and CNOT targets on lane bit J
+// directly: the partner amplitude of a pair sits in lane ^ 2^J, same register,
+// and is read with xlane<J> (DPP).  `hi` is the thread's lane bit J.
+
+// RX(theta): both sides of the pair take c a - i s a_partner
+// (the moved value is the first factor of a plain product, so the DPP move
+// folds into the multiply)
+template <int R, int J>
+__device__ __forceinline__ void rx_lane(St<R>& a, float c, float s) {
+  const float ns = -s;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float tr = xlane<J>(a.i[u]) * s, ti = xlane<J>(a.r[u]) * ns;
+    a.r[u] = fmaf(c, a.r[u], tr);
+    a.i[u] = fmaf(c, a.i[u], ti);
+  }
+}
+
+// RY(theta) = [c, -s; s, c]: the side with the bit clear takes c a - s a_partner,
+// the side with it set c a + s a_partner
+template <int R, int J>
+__device__ __forceinline__ void ry_lane(St<R>& a, float c, float s, uint32_t hi) {
+  const float sl = flip_sign(s, (hi ^ 1u) << 31);
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float tr = xlane<J>(a.r[u]) * sl, ti = xlane<J>(a.i[u]) * sl;
+    a.r[u] = fmaf(c, a.r[u], tr);
+    a.i[u] = fmaf(c, a.i[u], ti);
+  }
+}
+
+// Adjoint RX on lane bit J: this lane's share of Im<l|X|a>, then RX(-theta) on
+// both states (c a + i s a_partner).  The share pairs this lane's a with the
+// partner's l (the pair's two terms are split between its lanes either way);
+// the partner's l is needed for the update too, the partner's a only once, in
+// a product the DPP move folds into.
+template <int R, int J>
+__device__ __forceinline__ float adj_rx_lane(St<R>& a, St<R>& l, float c, float s) {
+  float acc = 0.f;
+  const float ns = -s;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
+    const float ar = a.r[u], ai = a.i[u];
+    acc += qr * ai - qi * ar;
+    const float tr = xlane<J>(ai) * ns, ti = xlane<J>(ar) * s;
+    a.r[u] = fmaf(c, ar, tr);
+    a.i[u] = fmaf(c, ai, ti);
+    l.r[u] = fmaf(c, l.r[u], qi * ns);
+    l.i[u] = fmaf(c, l.i[u], qr * s);
+  }
+  return acc;
+}
+
+// Adjoint RY on lane bit J: Im<l|Y|a> over a pair is
+// Re(conj(l1) a0) - Re(conj(l0) a1); the side with the bit clear holds a0 and
+// takes +Re(conj(l_partner) a), the other side -.  RY(-theta) = [c, s; -s, c]
+template <int R, int J>
+__device__ __forceinline__ float adj_ry_lane(St<R>& a, St<R>& l, float c, float s, uint32_t hi) {
+  float acc = 0.f;
+  const float sl = flip_sign(s, hi << 31);
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
+    const float ar = a.r[u], ai = a.i[u];
+    acc += qr * ar + qi * ai;
+    const float tr = xlane<J>(ar) * sl, ti = xlane<J>(ai) * sl;
+    a.r[u] = fmaf(c, ar, tr);
+    a.i[u] = fmaf(c, ai, ti);
+    l.r[u] = fmaf(c, l.r[u], qr * sl);
+    l.i[u] = fmaf(c, l.i[u], qi * sl);
+  }
+  return hi ? -acc : acc;
+}
+
+// CNOT with the target on lane bit J and the control on register bit C: the
+// amplitudes with the control set trade places with the partner lane's
+template <int R, int C, int J>
+__device__ __forceinline__ void cnot_rl(St<R>& a) {
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    if (!(u & (1 << C))) continue;
+    a.r[u] = xlane<J>(a.r[u]);
+    a.i[u] = xlane<J>(a.i[u]);
+  }
+}
+
+// CNOT with the target on lane bit J and the control on a thread / tile bit
+// (the same in both lanes of a pair)
+template <int R, int J>
+__device__ __forceinline__ void cnot_tl(St<R>& a, uint32_t flag) {
+  const uint32_t m = 0u - flag;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    a.r[u] = bit_select(m, xlane<J>(a.r[u]), a.r[u]);
+    a.i[u] = bit_select(m, xlane<J>(a.i[u]), a.i[u]);
+  }
+}
+
 // Sum over aligned groups of W lanes (W a power of two <= 64).  Every lane of a
 // group ends with the group's sum; the pairing order is fixed, so the result is
 // deterministic.  Pairs, quads, 8- and 16-lane rows use DPP (quad_perm 1032 and

@@ -42,6 +42,7 @@ struct Plan {
   int R = kDefaultRegBits;                // register bits of the resident kernels
   int Rf = kStreamRegBitsFwd, Rb = kStreamRegBitsBwd;  // streaming forward / adjoint
   int ng = 0;                             // global (streamed) qubits
+  int lanes = 0;                          // lane bits that take RX / RY / CNOT targets
   int P = 0, F = 0, n_ops = 0, path = 1;
   std::vector<Prim> prims;
   std::vector<int32_t> occ_src, occ_idx, occ_slot;
@@ -67,8 +68,10 @@ struct HostOp {
   float val[3], mul[3];
 };
 constexpr int kNumGateKinds = 32;  // VQC_RX .. VQC_CSWAP
+// lane_gates: the schedule may put RX / RY / CNOT targets on lane bits (only
+// the generated kernels run such schedules).
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
-               Plan& plan, std::string& msg);
+               Plan& plan, std::string& msg, bool lane_gates);
 // OpenQASM front end (qasm.cpp).  Returns 0 or a VQC_ERR_* code with msg.
 int parse_qasm(const char* source, const char* input_names, std::vector<vqc_op>& ops,
                int& n_qubits, int& n_params, int& n_inputs, std::string& msg);
