@@ -70,14 +70,13 @@ std::vector<int> next_need_table(const std::vector<Prim>& seq, int nq) {
 }
 
 // Exchange tables.  The LDS slot of an amplitude is a GF(2)-linear function
-// lam(x) of its tile position.  When the exchange only swaps register bits with
-// thread bits (every exchange the register planner makes), lam is chosen so
-// that the lanes of a 32-lane group hit 32 distinct 8-byte slots modulo 256
-// bytes both when writing in the old layout and when reading in the new one:
-// slot bit i (i < bank bits) = x[old lane-i qubit] xor x[new lane-i qubit] (the
-// second term only when that lane position changes hands), every other qubit
-// gets one high bit.  A general permutation falls back to a layout whose reads
-// are conflict free.
+// lam(x) of its tile position, chosen so that the lanes of a 32-lane group hit
+// 32 distinct banks both when writing in the old layout and when reading in the
+// new one.  With A the qubits on the old layout's first lane bits and B those
+// of the new layout: the qubit of A at lane i gets slot bit i; each qubit of
+// B \ A shares the slot bit of a distinct qubit of A \ B (so the slot bits of B
+// are independent too); every qubit outside A also gets one high bit of its
+// own, which keeps lam invertible (triangular).
 int emit_exchange(const Mapping& a, const Mapping& b, int k, int R, std::vector<uint32_t>& cols) {
   const int t = k - R;
   const int lb = std::min(kBankBits, t);
@@ -90,28 +89,21 @@ int emit_exchange(const Mapping& a, const Mapping& b, int k, int R, std::vector<
     in_a[a.p2q[R + i]] = true;
     in_b[b.p2q[R + i]] = true;
   }
-  bool swap_only = true;
+  std::vector<int> a_only_bit, b_only;
   for (int i = 0; i < lb; ++i) {
-    const int qa = a.p2q[R + i], qb = b.p2q[R + i];
-    if (qa != qb && (in_a[qb] || in_b[qa])) swap_only = false;
+    const int qa = a.p2q[R + i];
+    lam[qa] |= 1u << i;
+    if (!in_b[qa]) a_only_bit.push_back(i);
   }
-  if (swap_only) {
-    for (int i = 0; i < lb; ++i) {
-      const int qa = a.p2q[R + i], qb = b.p2q[R + i];
-      lam[qa] |= 1u << i;
-      if (qb != qa) lam[qb] |= 1u << i;
-    }
-    int nb = lb;
-    for (int p = 0; p < k; ++p) {
-      const int q = a.p2q[p];
-      if (!in_a[q]) lam[q] |= 1u << nb++;
-    }
-  } else {
-    // slot = thread bits of the new layout in the low bits, register bits on top
-    for (int p = 0; p < k; ++p) {
-      const int q = b.p2q[p];
-      lam[q] = 1u << (p >= R ? p - R : t + p);
-    }
+  for (int i = 0; i < lb; ++i) {
+    const int qb = b.p2q[R + i];
+    if (!in_a[qb]) b_only.push_back(qb);
+  }
+  for (size_t j = 0; j < b_only.size(); ++j) lam[b_only[j]] |= 1u << a_only_bit[j];
+  int nb = lb;
+  for (int p = 0; p < k; ++p) {
+    const int q = a.p2q[p];
+    if (!in_a[q]) lam[q] |= 1u << nb++;
   }
   const int off = (int)cols.size();
   for (int p = 0; p < k; ++p) cols.push_back(lam[a.p2q[p]]);
