@@ -141,6 +141,8 @@ def main():
                          "schedule interpreter (interp)")
     ap.add_argument("--reg-bits", type=int, default=0,
                     help="amplitudes per thread = 2^reg_bits (0: the library's default)")
+    ap.add_argument("--tile-qubits", type=int, default=0,
+                    help="streaming tile size, 13 or 14 (0: the library's default)")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP graph replays of the step instead of its launches")
     ap.add_argument("--separate", action="store_true",
@@ -174,7 +176,7 @@ def main():
     B, n = w.batch, w.n_qubits
     t0 = time.time()
     circ = Circuit(w.ops, n, w.n_params, w.n_inputs, device=0, engine=args.engine,
-                   reg_bits=args.reg_bits)
+                   reg_bits=args.reg_bits, tile_qubits=args.tile_qubits)
     compile_s = time.time() - t0
     info = circ.info()
     p = torch.from_numpy(w.params).to(dev)
@@ -324,6 +326,7 @@ def main():
                    "loss": w.loss, "path": "resident" if info["path"] == 1 else "stream",
                    "threads_per_workgroup": info["threads"], "engine": args.engine,
                    "reg_bits": args.reg_bits or "default",
+                   "tile_qubits": circ.info()["tile_qubits"] if circ.info()["path"] == 2 else None,
                    "compile_s": round(compile_s, 2),
                    "exchanges_fwd_bwd": [info["fwd_exchanges"], info["bwd_exchanges"]]},
         "step": ("vqc_forward + vqc_loss_grad + vqc_backward" if args.separate else

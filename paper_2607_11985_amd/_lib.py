@@ -42,7 +42,8 @@ class vqc_op(ctypes.Structure):
 class vqc_compile_opts(ctypes.Structure):
     _fields_ = [("device", ctypes.c_int32), ("path", ctypes.c_int32),
                 ("reg_bits", ctypes.c_int32), ("engine", ctypes.c_int32),
-                ("shared_params", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
+                ("shared_params", ctypes.c_int32), ("tile_qubits", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 2)]
 
 
 class vqc_info(ctypes.Structure):
@@ -151,11 +152,11 @@ def encode_ops(ops) -> ctypes.Array:
 
 def vqc_compile(ops, n_qubits: int, n_params: int, n_inputs: int, device: int = 0,
                 path: int = VQC_PATH_AUTO, reg_bits: int = 0, engine: int = VQC_ENGINE_JIT,
-                shared_params: int = 0):
+                shared_params: int = 0, tile_qubits: int = 0):
     lib = load()
     arr = encode_ops(ops)
     opts = vqc_compile_opts(device=device, path=path, reg_bits=reg_bits, engine=engine,
-                            shared_params=shared_params)
+                            shared_params=shared_params, tile_qubits=tile_qubits)
     h = _vp()
     _check(lib.vqc_compile(arr, len(ops), n_qubits, n_params, n_inputs, ctypes.byref(opts),
                            ctypes.byref(h)))
@@ -186,10 +187,10 @@ def vqc_parse_qasm(source: str, input_names: str | None = None):
 
 def vqc_compile_qasm(source: str, input_names: str | None = None, device: int = 0,
                      path: int = VQC_PATH_AUTO, reg_bits: int = 0, engine: int = VQC_ENGINE_JIT,
-                     shared_params: int = 0):
+                     shared_params: int = 0, tile_qubits: int = 0):
     lib = load()
     opts = vqc_compile_opts(device=device, path=path, reg_bits=reg_bits, engine=engine,
-                            shared_params=shared_params)
+                            shared_params=shared_params, tile_qubits=tile_qubits)
     h = _vp()
     _check(lib.vqc_compile_qasm(source.encode(), input_names.encode() if input_names else None,
                                 ctypes.byref(opts), ctypes.byref(h)))

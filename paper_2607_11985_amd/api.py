@@ -41,7 +41,7 @@ class Circuit:
 
     def __init__(self, ops, n_qubits: int, n_params: int, n_inputs: int, device: int = 0,
                  path: str = "auto", reg_bits: int = 0, engine: str = "jit",
-                 shared_params: bool = False):
+                 shared_params: bool = False, tile_qubits: int = 0):
         self.ops = list(ops)
         self.n = int(n_qubits)
         self.P = int(n_params)
@@ -50,7 +50,8 @@ class Circuit:
         self.device = torch.device("cuda", device)
         self.handle = _lib.vqc_compile(self.ops, self.n, self.P, self.F, device=device,
                                        path=_PATHS[path], reg_bits=reg_bits,
-                                       engine=_ENGINES[engine], shared_params=int(self.shared))
+                                       engine=_ENGINES[engine], shared_params=int(self.shared),
+                                       tile_qubits=tile_qubits)
 
     @classmethod
     def from_qasm(cls, source: str, inputs=(), device: int = 0, path: str = "auto",

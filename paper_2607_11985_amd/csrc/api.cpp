@@ -301,7 +301,7 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   if (n_ops < 0) return fail(VQC_ERR_INVALID_ARG, "n_ops must be >= 0");
   if (n_ops > 0 && !ops) return fail(VQC_ERR_INVALID_ARG, "ops is NULL");
   if (n_ops > (1 << 20)) return fail(VQC_ERR_TOO_LARGE, "more than 2^20 gates");
-  int device = 0, path = VQC_PATH_AUTO, reg_bits = 0, engine = VQC_ENGINE_JIT;
+  int device = 0, path = VQC_PATH_AUTO, reg_bits = 0, engine = VQC_ENGINE_JIT, tile = 0;
   bool shared = false;
   if (opts) {
     for (int r : opts->reserved)
@@ -315,6 +315,11 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
     if (opts->shared_params != 0 && opts->shared_params != 1)
       return fail(VQC_ERR_INVALID_ARG, "shared_params must be 0 or 1");
     shared = opts->shared_params == 1;
+    tile = opts->tile_qubits;
+    if (tile != 0 && tile != 13 && tile != 14)
+      return fail(VQC_ERR_INVALID_ARG, "tile_qubits must be 0 (default), 13 or 14");
+    if (tile == 13 && engine != VQC_ENGINE_JIT)
+      return fail(VQC_ERR_UNSUPPORTED, "13-qubit tiles need the generated kernels");
     if (path < VQC_PATH_AUTO || path > VQC_PATH_STREAM)
       return fail(VQC_ERR_INVALID_ARG, "unknown path option");
   } else if (hipGetDevice(&device) != hipSuccess) {
@@ -337,7 +342,7 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   if (!c) return fail(VQC_ERR_OOM, "out of host memory");
   std::string msg;
   int rc = vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, reg_bits, c->plan, msg,
-                           engine == VQC_ENGINE_JIT);
+                           engine == VQC_ENGINE_JIT, tile);
   if (rc != 0) {
     delete c;
     return fail(rc, msg);

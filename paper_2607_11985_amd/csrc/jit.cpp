@@ -627,7 +627,7 @@ std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
     << (stream ? "(const vqc::PassArgs A) {\n" : "(const vqc::TileArgs A) {\n")
     << "  __shared__ __align__(16) unsigned char smem[" << lds_size(tm.on ? tm.end : lds) << "];\n";
   if (stream)
-    o << "  vqc::stream_body<" << (bwd ? "true" : "false") << ", " << R
+    o << "  vqc::stream_body<" << (bwd ? "true" : "false") << ", " << R << ", " << p.k
       << ", vqc::Sched>(A, smem);\n}\n";
   else
     o << "  vqc::resident_body<" << threads << ", " << (bwd ? "true" : "false") << ", " << R

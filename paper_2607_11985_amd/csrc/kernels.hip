@@ -25,7 +25,7 @@ __global__ void __launch_bounds__(WG) resident_step_kernel(const TileArgs A) {
 template <bool BWD, int R>
 __global__ void __launch_bounds__(1 << (kMaxTileQubits - R)) stream_kernel(const PassArgs A) {
   extern __shared__ __align__(16) unsigned char smem[];
-  stream_body<BWD, R, InterpSched>(A, smem);
+  stream_body<BWD, R, kMaxTileQubits, InterpSched>(A, smem);
 }
 
 __global__ void reduce_e_kernel(int64_t B, int ng, int n, const float* __restrict__ epart,

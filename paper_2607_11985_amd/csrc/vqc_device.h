@@ -1335,9 +1335,10 @@ __device__ __forceinline__ void load_tile(St<R>& a, const float2* src, uint32_t 
   for (int j = 0; j < (1 << R); ++j) split(v[j], a.r[j], a.i[j]);
 }
 
-template <bool BWD, int R, typename Sched>
+template <bool BWD, int R, int K, typename Sched>
 __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* smem) {
-  constexpr int WG = 1 << (kMaxTileQubits - R);
+  static_assert(K <= kMaxTileQubits && K - R >= 6, "tile shape");
+  constexpr int WG = 1 << (K - R);
   constexpr int NA = 1 << R;
   constexpr int G = WG / 64;
   float* xbuf = reinterpret_cast<float*>(smem);

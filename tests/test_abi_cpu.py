@@ -62,8 +62,10 @@ def test_configs_plan_on_host(idx):
     assert info["n_rotations"] == rot and info["n_ops"] == nops
     stream = w.n_qubits >= 14
     assert info["path"] == (_lib.VQC_PATH_STREAM if stream else _lib.VQC_PATH_RESIDENT)
-    assert info["tile_qubits"] == (14 if stream else max(4, w.n_qubits))
-    if w.n_qubits > 14:
+    # the streaming path uses 13-qubit tiles (two workgroups per CU)
+    tile = 13 if stream else max(4, w.n_qubits)
+    assert info["tile_qubits"] == tile
+    if w.n_qubits >= 14:
         assert info["fwd_passes"] > 1 and info["bwd_passes"] > 1
     assert info["lds_bytes_bwd"] <= 160 * 1024
     # forward and backward sweep each hold one instruction per primitive plus exchanges
@@ -197,7 +199,8 @@ def test_random_circuits_plan(n):
     info = _lib.vqc_circuit_info(h)
     nq = max(n, 4)
     R = 2 if nq <= 8 else 3 if nq <= 10 else 4
-    assert info["threads"] == max(64, 1 << (nq - R))
+    k = 13 if nq >= 14 else nq  # streamed from 14 qubits, in 13-qubit tiles
+    assert info["threads"] == max(64, 1 << (k - R))
     _lib.vqc_destroy(h)
 
 
@@ -303,3 +306,22 @@ def test_shared_params_workspace(idx):
     assert sizes[1][0] == sizes[0][0]
     for m in (1, 2):
         assert sizes[1][m] >= sizes[0][m] + 10 * w.n_params * 4
+
+
+def test_tile_qubits_option():
+    ops, P, F = W.random_circuit(15, 20, seed=5)
+    arr = _lib.encode_ops(ops)
+    for tq, code in ((12, _lib.VQC_ERR_INVALID_ARG), (15, _lib.VQC_ERR_INVALID_ARG)):
+        rc, _ = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
+                                     _lib.vqc_compile_opts(device=-1, tile_qubits=tq))
+        assert rc == code and "tile_qubits" in _lib.vqc_last_error()
+    rc, _ = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
+                                 _lib.vqc_compile_opts(device=-1, tile_qubits=13, engine=1))
+    assert rc == _lib.VQC_ERR_UNSUPPORTED
+    rc, h = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
+                                 _lib.vqc_compile_opts(device=-1, tile_qubits=13))
+    assert rc == 0
+    info = _lib.vqc_circuit_info(h)
+    assert info["tile_qubits"] == 13 and info["threads"] == 512 and info["path"] == 2
+    _lib.vqc_jit_check(h)
+    _lib.vqc_destroy(h)
