@@ -308,7 +308,7 @@ int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, int R,
     if (passes.empty()) pp.flags |= bwd ? PF_MAKE_LAMBDA : PF_INIT;
     passes.push_back(pp);
   } while (remaining > 0);
-  if (!bwd) passes.back().flags |= PF_ZPART;
+  passes.back().flags |= bwd ? PF_LAST_ADJ : PF_ZPART;
   return 0;
 }
 

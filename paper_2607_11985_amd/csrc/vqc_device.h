@@ -1404,15 +1404,19 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   Sched::template run<R, BWD, true>(a, l, w, A.ins, A.n_ins);
 
   base = opaque(base);
-  {
+  // the adjoint's last pass ends at psi_0: its states are not needed
+  const bool store = !BWD || !(A.flags & PF_LAST_ADJ);
+  if (store) {
     float2* dst = reinterpret_cast<float2*>(A.psi_dst) + sbase;
 #pragma unroll
     for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(a.r[j], a.i[j]);
   }
   if (BWD) {
-    float2* dst = reinterpret_cast<float2*>(A.lam_dst) + sbase;
+    if (store) {
+      float2* dst = reinterpret_cast<float2*>(A.lam_dst) + sbase;
 #pragma unroll
-    for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(l.r[j], l.i[j]);
+      for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(l.r[j], l.i[j]);
+    }
     __syncthreads();
     float* gp = A.gpart + blk * A.n_slots;
     for (int i = tid; i < A.n_pslots; i += WG) {

@@ -60,6 +60,7 @@ enum PassFlag : int32_t {
   PF_INIT = 1,        // start from |0...0> instead of loading psi
   PF_MAKE_LAMBDA = 2, // (adjoint) lambda = H psi after loading psi_G
   PF_ZPART = 4,       // (forward) per-tile <Z> partial sums
+  PF_LAST_ADJ = 8,    // (adjoint) the last pass: psi and lambda are not stored
 };
 
 // Arguments of the resident kernels (one launch, whole sample on chip).
