@@ -135,7 +135,6 @@ std::vector<int> stream_rotations(const uint32_t* ins, int n_ins) {
   return occ;
 }
 
-int n_blocks(size_t rotations) { return (int)((rotations + kBlock - 1) / kBlock); }
 
 // Tables of one kernel, in LDS after the kernel's own layout.
 struct TanMode {
@@ -143,7 +142,7 @@ struct TanMode {
   int W = 0;
   std::vector<int> focc, bocc;  // rotations of the forward / adjoint stream, in stream order
   bool esign = false;
-  size_t off_bits = 0, off_gm = 0, off_es = 0, off_fs = 0, off_bs = 0, end = 0;
+  size_t off_bits = 0, off_gm = 0, off_es = 0, end = 0;
 };
 
 size_t align16(size_t v) { return (v + 15) / 16 * 16; }
@@ -163,10 +162,6 @@ TanMode tan_mode(const Plan& p, const uint32_t* fins, int fn, const uint32_t* bi
   if (bins) off = align16(off + (size_t)nocc * 4);
   t.off_es = off;
   if (esign) off = align16(off + (size_t)p.n * 4);
-  t.off_fs = off;
-  off = align16(off + (size_t)n_blocks(t.focc.size()) * 4);
-  t.off_bs = off;
-  off = align16(off + (size_t)n_blocks(t.bocc.size()) * 4);
   t.end = off;
   t.on = S == 1 && t.end <= (size_t)kLdsBytes;
   return t;
@@ -182,9 +177,9 @@ void emit_array(std::ostringstream& o, const char* type, const char* name, const
 
 // prepare(): (cos, sin)(theta/2) -> (t, cos phi') in place with the parity bits
 // (one ballot per 64 occurrences), then in one round over the streams'
-// rotations: the frame sign of each (t negated in place, once), the adjoint's
-// gradient factor (sign x square of the block's factors before it) and the
-// block factors; and the <Z> signs.  esigns(): those signs.
+// rotations: the frame sign of each (t negated in place, once) and the sign
+// of the adjoint's gradients; and the <Z> signs.  esigns(): those signs.  The
+// block factors are products the schedule forms as it goes (bp).
 void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const Frame& fr) {
   const int nocc = (int)p.occ_src.size(), W = t.W;
   o << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt) {\n";
@@ -221,29 +216,19 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
   emit_array(o, "uint16_t", "kOcc", inst);
   emit_array(o, "uint32_t", "kArow", rows);
   o << "  float* gm = reinterpret_cast<float*>(w.smem + " << t.off_gm << "u);\n"
-    << "  float* fs = reinterpret_cast<float*>(w.smem + " << t.off_fs << "u);\n"
-    << "  float* bs = reinterpret_cast<float*>(w.smem + " << t.off_bs << "u);\n"
-    << "  (void)gm; (void)fs; (void)bs;\n"
+    << "  (void)gm;\n"
     << "  for (int i = tid; i < " << ni << "; i += nt) {\n"
     << "    const bool f = i < " << nf << ";\n"
-    << "    const int m = f ? i : i - " << nf << ", base = f ? 0 : " << nf << ";\n"
-    << "    const int k = kOcc[i], b0 = m - m % " << kBlock << ";\n"
+    << "    const int k = kOcc[i];\n"
     << "    uint32_t par = 0u;\n"
     << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & kArow[i * " << W
     << " + j]);\n"
-    << "    float pr = 1.f;\n"
-    << "#pragma unroll 8\n"
-    << "    for (int j = b0; j < m; ++j) pr *= tab[kOcc[base + j]].y;\n"
-    << "    const bool last = m % " << kBlock << " == " << kBlock - 1 << " || m == (f ? "
-    << nf << " : " << ni - nf << ") - 1;\n"
     << "    if (f) {\n"
     << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n"
-    << "      if (last) fs[m / " << kBlock << "] = pr * tab[k].y;\n"
     << "    } else {\n";
   if (nf == 0)  // a lone adjoint stream applies the signs itself
     o << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n";
-  o << "      gm[k] = (par & 1u) ? -pr * pr : pr * pr;\n"
-    << "      if (last) bs[m / " << kBlock << "] = pr * tab[k].y;\n"
+  o << "      gm[k] = (par & 1u) ? -1.f : 1.f;\n"
     << "    }\n"
     << "  }\n";
   if (t.esign) {
@@ -399,9 +384,8 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
          "pd14 = 0.f, pd15 = 0.f;\n";
   if (tan && bwd)
     o << "  const float* gmul = reinterpret_cast<const float*>(w.smem + " << tm.off_gm << "u);\n";
-  if (tan)
-    o << "  const float* bscale = reinterpret_cast<const float*>(w.smem + "
-      << (bwd ? tm.off_bs : tm.off_fs) << "u);\n";
+  if (tan)  // product of the factors cos(phi') of the current block so far
+    o << "  float bp = 1.f;\n";
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
     const int op = w0 & 31, pa = (w0 >> 5) & 31, pb = (w0 >> 10) & 31;
@@ -500,7 +484,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         }
         const std::string at = std::to_string(arg) + " * " + std::to_string(S) + " + w.sl";
         if (tan) {
-          o << "  { const float t = w.tab[" << arg << "].x; ";
+          o << "  { const float2 tc = w.tab[" << arg << "]; const float t = tc.x; ";
           if (!bwd) {
             if (reg)
               o << kind << "_t<R, " << pa << ">(a, t);";
@@ -511,9 +495,11 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
               o << "float g = adj_" << kind << "_t<R, " << pa << ">(a, l, t);";
             else
               o << "float g = adj_phase_t<R>(a, l, t, tile_bit<R>(w, " << pa << "));";
-            o << " g *= gmul[" << arg << "];";
+            // the states carry 1 / (the factors of the block before this gate)
+            o << " g *= gmul[" << arg << "] * (bp * bp);";
             o << occ_scale(p, arg);
           }
+          o << " bp *= tc.y;";
         } else {
           o << "  { const float2 cs = w.tab[" << at << "]; ";
           // RX / RY off the register bits sit on a lane bit (planner option)
@@ -561,9 +547,9 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
               << slot << " * w.G + w.grp], gs); }";
         }
         if (tan && (m % kBlock == kBlock - 1 || m == nrot - 1)) {
-          o << " { const float f = bscale[" << m / kBlock << "]; rescale<R>(a, f);";
-          if (bwd) o << " rescale<R>(l, f);";
-          o << " }";
+          o << " rescale<R>(a, bp);";
+          if (bwd) o << " rescale<R>(l, bp);";
+          o << " bp = 1.f;";
         }
         ++m;
         // gate by gate instruction selection (see gate_boundary); the small
