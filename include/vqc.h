@@ -222,7 +222,7 @@ void vqc_destroy(vqc_circuit *c);
  *   training = 1: a training vqc_forward (the saved final states) and the
  *                 vqc_backward calls that use it (plus their scratch);
  *   training = 2: vqc_train_step;
- *   training = 3: vqc_fd_backward (0 off the resident path).
+ *   training = 3: vqc_fd_backward.
  * 0 means no workspace is needed.  Returns (size_t)-1 on invalid arguments.
  */
 size_t vqc_workspace_bytes(const vqc_circuit *c, int64_t batch, int32_t training);
@@ -324,12 +324,13 @@ int vqc_train_step(const vqc_circuit *c, int64_t batch, const float *params, con
  * the "no autograd" ablation of Sec. 4.2.4; kept to compare the mechanisms):
  * for every sample, parameter and input s,
  *   d L / d s = sum_q g[b,q] (E_q(s + h) - E_q(s - h)) / (2 h),
- * from 2 (P + F) shifted forward evaluations per sample run as one batch.
- * Resident path only (VQC_ERR_UNSUPPORTED otherwise).  h > 0.  workspace:
- * vqc_workspace_bytes(c, batch, 3) bytes (the shifted copies' E rows),
- * 256-byte aligned.  Outputs and shared_params as in vqc_backward.
- * Errors: VQC_ERR_INVALID_ARG, VQC_ERR_UNSUPPORTED, VQC_ERR_TOO_LARGE,
- * VQC_ERR_WORKSPACE, VQC_ERR_HIP.
+ * from 2 (P + F) shifted forward evaluations per sample, run as one batch on
+ * the resident path and, on the streaming path, as one batch per chunk of
+ * slots (as many slots as keep the shifted copies' states within 2 GiB).
+ * h > 0.  workspace: vqc_workspace_bytes(c, batch, 3) bytes (the shifted
+ * copies' E rows, and their states when streaming), 256-byte aligned.
+ * Outputs and shared_params as in vqc_backward.  Errors: VQC_ERR_INVALID_ARG,
+ * VQC_ERR_TOO_LARGE, VQC_ERR_WORKSPACE, VQC_ERR_HIP.
  */
 int vqc_fd_backward(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,
                     const float *grad_out, float h, void *workspace, size_t workspace_bytes,

@@ -191,7 +191,7 @@ class Circuit:
 
 
     def fd_backward(self, params, inputs, grad_out, h: float = 1e-2):
-        """Central-difference gradients (the paper's FD mode), resident path only."""
+        """Central-difference gradients (the paper's FD mode)."""
         B = int(grad_out.shape[0])
         params = self._params(params, B)
         inputs = _as_rows(inputs, B, self.F, self.device, "inputs")

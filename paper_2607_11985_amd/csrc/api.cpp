@@ -105,19 +105,35 @@ size_t shared_rows_offset(const Plan& p, int64_t batch, int mode) {
   return align_up(required_bytes_core(p, batch, mode), 256);
 }
 
-// Central differences (mode 3, resident path): the shifted copies' E rows
-// [B * 2 (P + F), n], then (shared parameters) the per-sample rows.
+// Central differences (mode 3).  Slots are taken in chunks of fd_chunk (all
+// of them on the resident path; on the streaming path as many as keep the
+// shifted copies' states within 2 GiB).  Workspace: [streaming: the states and
+// partials of one chunk's forward | the chunk's E rows [B * 2 chunk, n] |
+// (shared parameters) the per-sample rows [B, P]].
+constexpr size_t kFdStateBudget = size_t(2) << 30;
+
+int fd_chunk(const Plan& p, int64_t batch) {
+  const int NS = p.P + p.F;
+  if (p.path == VQC_PATH_RESIDENT || NS == 0 || batch == 0) return NS;
+  const size_t per_slot = (size_t)batch * 2 * ((size_t)1 << p.nq) * 8;
+  const size_t c = kFdStateBudget / per_slot;
+  return (int)std::max<size_t>(1, std::min<size_t>(c, (size_t)NS));
+}
+
+size_t fd_states_bytes(const Plan& p, int64_t batch) {
+  if (p.path == VQC_PATH_RESIDENT) return 0;
+  return required_bytes_core(p, batch * 2 * fd_chunk(p, batch), 0);
+}
+
 size_t fd_rows_bytes(const Plan& p, int64_t batch) {
-  return align_up((size_t)batch * 2 * (p.P + p.F) * p.n * 4, 256);
+  return fd_states_bytes(p, batch) +
+         align_up((size_t)batch * 2 * fd_chunk(p, batch) * p.n * 4, 256);
 }
 
 size_t required_bytes(const vqc_circuit* c, int64_t batch, int mode) {
   const Plan& p = c->plan;
   if (batch == 0) return 0;
-  if (mode == 3) {
-    if (p.path != VQC_PATH_RESIDENT) return 0;
-    return fd_rows_bytes(p, batch) + (c->shared ? (size_t)batch * p.P * 4 : 0);
-  }
+  if (mode == 3) return fd_rows_bytes(p, batch) + (c->shared ? (size_t)batch * p.P * 4 : 0);
   if (!c->shared || mode == 0 || p.P == 0) return required_bytes_core(p, batch, mode);
   return shared_rows_offset(p, batch, mode) + (size_t)batch * p.P * 4;
 }
@@ -222,10 +238,11 @@ int check_workspace(const void* workspace, size_t bytes, size_t need, const char
 }
 
 // Streaming forward: every pass (the first starts from |0...0> or reads psi0),
-// then the <Z> reduction into expvals; the last pass writes probs.
+// then the <Z> reduction into expvals; the last pass writes probs.  fd_slots > 0:
+// the batch is the central differences' shifted copies of slots fd_base ..
 int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
                    float* expvals, unsigned char* ws, void* stream, const void* psi0 = nullptr,
-                   float* probs = nullptr) {
+                   float* probs = nullptr, int fd_base = 0, int fd_slots = 0, float fd_h = 0.f) {
   const Plan& p = c->plan;
   const StreamLayout L = stream_layout(p, batch);
   int rc = 0;
@@ -241,6 +258,9 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
       a.psi_src = psi0;
     }
     if (a.flags & vqc::PF_ZPART) a.probs = probs;
+    a.fd_base = fd_base;
+    a.fd_slots = fd_slots;
+    a.fd_h = fd_h;
     a.epart = reinterpret_cast<float*>(ws + L.epart);
     rc = c->engine == VQC_ENGINE_JIT
              ? vqc::jit_launch(c->jit.pass_fwd[i], batch << p.ng, 1 << (p.k - p.Rf), &a, sizeof(a),
@@ -609,14 +629,13 @@ int vqc_fd_backward(const vqc_circuit* c, int64_t batch, const float* params, co
   if (rc) return rc;
   const Plan& p = c->plan;
   if (!(h > 0.f) || !std::isfinite(h)) return fail(VQC_ERR_INVALID_ARG, "h must be finite and > 0");
-  if (p.path != VQC_PATH_RESIDENT)
-    return fail(VQC_ERR_UNSUPPORTED, "central differences run on the resident path only");
   if ((rc = check_batch(c, batch))) return rc;
   const int NS = p.P + p.F;
   if (batch == 0 || NS == 0) return VQC_OK;
   if ((rc = check_rows(c, params, inputs))) return rc;
   if (!grad_out) return fail(VQC_ERR_INVALID_ARG, "grad_out is NULL");
-  const int64_t virt = batch * 2 * NS;
+  const int chunk = fd_chunk(p, batch);
+  const int64_t virt = batch * 2 * chunk;
   if ((rc = check_batch(c, virt))) return rc;
   if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(c, batch, 3),
                             "workspace smaller than vqc_workspace_bytes(c, batch, 3)")))
@@ -624,10 +643,27 @@ int vqc_fd_backward(const vqc_circuit* c, int64_t batch, const float* params, co
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
   unsigned char* ws = static_cast<unsigned char*>(workspace);
-  float* ev = reinterpret_cast<float*>(ws);
+  float* ev = reinterpret_cast<float*>(ws + fd_states_bytes(p, batch));
   float* dp = p.P > 0 ? dparams : nullptr;
   float* dx = p.F > 0 ? dinputs : nullptr;
   float* rows = (c->shared && dp) ? reinterpret_cast<float*>(ws + fd_rows_bytes(p, batch)) : nullptr;
+  if (p.path == VQC_PATH_STREAM) {
+    // one forward over the shifted copies of each chunk of slots, then its
+    // differences
+    for (int base = 0; base < NS; base += chunk) {
+      const int cs = std::min(chunk, NS - base);
+      const int64_t vb = batch * 2 * cs;
+      if ((rc = stream_forward(c, vb, params, inputs, ev, ws, stream, nullptr, nullptr, base, cs,
+                               h)))
+        return rc;
+      rc = vqc::launch_fd_combine(batch, cs, base, p.P, p.F, p.n, h, ev, grad_out,
+                                  rows ? rows : dp, dx, stream);
+      if (rc) return hip_fail("difference launch", rc);
+    }
+    if (rows && (rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream)))
+      return hip_fail("parameter gradient sum", rc);
+    return VQC_OK;
+  }
   vqc::TileArgs a = tile_args(c, false, virt);
   a.params = params;
   a.inputs = inputs;
@@ -638,7 +674,8 @@ int vqc_fd_backward(const vqc_circuit* c, int64_t batch, const float* params, co
            ? vqc::jit_launch(c->jit.res_fwd, resident_blocks(p, virt), p.WG, &a, sizeof(a), stream)
            : vqc::launch_resident_forward(p, a, resident_blocks(p, virt), stream);
   if (rc) return hip_fail("shifted forward launch", rc);
-  rc = vqc::launch_fd_combine(batch, NS, p.P, p.n, h, ev, grad_out, rows ? rows : dp, dx, stream);
+  rc = vqc::launch_fd_combine(batch, NS, 0, p.P, p.F, p.n, h, ev, grad_out, rows ? rows : dp, dx,
+                              stream);
   if (rc) return hip_fail("difference launch", rc);
   if (rows && (rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream)))
     return hip_fail("parameter gradient sum", rc);

@@ -217,10 +217,15 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
   emit_array(o, "uint32_t", "kArow", rows);
   o << "  float* gm = reinterpret_cast<float*>(w.smem + " << t.off_gm << "u);\n"
     << "  (void)gm;\n"
-    << "  for (int i = tid; i < " << ni << "; i += nt) {\n"
+    // a constant trip count, so that the rounds' table loads issue together
+    << "#pragma unroll\n"
+    << "  for (int i0 = 0; i0 < " << ni << "; i0 += nt) {\n"
+    << "    const int i = i0 + tid;\n"
+    << "    if (i < " << ni << ") {\n"
     << "    const bool f = i < " << nf << ";\n"
     << "    const int k = kOcc[i];\n"
     << "    uint32_t par = 0u;\n"
+    << "#pragma unroll\n"
     << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & kArow[i * " << W
     << " + j]);\n"
     << "    if (f) {\n"
@@ -229,6 +234,7 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
   if (nf == 0)  // a lone adjoint stream applies the signs itself
     o << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n";
   o << "      gm[k] = (par & 1u) ? -1.f : 1.f;\n"
+    << "    }\n"
     << "    }\n"
     << "  }\n";
   if (t.esign) {
@@ -593,7 +599,9 @@ size_t lds_size(size_t b) { return b < 16 ? 16 : b; }
 
 // Whether a kernel uses the tangent form: one sample per workgroup, and enough
 // work per launch that the tables' set-up latency pays off (the 4-amplitude
-// kernels of small states are latency-bound and keep the (cos, sin) form).
+// kernels of small states are latency-bound and keep the (cos, sin) form;
+// measured with gates on lane bits too: no faster).  Lane-bit gates come only
+// with 4 amplitudes per thread, so the tangent schedule never meets them.
 bool tangent_wanted(int S, int R) { return S == 1 && R >= 3; }
 
 // One kernel in a program of its own, so that the kernels of a circuit compile

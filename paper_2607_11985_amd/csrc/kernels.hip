@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(256) sum_rows_kernel(int64_t B, int P,
 
 // Central differences: d L / d slot s of row b = sum_q g[b,q] (E(+h) - E(-h)) / 2h,
 // with the shifted copies laid out as the forward's fd_slots mode writes them.
-__global__ void fd_combine_kernel(int64_t B, int NS, int P, int n, float h,
+__global__ void fd_combine_kernel(int64_t B, int NS, int base, int P, int F, int n, float h,
                                   const float* __restrict__ ev, const float* __restrict__ g,
                                   float* __restrict__ dparams, float* __restrict__ dinputs) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -88,10 +88,11 @@ __global__ void fd_combine_kernel(int64_t B, int NS, int P, int n, float h,
   float v = 0.f;
   for (int q = 0; q < n; ++q) v += gb[q] * (ep[q] - em[q]);
   v /= 2.f * h;
-  if (s < P) {
-    if (dparams) dparams[b * P + s] = v;
+  const int slot = base + s;
+  if (slot < P) {
+    if (dparams) dparams[b * P + slot] = v;
   } else if (dinputs) {
-    dinputs[b * (NS - P) + (s - P)] = v;
+    dinputs[b * F + (slot - P)] = v;
   }
 }
 
@@ -235,11 +236,12 @@ int launch_sum_rows(int64_t batch, int P, const float* rows, float* out, void* s
   return (int)hipGetLastError();
 }
 
-int launch_fd_combine(int64_t batch, int NS, int P, int n, float h, const float* ev,
-                      const float* g, float* dparams, float* dinputs, void* stream) {
+int launch_fd_combine(int64_t batch, int NS, int base, int P, int F, int n, float h,
+                      const float* ev, const float* g, float* dparams, float* dinputs,
+                      void* stream) {
   if (batch * NS == 0) return 0;
   hipLaunchKernelGGL(fd_combine_kernel, dim3(grid_1d(batch * NS, 256)), dim3(256), 0,
-                     (hipStream_t)stream, batch, NS, P, n, h, ev, g, dparams, dinputs);
+                     (hipStream_t)stream, batch, NS, base, P, F, n, h, ev, g, dparams, dinputs);
   return (int)hipGetLastError();
 }
 

@@ -887,14 +887,15 @@ __device__ __forceinline__ void run_schedule(St<R>& a, St<R>& l, const uint32_t*
 // occ_ma is null).  Constant angles come precomputed from the compile phase.
 // fd_slots > 0 (central differences): sample bb of the launch is the shifted
 // copy r = bb mod (2 fd_slots) of input row bb / (2 fd_slots), in which slot
-// r / 2 (a parameter, then an input) is moved by +fd_h (r even) or -fd_h.
+// fd_base + r / 2 (parameters, then inputs) is moved by +fd_h (r even) or
+// -fd_h.
 __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64_t b0, int64_t B,
                                             const int32_t* occ_src, const int32_t* occ_idx,
                                             const float* occ_cs, const float* occ_ma,
                                             const float* params, int P,
                                             const float* inputs, int F, int tid, int nthreads,
                                             int n_params = 0, int fd_slots = 0,
-                                            float fd_h = 0.f) {
+                                            float fd_h = 0.f, int fd_base = 0) {
   for (int i = tid; i < n_occ * S; i += nthreads) {
     const int o = i / S;
     const int s = i - o * S;
@@ -914,7 +915,7 @@ __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64
           row = bb / per;
           const int r = (int)(bb - row * per);
           const int slot = src == kSrcParam ? occ_idx[o] : n_params + occ_idx[o];
-          if (slot == (r >> 1)) shift = (r & 1) ? -fd_h : fd_h;
+          if (slot == fd_base + (r >> 1)) shift = (r & 1) ? -fd_h : fd_h;
         }
         th = (src == kSrcParam ? params[row * P + occ_idx[o]] : inputs[row * F + occ_idx[o]]) +
              shift;
@@ -1369,8 +1370,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
   angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params,
-              A.pstride, A.inputs,
-              A.F, tid, WG);
+              A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots, A.fd_h, A.fd_base);
   if (BWD)
     for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
   __syncthreads();

@@ -88,8 +88,10 @@ int launch_reduce_e(int64_t batch, int ng, int n, const float* epart, float* e, 
 int launch_reduce_grad(int64_t batch, int ng, int n_slots, int P, int F, const float* gpart,
                        float* dparams, float* dinputs, void* stream);
 int launch_fill_zero(float* p, int64_t count, void* stream);
-int launch_fd_combine(int64_t batch, int NS, int P, int n, float h, const float* ev,
-                      const float* g, float* dparams, float* dinputs, void* stream);
+// slots base .. base + NS - 1 of the central differences; ev [batch][NS][2][n]
+int launch_fd_combine(int64_t batch, int NS, int base, int P, int F, int n, float h,
+                      const float* ev, const float* g, float* dparams, float* dinputs,
+                      void* stream);
 // out[p] = sum over b of rows[b * P + p], in a fixed order
 int launch_sum_rows(int64_t batch, int P, const float* rows, float* out, void* stream);
 int launch_loss_grad(int kind, int64_t batch, int n, const float* e, const float* y, float* g,

@@ -136,5 +136,8 @@ struct PassArgs {
   const float* grad_out;
   uint32_t lds_tab, lds_acc;
   float* probs;                // (last forward pass) [B][2^n] probabilities, or null
+  // central differences: B counts shifted copies, 2 per slot of the chunk
+  int32_t fd_slots, fd_base;   // slots fd_base .. fd_base + fd_slots - 1, or fd_slots 0
+  float fd_h;
 };
 }  // namespace vqc

@@ -294,7 +294,8 @@ def test_shared_params_parity(torch_mod, n, path, engine):
 
 @pytest.mark.parametrize("n,engine,shared", [(4, "jit", False), (9, "jit", False),
                                              (12, "jit", False), (7, "interp", False),
-                                             (10, "jit", True)])
+                                             (10, "jit", True), (15, "jit", False),
+                                             (14, "interp", True)])
 def test_fd_backward(torch_mod, n, engine, shared):
     """Central differences through the shifted-batch forward, against the
     oracle's exact gradient.  Bound: truncation h^2/6 times the third
@@ -331,6 +332,29 @@ def test_fd_backward(torch_mod, n, engine, shared):
     assert np.all(np.abs(dp.cpu().numpy().reshape(dpr.shape) - dpr) <= bound)
     gsx = np.sum(np.abs(cot), axis=1, keepdims=True)
     assert np.all(np.abs(dx.cpu().numpy() - dxr) <= (h * h / 6 * k ** 3 + 2e-5 / h) * gsx)
+
+
+def test_fd_backward_streaming_chunks(torch_mod):
+    """The 16-qubit workload's structure at B = 64: the shifted copies of all
+    400 slots (51 GiB of states) run in chunks of 32 slots; sampled rows against
+    the oracle's exact gradient, with the bound of test_fd_backward."""
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit
+    w = W.make_config(5, batch=64)
+    rows = [0, 63]
+    note(f"fd backward streaming chunks {w.name} B={w.batch}")
+    c = Circuit(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    cot = W.random_cotangent(w.batch, w.n_qubits, seed=9600)
+    h = 1e-2
+    dp, dx = c.fd_backward(torch.from_numpy(w.params).cuda(), torch.from_numpy(w.inputs).cuda(),
+                           torch.from_numpy(cot).cuda(), h=h)
+    torch.cuda.synchronize()
+    dpr, dxr, _ = oracle.vjp(w.ops, w.n_qubits, w.params[rows], w.inputs[rows], cot[rows])
+    k = 1  # every parameter and input is used by one gate
+    gs = np.sum(np.abs(cot[rows]), axis=1, keepdims=True)
+    bound = (h * h / 6 * k ** 3 + 2e-5 / h) * gs
+    assert np.all(np.abs(dp.cpu().numpy()[rows] - dpr) <= bound)
+    assert np.all(np.abs(dx.cpu().numpy()[rows] - dxr) <= bound)
 
 
 def test_loss_grad_kernel(torch_mod):
