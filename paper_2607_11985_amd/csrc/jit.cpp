@@ -392,6 +392,17 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
     o << "  const float* gmul = reinterpret_cast<const float*>(w.smem + " << tm.off_gm << "u);\n";
   if (tan)  // product of the factors cos(phi') of the current block so far
     o << "  float bp = 1.f;\n";
+  // one sample per workgroup: the (cos, sin) table in registers (table_row)
+  const bool sreg = !tan && S == 1;
+  if (sreg) {
+    int last = -1;
+    for (int pc = 0; pc < n_ins; ++pc) {
+      const int op = ins[2 * pc] & 31;
+      if (op == OP_RX || op == OP_RY || op == OP_RZ) last = std::max(last, (int)ins[2 * pc + 1]);
+    }
+    for (int m = 0; 64 * m <= last; ++m)
+      o << "  const float2 T" << m << " = table_row(w, " << m << ", " << last << ");\n";
+  }
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
     const int op = w0 & 31, pa = (w0 >> 5) & 31, pb = (w0 >> 10) & 31;
@@ -507,7 +518,10 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           }
           o << " bp *= tc.y;";
         } else {
-          o << "  { const float2 cs = w.tab[" << at << "]; ";
+          if (sreg)
+            o << "  { const float2 cs = table_entry<" << arg % 64 << ">(T" << arg / 64 << "); ";
+          else
+            o << "  { const float2 cs = w.tab[" << at << "]; ";
           // RX / RY off the register bits sit on a lane bit (planner option)
           const std::string lane = std::to_string(pa - R);
           const std::string hi = "tile_bit<R>(w, " + std::to_string(pa) + ")";

@@ -824,6 +824,21 @@ __device__ __forceinline__ void gate_boundary(const Walk& w) {
   if (w.never) asm volatile("");
 }
 
+// Angle table of a one-sample workgroup held in registers: lane j of the
+// wave's copy row m holds occurrence 64 m + j, read at a gate into scalar
+// registers.  The values are uniform over the wave, so a gate needs no LDS
+// read (whose latency a lone wave per SIMD cannot hide).
+__device__ __forceinline__ float2 table_row(const Walk& w, int m, int last) {
+  const int j = 64 * m + (int)__lane_id();
+  return w.tab[j < last ? j : last];
+}
+
+template <int J>
+__device__ __forceinline__ float2 table_entry(const float2 row) {
+  return make_float2(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(row.x), J)),
+                     __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row.y), J)));
+}
+
 // Bit p >= R of the amplitude position (a thread or tile bit).  Taken from an
 // opaque copy of tb so that the compiler recomputes it at each gate instead of
 // keeping every bit (and the masks built from it) alive across the schedule.
