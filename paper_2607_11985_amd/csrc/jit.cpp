@@ -582,12 +582,42 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   if (batched) emit_flush(o, pend);
 }
 
+// The circuit's constants, compiled in (the interpreter reads them from the
+// plan's arrays): the qubit count, the mapping (qubit -> physical bit) that
+// the <Z> epilogue or the forming of lambda uses (map_off in the plan's maps),
+// and every angle occurrence's record.  A gate list's constants then cost no
+// dependent loads from device memory before the first gate.
+void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
+  o << "static constexpr int kN = " << p.n << ", kNocc = " << p.occ_src.size()
+    << ", kS = " << (p.path == VQC_PATH_RESIDENT ? p.S : 1) << ";\n"
+    << "__device__ __forceinline__ static int phys_of(const uint8_t*, int q) {\n";
+  std::vector<int> phys(p.maps.begin() + map_off, p.maps.begin() + map_off + p.n);
+  emit_array(o, "uint8_t", "t", phys);
+  o << "  return t[q];\n}\n"
+    << "__device__ __forceinline__ static OccRec occ(const int32_t*, const int32_t*, const float*, "
+       "const float*, int o) {\n"
+    << "  static constexpr OccRec t[] = {";
+  const size_t nocc = p.occ_src.size();
+  o << std::hexfloat;
+  for (size_t i = 0; i < nocc; ++i) {
+    const bool cst = p.occ_src[i] == kSrcConst;
+    const float a = cst ? p.occ_cs[2 * i] : p.affine ? p.occ_ma[2 * i] : 1.f;
+    const float b = cst ? p.occ_cs[2 * i + 1] : p.affine ? p.occ_ma[2 * i + 1] : 0.f;
+    o << (i ? ", " : "") << "{" << p.occ_src[i] << ", " << p.occ_idx[i] << ", " << (double)a
+      << "f, " << (double)b << "f}";
+  }
+  if (nocc == 0) o << "{0, 0, 0.f, 0.f}";
+  o << std::defaultfloat << "};\n  return t[o];\n}\n";
+}
+
 // A schedule struct: run() for one stream, the group sum used for <Z>, and
 // (when `tables`) the kernel's tangent-form tables.
 void emit_sched_struct(std::ostringstream& o, const std::string& name, const Plan& p,
                        const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S,
-                       const GradMode& gm, const TanMode& tm, const Frame* tables) {
-  o << "struct " << name << " {\n"
+                       const GradMode& gm, const TanMode& tm, const Frame* tables, int map_off) {
+  o << "struct " << name << " {\n";
+  emit_constants(o, p, map_off);
+  o
     << "template <int R, bool BWD, bool WIDE>\n"
     << "__device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w, "
        "const uint32_t*, int) {\n"
@@ -623,13 +653,14 @@ bool tangent_wanted(int S, int R) { return S == 1 && R >= 3; }
 // (adjoint).
 std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
                         const uint32_t* ins, int n_ins, bool bwd, bool stream, int R, int S,
-                        int threads, size_t lds, int n_slots, bool esign) {
+                        int threads, size_t lds, int n_slots, bool esign, int map_off) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
   const int lanes = stream ? threads : 1 << (p.k - R);
   TanMode tm = tan_mode(p, bwd ? nullptr : ins, n_ins, bwd ? ins : nullptr, n_ins, S, esign, lds);
   tm.on = tm.on && tangent_wanted(S, R);
-  emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr);
+  emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr,
+                    map_off);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << name
     << (stream ? "(const vqc::PassArgs A) {\n" : "(const vqc::TileArgs A) {\n")
@@ -652,8 +683,10 @@ std::string step_unit(const Plan& p, const Frame& fr) {
   const int nf = (int)p.fwd.size() / 2, nb = (int)p.bwd.size() / 2;
   TanMode tm = tan_mode(p, p.fwd.data(), nf, p.bwd.data(), nb, p.S, true, p.lds_step);
   tm.on = tm.on && tangent_wanted(p.S, p.R);
-  emit_sched_struct(o, "SchedF", p, p.fwd.data(), nf, false, p.R, p.k, p.S, gm, tm, &fr);
-  emit_sched_struct(o, "SchedB", p, p.bwd.data(), nb, true, p.R, p.k, p.S, gm, tm, nullptr);
+  emit_sched_struct(o, "SchedF", p, p.fwd.data(), nf, false, p.R, p.k, p.S, gm, tm, &fr,
+                    p.end_off);
+  emit_sched_struct(o, "SchedB", p, p.bwd.data(), nb, true, p.R, p.k, p.S, gm, tm, nullptr,
+                    p.end_off);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << p.WG << ") vqc_rs(const vqc::TileArgs A) {\n"
     << "  __shared__ __align__(16) unsigned char smem["
@@ -670,9 +703,11 @@ std::vector<JitUnit> jit_units(const Plan& p) {
   const Frame fr = frame_rows(p);
   if (p.path == VQC_PATH_RESIDENT) {
     u.push_back({"vqc_rf", kernel_unit(p, fr, "vqc_rf", p.fwd.data(), (int)p.fwd.size() / 2,
-                                       false, false, p.R, p.S, p.WG, p.lds_fwd, p.P + p.F, true)});
+                                       false, false, p.R, p.S, p.WG, p.lds_fwd, p.P + p.F, true,
+                                       p.end_off)});
     u.push_back({"vqc_rb", kernel_unit(p, fr, "vqc_rb", p.bwd.data(), (int)p.bwd.size() / 2,
-                                       true, false, p.R, p.S, p.WG, p.lds_bwd, p.P + p.F, true)});
+                                       true, false, p.R, p.S, p.WG, p.lds_bwd, p.P + p.F, true,
+                                       p.end_off)});
     u.push_back({"vqc_rs", step_unit(p, fr)});
     return u;
   }
@@ -681,14 +716,14 @@ std::vector<JitUnit> jit_units(const Plan& p) {
     const PassPlan& pp = p.fpass[i];
     u.push_back({name, kernel_unit(p, fr, name, p.fwd.data() + 2 * pp.ins_off, pp.n_ins, false,
                                    true, p.Rf, 1, 1 << (p.k - p.Rf), p.lds_fwd, pp.n_slots,
-                                   (pp.flags & PF_ZPART) != 0)});
+                                   (pp.flags & PF_ZPART) != 0, pp.end_off)});
   }
   for (size_t i = 0; i < p.bpass.size(); ++i) {
     const std::string name = "vqc_sb" + std::to_string(i);
     const PassPlan& pp = p.bpass[i];
     u.push_back({name, kernel_unit(p, fr, name, p.bwd.data() + 2 * pp.ins_off, pp.n_ins, true,
                                    true, p.Rb, 1, 1 << (p.k - p.Rb), p.lds_bwd, pp.n_slots,
-                                   (pp.flags & PF_MAKE_LAMBDA) != 0)});
+                                   (pp.flags & PF_MAKE_LAMBDA) != 0, pp.start_off)});
   }
   return u;
 }

@@ -665,7 +665,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     // training step: E and g rows of the workgroup's samples after the adjoint's
     // tables
     plan.lds_e = align_up(plan.lds_bwd, 16);
-    plan.lds_step = plan.lds_e + 2 * (size_t)plan.S * n * 4;
+    plan.lds_step = plan.lds_e + (2 * (size_t)plan.S * n + plan.S) * 4;  // E, g, targets
   } else {
     // 13-qubit tiles by default for the generated kernels: two workgroups per
     // CU overlap one's HBM traffic with the other's compute.  Measured: the

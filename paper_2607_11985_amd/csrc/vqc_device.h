@@ -801,6 +801,13 @@ __device__ __forceinline__ void exchange(St<R>& a, float* xbuf, uint32_t plane,
 // ------------------------------------------------------- schedule runner
 
 // Context of one workgroup's walk through an instruction stream.
+// One angle occurrence: its source (parameter / input / constant) and index,
+// and (mul, add), or (cos, sin)(theta/2) when the angle is constant.
+struct OccRec {
+  int32_t src, idx;
+  float a, b;
+};
+
 struct Walk {
   const uint32_t* cols;
   float* xbuf;        // planar exchange buffer: plane floats of real parts, then imaginary
@@ -903,7 +910,9 @@ __device__ __forceinline__ void run_schedule(St<R>& a, St<R>& l, const uint32_t*
 // fd_slots > 0 (central differences): sample bb of the launch is the shifted
 // copy r = bb mod (2 fd_slots) of input row bb / (2 fd_slots), in which slot
 // fd_base + r / 2 (parameters, then inputs) is moved by +fd_h (r even) or
-// -fd_h.
+// -fd_h.  Sched::occ gives an occurrence's source, index and (mul, add), or
+// its (cos, sin) when constant: read from the plan's arrays, or compiled in.
+template <typename Sched>
 __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64_t b0, int64_t B,
                                             const int32_t* occ_src, const int32_t* occ_idx,
                                             const float* occ_cs, const float* occ_ma,
@@ -911,39 +920,69 @@ __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64
                                             const float* inputs, int F, int tid, int nthreads,
                                             int n_params = 0, int fd_slots = 0,
                                             float fd_h = 0.f, int fd_base = 0) {
-  for (int i = tid; i < n_occ * S; i += nthreads) {
-    const int o = i / S;
-    const int s = i - o * S;
-    const int64_t bb = b0 + s;
-    const int src = occ_src[o];
-    float c, sn;
-    if (src == kSrcConst) {
-      c = occ_cs[2 * o];
-      sn = occ_cs[2 * o + 1];
-    } else {
-      float th = 0.f;
-      if (bb < B) {
-        int64_t row = bb;
-        float shift = 0.f;
-        if (fd_slots > 0) {
-          const int64_t per = 2 * (int64_t)fd_slots;
-          row = bb / per;
-          const int r = (int)(bb - row * per);
-          const int slot = src == kSrcParam ? occ_idx[o] : n_params + occ_idx[o];
-          if (slot == fd_base + (r >> 1)) shift = (r & 1) ? -fd_h : fd_h;
-        }
-        th = (src == kSrcParam ? params[row * P + occ_idx[o]] : inputs[row * F + occ_idx[o]]) +
-             shift;
-        if (occ_ma) th = fmaf(occ_ma[2 * o], th, occ_ma[2 * o + 1]);
-      }
-      sincosf(0.5f * th, &sn, &c);
+  if (Sched::kNocc >= 0) {  // compiled-in sizes: constant trip counts
+    n_occ = Sched::kNocc;
+    S = Sched::kS;
+  }
+  const int total = n_occ * S;
+  // Four rounds at a time: the rounds' occurrence records, then their values,
+  // are loaded together, so that a chunk waits for two load latencies before
+  // its sincos.  The value loads are unconditional (a lane with nothing to
+  // read reads the first word of occ_src), and the empty asm keeps the
+  // compiler from sinking them into the branches that use them.
+  constexpr int kRounds = 4;
+#pragma unroll
+  for (int c0 = 0; c0 < total; c0 += kRounds * nthreads) {
+    OccRec oc[kRounds];
+    float th[kRounds], shift[kRounds];
+    bool var[kRounds];
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const int i = c0 + r * nthreads + tid;
+      oc[r] = Sched::occ(occ_src, occ_idx, occ_cs, occ_ma, i < total ? i / S : 0);
     }
-    tab[i] = make_float2(c, sn);
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const int i = c0 + r * nthreads + tid;
+      const bool live = i < total;
+      const int64_t bb = b0 + (live ? i % S : 0);
+      var[r] = live && oc[r].src != kSrcConst && bb < B;
+      int64_t row = bb;
+      shift[r] = 0.f;
+      if (fd_slots > 0) {
+        const int64_t per = 2 * (int64_t)fd_slots;
+        row = bb / per;
+        const int rr = (int)(bb - row * per);
+        const int slot = oc[r].src == kSrcParam ? oc[r].idx : n_params + oc[r].idx;
+        if (slot == fd_base + (rr >> 1)) shift[r] = (rr & 1) ? -fd_h : fd_h;
+      }
+      const float* src = !var[r] ? reinterpret_cast<const float*>(occ_src)
+                         : oc[r].src == kSrcParam ? params + row * P + oc[r].idx
+                                                  : inputs + row * F + oc[r].idx;
+      th[r] = *src;
+    }
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) asm volatile("" : "+v"(th[r]));
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const int i = c0 + r * nthreads + tid;
+      if (i >= total) continue;
+      float c = 1.f, sn = 0.f;  // rows past the batch
+      if (oc[r].src == kSrcConst) {
+        c = oc[r].a;
+        sn = oc[r].b;
+      } else if (var[r]) {
+        float t = th[r] + shift[r];
+        if (occ_ma) t = fmaf(oc[r].a, t, oc[r].b);
+        sincosf(0.5f * t, &sn, &c);
+      }
+      tab[i] = make_float2(c, sn);
+    }
   }
 }
 
 // lambda = H psi with H = sum_q g_q Z_q, the Z signs read from the mapping
-template <int R>
+template <int R, typename Sched>
 __device__ __forceinline__ void make_lambda(St<R>& l, const St<R>& a, const float* g, int n,
                                             const uint8_t* phys, uint32_t tb, bool valid,
                                             const float* esign = nullptr) {
@@ -951,9 +990,10 @@ __device__ __forceinline__ void make_lambda(St<R>& l, const St<R>& a, const floa
 #pragma unroll
   for (int b = 0; b < R; ++b) gr[b] = 0.f;
   if (valid) {
-    for (int q = 0; q < n; ++q) {
+#pragma unroll
+    for (int q = 0; q < (Sched::kN >= 0 ? Sched::kN : n); ++q) {
       const float gq = esign ? g[q] * esign[q] : g[q];
-      const int p = phys[q];
+      const int p = Sched::phys_of(phys, q);
       if (p >= R) gt += ((tb >> (p - R)) & 1u) ? -gq : gq;
 #pragma unroll
       for (int b = 0; b < R; ++b)
@@ -987,8 +1027,9 @@ __device__ __forceinline__ void z_partials(const St<R>& a, float* ez, int n, con
     for (int b = 0; b < R; ++b) sr[b] += (u & (1 << b)) ? -pj : pj;
   }
   __syncthreads();  // the exchange buffer may still be read by other threads
-  for (int q = 0; q < n; ++q) {
-    const int p = phys[q];
+#pragma unroll
+  for (int q = 0; q < (Sched::kN >= 0 ? Sched::kN : n); ++q) {
+    const int p = Sched::phys_of(phys, q);
     float v = ((w.tb >> (p - R)) & 1u) ? -tot : tot;
 #pragma unroll
     for (int b = 0; b < R; ++b)
@@ -1000,8 +1041,32 @@ __device__ __forceinline__ void z_partials(const St<R>& a, float* ez, int n, con
   __syncthreads();
 }
 
-// The precompiled kernels' schedule runner: interprets the instruction stream.
+// The precompiled kernels' schedule runner: interprets the instruction stream;
+// the circuit's constants come from the plan's arrays in device memory.
 struct InterpSched {
+  // number of qubits when fixed at compile time, else -1 (then A.n)
+  static constexpr int kN = -1;
+  // occurrences and samples per workgroup when fixed at compile time, else -1
+  static constexpr int kNocc = -1, kS = -1;
+  // physical bit of qubit q under the mapping the epilogue / lambda use
+  __device__ __forceinline__ static int phys_of(const uint8_t* phys, int q) { return phys[q]; }
+  __device__ __forceinline__ static OccRec occ(const int32_t* src, const int32_t* idx,
+                                               const float* cs, const float* ma, int o) {
+    OccRec r;
+    r.src = src[o];
+    r.idx = idx[o];
+    if (r.src == kSrcConst) {
+      r.a = cs[2 * o];
+      r.b = cs[2 * o + 1];
+    } else if (ma) {
+      r.a = ma[2 * o];
+      r.b = ma[2 * o + 1];
+    } else {
+      r.a = 1.f;
+      r.b = 0.f;
+    }
+    return r;
+  }
   template <int R, bool BWD, bool WIDE>
   __device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w,
                                              const uint32_t* ins, int n_ins) {
@@ -1235,9 +1300,9 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
   const int64_t b = b0 + w.sl;
   const bool valid = b < A.B;
 
-  angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
-              A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F, tid, WG, A.P,
-              A.fd_slots, A.fd_h);
+  angle_table<Sched>(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B,
+                     A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs,
+                     A.F, tid, WG, A.P, A.fd_slots, A.fd_h);
   if (BWD)
     for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
@@ -1254,8 +1319,8 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
     for (int j = 0; j < NA; ++j) v[j] = ws[((size_t)blockIdx.x * NA + j) * WG + tid];
 #pragma unroll
     for (int j = 0; j < NA; ++j) split(v[j], a.r[j], a.i[j]);
-    make_lambda<R>(l, a, A.grad_out + (valid ? b : 0) * A.n, A.n, A.end_phys, w.tb, valid,
-                   Sched::esigns(w));
+    make_lambda<R, Sched>(l, a, A.grad_out + (valid ? b : 0) * A.n, A.n, A.end_phys, w.tb,
+                          valid, Sched::esigns(w));
   }
 
   Sched::template run<R, BWD, (WG > 64)>(a, l, w, A.ins, A.n_ins);
@@ -1287,9 +1352,17 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
   const bool valid = b0 + w.sl < A.B;
   float* e = reinterpret_cast<float*>(smem + A.lds_e);  // [S][n]
   float* g = e + A.S * A.n;                             // [S][n]
+  float* ys = g + A.S * A.n;                            // [S] the loss head's targets
 
-  angle_table(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B, A.occ_src,
-              A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F, tid, WG);
+  // the loss head's targets are fetched first, so that their latency is hidden
+  float y0 = 0.f;
+  if (A.target && tid < A.S && b0 + tid < A.B) y0 = A.target[b0 + tid];
+  angle_table<FS>(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B,
+                  A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F,
+                  tid, WG);
+  // stored where the table's loads have completed anyway (a load in the loss
+  // loop would wait for the stores of E issued before it)
+  if (tid < A.S) ys[tid] = y0;
   for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
   FS::prepare(w, tid, WG);  // the tables of both sweeps
@@ -1304,13 +1377,13 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
     const int s = i / A.n;
     const int q = i - s * A.n;
     const int64_t bb = b0 + s;
-    const float y = (A.target && bb < A.B) ? A.target[bb] : 0.f;
+    const float y = ys[s];
     const float v = loss_cot(A.loss, e + s * A.n, y, A.n, q, A.B);
     g[i] = v;
     if (A.cot_out && bb < A.B) A.cot_out[bb * A.n + q] = v;
   }
   __syncthreads();
-  make_lambda<R>(l, a, g + w.sl * A.n, A.n, A.end_phys, w.tb, valid, FS::esigns(w));
+  make_lambda<R, FS>(l, a, g + w.sl * A.n, A.n, A.end_phys, w.tb, valid, FS::esigns(w));
   BS::template run<R, true, (WG > 64)>(a, l, w, A.ins_b, A.n_ins_b);
   __syncthreads();
   resident_grads(A, w.acc, WG);
@@ -1384,8 +1457,9 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
-  angle_table(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params,
-              A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots, A.fd_h, A.fd_base);
+  angle_table<Sched>(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma,
+                     A.params, A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots, A.fd_h,
+                     A.fd_base);
   if (BWD)
     for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
   __syncthreads();
@@ -1408,8 +1482,8 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   }
   if (BWD) {
     if (A.flags & PF_MAKE_LAMBDA) {
-      make_lambda<R>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, w.tb, true,
-                     Sched::esigns(w));
+      make_lambda<R, Sched>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, w.tb, true,
+                            Sched::esigns(w));
     } else {
       const float2* src = reinterpret_cast<const float2*>(A.lam_src) + sbase;
       load_tile<R>(l, src, base, off);
