@@ -392,16 +392,20 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
     o << "  const float* gmul = reinterpret_cast<const float*>(w.smem + " << tm.off_gm << "u);\n";
   if (tan)  // product of the factors cos(phi') of the current block so far
     o << "  float bp = 1.f;\n";
-  // one sample per workgroup: the (cos, sin) table in registers (table_row)
-  const bool sreg = !tan && S == 1;
+  // one sample per workgroup and 4 amplitudes per thread (latency-bound): the
+  // angle table, and the adjoint's gradient signs, in registers (table_row)
+  const bool sreg = S == 1 && R <= 2;
   if (sreg) {
     int last = -1;
     for (int pc = 0; pc < n_ins; ++pc) {
       const int op = ins[2 * pc] & 31;
       if (op == OP_RX || op == OP_RY || op == OP_RZ) last = std::max(last, (int)ins[2 * pc + 1]);
     }
-    for (int m = 0; 64 * m <= last; ++m)
+    for (int m = 0; 64 * m <= last; ++m) {
       o << "  const float2 T" << m << " = table_row(w, " << m << ", " << last << ");\n";
+      if (tan && bwd)
+        o << "  const float G" << m << " = table_row(gmul, " << m << ", " << last << ");\n";
+    }
   }
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
@@ -501,19 +505,37 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         }
         const std::string at = std::to_string(arg) + " * " + std::to_string(S) + " + w.sl";
         if (tan) {
-          o << "  { const float2 tc = w.tab[" << arg << "]; const float t = tc.x; ";
+          if (sreg)
+            o << "  { const float2 tc = table_entry<" << arg % 64 << ">(T" << arg / 64 << "); ";
+          else
+            o << "  { const float2 tc = w.tab[" << arg << "]; ";
+          o << "const float t = tc.x; ";
+          // RX / RY off the register bits sit on a lane bit (planner option)
+          const std::string lane = std::to_string(pa - R);
+          const std::string hi = "tile_bit<R>(w, " + std::to_string(pa) + ")";
           if (!bwd) {
             if (reg)
               o << kind << "_t<R, " << pa << ">(a, t);";
+            else if (op == OP_RZ)
+              o << "phase_t<R>(a, flip_sign(t, " << hi << " << 31));";
+            else if (op == OP_RX)
+              o << "rx_lane_t<R, " << lane << ">(a, t);";
             else
-              o << "phase_t<R>(a, flip_sign(t, tile_bit<R>(w, " << pa << ") << 31));";
+              o << "ry_lane_t<R, " << lane << ">(a, t, " << hi << ");";
           } else {
             if (reg)
               o << "float g = adj_" << kind << "_t<R, " << pa << ">(a, l, t);";
+            else if (op == OP_RZ)
+              o << "float g = adj_phase_t<R>(a, l, t, " << hi << ");";
+            else if (op == OP_RX)
+              o << "float g = adj_rx_lane_t<R, " << lane << ">(a, l, t);";
             else
-              o << "float g = adj_phase_t<R>(a, l, t, tile_bit<R>(w, " << pa << "));";
+              o << "float g = adj_ry_lane_t<R, " << lane << ">(a, l, t, " << hi << ");";
             // the states carry 1 / (the factors of the block before this gate)
-            o << " g *= gmul[" << arg << "] * (bp * bp);";
+            if (sreg)
+              o << " g *= table_entry<" << arg % 64 << ">(G" << arg / 64 << ") * (bp * bp);";
+            else
+              o << " g *= gmul[" << arg << "] * (bp * bp);";
             o << occ_scale(p, arg);
           }
           o << " bp *= tc.y;";
@@ -641,12 +663,14 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
 
 size_t lds_size(size_t b) { return b < 16 ? 16 : b; }
 
-// Whether a kernel uses the tangent form: one sample per workgroup, and enough
-// work per launch that the tables' set-up latency pays off (the 4-amplitude
-// kernels of small states are latency-bound and keep the (cos, sin) form;
-// measured with gates on lane bits too: no faster).  Lane-bit gates come only
-// with 4 amplitudes per thread, so the tangent schedule never meets them.
-bool tangent_wanted(int S, int R) { return S == 1 && R >= 3; }
+// Whether a kernel uses the tangent form: one sample per workgroup (the frame
+// is per sample).  With 4 amplitudes per thread the tables are read from
+// registers (table_row), and rotations on lane bits take the lane forms
+// (rx_lane_t, ...).
+bool tangent_wanted(int S, int R) {
+  (void)R;
+  return S == 1;
+}
 
 // One kernel in a program of its own, so that the kernels of a circuit compile
 // in parallel.  esign: the kernel computes <Z> (forward) or forms lambda

@@ -686,6 +686,71 @@ __device__ __forceinline__ float adj_ry_lane(St<R>& a, St<R>& l, float c, float 
   return hi ? -acc : acc;
 }
 
+// The tangent form (I -+ i t P, see rx_t) on lane bit J: one FMA per real
+// component, the partner's value moved by DPP.
+// (I - i t X): a.r + t b.i, a.i - t b.r with b the partner amplitude
+template <int R, int J>
+__device__ __forceinline__ void rx_lane_t(St<R>& a, float t) {
+  const float nt = -t;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float br = xlane<J>(a.r[u]), bi = xlane<J>(a.i[u]);
+    a.r[u] = fmaf(t, bi, a.r[u]);
+    a.i[u] = fmaf(nt, br, a.i[u]);
+  }
+}
+
+// (I - i t Y) = [1, -t; t, 1]: the partner enters with -t on the side with
+// the bit clear and +t on the other
+template <int R, int J>
+__device__ __forceinline__ void ry_lane_t(St<R>& a, float t, uint32_t hi) {
+  const float tl = flip_sign(t, (hi ^ 1u) << 31);
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float br = xlane<J>(a.r[u]), bi = xlane<J>(a.i[u]);
+    a.r[u] = fmaf(tl, br, a.r[u]);
+    a.i[u] = fmaf(tl, bi, a.i[u]);
+  }
+}
+
+// Adjoint steps on lane bit J: this lane's share of Im<l|P|a> (as in
+// adj_rx_lane / adj_ry_lane), then the inverse (I + i t P) on both states.
+template <int R, int J>
+__device__ __forceinline__ float adj_rx_lane_t(St<R>& a, St<R>& l, float t) {
+  float acc = 0.f;
+  const float nt = -t;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
+    const float br = xlane<J>(a.r[u]), bi = xlane<J>(a.i[u]);
+    const float ar = a.r[u], ai = a.i[u];
+    acc += qr * ai - qi * ar;
+    a.r[u] = fmaf(nt, bi, ar);
+    a.i[u] = fmaf(t, br, ai);
+    l.r[u] = fmaf(nt, qi, l.r[u]);
+    l.i[u] = fmaf(t, qr, l.i[u]);
+  }
+  return acc;
+}
+
+template <int R, int J>
+__device__ __forceinline__ float adj_ry_lane_t(St<R>& a, St<R>& l, float t, uint32_t hi) {
+  float acc = 0.f;
+  const float tl = flip_sign(t, hi << 31);  // +t with the bit clear, -t with it set
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
+    const float br = xlane<J>(a.r[u]), bi = xlane<J>(a.i[u]);
+    const float ar = a.r[u], ai = a.i[u];
+    acc += qr * ar + qi * ai;
+    a.r[u] = fmaf(tl, br, ar);
+    a.i[u] = fmaf(tl, bi, ai);
+    l.r[u] = fmaf(tl, qr, l.r[u]);
+    l.i[u] = fmaf(tl, qi, l.i[u]);
+  }
+  return hi ? -acc : acc;
+}
+
 // CNOT with the target on lane bit J and the control on register bit C: the
 // amplitudes with the control set trade places with the partner lane's
 template <int R, int C, int J>
@@ -844,6 +909,17 @@ template <int J>
 __device__ __forceinline__ float2 table_entry(const float2 row) {
   return make_float2(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(row.x), J)),
                      __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row.y), J)));
+}
+
+// the same for a table of floats (the adjoint's gradient signs)
+__device__ __forceinline__ float table_row(const float* tab, int m, int last) {
+  const int j = 64 * m + (int)__lane_id();
+  return tab[j < last ? j : last];
+}
+
+template <int J>
+__device__ __forceinline__ float table_entry(const float row) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row), J));
 }
 
 // Bit p >= R of the amplitude position (a thread or tile bit).  Taken from an

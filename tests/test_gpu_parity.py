@@ -215,7 +215,7 @@ def check_cot(g, E_ref, y, loss, batch):
 
 @pytest.mark.parametrize("n,loss,path,engine", [
     (1, "sum", "auto", "jit"), (3, "mean", "auto", "jit"), (6, "mse_z0", "auto", "jit"),
-    (9, "mse_meanz", "auto", "jit"), (12, "mse_z0", "auto", "jit"),
+    (8, "mse_meanz", "auto", "jit"), (9, "mse_meanz", "auto", "jit"), (12, "mse_z0", "auto", "jit"),
     (13, "mse_meanz", "auto", "jit"), (14, "mean", "stream", "jit"),
     (15, "mse_meanz", "auto", "jit"), (7, "mse_meanz", "auto", "interp"),
     (14, "mse_z0", "resident", "interp")])
