@@ -253,8 +253,10 @@ __device__ __forceinline__ float adj_rx(St<R>& a, St<R>& l, float c, float s) {
     const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
     const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
     // X: <l|X|a> = conj(l0) a1 + conj(l1) a0
-    acc += lr * bi - li * br;
-    acc += mr * ai - mi * ar;
+    acc = fmaf(lr, bi, acc);
+    acc = fmaf(-li, br, acc);
+    acc = fmaf(mr, ai, acc);
+    acc = fmaf(-mi, ar, acc);
     // RX(-theta) = [c, is; is, c]
     a.r[u] = c * ar - s * bi;
     a.i[u] = c * ai + s * br;
@@ -278,8 +280,10 @@ __device__ __forceinline__ float adj_ry(St<R>& a, St<R>& l, float c, float s) {
     const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
     const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
     // Y a = (-i a1, i a0): Im<l|Y|a> = -Re(conj(l0) a1) + Re(conj(l1) a0)
-    acc -= lr * br + li * bi;
-    acc += mr * ar + mi * ai;
+    acc = fmaf(-lr, br, acc);
+    acc = fmaf(-li, bi, acc);
+    acc = fmaf(mr, ar, acc);
+    acc = fmaf(mi, ai, acc);
     // RY(-theta) = [c, s; -s, c]
     a.r[u] = c * ar + s * br;
     a.i[u] = c * ai + s * bi;
@@ -300,8 +304,9 @@ __device__ __forceinline__ float adj_rz(St<R>& a, St<R>& l, float c, float s) {
 #pragma unroll
   for (int u = 0; u < St<R>::N; ++u) {
     const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
-    const float v = lr * ai - li * ar;
-    if (u & (1 << P)) a1 += v; else a0 += v;
+    float& z = (u & (1 << P)) ? a1 : a0;
+    z = fmaf(lr, ai, z);
+    z = fmaf(-li, ar, z);
     const float ss = (u & (1 << P)) ? -s : s;  // the inverse phase
     a.r[u] = c * ar - ss * ai;
     a.i[u] = c * ai + ss * ar;
@@ -319,7 +324,8 @@ __device__ __forceinline__ float adj_rz_uniform(St<R>& a, St<R>& l, float c, flo
 #pragma unroll
   for (int u = 0; u < St<R>::N; ++u) {
     const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
-    acc += lr * ai - li * ar;
+    acc = fmaf(lr, ai, acc);
+    acc = fmaf(-li, ar, acc);
     a.r[u] = c * ar - ss * ai;
     a.i[u] = c * ai + ss * ar;
     l.r[u] = c * lr - ss * li;
@@ -408,8 +414,10 @@ __device__ __forceinline__ float adj_rx_t(St<R>& a, St<R>& l, float t) {
     const int v = u | (1 << P);
     const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
     const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
-    acc += lr * bi - li * br;
-    acc += mr * ai - mi * ar;
+    acc = fmaf(lr, bi, acc);
+    acc = fmaf(-li, br, acc);
+    acc = fmaf(mr, ai, acc);
+    acc = fmaf(-mi, ar, acc);
     a.r[u] = fmaf(-t, bi, ar);
     a.i[u] = fmaf(t, br, ai);
     a.r[v] = fmaf(-t, ai, br);
@@ -431,8 +439,10 @@ __device__ __forceinline__ float adj_ry_t(St<R>& a, St<R>& l, float t) {
     const int v = u | (1 << P);
     const float ar = a.r[u], ai = a.i[u], br = a.r[v], bi = a.i[v];
     const float lr = l.r[u], li = l.i[u], mr = l.r[v], mi = l.i[v];
-    acc -= lr * br + li * bi;
-    acc += mr * ar + mi * ai;
+    acc = fmaf(-lr, br, acc);
+    acc = fmaf(-li, bi, acc);
+    acc = fmaf(mr, ar, acc);
+    acc = fmaf(mi, ai, acc);
     a.r[u] = fmaf(t, br, ar);
     a.i[u] = fmaf(t, bi, ai);
     a.r[v] = fmaf(-t, ar, br);
@@ -451,8 +461,9 @@ __device__ __forceinline__ float adj_rz_t(St<R>& a, St<R>& l, float t) {
 #pragma unroll
   for (int u = 0; u < St<R>::N; ++u) {
     const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
-    const float v = lr * ai - li * ar;
-    if (u & (1 << P)) a1 += v; else a0 += v;
+    float& z = (u & (1 << P)) ? a1 : a0;
+    z = fmaf(lr, ai, z);
+    z = fmaf(-li, ar, z);
     const float tz = (u & (1 << P)) ? t : -t;  // the inverse: (1 + i t z)
     a.r[u] = fmaf(tz, ai, ar);
     a.i[u] = fmaf(-tz, ar, ai);
@@ -470,7 +481,8 @@ __device__ __forceinline__ float adj_phase_t(St<R>& a, St<R>& l, float t, uint32
 #pragma unroll
   for (int u = 0; u < St<R>::N; ++u) {
     const float ar = a.r[u], ai = a.i[u], lr = l.r[u], li = l.i[u];
-    acc += lr * ai - li * ar;
+    acc = fmaf(lr, ai, acc);
+    acc = fmaf(-li, ar, acc);
     a.r[u] = fmaf(tz, ai, ar);
     a.i[u] = fmaf(-tz, ar, ai);
     l.r[u] = fmaf(tz, li, lr);
@@ -655,7 +667,8 @@ __device__ __forceinline__ float adj_rx_lane(St<R>& a, St<R>& l, float c, float 
   for (int u = 0; u < St<R>::N; ++u) {
     const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
     const float ar = a.r[u], ai = a.i[u];
-    acc += qr * ai - qi * ar;
+    acc = fmaf(qr, ai, acc);
+    acc = fmaf(-qi, ar, acc);
     const float tr = xlane<J>(ai) * ns, ti = xlane<J>(ar) * s;
     a.r[u] = fmaf(c, ar, tr);
     a.i[u] = fmaf(c, ai, ti);
@@ -676,7 +689,8 @@ __device__ __forceinline__ float adj_ry_lane(St<R>& a, St<R>& l, float c, float 
   for (int u = 0; u < St<R>::N; ++u) {
     const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
     const float ar = a.r[u], ai = a.i[u];
-    acc += qr * ar + qi * ai;
+    acc = fmaf(qr, ar, acc);
+    acc = fmaf(qi, ai, acc);
     const float tr = xlane<J>(ar) * sl, ti = xlane<J>(ai) * sl;
     a.r[u] = fmaf(c, ar, tr);
     a.i[u] = fmaf(c, ai, ti);
@@ -724,7 +738,8 @@ __device__ __forceinline__ float adj_rx_lane_t(St<R>& a, St<R>& l, float t) {
     const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
     const float br = xlane<J>(a.r[u]), bi = xlane<J>(a.i[u]);
     const float ar = a.r[u], ai = a.i[u];
-    acc += qr * ai - qi * ar;
+    acc = fmaf(qr, ai, acc);
+    acc = fmaf(-qi, ar, acc);
     a.r[u] = fmaf(nt, bi, ar);
     a.i[u] = fmaf(t, br, ai);
     l.r[u] = fmaf(nt, qi, l.r[u]);
@@ -742,7 +757,8 @@ __device__ __forceinline__ float adj_ry_lane_t(St<R>& a, St<R>& l, float t, uint
     const float qr = xlane<J>(l.r[u]), qi = xlane<J>(l.i[u]);
     const float br = xlane<J>(a.r[u]), bi = xlane<J>(a.i[u]);
     const float ar = a.r[u], ai = a.i[u];
-    acc += qr * ar + qi * ai;
+    acc = fmaf(qr, ar, acc);
+    acc = fmaf(qi, ai, acc);
     a.r[u] = fmaf(tl, br, ar);
     a.i[u] = fmaf(tl, bi, ai);
     l.r[u] = fmaf(tl, qr, l.r[u]);
