@@ -180,15 +180,66 @@ void emit_array(std::ostringstream& o, const char* type, const char* name, const
 // rotations: the frame sign of each (t negated in place, once) and the sign
 // of the adjoint's gradients; and the <Z> signs.  esigns(): those signs.  The
 // block factors are products the schedule forms as it goes (bp).
-void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const Frame& fr) {
+void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const Frame& fr,
+                 int nt) {
   const int nocc = (int)p.occ_src.size(), W = t.W;
-  o << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt) {\n";
   if (!t.on) {
-    o << "  (void)w; (void)tid; (void)nt;\n}\n"
+    o << "struct Pre {};\n"
+      << "__device__ __forceinline__ static Pre preload(int) { return Pre(); }\n"
+      << "__device__ __forceinline__ static void prepare(const Walk&, int, int, const Pre&) {}\n"
       << "__device__ __forceinline__ static const float* esigns(const Walk&) { return nullptr; }\n";
     return;
   }
-  o << "  float2* tab = const_cast<float2*>(w.tab);\n"
+  // instances: the forward stream's rotations, then the adjoint's
+  std::vector<int> inst = t.focc;
+  inst.insert(inst.end(), t.bocc.begin(), t.bocc.end());
+  std::vector<uint32_t> rows;
+  for (int k : inst)
+    for (int j = 0; j < W; ++j) rows.push_back(j < fr.words ? fr.arow[(size_t)k * fr.words + j] : 0u);
+  std::vector<uint32_t> erows;
+  if (t.esign)
+    for (int q = 0; q < p.n; ++q)
+      for (int j = 0; j < W; ++j) erows.push_back(j < fr.words ? fr.erow[(size_t)q * fr.words + j] : 0u);
+  const int nf = (int)t.focc.size(), ni = (int)inst.size();
+  // preload(): each thread's entries of the constant rows, read before the
+  // angle table (their latency then overlaps its loads) when they fit in a
+  // few registers; prepare() reads them in place otherwise
+  const int ri = (ni + nt - 1) / nt, re = t.esign ? (p.n + nt - 1) / nt : 0;
+  const int nreg = ri * (1 + W) + re * W;
+  const bool pre = ni > 0 && nreg <= 48;
+  o << "struct Pre {";
+  if (pre) o << " uint32_t o[" << ri << "], r[" << ri * W << "], e[" << std::max(re * W, 1) << "];";
+  o << " };\n"
+    << "__device__ __forceinline__ static Pre preload(int tid) {\n"
+    << "  Pre p;\n";
+  if (pre) {
+    emit_array(o, "uint16_t", "kOcc", inst);
+    emit_array(o, "uint32_t", "kArow", rows);
+    o << "#pragma unroll\n"
+      << "  for (int r = 0; r < " << ri << "; ++r) {\n"
+      << "    const int i = min(r * " << nt << " + tid, " << ni - 1 << ");\n"
+      << "    p.o[r] = kOcc[i];\n"
+      << "#pragma unroll\n"
+      << "    for (int j = 0; j < " << W << "; ++j) p.r[r * " << W << " + j] = kArow[i * " << W
+      << " + j];\n"
+      << "  }\n";
+    if (re > 0) {
+      emit_array(o, "uint32_t", "kErow", erows);
+      o << "#pragma unroll\n"
+        << "  for (int r = 0; r < " << re << "; ++r) {\n"
+        << "    const int q = min(r * " << nt << " + tid, " << p.n - 1 << ");\n"
+        << "#pragma unroll\n"
+        << "    for (int j = 0; j < " << W << "; ++j) p.e[r * " << W << " + j] = kErow[q * " << W
+        << " + j];\n"
+        << "  }\n";
+    }
+  } else {
+    o << "  (void)tid;\n";
+  }
+  o << "  return p;\n}\n"
+    << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt, const Pre& pre) {\n"
+    << "  (void)pre;\n"
+    << "  float2* tab = const_cast<float2*>(w.tab);\n"
     << "  float* tx = reinterpret_cast<float*>(tab);  // tab[k].x = tx[2 k]\n"
     << "  uint32_t* bits = reinterpret_cast<uint32_t*>(w.smem + " << t.off_bits << "u);\n"
     << "  for (int i0 = 0; i0 < " << nocc << "; i0 += nt) {\n"
@@ -206,15 +257,10 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
     << "    }\n"
     << "  }\n"
     << "  __syncthreads();\n";
-  // instances: the forward stream's rotations, then the adjoint's
-  std::vector<int> inst = t.focc;
-  inst.insert(inst.end(), t.bocc.begin(), t.bocc.end());
-  std::vector<uint32_t> rows;
-  for (int k : inst)
-    for (int j = 0; j < W; ++j) rows.push_back(j < fr.words ? fr.arow[(size_t)k * fr.words + j] : 0u);
-  const int nf = (int)t.focc.size(), ni = (int)inst.size();
-  emit_array(o, "uint16_t", "kOcc", inst);
-  emit_array(o, "uint32_t", "kArow", rows);
+  if (!pre) {
+    emit_array(o, "uint16_t", "kOcc", inst);
+    emit_array(o, "uint32_t", "kArow", rows);
+  }
   o << "  float* gm = reinterpret_cast<float*>(w.smem + " << t.off_gm << "u);\n"
     << "  (void)gm;\n"
     // a constant trip count, so that the rounds' table loads issue together
@@ -222,12 +268,17 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
     << "  for (int i0 = 0; i0 < " << ni << "; i0 += nt) {\n"
     << "    const int i = i0 + tid;\n"
     << "    if (i < " << ni << ") {\n"
-    << "    const bool f = i < " << nf << ";\n"
-    << "    const int k = kOcc[i];\n"
-    << "    uint32_t par = 0u;\n"
+    << "    const bool f = i < " << nf << ";\n";
+  if (pre)
+    o << "    const int rr = i0 / " << nt << ";\n"
+      << "    const int k = pre.o[rr];\n";
+  else
+    o << "    const int k = kOcc[i];\n";
+  o << "    uint32_t par = 0u;\n"
     << "#pragma unroll\n"
-    << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & kArow[i * " << W
-    << " + j]);\n"
+    << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & "
+    << (pre ? "pre.r[rr * " + std::to_string(W) + " + j]" : "kArow[i * " + std::to_string(W) + " + j]")
+    << ");\n"
     << "    if (f) {\n"
     << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n"
     << "    } else {\n";
@@ -238,14 +289,17 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
     << "    }\n"
     << "  }\n";
   if (t.esign) {
-    std::vector<uint32_t> erows;
-    for (int q = 0; q < p.n; ++q)
-      for (int j = 0; j < W; ++j) erows.push_back(j < fr.words ? fr.erow[(size_t)q * fr.words + j] : 0u);
-    emit_array(o, "uint32_t", "kErow", erows);
-    o << "  for (int q = tid; q < " << p.n << "; q += nt) {\n"
+    if (!pre) emit_array(o, "uint32_t", "kErow", erows);
+    o << "#pragma unroll\n"
+      << "  for (int q0 = 0; q0 < " << p.n << "; q0 += nt) {\n"
+      << "    const int q = q0 + tid;\n"
+      << "    if (q >= " << p.n << ") break;\n"
       << "    uint32_t par = 0u;\n"
-      << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & kErow[q * "
-      << W << " + j]);\n"
+      << "#pragma unroll\n"
+      << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & "
+      << (pre ? "pre.e[(q0 / " + std::to_string(nt) + ") * " + std::to_string(W) + " + j]"
+              : "kErow[q * " + std::to_string(W) + " + j]")
+      << ");\n"
       << "    reinterpret_cast<float*>(w.smem + " << t.off_es << "u)[q] = (par & 1u) ? -1.f : 1.f;\n"
       << "  }\n";
   }
@@ -617,19 +671,48 @@ void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
   emit_array(o, "uint8_t", "t", phys);
   o << "  return t[q];\n}\n"
     << "__device__ __forceinline__ static OccRec occ(const int32_t*, const int32_t*, const float*, "
-       "const float*, int o) {\n"
-    << "  static constexpr OccRec t[] = {";
-  const size_t nocc = p.occ_src.size();
-  o << std::hexfloat;
-  for (size_t i = 0; i < nocc; ++i) {
-    const bool cst = p.occ_src[i] == kSrcConst;
-    const float a = cst ? p.occ_cs[2 * i] : p.affine ? p.occ_ma[2 * i] : 1.f;
-    const float b = cst ? p.occ_cs[2 * i + 1] : p.affine ? p.occ_ma[2 * i + 1] : 0.f;
-    o << (i ? ", " : "") << "{" << p.occ_src[i] << ", " << p.occ_idx[i] << ", " << (double)a
-      << "f, " << (double)b << "f}";
+       "const float*, int o) {\n";
+  // The records as runs of occurrences with one source and (a, b) whose index
+  // grows with the occurrence (parameters and inputs read in order, as most
+  // ansatz layers do): a few compares instead of a load from the code
+  // object's data, whose latency would come before the first parameter load.
+  // Circuits with many runs (constant gates each make one) use the table.
+  const int nocc = (int)p.occ_src.size();
+  auto rec_a = [&](int i) {
+    return p.occ_src[i] == kSrcConst ? p.occ_cs[2 * i] : p.affine ? p.occ_ma[2 * i] : 1.f;
+  };
+  auto rec_b = [&](int i) {
+    return p.occ_src[i] == kSrcConst ? p.occ_cs[2 * i + 1] : p.affine ? p.occ_ma[2 * i + 1] : 0.f;
+  };
+  std::vector<int> starts;
+  for (int i = 0; i < nocc; ++i) {
+    const bool cont = i > 0 && p.occ_src[i] != kSrcConst && p.occ_src[i] == p.occ_src[i - 1] &&
+                      p.occ_idx[i] == p.occ_idx[i - 1] + 1 && rec_a(i) == rec_a(i - 1) &&
+                      rec_b(i) == rec_b(i - 1);
+    if (!cont) starts.push_back(i);
   }
-  if (nocc == 0) o << "{0, 0, 0.f, 0.f}";
-  o << std::defaultfloat << "};\n  return t[o];\n}\n";
+  constexpr size_t kMaxRuns = 8;
+  o << std::hexfloat;
+  if (nocc > 0 && starts.size() <= kMaxRuns) {
+    o << "  OccRec r;\n";
+    for (size_t j = 0; j < starts.size(); ++j) {
+      const int i = starts[j];
+      const int end = j + 1 < starts.size() ? starts[j + 1] : nocc;
+      o << "  " << (j ? "else " : "") << (j + 1 < starts.size() ? "if (o < " +
+                                                                  std::to_string(end) + ") " : "")
+        << "r = OccRec{" << p.occ_src[i] << ", o + " << p.occ_idx[i] - i << ", "
+        << (double)rec_a(i) << "f, " << (double)rec_b(i) << "f};\n";
+    }
+    o << "  return r;\n}\n";
+  } else {
+    o << "  static constexpr OccRec t[] = {";
+    for (int i = 0; i < nocc; ++i)
+      o << (i ? ", " : "") << "{" << p.occ_src[i] << ", " << p.occ_idx[i] << ", "
+        << (double)rec_a(i) << "f, " << (double)rec_b(i) << "f}";
+    if (nocc == 0) o << "{0, 0, 0.f, 0.f}";
+    o << "};\n  return t[o];\n}\n";
+  }
+  o << std::defaultfloat;
 }
 
 // A schedule struct: run() for one stream, the group sum used for <Z>, and
@@ -657,7 +740,7 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
   o << "}\n"
     << "__device__ __forceinline__ static float lane_sum(float v, const Walk&) {\n"
     << "  return group_sum<" << gm.tm << ">(v);\n}\n";
-  if (tables) emit_tables(o, p, tm, *tables);
+  if (tables) emit_tables(o, p, tm, *tables, S << (k - R));
   o << "};\n";
 }
 

@@ -1020,8 +1020,9 @@ __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64
   // Four rounds at a time: the rounds' occurrence records, then their values,
   // are loaded together, so that a chunk waits for two load latencies before
   // its sincos.  The value loads are unconditional (a lane with nothing to
-  // read reads the first word of occ_src), and the empty asm keeps the
-  // compiler from sinking them into the branches that use them.
+  // read reads the first word of occ_src, a 256-byte aligned region of the
+  // schedule that other regions follow), and the empty asm keeps the compiler
+  // from sinking them into the branches that use them.
   constexpr int kRounds = 4;
 #pragma unroll
   for (int c0 = 0; c0 < total; c0 += kRounds * nthreads) {
@@ -1168,8 +1169,11 @@ struct InterpSched {
   __device__ __forceinline__ static float lane_sum(float v, const Walk& w) {
     return seg_sum(v, w.width);
   }
-  // per-sample tables built before the schedule (none here)
-  __device__ __forceinline__ static void prepare(const Walk&, int, int) {}
+  // per-sample tables built before the schedule (none here), and the
+  // constants they need, read at the start of the kernel (none)
+  struct Pre {};
+  __device__ __forceinline__ static Pre preload(int) { return Pre(); }
+  __device__ __forceinline__ static void prepare(const Walk&, int, int, const Pre&) {}
   // signs of <Z_q> of the thread's sample (none: the state is the true state)
   __device__ __forceinline__ static const float* esigns(const Walk&) { return nullptr; }
 };
@@ -1392,13 +1396,14 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
   const int64_t b = b0 + w.sl;
   const bool valid = b < A.B;
 
+  const typename Sched::Pre pre = Sched::preload(tid);
   angle_table<Sched>(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B,
                      A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs,
                      A.F, tid, WG, A.P, A.fd_slots, A.fd_h);
   if (BWD)
     for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
-  Sched::prepare(w, tid, WG);
+  Sched::prepare(w, tid, WG, pre);
 
   St<R> a, l;
   if (!BWD) {
@@ -1446,18 +1451,25 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
   float* g = e + A.S * A.n;                             // [S][n]
   float* ys = g + A.S * A.n;                            // [S] the loss head's targets
 
-  // the loss head's targets are fetched first, so that their latency is hidden
-  float y0 = 0.f;
-  if (A.target && tid < A.S && b0 + tid < A.B) y0 = A.target[b0 + tid];
+  // The loss head's targets and the frame tables' constants are read first, so
+  // that their latency is hidden.  The target load is unconditional, so that
+  // no branch makes the kernel wait for it at once; without targets it reads
+  // occ_src (a 256-byte aligned region of the schedule that other regions
+  // follow, so always readable).
+  const int64_t yrow = b0 + (tid < A.S ? tid : 0);
+  const float* yp = A.target ? A.target + (yrow < A.B ? yrow : A.B - 1)
+                             : reinterpret_cast<const float*>(A.occ_src);
+  const float y0 = *yp;
+  const typename FS::Pre pre = FS::preload(tid);
   angle_table<FS>(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B,
                   A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F,
                   tid, WG);
   // stored where the table's loads have completed anyway (a load in the loss
   // loop would wait for the stores of E issued before it)
-  if (tid < A.S) ys[tid] = y0;
+  if (tid < A.S) ys[tid] = A.target && b0 + tid < A.B ? y0 : 0.f;
   for (int i = tid; i < A.n_slots * A.G; i += WG) w.acc[i] = 0.f;
   __syncthreads();
-  FS::prepare(w, tid, WG);  // the tables of both sweeps
+  FS::prepare(w, tid, WG, pre);  // the tables of both sweeps
 
   St<R> a, l;
   zero_state<R>(a, w.stid);
@@ -1549,13 +1561,14 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
+  const typename Sched::Pre pre = Sched::preload(tid);
   angle_table<Sched>(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma,
                      A.params, A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots, A.fd_h,
                      A.fd_base);
   if (BWD)
     for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
   __syncthreads();
-  Sched::prepare(w, tid, WG);
+  Sched::prepare(w, tid, WG, pre);
 
   uint32_t base, off[NA];
   io_offsets<R>(A.io, A.k, A.ng, tid, g, base, off);
