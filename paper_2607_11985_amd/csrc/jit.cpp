@@ -673,10 +673,11 @@ void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
     << "__device__ __forceinline__ static OccRec occ(const int32_t*, const int32_t*, const float*, "
        "const float*, int o) {\n";
   // The records as runs of occurrences with one source and (a, b) whose index
-  // grows with the occurrence (parameters and inputs read in order, as most
-  // ansatz layers do): a few compares instead of a load from the code
-  // object's data, whose latency would come before the first parameter load.
-  // Circuits with many runs (constant gates each make one) use the table.
+  // grows by one (parameters and inputs read in order, as most ansatz layers
+  // do) or stays (one parameter shared by a layer): a few compares instead of
+  // a load from the code object's data, whose latency would come before the
+  // first parameter load.  Circuits with many runs (constant gates each make
+  // one) use the table.
   const int nocc = (int)p.occ_src.size();
   auto rec_a = [&](int i) {
     return p.occ_src[i] == kSrcConst ? p.occ_cs[2 * i] : p.affine ? p.occ_ma[2 * i] : 1.f;
@@ -684,14 +685,23 @@ void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
   auto rec_b = [&](int i) {
     return p.occ_src[i] == kSrcConst ? p.occ_cs[2 * i + 1] : p.affine ? p.occ_ma[2 * i + 1] : 0.f;
   };
-  std::vector<int> starts;
+  std::vector<int> starts, stride;
   for (int i = 0; i < nocc; ++i) {
-    const bool cont = i > 0 && p.occ_src[i] != kSrcConst && p.occ_src[i] == p.occ_src[i - 1] &&
-                      p.occ_idx[i] == p.occ_idx[i - 1] + 1 && rec_a(i) == rec_a(i - 1) &&
-                      rec_b(i) == rec_b(i - 1);
-    if (!cont) starts.push_back(i);
+    bool cont = i > 0 && p.occ_src[i] != kSrcConst && p.occ_src[i] == p.occ_src[i - 1] &&
+                rec_a(i) == rec_a(i - 1) && rec_b(i) == rec_b(i - 1);
+    const int d = i > 0 ? p.occ_idx[i] - p.occ_idx[i - 1] : -1;
+    if (cont && i - 1 == starts.back()) {  // the run's second member sets its stride
+      cont = d == 0 || d == 1;
+      if (cont) stride.back() = d;
+    } else if (cont) {
+      cont = d == stride.back();
+    }
+    if (!cont) {
+      starts.push_back(i);
+      stride.push_back(1);
+    }
   }
-  constexpr size_t kMaxRuns = 8;
+  constexpr size_t kMaxRuns = 16;
   o << std::hexfloat;
   if (nocc > 0 && starts.size() <= kMaxRuns) {
     o << "  OccRec r;\n";
@@ -700,8 +710,9 @@ void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
       const int end = j + 1 < starts.size() ? starts[j + 1] : nocc;
       o << "  " << (j ? "else " : "") << (j + 1 < starts.size() ? "if (o < " +
                                                                   std::to_string(end) + ") " : "")
-        << "r = OccRec{" << p.occ_src[i] << ", o + " << p.occ_idx[i] - i << ", "
-        << (double)rec_a(i) << "f, " << (double)rec_b(i) << "f};\n";
+        << "r = OccRec{" << p.occ_src[i] << ", "
+        << (stride[j] ? "o + " + std::to_string(p.occ_idx[i] - i) : std::to_string(p.occ_idx[i]))
+        << ", " << (double)rec_a(i) << "f, " << (double)rec_b(i) << "f};\n";
     }
     o << "  return r;\n}\n";
   } else {

@@ -157,3 +157,26 @@ def test_affine_fd_backward(torch_mod):
     bound = (h * h / 6 * k ** 3 + 2e-5 * max(k, 1.0) / h) * gs
     assert np.all(np.abs(dp.cpu().numpy() - dpr) <= bound)
     assert np.all(np.abs(dx.cpu().numpy() - dxr) <= bound)
+
+
+@pytest.mark.parametrize("n", [5, 8, 10])
+def test_layers_sharing_one_angle(torch_mod, n):
+    """Layers whose rotations all read one parameter (scaled and offset), next
+    to layers reading one parameter or input per qubit: the generated kernels
+    encode such occurrence runs as compares instead of a table."""
+    layers = []
+    for l in range(3):
+        mul, add = float(np.float32(1.5 - l)), float(np.float32(0.25 * l))
+        layers += [W.Op("RX", (q,), (("param", l, mul, add),)) for q in range(n)]
+        layers += [W.Op("RY", (q,), (("param", 3 + l * n + q),)) for q in range(n)]
+        layers += [W.Op("CNOT", (q, (q + 1) % n)) for q in range(n)]
+        layers += [W.Op("RZ", (q,), (("input", q, -2.0, 0.0),)) for q in range(n)]
+    P, F = 3 + 3 * n, n
+    B = 7
+    params, inputs = W.random_inputs(B, P, F, seed=12900 + n)
+    cot = W.random_cotangent(B, n, seed=13000 + n)
+    note(f"shared-angle layers n={n}")
+    r = gpu_run(torch_mod, layers, n, P, F, params, inputs, cot)
+    dpr, dxr, Er = oracle.vjp(layers, n, params, inputs, cot)
+    check_E(r["E"], Er)
+    check_grads(r, dpr, dxr, cot)
