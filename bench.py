@@ -142,7 +142,7 @@ def main():
     ap.add_argument("--reg-bits", type=int, default=0,
                     help="amplitudes per thread = 2^reg_bits (0: the library's default)")
     ap.add_argument("--tile-qubits", type=int, default=0,
-                    help="streaming tile size, 13 or 14 (0: the library's default)")
+                    help="streaming tile size, 12, 13 or 14 (0: the library's default)")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP graph replays of the step instead of its launches")
     ap.add_argument("--separate", action="store_true",

@@ -144,13 +144,14 @@ typedef struct {
                               every call and dparams is [P], the sum over the
                               samples.  Inputs stay per sample.  0: per-sample
                               rows [B, P] */
-    int32_t tile_qubits; /* streaming path: qubits per tile, 13 or 14 (0 = the
-                            default: 13 with the generated kernels, 14 with
-                            the interpreter).  13-qubit tiles take half the
-                            LDS, so two workgroups share a CU and one's HBM
-                            traffic overlaps the other's compute, at the cost
-                            of more passes.  Generated kernels only (the
-                            interpreter runs 14) */
+    int32_t tile_qubits; /* streaming path: qubits per tile, 12, 13 or 14
+                            (0 = the default: 13 with the generated kernels,
+                            14 with the interpreter).  Each qubit less halves
+                            a workgroup's LDS, so more workgroups share a CU
+                            and one's HBM traffic overlaps another's compute,
+                            at the cost of more passes where the circuit
+                            needs them.  12 and 13: generated kernels only
+                            (the interpreter runs 14) */
     int32_t reserved[2]; /* must be zero */
 } vqc_compile_opts;
 

@@ -336,10 +336,10 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
       return fail(VQC_ERR_INVALID_ARG, "shared_params must be 0 or 1");
     shared = opts->shared_params == 1;
     tile = opts->tile_qubits;
-    if (tile != 0 && tile != 13 && tile != 14)
-      return fail(VQC_ERR_INVALID_ARG, "tile_qubits must be 0 (default), 13 or 14");
-    if (tile == 13 && engine != VQC_ENGINE_JIT)
-      return fail(VQC_ERR_UNSUPPORTED, "13-qubit tiles need the generated kernels");
+    if (tile != 0 && tile != 12 && tile != 13 && tile != 14)
+      return fail(VQC_ERR_INVALID_ARG, "tile_qubits must be 0 (default), 12, 13 or 14");
+    if ((tile == 12 || tile == 13) && engine != VQC_ENGINE_JIT)
+      return fail(VQC_ERR_UNSUPPORTED, "12- and 13-qubit tiles need the generated kernels");
     if (path < VQC_PATH_AUTO || path > VQC_PATH_STREAM)
       return fail(VQC_ERR_INVALID_ARG, "unknown path option");
   } else if (hipGetDevice(&device) != hipSuccess) {

@@ -319,17 +319,19 @@ def test_shared_params_workspace(idx):
 def test_tile_qubits_option():
     ops, P, F = W.random_circuit(15, 20, seed=5)
     arr = _lib.encode_ops(ops)
-    for tq, code in ((12, _lib.VQC_ERR_INVALID_ARG), (15, _lib.VQC_ERR_INVALID_ARG)):
+    for tq, code in ((11, _lib.VQC_ERR_INVALID_ARG), (15, _lib.VQC_ERR_INVALID_ARG)):
         rc, _ = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
                                      _lib.vqc_compile_opts(device=-1, tile_qubits=tq))
         assert rc == code and "tile_qubits" in _lib.vqc_last_error()
-    rc, _ = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
-                                 _lib.vqc_compile_opts(device=-1, tile_qubits=13, engine=1))
-    assert rc == _lib.VQC_ERR_UNSUPPORTED
-    rc, h = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
-                                 _lib.vqc_compile_opts(device=-1, tile_qubits=13))
-    assert rc == 0
-    info = _lib.vqc_circuit_info(h)
-    assert info["tile_qubits"] == 13 and info["threads"] == 512 and info["path"] == 2
-    _lib.vqc_jit_check(h)
-    _lib.vqc_destroy(h)
+    for tq in (12, 13):
+        rc, _ = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
+                                     _lib.vqc_compile_opts(device=-1, tile_qubits=tq, engine=1))
+        assert rc == _lib.VQC_ERR_UNSUPPORTED
+        rc, h = _lib.vqc_compile_raw(arr, len(ops), 15, P, F,
+                                     _lib.vqc_compile_opts(device=-1, tile_qubits=tq))
+        assert rc == 0
+        info = _lib.vqc_circuit_info(h)
+        assert info["tile_qubits"] == tq and info["threads"] == 1 << (tq - 4)
+        assert info["path"] == 2
+        _lib.vqc_jit_check(h)
+        _lib.vqc_destroy(h)

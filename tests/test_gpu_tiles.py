@@ -1,6 +1,6 @@
-"""GPU parity of the streaming path with 13-qubit tiles (two workgroups per CU)
-against the oracle: forward, adjoint, the training step, Psi_0 and
-probabilities.  Bars as in test_gpu_parity / test_gpu_psi0_probs."""
+"""GPU parity of the streaming path with 13- and 12-qubit tiles (two and four
+workgroups per CU) against the oracle: forward, adjoint, the training step,
+Psi_0 and probabilities.  Bars as in test_gpu_parity / test_gpu_psi0_probs."""
 import numpy as np
 import pytest
 
@@ -13,7 +13,8 @@ pytestmark = pytest.mark.gpu
 
 @pytest.mark.parametrize("n,B,kinds,tile", [(14, 3, W.KINDS, 13), (15, 2, W.GENERAL_KINDS, 13),
                                              (16, 2, W.KINDS, 13), (17, 1, W.KINDS, 13),
-                                             (16, 2, W.GENERAL_KINDS, 14)])
+                                             (16, 2, W.GENERAL_KINDS, 14), (14, 3, W.KINDS, 12),
+                                             (16, 2, W.GENERAL_KINDS, 12)])
 def test_tile13_parity(torch_mod, n, B, kinds, tile):
     torch = torch_mod
     from paper_2607_11985_amd.api import Circuit
