@@ -71,15 +71,20 @@ size_t resident_state_bytes(const Plan& p, int64_t batch) {
 struct StreamLayout {
   size_t psi = 0, epart = 0, psiw = 0, lamw = 0, gpart = 0, end_inference = 0, end_training = 0;
   size_t cot = 0, end_step = 0;  // the training step's cotangent rows [B, n]
+  size_t tabs = 0, gsig = 0, esig = 0;  // the table kernel's per-sample tables
 };
 
 StreamLayout stream_layout(const Plan& p, int64_t batch) {
   StreamLayout L;
   const size_t state = (size_t)batch * ((size_t)1 << p.nq) * 8;
   const size_t tiles = (size_t)batch << p.ng;
+  const size_t nocc = p.occ_src.size();
   L.psi = 0;
   L.epart = align_up(L.psi + state, 256);
-  L.end_inference = align_up(L.epart + tiles * (size_t)p.n * 4, 256);
+  L.tabs = align_up(L.epart + tiles * (size_t)p.n * 4, 256);
+  L.gsig = align_up(L.tabs + (size_t)batch * nocc * 8, 256);
+  L.esig = align_up(L.gsig + (size_t)batch * nocc * 4, 256);
+  L.end_inference = align_up(L.esig + (size_t)batch * p.n * 4, 256);
   L.psiw = L.end_inference;
   L.lamw = align_up(L.psiw + state, 256);
   L.gpart = align_up(L.lamw + state, 256);
@@ -237,6 +242,19 @@ int check_workspace(const void* workspace, size_t bytes, size_t need, const char
   return VQC_OK;
 }
 
+// The generated kernels' per-sample tables, once per call before the passes
+// (the passes read them through PassArgs::tabs / gsig / esig).
+int launch_tables(const vqc_circuit* c, vqc::PassArgs a, int64_t batch, void* stream) {
+  if (!c->jit.tables || batch == 0) return 0;
+  return vqc::jit_launch(c->jit.tables, batch, vqc::kTableThreads, &a, sizeof(a), stream);
+}
+
+void set_tables(vqc::PassArgs& a, unsigned char* ws, const StreamLayout& L) {
+  a.tabs = reinterpret_cast<float*>(ws + L.tabs);
+  a.gsig = reinterpret_cast<float*>(ws + L.gsig);
+  a.esig = reinterpret_cast<float*>(ws + L.esig);
+}
+
 // Streaming forward: every pass (the first starts from |0...0> or reads psi0),
 // then the <Z> reduction into expvals; the last pass writes probs.  fd_slots > 0:
 // the batch is the central differences' shifted copies of slots fd_base ..
@@ -251,6 +269,7 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     const size_t i = &pp - p.fpass.data();
     a.params = params;
     a.inputs = inputs;
+    set_tables(a, ws, L);
     a.psi_src = ws + L.psi;
     a.psi_dst = ws + L.psi;
     if (psi0 && (a.flags & vqc::PF_INIT)) {
@@ -262,6 +281,10 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     a.fd_slots = fd_slots;
     a.fd_h = fd_h;
     a.epart = reinterpret_cast<float*>(ws + L.epart);
+    if (i == 0) {
+      rc = launch_tables(c, a, batch, stream);
+      if (rc) return hip_fail("table kernel launch", rc);
+    }
     rc = c->engine == VQC_ENGINE_JIT
              ? vqc::jit_launch(c->jit.pass_fwd[i], batch << p.ng, 1 << (p.k - p.Rf), &a, sizeof(a),
                                stream)
@@ -296,6 +319,11 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     a.lam_src = ws + L.lamw;
     a.lam_dst = ws + L.lamw;
     a.gpart = gpart;
+    set_tables(a, ws, L);
+    if (first) {
+      rc = launch_tables(c, a, batch, stream);
+      if (rc) return hip_fail("table kernel launch", rc);
+    }
     rc = c->engine == VQC_ENGINE_JIT
              ? vqc::jit_launch(c->jit.pass_bwd[j], batch << p.ng, 1 << (p.k - p.Rb), &a, sizeof(a),
                                stream)

@@ -181,14 +181,33 @@ void emit_array(std::ostringstream& o, const char* type, const char* name, const
 // of the adjoint's gradients; and the <Z> signs.  esigns(): those signs.  The
 // block factors are products the schedule forms as it goes (bp).
 void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const Frame& fr,
-                 int nt) {
+                 int nt, bool all = false, bool load = false) {
   const int nocc = (int)p.occ_src.size(), W = t.W;
+  o << "static constexpr bool kLoadTables = " << (t.on && load ? "true" : "false") << ";\n"
+    << "static constexpr uint32_t kOffGm = " << t.off_gm << "u;\n";
   if (!t.on) {
     o << "struct Pre {};\n"
       << "__device__ __forceinline__ static Pre preload(int) { return Pre(); }\n"
       << "__device__ __forceinline__ static void prepare(const Walk&, int, int, const Pre&) {}\n"
       << "__device__ __forceinline__ static const float* esigns(const Walk&) { return nullptr; }\n";
     return;
+  }
+  if (load) {
+    // the pass reads the sample's tables that the table kernel wrote
+    o << "__device__ __forceinline__ static void load_tables(const Walk& w, const PassArgs& A, "
+         "int64_t b, int tid, int nt) {\n"
+      << "  float2* tab = const_cast<float2*>(w.tab);\n"
+      << "  const float2* T = reinterpret_cast<const float2*>(A.tabs) + b * " << nocc << ";\n"
+      << "  for (int i = tid; i < " << nocc << "; i += nt) tab[i] = T[i];\n";
+    if (!t.bocc.empty())
+      o << "  float* gm = reinterpret_cast<float*>(w.smem + " << t.off_gm << "u);\n"
+        << "  const float* G = A.gsig + b * " << nocc << ";\n"
+        << "  for (int i = tid; i < " << nocc << "; i += nt) gm[i] = G[i];\n";
+    if (t.esign)
+      o << "  float* es = reinterpret_cast<float*>(w.smem + " << t.off_es << "u);\n"
+        << "  for (int q = tid; q < " << p.n << "; q += nt) es[q] = A.esig[b * " << p.n
+        << " + q];\n";
+    o << "}\n";
   }
   // instances: the forward stream's rotations, then the adjoint's
   std::vector<int> inst = t.focc;
@@ -280,8 +299,10 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
     << (pre ? "pre.r[rr * " + std::to_string(W) + " + j]" : "kArow[i * " + std::to_string(W) + " + j]")
     << ");\n"
     << "    if (f) {\n"
-    << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n"
-    << "    } else {\n";
+    << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n";
+  if (all)  // the table kernel: every occurrence's t and gradient sign
+    o << "      gm[k] = (par & 1u) ? -1.f : 1.f;\n";
+  o << "    } else {\n";
   if (nf == 0)  // a lone adjoint stream applies the signs itself
     o << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n";
   o << "      gm[k] = (par & 1u) ? -1.f : 1.f;\n"
@@ -730,7 +751,8 @@ void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
 // (when `tables`) the kernel's tangent-form tables.
 void emit_sched_struct(std::ostringstream& o, const std::string& name, const Plan& p,
                        const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S,
-                       const GradMode& gm, const TanMode& tm, const Frame* tables, int map_off) {
+                       const GradMode& gm, const TanMode& tm, const Frame* tables, int map_off,
+                       bool load = false) {
   o << "struct " << name << " {\n";
   emit_constants(o, p, map_off);
   o
@@ -751,7 +773,7 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
   o << "}\n"
     << "__device__ __forceinline__ static float lane_sum(float v, const Walk&) {\n"
     << "  return group_sum<" << gm.tm << ">(v);\n}\n";
-  if (tables) emit_tables(o, p, tm, *tables, S << (k - R));
+  if (tables) emit_tables(o, p, tm, *tables, S << (k - R), false, load);
   o << "};\n";
 }
 
@@ -771,14 +793,15 @@ bool tangent_wanted(int S, int R) {
 // (adjoint).
 std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
                         const uint32_t* ins, int n_ins, bool bwd, bool stream, int R, int S,
-                        int threads, size_t lds, int n_slots, bool esign, int map_off) {
+                        int threads, size_t lds, int n_slots, bool esign, int map_off,
+                        bool load = false) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
   const int lanes = stream ? threads : 1 << (p.k - R);
   TanMode tm = tan_mode(p, bwd ? nullptr : ins, n_ins, bwd ? ins : nullptr, n_ins, S, esign, lds);
   tm.on = tm.on && tangent_wanted(S, R);
   emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr,
-                    map_off);
+                    map_off, load);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << name
     << (stream ? "(const vqc::PassArgs A) {\n" : "(const vqc::TileArgs A) {\n")
@@ -816,6 +839,37 @@ std::string step_unit(const Plan& p, const Frame& fr) {
 
 }  // namespace
 
+// The table kernel of a streaming circuit: the angle table and the frame signs
+// of every occurrence, per sample (table_body), or "" when they do not fit in
+// LDS (the passes then compute their own).
+std::string table_unit(const Plan& p, const Frame& fr) {
+  TanMode t;
+  const int nocc = (int)p.occ_src.size();
+  t.W = std::max(1, (nocc + 31) / 32);
+  for (int k = 0; k < nocc; ++k) t.focc.push_back(k);
+  t.esign = true;
+  size_t off = align16((size_t)std::max(nocc, 1) * 8);
+  t.off_bits = off;
+  off = align16(off + (size_t)(t.W + 1) * 4);
+  t.off_gm = off;
+  off = align16(off + (size_t)std::max(nocc, 1) * 4);
+  t.off_es = off;
+  off = align16(off + (size_t)p.n * 4);
+  t.end = off;
+  t.on = nocc > 0 && t.end <= (size_t)kLdsBytes;
+  if (!t.on) return "";
+  std::ostringstream o;
+  o << "#include \"vqc_device.h\"\nnamespace vqc {\nstruct Sched {\n";
+  emit_constants(o, p, p.end_off);
+  emit_tables(o, p, t, fr, kTableThreads, true);
+  o << "};\n}  // namespace vqc\n"
+    << "extern \"C\" __global__ void __launch_bounds__(" << kTableThreads
+    << ") vqc_st(const vqc::PassArgs A) {\n"
+    << "  __shared__ __align__(16) unsigned char smem[" << t.end << "];\n"
+    << "  vqc::table_body<" << kTableThreads << ", vqc::Sched>(A, smem);\n}\n";
+  return o.str();
+}
+
 std::vector<JitUnit> jit_units(const Plan& p) {
   std::vector<JitUnit> u;
   const Frame fr = frame_rows(p);
@@ -829,20 +883,23 @@ std::vector<JitUnit> jit_units(const Plan& p) {
     u.push_back({"vqc_rs", step_unit(p, fr)});
     return u;
   }
+  const std::string tables = table_unit(p, fr);
+  const bool load = !tables.empty();
   for (size_t i = 0; i < p.fpass.size(); ++i) {
     const std::string name = "vqc_sf" + std::to_string(i);
     const PassPlan& pp = p.fpass[i];
     u.push_back({name, kernel_unit(p, fr, name, p.fwd.data() + 2 * pp.ins_off, pp.n_ins, false,
                                    true, p.Rf, 1, 1 << (p.k - p.Rf), p.lds_fwd, pp.n_slots,
-                                   (pp.flags & PF_ZPART) != 0, pp.end_off)});
+                                   (pp.flags & PF_ZPART) != 0, pp.end_off, load)});
   }
   for (size_t i = 0; i < p.bpass.size(); ++i) {
     const std::string name = "vqc_sb" + std::to_string(i);
     const PassPlan& pp = p.bpass[i];
     u.push_back({name, kernel_unit(p, fr, name, p.bwd.data() + 2 * pp.ins_off, pp.n_ins, true,
                                    true, p.Rb, 1, 1 << (p.k - p.Rb), p.lds_bwd, pp.n_slots,
-                                   (pp.flags & PF_MAKE_LAMBDA) != 0, pp.start_off)});
+                                   (pp.flags & PF_MAKE_LAMBDA) != 0, pp.start_off, load)});
   }
+  if (load) u.push_back({"vqc_st", tables});
   return u;
 }
 
@@ -1065,8 +1122,10 @@ int jit_build(const Plan& p, int device, JitKernels& out, std::string& msg) {
     out.res_bwd = fns[1];
     out.res_step = fns[2];
   } else {
-    out.pass_fwd.assign(fns.begin(), fns.begin() + p.fpass.size());
-    out.pass_bwd.assign(fns.begin() + p.fpass.size(), fns.end());
+    const size_t nf = p.fpass.size(), nb = p.bpass.size();
+    out.pass_fwd.assign(fns.begin(), fns.begin() + nf);
+    out.pass_bwd.assign(fns.begin() + nf, fns.begin() + nf + nb);
+    if (fns.size() > nf + nb) out.tables = fns[nf + nb];
   }
   return VQC_OK;
 }

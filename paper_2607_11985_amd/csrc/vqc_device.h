@@ -1141,6 +1141,8 @@ struct InterpSched {
   static constexpr int kN = -1;
   // occurrences and samples per workgroup when fixed at compile time, else -1
   static constexpr int kNocc = -1, kS = -1;
+  // the streaming passes compute their tables (no per-sample table kernel)
+  static constexpr bool kLoadTables = false;
   // physical bit of qubit q under the mapping the epilogue / lambda use
   __device__ __forceinline__ static int phys_of(const uint8_t* phys, int q) { return phys[q]; }
   __device__ __forceinline__ static OccRec occ(const int32_t* src, const int32_t* idx,
@@ -1528,6 +1530,36 @@ __device__ __forceinline__ void load_tile(St<R>& a, const float2* src, uint32_t 
   for (int j = 0; j < (1 << R); ++j) split(v[j], a.r[j], a.i[j]);
 }
 
+// The per-sample tables of the streaming passes (generated kernels, tangent
+// form): one workgroup per sample computes the angle table and the frame
+// signs of every occurrence (Sched::prepare over all of them) once, and
+// writes (t, cos phi'), the adjoint's gradient signs and the <Z> signs for
+// every pass of the call to read (so that no pass repeats the sincos, the
+// divisions and the parity sums).
+template <int WG, typename Sched>
+__device__ __forceinline__ void table_body(const PassArgs& A, unsigned char* smem) {
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.x;
+  Walk w;
+  w.tab = reinterpret_cast<float2*>(smem);
+  w.smem = smem;
+  const typename Sched::Pre pre = Sched::preload(tid);
+  angle_table<Sched>(const_cast<float2*>(w.tab), A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx,
+                     A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F, tid, WG, A.P,
+                     A.fd_slots, A.fd_h, A.fd_base);
+  __syncthreads();
+  Sched::prepare(w, tid, WG, pre);  // ends with a barrier
+  const float* gm = reinterpret_cast<const float*>(smem + Sched::kOffGm);
+  const float* es = Sched::esigns(w);
+  float2* T = reinterpret_cast<float2*>(A.tabs) + b * A.n_occ;
+  float* Gs = A.gsig + b * A.n_occ;
+  for (int i = tid; i < A.n_occ; i += WG) {
+    T[i] = w.tab[i];
+    Gs[i] = gm[i];
+  }
+  for (int q = tid; q < A.n; q += WG) A.esig[b * A.n + q] = es[q];
+}
+
 template <bool BWD, int R, int K, typename Sched>
 __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* smem) {
   static_assert(K <= kMaxTileQubits && K - R >= 6, "tile shape");
@@ -1561,14 +1593,22 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
 
-  const typename Sched::Pre pre = Sched::preload(tid);
-  angle_table<Sched>(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma,
-                     A.params, A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots, A.fd_h,
-                     A.fd_base);
-  if (BWD)
-    for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
-  __syncthreads();
-  Sched::prepare(w, tid, WG, pre);
+  if constexpr (Sched::kLoadTables) {
+    // the sample's tables, written once per call by the table kernel
+    Sched::load_tables(w, A, b, tid, WG);
+    if (BWD)
+      for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
+    __syncthreads();
+  } else {
+    const typename Sched::Pre pre = Sched::preload(tid);
+    angle_table<Sched>(tab, A.n_occ, 1, b, A.B, A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma,
+                       A.params, A.pstride, A.inputs, A.F, tid, WG, A.P, A.fd_slots, A.fd_h,
+                       A.fd_base);
+    if (BWD)
+      for (int i = tid; i < A.n_pslots * G; i += WG) acc[i] = 0.f;
+    __syncthreads();
+    Sched::prepare(w, tid, WG, pre);
+  }
 
   uint32_t base, off[NA];
   io_offsets<R>(A.io, A.k, A.ng, tid, g, base, off);

@@ -104,7 +104,9 @@ struct JitKernels {
   void* res_bwd = nullptr;
   void* res_step = nullptr;           // forward, loss head and adjoint in one launch
   std::vector<void*> pass_fwd, pass_bwd;
+  void* tables = nullptr;             // streaming: the per-sample table kernel, or none
 };
+constexpr int kTableThreads = 256;    // threads of the table kernel's workgroups
 struct JitUnit {
   std::string name, src;
 };

@@ -139,5 +139,11 @@ struct PassArgs {
   // central differences: B counts shifted copies, 2 per slot of the chunk
   int32_t fd_slots, fd_base;   // slots fd_base .. fd_base + fd_slots - 1, or fd_slots 0
   float fd_h;
+  // per-sample tables of the generated kernels' tangent form, written once per
+  // call by the table kernel and read by every pass: (t, cos phi') pairs
+  // [B][n_occ][2], the adjoint's gradient signs [B][n_occ], the <Z> signs [B][n]
+  float* tabs;
+  float* gsig;
+  float* esig;
 };
 }  // namespace vqc
