@@ -395,15 +395,17 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
     delete c;
     return fail(rc, msg);
   }
-  // Default tiles of the generated kernels: 12 qubits when that takes no more
-  // passes than 13 (four workgroups per CU instead of two; measured 1.6 %
-  // faster on the 14-qubit re-uploading workload), else 13.
+  // Default tiles of the generated kernels: 12 qubits unless that takes more
+  // than a quarter more passes than 13.  Four workgroups per CU instead of two
+  // hide more latency: measured 1.6-4 % faster on the 14-qubit re-uploading
+  // workload (same passes) and 3.5 % on the 16-qubit ring (29 passes, not 24).
   if (engine == VQC_ENGINE_JIT && tile == 0 && c->plan.path == VQC_PATH_STREAM) {
     Plan p12;
     std::string msg12;
+    const size_t n13 = c->plan.fpass.size() + c->plan.bpass.size();
     if (vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, reg_bits, p12, msg12, true, 12) ==
             0 &&
-        p12.fpass.size() + p12.bpass.size() <= c->plan.fpass.size() + c->plan.bpass.size())
+        4 * (p12.fpass.size() + p12.bpass.size()) <= 5 * n13)
       c->plan = std::move(p12);
   }
   c->device = device;
