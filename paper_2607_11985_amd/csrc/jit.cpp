@@ -454,10 +454,14 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   const bool tan = tm.on;
   const int nrot = (int)(bwd ? tm.bocc.size() : tm.focc.size());
   int m = 0;  // rotation index in the stream
-  // batched only with up to 8 amplitudes per thread: with 16 the sixteen
-  // pending partials no longer fit beside psi and lambda, and the per-rotation
-  // group sum is a small part of a rotation's work there anyway
-  const bool batched = bwd && gm.regs && gm.tm == 64 && R <= 3;
+  // batched up to 8 amplitudes per thread, and with 16 in the streaming passes
+  // (the pending partials fit beside psi and lambda: 109-120 VGPRs, four waves
+  // per SIMD; the 16-qubit adjoint 15 % fewer instructions, 1.93 -> 1.79 ms).
+  // The resident 16-amplitude kernels are left out: there the partials took
+  // the kernel from 108 to 147 VGPRs and one wave per SIMD, and the 12-qubit
+  // step ran 5 % slower.
+  const bool batched =
+      bwd && gm.regs && gm.tm == 64 && (R <= 3 || (R == 4 && p.path == VQC_PATH_STREAM));
   Pending pend;
   if (batched)
     o << "  float pd0 = 0.f, pd1 = 0.f, pd2 = 0.f, pd3 = 0.f, pd4 = 0.f, pd5 = 0.f, pd6 = 0.f, "
