@@ -474,6 +474,20 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   // one sample per workgroup and 4 amplitudes per thread (latency-bound): the
   // angle table, and the adjoint's gradient signs, in registers (table_row)
   const bool sreg = S == 1 && R <= 2;
+  // several samples per wave (small states): each lane reads its sample's
+  // (cos, sin) of every rotation of the stream into registers at once, when
+  // they are few, instead of one LDS read (and its latency) per gate
+  std::vector<int> used;
+  for (int pc = 0; pc < n_ins; ++pc) {
+    const int op = ins[2 * pc] & 31;
+    if (op == OP_RX || op == OP_RY || op == OP_RZ) used.push_back((int)ins[2 * pc + 1]);
+  }
+  std::sort(used.begin(), used.end());
+  used.erase(std::unique(used.begin(), used.end()), used.end());
+  const bool vreg = !tan && S > 1 && used.size() <= 32;
+  if (vreg)
+    for (int k : used)
+      o << "  const float2 V" << k << " = w.tab[" << k << " * " << S << " + w.sl];\n";
   if (sreg) {
     int last = -1;
     for (int pc = 0; pc < n_ins; ++pc) {
@@ -621,6 +635,8 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         } else {
           if (sreg)
             o << "  { const float2 cs = table_entry<" << arg % 64 << ">(T" << arg / 64 << "); ";
+          else if (vreg)
+            o << "  { const float2 cs = V" << arg << "; ";
           else
             o << "  { const float2 cs = w.tab[" << at << "]; ";
           // RX / RY off the register bits sit on a lane bit (planner option)
