@@ -214,11 +214,13 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
   inst.insert(inst.end(), t.bocc.begin(), t.bocc.end());
   std::vector<uint32_t> rows;
   for (int k : inst)
-    for (int j = 0; j < W; ++j) rows.push_back(j < fr.words ? fr.arow[(size_t)k * fr.words + j] : 0u);
+    for (int j = 0; j < W; ++j)
+      rows.push_back(j < fr.words ? fr.arow[(size_t)k * fr.words + j] : 0u);
   std::vector<uint32_t> erows;
   if (t.esign)
     for (int q = 0; q < p.n; ++q)
-      for (int j = 0; j < W; ++j) erows.push_back(j < fr.words ? fr.erow[(size_t)q * fr.words + j] : 0u);
+      for (int j = 0; j < W; ++j)
+        erows.push_back(j < fr.words ? fr.erow[(size_t)q * fr.words + j] : 0u);
   const int nf = (int)t.focc.size(), ni = (int)inst.size();
   // preload(): each thread's entries of the constant rows, read before the
   // angle table (their latency then overlaps its loads) when they fit in a
@@ -256,7 +258,8 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
     o << "  (void)tid;\n";
   }
   o << "  return p;\n}\n"
-    << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt, const Pre& pre) {\n"
+    << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt, "
+       "const Pre& pre) {\n"
     << "  (void)pre;\n"
     << "  float2* tab = const_cast<float2*>(w.tab);\n"
     << "  float* tx = reinterpret_cast<float*>(tab);  // tab[k].x = tx[2 k]\n"
@@ -296,7 +299,8 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
   o << "    uint32_t par = 0u;\n"
     << "#pragma unroll\n"
     << "    for (int j = 0; j < " << W << "; ++j) par ^= __builtin_popcount(bits[j] & "
-    << (pre ? "pre.r[rr * " + std::to_string(W) + " + j]" : "kArow[i * " + std::to_string(W) + " + j]")
+    << (pre ? "pre.r[rr * " + std::to_string(W) + " + j]"
+            : "kArow[i * " + std::to_string(W) + " + j]")
     << ");\n"
     << "    if (f) {\n"
     << "      if (par & 1u) tx[2 * k] = -tx[2 * k];\n";
