@@ -534,7 +534,9 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       case OP_CNOT: {
         const char* sts[2] = {"a", "l"};
         for (int s = 0; s < (bwd ? 2 : 1); ++s) {
-          if (pb >= R)  // target on a lane bit
+          if (pb >= R && pa >= R + 2 && pa < R + 6)  // lane target, bank / row control
+            o << "  cnot_ll<R, " << pb - R << ", " << pa - R << ">(" << sts[s] << ");\n";
+          else if (pb >= R)  // target on a lane bit
             o << (pa < R ? "  cnot_rl<R, " + std::to_string(pa) + ", " + std::to_string(pb - R) +
                                ">(" + sts[s] + ");\n"
                          : "  cnot_tl<R, " + std::to_string(pb - R) + ">(" + sts[s] +

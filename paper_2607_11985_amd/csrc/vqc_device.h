@@ -791,6 +791,37 @@ __device__ __forceinline__ void cnot_tl(St<R>& a, uint32_t flag) {
   }
 }
 
+// CNOT with the target on lane bit J and the control on lane bit C >= 2: the
+// lanes with the control set are whole DPP banks (C = 2, 3: lane bits 2 and 3
+// within a row) or rows (C = 4, 5), so one DPP move under that mask gives them
+// the partner's value while the others keep their own (no select).
+template <int J, int ROW, int BANK>
+__device__ __forceinline__ float masked_xlane(float v) {
+  static_assert(J >= 0 && J < 4, "lane bit");
+  const int x = __float_as_int(v);
+  if constexpr (J == 0)
+    return __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0xB1, ROW, BANK, false));
+  else if constexpr (J == 1)
+    return __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x4E, ROW, BANK, false));
+  else if constexpr (J == 2)
+    return __int_as_float(__builtin_amdgcn_update_dpp(
+        x, __float_as_int(mov_dpp_f<0x141>(v)), 0x1B, ROW, BANK, false));
+  else
+    return __int_as_float(__builtin_amdgcn_update_dpp(x, x, 0x128, ROW, BANK, false));
+}
+
+template <int R, int J, int C>
+__device__ __forceinline__ void cnot_ll(St<R>& a) {
+  static_assert(C >= 2 && C <= 5 && C != J, "control on a bank or row bit");
+  constexpr int BANK = C == 2 ? 0xA : C == 3 ? 0xC : 0xF;
+  constexpr int ROW = C == 4 ? 0xA : C == 5 ? 0xC : 0xF;
+#pragma unroll
+  for (int u = 0; u < St<R>::N; ++u) {
+    a.r[u] = masked_xlane<J, ROW, BANK>(a.r[u]);
+    a.i[u] = masked_xlane<J, ROW, BANK>(a.i[u]);
+  }
+}
+
 // Sum over aligned groups of W lanes (W a power of two <= 64).  Every lane of a
 // group ends with the group's sum; the pairing order is fixed, so the result is
 // deterministic.  Pairs, quads, 8- and 16-lane rows use DPP (quad_perm 1032 and
