@@ -423,3 +423,31 @@ def test_autograd_function(torch_mod):
     check_E(E.detach().cpu().numpy(), Er)
     check_grads({"dp": p.grad.cpu().numpy(), "dx": x.grad.cpu().numpy()}, dpr, dxr,
                 np.ones((w.batch, 4)))
+
+
+@pytest.mark.parametrize("n,reg_bits,loss", [(9, 2, "mse_meanz"), (11, 2, "mean"), (8, 3, "mse_z0")])
+def test_four_amplitude_kernels_spanning_waves(torch_mod, n, reg_bits, loss):
+    """Four amplitudes per thread with a sample over several waves (lane-bit
+    gates, lane swaps, exchanges across waves, the tangent form's factor
+    tables), and eight per thread at n = 8: forward, adjoint and the one-launch
+    training step against the oracle."""
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit
+    ops, P, F = W.random_circuit(n, 12 * n, seed=16000 + n)
+    B = 5
+    params, inputs = W.random_inputs(B, P, F, seed=16100 + n)
+    cot = W.random_cotangent(B, n, seed=16200 + n)
+    note(f"4-amplitude kernels n={n} reg_bits={reg_bits}")
+    r = gpu_run(torch, ops, n, P, F, params, inputs, cot, reg_bits=reg_bits)
+    dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
+    check_E(r["E"], Er)
+    check_grads(r, dpr, dxr, cot)
+    y = np.random.default_rng(16300 + n).uniform(-1, 1, size=B).astype(np.float32)
+    c = Circuit(ops, n, P, F, reg_bits=reg_bits)
+    E, dp, dx, g = c.train_step(torch.from_numpy(params).cuda(), torch.from_numpy(inputs).cuda(),
+                                loss, torch.from_numpy(y).cuda(), want_cot=True)
+    torch.cuda.synchronize()
+    E, dp, dx, g = (t.cpu().numpy() for t in (E, dp, dx, g))
+    check_E(E, oracle.forward(ops, n, params, inputs))
+    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, g.astype(np.float64))
+    check_grads({"dp": dp, "dx": dx}, dpr, dxr, g)
