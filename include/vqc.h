@@ -145,9 +145,11 @@ typedef struct {
                               samples.  Inputs stay per sample.  0: per-sample
                               rows [B, P] */
     int32_t tile_qubits; /* streaming path: qubits per tile, 12, 13 or 14
-                            (0 = the default: 13 with the generated kernels,
-                            14 with the interpreter).  Each qubit less halves
-                            a workgroup's LDS, so more workgroups share a CU
+                            (0 = the default: with the generated kernels 12,
+                            unless its plan takes more than a quarter more
+                            passes than 13, then 13; 14 with the
+                            interpreter).  Each qubit less halves a
+                            workgroup's LDS, so more workgroups share a CU
                             and one's HBM traffic overlaps another's compute,
                             at the cost of more passes where the circuit
                             needs them.  12 and 13: generated kernels only
