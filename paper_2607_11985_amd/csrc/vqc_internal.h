@@ -70,9 +70,11 @@ struct HostOp {
 constexpr int kNumGateKinds = 32;  // VQC_RX .. VQC_CSWAP
 // lane_gates: the schedule may put RX / RY / CNOT targets on lane bits (only
 // the generated kernels run such schedules).
-// tile_qubits: streaming tile size (0 = default).
+// tile_qubits: streaming tile size (0 = default).  bwd_reg_bits: register
+// bits of the streaming adjoint when reg_bits is 0 (0 = default).
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
-               Plan& plan, std::string& msg, bool lane_gates, int tile_qubits = 0);
+               Plan& plan, std::string& msg, bool lane_gates, int tile_qubits = 0,
+               int bwd_reg_bits = 0);
 // OpenQASM front end (qasm.cpp).  Returns 0 or a VQC_ERR_* code with msg.
 int parse_qasm(const char* source, const char* input_names, std::vector<vqc_op>& ops,
                int& n_qubits, int& n_params, int& n_inputs, std::string& msg);
