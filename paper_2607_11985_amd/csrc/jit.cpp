@@ -498,12 +498,21 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       const int op = ins[2 * pc] & 31;
       if (op == OP_RX || op == OP_RY || op == OP_RZ) last = std::max(last, (int)ins[2 * pc + 1]);
     }
+    // the sample's thread bits, computed once: with one wave per SIMD there
+    // are registers to spare, and each lane-bit gate then skips recomputing
+    // its bit (and the sign mask formed from it) from an opaque copy of tb
+    for (int j = 0; j < t; ++j)
+      o << "  const uint32_t hb" << j << " = (w.tb >> " << j << ") & 1u;\n";
     for (int m = 0; 64 * m <= last; ++m) {
       o << "  const float2 T" << m << " = table_row(w, " << m << ", " << last << ");\n";
       if (tan && bwd)
         o << "  const float G" << m << " = table_row(gmul, " << m << ", " << last << ");\n";
     }
   }
+  // a thread bit of the amplitude position (physical bit p >= R)
+  auto bit = [&](int p) {
+    return sreg ? "hb" + std::to_string(p - R) : "tile_bit<R>(w, " + std::to_string(p) + ")";
+  };
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
     const int op = w0 & 31, pa = (w0 >> 5) & 31, pb = (w0 >> 10) & 31;
@@ -539,12 +548,12 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           else if (pb >= R)  // target on a lane bit
             o << (pa < R ? "  cnot_rl<R, " + std::to_string(pa) + ", " + std::to_string(pb - R) +
                                ">(" + sts[s] + ");\n"
-                         : "  cnot_tl<R, " + std::to_string(pb - R) + ">(" + sts[s] +
-                               ", tile_bit<R>(w, " + std::to_string(pa) + "));\n");
+                         : "  cnot_tl<R, " + std::to_string(pb - R) + ">(" + sts[s] + ", " +
+                               bit(pa) + ");\n");
           else if (pa < R)
             o << "  cnot_rr<R, " << pa << ", " << pb << ">(" << sts[s] << ");\n";
           else
-            o << "  cnot_tr<R, " << pb << ">(" << sts[s] << ", tile_bit<R>(w, " << pa << "));\n";
+            o << "  cnot_tr<R, " << pb << ">(" << sts[s] << ", " << bit(pa) << ");\n";
         }
         break;
       }
@@ -611,7 +620,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           o << "const float t = tc.x; ";
           // RX / RY off the register bits sit on a lane bit (planner option)
           const std::string lane = std::to_string(pa - R);
-          const std::string hi = "tile_bit<R>(w, " + std::to_string(pa) + ")";
+          const std::string hi = pa >= R ? bit(pa) : "0u";
           if (!bwd) {
             if (reg)
               o << kind << "_t<R, " << pa << ">(a, t);";
@@ -647,7 +656,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
             o << "  { const float2 cs = w.tab[" << at << "]; ";
           // RX / RY off the register bits sit on a lane bit (planner option)
           const std::string lane = std::to_string(pa - R);
-          const std::string hi = "tile_bit<R>(w, " + std::to_string(pa) + ")";
+          const std::string hi = pa >= R ? bit(pa) : "0u";
           if (!bwd) {
             if (reg)
               o << kind << "_reg<R, " << pa << ">(a, cs.x, cs.y);";
