@@ -498,20 +498,24 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       const int op = ins[2 * pc] & 31;
       if (op == OP_RX || op == OP_RY || op == OP_RZ) last = std::max(last, (int)ins[2 * pc + 1]);
     }
-    // the sample's thread bits, computed once: with one wave per SIMD there
-    // are registers to spare, and each lane-bit gate then skips recomputing
-    // its bit (and the sign mask formed from it) from an opaque copy of tb
-    for (int j = 0; j < t; ++j)
-      o << "  const uint32_t hb" << j << " = (w.tb >> " << j << ") & 1u;\n";
     for (int m = 0; 64 * m <= last; ++m) {
       o << "  const float2 T" << m << " = table_row(w, " << m << ", " << last << ");\n";
       if (tan && bwd)
         o << "  const float G" << m << " = table_row(gmul, " << m << ", " << last << ");\n";
     }
   }
+  // The sample's thread bits, computed once in the 4-amplitude kernels: their
+  // few waves leave registers to spare, and each lane-bit gate then skips
+  // recomputing its bit (and the sign mask formed from it) from an opaque
+  // copy of tb, which keeps the big kernels from holding masks across the
+  // schedule.
+  const bool hbits = R <= 2;
+  if (hbits)
+    for (int j = 0; j < t; ++j)
+      o << "  const uint32_t hb" << j << " = (w.tb >> " << j << ") & 1u;\n";
   // a thread bit of the amplitude position (physical bit p >= R)
   auto bit = [&](int p) {
-    return sreg ? "hb" + std::to_string(p - R) : "tile_bit<R>(w, " + std::to_string(p) + ")";
+    return hbits ? "hb" + std::to_string(p - R) : "tile_bit<R>(w, " + std::to_string(p) + ")";
   };
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
