@@ -180,3 +180,29 @@ def test_layers_sharing_one_angle(torch_mod, n):
     dpr, dxr, Er = oracle.vjp(layers, n, params, inputs, cot)
     check_E(r["E"], Er)
     check_grads(r, dpr, dxr, cot)
+
+
+@pytest.mark.parametrize("n", [6, 8, 9])
+def test_cnot_on_every_qubit_pair(torch_mod, n):
+    """CNOTs between every ordered pair of qubits, between rotation layers, so
+    that controls and targets meet on register bits, lane bits (DPP moves, the
+    masked moves of controls on lane bits 2-5) and wave bits."""
+    ops = []
+    k = 0
+    for c in range(n):
+        ops += [W.Op("RY", (q,), (("param", k + q),)) for q in range(n)]
+        k += n
+        for t in range(n):
+            if t != c:
+                ops.append(W.Op("CNOT", (c, t)))
+        ops += [W.Op("RX", (q,), (("input", q),)) for q in range(n)]
+    P, F = k, n
+    B = 3
+    params, inputs = W.random_inputs(B, P, F, seed=13100 + n)
+    cot = W.random_cotangent(B, n, seed=13200 + n)
+    note(f"cnot pairs n={n}")
+    dpr, dxr, Er = oracle.vjp(ops, n, params, inputs, cot)
+    for reg_bits in (0, 2):
+        r = gpu_run(torch_mod, ops, n, P, F, params, inputs, cot, reg_bits=reg_bits)
+        check_E(r["E"], Er)
+        check_grads(r, dpr, dxr, cot)
