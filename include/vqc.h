@@ -54,7 +54,7 @@ extern "C" {
 /* status codes */
 #define VQC_OK 0
 #define VQC_ERR_INVALID_ARG -1 /* bad argument: null pointer, bad wire, bad index */
-#define VQC_ERR_UNSUPPORTED -2 /* valid request this build cannot run */
+#define VQC_ERR_UNSUPPORTED -2 /* valid request the library does not support */
 #define VQC_ERR_TOO_LARGE -3   /* size limits exceeded (qubits, batch, schedule) */
 #define VQC_ERR_WORKSPACE -4   /* workspace missing or smaller than required */
 #define VQC_ERR_HIP -5         /* a HIP runtime call failed */
