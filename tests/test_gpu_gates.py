@@ -8,6 +8,7 @@ import pytest
 
 import oracle
 from paper_2607_11985_amd import workloads as W
+from tests.parity_util import check_step, fd_bound, oracle_central_differences
 from tests.test_gpu_parity import (check_E, check_grad, check_grads, gpu_run, note,  # noqa: F401
                                    samples_per_wg, torch_mod)
 
@@ -97,10 +98,7 @@ def test_general_gates_train_step(torch_mod, n, loss, path):
                                 loss, torch.from_numpy(y).cuda(), want_cot=True)
     torch.cuda.synchronize()
     E, dp, dx, g = (t.cpu().numpy() for t in (E, dp, dx, g))
-    Er = oracle.forward(ops, n, params, inputs)
-    check_E(E, Er)
-    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, g.astype(np.float64))
-    check_grads({"dp": dp, "dx": dx}, dpr, dxr, g)
+    check_step(E, g, dp, dx, ops, n, params, inputs, y.astype(np.float64), loss, B)
 
 
 def test_general_gates_shared_params(torch_mod):
@@ -128,8 +126,8 @@ def test_general_gates_shared_params(torch_mod):
 
 
 def test_affine_fd_backward(torch_mod):
-    """Central differences move the source value (then mul * value + add), so
-    they approximate the same chain-rule gradient the oracle gives."""
+    """Central differences move the source value (then mul * value + add): the
+    same differences at the same h on the oracle side, bound by fd_bound."""
     torch = torch_mod
     from paper_2607_11985_amd.api import Circuit
     n, B = 6, 3
@@ -139,22 +137,12 @@ def test_affine_fd_backward(torch_mod):
     cot = W.random_cotangent(B, n, seed=12900)
     note("affine fd backward")
     c = Circuit(ops, n, P, F)
-    h = 1e-2
+    h = 0.25
     dp, dx = c.fd_backward(torch.from_numpy(params).cuda(), torch.from_numpy(inputs).cuda(),
                            torch.from_numpy(cot).cuda(), h=h)
     torch.cuda.synchronize()
-    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, cot)
-    # truncation h^2/6 |f'''| with f''' bounded by (sum over uses of |mul|)^3 sum|g|,
-    # plus the float32 rounding of E (2e-5 per evaluation) over h
-    uses = {}
-    for o in ops:
-        for spec in o.angles:
-            if spec[0] != "const":
-                m = abs(spec[2]) if len(spec) > 2 else 1.0
-                uses[(spec[0], spec[1])] = uses.get((spec[0], spec[1]), 0.0) + m
-    k = max(uses.values())
-    gs = np.sum(np.abs(cot), axis=1, keepdims=True)
-    bound = (h * h / 6 * k ** 3 + 2e-5 * max(k, 1.0) / h) * gs
+    dpr, dxr = oracle_central_differences(ops, n, params, inputs, cot, h)
+    bound = fd_bound(ops, params, inputs, cot, h)
     assert np.all(np.abs(dp.cpu().numpy() - dpr) <= bound)
     assert np.all(np.abs(dx.cpu().numpy() - dxr) <= bound)
 

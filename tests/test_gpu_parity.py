@@ -1,29 +1,21 @@
 """GPU parity: the HIP path (through the C ABI) against the double-precision oracle.
 
-Bars (complex64 on the GPU, complex128 in the oracle):
-  E      : max |E - E_ref| <= 1e-5 (absolute)
-  grads  : per sample row, over the row's whole gradient vector (every parameter and
-           every input of that sample together),
-           max |g - g_ref| <= 1e-4 * max |g_ref| + 1e-6 * sum_j |cot_j|
-           (row max-norm relative error; the floor, scaled by the cotangent, only
-           matters for rows whose gradient is all but zero)
+Bars (tests/parity_util.py): E within 1e-5 absolute; gradients per sample row
+within 1e-4 of the row's max-norm (+ a floor of 1e-6 sum |cot|), over the whole
+row and, with at least four parameters and four inputs, over each array.
 Every input and cotangent is seeded and synthetic and reaches both sides as the
 same float32 values; nothing the oracle sees comes from the GPU.
 """
-import sys
-
 import numpy as np
 import pytest
 
 import oracle
 from paper_2607_11985_amd import workloads as W
+from tests.parity_util import (E_TOL, G_FLOOR, G_REL, check_E, check_grad,  # noqa: F401
+                               check_grads, check_rows, check_step, fd_bound, gpu_run, note,
+                               oracle_central_differences)
 
 pytestmark = pytest.mark.gpu
-
-E_TOL = 1e-5
-G_REL = 1e-4
-G_FLOOR = 1e-6
-
 
 @pytest.fixture(scope="module")
 def torch_mod():
@@ -32,55 +24,6 @@ def torch_mod():
     from paper_2607_11985_amd import _lib
     _lib.load()  # fails loudly if the HIP library is not built
     return torch
-
-
-def note(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
-
-
-def gpu_run(torch, ops, n, P, F, params, inputs, cot=None, path="auto", engine="jit",
-            reg_bits=0):
-    from paper_2607_11985_amd.api import Circuit
-    circ = Circuit(ops, n, P, F, path=path, engine=engine, reg_bits=reg_bits)
-    p = torch.from_numpy(np.ascontiguousarray(params)).cuda()
-    x = torch.from_numpy(np.ascontiguousarray(inputs)).cuda()
-    E, ws = circ.forward(p, x, training=True)
-    out = {"E": None, "dp": None, "dx": None, "circ": circ}
-    if cot is not None:
-        g = torch.from_numpy(np.ascontiguousarray(cot, dtype=np.float32)).cuda()
-        dp, dx = circ.backward(p, x, g, ws)
-        torch.cuda.synchronize()
-        out["dp"], out["dx"] = dp.cpu().numpy(), dx.cpu().numpy()
-    torch.cuda.synchronize()
-    out["E"] = E.cpu().numpy()
-    return out
-
-
-def check_E(E, Eref):
-    err = float(np.max(np.abs(E.astype(np.float64) - Eref))) if E.size else 0.0
-    assert err <= E_TOL, f"E max abs err {err:.3e}"
-    return err
-
-
-def check_grads(r, dpr, dxr, cot):
-    """Row max-norm check of the concatenated [dparams | dinputs] vector."""
-    g = np.concatenate([r["dp"], r["dx"]], axis=1)
-    gref = np.concatenate([dpr, dxr], axis=1)
-    return check_grad(g, gref, cot, "gradient")
-
-
-def check_grad(g, gref, cot, what):
-    if g.size == 0:
-        return 0.0
-    g = g.astype(np.float64)
-    err = np.max(np.abs(g - gref), axis=1)
-    scale = np.max(np.abs(gref), axis=1)
-    floor = G_FLOOR * np.sum(np.abs(np.asarray(cot, dtype=np.float64)), axis=1)
-    bad = err > G_REL * scale + floor
-    assert not np.any(bad), (f"{what}: rows {np.nonzero(bad)[0][:8]} err {err[bad][:4]} "
-                             f"scale {scale[bad][:4]}")
-    return float(np.max(err / np.maximum(scale, 1e-30)))
 
 
 def samples_per_wg(n):
@@ -195,24 +138,6 @@ def test_config_full_batch_sampled(torch_mod, idx, rows):
     check_grads({"dp": r["dp"][rows], "dx": r["dx"][rows]}, dpr, dxr, cot[rows])
 
 
-def check_cot(g, E_ref, y, loss, batch):
-    """The step's cotangent against the loss head evaluated on the oracle's E
-    (batch: the batch size the MSE mean runs over)."""
-    n = E_ref.shape[1]
-    if loss == "sum":
-        ref = np.ones_like(E_ref)
-    elif loss == "mean":
-        ref = np.full_like(E_ref, 1.0 / n)
-    elif loss == "mse_z0":
-        ref = np.zeros_like(E_ref)
-        ref[:, 0] = 2.0 * (E_ref[:, 0] - y) / batch
-    else:
-        ref = np.repeat((2.0 * (E_ref.mean(axis=1) - y) / (n * batch))[:, None], n, axis=1)
-    # E is within E_TOL, so the cotangent is within 2 E_TOL / batch (+ rounding)
-    err = float(np.max(np.abs(g.astype(np.float64) - ref)))
-    assert err <= 2 * E_TOL / batch + 1e-6 * max(1.0, float(np.max(np.abs(ref)))), err
-
-
 @pytest.mark.parametrize("n,loss,path,engine", [
     (1, "sum", "auto", "jit"), (3, "mean", "auto", "jit"), (6, "mse_z0", "auto", "jit"),
     (8, "mse_meanz", "auto", "jit"), (9, "mse_meanz", "auto", "jit"), (12, "mse_z0", "auto", "jit"),
@@ -237,11 +162,7 @@ def test_train_step_parity(torch_mod, n, loss, path, engine):
     E, dp, dx, g = c.train_step(p, x, loss, yt, want_cot=True)
     torch.cuda.synchronize()
     E, dp, dx, g = (t.cpu().numpy() for t in (E, dp, dx, g))
-    Er = oracle.forward(ops, n, params, inputs)
-    check_E(E, Er)
-    check_cot(g, Er, y.astype(np.float64), loss, B)
-    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, g.astype(np.float64))
-    check_grads({"dp": dp, "dx": dx}, dpr, dxr, g)
+    check_step(E, g, dp, dx, ops, n, params, inputs, y.astype(np.float64), loss, B)
     # the separate calls give the same results (up to the compiler's rounding)
     E2, ws = c.forward(p, x, training=True)
     g2 = loss_grad(loss, E2, yt)
@@ -297,10 +218,10 @@ def test_shared_params_parity(torch_mod, n, path, engine):
                                              (10, "jit", True), (15, "jit", False),
                                              (14, "interp", True)])
 def test_fd_backward(torch_mod, n, engine, shared):
-    """Central differences through the shifted-batch forward, against the
-    oracle's exact gradient.  Bound: truncation h^2/6 times the third
-    derivative (at most k^3 sum|g| for a slot used by k gates), plus the
-    float32 rounding of E (2e-5 per evaluation, twice the tested bar) over h."""
+    """Central differences through the shifted-batch forward, against the same
+    differences at the same h on the oracle side (every slot moved in the
+    params / inputs arrays).  The truncation error is common to both, so the
+    bound is the float32 rounding of E over h (fd_bound)."""
     torch = torch_mod
     from paper_2607_11985_amd.api import Circuit
     ops, P, F = W.random_circuit(n, 30 + 4 * n, seed=9300 + n)
@@ -311,33 +232,26 @@ def test_fd_backward(torch_mod, n, engine, shared):
     cot = W.random_cotangent(B, n, seed=9500 + n)
     note(f"fd backward n={n} engine={engine} shared={shared}")
     c = Circuit(ops, n, P, F, engine=engine, shared_params=shared)
-    h = 1e-2
+    h = 0.25
     p = torch.from_numpy(np.ascontiguousarray(params[0] if shared else params)).cuda()
     dp, dx = c.fd_backward(p, torch.from_numpy(inputs).cuda(),
                            torch.from_numpy(cot.astype(np.float32)).cuda(), h=h)
     torch.cuda.synchronize()
-    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, cot)
+    dpr, dxr = oracle_central_differences(ops, n, params, inputs, cot, h)
+    bound = fd_bound(ops, params, inputs, cot, h)
     if shared:
         dpr = dpr.sum(axis=0, keepdims=True)
-    uses = {}
-    for o in ops:
-        for src, v in o.angles:
-            if src != "const":
-                uses[(src, v)] = uses.get((src, v), 0) + 1
-    k = max(uses.values())
-    gsum = np.sum(np.abs(cot), axis=1, keepdims=True)
-    if shared:
-        gsum = gsum.sum(keepdims=True)
-    bound = (h * h / 6 * k ** 3 + 2e-5 / h) * gsum
-    assert np.all(np.abs(dp.cpu().numpy().reshape(dpr.shape) - dpr) <= bound)
-    gsx = np.sum(np.abs(cot), axis=1, keepdims=True)
-    assert np.all(np.abs(dx.cpu().numpy() - dxr) <= (h * h / 6 * k ** 3 + 2e-5 / h) * gsx)
+        bp = bound.sum(keepdims=True)
+    else:
+        bp = bound
+    assert np.all(np.abs(dp.cpu().numpy().reshape(dpr.shape) - dpr) <= bp)
+    assert np.all(np.abs(dx.cpu().numpy() - dxr) <= bound)
 
 
 def test_fd_backward_streaming_chunks(torch_mod):
     """The 16-qubit workload's structure at B = 64: the shifted copies of all
     400 slots (51 GiB of states) run in chunks of 32 slots; sampled rows against
-    the oracle's exact gradient, with the bound of test_fd_backward."""
+    the oracle's differences at the same h."""
     torch = torch_mod
     from paper_2607_11985_amd.api import Circuit
     w = W.make_config(5, batch=64)
@@ -345,14 +259,13 @@ def test_fd_backward_streaming_chunks(torch_mod):
     note(f"fd backward streaming chunks {w.name} B={w.batch}")
     c = Circuit(w.ops, w.n_qubits, w.n_params, w.n_inputs)
     cot = W.random_cotangent(w.batch, w.n_qubits, seed=9600)
-    h = 1e-2
+    h = 0.25
     dp, dx = c.fd_backward(torch.from_numpy(w.params).cuda(), torch.from_numpy(w.inputs).cuda(),
                            torch.from_numpy(cot).cuda(), h=h)
     torch.cuda.synchronize()
-    dpr, dxr, _ = oracle.vjp(w.ops, w.n_qubits, w.params[rows], w.inputs[rows], cot[rows])
-    k = 1  # every parameter and input is used by one gate
-    gs = np.sum(np.abs(cot[rows]), axis=1, keepdims=True)
-    bound = (h * h / 6 * k ** 3 + 2e-5 / h) * gs
+    dpr, dxr = oracle_central_differences(w.ops, w.n_qubits, w.params[rows], w.inputs[rows],
+                                          cot[rows], h)
+    bound = fd_bound(w.ops, w.params[rows], w.inputs[rows], cot[rows], h)
     assert np.all(np.abs(dp.cpu().numpy()[rows] - dpr) <= bound)
     assert np.all(np.abs(dx.cpu().numpy()[rows] - dxr) <= bound)
 
@@ -448,6 +361,4 @@ def test_four_amplitude_kernels_spanning_waves(torch_mod, n, reg_bits, loss):
                                 loss, torch.from_numpy(y).cuda(), want_cot=True)
     torch.cuda.synchronize()
     E, dp, dx, g = (t.cpu().numpy() for t in (E, dp, dx, g))
-    check_E(E, oracle.forward(ops, n, params, inputs))
-    dpr, dxr, _ = oracle.vjp(ops, n, params, inputs, g.astype(np.float64))
-    check_grads({"dp": dp, "dx": dx}, dpr, dxr, g)
+    check_step(E, g, dp, dx, ops, n, params, inputs, y.astype(np.float64), loss, B)

@@ -6,6 +6,7 @@ import pytest
 
 import oracle
 from paper_2607_11985_amd import workloads as W
+from tests.parity_util import check_step
 from tests.test_gpu_parity import check_E, check_grads, note, torch_mod  # noqa: F401
 
 pytestmark = pytest.mark.gpu
@@ -49,8 +50,5 @@ def test_tile13_train_step_config5_sampled(torch_mod):
                                 torch.from_numpy(w.inputs).cuda(), w.loss, None, want_cot=True)
     torch.cuda.synchronize()
     E, dp, dx, g = (t.cpu().numpy() for t in (E, dp, dx, g))
-    Er = oracle.forward(w.ops, w.n_qubits, w.params[rows], w.inputs[rows])
-    check_E(E[rows], Er)
-    dpr, dxr, _ = oracle.vjp(w.ops, w.n_qubits, w.params[rows], w.inputs[rows],
-                             g[rows].astype(np.float64))
-    check_grads({"dp": dp[rows], "dx": dx[rows]}, dpr, dxr, g[rows])
+    check_step(E[rows], g[rows], dp[rows], dx[rows], w.ops, w.n_qubits, w.params[rows],
+               w.inputs[rows], None, w.loss, w.batch)
