@@ -322,6 +322,26 @@ int vqc_train_step(const vqc_circuit *c, int64_t batch, const float *params, con
                    void *stream);
 
 /*
+ * vqc_train_step_noalloc -- vqc_train_step for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  The workspace is a static device array of
+ * VQC_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends; the call itself allocates and frees nothing.
+ * Arguments, results and errors as vqc_train_step without the workspace, plus
+ * VQC_ERR_TOO_LARGE when vqc_workspace_bytes(c, batch, 2) exceeds
+ * VQC_NOALLOC_SCRATCH_BYTES (e.g. 16 qubits on the streaming path: about 1.5
+ * MiB per sample).  Every call on one GPU uses that GPU's single array and
+ * finds there what the last call left (the call clears what must start at
+ * zero): calls that overlap on one GPU, from other streams or threads, race
+ * and must be ordered by the caller.
+ */
+#define VQC_NOALLOC_SCRATCH_BYTES 67108864
+int vqc_train_step_noalloc(const vqc_circuit *c, int64_t batch, const float *params,
+                           const float *inputs, int32_t loss_kind, const float *target,
+                           float *expvals, float *grad_out, float *dparams, float *dinputs,
+                           void *stream);
+
+/*
  * vqc_fd_backward -- the same gradient as vqc_backward by central differences
  * (the matched central finite-difference training policy of Sec. 4.2.3 and
  * the "no autograd" ablation of Sec. 4.2.4; kept to compare the mechanisms):

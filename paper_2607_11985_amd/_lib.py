@@ -22,6 +22,7 @@ VQC_ERR_TOO_LARGE = -3
 VQC_ERR_WORKSPACE = -4
 VQC_ERR_HIP = -5
 VQC_ERR_OOM = -6
+VQC_NOALLOC_SCRATCH_BYTES = 64 << 20
 VQC_PATH_AUTO, VQC_PATH_RESIDENT, VQC_PATH_STREAM = 0, 1, 2
 VQC_ENGINE_JIT, VQC_ENGINE_INTERP = 0, 1
 KIND = {name: code for code, name in enumerate((
@@ -101,6 +102,9 @@ def load():
     lib.vqc_train_step.argtypes = [_vp, ctypes.c_int64, _vp, _vp, ctypes.c_int32, _vp, _vp, _vp,
                                    _vp, _vp, _vp, ctypes.c_size_t, _vp]
     lib.vqc_train_step.restype = ctypes.c_int
+    lib.vqc_train_step_noalloc.argtypes = [_vp, ctypes.c_int64, _vp, _vp, ctypes.c_int32, _vp,
+                                           _vp, _vp, _vp, _vp, _vp]
+    lib.vqc_train_step_noalloc.restype = ctypes.c_int
     lib.vqc_fd_backward.argtypes = [_vp, ctypes.c_int64, _vp, _vp, _vp, ctypes.c_float, _vp,
                                     ctypes.c_size_t, _vp, _vp, _vp]
     lib.vqc_fd_backward.restype = ctypes.c_int
@@ -226,6 +230,12 @@ def vqc_train_step(h, batch, params_ptr, inputs_ptr, loss_kind, y_ptr, expvals_p
                    dparams_ptr, dinputs_ptr, ws_ptr, ws_bytes, stream):
     _check(load().vqc_train_step(h, batch, params_ptr, inputs_ptr, loss_kind, y_ptr, expvals_ptr,
                                  grad_ptr, dparams_ptr, dinputs_ptr, ws_ptr, ws_bytes, stream))
+
+
+def vqc_train_step_noalloc(h, batch, params_ptr, inputs_ptr, loss_kind, y_ptr, expvals_ptr,
+                           grad_ptr, dparams_ptr, dinputs_ptr, stream):
+    _check(load().vqc_train_step_noalloc(h, batch, params_ptr, inputs_ptr, loss_kind, y_ptr,
+                                         expvals_ptr, grad_ptr, dparams_ptr, dinputs_ptr, stream))
 
 
 def vqc_loss_grad(kind: int, batch: int, n: int, e_ptr, y_ptr, g_ptr, stream):

@@ -617,10 +617,14 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
   return VQC_OK;
 }
 
-int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
-                   int32_t loss_kind, const float* target, float* expvals, float* grad_out,
-                   float* dparams, float* dinputs, void* workspace, size_t workspace_bytes,
-                   void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The argument checks of vqc_train_step (those that need no workspace).
+int check_step_args(const vqc_circuit* c, int64_t batch, const float* params,
+                    const float* inputs, int32_t loss_kind, const float* target,
+                    const float* expvals) {
   int rc = check_runnable(c);
   if (rc) return rc;
   if (loss_kind < VQC_LOSS_SUM || loss_kind > VQC_LOSS_MSE_MEANZ)
@@ -631,12 +635,17 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
   if (!expvals) return fail(VQC_ERR_INVALID_ARG, "expvals is NULL");
   if ((loss_kind == VQC_LOSS_MSE_Z0 || loss_kind == VQC_LOSS_MSE_MEANZ) && !target)
     return fail(VQC_ERR_INVALID_ARG, "MSE losses need a target");
+  return VQC_OK;
+}
+
+// The training step on a checked, large enough workspace, with the handle's
+// device current.
+int train_step_impl(const vqc_circuit* c, int64_t batch, const float* params,
+                    const float* inputs, int32_t loss_kind, const float* target, float* expvals,
+                    float* grad_out, float* dparams, float* dinputs, void* workspace,
+                    void* stream) {
   const Plan& p = c->plan;
-  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(c, batch, 2),
-                            "workspace smaller than vqc_workspace_bytes(c, batch, 2)")))
-    return rc;
-  DeviceGuard g(c->device);
-  if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
+  int rc = 0;
   float* dp = p.P > 0 ? dparams : nullptr;
   float* dx = p.F > 0 ? dinputs : nullptr;
   float* rows = (c->shared && dp) ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
@@ -674,6 +683,46 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
   if (rows && (rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream)))
     return hip_fail("parameter gradient sum", rc);
   return VQC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
+                   int32_t loss_kind, const float* target, float* expvals, float* grad_out,
+                   float* dparams, float* dinputs, void* workspace, size_t workspace_bytes,
+                   void* stream) {
+  int rc = check_step_args(c, batch, params, inputs, loss_kind, target, expvals);
+  if (rc || batch == 0) return rc;
+  if ((rc = check_workspace(workspace, workspace_bytes, required_bytes(c, batch, 2),
+                            "workspace smaller than vqc_workspace_bytes(c, batch, 2)")))
+    return rc;
+  DeviceGuard g(c->device);
+  if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
+  return train_step_impl(c, batch, params, inputs, loss_kind, target, expvals, grad_out, dparams,
+                         dinputs, workspace, stream);
+}
+
+int vqc_train_step_noalloc(const vqc_circuit* c, int64_t batch, const float* params,
+                           const float* inputs, int32_t loss_kind, const float* target,
+                           float* expvals, float* grad_out, float* dparams, float* dinputs,
+                           void* stream) {
+  int rc = check_step_args(c, batch, params, inputs, loss_kind, target, expvals);
+  if (rc || batch == 0) return rc;
+  const size_t need = required_bytes(c, batch, 2);
+  if (need > (size_t)VQC_NOALLOC_SCRATCH_BYTES)
+    return fail(VQC_ERR_TOO_LARGE,
+                "the step needs " + std::to_string(need) + " bytes of workspace; the static "
+                "scratch of vqc_train_step_noalloc holds " +
+                    std::to_string((size_t)VQC_NOALLOC_SCRATCH_BYTES));
+  DeviceGuard g(c->device);
+  if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
+  void* ws = nullptr;
+  if (need > 0 && (rc = vqc::scratch_pointer(c->device, &ws)))
+    return hip_fail("lookup of the static scratch", rc);
+  return train_step_impl(c, batch, params, inputs, loss_kind, target, expvals, grad_out, dparams,
+                         dinputs, ws, stream);
 }
 
 int vqc_fd_backward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,

@@ -3,9 +3,17 @@
 // loss cotangent, and the launchers.  The device code lives in vqc_device.h.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "vqc.h"
 #include "vqc_device.h"
 #include "vqc_internal.h"
+
+// The workspace of vqc_train_step_noalloc: a static device array, one copy per
+// GPU that loads this library, held until the process ends.  In host code this
+// name is only a stand-in for the registration of the variable: kernels receive
+// the device address that scratch_pointer() looks up once per device.
+static __device__ __align__(256) unsigned char scratch[VQC_NOALLOC_SCRATCH_BYTES];
 
 namespace vqc {
 namespace {
@@ -250,6 +258,27 @@ int launch_fill_zero(float* p, int64_t count, void* stream) {
   hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_1d(count, 256)), dim3(256), 0,
                      (hipStream_t)stream, p, count);
   return (int)hipGetLastError();
+}
+
+int scratch_pointer(int device, void** out) {
+  static std::mutex mu;
+  static void* ptr[kScratchDevices] = {};
+  *out = nullptr;
+  if (device < 0 || device >= kScratchDevices) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[device]) {
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return (int)e;
+    if (cur != device) return (int)hipErrorInvalidDevice;  // the caller makes it current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return (int)e;
+    if (!p) return (int)hipErrorInvalidSymbol;
+    ptr[device] = p;
+  }
+  *out = ptr[device];
+  return 0;
 }
 
 int launch_loss_grad(int kind, int64_t batch, int n, const float* e, const float* y, float* g,

@@ -98,6 +98,11 @@ int launch_fd_combine(int64_t batch, int NS, int base, int P, int F, int n, floa
 int launch_sum_rows(int64_t batch, int P, const float* rows, float* out, void* stream);
 int launch_loss_grad(int kind, int64_t batch, int n, const float* e, const float* y, float* g,
                      void* stream);
+// Device address of the static scratch array (VQC_NOALLOC_SCRATCH_BYTES) on
+// `device`, which must be the current device; looked up once per device and
+// kept.  Returns 0 or a hipError_t value.
+constexpr int kScratchDevices = 64;
+int scratch_pointer(int device, void** out);
 int prepare_kernels(const Plan& plan);
 
 // Kernels compiled at run time for one circuit (jit.cpp).
