@@ -352,16 +352,17 @@ def measure(idx, args, torch, dev, want_cpu, cpu_budget):
             raise SystemExit(f"{w.name}: a timed step differs from the first one")
     gpu_out = [t.cpu().numpy() for t in (E, g, dp, dx)]
 
-    # ---- repeats: >= 5 brackets of K' >= K steps, each >= 0.2 s
-    Kr = max(K, int(math.ceil(0.2 / max(ms_per_step / 1e3, 1e-9))))
+    # ---- repeats: >= 5 brackets of K' >= K steps, each >= 0.2 s (--repeats 0:
+    # none, for profiler runs)
+    Kr = max(K, int(math.ceil(0.2 / max(ms_per_step / 1e3, 1e-9)))) if args.repeats else K
     rates = []
-    for _ in range(max(args.repeats, 5)):
+    for _ in range(max(args.repeats, 5) if args.repeats else 0):
         ms = timed(step, Kr)
         rates.append(B * Kr / (ms / 1e3))
     for t, r in zip((E, g, dp, dx), first):
         if not torch.equal(t, r):
             raise SystemExit(f"{w.name}: a repeated step differs from the first one")
-    rates = np.array(rates)
+    rates = np.array(rates) if rates else np.array([value, value])
 
     # ---- per-call times of the separate calls (events around each call)
     Kc = max(3, min(K, 50))
@@ -455,7 +456,8 @@ def main():
     ap.add_argument("--batch", type=int, default=0,
                     help="override the workload's batch (e.g. 1024 for the 16-qubit "
                          "workload to overflow the 256 MB Infinity Cache)")
-    ap.add_argument("--repeats", type=int, default=5)
+    ap.add_argument("--repeats", type=int, default=5,
+                    help="repeat brackets for mean/std/median (at least 5; 0 = none)")
     ap.add_argument("--engine", default="jit", choices=["jit", "interp"])
     ap.add_argument("--path", default="auto", choices=["auto", "resident", "stream"])
     ap.add_argument("--reg-bits", type=int, default=0)

@@ -67,9 +67,15 @@ size_t resident_state_bytes(const Plan& p, int64_t batch) {
   return (size_t)resident_blocks(p, batch) * (size_t)p.WG * ((size_t)1 << p.R) * 8;
 }
 
-// Streaming workspace: [psi | E partials | psi work | lambda work | grad partials]
+// Streaming workspace: [forward states fa, fb | E partials | tables | adjoint
+// states (psi, lambda) x 2 | grad partials | cotangent].  Consecutive passes
+// store the state in different memory layouts, so every pass reads one buffer
+// and writes the other: forward pass i writes f[i % 2] (the last one leaves
+// psi_G there, kept for the backward), adjoint pass j writes w[j % 2], l[j % 2].
 struct StreamLayout {
-  size_t psi = 0, epart = 0, psiw = 0, lamw = 0, gpart = 0, end_inference = 0, end_training = 0;
+  size_t f[2] = {0, 0}, psi = 0;  // psi: the buffer the forward's last pass writes
+  size_t epart = 0, end_inference = 0;
+  size_t w[2] = {0, 0}, l[2] = {0, 0}, gpart = 0, end_training = 0;
   size_t cot = 0, end_step = 0;  // the training step's cotangent rows [B, n]
   size_t tabs = 0, gsig = 0, esig = 0;  // the table kernel's per-sample tables
 };
@@ -79,15 +85,21 @@ StreamLayout stream_layout(const Plan& p, int64_t batch) {
   const size_t state = (size_t)batch * ((size_t)1 << p.nq) * 8;
   const size_t tiles = (size_t)batch << p.ng;
   const size_t nocc = p.occ_src.size();
-  L.psi = 0;
-  L.epart = align_up(L.psi + state, 256);
+  L.f[0] = 0;
+  L.f[1] = align_up(L.f[0] + state, 256);
+  L.psi = L.f[(p.fpass.size() + 1) % 2];
+  L.epart = align_up(L.f[1] + state, 256);
   L.tabs = align_up(L.epart + tiles * (size_t)p.n * 4, 256);
   L.gsig = align_up(L.tabs + (size_t)batch * nocc * 8, 256);
   L.esig = align_up(L.gsig + (size_t)batch * nocc * 4, 256);
   L.end_inference = align_up(L.esig + (size_t)batch * p.n * 4, 256);
-  L.psiw = L.end_inference;
-  L.lamw = align_up(L.psiw + state, 256);
-  L.gpart = align_up(L.lamw + state, 256);
+  size_t o = L.end_inference;
+  for (int s = 0; s < 2; ++s) {
+    L.w[s] = o;
+    L.l[s] = align_up(L.w[s] + state, 256);
+    o = align_up(L.l[s] + state, 256);
+  }
+  L.gpart = o;
   L.end_training = align_up(L.gpart + tiles * (size_t)(p.P + p.F) * 4, 256);
   L.cot = L.end_training;
   L.end_step = align_up(L.cot + (size_t)batch * (size_t)p.n * 4, 256);
@@ -120,7 +132,7 @@ constexpr size_t kFdStateBudget = size_t(2) << 30;
 int fd_chunk(const Plan& p, int64_t batch) {
   const int NS = p.P + p.F;
   if (p.path == VQC_PATH_RESIDENT || NS == 0 || batch == 0) return NS;
-  const size_t per_slot = (size_t)batch * 2 * ((size_t)1 << p.nq) * 8;
+  const size_t per_slot = (size_t)batch * 2 * 2 * ((size_t)1 << p.nq) * 8;  // two buffers
   const size_t c = kFdStateBudget / per_slot;
   return (int)std::max<size_t>(1, std::min<size_t>(c, (size_t)NS));
 }
@@ -201,6 +213,9 @@ vqc::PassArgs pass_args(const vqc_circuit* c, const vqc::PassPlan& pp, bool bwd,
   a.n_ins = pp.n_ins;
   a.cols = at<uint32_t>(c, c->off_cols);
   a.io = a.cols + pp.io_off;
+  a.io_out = a.cols + pp.io_out_off;
+  a.io_lin = a.cols + pp.io_lin_off;
+  a.io_lout = a.cols + pp.io_lout_off;
   a.start_phys = at<uint8_t>(c, c->off_maps) + pp.start_off;
   a.end_phys = at<uint8_t>(c, c->off_maps) + pp.end_off;
   a.pslots = at<int32_t>(c, c->off_pslots) + pp.slots_off;
@@ -270,11 +285,12 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     a.params = params;
     a.inputs = inputs;
     set_tables(a, ws, L);
-    a.psi_src = ws + L.psi;
-    a.psi_dst = ws + L.psi;
+    a.psi_src = ws + L.f[(i + 1) % 2];
+    a.psi_dst = ws + L.f[i % 2];
     if (psi0 && (a.flags & vqc::PF_INIT)) {
       a.flags &= ~vqc::PF_INIT;
       a.psi_src = psi0;
+      a.psi0_in = 1;
     }
     if (a.flags & vqc::PF_ZPART) a.probs = probs;
     a.fd_base = fd_base;
@@ -314,10 +330,10 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     a.params = params;
     a.inputs = inputs;
     a.grad_out = grad_out;
-    a.psi_src = ws + (first ? L.psi : L.psiw);
-    a.psi_dst = ws + L.psiw;
-    a.lam_src = ws + L.lamw;
-    a.lam_dst = ws + L.lamw;
+    a.psi_src = ws + (first ? L.psi : L.w[(j + 1) % 2]);
+    a.psi_dst = ws + L.w[j % 2];
+    a.lam_src = ws + L.l[(j + 1) % 2];
+    a.lam_dst = ws + L.l[j % 2];
     a.gpart = gpart;
     set_tables(a, ws, L);
     if (first) {

@@ -75,9 +75,11 @@ GradMode grad_mode(int lanes_per_sample, int n_slots) {
 // the streaming planner reorders commute, and a Pauli carried through a
 // commuting gate is unchanged, so the rows hold for every execution order.
 // The factors cos(phi') are applied to the state after every kBlock rotations
-// of a stream (each unscaled gate grows the state by at most sqrt 2), and the
-// adjoint scales each gradient by the square of the factors not yet applied.
-constexpr int kBlock = 24;
+// of a stream and at its end (each unscaled gate grows the state by at most
+// sqrt 2, so a block grows it by at most 2^32, far inside the float range), and
+// the adjoint scales each gradient by the square of the factors not yet
+// applied (at least 2^-64).
+constexpr int kBlock = 64;
 
 struct Frame {
   int words = 0;
@@ -536,10 +538,11 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         }
         o << "  { static constexpr uint32_t col[] = {";
         for (int i = 0; i < 2 * k; ++i) o << (i ? "," : "") << hex(p.cols[arg + i]);
-        o << "};\n    exchange<R>(a, w.xbuf, w.plane, col, " << k << ", " << t
-          << ", w.stid, w.sl);\n";
         if (bwd)
-          o << "    exchange<R>(l, w.xbuf, w.plane, col, " << k << ", " << t
+          o << "};\n    exchange2<R>(a, l, w.xbuf, w.plane, col, " << k << ", " << t
+            << ", w.stid, w.sl);\n";
+        else
+          o << "};\n    exchange<R>(a, w.xbuf, w.plane, col, " << k << ", " << t
             << ", w.stid, w.sl);\n";
         o << "  }\n";
         break;

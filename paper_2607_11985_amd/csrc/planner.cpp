@@ -4,12 +4,13 @@
 // schedules of the forward sweep and of the adjoint (reverse) sweep.
 //
 // Resident path (n <= 13 by default): one pass holds every qubit on chip.
-// Streaming path (n >= 14): a pass holds 14 "local" qubits of one sample in a
-// workgroup; the other ng = n - 14 "global" qubits are fixed per workgroup (its
-// tile index).  A pass runs every gate whose qubit lines are ready and whose
-// register-bit qubit is local -- gates on disjoint qubits commute, so a gate
-// that must wait blocks only its own lines.  Diagonal gates and CNOT controls
-// may sit on global qubits (their value is uniform over the tile).
+// Streaming path (n >= 14): a pass holds k "local" qubits of one sample in a
+// workgroup (k = 12, 13 or 14); the other ng = n - k "global" qubits are fixed
+// per workgroup (its tile index).  A pass runs every gate whose qubit lines are
+// ready and whose register-bit qubit is local -- gates on disjoint qubits
+// commute, so a gate that must wait blocks only its own lines.  Diagonal gates
+// and CNOT controls may sit on global qubits (their value is uniform over the
+// tile).
 //
 // Host-only code: no device calls, so it can run (and be tested) without a GPU.
 #include <algorithm>
@@ -193,92 +194,196 @@ int append_map(const Mapping& m, std::vector<uint8_t>& maps) {
   return off;
 }
 
-// Tile I/O layout of a streaming pass: the 14 local qubits in ascending order
-// are the tile ranks; ranks 0..13-R sit on the thread bits, the top R on the
-// register bits, so consecutive lanes touch consecutive low qubits in HBM.
-Mapping io_mapping(const std::vector<int>& local, const std::vector<int>& glob, int k, int R,
-                   int nq) {
+// ------------------------------------------------------------ streaming passes
+// A pass holds k local qubits of one sample per workgroup; the other ng global
+// qubits are fixed by the workgroup's tile index.  Between two passes the state
+// sits in HBM in a memory layout of its own: a permutation of the qubits over
+// the address bits, chosen so that the qubits local in both the writing and
+// the reading pass take the lowest address bits.  Any qubit may then be global
+// in a pass (the tile I/O of both passes stays in runs of consecutive
+// addresses), so a pass takes the global set that lets it run the most gates.
+
+// A pass before its sweep is planned: its global qubits and the gates it runs.
+struct StreamGroup {
+  uint32_t glob = 0;
+  std::vector<Prim> prims;
+};
+
+uint32_t lines_of(const Prim& p) {
+  return (1u << p.q0) | (two_qubit(p) ? 1u << p.q1 : 0u);
+}
+
+// The gates of `seq` not yet done that one pass with global set `glob` runs:
+// in circuit order, every gate whose lines no earlier waiting gate blocks and
+// whose register qubit is local.  Returns their count; `took` gets them.
+int pass_gates(const std::vector<Prim>& seq, const std::vector<char>& done, uint32_t glob,
+               uint32_t all, std::vector<int>* took) {
+  uint32_t blocked = 0;
+  int count = 0;
+  for (size_t i = 0; i < seq.size() && blocked != all; ++i) {
+    if (done[i]) continue;
+    const Prim& p = seq[i];
+    const uint32_t lines = lines_of(p);
+    const int need = register_need(p);
+    if (!(blocked & lines) && (need < 0 || !((glob >> need) & 1u))) {
+      ++count;
+      if (took) took->push_back((int)i);
+    } else {
+      blocked |= lines;
+    }
+  }
+  return count;
+}
+
+uint64_t binomial(int n, int r) {
+  uint64_t v = 1;
+  for (int i = 1; i <= r; ++i) v = v * (uint64_t)(n - r + i) / (uint64_t)i;
+  return v;
+}
+
+constexpr uint64_t kMaxGlobalCandidates = 20000;
+
+// Pass partition.  Each pass takes, among all sets of ng qubits, the one that
+// lets it run the most gates; ties go to the set whose qubits are needed on a
+// register latest.  With more than kMaxGlobalCandidates sets, the ng qubits
+// needed latest.
+int partition_stream(const std::vector<Prim>& seq, int nq, int ng,
+                     std::vector<StreamGroup>& groups, std::string& msg) {
+  const uint32_t all = nq >= 32 ? ~0u : (1u << nq) - 1u;
+  std::vector<char> done(seq.size(), 0);
+  size_t remaining = seq.size();
+  const bool search = binomial(nq, ng) <= kMaxGlobalCandidates;
+  do {
+    // rank of each qubit's first pending register need (never needed: last)
+    int rank[kMaxQubits];
+    for (int q = 0; q < nq; ++q) rank[q] = INT_MAX;
+    int r = 0;
+    for (size_t i = 0; i < seq.size(); ++i) {
+      if (done[i]) continue;
+      const int q = register_need(seq[i]);
+      if (q >= 0 && rank[q] == INT_MAX) rank[q] = r++;
+    }
+    for (int q = 0; q < nq; ++q)
+      if (rank[q] == INT_MAX) rank[q] = r++;
+    uint32_t best = 0;
+    if (ng > 0) {
+      // the ng qubits needed latest
+      std::vector<int> order(nq);
+      for (int q = 0; q < nq; ++q) order[rank[q]] = q;
+      for (int j = 0; j < ng; ++j) best |= 1u << order[nq - 1 - j];
+      if (search) {
+        int best_count = -1;
+        long best_tie = -1;
+        // every ng-subset of the nq qubits (Gosper's enumeration of masks)
+        for (uint32_t g = (1u << ng) - 1u; g <= all && g != 0;) {
+          const int c = pass_gates(seq, done, g, all, nullptr);
+          long tie = 0;
+          for (int q = 0; q < nq; ++q)
+            if ((g >> q) & 1u) tie += rank[q];
+          if (c > best_count || (c == best_count && tie > best_tie)) {
+            best_count = c;
+            best_tie = tie;
+            best = g;
+          }
+          const uint32_t lo = g & (0u - g), hi = g + lo;
+          if (hi == 0) break;
+          g = (((hi ^ g) >> 2) / lo) | hi;
+        }
+      }
+    }
+    std::vector<int> took;
+    pass_gates(seq, done, best, all, &took);
+    if (took.empty()) {
+      msg = "internal: streaming pass made no progress";
+      return VQC_ERR_UNSUPPORTED;
+    }
+    StreamGroup grp;
+    grp.glob = best;
+    for (int i : took) {
+      grp.prims.push_back(seq[i]);
+      done[i] = 1;
+    }
+    remaining -= took.size();
+    groups.push_back(std::move(grp));
+  } while (remaining > 0);
+  return 0;
+}
+
+// Memory layout at the boundary between a pass that writes (global set
+// wglob) and one that reads (rglob): the qubits local in both come first
+// (ascending), then the others (ascending).  pos[q] = address bit of qubit q.
+void boundary_layout(uint32_t wglob, uint32_t rglob, int nq, int* pos) {
+  int b = 0;
+  for (int q = 0; q < nq; ++q)
+    if (!((wglob >> q) & 1u) && !((rglob >> q) & 1u)) pos[q] = b++;
+  for (int q = 0; q < nq; ++q)
+    if (((wglob >> q) & 1u) || ((rglob >> q) & 1u)) pos[q] = b++;
+}
+
+void identity_layout(int nq, int* pos) {
+  for (int q = 0; q < nq; ++q) pos[q] = q;
+}
+
+// Tile I/O mapping of a pass for memory layout `pos`: the local qubits ordered
+// by address bit are the tile ranks; ranks 0..k-R-1 sit on the thread bits and
+// the top R on the register bits, so consecutive lanes touch consecutive
+// addresses.  Global qubits, ascending, take the tile index bits.
+Mapping io_mapping(uint32_t glob, const int* pos, int k, int R, int nq) {
   Mapping m;
   m.k = k;
   m.nq = nq;
   for (int q = 0; q < kMaxQubits; ++q) m.q2p[q] = -1;
+  std::vector<int> local;
+  for (int q = 0; q < nq; ++q)
+    if (!((glob >> q) & 1u)) local.push_back(q);
+  std::sort(local.begin(), local.end(), [&](int x, int y) { return pos[x] < pos[y]; });
   const int nt = k - R;
   for (int r = 0; r < k; ++r) {
     const int p = r < nt ? R + r : r - nt;
     m.p2q[p] = local[r];
     m.q2p[local[r]] = p;
   }
-  for (size_t i = 0; i < glob.size(); ++i) m.q2p[glob[i]] = k + (int)i;
+  int j = 0;
+  for (int q = 0; q < nq; ++q)
+    if ((glob >> q) & 1u) m.q2p[q] = k + j++;
   return m;
 }
 
-int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, int R,
+// The k + ng address columns of a tile under mapping m and layout pos: one per
+// tile rank (thread bits first, then register bits), then one per global bit.
+void push_io(const Mapping& m, const int* pos, int k, int R, std::vector<uint32_t>& cols) {
+  const int nt = k - R;
+  for (int r = 0; r < k; ++r) {
+    const int p = r < nt ? R + r : r - nt;
+    cols.push_back(1u << pos[m.p2q[p]]);
+  }
+  std::vector<uint32_t> g(m.nq - k, 0u);
+  for (int q = 0; q < m.nq; ++q)
+    if (m.q2p[q] >= k) g[m.q2p[q] - k] = 1u << pos[q];
+  cols.insert(cols.end(), g.begin(), g.end());
+}
+
+// Plans the sweeps of the passes `groups` (one direction): each starts in the
+// tile I/O mapping of its input layout, runs its gates, and ends in the I/O
+// mapping of its output layout (no closing exchange when it stores nothing).
+// in_pos / out_pos: the layout each pass reads / writes.
+int plan_stream(Plan& plan, const std::vector<StreamGroup>& groups,
+                const std::vector<std::vector<int>>& in_pos,
+                const std::vector<std::vector<int>>& out_pos, bool bwd, int R,
                 std::vector<uint32_t>& out, std::vector<PassPlan>& passes, int& exchanges,
                 std::string& msg) {
-  const int nq = plan.nq, k = plan.k, ng = plan.ng;
-  std::vector<char> done(seq.size(), 0);
-  size_t remaining = seq.size();
-  do {
-    // rank the qubits by their first pending register need
-    std::vector<int> order;
-    std::vector<char> seen(nq, 0);
-    for (size_t i = 0; i < seq.size(); ++i) {
-      if (done[i]) continue;
-      const int q = register_need(seq[i]);
-      if (q >= 0 && !seen[q]) {
-        seen[q] = 1;
-        order.push_back(q);
-      }
-    }
-    for (int q = 0; q < nq; ++q)
-      if (!seen[q]) order.push_back(q);
-    // global qubits: needed last, preferring qubits >= 6 so that the low qubits
-    // stay on the lanes and tile I/O stays contiguous
-    const int lowlim = std::min(6, nq - ng);
-    std::vector<char> is_glob(nq, 0);
-    std::vector<int> glob;
-    for (auto it = order.rbegin(); it != order.rend() && (int)glob.size() < ng; ++it)
-      if (*it >= lowlim) {
-        glob.push_back(*it);
-        is_glob[*it] = 1;
-      }
-    for (auto it = order.rbegin(); it != order.rend() && (int)glob.size() < ng; ++it)
-      if (!is_glob[*it]) {
-        glob.push_back(*it);
-        is_glob[*it] = 1;
-      }
-    std::sort(glob.begin(), glob.end());
-    std::vector<int> local;
-    for (int q = 0; q < nq; ++q)
-      if (!is_glob[q]) local.push_back(q);
-    // the pass: every ready gate whose register qubit is local
-    std::vector<char> blocked(nq, 0);
-    std::vector<Prim> pass_prims;
-    for (size_t i = 0; i < seq.size(); ++i) {
-      if (done[i]) continue;
-      const Prim& pr = seq[i];
-      const bool two = two_qubit(pr);
-      const bool ready = !blocked[pr.q0] && !(two && blocked[pr.q1]);
-      const int need = register_need(pr);
-      if (ready && (need < 0 || !is_glob[need])) {
-        pass_prims.push_back(pr);
-        done[i] = 1;
-        --remaining;
-      } else {
-        blocked[pr.q0] = 1;
-        if (two) blocked[pr.q1] = 1;
-      }
-    }
-    if (pass_prims.empty() && remaining > 0) {
-      msg = "internal: streaming pass made no progress";
-      return VQC_ERR_UNSUPPORTED;
-    }
-    const Mapping io = io_mapping(local, glob, k, R, nq);
-    Mapping m = io;
+  const int nq = plan.nq, k = plan.k;
+  int ident[kMaxQubits];
+  identity_layout(nq, ident);
+  for (size_t i = 0; i < groups.size(); ++i) {
+    const StreamGroup& grp = groups[i];
+    const bool last = i + 1 == groups.size();
+    const Mapping io_in = io_mapping(grp.glob, in_pos[i].data(), k, R, nq);
+    const Mapping io_out = io_mapping(grp.glob, out_pos[i].data(), k, R, nq);
+    Mapping m = io_in;
     PassPlan pp;
     pp.ins_off = (int)out.size() / 2;
-    pp.start_off = append_map(io, plan.maps);
-    pp.end_off = pp.start_off;
+    pp.start_off = append_map(io_in, plan.maps);
     std::map<int, int> local_slot;
     std::vector<int32_t> slots;
     auto slot_of = [&](int occ) -> int {
@@ -291,25 +396,68 @@ int plan_stream(Plan& plan, const std::vector<Prim>& seq, bool bwd, int R,
       slots.push_back(s);
       return id;
     };
-    int rc = plan_sweep(pass_prims, nq, k, R, m, out, plan.cols, exchanges, slot_of, msg);
+    int rc = plan_sweep(grp.prims, nq, k, R, m, out, plan.cols, exchanges, slot_of, msg);
     if (rc < 0) return rc;
-    if (!(m == io)) {
-      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, io, k, R, plan.cols));
+    const bool stores = !(bwd && last);  // the adjoint's last pass ends at psi_0
+    if (stores && !(m == io_out)) {
+      emit(out, OP_EXCHANGE, 0, 0, -1, (uint32_t)emit_exchange(m, io_out, k, R, plan.cols));
       ++exchanges;
+      m = io_out;
     }
+    pp.end_off = append_map(m, plan.maps);
     pp.n_ins = (int)out.size() / 2 - pp.ins_off;
     pp.io_off = (int)plan.cols.size();
-    for (int r = 0; r < k; ++r) plan.cols.push_back(1u << local[r]);
-    for (int i = 0; i < ng; ++i) plan.cols.push_back(1u << glob[i]);
+    push_io(io_in, in_pos[i].data(), k, R, plan.cols);
+    pp.io_out_off = (int)plan.cols.size();
+    push_io(m, stores ? out_pos[i].data() : ident, k, R, plan.cols);
+    pp.io_lin_off = (int)plan.cols.size();
+    push_io(io_in, ident, k, R, plan.cols);
+    pp.io_lout_off = (int)plan.cols.size();
+    push_io(m, ident, k, R, plan.cols);
     pp.slots_off = (int)plan.pslots.size();
     pp.n_slots = (int)slots.size();
     plan.pslots.insert(plan.pslots.end(), slots.begin(), slots.end());
     plan.max_pass_slots = std::max(plan.max_pass_slots, pp.n_slots);
-    if (passes.empty()) pp.flags |= bwd ? PF_MAKE_LAMBDA : PF_INIT;
+    if (i == 0) pp.flags |= bwd ? PF_MAKE_LAMBDA : PF_INIT;
+    if (last) pp.flags |= bwd ? PF_LAST_ADJ : PF_ZPART;
     passes.push_back(pp);
-  } while (remaining > 0);
-  passes.back().flags |= bwd ? PF_LAST_ADJ : PF_ZPART;
+  }
   return 0;
+}
+
+// Both directions of the streaming path: partitions, boundary layouts, sweeps.
+// The forward's first pass reads (Psi_0) in logical order; its last pass writes
+// psi_G in the layout the adjoint's first pass reads.
+int plan_stream_both(Plan& plan, const std::vector<Prim>& rev, std::string& msg) {
+  const int nq = plan.nq;
+  std::vector<StreamGroup> fg, bg;
+  int rc = partition_stream(plan.prims, nq, plan.ng, fg, msg);
+  if (rc < 0) return rc;
+  rc = partition_stream(rev, nq, plan.ng, bg, msg);
+  if (rc < 0) return rc;
+  const size_t nf = fg.size(), nb = bg.size();
+  std::vector<std::vector<int>> fin(nf, std::vector<int>(nq)), fout(nf, std::vector<int>(nq));
+  std::vector<std::vector<int>> bin(nb, std::vector<int>(nq)), bout(nb, std::vector<int>(nq));
+  identity_layout(nq, fin[0].data());
+  for (size_t i = 0; i < nf; ++i) {
+    const uint32_t next = i + 1 < nf ? fg[i + 1].glob : bg[0].glob;
+    boundary_layout(fg[i].glob, next, nq, fout[i].data());
+    if (i + 1 < nf) fin[i + 1] = fout[i];
+  }
+  bin[0] = fout[nf - 1];
+  for (size_t j = 0; j < nb; ++j) {
+    if (j + 1 < nb) {
+      boundary_layout(bg[j].glob, bg[j + 1].glob, nq, bout[j].data());
+      bin[j + 1] = bout[j];
+    } else {
+      identity_layout(nq, bout[j].data());  // stores nothing
+    }
+  }
+  rc = plan_stream(plan, fg, fin, fout, false, plan.Rf, plan.fwd, plan.fpass, plan.fwd_exchanges,
+                   msg);
+  if (rc < 0) return rc;
+  return plan_stream(plan, bg, bin, bout, true, plan.Rb, plan.bwd, plan.bpass,
+                     plan.bwd_exchanges, msg);
 }
 
 // ------------------------------------------------------------- lowering
@@ -681,10 +829,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     plan.WG = 1 << plan.t;
     plan.S = 1;
     plan.G = plan.WG / 64;
-    rc = plan_stream(plan, plan.prims, false, plan.Rf, plan.fwd, plan.fpass, plan.fwd_exchanges,
-                     msg);
-    if (rc < 0) return rc;
-    rc = plan_stream(plan, rev, true, plan.Rb, plan.bwd, plan.bpass, plan.bwd_exchanges, msg);
+    rc = plan_stream_both(plan, rev, msg);
     if (rc < 0) return rc;
     const size_t xbuf = ((size_t)1 << plan.k) * 8;
     plan.lds_tab = xbuf;

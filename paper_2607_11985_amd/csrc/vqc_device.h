@@ -865,14 +865,18 @@ __device__ __forceinline__ uint32_t xor_cols(int u, const uint32_t (&c)[R]) {
 // col[0..k) are the write-side columns, col[k..2k) the read-side columns.  The
 // buffer is planar (real parts, then imaginary parts, `plane` floats apart) so
 // every access is a 32-bit one: no 64-bit register tuples enter the schedule
-// loop, and 32 lanes hit 32 banks.
+// loop, and 32 lanes hit 32 banks.  Addresses are formed in bytes (columns
+// scaled by 4 once), so an access costs one XOR and no shift.
+
+// The thread's byte offsets of its write and read slots (register bits 0).
 template <int R>
-__device__ __forceinline__ void exchange(St<R>& a, float* xbuf, uint32_t plane,
-                                         const uint32_t* col, int k, int t, int stid, int sl) {
+__device__ __forceinline__ void exchange_bases(const uint32_t* col, int k, int t, int stid, int sl,
+                                               uint32_t& bw, uint32_t& br) {
   // an opaque thread index: the addresses of one exchange are not merged with
   // equal ones of later exchanges (which would keep them alive in between)
   const uint32_t ot = opaque((uint32_t)stid);
-  uint32_t bw = 0, br = 0;
+  bw = 0;
+  br = 0;
 #pragma unroll
   for (int i = 0; i < kMaxTileQubits - 2; ++i) {
     if (i < t && ((ot >> i) & 1)) {
@@ -884,30 +888,55 @@ __device__ __forceinline__ void exchange(St<R>& a, float* xbuf, uint32_t plane,
   const uint32_t lowmask = (1u << (k < kBankBits ? k : kBankBits)) - 1u;
   const uint32_t xs = ((uint32_t)sl << t) & lowmask;
   const uint32_t base = (uint32_t)sl << k;
-  bw = base | (bw ^ xs);
-  br = base | (br ^ xs);
+  bw = (base | (bw ^ xs)) << 2;
+  br = (base | (br ^ xs)) << 2;
+}
+
+template <int R>
+__device__ __forceinline__ void exchange_at(St<R>& a, float* xbuf, uint32_t plane,
+                                            const uint32_t* col, int k, uint32_t bw,
+                                            uint32_t br) {
   uint32_t cw[R], cr[R];
 #pragma unroll
   for (int b = 0; b < R; ++b) {
-    cw[b] = col[b];
-    cr[b] = col[k + b];
+    cw[b] = col[b] << 2;
+    cr[b] = col[k + b] << 2;
   }
-  float* xr = xbuf;
-  float* xi = xbuf + plane;
+  unsigned char* xr = reinterpret_cast<unsigned char*>(xbuf);
+  unsigned char* xi = xr + 4 * plane;
 #pragma unroll
   for (int u = 0; u < St<R>::N; ++u) {
     const uint32_t o = bw ^ xor_cols<R>(u, cw);
-    xr[o] = a.r[u];
-    xi[o] = a.i[u];
+    *reinterpret_cast<float*>(xr + o) = a.r[u];
+    *reinterpret_cast<float*>(xi + o) = a.i[u];
   }
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < St<R>::N; ++u) {
     const uint32_t o = br ^ xor_cols<R>(u, cr);
-    a.r[u] = xr[o];
-    a.i[u] = xi[o];
+    a.r[u] = *reinterpret_cast<const float*>(xr + o);
+    a.i[u] = *reinterpret_cast<const float*>(xi + o);
   }
   __syncthreads();
+}
+
+template <int R>
+__device__ __forceinline__ void exchange(St<R>& a, float* xbuf, uint32_t plane,
+                                         const uint32_t* col, int k, int t, int stid, int sl) {
+  uint32_t bw, br;
+  exchange_bases<R>(col, k, t, stid, sl, bw, br);
+  exchange_at<R>(a, xbuf, plane, col, k, bw, br);
+}
+
+// The same permutation of two states (the adjoint's psi and lambda), one after
+// the other through the buffer, with the slot bases formed once.
+template <int R>
+__device__ __forceinline__ void exchange2(St<R>& a, St<R>& l, float* xbuf, uint32_t plane,
+                                          const uint32_t* col, int k, int t, int stid, int sl) {
+  uint32_t bw, br;
+  exchange_bases<R>(col, k, t, stid, sl, bw, br);
+  exchange_at<R>(a, xbuf, plane, col, k, bw, br);
+  exchange_at<R>(l, xbuf, plane, col, k, bw, br);
 }
 
 // ------------------------------------------------------- schedule runner
@@ -998,8 +1027,10 @@ __device__ __forceinline__ void run_schedule(St<R>& a, St<R>& l, const uint32_t*
     const int pa = (w0 >> 5) & 31;
     const int pb = (w0 >> 10) & 31;
     if (op == OP_EXCHANGE) {
-      exchange<R>(a, w.xbuf, w.plane, w.cols + arg, w.k, w.t, w.stid, w.sl);
-      if (BWD) exchange<R>(l, w.xbuf, w.plane, w.cols + arg, w.k, w.t, w.stid, w.sl);
+      if (BWD)
+        exchange2<R>(a, l, w.xbuf, w.plane, w.cols + arg, w.k, w.t, w.stid, w.sl);
+      else
+        exchange<R>(a, w.xbuf, w.plane, w.cols + arg, w.k, w.t, w.stid, w.sl);
       continue;
     }
     if (op == OP_CNOT) {
@@ -1642,7 +1673,9 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   }
 
   uint32_t base, off[NA];
-  io_offsets<R>(A.io, A.k, A.ng, tid, g, base, off);
+  // Psi_0 is read in logical order; the passes' own states in their layouts
+  const bool logical_in = !BWD && !(A.flags & PF_INIT) && A.psi0_in;
+  io_offsets<R>(logical_in ? A.io_lin : A.io, A.k, A.ng, tid, g, base, off);
   const size_t sbase = (size_t)b << (A.k + A.ng);
   St<R> a, l;
   if (!BWD && (A.flags & PF_INIT)) {
@@ -1668,6 +1701,8 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
 
   Sched::template run<R, BWD, true>(a, l, w, A.ins, A.n_ins);
 
+  // the stores, in the layout this pass writes
+  io_offsets<R>(A.io_out, A.k, A.ng, tid, g, base, off);
   base = opaque(base);
   // the adjoint's last pass ends at psi_0: its states are not needed
   const bool store = !BWD || !(A.flags & PF_LAST_ADJ);
@@ -1695,6 +1730,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
       // state's addresses, so the stores stay coalesced
       const uint32_t xm = frame_xmask(Sched::esigns(w), A.n);
       float* pd = A.probs + sbase;
+      io_offsets<R>(A.io_lout, A.k, A.ng, tid, g, base, off);
 #pragma unroll
       for (int j = 0; j < NA; ++j) pd[(base | off[j]) ^ xm] = a.r[j] * a.r[j] + a.i[j] * a.i[j];
     }

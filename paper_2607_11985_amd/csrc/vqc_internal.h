@@ -24,8 +24,12 @@ namespace vqc {
 
 struct PassPlan {
   int ins_off = 0, n_ins = 0;   // instruction pairs (offset in pairs)
-  int io_off = 0;               // k + ng words: x offset of each tile rank bit, then
-                                // of each global bit
+  // tile I/O columns, k + ng words each: the address bit of each tile rank bit
+  // (thread bits, then register bits), then of each global bit
+  int io_off = 0;               // loads, in the memory layout the pass reads
+  int io_out_off = 0;           // stores, in the layout it writes
+  int io_lin_off = 0;           // loads in logical order (Psi_0)
+  int io_lout_off = 0;          // stores in logical order (probabilities)
   int start_off = 0, end_off = 0;  // nq bytes each: logical qubit -> physical bit
   int slots_off = 0, n_slots = 0;  // pass-local gradient slot -> global slot
   int flags = 0;

@@ -112,12 +112,16 @@ struct PassArgs {
   const uint32_t* ins;
   int32_t n_ins;
   const uint32_t* cols;
-  const uint32_t* io;          // tile I/O columns (k + ng)
+  const uint32_t* io;          // tile I/O columns (k + ng): loads, in the layout read
+  const uint32_t* io_out;      // stores, in the layout written
+  const uint32_t* io_lin;      // loads in logical order (Psi_0)
+  const uint32_t* io_lout;     // stores in logical order (probabilities)
   const uint8_t* start_phys;   // logical -> phys at pass start
   const uint8_t* end_phys;     // logical -> phys at pass end
   const int32_t* pslots;       // pass-local -> global gradient slot
   int32_t n_pslots;
   int32_t flags;
+  int32_t psi0_in;             // 1: this (first forward) pass reads Psi_0, logical order
   const int32_t* occ_src;
   const int32_t* occ_idx;
   const float* occ_cs;
@@ -127,7 +131,8 @@ struct PassArgs {
   int64_t B;
   const float* params;
   const float* inputs;
-  const void* psi_src;        // float2 states, logical order [B][2^n]
+  const void* psi_src;        // float2 states [B][2^n] in the pass's input / output
+                               // memory layouts (Psi_0: logical order)
   void* psi_dst;
   const void* lam_src;
   void* lam_dst;

@@ -278,12 +278,13 @@ def test_fd_backward_validation(lib):
     w = W.make_config(5, batch=2)
     rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
     assert rc == 0
-    # streaming: one chunk of slots at a time, its shifted copies' states within
-    # 2 GiB: 4 samples x 2 shifts x 512 KiB = 4 MiB per slot, all 400 slots in one
-    # chunk (1.6 GiB of states) plus their E rows
+    # streaming: one chunk of slots at a time, its shifted copies' states (two
+    # buffers, passes alternate between them) within 2 GiB: 4 samples x 2
+    # shifts x 2 buffers x 512 KiB = 8 MiB per slot, 256 of the 400 slots per
+    # chunk (2 GiB of states) plus their E rows
     nb = _lib.vqc_workspace_bytes(h, 4, 3)
     state = (1 << 16) * 8
-    assert 4 * 2 * 400 * state <= nb < 4 * 2 * 400 * state * 1.2
+    assert 4 * 2 * 2 * 256 * state <= nb < 4 * 2 * 2 * 256 * state * 1.2
     # a large batch takes smaller chunks: the workspace stays near the budget
     nb = _lib.vqc_workspace_bytes(h, 256, 3)
     assert (2 << 30) * 0.9 <= nb <= (2 << 30) * 1.2

@@ -250,7 +250,7 @@ def test_fd_backward(torch_mod, n, engine, shared):
 
 def test_fd_backward_streaming_chunks(torch_mod):
     """The 16-qubit workload's structure at B = 64: the shifted copies of all
-    400 slots (51 GiB of states) run in chunks of 32 slots; sampled rows against
+    400 slots (51 GiB of states in two buffers) run in chunks of slots; sampled rows against
     the oracle's differences at the same h."""
     torch = torch_mod
     from paper_2607_11985_amd.api import Circuit
