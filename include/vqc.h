@@ -37,8 +37,8 @@
  *   - A compiled circuit is immutable: it may be used from several threads
  *     and streams at once.
  */
-#ifndef VQC_H
-#define VQC_H
+#ifndef VQC_ABI_H_
+#define VQC_ABI_H_
 
 #ifndef __HIPCC_RTC__ /* the run-time compiler predefines the fixed-width types */
 #include <stddef.h>
@@ -392,4 +392,4 @@ const char *vqc_last_error(void);
 #ifdef __cplusplus
 }
 #endif
-#endif /* VQC_H */
+#endif /* VQC_ABI_H_ */

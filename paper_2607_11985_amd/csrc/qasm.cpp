@@ -609,7 +609,21 @@ class Parser {
     return a;
   }
 
+  // Angle expressions nest at most kMaxNest deep (parentheses, signs, powers,
+  // function calls): the parser recurses once per level.
+  static constexpr int kMaxNest = 256;
+  int nest_ = 0;
+  struct Nest {
+    int& d;
+    Nest(Parser* p, const Tok& t) : d(p->nest_) {
+      if (d >= kMaxNest) p->err(t, "angle expression nests more than 256 deep", VQC_ERR_TOO_LARGE);
+      ++d;
+    }
+    ~Nest() { --d; }
+  };
+
   Affine expr(Ctx& c) {
+    Nest guard(this, c.peek());
     Affine a = term(c);
     while (c.peek().kind == Tok::SYM && (c.peek().text == "+" || c.peek().text == "-")) {
       const Tok& op = c.next();
@@ -636,6 +650,7 @@ class Parser {
     return a;
   }
   Affine unary(Ctx& c) {
+    Nest guard(this, c.peek());
     if (accept(c, "-")) return scale(unary(c), -1.0);
     if (accept(c, "+")) return unary(c);
     return power(c);
