@@ -75,12 +75,14 @@ def io_bytes(w):
 def state_rw_per_sample(info):
     """State reads + writes (in units of one 2^n complex64 state) of one streaming
     training step.  Forward: the first pass only writes (it starts from
-    |0...0>), every later pass reads and writes psi.  Adjoint: the first pass
-    reads psi_G and writes psi and lambda, the middle ones read and write both,
-    the last reads both and stores nothing; a single pass only reads psi_G."""
+    |0...0>), every later pass reads and writes psi (each pass's output is
+    kept).  Adjoint (one pass per forward pass, in reverse): the first reads
+    psi_G and writes lambda, the middle ones read the state their forward pass
+    saved and lambda and write lambda, the last reads both and stores nothing;
+    a single pass only reads psi_G."""
     nf, nb = info["fwd_passes"], info["bwd_passes"]
     fwd = 1 + 2 * (nf - 1)
-    adj = 1 if nb == 1 else 3 + 4 * (nb - 2) + 2
+    adj = 1 if nb == 1 else 2 + 3 * (nb - 2) + 2
     return fwd + adj
 
 

@@ -67,39 +67,36 @@ size_t resident_state_bytes(const Plan& p, int64_t batch) {
   return (size_t)resident_blocks(p, batch) * (size_t)p.WG * ((size_t)1 << p.R) * 8;
 }
 
-// Streaming workspace: [forward states fa, fb | E partials | tables | adjoint
-// states (psi, lambda) x 2 | grad partials | cotangent].  Consecutive passes
-// store the state in different memory layouts, so every pass reads one buffer
-// and writes the other: forward pass i writes f[i % 2] (the last one leaves
-// psi_G there, kept for the backward), adjoint pass j writes w[j % 2], l[j % 2].
+// Streaming workspace: [E partials | tables | states ck[0..] | lambda x 2 |
+// grad partials | cotangent].  Consecutive passes store the state in different
+// memory layouts, so no pass writes the buffer it reads.  A training forward
+// keeps every pass's output: pass i writes ck[i] (ck[nf - 1] is psi_G), and the
+// adjoint's mirror of pass i reads it.  An inference forward alternates
+// between ck[0] and ck[1].  The adjoint alternates lambda between l[0], l[1].
 struct StreamLayout {
-  size_t f[2] = {0, 0}, psi = 0;  // psi: the buffer the forward's last pass writes
-  size_t epart = 0, end_inference = 0;
-  size_t w[2] = {0, 0}, l[2] = {0, 0}, gpart = 0, end_training = 0;
+  size_t epart = 0, tabs = 0, gsig = 0, esig = 0;  // the table kernel's per-sample tables
+  size_t ck0 = 0, state = 0;  // ck[i] = ck0 + i * state
+  size_t end_inference = 0;
+  size_t l[2] = {0, 0}, gpart = 0, end_training = 0;
   size_t cot = 0, end_step = 0;  // the training step's cotangent rows [B, n]
-  size_t tabs = 0, gsig = 0, esig = 0;  // the table kernel's per-sample tables
+  size_t ck(size_t i) const { return ck0 + i * state; }
 };
 
 StreamLayout stream_layout(const Plan& p, int64_t batch) {
   StreamLayout L;
-  const size_t state = (size_t)batch * ((size_t)1 << p.nq) * 8;
   const size_t tiles = (size_t)batch << p.ng;
   const size_t nocc = p.occ_src.size();
-  L.f[0] = 0;
-  L.f[1] = align_up(L.f[0] + state, 256);
-  L.psi = L.f[(p.fpass.size() + 1) % 2];
-  L.epart = align_up(L.f[1] + state, 256);
+  const size_t nf = p.fpass.size();
+  L.state = align_up((size_t)batch * ((size_t)1 << p.nq) * 8, 256);
+  L.epart = 0;
   L.tabs = align_up(L.epart + tiles * (size_t)p.n * 4, 256);
   L.gsig = align_up(L.tabs + (size_t)batch * nocc * 8, 256);
   L.esig = align_up(L.gsig + (size_t)batch * nocc * 4, 256);
-  L.end_inference = align_up(L.esig + (size_t)batch * p.n * 4, 256);
-  size_t o = L.end_inference;
-  for (int s = 0; s < 2; ++s) {
-    L.w[s] = o;
-    L.l[s] = align_up(L.w[s] + state, 256);
-    o = align_up(L.l[s] + state, 256);
-  }
-  L.gpart = o;
+  L.ck0 = align_up(L.esig + (size_t)batch * p.n * 4, 256);
+  L.end_inference = L.ck(std::min<size_t>(nf, 2));
+  L.l[0] = L.ck(nf);
+  L.l[1] = L.l[0] + L.state;
+  L.gpart = L.l[1] + L.state;
   L.end_training = align_up(L.gpart + tiles * (size_t)(p.P + p.F) * 4, 256);
   L.cot = L.end_training;
   L.end_step = align_up(L.cot + (size_t)batch * (size_t)p.n * 4, 256);
@@ -274,8 +271,9 @@ void set_tables(vqc::PassArgs& a, unsigned char* ws, const StreamLayout& L) {
 // then the <Z> reduction into expvals; the last pass writes probs.  fd_slots > 0:
 // the batch is the central differences' shifted copies of slots fd_base ..
 int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
-                   float* expvals, unsigned char* ws, void* stream, const void* psi0 = nullptr,
-                   float* probs = nullptr, int fd_base = 0, int fd_slots = 0, float fd_h = 0.f) {
+                   float* expvals, unsigned char* ws, void* stream, bool keep,
+                   const void* psi0 = nullptr, float* probs = nullptr, int fd_base = 0,
+                   int fd_slots = 0, float fd_h = 0.f) {
   const Plan& p = c->plan;
   const StreamLayout L = stream_layout(p, batch);
   int rc = 0;
@@ -285,8 +283,8 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     a.params = params;
     a.inputs = inputs;
     set_tables(a, ws, L);
-    a.psi_src = ws + L.f[(i + 1) % 2];
-    a.psi_dst = ws + L.f[i % 2];
+    a.psi_src = ws + (keep ? L.ck(i ? i - 1 : 0) : L.ck((i + 1) % 2));
+    a.psi_dst = ws + (keep ? L.ck(i) : L.ck(i % 2));
     if (psi0 && (a.flags & vqc::PF_INIT)) {
       a.flags &= ~vqc::PF_INIT;
       a.psi_src = psi0;
@@ -330,8 +328,8 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     a.params = params;
     a.inputs = inputs;
     a.grad_out = grad_out;
-    a.psi_src = ws + (first ? L.psi : L.w[(j + 1) % 2]);
-    a.psi_dst = ws + L.w[j % 2];
+    a.psi_src = ws + L.ck(p.fpass.size() - 1 - j);  // the state its forward pass saved
+    a.psi_dst = nullptr;
     a.lam_src = ws + L.l[(j + 1) % 2];
     a.lam_dst = ws + L.l[j % 2];
     a.gpart = gpart;
@@ -572,9 +570,12 @@ int vqc_forward_ex(const vqc_circuit* c, int64_t batch, const float* params, con
   }
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
-  if (p.path == VQC_PATH_STREAM)
+  if (p.path == VQC_PATH_STREAM) {
+    // a workspace that holds the training layout keeps every pass's state
+    const bool keep = workspace_bytes >= required_bytes_core(p, batch, 1);
     return stream_forward(c, batch, params, inputs, expvals,
-                          static_cast<unsigned char*>(workspace), stream, psi0, probs);
+                          static_cast<unsigned char*>(workspace), stream, keep, psi0, probs);
+  }
   vqc::TileArgs a = tile_args(c, false, batch);
   a.params = params;
   a.inputs = inputs;
@@ -671,7 +672,7 @@ int train_step_impl(const vqc_circuit* c, int64_t batch, const float* params,
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     float* cot = grad_out ? grad_out
                           : reinterpret_cast<float*>(ws + stream_layout(p, batch).cot);
-    if ((rc = stream_forward(c, batch, params, inputs, expvals, ws, stream))) return rc;
+    if ((rc = stream_forward(c, batch, params, inputs, expvals, ws, stream, true))) return rc;
     rc = vqc::launch_loss_grad(loss_kind, batch, p.n, expvals, target, cot, stream);
     if (rc) return hip_fail("loss launch", rc);
     rc = stream_backward(c, batch, params, inputs, cot, ws, rows ? rows : dp, dx, stream);
@@ -772,7 +773,8 @@ int vqc_fd_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     for (int base = 0; base < NS; base += chunk) {
       const int cs = std::min(chunk, NS - base);
       const int64_t vb = batch * 2 * cs;
-      if ((rc = stream_forward(c, vb, params, inputs, ev, ws, stream, nullptr, nullptr, base, cs,
+      if ((rc = stream_forward(c, vb, params, inputs, ev, ws, stream, false, nullptr, nullptr,
+                               base, cs,
                                h)))
         return rc;
       rc = vqc::launch_fd_combine(batch, cs, base, p.P, p.F, p.n, h, ev, grad_out,

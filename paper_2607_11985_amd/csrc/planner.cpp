@@ -425,33 +425,38 @@ int plan_stream(Plan& plan, const std::vector<StreamGroup>& groups,
   return 0;
 }
 
-// Both directions of the streaming path: partitions, boundary layouts, sweeps.
-// The forward's first pass reads (Psi_0) in logical order; its last pass writes
-// psi_G in the layout the adjoint's first pass reads.
-int plan_stream_both(Plan& plan, const std::vector<Prim>& rev, std::string& msg) {
+// Both directions of the streaming path.  The forward is partitioned into
+// passes; the adjoint runs the same passes in reverse order, each over its
+// forward pass's gates reversed, so that it reads the state that forward pass
+// saved (a training forward keeps every pass's output) instead of rewriting
+// psi: an adjoint pass reads psi and lambda and writes only lambda.  The
+// forward's first pass reads (Psi_0) in logical order; the mirror of pass i
+// reads in the layout pass i wrote and writes in the layout pass i read.
+int plan_stream_both(Plan& plan, std::string& msg) {
   const int nq = plan.nq;
-  std::vector<StreamGroup> fg, bg;
+  std::vector<StreamGroup> fg;
   int rc = partition_stream(plan.prims, nq, plan.ng, fg, msg);
   if (rc < 0) return rc;
-  rc = partition_stream(rev, nq, plan.ng, bg, msg);
-  if (rc < 0) return rc;
-  const size_t nf = fg.size(), nb = bg.size();
+  const size_t nf = fg.size();
+  std::vector<StreamGroup> bg(nf);
+  for (size_t j = 0; j < nf; ++j) {
+    const StreamGroup& f = fg[nf - 1 - j];
+    bg[j].glob = f.glob;
+    bg[j].prims.assign(f.prims.rbegin(), f.prims.rend());
+  }
   std::vector<std::vector<int>> fin(nf, std::vector<int>(nq)), fout(nf, std::vector<int>(nq));
-  std::vector<std::vector<int>> bin(nb, std::vector<int>(nq)), bout(nb, std::vector<int>(nq));
+  std::vector<std::vector<int>> bin(nf, std::vector<int>(nq)), bout(nf, std::vector<int>(nq));
   identity_layout(nq, fin[0].data());
   for (size_t i = 0; i < nf; ++i) {
-    const uint32_t next = i + 1 < nf ? fg[i + 1].glob : bg[0].glob;
+    // the last output is read by its own mirror: same local qubits on both sides
+    const uint32_t next = i + 1 < nf ? fg[i + 1].glob : fg[i].glob;
     boundary_layout(fg[i].glob, next, nq, fout[i].data());
     if (i + 1 < nf) fin[i + 1] = fout[i];
   }
-  bin[0] = fout[nf - 1];
-  for (size_t j = 0; j < nb; ++j) {
-    if (j + 1 < nb) {
-      boundary_layout(bg[j].glob, bg[j + 1].glob, nq, bout[j].data());
-      bin[j + 1] = bout[j];
-    } else {
-      identity_layout(nq, bout[j].data());  // stores nothing
-    }
+  for (size_t j = 0; j < nf; ++j) {
+    bin[j] = fout[nf - 1 - j];
+    if (j + 1 < nf) bout[j] = fin[nf - 1 - j];
+    else identity_layout(nq, bout[j].data());  // the last adjoint pass stores nothing
   }
   rc = plan_stream(plan, fg, fin, fout, false, plan.Rf, plan.fwd, plan.fpass, plan.fwd_exchanges,
                    msg);
@@ -829,7 +834,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     plan.WG = 1 << plan.t;
     plan.S = 1;
     plan.G = plan.WG / 64;
-    rc = plan_stream_both(plan, rev, msg);
+    rc = plan_stream_both(plan, msg);
     if (rc < 0) return rc;
     const size_t xbuf = ((size_t)1 << plan.k) * 8;
     plan.lds_tab = xbuf;

@@ -1704,15 +1704,15 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   // the stores, in the layout this pass writes
   io_offsets<R>(A.io_out, A.k, A.ng, tid, g, base, off);
   base = opaque(base);
-  // the adjoint's last pass ends at psi_0: its states are not needed
-  const bool store = !BWD || !(A.flags & PF_LAST_ADJ);
-  if (store) {
+  // the adjoint stores lambda only (its psi is the state the forward saved at
+  // this pass's start), and nothing at all in its last pass
+  if (!BWD) {
     float2* dst = reinterpret_cast<float2*>(A.psi_dst) + sbase;
 #pragma unroll
     for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(a.r[j], a.i[j]);
   }
   if (BWD) {
-    if (store) {
+    if (!(A.flags & PF_LAST_ADJ)) {
       float2* dst = reinterpret_cast<float2*>(A.lam_dst) + sbase;
 #pragma unroll
       for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(l.r[j], l.i[j]);
