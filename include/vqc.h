@@ -124,9 +124,12 @@ typedef struct {
 typedef struct vqc_circuit vqc_circuit;
 
 /* compile options (pass NULL for the defaults) */
-#define VQC_PATH_AUTO 0     /* resident for n <= 13, streaming from n = 14 */
+#define VQC_PATH_AUTO 0     /* resident for n <= 13, streaming from n = 14 (at 14
+                               qubits the streaming passes were measured faster
+                               than the one-launch resident step) */
 #define VQC_PATH_RESIDENT 1 /* one launch, state on chip; requires n <= 14 */
-#define VQC_PATH_STREAM 2   /* tiles of 2^14 amplitudes streamed through HBM; n >= 14 */
+#define VQC_PATH_STREAM 2   /* tiles of 2^k amplitudes (k = tile_qubits) streamed
+                               through HBM, one launch per pass; n >= 14 */
 #define VQC_ENGINE_JIT 0    /* kernels generated for this circuit and compiled at
                                vqc_compile time (straight-line schedule) */
 #define VQC_ENGINE_INTERP 1 /* precompiled kernels that interpret the schedule */

@@ -20,7 +20,7 @@ struct vqc_circuit {
   vqc::JitKernels jit;
   void* blob = nullptr;
   size_t off_fwd = 0, off_bwd = 0, off_cols = 0, off_src = 0, off_idx = 0, off_cs = 0,
-         off_maps = 0, off_pslots = 0, off_ma = 0;
+         off_maps = 0, off_pslots = 0, off_ma = 0, off_zm = 0, off_pc = 0;
 };
 
 namespace {
@@ -170,6 +170,8 @@ vqc::TileArgs tile_args(const vqc_circuit* c, bool bwd, int64_t batch) {
   a.occ_ma = p.affine ? at<float>(c, c->off_ma) : nullptr;
   a.end_phys = at<uint8_t>(c, c->off_maps) + p.end_off;
   a.start_phys = at<uint8_t>(c, c->off_maps) + p.start_off;
+  a.zmask = p.zmask.empty() ? nullptr : at<uint32_t>(c, c->off_zm);
+  a.pcol = p.pcol.empty() ? nullptr : at<uint32_t>(c, c->off_pc);
   a.n_occ = (int32_t)p.occ_src.size();
   a.n_slots = p.P + p.F;
   a.P = p.P;
@@ -215,6 +217,7 @@ vqc::PassArgs pass_args(const vqc_circuit* c, const vqc::PassPlan& pp, bool bwd,
   a.io_lout = a.cols + pp.io_lout_off;
   a.start_phys = at<uint8_t>(c, c->off_maps) + pp.start_off;
   a.end_phys = at<uint8_t>(c, c->off_maps) + pp.end_off;
+  a.zmask = p.zmask.empty() ? nullptr : at<uint32_t>(c, c->off_zm);
   a.pslots = at<int32_t>(c, c->off_pslots) + pp.slots_off;
   a.n_pslots = pp.n_slots;
   a.flags = pp.flags;
@@ -423,16 +426,19 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
       c->plan = std::move(p12);
   }
   // The generated adjoint passes hold 16 amplitudes per thread by default (the
-  // batched gradient reduction fits there).  32 pay off where they remove at
-  // least a fifth of the adjoint's exchanges: measured on the 14-qubit
-  // re-uploading workload (36 -> 27 exchanges) 3 % faster, on the 16-qubit ring
-  // (71 -> 61) 25 % slower.
+  // batched gradient reduction fits there).  32 halve the workgroups per CU that
+  // hide each pass's loads and stores, and pay off only where they remove at
+  // least a fifth of the adjoint's exchanges and at least three per pass.
+  // Measured: the 14-qubit re-uploading workload (2 passes, 36 -> 27
+  // exchanges) 3 % faster; the 16-qubit ring (10-11 passes, 71 -> 61 and
+  // 62 -> 49 exchanges) 13-25 % slower.
   if (engine == VQC_ENGINE_JIT && reg_bits == 0 && c->plan.path == VQC_PATH_STREAM) {
     Plan p5;
     std::string msg5;
     if (vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, 0, p5, msg5, true, c->plan.k,
                         5) == 0 &&
-        5 * p5.bwd_exchanges <= 4 * c->plan.bwd_exchanges)
+        5 * p5.bwd_exchanges <= 4 * c->plan.bwd_exchanges &&
+        c->plan.bwd_exchanges - p5.bwd_exchanges >= 3 * (int)c->plan.bpass.size())
       c->plan = std::move(p5);
   }
   c->device = device;
@@ -455,6 +461,8 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
     c->off_ma = append(blob, p.occ_ma);
     c->off_maps = append(blob, p.maps);
     c->off_pslots = append(blob, p.pslots);
+    c->off_zm = append(blob, p.zmask);
+    c->off_pc = append(blob, p.pcol);
     DeviceGuard g(device);
     if (!g.ok()) {
       delete c;

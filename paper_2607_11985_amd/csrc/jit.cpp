@@ -93,21 +93,26 @@ void pauli_bits(int kind, uint32_t& x, uint32_t& z) {
 }
 
 Frame frame_rows(const Plan& p) {
+  // the circuit in an order equivalent to the original: the gates run, then the
+  // trailing entanglers folded into the measurement (the rows describe the
+  // frame on the final state)
+  std::vector<Prim> all(p.prims);
+  all.insert(all.end(), p.tail.begin(), p.tail.end());
   Frame f;
   const int nocc = (int)p.occ_src.size();
   f.words = (nocc + 31) / 32;
   const int W = f.words;
   f.arow.assign((size_t)nocc * W, 0u);
   f.erow.assign((size_t)p.n * W, 0u);
-  for (size_t i = 0; i < p.prims.size(); ++i) {
-    const Prim& src = p.prims[i];
+  for (size_t i = 0; i < all.size(); ++i) {
+    const Prim& src = all[i];
     if (src.occ < 0) continue;
     const int k = src.occ;
     uint32_t px, pz;
     pauli_bits(src.kind, px, pz);
     uint32_t x = px << src.q0, z = pz << src.q0;
-    for (size_t j = i + 1; j < p.prims.size(); ++j) {
-      const Prim& g = p.prims[j];
+    for (size_t j = i + 1; j < all.size(); ++j) {
+      const Prim& g = all[j];
       if (g.kind == P_CNOT) {  // X_c -> X_c X_t, Z_t -> Z_c Z_t
         const uint32_t xc = (x >> g.q0) & 1u, zt = (z >> g.q1) & 1u;
         x ^= xc << g.q1;
@@ -729,9 +734,18 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
 void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
   o << "static constexpr int kN = " << p.n << ", kNocc = " << p.occ_src.size()
     << ", kS = " << (p.path == VQC_PATH_RESIDENT ? p.S : 1) << ";\n"
-    << "__device__ __forceinline__ static int phys_of(const uint8_t*, int q) {\n";
-  std::vector<int> phys(p.maps.begin() + map_off, p.maps.begin() + map_off + p.n);
-  emit_array(o, "uint8_t", "t", phys);
+    << "__device__ __forceinline__ static uint32_t zmask(const uint8_t*, const uint32_t*, "
+       "int q) {\n";
+  // physical bits of each measured qubit's Z-string under this mapping
+  std::vector<uint32_t> zm(p.n);
+  for (int q = 0; q < p.n; ++q) {
+    const uint32_t m = p.zmask.empty() ? 1u << q : p.zmask[q];
+    uint32_t pm = 0;
+    for (int b = 0; b < p.n; ++b)
+      if ((m >> b) & 1u) pm |= 1u << p.maps[map_off + b];
+    zm[q] = pm;
+  }
+  emit_array(o, "uint32_t", "t", zm);
   o << "  return t[q];\n}\n"
     << "__device__ __forceinline__ static OccRec occ(const int32_t*, const int32_t*, const float*, "
        "const float*, int o) {\n";
@@ -794,9 +808,10 @@ void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
 void emit_sched_struct(std::ostringstream& o, const std::string& name, const Plan& p,
                        const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S,
                        const GradMode& gm, const TanMode& tm, const Frame* tables, int map_off,
-                       bool load = false) {
+                       bool load = false, int fixed_flags = -1) {
   o << "struct " << name << " {\n";
   emit_constants(o, p, map_off);
+  o << "static constexpr int kFixedFlags = " << fixed_flags << ";\n";
   o
     << "template <int R, bool BWD, bool WIDE>\n"
     << "__device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w, "
@@ -836,14 +851,14 @@ bool tangent_wanted(int S, int R) {
 std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
                         const uint32_t* ins, int n_ins, bool bwd, bool stream, int R, int S,
                         int threads, size_t lds, int n_slots, bool esign, int map_off,
-                        bool load = false) {
+                        bool load = false, int fixed_flags = -1) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
   const int lanes = stream ? threads : 1 << (p.k - R);
   TanMode tm = tan_mode(p, bwd ? nullptr : ins, n_ins, bwd ? ins : nullptr, n_ins, S, esign, lds);
   tm.on = tm.on && tangent_wanted(S, R);
   emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr,
-                    map_off, load);
+                    map_off, load, fixed_flags);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << name
     << (stream ? "(const vqc::PassArgs A) {\n" : "(const vqc::TileArgs A) {\n")
@@ -932,14 +947,16 @@ std::vector<JitUnit> jit_units(const Plan& p) {
     const PassPlan& pp = p.fpass[i];
     u.push_back({name, kernel_unit(p, fr, name, p.fwd.data() + 2 * pp.ins_off, pp.n_ins, false,
                                    true, p.Rf, 1, 1 << (p.k - p.Rf), p.lds_fwd, pp.n_slots,
-                                   (pp.flags & PF_ZPART) != 0, pp.end_off, load)});
+                                   (pp.flags & PF_ZPART) != 0, pp.end_off, load,
+                                   (int)(pp.flags & ~PF_INIT))});
   }
   for (size_t i = 0; i < p.bpass.size(); ++i) {
     const std::string name = "vqc_sb" + std::to_string(i);
     const PassPlan& pp = p.bpass[i];
     u.push_back({name, kernel_unit(p, fr, name, p.bwd.data() + 2 * pp.ins_off, pp.n_ins, true,
                                    true, p.Rb, 1, 1 << (p.k - p.Rb), p.lds_bwd, pp.n_slots,
-                                   (pp.flags & PF_MAKE_LAMBDA) != 0, pp.start_off, load)});
+                                   (pp.flags & PF_MAKE_LAMBDA) != 0, pp.start_off, load,
+                                   (int)(pp.flags & ~PF_INIT))});
   }
   if (load) u.push_back({"vqc_st", tables});
   return u;

@@ -293,7 +293,7 @@ int partition_stream(const std::vector<Prim>& seq, int nq, int ng,
     }
     std::vector<int> took;
     pass_gates(seq, done, best, all, &took);
-    if (took.empty()) {
+    if (took.empty() && remaining > 0) {
       msg = "internal: streaming pass made no progress";
       return VQC_ERR_UNSUPPORTED;
     }
@@ -351,15 +351,19 @@ Mapping io_mapping(uint32_t glob, const int* pos, int k, int R, int nq) {
 
 // The k + ng address columns of a tile under mapping m and layout pos: one per
 // tile rank (thread bits first, then register bits), then one per global bit.
-void push_io(const Mapping& m, const int* pos, int k, int R, std::vector<uint32_t>& cols) {
+// Addresses are the XOR of the columns of the set bits; with `col` a qubit's
+// column is col[pos[q]] instead of a single bit (a GF(2) map of the index).
+void push_io(const Mapping& m, const int* pos, int k, int R, std::vector<uint32_t>& cols,
+             const uint32_t* col = nullptr) {
   const int nt = k - R;
+  auto c = [&](int q) { return col ? col[pos[q]] : 1u << pos[q]; };
   for (int r = 0; r < k; ++r) {
     const int p = r < nt ? R + r : r - nt;
-    cols.push_back(1u << pos[m.p2q[p]]);
+    cols.push_back(c(m.p2q[p]));
   }
   std::vector<uint32_t> g(m.nq - k, 0u);
   for (int q = 0; q < m.nq; ++q)
-    if (m.q2p[q] >= k) g[m.q2p[q] - k] = 1u << pos[q];
+    if (m.q2p[q] >= k) g[m.q2p[q] - k] = c(q);
   cols.insert(cols.end(), g.begin(), g.end());
 }
 
@@ -413,7 +417,7 @@ int plan_stream(Plan& plan, const std::vector<StreamGroup>& groups,
     pp.io_lin_off = (int)plan.cols.size();
     push_io(io_in, ident, k, R, plan.cols);
     pp.io_lout_off = (int)plan.cols.size();
-    push_io(m, ident, k, R, plan.cols);
+    push_io(m, ident, k, R, plan.cols, plan.pcol.empty() ? nullptr : plan.pcol.data());
     pp.slots_off = (int)plan.pslots.size();
     pp.n_slots = (int)slots.size();
     plan.pslots.insert(plan.pslots.end(), slots.begin(), slots.end());
@@ -665,6 +669,53 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
+// Measurement of the trailing entanglers.  A CNOT or CZ none of whose qubits
+// carries a later rotation can move to the end of the circuit (everything after
+// it on its lines is such a gate too), and the entanglers there need not run:
+// with T their product, <Z_j> of the final state is <psi| T^dag Z_j T |psi> for
+// the state psi before them, and T^dag Z_j T is a Z-string (CNOT(c, t) takes Z_t
+// to Z_c Z_t, CZ leaves Z-strings alone); the probability of basis state A x
+// after them is that of x before them, A the GF(2) map of the CNOTs.  The
+// adjoint starts from lambda = (sum_j g_j T^dag Z_j T) psi.  (The tangent
+// form's frame rows still propagate through the tail: they describe the final
+// state.)
+void fold_trailing_entanglers(Plan& plan) {
+  std::vector<char> tail(plan.prims.size(), 0);
+  uint32_t blocked = 0;
+  bool any = false;
+  for (size_t i = plan.prims.size(); i-- > 0;) {
+    const Prim& g = plan.prims[i];
+    const uint32_t lines = lines_of(g);
+    if ((g.kind == P_CNOT || g.kind == P_CZ) && !(blocked & lines)) {
+      tail[i] = 1;
+      any = true;
+    } else {
+      blocked |= lines;
+    }
+  }
+  if (!any) return;
+  std::vector<Prim> body;
+  for (size_t i = 0; i < plan.prims.size(); ++i)
+    (tail[i] ? plan.tail : body).push_back(plan.prims[i]);
+  plan.prims.swap(body);
+  plan.zmask.assign(plan.n, 0u);
+  for (int j = 0; j < plan.n; ++j) {
+    uint32_t m = 1u << j;
+    for (size_t i = plan.tail.size(); i-- > 0;) {
+      const Prim& g = plan.tail[i];
+      if (g.kind == P_CNOT && ((m >> g.q1) & 1u)) m ^= 1u << g.q0;
+    }
+    plan.zmask[j] = m;
+  }
+  plan.pcol.assign(plan.n, 0u);
+  for (size_t q = 0; q < plan.pcol.size(); ++q) {
+    uint32_t v = 1u << q;
+    for (const Prim& g : plan.tail)
+      if (g.kind == P_CNOT && ((v >> g.q0) & 1u)) v ^= 1u << g.q1;
+    plan.pcol[q] = v;
+  }
+}
+
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
                Plan& plan, std::string& msg, bool lane_gates, int tile_qubits,
                int bwd_reg_bits) {
@@ -729,6 +780,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     }
     lower_gate(o, plan);
   }
+  fold_trailing_entanglers(plan);
   const int n_occ = (int)plan.occ_src.size();
   if (reg_bits != 0 && (reg_bits < 2 || reg_bits > 5)) {
     msg = "reg_bits must be 0 (default) or in [2, 5]";

@@ -1136,59 +1136,55 @@ __device__ __forceinline__ void angle_table(float2* tab, int n_occ, int S, int64
   }
 }
 
-// lambda = H psi with H = sum_q g_q Z_q, the Z signs read from the mapping
+// lambda = H psi with H = sum_q g_q Z(q), where Z(q) is the Z-string measured for
+// qubit q's <Z> (Z_q itself, or Z_q pulled back through the circuit's trailing
+// entanglers); Sched::zmask gives its physical bits under `phys`.
 template <int R, typename Sched>
 __device__ __forceinline__ void make_lambda(St<R>& l, const St<R>& a, const float* g, int n,
-                                            const uint8_t* phys, uint32_t tb, bool valid,
-                                            const float* esign = nullptr) {
-  float gt = 0.f, gr[R];
+                                            const uint8_t* phys, const uint32_t* zm, uint32_t tb,
+                                            bool valid, const float* esign = nullptr) {
+  constexpr uint32_t rbits = (1u << R) - 1u;
+  float h[St<R>::N];
 #pragma unroll
-  for (int b = 0; b < R; ++b) gr[b] = 0.f;
+  for (int u = 0; u < St<R>::N; ++u) h[u] = 0.f;
   if (valid) {
 #pragma unroll
     for (int q = 0; q < (Sched::kN >= 0 ? Sched::kN : n); ++q) {
-      const float gq = esign ? g[q] * esign[q] : g[q];
-      const int p = Sched::phys_of(phys, q);
-      if (p >= R) gt += ((tb >> (p - R)) & 1u) ? -gq : gq;
+      float gq = esign ? g[q] * esign[q] : g[q];
+      const uint32_t pm = Sched::zmask(phys, zm, q);
+      if (__builtin_popcount(tb & (pm >> R)) & 1) gq = -gq;
 #pragma unroll
-      for (int b = 0; b < R; ++b)
-        if (p == b) gr[b] += gq;
+      for (int u = 0; u < St<R>::N; ++u)
+        h[u] += (__builtin_popcount((uint32_t)u & pm & rbits) & 1) ? -gq : gq;
     }
   }
 #pragma unroll
   for (int u = 0; u < St<R>::N; ++u) {
-    float h = gt;
-#pragma unroll
-    for (int b = 0; b < R; ++b) h += (u & (1 << b)) ? -gr[b] : gr[b];
-    l.r[u] = h * a.r[u];
-    l.i[u] = h * a.i[u];
+    l.r[u] = h[u] * a.r[u];
+    l.i[u] = h[u] * a.i[u];
   }
 }
 
-// Per-qubit signed probability sums of this workgroup's amplitudes:
-// ez[q * G + grp] = sum over the group's amplitudes of (-1)^{x_q} |a|^2.
-// Must be called by every thread; ez may alias the exchange buffer.
+// Signed probability sums of this workgroup's amplitudes for every measured
+// qubit q: ez[q * G + grp] = sum over the group's amplitudes of
+// (-1)^{parity(x & Z(q))} |a|^2, Z(q) the qubit's measured Z-string.  Must be
+// called by every thread; ez may alias the exchange buffer.
 template <int R, typename Sched>
 __device__ __forceinline__ void z_partials(const St<R>& a, float* ez, int n, const uint8_t* phys,
-                                           const Walk& w) {
-  float tot = 0.f, sr[R];
+                                           const uint32_t* zm, const Walk& w) {
+  constexpr uint32_t rbits = (1u << R) - 1u;
+  float pj[St<R>::N];
 #pragma unroll
-  for (int b = 0; b < R; ++b) sr[b] = 0.f;
-#pragma unroll
-  for (int u = 0; u < St<R>::N; ++u) {
-    const float pj = a.r[u] * a.r[u] + a.i[u] * a.i[u];
-    tot += pj;
-#pragma unroll
-    for (int b = 0; b < R; ++b) sr[b] += (u & (1 << b)) ? -pj : pj;
-  }
+  for (int u = 0; u < St<R>::N; ++u) pj[u] = a.r[u] * a.r[u] + a.i[u] * a.i[u];
   __syncthreads();  // the exchange buffer may still be read by other threads
 #pragma unroll
   for (int q = 0; q < (Sched::kN >= 0 ? Sched::kN : n); ++q) {
-    const int p = Sched::phys_of(phys, q);
-    float v = ((w.tb >> (p - R)) & 1u) ? -tot : tot;
+    const uint32_t pm = Sched::zmask(phys, zm, q);
+    float v = 0.f;
 #pragma unroll
-    for (int b = 0; b < R; ++b)
-      if (p == b) v = sr[b];
+    for (int u = 0; u < St<R>::N; ++u)
+      v += (__builtin_popcount((uint32_t)u & pm & rbits) & 1) ? -pj[u] : pj[u];
+    if (__builtin_popcount(w.tb & (pm >> R)) & 1) v = -v;
     v = Sched::lane_sum(v, w);
     if (const float* es = Sched::esigns(w)) v *= es[q];
     if (w.leader) ez[q * w.G + w.grp] = v;
@@ -1205,8 +1201,20 @@ struct InterpSched {
   static constexpr int kNocc = -1, kS = -1;
   // the streaming passes compute their tables (no per-sample table kernel)
   static constexpr bool kLoadTables = false;
-  // physical bit of qubit q under the mapping the epilogue / lambda use
-  __device__ __forceinline__ static int phys_of(const uint8_t* phys, int q) { return phys[q]; }
+  // a pass's flags other than PF_INIT when fixed at compile time, else -1
+  static constexpr int kFixedFlags = -1;
+  // physical bits of qubit q's measured Z-string under the mapping the epilogue /
+  // lambda use (zm: the logical strings, or null for Z_q itself)
+  __device__ __forceinline__ static uint32_t zmask(const uint8_t* phys, const uint32_t* zm,
+                                                   int q) {
+    if (!zm) return 1u << phys[q];
+    uint32_t m = zm[q], pm = 0u;
+    while (m) {
+      pm |= 1u << phys[__builtin_ctz(m)];
+      m &= m - 1u;
+    }
+    return pm;
+  }
   __device__ __forceinline__ static OccRec occ(const int32_t* src, const int32_t* idx,
                                                const float* cs, const float* ma, int o) {
     OccRec r;
@@ -1350,9 +1358,13 @@ struct LogicalIndex {
   }
 };
 
+// The logical index of each of the thread's amplitudes under mapping `phys`,
+// as the XOR of per-qubit columns: 1 << q, or pc[q] where the index is mapped
+// through the trailing entanglers' basis permutation (probabilities).
 template <int R>
 __device__ __forceinline__ LogicalIndex<R> logical_index(const uint8_t* phys, int n, int k,
-                                                         uint32_t tb) {
+                                                         uint32_t tb,
+                                                         const uint32_t* pc = nullptr) {
   LogicalIndex<R> li;
   li.xt = 0u;
   li.pr = 0u;
@@ -1361,15 +1373,16 @@ __device__ __forceinline__ LogicalIndex<R> logical_index(const uint8_t* phys, in
   for (int b = 0; b < R; ++b) li.rq[b] = 0u;
   for (int q = 0; q < k; ++q) {
     const int p = phys[q];
+    const uint32_t col = q < n ? (pc ? pc[q] : 1u << q) : 0u;
     if (p >= R) {
       const uint32_t bit = (tb >> (p - R)) & 1u;
-      if (q < n) li.xt |= bit << q;
+      if (q < n) li.xt ^= bit ? col : 0u;
       else li.pt = li.pt || bit;
     } else {
 #pragma unroll
       for (int b = 0; b < R; ++b)
         if (p == b) {
-          if (q < n) li.rq[b] = 1u << q;
+          if (q < n) li.rq[b] = col;
           else li.pr |= 1u << b;
         }
     }
@@ -1424,7 +1437,7 @@ template <int WG, int R, typename Sched>
 __device__ __forceinline__ void resident_probs(const St<R>& a, const TileArgs& A, const Walk& w) {
   const int N = 1 << A.n;
   const uint32_t xm = frame_xmask(Sched::esigns(w), A.n);
-  const LogicalIndex<R> li = logical_index<R>(A.end_phys, A.n, A.k, w.tb);
+  const LogicalIndex<R> li = logical_index<R>(A.end_phys, A.n, A.k, w.tb, A.pcol);
   float* pb = w.xbuf;
   __syncthreads();  // the exchange buffer may still be read
   if (!li.pt) {
@@ -1480,8 +1493,8 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
     for (int j = 0; j < NA; ++j) v[j] = ws[((size_t)blockIdx.x * NA + j) * WG + tid];
 #pragma unroll
     for (int j = 0; j < NA; ++j) split(v[j], a.r[j], a.i[j]);
-    make_lambda<R, Sched>(l, a, A.grad_out + (valid ? b : 0) * A.n, A.n, A.end_phys, w.tb,
-                          valid, Sched::esigns(w));
+    make_lambda<R, Sched>(l, a, A.grad_out + (valid ? b : 0) * A.n, A.n, A.end_phys, A.zmask,
+                          w.tb, valid, Sched::esigns(w));
   }
 
   Sched::template run<R, BWD, (WG > 64)>(a, l, w, A.ins, A.n_ins);
@@ -1493,7 +1506,7 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
       for (int j = 0; j < NA; ++j)
         ws[((size_t)blockIdx.x * NA + j) * WG + tid] = make_float2(a.r[j], a.i[j]);
     }
-    z_partials<R, Sched>(a, w.xbuf, A.n, A.end_phys, w);
+    z_partials<R, Sched>(a, w.xbuf, A.n, A.end_phys, A.zmask, w);
     resident_expvals(A, w.xbuf, nullptr, WG);
     if (A.probs) resident_probs<WG, R, Sched>(a, A, w);
   } else {
@@ -1538,7 +1551,7 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
   St<R> a, l;
   zero_state<R>(a, w.stid);
   FS::template run<R, false, (WG > 64)>(a, l, w, A.ins, A.n_ins);
-  z_partials<R, FS>(a, w.xbuf, A.n, A.end_phys, w);
+  z_partials<R, FS>(a, w.xbuf, A.n, A.end_phys, A.zmask, w);
   resident_expvals(A, w.xbuf, e, WG);
   __syncthreads();
   for (int i = tid; i < A.S * A.n; i += WG) {
@@ -1551,18 +1564,19 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
     if (A.cot_out && bb < A.B) A.cot_out[bb * A.n + q] = v;
   }
   __syncthreads();
-  make_lambda<R, FS>(l, a, g + w.sl * A.n, A.n, A.end_phys, w.tb, valid, FS::esigns(w));
+  make_lambda<R, FS>(l, a, g + w.sl * A.n, A.n, A.end_phys, A.zmask, w.tb, valid,
+                     FS::esigns(w));
   BS::template run<R, true, (WG > 64)>(a, l, w, A.ins_b, A.n_ins_b);
   __syncthreads();
   resident_grads(A, w.acc, WG);
 }
 
 // ----------------------------------------------------- streaming kernel
-// One pass over B * 2^ng tiles of 2^14 amplitudes (2^(14-R) threads x 2^R).
-// Tiles are read and written in the pass's I/O layout: tile rank r (the
-// position of an amplitude among the 14 local qubits in ascending order) is
-// r = stid + 2^(14-R) j, so consecutive lanes touch consecutive low-qubit
-// addresses.
+// One pass over B * 2^ng tiles of 2^k amplitudes (2^(k-R) threads x 2^R).
+// A tile is loaded in the memory layout the pass reads and stored in the one
+// it writes: tile rank r (the amplitude's position among the k local qubits
+// ordered by address bit) is r = stid + 2^(k-R) j, so consecutive lanes touch
+// consecutive addresses.  Addresses are the XOR of per-bit columns (io_*).
 
 template <int R>
 __device__ __forceinline__ void io_offsets(const uint32_t* io, int k, int ng, int stid, int g,
@@ -1571,9 +1585,9 @@ __device__ __forceinline__ void io_offsets(const uint32_t* io, int k, int ng, in
   base = 0;
 #pragma unroll
   for (int i = 0; i < kMaxTileQubits - 2; ++i)
-    if (i < nt && ((stid >> i) & 1)) base |= io[i];
+    if (i < nt && ((stid >> i) & 1)) base ^= io[i];
   for (int i = 0; i < ng; ++i)
-    if ((g >> i) & 1) base |= io[k + i];
+    if ((g >> i) & 1) base ^= io[k + i];
   uint32_t c[R];
 #pragma unroll
   for (int b = 0; b < R; ++b) c[b] = io[nt + b];
@@ -1587,7 +1601,7 @@ __device__ __forceinline__ void load_tile(St<R>& a, const float2* src, uint32_t 
                                           const uint32_t (&off)[1 << R]) {
   float2 v[1 << R];
 #pragma unroll
-  for (int j = 0; j < (1 << R); ++j) v[j] = src[base | off[j]];
+  for (int j = 0; j < (1 << R); ++j) v[j] = src[base ^ off[j]];
 #pragma unroll
   for (int j = 0; j < (1 << R); ++j) split(v[j], a.r[j], a.i[j]);
 }
@@ -1672,13 +1686,19 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
     Sched::prepare(w, tid, WG, pre);
   }
 
+  // A generated pass knows its flags (all but PF_INIT, which a caller's Psi_0
+  // clears): a runtime branch between forming lambda and loading it would have
+  // the compiler copy the whole gate sequence into both arms.
+  const uint32_t flags = Sched::kFixedFlags >= 0
+                             ? (A.flags & PF_INIT) | (uint32_t)Sched::kFixedFlags
+                             : A.flags;
   uint32_t base, off[NA];
   // Psi_0 is read in logical order; the passes' own states in their layouts
-  const bool logical_in = !BWD && !(A.flags & PF_INIT) && A.psi0_in;
+  const bool logical_in = !BWD && !(flags & PF_INIT) && A.psi0_in;
   io_offsets<R>(logical_in ? A.io_lin : A.io, A.k, A.ng, tid, g, base, off);
   const size_t sbase = (size_t)b << (A.k + A.ng);
   St<R> a, l;
-  if (!BWD && (A.flags & PF_INIT)) {
+  if (!BWD && (flags & PF_INIT)) {
 #pragma unroll
     for (int j = 0; j < NA; ++j) {
       a.r[j] = 0.f;
@@ -1690,8 +1710,8 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
     load_tile<R>(a, src, base, off);
   }
   if (BWD) {
-    if (A.flags & PF_MAKE_LAMBDA) {
-      make_lambda<R, Sched>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, w.tb, true,
+    if (flags & PF_MAKE_LAMBDA) {
+      make_lambda<R, Sched>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, A.zmask, w.tb, true,
                             Sched::esigns(w));
     } else {
       const float2* src = reinterpret_cast<const float2*>(A.lam_src) + sbase;
@@ -1709,13 +1729,13 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   if (!BWD) {
     float2* dst = reinterpret_cast<float2*>(A.psi_dst) + sbase;
 #pragma unroll
-    for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(a.r[j], a.i[j]);
+    for (int j = 0; j < NA; ++j) dst[base ^ off[j]] = make_float2(a.r[j], a.i[j]);
   }
   if (BWD) {
-    if (!(A.flags & PF_LAST_ADJ)) {
+    if (!(flags & PF_LAST_ADJ)) {
       float2* dst = reinterpret_cast<float2*>(A.lam_dst) + sbase;
 #pragma unroll
-      for (int j = 0; j < NA; ++j) dst[base | off[j]] = make_float2(l.r[j], l.i[j]);
+      for (int j = 0; j < NA; ++j) dst[base ^ off[j]] = make_float2(l.r[j], l.i[j]);
     }
     __syncthreads();
     float* gp = A.gpart + blk * A.n_slots;
@@ -1724,7 +1744,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
       for (int r = 0; r < G; ++r) v += acc[i * G + r];
       gp[A.pslots[i]] += v;
     }
-  } else if (A.flags & PF_ZPART) {
+  } else if (flags & PF_ZPART) {
     if (A.probs) {
       // the tile's rows are in logical order: a permutation of the stored
       // state's addresses, so the stores stay coalesced
@@ -1732,10 +1752,10 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
       float* pd = A.probs + sbase;
       io_offsets<R>(A.io_lout, A.k, A.ng, tid, g, base, off);
 #pragma unroll
-      for (int j = 0; j < NA; ++j) pd[(base | off[j]) ^ xm] = a.r[j] * a.r[j] + a.i[j] * a.i[j];
+      for (int j = 0; j < NA; ++j) pd[(base ^ off[j]) ^ xm] = a.r[j] * a.r[j] + a.i[j] * a.i[j];
     }
     float* ez = xbuf;
-    z_partials<R, Sched>(a, ez, A.n, A.end_phys, w);
+    z_partials<R, Sched>(a, ez, A.n, A.end_phys, A.zmask, w);
     for (int q = tid; q < A.n; q += WG) {
       float e = 0.f;
       for (int r = 0; r < G; ++r) e += ez[q * G + r];

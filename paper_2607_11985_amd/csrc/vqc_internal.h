@@ -49,6 +49,12 @@ struct Plan {
   int lanes = 0;                          // lane bits that take RX / RY / CNOT targets
   int P = 0, F = 0, n_ops = 0, path = 1;
   std::vector<Prim> prims;
+  // Trailing entanglers (CNOT / CZ with no later rotation on their qubits) are
+  // not run: <Z_j> after them is the expectation of the Z-string zmask[j]
+  // before them, and a basis state x before them is A x after them, A the
+  // GF(2) map with columns pcol[q].  Both empty when there are none.
+  std::vector<Prim> tail;
+  std::vector<uint32_t> zmask, pcol;
   std::vector<int32_t> occ_src, occ_idx, occ_slot;
   std::vector<float> occ_cs;              // 2 per occurrence
   std::vector<float> occ_ma;              // 2 per occurrence: angle = mul * value + add

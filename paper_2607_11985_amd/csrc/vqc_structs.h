@@ -74,6 +74,11 @@ struct TileArgs {
   const float* occ_ma;      // per occurrence (mul, add): angle = mul * value + add;
                             // null when every occurrence is (1, 0)
   const uint8_t* end_phys;  // per logical qubit: physical bit at forward end
+  // the circuit's trailing entanglers, folded into the measurement (null when
+  // it has none): per measured qubit the logical Z-string whose expectation is
+  // its <Z>, and per qubit the image of its basis-index bit (probabilities)
+  const uint32_t* zmask;
+  const uint32_t* pcol;
   int32_t n_occ, n_slots, P, F;
   int32_t pstride;          // row stride of params: P, or 0 when shared by the batch
   int32_t n;                // real qubits (E and g have n columns)
@@ -107,7 +112,7 @@ struct TileArgs {
   float* probs;             // [B][2^n] |psi_x|^2 of the final states, or null
 };
 
-// Arguments of one streaming pass (1024 threads, one 2^14 tile per workgroup).
+// Arguments of one streaming pass (one 2^k tile per workgroup, k <= 14).
 struct PassArgs {
   const uint32_t* ins;
   int32_t n_ins;
@@ -118,6 +123,7 @@ struct PassArgs {
   const uint32_t* io_lout;     // stores in logical order (probabilities)
   const uint8_t* start_phys;   // logical -> phys at pass start
   const uint8_t* end_phys;     // logical -> phys at pass end
+  const uint32_t* zmask;       // measured Z-strings (as in TileArgs), or null
   const int32_t* pslots;       // pass-local -> global gradient slot
   int32_t n_pslots;
   int32_t flags;

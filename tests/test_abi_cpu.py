@@ -69,8 +69,18 @@ def test_configs_plan_on_host(idx):
     if w.n_qubits >= 14:
         assert info["fwd_passes"] > 1 and info["bwd_passes"] > 1
     assert info["lds_bytes_bwd"] <= 160 * 1024
-    # forward and backward sweep each hold one instruction per primitive plus exchanges
-    n_prims = sum(3 if o.kind == "ROT" else 1 for o in w.ops)
+    # forward and backward sweep each hold one instruction per primitive plus
+    # exchanges, except the trailing entanglers (no rotation after them on their
+    # qubits), which the measurement absorbs: here the last layer's CNOT ring / CZ
+    # chain
+    blocked, trailing = set(), 0
+    for o in reversed(w.ops):
+        if o.kind in ("CNOT", "CZ") and not blocked & set(o.wires):
+            trailing += 1
+        else:
+            blocked |= set(o.wires)
+    assert trailing == (w.n_qubits - 1 if idx == 4 else w.n_qubits)
+    n_prims = sum(3 if o.kind == "ROT" else 1 for o in w.ops) - trailing
     assert info["fwd_instructions"] == n_prims + info["fwd_exchanges"]
     assert info["bwd_instructions"] == n_prims + info["bwd_exchanges"]
     assert _lib.vqc_workspace_bytes(h, 0, 1) == 0
