@@ -316,6 +316,14 @@ int vqc_loss_grad(int32_t kind, int64_t batch, int32_t n_qubits, const float *ex
  *   [batch, F] written (either may be NULL); workspace:
  *   vqc_workspace_bytes(c, batch, 2) bytes, 256-byte aligned (on the resident
  *   path 0 bytes / NULL unless shared_params).
+ * On the streaming path (batch >= 2) the call runs the first ceil(batch / 2)
+ * samples on `stream` and the rest on a side stream that the library creates
+ * on the device at first use (default priority) and keeps until exit: the
+ * side stream waits for the work queued on `stream` before the call, and
+ * `stream` waits for the side stream at its end, so the call is ordered on
+ * `stream` like a single launch.  Calls that overlap on one device share the
+ * side stream (they stay correct but queue behind each other there); under
+ * stream capture the side stream joins the capture.
  * Results equal those of the three separate calls.  Errors: those of the
  * three calls.
  */
@@ -336,7 +344,8 @@ int vqc_train_step(const vqc_circuit *c, int64_t batch, const float *params, con
  * MiB per sample).  Every call on one GPU uses that GPU's single array and
  * finds there what the last call left (the call clears what must start at
  * zero): calls that overlap on one GPU, from other streams or threads, race
- * and must be ordered by the caller.
+ * and must be ordered by the caller.  The whole step runs on `stream` (no side
+ * stream).
  */
 #define VQC_NOALLOC_SCRATCH_BYTES 67108864
 int vqc_train_step_noalloc(const vqc_circuit *c, int64_t batch, const float *params,

@@ -4,6 +4,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -103,10 +104,24 @@ StreamLayout stream_layout(const Plan& p, int64_t batch) {
   return L;
 }
 
+// The streaming training step runs its batch as two halves, one on the
+// caller's stream and one on a side stream, so that one half's passes fill
+// the CUs the other's leave idle (the tail of each pass; the HBM-bound forward
+// of one half beside the VALU-bound adjoint of the other).  Each half has a
+// layout of its own: [half 0 | half 1].
+bool split_step(const Plan& p, int64_t batch) { return p.path == VQC_PATH_STREAM && batch >= 2; }
+int64_t first_half(int64_t batch) { return (batch + 1) / 2; }
+size_t second_half_offset(const Plan& p, int64_t batch) {
+  return align_up(stream_layout(p, first_half(batch)).end_step, 256);
+}
+
 // mode: 0 inference forward, 1 training forward (+ backward), 2 training step
 size_t required_bytes_core(const Plan& p, int64_t batch, int mode) {
   if (batch == 0) return 0;
   if (p.path == VQC_PATH_STREAM) {
+    if (mode == 2 && split_step(p, batch))
+      return second_half_offset(p, batch) +
+             stream_layout(p, batch - first_half(batch)).end_step;
     const StreamLayout L = stream_layout(p, batch);
     return mode == 0 ? L.end_inference : mode == 1 ? L.end_training : L.end_step;
   }
@@ -663,12 +678,96 @@ int check_step_args(const vqc_circuit* c, int64_t batch, const float* params,
   return VQC_OK;
 }
 
+// The library's side stream on `device` (the caller makes it current),
+// created on first use with the default priority and kept until exit.
+int side_stream(int device, hipStream_t* out) {
+  static std::mutex mu;
+  static hipStream_t streams[vqc::kScratchDevices] = {};
+  *out = nullptr;
+  if (device < 0 || device >= vqc::kScratchDevices) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!streams[device]) {
+    hipStream_t s = nullptr;
+    const hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    if (e != hipSuccess) return (int)e;
+    streams[device] = s;
+  }
+  *out = streams[device];
+  return 0;
+}
+
+// Streaming forward, loss cotangent and adjoint of `batch` rows of a batch of
+// `norm` samples (pointers at the rows' start, the workspace laid out for
+// `batch`).
+int stream_step(const vqc_circuit* c, int64_t batch, int64_t norm, const float* params,
+                const float* inputs, int32_t loss_kind, const float* target, float* expvals,
+                float* grad_out, float* dp, float* dx, unsigned char* ws, void* stream) {
+  const Plan& p = c->plan;
+  float* cot = grad_out ? grad_out : reinterpret_cast<float*>(ws + stream_layout(p, batch).cot);
+  int rc = stream_forward(c, batch, params, inputs, expvals, ws, stream, true);
+  if (rc) return rc;
+  rc = vqc::launch_loss_grad(loss_kind, batch, norm, p.n, expvals, target, cot, stream);
+  if (rc) return hip_fail("loss launch", rc);
+  return stream_backward(c, batch, params, inputs, cot, ws, dp, dx, stream);
+}
+
+template <typename T>
+T* rows_at(T* base, int64_t row, int64_t width) {
+  return base ? base + row * width : nullptr;
+}
+
+// The two halves of a streaming step: the first on `stream`, the second on the
+// side stream, which waits for the work queued on `stream` before the call;
+// `stream` then waits for the second half, so work queued on it later sees
+// the whole step.
+int stream_step_split(const vqc_circuit* c, int64_t batch, const float* params,
+                      const float* inputs, int32_t loss_kind, const float* target,
+                      float* expvals, float* grad_out, float* dp, float* dx, unsigned char* ws,
+                      void* stream) {
+  const Plan& p = c->plan;
+  const int64_t b0 = first_half(batch), b1 = batch - b0;
+  hipStream_t side = nullptr;
+  int rc = side_stream(c->device, &side);
+  if (rc) return hip_fail("side stream creation", rc);
+  hipEvent_t fork = nullptr, join = nullptr;
+  if ((rc = hipEventCreateWithFlags(&fork, hipEventDisableTiming)))
+    return hip_fail("event creation", rc);
+  if ((rc = hipEventCreateWithFlags(&join, hipEventDisableTiming))) {
+    (void)hipEventDestroy(fork);
+    return hip_fail("event creation", rc);
+  }
+  struct Events {
+    hipEvent_t a, b;
+    ~Events() {
+      (void)hipEventDestroy(a);  // released once the device has passed them
+      (void)hipEventDestroy(b);
+    }
+  } events{fork, join};
+  if ((rc = hipEventRecord(fork, (hipStream_t)stream)) ||
+      (rc = hipStreamWaitEvent(side, fork, 0)))
+    return hip_fail("stream fork", rc);
+  rc = stream_step(c, b0, batch, params, inputs, loss_kind, target, expvals, grad_out, dp, dx, ws,
+                   stream);
+  if (rc) return rc;
+  const int64_t P = c->shared ? 0 : p.P;
+  const int rc1 = stream_step(c, b1, batch, rows_at(params, b0, P), rows_at(inputs, b0, p.F),
+                              loss_kind, rows_at(target, b0, 1), rows_at(expvals, b0, p.n),
+                              rows_at(grad_out, b0, p.n), rows_at(dp, b0, p.P),
+                              rows_at(dx, b0, p.F), ws + second_half_offset(p, batch), side);
+  // join even after a failed launch, so that `stream` never runs ahead of
+  // what the side stream already holds
+  if ((rc = hipEventRecord(join, side)) || (rc = hipStreamWaitEvent((hipStream_t)stream, join, 0)))
+    return hip_fail("stream join", rc);
+  return rc1;
+}
+
 // The training step on a checked, large enough workspace, with the handle's
-// device current.
+// device current.  split: the streaming path may run the two halves of the
+// batch on two streams (the workspace then holds the split layout).
 int train_step_impl(const vqc_circuit* c, int64_t batch, const float* params,
                     const float* inputs, int32_t loss_kind, const float* target, float* expvals,
                     float* grad_out, float* dparams, float* dinputs, void* workspace,
-                    void* stream) {
+                    void* stream, bool split) {
   const Plan& p = c->plan;
   int rc = 0;
   float* dp = p.P > 0 ? dparams : nullptr;
@@ -678,12 +777,11 @@ int train_step_impl(const vqc_circuit* c, int64_t batch, const float* params,
                                   : nullptr;
   if (p.path == VQC_PATH_STREAM) {
     unsigned char* ws = static_cast<unsigned char*>(workspace);
-    float* cot = grad_out ? grad_out
-                          : reinterpret_cast<float*>(ws + stream_layout(p, batch).cot);
-    if ((rc = stream_forward(c, batch, params, inputs, expvals, ws, stream, true))) return rc;
-    rc = vqc::launch_loss_grad(loss_kind, batch, p.n, expvals, target, cot, stream);
-    if (rc) return hip_fail("loss launch", rc);
-    rc = stream_backward(c, batch, params, inputs, cot, ws, rows ? rows : dp, dx, stream);
+    rc = split && split_step(p, batch)
+             ? stream_step_split(c, batch, params, inputs, loss_kind, target, expvals, grad_out,
+                                 rows ? rows : dp, dx, ws, stream)
+             : stream_step(c, batch, batch, params, inputs, loss_kind, target, expvals, grad_out,
+                           rows ? rows : dp, dx, ws, stream);
     if (rc || !rows) return rc;
     rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream);
     return rc ? hip_fail("parameter gradient sum", rc) : VQC_OK;
@@ -726,7 +824,7 @@ int vqc_train_step(const vqc_circuit* c, int64_t batch, const float* params, con
   DeviceGuard g(c->device);
   if (!g.ok()) return fail(VQC_ERR_HIP, "hipSetDevice failed");
   return train_step_impl(c, batch, params, inputs, loss_kind, target, expvals, grad_out, dparams,
-                         dinputs, workspace, stream);
+                         dinputs, workspace, stream, true);
 }
 
 int vqc_train_step_noalloc(const vqc_circuit* c, int64_t batch, const float* params,
@@ -746,8 +844,9 @@ int vqc_train_step_noalloc(const vqc_circuit* c, int64_t batch, const float* par
   void* ws = nullptr;
   if (need > 0 && (rc = vqc::scratch_pointer(c->device, &ws)))
     return hip_fail("lookup of the static scratch", rc);
+  // one stream: the side stream and its events would be created on first use
   return train_step_impl(c, batch, params, inputs, loss_kind, target, expvals, grad_out, dparams,
-                         dinputs, ws, stream);
+                         dinputs, ws, stream, false);
 }
 
 int vqc_fd_backward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
@@ -822,7 +921,7 @@ int vqc_loss_grad(int32_t kind, int64_t batch, int32_t n_qubits, const float* ex
   if (!expvals || !grad_out) return fail(VQC_ERR_INVALID_ARG, "expvals or grad_out is NULL");
   if ((kind == VQC_LOSS_MSE_Z0 || kind == VQC_LOSS_MSE_MEANZ) && !target)
     return fail(VQC_ERR_INVALID_ARG, "MSE losses need a target");
-  int rc = vqc::launch_loss_grad(kind, batch, n_qubits, expvals, target, grad_out, stream);
+  int rc = vqc::launch_loss_grad(kind, batch, batch, n_qubits, expvals, target, grad_out, stream);
   if (rc) return fail(VQC_ERR_HIP, std::string("loss launch failed: ") +
                                        hipGetErrorString((hipError_t)rc));
   return VQC_OK;

@@ -109,14 +109,16 @@ __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
   if (i < count) p[i] = 0.f;
 }
 
-__global__ void loss_grad_kernel(int kind, int64_t B, int n, const float* __restrict__ e,
-                                 const float* __restrict__ y, float* __restrict__ g) {
+// rows b < B of a batch of `norm` samples (the MSE losses average over norm)
+__global__ void loss_grad_kernel(int kind, int64_t B, int64_t norm, int n,
+                                 const float* __restrict__ e, const float* __restrict__ y,
+                                 float* __restrict__ g) {
   const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= B) return;
   const float* eb = e + b * n;
   float* gb = g + b * n;
   const float yb = y ? y[b] : 0.f;
-  for (int j = 0; j < n; ++j) gb[j] = loss_cot(kind, eb, yb, n, j, B);
+  for (int j = 0; j < n; ++j) gb[j] = loss_cot(kind, eb, yb, n, j, norm);
 }
 
 // ------------------------------------------------------------ launchers
@@ -281,12 +283,12 @@ int scratch_pointer(int device, void** out) {
   return 0;
 }
 
-int launch_loss_grad(int kind, int64_t batch, int n, const float* e, const float* y, float* g,
-                     void* stream) {
+int launch_loss_grad(int kind, int64_t batch, int64_t norm, int n, const float* e,
+                     const float* y, float* g, void* stream) {
   const int threads = 256;
   const int64_t blocks = (batch + threads - 1) / threads;
   hipLaunchKernelGGL(loss_grad_kernel, dim3((unsigned)blocks), dim3(threads), 0,
-                     (hipStream_t)stream, kind, batch, n, e, y, g);
+                     (hipStream_t)stream, kind, batch, norm, n, e, y, g);
   return (int)hipGetLastError();
 }
 

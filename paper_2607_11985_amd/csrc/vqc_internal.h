@@ -106,8 +106,9 @@ int launch_fd_combine(int64_t batch, int NS, int base, int P, int F, int n, floa
                       void* stream);
 // out[p] = sum over b of rows[b * P + p], in a fixed order
 int launch_sum_rows(int64_t batch, int P, const float* rows, float* out, void* stream);
-int launch_loss_grad(int kind, int64_t batch, int n, const float* e, const float* y, float* g,
-                     void* stream);
+// rows [0, batch) of a batch of `norm` samples (the MSE losses divide by norm)
+int launch_loss_grad(int kind, int64_t batch, int64_t norm, int n, const float* e, const float* y,
+                     float* g, void* stream);
 // Device address of the static scratch array (VQC_NOALLOC_SCRATCH_BYTES) on
 // `device`, which must be the current device; looked up once per device and
 // kept.  Returns 0 or a hipError_t value.

@@ -39,7 +39,7 @@ int launch_fd_combine(int64_t, int, int, int, int, int, float, const float*, con
   no_device("fd");
 }
 int launch_sum_rows(int64_t, int, const float*, float*, void*) { no_device("sum_rows"); }
-int launch_loss_grad(int, int64_t, int, const float*, const float*, float*, void*) {
+int launch_loss_grad(int, int64_t, int64_t, int, const float*, const float*, float*, void*) {
   no_device("loss");
 }
 int prepare_kernels(const Plan&) { no_device("prepare"); }

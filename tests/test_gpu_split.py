@@ -1,0 +1,82 @@
+"""The streaming training step runs the two halves of its batch on two streams
+(the caller's and the library's side stream).  Checked here: equal bit for bit
+to the separate forward, loss and backward calls (one stream, the whole batch)
+for odd and even batches and every loss head (the MSE heads average over the
+whole batch, not over a half), with shared parameters, and within the oracle's
+bars on sampled rows; and ordered on the caller's stream, so that work queued
+there after the call sees the whole step."""
+import numpy as np
+import pytest
+
+from paper_2607_11985_amd import workloads as W
+from tests.parity_util import check_step, note
+from tests.test_gpu_parity import torch_mod  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+
+def separate(torch, c, p, x, loss, yt):
+    from paper_2607_11985_amd.api import loss_grad
+    E, ws = c.forward(p, x, training=True)
+    g = loss_grad(loss, E, yt)
+    dp, dx = c.backward(p, x, g, ws)
+    torch.cuda.synchronize()
+    return [t.cpu().numpy() for t in (E, g, dp, dx)]
+
+
+@pytest.mark.parametrize("n,B,loss,shared", [(14, 2, "mse_z0", False), (14, 3, "mse_meanz", False),
+                                             (15, 5, "mean", True), (16, 4, "mse_meanz", False),
+                                             (16, 7, "sum", False)])
+def test_split_step_equals_separate_calls(torch_mod, n, B, loss, shared):
+    torch = torch_mod
+    from paper_2607_11985_amd.api import Circuit
+    ops, P, F = W.random_circuit(n, 12 * n, seed=21000 + n + B)
+    params, inputs = W.random_inputs(B, P, F, seed=21100 + n + B)
+    y = np.random.default_rng(21200 + B).uniform(-1, 1, size=B).astype(np.float32)
+    c = Circuit(ops, n, P, F, path="stream", shared_params=shared)
+    note(f"split step n={n} B={B} loss={loss} shared={shared} tiles={c.info()['tile_qubits']}")
+    p = torch.from_numpy(np.ascontiguousarray(params[0] if shared else params)).cuda()
+    x = torch.from_numpy(inputs).cuda()
+    yt = torch.from_numpy(y).cuda()
+    E, dp, dx, g = c.train_step(p, x, loss, yt, want_cot=True)
+    torch.cuda.synchronize()
+    got = [t.cpu().numpy() for t in (E, g, dp, dx)]
+    ref = separate(torch, c, p, x, loss, yt)
+    for name, a, b in zip(("E", "g", "dparams", "dinputs"), got, ref):
+        assert np.array_equal(a, b), f"{name} differs from the separate calls"
+    if not shared:
+        rows = [0, B - 1]  # one row from each half
+        check_step(got[0][rows], got[1][rows], got[2][rows], got[3][rows], ops, n,
+                   params[rows], inputs[rows], y[rows].astype(np.float64), loss, B)
+
+
+def test_split_step_ordered_on_caller_stream(torch_mod):
+    """On a non-default stream: a copy queued there right after the call (no
+    synchronization in between) reads the finished gradients of both halves."""
+    torch = torch_mod
+    from paper_2607_11985_amd import _lib
+    from paper_2607_11985_amd.api import Circuit
+    w = W.make_config(5, batch=16)
+    B, n = w.batch, w.n_qubits
+    c = Circuit(w.ops, n, w.n_params, w.n_inputs)
+    dev = torch.device("cuda", 0)
+    note(f"{w.name} B={B}: step on a side stream of the caller, then a copy on it")
+    p = torch.from_numpy(w.params).to(dev)
+    x = torch.from_numpy(w.inputs).to(dev)
+    E = torch.full((B, n), float("nan"), device=dev)
+    dp = torch.full((B, w.n_params), float("nan"), device=dev)
+    dx = torch.full((B, w.n_inputs), float("nan"), device=dev)
+    nb = c.workspace_bytes(B, 2)
+    ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    s = torch.cuda.Stream(dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s):
+        _lib.vqc_train_step(c.handle, B, p.data_ptr(), x.data_ptr(), _lib.LOSS["sum"], None,
+                            E.data_ptr(), None, dp.data_ptr(), dx.data_ptr(), ws.data_ptr(), nb,
+                            s.cuda_stream)
+        copies = [t.clone() for t in (E, dp, dx)]
+    torch.cuda.synchronize()
+    for a, b in zip(copies, (E, dp, dx)):
+        a, b = a.cpu().numpy(), b.cpu().numpy()
+        assert np.all(np.isfinite(a)), "a copy ran before the step finished"
+        assert np.array_equal(a, b)
