@@ -42,6 +42,12 @@ std::string hex(uint32_t v) {
   return b;
 }
 
+std::string hex64(uint64_t v) {
+  char b[24];
+  std::snprintf(b, sizeof b, "0x%llxull", (unsigned long long)v);
+  return b;
+}
+
 // How the adjoint kernels collect gradient partials.  Lanes are grouped by
 // sample (tm lanes: the sample's threads, at most one wave).  With `regs`, lane
 // j of a group keeps slots j, j + tm, ... in registers (nr of them) and adds
@@ -188,7 +194,8 @@ void emit_array(std::ostringstream& o, const char* type, const char* name, const
 // of the adjoint's gradients; and the <Z> signs.  esigns(): those signs.  The
 // block factors are products the schedule forms as it goes (bp).
 void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const Frame& fr,
-                 int nt, bool all = false, bool load = false) {
+                 int nt, bool all = false, bool load = false,
+                 const std::vector<char>* head = nullptr) {
   const int nocc = (int)p.occ_src.size(), W = t.W;
   o << "static constexpr bool kLoadTables = " << (t.on && load ? "true" : "false") << ";\n"
     << "static constexpr uint32_t kOffGm = " << t.off_gm << "u;\n";
@@ -264,8 +271,23 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
   } else {
     o << "  (void)tid;\n";
   }
-  o << "  return p;\n}\n"
-    << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt, "
+  o << "  return p;\n}\n";
+  if (head) {
+    // whether occurrence i0 + tid is a head rotation: one 64-bit mask per 64
+    // occurrences, picked by the wave-uniform chunk index
+    o << "__device__ __forceinline__ static bool head_occ(int i0, int tid) {\n"
+      << "  const uint32_t c = (uint32_t)(i0 >> 6) + "
+         "__builtin_amdgcn_readfirstlane((uint32_t)tid >> 6);\n"
+      << "  uint64_t m = 0ull;\n";
+    for (int c = 0; 64 * c < nocc; ++c) {
+      uint64_t m = 0;
+      for (int j = 0; j < 64 && 64 * c + j < nocc; ++j)
+        if ((*head)[64 * c + j]) m |= 1ull << j;
+      if (m) o << "  if (c == " << c << "u) m = " << hex64(m) << ";\n";
+    }
+    o << "  return (m >> (tid & 63)) & 1ull;\n}\n";
+  }
+  o << "__device__ __forceinline__ static void prepare(const Walk& w, int tid, int nt, "
        "const Pre& pre) {\n"
     << "  (void)pre;\n"
     << "  float2* tab = const_cast<float2*>(w.tab);\n"
@@ -274,7 +296,8 @@ void emit_tables(std::ostringstream& o, const Plan& p, const TanMode& t, const F
     << "  for (int i0 = 0; i0 < " << nocc << "; i0 += nt) {\n"
     << "    const int i = i0 + tid;\n"
     << "    bool odd = false;\n"
-    << "    if (i < " << nocc << ") {\n"
+    // head rotations run exactly (their parity stays 0, their (cos, sin) stay)
+    << "    if (i < " << nocc << (head ? " && !head_occ(i0, tid)" : "") << ") {\n"
     << "      const float2 cs = tab[i];\n"
     << "      odd = fabsf(cs.y) > fabsf(cs.x);\n"
     << "      tab[i] = make_float2(odd ? -cs.x / cs.y : cs.y / cs.x, odd ? fabsf(cs.y) : fabsf(cs.x));\n"
@@ -460,7 +483,8 @@ std::string occ_scale(const Plan& p, uint32_t occ) {
 // Statements of one instruction stream for register width R.  With tangent
 // tables (tm.on) rotations use the tangent form and blocks are rescaled.
 void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, int n_ins, bool bwd,
-                   int R, int k, int S, const GradMode& gm, const TanMode& tm) {
+                   int R, int k, int S, const GradMode& gm, const TanMode& tm,
+                   const std::vector<char>* skip = nullptr) {
   const int t = k - R;
   const bool tan = tm.on;
   const int nrot = (int)(bwd ? tm.bocc.size() : tm.focc.size());
@@ -617,6 +641,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         break;
       }
       default: {
+        if (skip && (*skip)[arg]) break;  // a head rotation: run by the product start
         const bool reg = pa < R;
         const char* kind = op == OP_RX ? "rx" : op == OP_RY ? "ry" : "rz";
         if (batched && slot >= 0) {  // the slot's position is taken by another slot
@@ -808,7 +833,8 @@ void emit_constants(std::ostringstream& o, const Plan& p, int map_off) {
 void emit_sched_struct(std::ostringstream& o, const std::string& name, const Plan& p,
                        const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S,
                        const GradMode& gm, const TanMode& tm, const Frame* tables, int map_off,
-                       bool load = false, int fixed_flags = -1) {
+                       bool load = false, int fixed_flags = -1,
+                       const std::vector<char>* skip = nullptr) {
   o << "struct " << name << " {\n";
   emit_constants(o, p, map_off);
   o << "static constexpr int kFixedFlags = " << fixed_flags << ";\n";
@@ -822,7 +848,7 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
     o << "  const uint32_t ln = (uint32_t)w.stid & " << gm.tm - 1 << "u;\n"
       << "  float ga[" << gm.nr << "];\n"
       << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) ga[j] = 0.f;\n";
-  emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm, tm);
+  emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm, tm, skip);
   if (regs)  // every (slot, group) accumulator is written by exactly one lane
     o << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) {\n"
       << "    const uint32_t slot = j * " << gm.tm << "u + ln;\n"
@@ -830,7 +856,7 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
   o << "}\n"
     << "__device__ __forceinline__ static float lane_sum(float v, const Walk&) {\n"
     << "  return group_sum<" << gm.tm << ">(v);\n}\n";
-  if (tables) emit_tables(o, p, tm, *tables, S << (k - R), false, load);
+  if (tables) emit_tables(o, p, tm, *tables, S << (k - R), false, load, skip);
   o << "};\n";
 }
 
@@ -872,6 +898,197 @@ std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
   return o.str();
 }
 
+// The product head of the training step (vqc_device.h, "product head"): the
+// occurrences of the head rotations (per occurrence, 1 for a head rotation),
+// or an empty vector when the step runs every rotation.  Needs the tangent
+// form's one sample per workgroup, one lane per qubit and 16-bit occurrence
+// and slot numbers.
+std::vector<char> head_occurrences(const Plan& p, const TanMode& tm) {
+  std::vector<char> h;
+  if (!tm.on || p.S != 1 || p.n > 64 || p.head.empty()) return h;
+  const size_t nocc = p.occ_src.size();
+  bool any = false;
+  for (const auto& hq : p.head)
+    for (const Prim& g : hq) {
+      if (g.occ >= 65536 || p.occ_slot[g.occ] >= 65535) return {};
+      any = true;
+    }
+  if (!any) return h;
+  h.assign(nocc, 0);
+  for (const auto& hq : p.head)
+    for (const Prim& g : hq) h[g.occ] = 1;
+  return h;
+}
+
+// struct Head of the training step: the head tables and mappings.
+void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
+  int L = 0;
+  for (const auto& hq : p.head) L = std::max(L, (int)hq.size());
+  const int n = p.n, k = p.k, R = p.R;
+  o << "struct Head {\n"
+    << "static constexpr bool kOn = true;\n"
+    << "static constexpr int kN = " << n << ", kK = " << k << ", kL = " << L << ";\n"
+    << "static constexpr uint32_t kOff = " << off << "u;\n";
+  std::vector<uint32_t> words, slots;
+  std::vector<float> muls;
+  bool scaled = false;
+  for (int q = 0; q < n; ++q)
+    for (int i = 0; i < L; ++i) {
+      if (i < (int)p.head[q].size()) {
+        const Prim& g = p.head[q][i];
+        const uint32_t kind = g.kind == P_RX ? 0u : g.kind == P_RY ? 1u : 2u;
+        words.push_back((uint32_t)g.occ | kind << 16);
+        slots.push_back((uint32_t)(p.occ_slot[g.occ] + 1));
+        const float m = p.affine ? p.occ_ma[2 * g.occ] : 1.f;
+        muls.push_back(m);
+        scaled = scaled || m != 1.f;
+      } else {
+        words.push_back(3u << 16);
+        slots.push_back(0u);
+        muls.push_back(1.f);
+      }
+    }
+  o << "using Pre = HeadPre<kL>;\n"
+    << "__device__ __forceinline__ static Pre preload(int tid) {\n";
+  emit_array(o, "uint32_t", "kW", words);
+  emit_array(o, "uint32_t", "kS", slots);
+  if (scaled) {
+    o << "  static constexpr float kM[] = {";
+    for (size_t i = 0; i < muls.size(); ++i)
+      o << (i ? "," : "") << std::hexfloat << (double)muls[i] << "f" << std::defaultfloat;
+    o << "};\n";
+  }
+  o << "  const int q = min(tid & 63, " << n - 1 << ");\n"
+    << "  Pre h;\n"
+    << "#pragma unroll\n"
+    << "  for (int i = 0; i < kL; ++i) {\n"
+    << "    h.w[i] = kW[q * kL + i];\n"
+    << "    h.s[i] = (int32_t)kS[q * kL + i];\n"
+    << "    h.m[i] = " << (scaled ? "kM[q * kL + i]" : "1.f") << ";\n"
+    << "  }\n"
+    << "  return h;\n}\n";
+  // qubit -> register / thread bit under the two mappings
+  auto bits = [&](int map_off, std::vector<int>& reg, std::vector<int>& thr) {
+    reg.assign(R, 0);
+    thr.assign(k - R, 0);
+    for (int q = 0; q < k; ++q) {
+      const int ph = p.maps[map_off + q];
+      if (ph < R) reg[ph] = q;
+      else thr[ph - R] = q;
+    }
+  };
+  std::vector<int> sreg, sthr, ereg, ethr;
+  bits(p.start_off, sreg, sthr);
+  bits(p.bwd_end_off, ereg, ethr);
+  const int t = k - R;
+  const std::string q_a = "a", q_b = "b";
+  auto pad_states = [&]() {
+    for (int q = n; q < k; ++q)
+      o << "  const float2 a" << q << " = make_float2(1.f, 0.f), b" << q
+        << " = make_float2(0.f, 0.f);\n";
+  };
+  // init(): every head walked by its qubit's lane, then the product state in
+  // the forward's start mapping
+  o << "template <int R>\n"
+    << "__device__ __forceinline__ static void init(St<R>& a, const Walk& w, const Pre& hp) {\n"
+    << "  static_assert(R == " << R << ", \"register width\");\n"
+    << "  HeadRec* rec = reinterpret_cast<HeadRec*>(w.smem + kOff);\n"
+    << "  float4* fin = reinterpret_cast<float4*>(w.smem + kOff + " << n * L * 32 << "u);\n"
+    << "  float2 fa, fb;\n"
+    << "  head_walk<kL>(w, hp, rec, fin, kN, fa, fb);\n";
+  for (int q = 0; q < n; ++q)
+    o << "  const float2 a" << q << " = make_float2(lane_value(fa.x, " << q << "), lane_value(fa.y, "
+      << q << ")), b" << q << " = make_float2(lane_value(fb.x, " << q << "), lane_value(fb.y, " << q
+      << "));\n";
+  pad_states();
+  o << "  const uint32_t tb = w.tb;\n"
+    << "  float2 t = make_float2(1.f, 0.f);\n";
+  for (int j = 0; j < t; ++j)
+    o << "  t = cmul(t, ((tb >> " << j << ") & 1u) ? b" << sthr[j] << " : a" << sthr[j] << ");\n";
+  o << "  const float2 A0_0 = t;\n";
+  for (int pb = 0; pb < R; ++pb)
+    for (int u = 0; u < (2 << pb); ++u) {
+      const int src = u & ~(1 << pb);
+      o << "  const float2 A" << pb + 1 << "_" << u << " = cmul(A" << pb << "_" << src << ", "
+        << (((u >> pb) & 1) ? "b" : "a") << sreg[pb] << ");\n";
+    }
+  for (int u = 0; u < (1 << R); ++u)
+    o << "  a.r[" << u << "] = A" << R << "_" << u << ".x; a.i[" << u << "] = A" << R << "_" << u
+      << ".y;\n";
+  o << "}\n";
+  // grads(): the 2-vector partials of every qubit from lambda in the adjoint's
+  // end mapping, then the sums and the walks back (head_finish)
+  const int NV = (4 * n + 15) / 16 * 16;
+  o << "template <int WG, int R>\n"
+    << "__device__ __forceinline__ static void grads(const St<R>& l, const Walk& w) {\n"
+    << "  const HeadRec* rec = reinterpret_cast<const HeadRec*>(w.smem + kOff);\n"
+    << "  const float4* fin = reinterpret_cast<const float4*>(w.smem + kOff + " << n * L * 32
+    << "u);\n";
+  for (int q = 0; q < n; ++q)
+    o << "  const float4 F" << q << " = fin[" << q << "];\n"
+      << "  const float2 a" << q << " = make_float2(F" << q << ".x, F" << q << ".y), b" << q
+      << " = make_float2(F" << q << ".z, F" << q << ".w);\n";
+  pad_states();
+  o << "  const uint32_t tb = w.tb;\n";
+  // the thread bits' factors, and their products leaving one out
+  for (int j = 0; j < t; ++j)
+    o << "  const float2 f" << j << " = ((tb >> " << j << ") & 1u) ? b" << ethr[j] << " : a"
+      << ethr[j] << ";\n";
+  o << "  const float2 P0 = make_float2(1.f, 0.f);\n";
+  for (int j = 0; j < t; ++j)
+    o << "  const float2 P" << j + 1 << " = cmul(P" << j << ", f" << j << ");\n";
+  if (t > 0) o << "  const float2 S" << t - 1 << " = make_float2(1.f, 0.f);\n";
+  for (int j = t - 2; j >= 0; --j)
+    o << "  const float2 S" << j << " = cmul(S" << j + 1 << ", f" << j + 1 << ");\n";
+  for (int j = 0; j < t; ++j)
+    o << "  const float2 T" << j << " = cmul(P" << j << ", S" << j << ");\n";
+  o << "  const float2 tall = P" << t << ";\n";
+  for (int u = 0; u < (1 << R); ++u)
+    o << "  const float2 x" << u << " = make_float2(l.r[" << u << "], l.i[" << u << "]);\n";
+  // for each register bit: lambda contracted over the other register bits
+  for (int pb = 0; pb < R; ++pb) {
+    std::vector<std::string> name(1 << R);
+    for (int u = 0; u < (1 << R); ++u) name[u] = "x" + std::to_string(u);
+    int done = 0;
+    for (int c = R - 1; c >= 0; --c) {
+      if (c == pb) continue;
+      for (int u = 0; u < (1 << R); ++u) {
+        if (((u >> c) & 1) || (u & done)) continue;
+        const std::string nm = "y" + std::to_string(pb) + "_" + std::to_string(c) + "_" +
+                               std::to_string(u);
+        o << "  const float2 " << nm << " = cadd(cmulc(a" << ereg[c] << ", " << name[u]
+          << "), cmulc(b" << ereg[c] << ", " << name[u | (1 << c)] << "));\n";
+        name[u] = nm;
+      }
+      done |= 1 << c;
+    }
+    o << "  const float2 C" << pb << "_0 = " << name[0] << ", C" << pb << "_1 = " << name[1 << pb]
+      << ";\n";
+  }
+  o << "  const float2 sall = cadd(cmulc(a" << ereg[0] << ", C0_0), cmulc(b" << ereg[0]
+    << ", C0_1));\n"
+    << "  float v[" << NV << "];\n"
+    << "#pragma unroll\n  for (int j = 0; j < " << NV << "; ++j) v[j] = 0.f;\n";
+  for (int pb = 0; pb < R; ++pb) {
+    const int q = ereg[pb];
+    if (q >= n) continue;
+    o << "  { const float2 u0 = cmulc(tall, C" << pb << "_0), u1 = cmulc(tall, C" << pb << "_1);\n"
+      << "    v[" << 4 * q << "] = u0.x; v[" << 4 * q + 1 << "] = u0.y; v[" << 4 * q + 2
+      << "] = u1.x; v[" << 4 * q + 3 << "] = u1.y; }\n";
+  }
+  for (int j = 0; j < t; ++j) {
+    const int q = ethr[j];
+    if (q >= n) continue;
+    o << "  { const float2 c = cmulc(T" << j << ", sall); const bool one = (tb >> " << j
+      << ") & 1u;\n"
+      << "    v[" << 4 * q << "] = one ? 0.f : c.x; v[" << 4 * q + 1 << "] = one ? 0.f : c.y; v["
+      << 4 * q + 2 << "] = one ? c.x : 0.f; v[" << 4 * q + 3 << "] = one ? c.y : 0.f; }\n";
+  }
+  o << "  head_finish<WG, kL, " << NV << ">(v, w, rec, kN);\n"
+    << "}\n"
+    << "};\n";
+}
+
 // The training step: forward and adjoint sweeps in one kernel.
 std::string step_unit(const Plan& p, const Frame& fr) {
   std::ostringstream o;
@@ -881,16 +1098,37 @@ std::string step_unit(const Plan& p, const Frame& fr) {
   const int nf = (int)p.fwd.size() / 2, nb = (int)p.bwd.size() / 2;
   TanMode tm = tan_mode(p, p.fwd.data(), nf, p.bwd.data(), nb, p.S, true, p.lds_step);
   tm.on = tm.on && tangent_wanted(p.S, p.R);
+  std::vector<char> head = head_occurrences(p, tm);
+  size_t head_off = 0, end = tm.on ? tm.end : p.lds_step;
+  if (!head.empty()) {
+    int L = 0;
+    for (const auto& hq : p.head) L = std::max(L, (int)hq.size());
+    head_off = align16(end);
+    const size_t head_end = head_off + (size_t)p.n * L * 32 + (size_t)p.n * 16;
+    if (head_end <= (size_t)kLdsBytes) {
+      end = head_end;
+      // the sweeps' own rotations (the tables' signs and the block rescales)
+      auto drop = [&](std::vector<int>& v) {
+        v.erase(std::remove_if(v.begin(), v.end(), [&](int occ) { return head[occ] != 0; }),
+                v.end());
+      };
+      drop(tm.focc);
+      drop(tm.bocc);
+    } else {
+      head.clear();
+    }
+  }
+  const std::vector<char>* skip = head.empty() ? nullptr : &head;
   emit_sched_struct(o, "SchedF", p, p.fwd.data(), nf, false, p.R, p.k, p.S, gm, tm, &fr,
-                    p.end_off);
+                    p.end_off, false, -1, skip);
   emit_sched_struct(o, "SchedB", p, p.bwd.data(), nb, true, p.R, p.k, p.S, gm, tm, nullptr,
-                    p.end_off);
+                    p.end_off, false, -1, skip);
+  if (skip) emit_head(o, p, head_off);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << p.WG << ") vqc_rs(const vqc::TileArgs A) {\n"
-    << "  __shared__ __align__(16) unsigned char smem["
-    << lds_size(tm.on ? tm.end : p.lds_step) << "];\n"
-    << "  vqc::resident_step_body<" << p.WG << ", " << p.R
-    << ", vqc::SchedF, vqc::SchedB>(A, smem);\n}\n";
+    << "  __shared__ __align__(16) unsigned char smem[" << lds_size(end) << "];\n"
+    << "  vqc::resident_step_body<" << p.WG << ", " << p.R << ", vqc::SchedF, vqc::SchedB"
+    << (skip ? ", vqc::Head" : "") << ">(A, smem);\n}\n";
   return o.str();
 }
 

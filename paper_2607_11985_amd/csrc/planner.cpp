@@ -716,6 +716,20 @@ void fold_trailing_entanglers(Plan& plan) {
   }
 }
 
+// Each qubit's head (the rotations on it before the first entangler on it).
+void find_heads(Plan& plan) {
+  plan.head.assign(plan.n, {});
+  uint32_t blocked = 0;
+  for (const Prim& g : plan.prims) {
+    const uint32_t lines = lines_of(g);
+    const bool rot = g.kind == P_RX || g.kind == P_RY || g.kind == P_RZ;
+    if (rot && g.occ >= 0 && !(blocked & lines))
+      plan.head[g.q0].push_back(g);
+    else
+      blocked |= lines;
+  }
+}
+
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
                Plan& plan, std::string& msg, bool lane_gates, int tile_qubits,
                int bwd_reg_bits) {
@@ -781,6 +795,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     lower_gate(o, plan);
   }
   fold_trailing_entanglers(plan);
+  find_heads(plan);
   const int n_occ = (int)plan.occ_src.size();
   if (reg_bits != 0 && (reg_bits < 2 || reg_bits > 5)) {
     msg = "reg_bits must be 0 (default) or in [2, 5]";
@@ -860,6 +875,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     rc = plan_sweep(rev, nq, plan.k, plan.R, m, plan.bwd, plan.cols, plan.bwd_exchanges,
                     global_slot, msg, plan.lanes);
     if (rc < 0) return rc;
+    plan.bwd_end_off = append_map(m, plan.maps);
     // LDS: exchange buffer | angle table [occ][S] | gradient accumulators [slot][G]
     const size_t xbuf = (size_t)plan.WG * ((size_t)1 << plan.R) * 8;
     plan.lds_tab = xbuf;

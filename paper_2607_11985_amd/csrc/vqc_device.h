@@ -1518,7 +1518,192 @@ __device__ __forceinline__ void resident_body(const TileArgs& A, unsigned char* 
 // Training step in one launch: forward (FS), <Z>, the loss head's cotangent,
 // lambda = (sum_j g_j Z_j) psi and the adjoint sweep (BS).  The state stays on
 // chip between the two sweeps; nothing is saved to HBM.
-template <int WG, int R, typename FS, typename BS>
+// ------------------------------------------------------------ product head
+// A qubit's head is the run of rotations on it before any entangler touches
+// it.  Heads commute with every other gate up to their ends, so the state after
+// all of them is the product of one-qubit states phi_q = U_q |0> applied to
+// |0...0> (Sec. 3's initial state).  The generated training step builds that
+// product instead of running the head rotations, and its adjoint stops where
+// the heads end.  There, with psi the product state, the gradient of a head
+// rotation R_P of qubit q, Im <lambda|P|psi> at its place, equals
+// Im <mu|P|phi> in the qubit's own two dimensions: phi the qubit's state after
+// the rotation, mu = (I_q (x) <phi_{not q}|) lambda walked back through the
+// rotations of the head after it.  The 2-vectors v_q = (I_q (x) <phi_{not q}|)
+// lambda are sums over the whole state; one lane per qubit then walks its head.
+
+// Lane q's head (q < n), one entry per step i: word = occurrence | kind << 16
+// (kind 0 X, 1 Y, 2 Z, 3 no step), gradient slot + 1 (0: a constant angle),
+// chain-rule factor of the angle.
+template <int L>
+struct HeadPre {
+  uint32_t w[L];
+  int32_t s[L];
+  float m[L];
+};
+
+// No head (the default of the step kernel).
+struct NoHead {
+  static constexpr bool kOn = false;
+  struct Pre {};
+  __device__ __forceinline__ static Pre preload(int) { return Pre(); }
+};
+
+// One head step in LDS: the qubit's state after it, and its record.
+struct HeadRec {
+  float4 phi;  // (a.re, a.im, b.re, b.im) of a|0> + b|1>
+  uint32_t word;
+  int32_t slot1;
+  float mul;
+  float pad;
+};
+
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, -a.y * b.y), fmaf(a.x, b.y, a.y * b.x));
+}
+// conj(a) * b
+__device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, a.y * b.y), fmaf(a.x, b.y, -a.y * b.x));
+}
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) {
+  return make_float2(a.x + b.x, a.y + b.y);
+}
+
+// P (a|0> + b|1>) for P = X (kind 0), Y (1), Z (2)
+__device__ __forceinline__ void pauli2(uint32_t kind, float2 a, float2 b, float2& pa, float2& pb) {
+  pa = kind == 0u ? b : kind == 1u ? make_float2(b.y, -b.x) : a;
+  pb = kind == 0u ? a : kind == 1u ? make_float2(-a.y, a.x) : make_float2(-b.x, -b.y);
+}
+
+__device__ __forceinline__ float lane_value(float v, int q) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), q));
+}
+
+// Reduce-scatter of 16 values over the wave's 64 lanes: lane L returns the sum
+// of value L % 16 over all lanes.  Value-index bit b pairs with lane bit b: bit
+// 2 first (row_half_mirror pairs lane l with l ^ 7 while every lane still holds
+// all 16 values), then bits 0 and 1 (quad_perm 1032, 2301) and 3 (row_ror 8);
+// two more additions (lane ^ 16 by a swizzle, lane ^ 32) complete the sums.
+// The pairing order is fixed, so the sums are deterministic.  Written with
+// named values: selects between elements of one array would become a
+// run-time index into it.
+#define VQC_RS_PAIR(CTRL, HB, K, A, B) \
+  do {                                 \
+    const float k_ = (HB) ? (B) : (A); \
+    const float s_ = (HB) ? (A) : (B); \
+    K = k_ + dpp_f<CTRL>(s_);          \
+  } while (0)
+__device__ __forceinline__ float wave_reduce16(const float (&v)[16], uint32_t lane) {
+  float x0 = v[0], x1 = v[1], x2 = v[2], x3 = v[3], x4 = v[4], x5 = v[5], x6 = v[6], x7 = v[7];
+  float x8 = v[8], x9 = v[9], x10 = v[10], x11 = v[11], x12 = v[12], x13 = v[13], x14 = v[14],
+        x15 = v[15];
+  const bool h2 = (lane >> 2) & 1u, h0 = lane & 1u, h1 = (lane >> 1) & 1u, h3 = (lane >> 3) & 1u;
+  float y0, y1, y2, y3, y4, y5, y6, y7;  // value bit 2 gone: y[q] holds values with bits 0, 1, 3 of q
+  VQC_RS_PAIR(0x141, h2, y0, x0, x4);
+  VQC_RS_PAIR(0x141, h2, y1, x1, x5);
+  VQC_RS_PAIR(0x141, h2, y2, x2, x6);
+  VQC_RS_PAIR(0x141, h2, y3, x3, x7);
+  VQC_RS_PAIR(0x141, h2, y4, x8, x12);
+  VQC_RS_PAIR(0x141, h2, y5, x9, x13);
+  VQC_RS_PAIR(0x141, h2, y6, x10, x14);
+  VQC_RS_PAIR(0x141, h2, y7, x11, x15);
+  float z0, z1, z2, z3;  // value bit 0 gone
+  VQC_RS_PAIR(0xB1, h0, z0, y0, y1);
+  VQC_RS_PAIR(0xB1, h0, z1, y2, y3);
+  VQC_RS_PAIR(0xB1, h0, z2, y4, y5);
+  VQC_RS_PAIR(0xB1, h0, z3, y6, y7);
+  float w0, w1;  // value bit 1 gone
+  VQC_RS_PAIR(0x4E, h1, w0, z0, z1);
+  VQC_RS_PAIR(0x4E, h1, w1, z2, z3);
+  float tot;  // value bit 3 gone
+  VQC_RS_PAIR(0x128, h3, tot, w0, w1);
+  tot += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(tot), 0x401F));
+  tot += __shfl_xor(tot, 32, 64);
+  return tot;
+}
+#undef VQC_RS_PAIR
+
+// Lane q's walk through the head of qubit q (lanes of every wave do it; wave
+// 0 records each step's state in LDS): fa, fb end as the qubit's state.
+template <int L>
+__device__ __forceinline__ void head_walk(const Walk& w, const HeadPre<L>& hp, HeadRec* rec,
+                                          float4* fin, int n, float2& fa, float2& fb) {
+  const int lane = (int)__lane_id();
+  const bool writer = lane < n && threadIdx.x < 64;
+  fa = make_float2(1.f, 0.f);
+  fb = make_float2(0.f, 0.f);
+#pragma unroll
+  for (int i = 0; i < L; ++i) {
+    const uint32_t word = hp.w[i], kind = word >> 16;
+    float2 cs = w.tab[word & 0xFFFFu];  // (cos, sin)(theta / 2), exact for head steps
+    if (kind == 3u) cs = make_float2(1.f, 0.f);
+    float2 pa, pb;
+    pauli2(kind, fa, fb, pa, pb);
+    // (c I - i s P) phi
+    fa = make_float2(fmaf(cs.x, fa.x, cs.y * pa.y), fmaf(cs.x, fa.y, -cs.y * pa.x));
+    fb = make_float2(fmaf(cs.x, fb.x, cs.y * pb.y), fmaf(cs.x, fb.y, -cs.y * pb.x));
+    if (writer) {
+      HeadRec r;
+      r.phi = make_float4(fa.x, fa.y, fb.x, fb.y);
+      r.word = word;
+      r.slot1 = hp.s[i];
+      r.mul = hp.m[i];
+      r.pad = 0.f;
+      rec[lane * L + i] = r;
+    }
+  }
+  if (writer) fin[lane] = make_float4(fa.x, fa.y, fb.x, fb.y);
+}
+
+// The head gradients from the per-thread 2-vector partials v[4 q .. 4 q + 3]
+// (v_q(0), v_q(1) as re, im): sums over the workgroup (each wave, then the
+// waves through the exchange buffer), then lane q of wave 0 walks qubit q's
+// head back and adds each rotation's gradient to accumulator group 0.  Every
+// thread calls it, after a barrier.
+template <int WG, int L, int NV>
+__device__ __forceinline__ void head_finish(const float (&v)[NV], const Walk& w,
+                                            const HeadRec* rec, int n) {
+  const uint32_t lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  float* red = w.xbuf;
+#pragma unroll
+  for (int c = 0; c < NV / 16; ++c) {
+    float x16[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) x16[j] = v[16 * c + j];
+    const float tot = wave_reduce16(x16, lane);
+    if (lane < 16u) red[wave * NV + 16 * c + (int)lane] = tot;
+  }
+  __syncthreads();
+  const int q = threadIdx.x;
+  if (q >= n) return;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int g = 0; g < WG / 64; ++g) {
+    s.x += red[g * NV + 4 * q];
+    s.y += red[g * NV + 4 * q + 1];
+    s.z += red[g * NV + 4 * q + 2];
+    s.w += red[g * NV + 4 * q + 3];
+  }
+  float2 m0 = make_float2(s.x, s.y), m1 = make_float2(s.z, s.w);
+#pragma unroll
+  for (int i = L - 1; i >= 0; --i) {
+    const HeadRec r = rec[q * L + i];
+    const uint32_t kind = r.word >> 16;
+    if (kind == 3u) continue;
+    const float2 cs = w.tab[r.word & 0xFFFFu];
+    float2 p0, p1;
+    pauli2(kind, make_float2(r.phi.x, r.phi.y), make_float2(r.phi.z, r.phi.w), p0, p1);
+    // Im(conj(mu_0) (P phi)_0 + conj(mu_1) (P phi)_1)
+    const float g = fmaf(m0.x, p0.y, -m0.y * p0.x) + fmaf(m1.x, p1.y, -m1.y * p1.x);
+    if (r.slot1 > 0) atomicAdd(&w.acc[(r.slot1 - 1) * w.G], g * r.mul);
+    // mu <- (c I + i s P) mu, the rotation undone
+    float2 q0, q1;
+    pauli2(kind, m0, m1, q0, q1);
+    m0 = make_float2(fmaf(cs.x, m0.x, -cs.y * q0.y), fmaf(cs.x, m0.y, cs.y * q0.x));
+    m1 = make_float2(fmaf(cs.x, m1.x, -cs.y * q1.y), fmaf(cs.x, m1.y, cs.y * q1.x));
+  }
+}
+
+template <int WG, int R, typename FS, typename BS, typename HD = NoHead>
 __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned char* smem) {
   const int tid = threadIdx.x;
   const Walk w = resident_walk<WG, R>(A, smem);
@@ -1538,6 +1723,7 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
                              : reinterpret_cast<const float*>(A.occ_src);
   const float y0 = *yp;
   const typename FS::Pre pre = FS::preload(tid);
+  const typename HD::Pre hpre = HD::preload(tid);
   angle_table<FS>(reinterpret_cast<float2*>(smem + A.lds_tab), A.n_occ, A.S, b0, A.B,
                   A.occ_src, A.occ_idx, A.occ_cs, A.occ_ma, A.params, A.pstride, A.inputs, A.F,
                   tid, WG);
@@ -1549,7 +1735,10 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
   FS::prepare(w, tid, WG, pre);  // the tables of both sweeps
 
   St<R> a, l;
-  zero_state<R>(a, w.stid);
+  if constexpr (HD::kOn)
+    HD::template init<R>(a, w, hpre);
+  else
+    zero_state<R>(a, w.stid);
   FS::template run<R, false, (WG > 64)>(a, l, w, A.ins, A.n_ins);
   z_partials<R, FS>(a, w.xbuf, A.n, A.end_phys, A.zmask, w);
   resident_expvals(A, w.xbuf, e, WG);
@@ -1568,6 +1757,10 @@ __device__ __forceinline__ void resident_step_body(const TileArgs& A, unsigned c
                      FS::esigns(w));
   BS::template run<R, true, (WG > 64)>(a, l, w, A.ins_b, A.n_ins_b);
   __syncthreads();
+  if constexpr (HD::kOn) {
+    HD::template grads<WG, R>(l, w);
+    __syncthreads();
+  }
   resident_grads(A, w.acc, WG);
 }
 

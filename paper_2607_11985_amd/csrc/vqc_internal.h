@@ -55,6 +55,11 @@ struct Plan {
   // GF(2) map with columns pcol[q].  Both empty when there are none.
   std::vector<Prim> tail;
   std::vector<uint32_t> zmask, pcol;
+  // Each qubit's head: the rotations on it before any entangler touches it, in
+  // circuit order.  The state after every head is a product state, which the
+  // generated training step builds directly (and whose gradients it takes from
+  // lambda contracted against the other qubits' states).
+  std::vector<std::vector<Prim>> head;
   std::vector<int32_t> occ_src, occ_idx, occ_slot;
   std::vector<float> occ_cs;              // 2 per occurrence
   std::vector<float> occ_ma;              // 2 per occurrence: angle = mul * value + add
@@ -65,6 +70,7 @@ struct Plan {
   std::vector<int32_t> pslots;            // pass-local -> global gradient slots
   std::vector<PassPlan> fpass, bpass;     // streaming passes
   int start_off = 0, end_off = 0;         // resident: forward start / end mapping in `maps`
+  int bwd_end_off = 0;                    // resident: the adjoint's end mapping in `maps`
   int fwd_exchanges = 0, bwd_exchanges = 0;
   int max_pass_slots = 0;
   size_t lds_fwd = 0, lds_bwd = 0, lds_tab = 0, lds_acc = 0;

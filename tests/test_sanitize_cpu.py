@@ -41,7 +41,10 @@ def _env(extra):
 @pytest.fixture(scope="module")
 def harness():
     from paper_2607_11985_amd.build import BUILD, write_embedded_headers
-    os.makedirs(OUT, exist_ok=True)
+    # a directory per process: parallel test workers must not overwrite an
+    # executable another one runs
+    out = os.path.join(OUT, str(os.getpid()))
+    os.makedirs(out, exist_ok=True)
     os.makedirs(BUILD, exist_ok=True)
     srcs = [os.path.join(ROOT, "tests", "sanitize", "host_harness.cpp"),
             write_embedded_headers()] + \
@@ -51,13 +54,13 @@ def harness():
              "-I", os.path.join(ROOT, "include"), "-I", CSRC] + SAN
 
     def obj(src):
-        o = os.path.join(OUT, os.path.basename(src) + ".o")
+        o = os.path.join(out, os.path.basename(src) + ".o")
         _run(flags + ["-c", src, "-o", o])
         return o
 
     with ThreadPoolExecutor(max_workers=min(6, os.cpu_count() or 1)) as ex:
         objs = list(ex.map(obj, srcs))
-    exe = os.path.join(OUT, "host_harness")
+    exe = os.path.join(out, "host_harness")
     _run(["g++"] + SAN + objs + ["-L", os.path.join(ROCM, "lib"),
                                  "-Wl,-rpath," + os.path.join(ROCM, "lib"), "-lamdhip64",
                                  "-lhiprtc", "-o", exe])
@@ -96,8 +99,9 @@ print("oracle ok")
 
 
 def test_oracle_under_sanitizers():
-    os.makedirs(OUT, exist_ok=True)
-    lib = os.path.join(OUT, "liboracle_san.so")
+    out = os.path.join(OUT, str(os.getpid()))
+    os.makedirs(out, exist_ok=True)
+    lib = os.path.join(out, "liboracle_san.so")
     _run(["gcc", "-std=c99", "-fopenmp", "-fPIC", "-shared"] + SAN +
          ["-o", lib, os.path.join(ROOT, "oracle", "vqc_oracle.c"), "-lm"])
     asan = subprocess.run(["gcc", "-print-file-name=libasan.so"], capture_output=True,
