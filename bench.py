@@ -394,9 +394,11 @@ def measure(idx, args, torch, dev, want_cpu, cpu_budget):
     resident = info["path"] == 1
     if args.engine == "jit":
         kname = "vqc_rs (one launch)" if resident else \
-            "vqc_st, vqc_sf*, reduce_e, loss_grad, fill_zero, vqc_sb*, reduce_grad (one step)"
+            ("vqc_st, vqc_sf*, reduce_e, loss_grad, fill_zero, vqc_sb*, reduce_grad (one step: "
+             "each batch half on its own stream)")
     else:
-        kname = "resident_step_kernel" if resident else "stream_kernel passes (one step)"
+        kname = "resident_step_kernel" if resident else \
+            "stream_kernel passes (one step: each batch half on its own stream)"
     if args.separate:
         kname = "vqc_forward + vqc_loss_grad + vqc_backward (one step)"
     if hbm_frac >= alu_frac:

@@ -889,11 +889,13 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     plan.lds_e = align_up(plan.lds_bwd, 16);
     plan.lds_step = plan.lds_e + (2 * (size_t)plan.S * n + plan.S) * 4;  // E, g, targets
   } else {
-    // 13-qubit tiles by default for the generated kernels: two workgroups per
-    // CU overlap one's HBM traffic with the other's compute.  Measured: the
-    // 16-qubit workload 63 k -> 77-81 k evals/s despite 24 passes instead of
-    // 21; the 14-qubit one 512 k -> 534 k although its state no longer fits
-    // one tile.
+    // Tiles of the generated kernels: 13 qubits unless tile_qubits says
+    // otherwise (vqc_compile also plans 12 and keeps that plan when it takes at
+    // most a quarter more passes).  Below 14 qubits several workgroups share a
+    // CU and one's HBM traffic overlaps another's compute.  Measured: the
+    // 16-qubit workload 63 k -> 77-81 k evals/s at 13 qubits despite more
+    // passes; the 14-qubit one 512 k -> 534 k although its state no longer
+    // fits one tile.
     plan.k = tile_qubits ? tile_qubits : lane_gates ? kMaxTileQubits - 1 : kMaxTileQubits;
     plan.ng = nq - plan.k;
     plan.Rf = reg_bits ? reg_bits : kStreamRegBitsFwd;
