@@ -230,6 +230,17 @@ void vqc_destroy(vqc_circuit *c);
  *   training = 2: vqc_train_step;
  *   training = 3: vqc_fd_backward.
  * 0 means no workspace is needed.  Returns (size_t)-1 on invalid arguments.
+ *
+ * Streams.  On the streaming path (batch >= 2) vqc_forward, vqc_forward_ex,
+ * vqc_backward and vqc_train_step run the first ceil(batch / 2) samples on
+ * `stream` and the rest on a side stream that the library creates on the
+ * device at first use (default priority) and keeps until exit: the side
+ * stream waits for the work queued on `stream` before the call, and `stream`
+ * waits for the side stream at its end, so each call is ordered on `stream`
+ * like a single launch.  Calls that overlap on one device share the side
+ * stream (they stay correct but queue behind each other there); under stream
+ * capture the side stream joins the capture.  The two halves have workspace
+ * layouts of their own, which vqc_workspace_bytes accounts for.
  */
 size_t vqc_workspace_bytes(const vqc_circuit *c, int64_t batch, int32_t training);
 
@@ -316,15 +327,8 @@ int vqc_loss_grad(int32_t kind, int64_t batch, int32_t n_qubits, const float *ex
  *   [batch, F] written (either may be NULL); workspace:
  *   vqc_workspace_bytes(c, batch, 2) bytes, 256-byte aligned (on the resident
  *   path 0 bytes / NULL unless shared_params).
- * On the streaming path (batch >= 2) the call runs the first ceil(batch / 2)
- * samples on `stream` and the rest on a side stream that the library creates
- * on the device at first use (default priority) and keeps until exit: the
- * side stream waits for the work queued on `stream` before the call, and
- * `stream` waits for the side stream at its end, so the call is ordered on
- * `stream` like a single launch.  Calls that overlap on one device share the
- * side stream (they stay correct but queue behind each other there); under
- * stream capture the side stream joins the capture.
- * Results equal those of the three separate calls.  Errors: those of the
+ * On the streaming path the batch halves run on two streams (see
+ * vqc_workspace_bytes).  Results equal those of the three separate calls.  Errors: those of the
  * three calls.
  */
 int vqc_train_step(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,

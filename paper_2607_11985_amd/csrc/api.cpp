@@ -104,26 +104,33 @@ StreamLayout stream_layout(const Plan& p, int64_t batch) {
   return L;
 }
 
-// The streaming training step runs its batch as two halves, one on the
-// caller's stream and one on a side stream, so that one half's passes fill
-// the CUs the other's leave idle (the tail of each pass; the HBM-bound forward
-// of one half beside the VALU-bound adjoint of the other).  Each half has a
-// layout of its own: [half 0 | half 1].
-bool split_step(const Plan& p, int64_t batch) { return p.path == VQC_PATH_STREAM && batch >= 2; }
+// The end of the streaming layout of `batch` samples for `mode` (0 inference
+// forward, 1 training forward (+ backward), 2 training step).
+size_t stream_end(const Plan& p, int64_t batch, int mode) {
+  const StreamLayout L = stream_layout(p, batch);
+  return mode == 0 ? L.end_inference : mode == 1 ? L.end_training : L.end_step;
+}
+
+// The streaming calls run their batch as two halves, one on the caller's
+// stream and one on a side stream, so that one half's passes fill the CUs the
+// other's leave idle (the tail of each pass; in the training step also the
+// HBM-bound forward of one half beside the VALU-bound adjoint of the other).
+// Each half has a layout of its own: [half 0 | half 1].
+bool split_batch(const Plan& p, int64_t batch) {
+  return p.path == VQC_PATH_STREAM && batch >= 2;
+}
 int64_t first_half(int64_t batch) { return (batch + 1) / 2; }
-size_t second_half_offset(const Plan& p, int64_t batch) {
-  return align_up(stream_layout(p, first_half(batch)).end_step, 256);
+size_t second_half_offset(const Plan& p, int64_t batch, int mode) {
+  return align_up(stream_end(p, first_half(batch), mode), 256);
 }
 
 // mode: 0 inference forward, 1 training forward (+ backward), 2 training step
 size_t required_bytes_core(const Plan& p, int64_t batch, int mode) {
   if (batch == 0) return 0;
   if (p.path == VQC_PATH_STREAM) {
-    if (mode == 2 && split_step(p, batch))
-      return second_half_offset(p, batch) +
-             stream_layout(p, batch - first_half(batch)).end_step;
-    const StreamLayout L = stream_layout(p, batch);
-    return mode == 0 ? L.end_inference : mode == 1 ? L.end_training : L.end_step;
+    if (split_batch(p, batch))
+      return second_half_offset(p, batch, mode) + stream_end(p, batch - first_half(batch), mode);
+    return stream_end(p, batch, mode);
   }
   return mode == 1 ? resident_state_bytes(p, batch) : 0;
 }
@@ -151,7 +158,7 @@ int fd_chunk(const Plan& p, int64_t batch) {
 
 size_t fd_states_bytes(const Plan& p, int64_t batch) {
   if (p.path == VQC_PATH_RESIDENT) return 0;
-  return required_bytes_core(p, batch * 2 * fd_chunk(p, batch), 0);
+  return stream_end(p, batch * 2 * fd_chunk(p, batch), 0);
 }
 
 size_t fd_rows_bytes(const Plan& p, int64_t batch) {
@@ -283,6 +290,67 @@ void set_tables(vqc::PassArgs& a, unsigned char* ws, const StreamLayout& L) {
   a.tabs = reinterpret_cast<float*>(ws + L.tabs);
   a.gsig = reinterpret_cast<float*>(ws + L.gsig);
   a.esig = reinterpret_cast<float*>(ws + L.esig);
+}
+
+// The library's side stream on `device` (the caller makes it current),
+// created on first use with the default priority and kept until exit.
+int side_stream(int device, hipStream_t* out) {
+  static std::mutex mu;
+  static hipStream_t streams[vqc::kScratchDevices] = {};
+  *out = nullptr;
+  if (device < 0 || device >= vqc::kScratchDevices) return (int)hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!streams[device]) {
+    hipStream_t s = nullptr;
+    const hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    if (e != hipSuccess) return (int)e;
+    streams[device] = s;
+  }
+  *out = streams[device];
+  return 0;
+}
+
+template <typename T>
+T* rows_at(T* base, int64_t row, int64_t width) {
+  return base ? base + row * width : nullptr;
+}
+
+// Runs f(first row, rows, half's workspace offset index, stream) for the two
+// halves of a streaming call: the first on `stream`, the second on the side
+// stream, which waits for the work queued on `stream` before the call;
+// `stream` then waits for the second half, so work queued on it later sees
+// the whole call.
+template <typename F>
+int on_two_streams(const vqc_circuit* c, int64_t batch, void* stream, F&& f) {
+  const int64_t b0 = first_half(batch), b1 = batch - b0;
+  hipStream_t side = nullptr;
+  int rc = side_stream(c->device, &side);
+  if (rc) return hip_fail("side stream creation", rc);
+  hipEvent_t fork = nullptr, join = nullptr;
+  if ((rc = hipEventCreateWithFlags(&fork, hipEventDisableTiming)))
+    return hip_fail("event creation", rc);
+  if ((rc = hipEventCreateWithFlags(&join, hipEventDisableTiming))) {
+    (void)hipEventDestroy(fork);
+    return hip_fail("event creation", rc);
+  }
+  struct Events {
+    hipEvent_t a, b;
+    ~Events() {
+      (void)hipEventDestroy(a);  // released once the device has passed them
+      (void)hipEventDestroy(b);
+    }
+  } events{fork, join};
+  if ((rc = hipEventRecord(fork, (hipStream_t)stream)) ||
+      (rc = hipStreamWaitEvent(side, fork, 0)))
+    return hip_fail("stream fork", rc);
+  rc = f((int64_t)0, b0, 0, stream);
+  if (rc) return rc;
+  const int rc1 = f(b0, b1, 1, (void*)side);
+  // join even after a failed launch, so that `stream` never runs ahead of
+  // what the side stream already holds
+  if ((rc = hipEventRecord(join, side)) || (rc = hipStreamWaitEvent((hipStream_t)stream, join, 0)))
+    return hip_fail("stream join", rc);
+  return rc1;
 }
 
 // Streaming forward: every pass (the first starts from |0...0> or reads psi0),
@@ -596,8 +664,17 @@ int vqc_forward_ex(const vqc_circuit* c, int64_t batch, const float* params, con
   if (p.path == VQC_PATH_STREAM) {
     // a workspace that holds the training layout keeps every pass's state
     const bool keep = workspace_bytes >= required_bytes_core(p, batch, 1);
-    return stream_forward(c, batch, params, inputs, expvals,
-                          static_cast<unsigned char*>(workspace), stream, keep, psi0, probs);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    if (!split_batch(p, batch))
+      return stream_forward(c, batch, params, inputs, expvals, ws, stream, keep, psi0, probs);
+    const int64_t P = c->shared ? 0 : p.P, N = (int64_t)1 << p.n;
+    const size_t off = second_half_offset(p, batch, keep ? 1 : 0);
+    return on_two_streams(c, batch, stream, [&](int64_t b0, int64_t nb, int h, void* st) {
+      const void* s0 = psi0 ? static_cast<const unsigned char*>(psi0) + b0 * N * 8 : nullptr;
+      return stream_forward(c, nb, rows_at(params, b0, P), rows_at(inputs, b0, p.F),
+                            rows_at(expvals, b0, p.n), ws + h * off, st, keep, s0,
+                            rows_at(probs, b0, N));
+    });
   }
   vqc::TileArgs a = tile_args(c, false, batch);
   a.params = params;
@@ -635,8 +712,19 @@ int vqc_backward(const vqc_circuit* c, int64_t batch, const float* params, const
                                                              shared_rows_offset(p, batch, 1))
                                   : nullptr;
   if (p.path == VQC_PATH_STREAM) {
-    rc = stream_backward(c, batch, params, inputs, grad_out,
-                         static_cast<unsigned char*>(workspace), rows ? rows : dp, dx, stream);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    float* dprows = rows ? rows : dp;
+    if (split_batch(p, batch)) {
+      const int64_t P = c->shared ? 0 : p.P;
+      const size_t off = second_half_offset(p, batch, 1);
+      rc = on_two_streams(c, batch, stream, [&](int64_t b0, int64_t nb, int h, void* st) {
+        return stream_backward(c, nb, rows_at(params, b0, P), rows_at(inputs, b0, p.F),
+                               rows_at(grad_out, b0, p.n), ws + h * off,
+                               rows_at(dprows, b0, p.P), rows_at(dx, b0, p.F), st);
+      });
+    } else {
+      rc = stream_backward(c, batch, params, inputs, grad_out, ws, dprows, dx, stream);
+    }
     if (rc || !rows) return rc;
     rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream);
     return rc ? hip_fail("parameter gradient sum", rc) : VQC_OK;
@@ -678,24 +766,6 @@ int check_step_args(const vqc_circuit* c, int64_t batch, const float* params,
   return VQC_OK;
 }
 
-// The library's side stream on `device` (the caller makes it current),
-// created on first use with the default priority and kept until exit.
-int side_stream(int device, hipStream_t* out) {
-  static std::mutex mu;
-  static hipStream_t streams[vqc::kScratchDevices] = {};
-  *out = nullptr;
-  if (device < 0 || device >= vqc::kScratchDevices) return (int)hipErrorInvalidDevice;
-  std::lock_guard<std::mutex> lock(mu);
-  if (!streams[device]) {
-    hipStream_t s = nullptr;
-    const hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
-    if (e != hipSuccess) return (int)e;
-    streams[device] = s;
-  }
-  *out = streams[device];
-  return 0;
-}
-
 // Streaming forward, loss cotangent and adjoint of `batch` rows of a batch of
 // `norm` samples (pointers at the rows' start, the workspace laid out for
 // `batch`).
@@ -709,56 +779,6 @@ int stream_step(const vqc_circuit* c, int64_t batch, int64_t norm, const float* 
   rc = vqc::launch_loss_grad(loss_kind, batch, norm, p.n, expvals, target, cot, stream);
   if (rc) return hip_fail("loss launch", rc);
   return stream_backward(c, batch, params, inputs, cot, ws, dp, dx, stream);
-}
-
-template <typename T>
-T* rows_at(T* base, int64_t row, int64_t width) {
-  return base ? base + row * width : nullptr;
-}
-
-// The two halves of a streaming step: the first on `stream`, the second on the
-// side stream, which waits for the work queued on `stream` before the call;
-// `stream` then waits for the second half, so work queued on it later sees
-// the whole step.
-int stream_step_split(const vqc_circuit* c, int64_t batch, const float* params,
-                      const float* inputs, int32_t loss_kind, const float* target,
-                      float* expvals, float* grad_out, float* dp, float* dx, unsigned char* ws,
-                      void* stream) {
-  const Plan& p = c->plan;
-  const int64_t b0 = first_half(batch), b1 = batch - b0;
-  hipStream_t side = nullptr;
-  int rc = side_stream(c->device, &side);
-  if (rc) return hip_fail("side stream creation", rc);
-  hipEvent_t fork = nullptr, join = nullptr;
-  if ((rc = hipEventCreateWithFlags(&fork, hipEventDisableTiming)))
-    return hip_fail("event creation", rc);
-  if ((rc = hipEventCreateWithFlags(&join, hipEventDisableTiming))) {
-    (void)hipEventDestroy(fork);
-    return hip_fail("event creation", rc);
-  }
-  struct Events {
-    hipEvent_t a, b;
-    ~Events() {
-      (void)hipEventDestroy(a);  // released once the device has passed them
-      (void)hipEventDestroy(b);
-    }
-  } events{fork, join};
-  if ((rc = hipEventRecord(fork, (hipStream_t)stream)) ||
-      (rc = hipStreamWaitEvent(side, fork, 0)))
-    return hip_fail("stream fork", rc);
-  rc = stream_step(c, b0, batch, params, inputs, loss_kind, target, expvals, grad_out, dp, dx, ws,
-                   stream);
-  if (rc) return rc;
-  const int64_t P = c->shared ? 0 : p.P;
-  const int rc1 = stream_step(c, b1, batch, rows_at(params, b0, P), rows_at(inputs, b0, p.F),
-                              loss_kind, rows_at(target, b0, 1), rows_at(expvals, b0, p.n),
-                              rows_at(grad_out, b0, p.n), rows_at(dp, b0, p.P),
-                              rows_at(dx, b0, p.F), ws + second_half_offset(p, batch), side);
-  // join even after a failed launch, so that `stream` never runs ahead of
-  // what the side stream already holds
-  if ((rc = hipEventRecord(join, side)) || (rc = hipStreamWaitEvent((hipStream_t)stream, join, 0)))
-    return hip_fail("stream join", rc);
-  return rc1;
 }
 
 // The training step on a checked, large enough workspace, with the handle's
@@ -777,11 +797,20 @@ int train_step_impl(const vqc_circuit* c, int64_t batch, const float* params,
                                   : nullptr;
   if (p.path == VQC_PATH_STREAM) {
     unsigned char* ws = static_cast<unsigned char*>(workspace);
-    rc = split && split_step(p, batch)
-             ? stream_step_split(c, batch, params, inputs, loss_kind, target, expvals, grad_out,
-                                 rows ? rows : dp, dx, ws, stream)
-             : stream_step(c, batch, batch, params, inputs, loss_kind, target, expvals, grad_out,
-                           rows ? rows : dp, dx, ws, stream);
+    float* dprows = rows ? rows : dp;
+    if (split && split_batch(p, batch)) {
+      const int64_t P = c->shared ? 0 : p.P;
+      const size_t off = second_half_offset(p, batch, 2);
+      rc = on_two_streams(c, batch, stream, [&](int64_t b0, int64_t nb, int h, void* st) {
+        return stream_step(c, nb, batch, rows_at(params, b0, P), rows_at(inputs, b0, p.F),
+                           loss_kind, rows_at(target, b0, 1), rows_at(expvals, b0, p.n),
+                           rows_at(grad_out, b0, p.n), rows_at(dprows, b0, p.P),
+                           rows_at(dx, b0, p.F), ws + h * off, st);
+      });
+    } else {
+      rc = stream_step(c, batch, batch, params, inputs, loss_kind, target, expvals, grad_out,
+                       dprows, dx, ws, stream);
+    }
     if (rc || !rows) return rc;
     rc = vqc::launch_sum_rows(batch, p.P, rows, dp, stream);
     return rc ? hip_fail("parameter gradient sum", rc) : VQC_OK;
