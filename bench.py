@@ -343,6 +343,17 @@ def measure(idx, args, torch, dev, want_cpu, cpu_budget):
     for _ in range(Wm):
         step(s)
     torch.cuda.synchronize()
+    graph = None
+    if args.graph:
+        # one step captured into a HIP graph, then timed as replays
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(torch.cuda.current_stream(dev).cuda_stream)
+        torch.cuda.synchronize()
+        step = lambda st: graph.replay()  # noqa: E731
+        for _ in range(max(Wm, 1)):
+            step(s)
+        torch.cuda.synchronize()
     first = [t.clone() for t in (E, g, dp, dx)]
 
     # ---- the timed region: exactly K steps
@@ -468,6 +479,8 @@ def main():
     ap.add_argument("--tile-qubits", type=int, default=0)
     ap.add_argument("--separate", action="store_true",
                     help="time vqc_forward + vqc_loss_grad + vqc_backward")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one step captured into a HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=5.0,
                     help="seconds of oracle work per workload (twice that for the headline)")
@@ -514,7 +527,9 @@ def main():
                                      "passes_fwd_bwd", "engine", "compile_s")},
         "step": ("vqc_forward + vqc_loss_grad + vqc_backward" if args.separate else
                  "vqc_train_step"),
-        "timing": "launches on one stream, HIP events",
+        "timing": ("replays of a HIP graph of one step, HIP events" if args.graph else
+                   "launches on the caller's stream (the streaming path forks each batch "
+                   "half to its own stream and joins), HIP events"),
         "repeats": r["repeats"],
         "kernel_ms": r["kernel_ms"],
         "forward_only_evals_per_s": r["forward_only_evals_per_s"],
