@@ -862,6 +862,16 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
 
 size_t lds_size(size_t b) { return b < 16 ? 16 : b; }
 
+// Kernels holding 16 amplitudes per thread ask for three waves per SIMD (at
+// most 168 VGPRs, a few spilled to scratch): left free, the compiler gave the
+// 12-qubit training step 178 VGPRs and two waves, and the 14-qubit forward
+// passes 178-184.  Measured: 12-qubit step 1.37 -> 1.05 ms, 14-qubit step
+// 13.5 -> 12.9 ms; four waves (128 VGPRs) spill too much (14.2 ms).  The
+// 32-amplitude adjoint passes gained nothing from it.
+std::string occupancy(int R) {
+  return R == 4 ? "__attribute__((amdgpu_waves_per_eu(3))) " : "";
+}
+
 // Whether a kernel uses the tangent form: one sample per workgroup (the frame
 // is per sample).  With 4 amplitudes per thread the tables are read from
 // registers (table_row), and rotations on lane bits take the lane forms
@@ -886,7 +896,8 @@ std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
   emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr,
                     map_off, load, fixed_flags);
   o << "}  // namespace vqc\n"
-    << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << name
+    << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << occupancy(R)
+    << name
     << (stream ? "(const vqc::PassArgs A) {\n" : "(const vqc::TileArgs A) {\n")
     << "  __shared__ __align__(16) unsigned char smem[" << lds_size(tm.on ? tm.end : lds) << "];\n";
   if (stream)
@@ -1125,7 +1136,8 @@ std::string step_unit(const Plan& p, const Frame& fr) {
                     p.end_off, false, -1, skip);
   if (skip) emit_head(o, p, head_off);
   o << "}  // namespace vqc\n"
-    << "extern \"C\" __global__ void __launch_bounds__(" << p.WG << ") vqc_rs(const vqc::TileArgs A) {\n"
+    << "extern \"C\" __global__ void __launch_bounds__(" << p.WG << ") " << occupancy(p.R)
+    << "vqc_rs(const vqc::TileArgs A) {\n"
     << "  __shared__ __align__(16) unsigned char smem[" << lds_size(end) << "];\n"
     << "  vqc::resident_step_body<" << p.WG << ", " << p.R << ", vqc::SchedF, vqc::SchedB"
     << (skip ? ", vqc::Head" : "") << ">(A, smem);\n}\n";
