@@ -79,8 +79,11 @@ def state_rw_per_sample(info):
     kept).  Adjoint (one pass per forward pass, in reverse): the first reads
     psi_G and writes lambda, the middle ones read the state their forward pass
     saved and lambda and write lambda, the last reads both and stores nothing;
-    a single pass only reads psi_G."""
+    a single pass only reads psi_G.  The training step runs the passes of its own
+    plan when the circuit has heads (first pass: the product state)."""
     nf, nb = info["fwd_passes"], info["bwd_passes"]
+    if info.get("step_fwd_passes"):
+        nf, nb = info["step_fwd_passes"], info["step_bwd_passes"]
     fwd = 1 + 2 * (nf - 1)
     adj = 1 if nb == 1 else 2 + 3 * (nb - 2) + 2
     return fwd + adj
@@ -405,8 +408,8 @@ def measure(idx, args, torch, dev, want_cpu, cpu_budget):
     resident = info["path"] == 1
     if args.engine == "jit":
         kname = "vqc_rs (one launch)" if resident else \
-            ("vqc_st, vqc_sf*, reduce_e, loss_grad, fill_zero, vqc_sb*, reduce_grad (one step: "
-             "each batch half on its own stream)")
+            ("vqc_st, vqc_sf*, reduce_e, loss_grad, fill_zero, vqc_sb*, vqc_sh, reduce_grad (one "
+             "step: each batch half on its own stream)")
     else:
         kname = "resident_step_kernel" if resident else \
             "stream_kernel passes (one step: each batch half on its own stream)"
@@ -433,6 +436,7 @@ def measure(idx, args, torch, dev, want_cpu, cpu_budget):
         "threads_per_workgroup": info["threads"], "engine": args.engine,
         "tile_qubits": info["tile_qubits"] if not resident else None,
         "passes_fwd_bwd": [info["fwd_passes"], info["bwd_passes"]],
+        "step_head_rotations": info["step_head_rotations"],
         "exchanges_fwd_bwd": [info["fwd_exchanges"], info["bwd_exchanges"]],
         "compile_s": round(compile_s, 2),
         "value": value, "ms_per_step": ms_per_step, "steps": K,
@@ -524,7 +528,8 @@ def main():
         "data": "synthetic (seeded draws of the configuration; no dataset)",
         "config": {k: r[k] for k in ("workload", "description", "n_qubits", "batch", "n_params",
                                      "n_inputs", "ops", "loss", "path", "tile_qubits",
-                                     "passes_fwd_bwd", "engine", "compile_s")},
+                                     "passes_fwd_bwd", "step_head_rotations", "engine",
+                                     "compile_s")},
         "step": ("vqc_forward + vqc_loss_grad + vqc_backward" if args.separate else
                  "vqc_train_step"),
         "timing": ("replays of a HIP graph of one step, HIP events" if args.graph else

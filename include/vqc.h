@@ -390,7 +390,11 @@ typedef struct {
     int32_t lds_bytes_fwd, lds_bytes_bwd;
     int32_t engine;         /* VQC_ENGINE_* */
     int32_t shared_params;  /* the compile option */
-    int32_t reserved[6];
+    /* streaming path, generated kernels: rotations that vqc_train_step builds
+       as a product state instead of running them (0: none), and that step's
+       passes; 0 otherwise */
+    int32_t step_head_rotations, step_fwd_passes, step_bwd_passes;
+    int32_t reserved[3];
 } vqc_info;
 int vqc_circuit_info(const vqc_circuit *c, vqc_info *info);
 

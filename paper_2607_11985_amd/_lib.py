@@ -52,7 +52,8 @@ class vqc_info(ctypes.Structure):
         "n_qubits", "n_params", "n_inputs", "n_ops", "n_rotations", "path",
         "tile_qubits", "threads", "fwd_passes", "bwd_passes", "fwd_exchanges",
         "bwd_exchanges", "fwd_instructions", "bwd_instructions", "lds_bytes_fwd",
-        "lds_bytes_bwd", "engine", "shared_params")] + [("reserved", ctypes.c_int32 * 6)]
+        "lds_bytes_bwd", "engine", "shared_params", "step_head_rotations",
+        "step_fwd_passes", "step_bwd_passes")] + [("reserved", ctypes.c_int32 * 3)]
 
 
 class VQCError(RuntimeError):

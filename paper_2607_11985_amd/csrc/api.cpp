@@ -22,6 +22,10 @@ struct vqc_circuit {
   void* blob = nullptr;
   size_t off_fwd = 0, off_bwd = 0, off_cols = 0, off_src = 0, off_idx = 0, off_cs = 0,
          off_maps = 0, off_pslots = 0, off_ma = 0, off_zm = 0, off_pc = 0;
+  // Streaming path, generated kernels: the training step's own circuit, whose
+  // plan leaves out the heads' rotations (Plan::product_head), or null.
+  vqc_circuit* step = nullptr;
+  ~vqc_circuit();
 };
 
 namespace {
@@ -80,8 +84,12 @@ struct StreamLayout {
   size_t end_inference = 0;
   size_t l[2] = {0, 0}, gpart = 0, end_training = 0;
   size_t cot = 0, end_step = 0;  // the training step's cotangent rows [B, n]
+  size_t vpart = 0;              // product head: per-tile partials of v_q [B * 2^ng][NV]
   size_t ck(size_t i) const { return ck0 + i * state; }
 };
+
+// Head partials per tile (4 n floats rounded up to 16).
+int head_nv(const Plan& p) { return (4 * p.n + 15) / 16 * 16; }
 
 StreamLayout stream_layout(const Plan& p, int64_t batch) {
   StreamLayout L;
@@ -101,6 +109,10 @@ StreamLayout stream_layout(const Plan& p, int64_t batch) {
   L.end_training = align_up(L.gpart + tiles * (size_t)(p.P + p.F) * 4, 256);
   L.cot = L.end_training;
   L.end_step = align_up(L.cot + (size_t)batch * (size_t)p.n * 4, 256);
+  if (p.product_head) {
+    L.vpart = L.end_step;
+    L.end_step = align_up(L.vpart + tiles * (size_t)head_nv(p) * 4, 256);
+  }
   return L;
 }
 
@@ -167,6 +179,7 @@ size_t fd_rows_bytes(const Plan& p, int64_t batch) {
 }
 
 size_t required_bytes(const vqc_circuit* c, int64_t batch, int mode) {
+  if (mode == 2 && c->step) c = c->step;  // the training step runs the step circuit
   const Plan& p = c->plan;
   if (batch == 0) return 0;
   if (mode == 3) return fd_rows_bytes(p, batch) + (c->shared ? (size_t)batch * p.P * 4 : 0);
@@ -372,6 +385,7 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     a.psi_src = ws + (keep ? L.ck(i ? i - 1 : 0) : L.ck((i + 1) % 2));
     a.psi_dst = ws + (keep ? L.ck(i) : L.ck(i % 2));
     if (psi0 && (a.flags & vqc::PF_INIT)) {
+      if (p.product_head) return fail(VQC_ERR_UNSUPPORTED, "internal: Psi_0 with a product head");
       a.flags &= ~vqc::PF_INIT;
       a.psi_src = psi0;
       a.psi0_in = 1;
@@ -419,6 +433,7 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     a.lam_src = ws + L.l[(j + 1) % 2];
     a.lam_dst = ws + L.l[j % 2];
     a.gpart = gpart;
+    a.vpart = p.product_head ? reinterpret_cast<float*>(ws + L.vpart) : nullptr;
     set_tables(a, ws, L);
     if (first) {
       rc = launch_tables(c, a, batch, stream);
@@ -431,8 +446,69 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     if (rc) return hip_fail("backward pass launch", rc);
     first = false;
   }
+  if (p.product_head) {
+    // the heads' gradients into the partials of each sample's first tile
+    vqc::PassArgs a = pass_args(c, p.bpass.back(), true, batch);
+    a.gpart = gpart;
+    a.vpart = reinterpret_cast<float*>(ws + L.vpart);
+    set_tables(a, ws, L);
+    rc = c->jit.head_finish ? vqc::jit_launch(c->jit.head_finish, batch, 64, &a, sizeof(a), stream)
+                            : (int)hipErrorInvalidDeviceFunction;
+    if (rc) return hip_fail("head gradient launch", rc);
+  }
   rc = vqc::launch_reduce_grad(batch, p.ng, p.P + p.F, p.P, p.F, gpart, dp, dx, stream);
   if (rc) return hip_fail("gradient reduction launch", rc);
+  return VQC_OK;
+}
+
+}  // namespace
+
+vqc_circuit::~vqc_circuit() {
+  delete step;
+  if (blob) {
+    DeviceGuard g(device);
+    (void)hipFree(blob);
+  }
+}
+
+namespace {
+
+// The plan's tables in device memory (one allocation) and its kernels: the
+// generated ones, or the fixed ones' attributes.
+int load_device(vqc_circuit* c, std::string& msg) {
+  const Plan& p = c->plan;
+  std::vector<unsigned char> blob;
+  c->off_fwd = append(blob, p.fwd);
+  c->off_bwd = append(blob, p.bwd);
+  c->off_cols = append(blob, p.cols);
+  c->off_src = append(blob, p.occ_src);
+  c->off_idx = append(blob, p.occ_idx);
+  c->off_cs = append(blob, p.occ_cs);
+  c->off_ma = append(blob, p.occ_ma);
+  c->off_maps = append(blob, p.maps);
+  c->off_pslots = append(blob, p.pslots);
+  c->off_zm = append(blob, p.zmask);
+  c->off_pc = append(blob, p.pcol);
+  DeviceGuard g(c->device);
+  if (!g.ok()) {
+    msg = "hipSetDevice failed";
+    return VQC_ERR_HIP;
+  }
+  if (hipMalloc(&c->blob, blob.size()) != hipSuccess) {
+    c->blob = nullptr;
+    msg = "hipMalloc of the schedule failed";
+    return VQC_ERR_HIP;
+  }
+  if (hipMemcpy(c->blob, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) {
+    msg = "copy of the schedule failed";
+    return VQC_ERR_HIP;
+  }
+  if (c->engine == VQC_ENGINE_JIT) return vqc::jit_build(p, c->device, c->jit, msg);
+  const int rc = vqc::prepare_kernels(p);
+  if (rc != 0) {
+    msg = std::string("hipFuncSetAttribute failed: ") + hipGetErrorString((hipError_t)rc);
+    return VQC_ERR_HIP;
+  }
   return VQC_OK;
 }
 
@@ -527,54 +603,37 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
   c->device = device;
   c->engine = engine;
   c->shared = shared;
+  // The streaming training step builds the product state after every qubit's
+  // head instead of running the heads' rotations (generated kernels; the
+  // heads' exact angles come from the table kernel).  Measured on the 16-qubit
+  // ring and the 14-qubit re-uploading workloads: without their heads' gates
+  // the steps take 11.5 % and 9.5 % less time.
+  if (engine == VQC_ENGINE_JIT && c->plan.path == VQC_PATH_STREAM) {
+    Plan sp;
+    std::string msg_s;
+    if (vqc::build_step_plan(c->plan, sp, msg_s) == 0 && vqc::stream_tables_fit(sp)) {
+      c->step = new (std::nothrow) vqc_circuit();
+      if (!c->step) {
+        delete c;
+        return fail(VQC_ERR_OOM, "out of host memory");
+      }
+      c->step->plan = std::move(sp);
+      c->step->device = device;
+      c->step->engine = engine;
+      c->step->shared = shared;
+    }
+  }
   if (device >= 0) {
     int count = 0;
     if (hipGetDeviceCount(&count) != hipSuccess || device >= count) {
       delete c;
       return fail(VQC_ERR_INVALID_ARG, "no HIP device " + std::to_string(device));
     }
-    const Plan& p = c->plan;
-    std::vector<unsigned char> blob;
-    c->off_fwd = append(blob, p.fwd);
-    c->off_bwd = append(blob, p.bwd);
-    c->off_cols = append(blob, p.cols);
-    c->off_src = append(blob, p.occ_src);
-    c->off_idx = append(blob, p.occ_idx);
-    c->off_cs = append(blob, p.occ_cs);
-    c->off_ma = append(blob, p.occ_ma);
-    c->off_maps = append(blob, p.maps);
-    c->off_pslots = append(blob, p.pslots);
-    c->off_zm = append(blob, p.zmask);
-    c->off_pc = append(blob, p.pcol);
-    DeviceGuard g(device);
-    if (!g.ok()) {
+    rc = load_device(c, msg);
+    if (rc == VQC_OK && c->step) rc = load_device(c->step, msg);
+    if (rc != VQC_OK) {
       delete c;
-      return fail(VQC_ERR_HIP, "hipSetDevice failed");
-    }
-    if (hipMalloc(&c->blob, blob.size()) != hipSuccess) {
-      delete c;
-      return fail(VQC_ERR_HIP, "hipMalloc of the schedule failed");
-    }
-    if (hipMemcpy(c->blob, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) {
-      (void)hipFree(c->blob);
-      delete c;
-      return fail(VQC_ERR_HIP, "copy of the schedule failed");
-    }
-    if (engine == VQC_ENGINE_JIT) {
-      rc = vqc::jit_build(p, device, c->jit, msg);
-      if (rc != 0) {
-        (void)hipFree(c->blob);
-        delete c;
-        return fail(rc, msg);
-      }
-    } else {
-      rc = vqc::prepare_kernels(p);
-      if (rc != 0) {
-        (void)hipFree(c->blob);
-        delete c;
-        return fail(VQC_ERR_HIP, std::string("hipFuncSetAttribute failed: ") +
-                                     hipGetErrorString((hipError_t)rc));
-      }
+      return fail(rc, msg);
     }
   }
   *out = c;
@@ -615,14 +674,7 @@ int vqc_compile_qasm(const char* source, const char* input_names, const vqc_comp
   return vqc_compile(v.data(), (int32_t)v.size(), nq, np, ni, opts, out);
 }
 
-void vqc_destroy(vqc_circuit* c) {
-  if (!c) return;
-  if (c->blob) {
-    DeviceGuard g(c->device);
-    (void)hipFree(c->blob);
-  }
-  delete c;
-}
+void vqc_destroy(vqc_circuit* c) { delete c; }
 
 size_t vqc_workspace_bytes(const vqc_circuit* c, int64_t batch, int32_t training) {
   if (!c || batch < 0 || training < 0 || training > 3) return (size_t)-1;
@@ -789,26 +841,28 @@ int train_step_impl(const vqc_circuit* c, int64_t batch, const float* params,
                     float* grad_out, float* dparams, float* dinputs, void* workspace,
                     void* stream, bool split) {
   const Plan& p = c->plan;
+  // with a product head the streaming step runs the circuit planned without the heads
+  const vqc_circuit* sc = c->step ? c->step : c;
   int rc = 0;
   float* dp = p.P > 0 ? dparams : nullptr;
   float* dx = p.F > 0 ? dinputs : nullptr;
   float* rows = (c->shared && dp) ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
-                                                             shared_rows_offset(p, batch, 2))
+                                                             shared_rows_offset(sc->plan, batch, 2))
                                   : nullptr;
   if (p.path == VQC_PATH_STREAM) {
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     float* dprows = rows ? rows : dp;
     if (split && split_batch(p, batch)) {
       const int64_t P = c->shared ? 0 : p.P;
-      const size_t off = second_half_offset(p, batch, 2);
+      const size_t off = second_half_offset(sc->plan, batch, 2);
       rc = on_two_streams(c, batch, stream, [&](int64_t b0, int64_t nb, int h, void* st) {
-        return stream_step(c, nb, batch, rows_at(params, b0, P), rows_at(inputs, b0, p.F),
+        return stream_step(sc, nb, batch, rows_at(params, b0, P), rows_at(inputs, b0, p.F),
                            loss_kind, rows_at(target, b0, 1), rows_at(expvals, b0, p.n),
                            rows_at(grad_out, b0, p.n), rows_at(dprows, b0, p.P),
                            rows_at(dx, b0, p.F), ws + h * off, st);
       });
     } else {
-      rc = stream_step(c, batch, batch, params, inputs, loss_kind, target, expvals, grad_out,
+      rc = stream_step(sc, batch, batch, params, inputs, loss_kind, target, expvals, grad_out,
                        dprows, dx, ws, stream);
     }
     if (rc || !rows) return rc;
@@ -978,13 +1032,20 @@ int vqc_circuit_info(const vqc_circuit* c, vqc_info* info) {
   info->lds_bytes_bwd = (int32_t)p.lds_bwd;
   info->engine = c->engine;
   info->shared_params = c->shared ? 1 : 0;
+  if (c->step) {
+    const Plan& s = c->step->plan;
+    for (const auto& hq : s.head) info->step_head_rotations += (int32_t)hq.size();
+    info->step_fwd_passes = (int32_t)s.fpass.size();
+    info->step_bwd_passes = (int32_t)s.bpass.size();
+  }
   return VQC_OK;
 }
 
 int vqc_jit_check(const vqc_circuit* c) {
   if (!c) return fail(VQC_ERR_INVALID_ARG, "circuit handle is NULL");
   std::string log;
-  const int rc = vqc::jit_compile_only(c->plan, log);
+  int rc = vqc::jit_compile_only(c->plan, log);
+  if (!rc && c->step) rc = vqc::jit_compile_only(c->step->plan, log);
   if (rc) return fail(rc, "run-time compilation failed: " + log.substr(0, 4000));
   return VQC_OK;
 }

@@ -834,10 +834,14 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
                        const uint32_t* ins, int n_ins, bool bwd, int R, int k, int S,
                        const GradMode& gm, const TanMode& tm, const Frame* tables, int map_off,
                        bool load = false, int fixed_flags = -1,
-                       const std::vector<char>* skip = nullptr) {
+                       const std::vector<char>* skip = nullptr,
+                       const std::string& head = std::string()) {
   o << "struct " << name << " {\n";
   emit_constants(o, p, map_off);
   o << "static constexpr int kFixedFlags = " << fixed_flags << ";\n";
+  // the streaming step's product head (stream_product_start, stream_head_partials)
+  if (head.empty()) o << "static constexpr bool kProductStart = false, kHeadPartials = false;\n";
+  else o << head;
   o
     << "template <int R, bool BWD, bool WIDE>\n"
     << "__device__ __forceinline__ static void run(St<R>& a, St<R>& l, const Walk& w, "
@@ -887,14 +891,15 @@ bool tangent_wanted(int S, int R) {
 std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
                         const uint32_t* ins, int n_ins, bool bwd, bool stream, int R, int S,
                         int threads, size_t lds, int n_slots, bool esign, int map_off,
-                        bool load = false, int fixed_flags = -1) {
+                        bool load = false, int fixed_flags = -1,
+                        const std::string& head = std::string()) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\n";
   const int lanes = stream ? threads : 1 << (p.k - R);
   TanMode tm = tan_mode(p, bwd ? nullptr : ins, n_ins, bwd ? ins : nullptr, n_ins, S, esign, lds);
   tm.on = tm.on && tangent_wanted(S, R);
   emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr,
-                    map_off, load, fixed_flags);
+                    map_off, load, fixed_flags, nullptr, head);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << occupancy(R)
     << name
@@ -931,15 +936,18 @@ std::vector<char> head_occurrences(const Plan& p, const TanMode& tm) {
   return h;
 }
 
-// struct Head of the training step: the head tables and mappings.
-void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
+// Longest head.
+int head_len(const Plan& p) {
   int L = 0;
   for (const auto& hq : p.head) L = std::max(L, (int)hq.size());
-  const int n = p.n, k = p.k, R = p.R;
-  o << "struct Head {\n"
-    << "static constexpr bool kOn = true;\n"
-    << "static constexpr int kN = " << n << ", kK = " << k << ", kL = " << L << ";\n"
-    << "static constexpr uint32_t kOff = " << off << "u;\n";
+  return L;
+}
+
+// kL and fn(tid): lane q's head steps (HeadPre: word = occurrence | kind << 16,
+// gradient slot + 1, chain-rule factor), lanes >= n clamped to qubit n - 1.
+void emit_head_pre(std::ostringstream& o, const Plan& p, const char* fn) {
+  const int L = head_len(p), n = p.n;
+  o << "static constexpr int kL = " << L << ";\n";
   std::vector<uint32_t> words, slots;
   std::vector<float> muls;
   bool scaled = false;
@@ -959,8 +967,7 @@ void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
         muls.push_back(1.f);
       }
     }
-  o << "using Pre = HeadPre<kL>;\n"
-    << "__device__ __forceinline__ static Pre preload(int tid) {\n";
+  o << "__device__ __forceinline__ static HeadPre<kL> " << fn << "(int tid) {\n";
   emit_array(o, "uint32_t", "kW", words);
   emit_array(o, "uint32_t", "kS", slots);
   if (scaled) {
@@ -970,7 +977,7 @@ void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
     o << "};\n";
   }
   o << "  const int q = min(tid & 63, " << n - 1 << ");\n"
-    << "  Pre h;\n"
+    << "  HeadPre<kL> h;\n"
     << "#pragma unroll\n"
     << "  for (int i = 0; i < kL; ++i) {\n"
     << "    h.w[i] = kW[q * kL + i];\n"
@@ -978,73 +985,67 @@ void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
     << "    h.m[i] = " << (scaled ? "kM[q * kL + i]" : "1.f") << ";\n"
     << "  }\n"
     << "  return h;\n}\n";
-  // qubit -> register / thread bit under the two mappings
-  auto bits = [&](int map_off, std::vector<int>& reg, std::vector<int>& thr) {
-    reg.assign(R, 0);
-    thr.assign(k - R, 0);
-    for (int q = 0; q < k; ++q) {
-      const int ph = p.maps[map_off + q];
-      if (ph < R) reg[ph] = q;
-      else thr[ph - R] = q;
-    }
-  };
-  std::vector<int> sreg, sthr, ereg, ethr;
-  bits(p.start_off, sreg, sthr);
-  bits(p.bwd_end_off, ereg, ethr);
-  const int t = k - R;
-  const std::string q_a = "a", q_b = "b";
-  auto pad_states = [&]() {
-    for (int q = n; q < k; ++q)
-      o << "  const float2 a" << q << " = make_float2(1.f, 0.f), b" << q
-        << " = make_float2(0.f, 0.f);\n";
-  };
-  // init(): every head walked by its qubit's lane, then the product state in
-  // the forward's start mapping
-  o << "template <int R>\n"
-    << "__device__ __forceinline__ static void init(St<R>& a, const Walk& w, const Pre& hp) {\n"
-    << "  static_assert(R == " << R << ", \"register width\");\n"
-    << "  HeadRec* rec = reinterpret_cast<HeadRec*>(w.smem + kOff);\n"
-    << "  float4* fin = reinterpret_cast<float4*>(w.smem + kOff + " << n * L * 32 << "u);\n"
-    << "  float2 fa, fb;\n"
-    << "  head_walk<kL>(w, hp, rec, fin, kN, fa, fb);\n";
-  for (int q = 0; q < n; ++q)
+}
+
+// The qubits on the register bits (reg, R of them) and on the bits of w.tb
+// (tb: thread bits, then a streaming tile's index bits) under the mapping at
+// map_off; -1 where no qubit sits (tile ranks >= nq of a small state).
+void head_bits(const Plan& p, int map_off, int R, int ntb, std::vector<int>& reg,
+               std::vector<int>& tb) {
+  reg.assign(R, -1);
+  tb.assign(ntb, -1);
+  for (int q = 0; q < p.nq; ++q) {
+    const int ph = p.maps[map_off + q];
+    if (ph < R) reg[ph] = q;
+    else if (ph - R < ntb) tb[ph - R] = q;
+  }
+}
+
+// const float2 a<q>, b<q>: qubit q's head state from lane q (after head_walk
+// or head_state left it in fa, fb); qubits >= n stay |0>.
+void emit_head_broadcast(std::ostringstream& o, const Plan& p) {
+  for (int q = 0; q < p.n; ++q)
     o << "  const float2 a" << q << " = make_float2(lane_value(fa.x, " << q << "), lane_value(fa.y, "
       << q << ")), b" << q << " = make_float2(lane_value(fb.x, " << q << "), lane_value(fb.y, " << q
       << "));\n";
-  pad_states();
+  for (int q = p.n; q < std::max(p.nq, p.k); ++q)
+    o << "  const float2 a" << q << " = make_float2(1.f, 0.f), b" << q
+      << " = make_float2(0.f, 0.f);\n";
+}
+
+// The product state's amplitudes in a: the factors of the tb bits, then one
+// doubling per register bit.
+void emit_product_state(std::ostringstream& o, const std::vector<int>& reg,
+                        const std::vector<int>& tbq) {
+  const int R = (int)reg.size();
   o << "  const uint32_t tb = w.tb;\n"
     << "  float2 t = make_float2(1.f, 0.f);\n";
-  for (int j = 0; j < t; ++j)
-    o << "  t = cmul(t, ((tb >> " << j << ") & 1u) ? b" << sthr[j] << " : a" << sthr[j] << ");\n";
+  for (size_t j = 0; j < tbq.size(); ++j)
+    if (tbq[j] >= 0)
+      o << "  t = cmul(t, ((tb >> " << j << ") & 1u) ? b" << tbq[j] << " : a" << tbq[j] << ");\n";
   o << "  const float2 A0_0 = t;\n";
   for (int pb = 0; pb < R; ++pb)
     for (int u = 0; u < (2 << pb); ++u) {
       const int src = u & ~(1 << pb);
       o << "  const float2 A" << pb + 1 << "_" << u << " = cmul(A" << pb << "_" << src << ", "
-        << (((u >> pb) & 1) ? "b" : "a") << sreg[pb] << ");\n";
+        << (((u >> pb) & 1) ? "b" : "a") << reg[pb] << ");\n";
     }
   for (int u = 0; u < (1 << R); ++u)
     o << "  a.r[" << u << "] = A" << R << "_" << u << ".x; a.i[" << u << "] = A" << R << "_" << u
       << ".y;\n";
-  o << "}\n";
-  // grads(): the 2-vector partials of every qubit from lambda in the adjoint's
-  // end mapping, then the sums and the walks back (head_finish)
-  const int NV = (4 * n + 15) / 16 * 16;
-  o << "template <int WG, int R>\n"
-    << "__device__ __forceinline__ static void grads(const St<R>& l, const Walk& w) {\n"
-    << "  const HeadRec* rec = reinterpret_cast<const HeadRec*>(w.smem + kOff);\n"
-    << "  const float4* fin = reinterpret_cast<const float4*>(w.smem + kOff + " << n * L * 32
-    << "u);\n";
-  for (int q = 0; q < n; ++q)
-    o << "  const float4 F" << q << " = fin[" << q << "];\n"
-      << "  const float2 a" << q << " = make_float2(F" << q << ".x, F" << q << ".y), b" << q
-      << " = make_float2(F" << q << ".z, F" << q << ".w);\n";
-  pad_states();
+}
+
+// float v[NV]: this thread's terms of v_q = (I_q (x) <phi_{not q}|) lambda for
+// every qubit q < n (v[4 q .. 4 q + 3] = v_q(0), v_q(1) as re, im), from
+// lambda in l under the mapping given by reg / tbq; a<q>, b<q> in scope.
+void emit_head_contraction(std::ostringstream& o, const Plan& p, const std::vector<int>& reg,
+                           const std::vector<int>& tbq, int NV) {
+  const int R = (int)reg.size(), t = (int)tbq.size(), n = p.n;
   o << "  const uint32_t tb = w.tb;\n";
-  // the thread bits' factors, and their products leaving one out
+  // the tb bits' factors, and their products leaving one out
   for (int j = 0; j < t; ++j)
-    o << "  const float2 f" << j << " = ((tb >> " << j << ") & 1u) ? b" << ethr[j] << " : a"
-      << ethr[j] << ";\n";
+    o << "  const float2 f" << j << " = ((tb >> " << j << ") & 1u) ? b" << tbq[j] << " : a"
+      << tbq[j] << ";\n";
   o << "  const float2 P0 = make_float2(1.f, 0.f);\n";
   for (int j = 0; j < t; ++j)
     o << "  const float2 P" << j + 1 << " = cmul(P" << j << ", f" << j << ");\n";
@@ -1067,8 +1068,8 @@ void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
         if (((u >> c) & 1) || (u & done)) continue;
         const std::string nm = "y" + std::to_string(pb) + "_" + std::to_string(c) + "_" +
                                std::to_string(u);
-        o << "  const float2 " << nm << " = cadd(cmulc(a" << ereg[c] << ", " << name[u]
-          << "), cmulc(b" << ereg[c] << ", " << name[u | (1 << c)] << "));\n";
+        o << "  const float2 " << nm << " = cadd(cmulc(a" << reg[c] << ", " << name[u]
+          << "), cmulc(b" << reg[c] << ", " << name[u | (1 << c)] << "));\n";
         name[u] = nm;
       }
       done |= 1 << c;
@@ -1076,28 +1077,155 @@ void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
     o << "  const float2 C" << pb << "_0 = " << name[0] << ", C" << pb << "_1 = " << name[1 << pb]
       << ";\n";
   }
-  o << "  const float2 sall = cadd(cmulc(a" << ereg[0] << ", C0_0), cmulc(b" << ereg[0]
+  o << "  const float2 sall = cadd(cmulc(a" << reg[0] << ", C0_0), cmulc(b" << reg[0]
     << ", C0_1));\n"
     << "  float v[" << NV << "];\n"
     << "#pragma unroll\n  for (int j = 0; j < " << NV << "; ++j) v[j] = 0.f;\n";
   for (int pb = 0; pb < R; ++pb) {
-    const int q = ereg[pb];
+    const int q = reg[pb];
     if (q >= n) continue;
     o << "  { const float2 u0 = cmulc(tall, C" << pb << "_0), u1 = cmulc(tall, C" << pb << "_1);\n"
       << "    v[" << 4 * q << "] = u0.x; v[" << 4 * q + 1 << "] = u0.y; v[" << 4 * q + 2
       << "] = u1.x; v[" << 4 * q + 3 << "] = u1.y; }\n";
   }
   for (int j = 0; j < t; ++j) {
-    const int q = ethr[j];
+    const int q = tbq[j];
     if (q >= n) continue;
     o << "  { const float2 c = cmulc(T" << j << ", sall); const bool one = (tb >> " << j
       << ") & 1u;\n"
       << "    v[" << 4 * q << "] = one ? 0.f : c.x; v[" << 4 * q + 1 << "] = one ? 0.f : c.y; v["
       << 4 * q + 2 << "] = one ? c.x : 0.f; v[" << 4 * q + 3 << "] = one ? c.y : 0.f; }\n";
   }
+}
+
+int head_nv(const Plan& p) { return (4 * p.n + 15) / 16 * 16; }
+
+// struct Head of the training step: the head tables and mappings.
+void emit_head(std::ostringstream& o, const Plan& p, size_t off) {
+  const int L = head_len(p), n = p.n, k = p.k, R = p.R;
+  o << "struct Head {\n"
+    << "static constexpr bool kOn = true;\n"
+    << "static constexpr int kN = " << n << ", kK = " << k << ";\n"
+    << "static constexpr uint32_t kOff = " << off << "u;\n";
+  emit_head_pre(o, p, "preload");
+  o << "using Pre = HeadPre<kL>;\n";
+  std::vector<int> sreg, sthr, ereg, ethr;
+  head_bits(p, p.start_off, R, k - R, sreg, sthr);
+  head_bits(p, p.bwd_end_off, R, k - R, ereg, ethr);
+  // init(): every head walked by its qubit's lane, then the product state in
+  // the forward's start mapping
+  o << "template <int R>\n"
+    << "__device__ __forceinline__ static void init(St<R>& a, const Walk& w, const Pre& hp) {\n"
+    << "  static_assert(R == " << R << ", \"register width\");\n"
+    << "  HeadRec* rec = reinterpret_cast<HeadRec*>(w.smem + kOff);\n"
+    << "  float4* fin = reinterpret_cast<float4*>(w.smem + kOff + " << n * L * 32 << "u);\n"
+    << "  float2 fa, fb;\n"
+    << "  head_walk<kL>(w, hp, rec, fin, kN, fa, fb);\n";
+  emit_head_broadcast(o, p);
+  emit_product_state(o, sreg, sthr);
+  o << "}\n";
+  // grads(): the 2-vector partials of every qubit from lambda in the adjoint's
+  // end mapping, then the sums and the walks back (head_finish)
+  const int NV = head_nv(p);
+  o << "template <int WG, int R>\n"
+    << "__device__ __forceinline__ static void grads(const St<R>& l, const Walk& w) {\n"
+    << "  const HeadRec* rec = reinterpret_cast<const HeadRec*>(w.smem + kOff);\n"
+    << "  const float4* fin = reinterpret_cast<const float4*>(w.smem + kOff + " << n * L * 32
+    << "u);\n";
+  for (int q = 0; q < n; ++q)
+    o << "  const float4 F" << q << " = fin[" << q << "];\n"
+      << "  const float2 a" << q << " = make_float2(F" << q << ".x, F" << q << ".y), b" << q
+      << " = make_float2(F" << q << ".z, F" << q << ".w);\n";
+  for (int q = n; q < k; ++q)
+    o << "  const float2 a" << q << " = make_float2(1.f, 0.f), b" << q
+      << " = make_float2(0.f, 0.f);\n";
+  emit_head_contraction(o, p, ereg, ethr, NV);
   o << "  head_finish<WG, kL, " << NV << ">(v, w, rec, kN);\n"
     << "}\n"
     << "};\n";
+}
+
+// The streaming training step's first forward pass: product_start() builds the
+// state after the heads in the pass's start mapping (map_off).
+std::string stream_product_start(const Plan& p, int map_off, int R) {
+  std::ostringstream o;
+  std::vector<int> reg, tbq;
+  head_bits(p, map_off, R, p.k - R + p.ng, reg, tbq);
+  o << "static constexpr bool kProductStart = true, kHeadPartials = false;\n";
+  emit_head_pre(o, p, "head_pre");
+  o << "template <int R>\n"
+    << "__device__ __forceinline__ static void product_start(St<R>& a, const Walk& w) {\n"
+    << "  static_assert(R == " << R << ", \"register width\");\n"
+    << "  const HeadPre<kL> hp = head_pre((int)threadIdx.x);\n"
+    << "  float2 fa, fb;\n"
+    << "  head_state<kL>(w, hp, fa, fb);\n";
+  emit_head_broadcast(o, p);
+  emit_product_state(o, reg, tbq);
+  o << "}\n";
+  return o.str();
+}
+
+// The streaming training step's last adjoint pass: head_partials() sums this
+// tile's terms of every v_q over the workgroup and stores them to out[0, NV).
+std::string stream_head_partials(const Plan& p, int map_off, int R) {
+  std::ostringstream o;
+  std::vector<int> reg, tbq;
+  head_bits(p, map_off, R, p.k - R + p.ng, reg, tbq);
+  const int NV = head_nv(p);
+  o << "static constexpr bool kProductStart = false, kHeadPartials = true;\n"
+    << "static constexpr int kNV = " << NV << ";\n";
+  emit_head_pre(o, p, "head_pre");
+  o << "template <int WG, int R>\n"
+    << "__device__ __forceinline__ static void head_partials(const St<R>& l, const Walk& w, "
+       "float* out) {\n"
+    << "  static_assert(R == " << R << ", \"register width\");\n"
+    << "  const HeadPre<kL> hp = head_pre((int)threadIdx.x);\n"
+    << "  float2 fa, fb;\n"
+    << "  head_state<kL>(w, hp, fa, fb);\n";
+  emit_head_broadcast(o, p);
+  emit_head_contraction(o, p, reg, tbq, NV);
+  o << "  const float s = workgroup_sums<WG, " << NV << ">(v, w.xbuf);\n"
+    << "  if ((int)threadIdx.x < " << NV << ") out[threadIdx.x] = s;\n"
+    << "}\n";
+  return o.str();
+}
+
+// The streaming training step's head gradient kernel (head_finish_stream): its
+// Head struct holds the head tables and, per gradient slot of a head rotation,
+// the list of its (qubit, step) terms.
+std::string head_finish_unit(const Plan& p) {
+  std::ostringstream o;
+  const int L = head_len(p), n = p.n, NV = head_nv(p);
+  o << "#include \"vqc_device.h\"\nnamespace vqc {\nstruct Head {\n"
+    << "static constexpr int kN = " << n << ", kNV = " << NV << ";\n";
+  emit_head_pre(o, p, "head_pre");
+  std::map<int, std::vector<int>> terms;  // slot -> q * L + i
+  for (int q = 0; q < n; ++q)
+    for (int i = 0; i < (int)p.head[q].size(); ++i) {
+      const int s = p.occ_slot[p.head[q][i].occ];
+      if (s >= 0) terms[s].push_back(q * L + i);
+    }
+  std::vector<uint32_t> start{0}, idx, slot;
+  for (const auto& kv : terms) {
+    slot.push_back((uint32_t)kv.first);
+    idx.insert(idx.end(), kv.second.begin(), kv.second.end());
+    start.push_back((uint32_t)idx.size());
+  }
+  o << "__device__ __forceinline__ static void add_grads(const float* gs, float* gp, int tid) {\n";
+  emit_array(o, "uint32_t", "kStart", start);
+  emit_array(o, "uint32_t", "kIdx", idx);
+  emit_array(o, "uint32_t", "kSlot", slot);
+  o << "  for (int i = tid; i < " << slot.size() << "; i += 64) {\n"
+    << "    float s = 0.f;\n"
+    << "    for (uint32_t e = kStart[i]; e < kStart[i + 1]; ++e) s += gs[kIdx[e]];\n"
+    << "    gp[kSlot[i]] += s;\n"
+    << "  }\n}\n"
+    << "};\n}  // namespace vqc\n";
+  const size_t lds = (size_t)n * L * 32 + (size_t)n * 16 + (size_t)(NV + n * L) * 4;
+  o << "extern \"C\" __global__ void __launch_bounds__(64) vqc_sh(const vqc::PassArgs A) {\n"
+    << "  __shared__ __align__(16) unsigned char smem[" << lds_size(lds) << "];\n"
+    << "  vqc::head_finish_stream<vqc::Head>(A, smem);\n}\n";
+  return o.str();
 }
 
 // The training step: forward and adjoint sweeps in one kernel.
@@ -1149,11 +1277,20 @@ std::string step_unit(const Plan& p, const Frame& fr) {
 // The table kernel of a streaming circuit: the angle table and the frame signs
 // of every occurrence, per sample (table_body), or "" when they do not fit in
 // LDS (the passes then compute their own).
+// With a product head the head rotations keep their exact (cos, sin) and
+// take no part in the frame.
 std::string table_unit(const Plan& p, const Frame& fr) {
   TanMode t;
   const int nocc = (int)p.occ_src.size();
   t.W = std::max(1, (nocc + 31) / 32);
-  for (int k = 0; k < nocc; ++k) t.focc.push_back(k);
+  std::vector<char> head;
+  if (p.product_head) {
+    head.assign(nocc, 0);
+    for (const auto& hq : p.head)
+      for (const Prim& g : hq) head[g.occ] = 1;
+  }
+  for (int k = 0; k < nocc; ++k)
+    if (head.empty() || !head[k]) t.focc.push_back(k);
   t.esign = true;
   size_t off = align16((size_t)std::max(nocc, 1) * 8);
   t.off_bits = off;
@@ -1168,7 +1305,7 @@ std::string table_unit(const Plan& p, const Frame& fr) {
   std::ostringstream o;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\nstruct Sched {\n";
   emit_constants(o, p, p.end_off);
-  emit_tables(o, p, t, fr, kTableThreads, true);
+  emit_tables(o, p, t, fr, kTableThreads, true, false, head.empty() ? nullptr : &head);
   o << "};\n}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << kTableThreads
     << ") vqc_st(const vqc::PassArgs A) {\n"
@@ -1192,24 +1329,36 @@ std::vector<JitUnit> jit_units(const Plan& p) {
   }
   const std::string tables = table_unit(p, fr);
   const bool load = !tables.empty();
+  const bool ph = p.product_head && load;  // the heads' exact angles come from the tables
   for (size_t i = 0; i < p.fpass.size(); ++i) {
     const std::string name = "vqc_sf" + std::to_string(i);
     const PassPlan& pp = p.fpass[i];
+    const std::string head = ph && (pp.flags & PF_INIT)
+                                 ? stream_product_start(p, pp.start_off, p.Rf) : std::string();
     u.push_back({name, kernel_unit(p, fr, name, p.fwd.data() + 2 * pp.ins_off, pp.n_ins, false,
                                    true, p.Rf, 1, 1 << (p.k - p.Rf), p.lds_fwd, pp.n_slots,
                                    (pp.flags & PF_ZPART) != 0, pp.end_off, load,
-                                   (int)(pp.flags & ~PF_INIT))});
+                                   (int)(pp.flags & ~PF_INIT), head)});
   }
   for (size_t i = 0; i < p.bpass.size(); ++i) {
     const std::string name = "vqc_sb" + std::to_string(i);
     const PassPlan& pp = p.bpass[i];
+    const std::string head = ph && (pp.flags & PF_LAST_ADJ)
+                                 ? stream_head_partials(p, pp.end_off, p.Rb) : std::string();
     u.push_back({name, kernel_unit(p, fr, name, p.bwd.data() + 2 * pp.ins_off, pp.n_ins, true,
                                    true, p.Rb, 1, 1 << (p.k - p.Rb), p.lds_bwd, pp.n_slots,
                                    (pp.flags & PF_MAKE_LAMBDA) != 0, pp.start_off, load,
-                                   (int)(pp.flags & ~PF_INIT))});
+                                   (int)(pp.flags & ~PF_INIT), head)});
   }
   if (load) u.push_back({"vqc_st", tables});
+  if (ph) u.push_back({"vqc_sh", head_finish_unit(p)});
   return u;
+}
+
+// Whether a streaming plan's passes read their tables from the table kernel
+// (which a product head needs).
+bool stream_tables_fit(const Plan& p) {
+  return !table_unit(p, frame_rows(p)).empty();
 }
 
 namespace {
@@ -1426,15 +1575,15 @@ int jit_build(const Plan& p, int device, JitKernels& out, std::string& msg) {
     }
   }
   out = JitKernels();
-  if (p.path == VQC_PATH_RESIDENT) {
-    out.res_fwd = fns[0];
-    out.res_bwd = fns[1];
-    out.res_step = fns[2];
-  } else {
-    const size_t nf = p.fpass.size(), nb = p.bpass.size();
-    out.pass_fwd.assign(fns.begin(), fns.begin() + nf);
-    out.pass_bwd.assign(fns.begin() + nf, fns.begin() + nf + nb);
-    if (fns.size() > nf + nb) out.tables = fns[nf + nb];
+  for (size_t i = 0; i < units.size(); ++i) {
+    const std::string& nm = units[i].name;
+    if (nm == "vqc_rf") out.res_fwd = fns[i];
+    else if (nm == "vqc_rb") out.res_bwd = fns[i];
+    else if (nm == "vqc_rs") out.res_step = fns[i];
+    else if (nm == "vqc_st") out.tables = fns[i];
+    else if (nm == "vqc_sh") out.head_finish = fns[i];
+    else if (nm.compare(0, 6, "vqc_sf") == 0) out.pass_fwd.push_back(fns[i]);
+    else if (nm.compare(0, 6, "vqc_sb") == 0) out.pass_bwd.push_back(fns[i]);
   }
   return VQC_OK;
 }

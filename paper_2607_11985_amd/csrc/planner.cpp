@@ -499,6 +499,34 @@ GateShape gate_shape(int kind) {
 
 constexpr double kPi = 3.14159265358979323846;
 
+// (cos, sin)(th / 2) of a constant rotation in float.  The nearest floats of
+// common angles all shrink the norm the same way (cos^2 + sin^2 - 1 is about
+// -3e-8 at 45 and 22.5 degrees), so that a circuit with hundreds of such gates
+// loses 1e-5 of its norm.  Among the pairs within one float step of the
+// nearest ones this takes the pair whose norm error brings the running sum of
+// the circuit's errors (drift) closest to zero (ties: the nearer pair), which
+// keeps the product of the constant gates' norms within one step's error of 1.
+void constant_pair(double th, double& drift, float& c, float& s) {
+  const double cd = std::cos(0.5 * th), sd = std::sin(0.5 * th);
+  const float c0 = (float)cd, s0 = (float)sd;
+  const float cs[3] = {std::nextafter(c0, -2.f), c0, std::nextafter(c0, 2.f)};
+  const float ss[3] = {std::nextafter(s0, -2.f), s0, std::nextafter(s0, 2.f)};
+  double best = -1.0, best_d = 0.0, best_e = 0.0;
+  for (float cc : cs)
+    for (float sc : ss) {
+      const double e = (double)cc * cc + (double)sc * sc - 1.0;
+      const double score = std::fabs(drift + e), d = std::fabs(cc - cd) + std::fabs(sc - sd);
+      if (best < 0.0 || score < best || (score == best && d < best_d)) {
+        best = score;
+        best_d = d;
+        best_e = e;
+        c = cc;
+        s = sc;
+      }
+    }
+  drift += best_e;
+}
+
 // Emits the primitives of one (validated) gate into plan.prims, with one
 // angle occurrence per rotation: m * (the gate's angle slot s) + a, or the
 // constant a when s < 0.
@@ -515,8 +543,10 @@ class Lowering {
       p_.occ_src.push_back(VQC_SRC_CONST);
       p_.occ_idx.push_back(0);
       p_.occ_slot.push_back(-1);
-      p_.occ_cs.push_back((float)std::cos(0.5 * th));
-      p_.occ_cs.push_back((float)std::sin(0.5 * th));
+      float c = 0.f, sn = 0.f;
+      constant_pair(th, p_.const_drift, c, sn);
+      p_.occ_cs.push_back(c);
+      p_.occ_cs.push_back(sn);
       p_.occ_ma.push_back(1.f);
       p_.occ_ma.push_back(0.f);
     } else {
@@ -730,6 +760,19 @@ void find_heads(Plan& plan) {
   }
 }
 
+// LDS of the streaming passes: exchange buffer | angle table | gradient
+// accumulators [slot][group] of the adjoint.
+void stream_lds(Plan& plan) {
+  const size_t xbuf = ((size_t)1 << plan.k) * 8;
+  plan.lds_tab = xbuf;
+  const size_t tab = align_up(plan.occ_src.size() * 8, 16);
+  plan.lds_acc = xbuf + tab;
+  const size_t groups_bwd = ((size_t)1 << (plan.k - plan.Rb)) / 64;
+  const size_t acc = align_up((size_t)plan.max_pass_slots * groups_bwd * 4, 16);
+  plan.lds_fwd = xbuf + tab;
+  plan.lds_bwd = xbuf + tab + acc;
+}
+
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
                Plan& plan, std::string& msg, bool lane_gates, int tile_qubits,
                int bwd_reg_bits) {
@@ -906,19 +949,54 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     plan.G = plan.WG / 64;
     rc = plan_stream_both(plan, msg);
     if (rc < 0) return rc;
-    const size_t xbuf = ((size_t)1 << plan.k) * 8;
-    plan.lds_tab = xbuf;
-    const size_t tab = align_up((size_t)n_occ * 8, 16);
-    plan.lds_acc = xbuf + tab;
-    const size_t groups_bwd = ((size_t)1 << (plan.k - plan.Rb)) / 64;
-    const size_t acc = align_up((size_t)plan.max_pass_slots * groups_bwd * 4, 16);
-    plan.lds_fwd = xbuf + tab;
-    plan.lds_bwd = xbuf + tab + acc;
+    stream_lds(plan);
   }
   if (std::max(plan.lds_bwd, plan.lds_step) > (size_t)kLdsBytes) {
     msg = "circuit too large for on-chip tables: " +
           std::to_string(std::max(plan.lds_bwd, plan.lds_step)) +
           " bytes of LDS needed (limit " + std::to_string(kLdsBytes) + ")";
+    return VQC_ERR_TOO_LARGE;
+  }
+  return 0;
+}
+
+// The streaming training step's plan: the passes of `full` planned again
+// without the heads' rotations.  Its first forward pass starts from the
+// product state after the heads, its last adjoint pass ends where the heads
+// end and contracts lambda against the heads' states (the per-tile partials of
+// the vectors v_q), and a last kernel sums those partials and takes the head
+// rotations' gradients.  Returns 1 (and leaves `step` unspecified) when the
+// circuit has no head rotation.
+int build_step_plan(const Plan& full, Plan& step, std::string& msg) {
+  if (full.path != VQC_PATH_STREAM) return 1;
+  std::vector<char> in_head(full.occ_src.size(), 0);
+  bool any = false;
+  for (const auto& hq : full.head)
+    for (const Prim& g : hq) {
+      if (g.occ >= 65536) return 1;  // the head tables hold 16-bit occurrence numbers
+      in_head[g.occ] = 1;
+      any = true;
+    }
+  if (!any || full.n > 64) return 1;  // one lane per qubit walks its head
+  step = full;
+  step.prims.clear();
+  for (const Prim& g : full.prims)
+    if (!(g.occ >= 0 && in_head[g.occ])) step.prims.push_back(g);
+  step.fwd.clear();
+  step.bwd.clear();
+  step.cols.clear();
+  step.maps.clear();
+  step.pslots.clear();
+  step.fpass.clear();
+  step.bpass.clear();
+  step.fwd_exchanges = step.bwd_exchanges = 0;
+  step.max_pass_slots = 0;
+  step.product_head = true;
+  const int rc = plan_stream_both(step, msg);
+  if (rc < 0) return rc;
+  stream_lds(step);
+  if (step.lds_bwd > (size_t)kLdsBytes) {
+    msg = "circuit too large for on-chip tables";
     return VQC_ERR_TOO_LARGE;
   }
   return 0;

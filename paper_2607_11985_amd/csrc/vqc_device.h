@@ -1203,6 +1203,10 @@ struct InterpSched {
   static constexpr bool kLoadTables = false;
   // a pass's flags other than PF_INIT when fixed at compile time, else -1
   static constexpr int kFixedFlags = -1;
+  // the training step's product head (generated passes only): the first
+  // forward pass starts from the product state, the last adjoint pass writes
+  // the head partials
+  static constexpr bool kProductStart = false, kHeadPartials = false;
   // physical bits of qubit q's measured Z-string under the mapping the epilogue /
   // lambda use (zm: the logical strings, or null for Z_q itself)
   __device__ __forceinline__ static uint32_t zmask(const uint8_t* phys, const uint32_t* zm,
@@ -1622,6 +1626,29 @@ __device__ __forceinline__ float wave_reduce16(const float (&v)[16], uint32_t la
 }
 #undef VQC_RS_PAIR
 
+// One head step on the qubit's state: (c I - i s P) phi, (c, s) the rotation's
+// exact (cos, sin)(theta / 2) (kind 3: no step).
+__device__ __forceinline__ void head_step(const Walk& w, uint32_t word, float2& fa, float2& fb) {
+  const uint32_t kind = word >> 16;
+  float2 cs = w.tab[word & 0xFFFFu];
+  if (kind == 3u) cs = make_float2(1.f, 0.f);
+  float2 pa, pb;
+  pauli2(kind, fa, fb, pa, pb);
+  fa = make_float2(fmaf(cs.x, fa.x, cs.y * pa.y), fmaf(cs.x, fa.y, -cs.y * pa.x));
+  fb = make_float2(fmaf(cs.x, fb.x, cs.y * pb.y), fmaf(cs.x, fb.y, -cs.y * pb.x));
+}
+
+// Lane q's head state phi_q (lanes of every wave; lanes >= n walk a clamped
+// copy whose values are not used).
+template <int L>
+__device__ __forceinline__ void head_state(const Walk& w, const HeadPre<L>& hp, float2& fa,
+                                           float2& fb) {
+  fa = make_float2(1.f, 0.f);
+  fb = make_float2(0.f, 0.f);
+#pragma unroll
+  for (int i = 0; i < L; ++i) head_step(w, hp.w[i], fa, fb);
+}
+
 // Lane q's walk through the head of qubit q (lanes of every wave do it; wave
 // 0 records each step's state in LDS): fa, fb end as the qubit's state.
 template <int L>
@@ -1633,14 +1660,8 @@ __device__ __forceinline__ void head_walk(const Walk& w, const HeadPre<L>& hp, H
   fb = make_float2(0.f, 0.f);
 #pragma unroll
   for (int i = 0; i < L; ++i) {
-    const uint32_t word = hp.w[i], kind = word >> 16;
-    float2 cs = w.tab[word & 0xFFFFu];  // (cos, sin)(theta / 2), exact for head steps
-    if (kind == 3u) cs = make_float2(1.f, 0.f);
-    float2 pa, pb;
-    pauli2(kind, fa, fb, pa, pb);
-    // (c I - i s P) phi
-    fa = make_float2(fmaf(cs.x, fa.x, cs.y * pa.y), fmaf(cs.x, fa.y, -cs.y * pa.x));
-    fb = make_float2(fmaf(cs.x, fb.x, cs.y * pb.y), fmaf(cs.x, fb.y, -cs.y * pb.x));
+    const uint32_t word = hp.w[i];
+    head_step(w, word, fa, fb);
     if (writer) {
       HeadRec r;
       r.phi = make_float4(fa.x, fa.y, fb.x, fb.y);
@@ -1652,6 +1673,55 @@ __device__ __forceinline__ void head_walk(const Walk& w, const HeadPre<L>& hp, H
     }
   }
   if (writer) fin[lane] = make_float4(fa.x, fa.y, fb.x, fb.y);
+}
+
+// Lane q's walk back through its head from mu = v_q = (m0, m1): at every step
+// (last first) the rotation's gradient Im <mu|P|phi>, phi the recorded state
+// after it, goes to emit(i, record, gradient); then mu <- (c I + i s P) mu.
+template <int L, typename Emit>
+__device__ __forceinline__ void head_back(const Walk& w, const HeadRec* rec, int q, float2 m0,
+                                          float2 m1, Emit&& emit) {
+#pragma unroll
+  for (int i = L - 1; i >= 0; --i) {
+    const HeadRec r = rec[q * L + i];
+    const uint32_t kind = r.word >> 16;
+    if (kind == 3u) continue;
+    const float2 cs = w.tab[r.word & 0xFFFFu];
+    float2 p0, p1;
+    pauli2(kind, make_float2(r.phi.x, r.phi.y), make_float2(r.phi.z, r.phi.w), p0, p1);
+    // Im(conj(mu_0) (P phi)_0 + conj(mu_1) (P phi)_1)
+    const float g = fmaf(m0.x, p0.y, -m0.y * p0.x) + fmaf(m1.x, p1.y, -m1.y * p1.x);
+    emit(i, r, g);
+    float2 q0, q1;
+    pauli2(kind, m0, m1, q0, q1);
+    m0 = make_float2(fmaf(cs.x, m0.x, -cs.y * q0.y), fmaf(cs.x, m0.y, cs.y * q0.x));
+    m1 = make_float2(fmaf(cs.x, m1.x, -cs.y * q1.y), fmaf(cs.x, m1.y, cs.y * q1.x));
+  }
+}
+
+// Sums of the per-thread values v[0 .. NV) over the workgroup (each wave by
+// wave_reduce16, then the waves through the exchange buffer, in a fixed
+// order): thread j < NV gets sum j.  Every thread calls it; it starts with a
+// barrier (the exchange buffer may still be in use) and ends with one.
+template <int WG, int NV>
+__device__ __forceinline__ float workgroup_sums(const float (&v)[NV], float* red) {
+  const uint32_t lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < NV / 16; ++c) {
+    float x16[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) x16[j] = v[16 * c + j];
+    const float tot = wave_reduce16(x16, lane);
+    if (lane < 16u) red[wave * NV + 16 * c + (int)lane] = tot;
+  }
+  __syncthreads();
+  float s = 0.f;
+  if ((int)threadIdx.x < NV)
+    for (int g = 0; g < WG / 64; ++g) s += red[g * NV + threadIdx.x];
+  __syncthreads();
+  return s;
 }
 
 // The head gradients from the per-thread 2-vector partials v[4 q .. 4 q + 3]
@@ -1683,24 +1753,47 @@ __device__ __forceinline__ void head_finish(const float (&v)[NV], const Walk& w,
     s.z += red[g * NV + 4 * q + 2];
     s.w += red[g * NV + 4 * q + 3];
   }
-  float2 m0 = make_float2(s.x, s.y), m1 = make_float2(s.z, s.w);
-#pragma unroll
-  for (int i = L - 1; i >= 0; --i) {
-    const HeadRec r = rec[q * L + i];
-    const uint32_t kind = r.word >> 16;
-    if (kind == 3u) continue;
-    const float2 cs = w.tab[r.word & 0xFFFFu];
-    float2 p0, p1;
-    pauli2(kind, make_float2(r.phi.x, r.phi.y), make_float2(r.phi.z, r.phi.w), p0, p1);
-    // Im(conj(mu_0) (P phi)_0 + conj(mu_1) (P phi)_1)
-    const float g = fmaf(m0.x, p0.y, -m0.y * p0.x) + fmaf(m1.x, p1.y, -m1.y * p1.x);
-    if (r.slot1 > 0) atomicAdd(&w.acc[(r.slot1 - 1) * w.G], g * r.mul);
-    // mu <- (c I + i s P) mu, the rotation undone
-    float2 q0, q1;
-    pauli2(kind, m0, m1, q0, q1);
-    m0 = make_float2(fmaf(cs.x, m0.x, -cs.y * q0.y), fmaf(cs.x, m0.y, cs.y * q0.x));
-    m1 = make_float2(fmaf(cs.x, m1.x, -cs.y * q1.y), fmaf(cs.x, m1.y, cs.y * q1.x));
+  head_back<L>(w, rec, q, make_float2(s.x, s.y), make_float2(s.z, s.w),
+               [&](int, const HeadRec& r, float g) {
+                 if (r.slot1 > 0) atomicAdd(&w.acc[(r.slot1 - 1) * w.G], g * r.mul);
+               });
+}
+
+// The streaming training step's head gradients: one 64-thread workgroup per
+// sample, after its last adjoint pass.  v_q is the sum of the sample's tiles'
+// partials (in tile order); lane q walks qubit q's head forward (recording
+// the states) and back, writing each rotation's gradient times its chain-rule
+// factor to LDS; then each gradient slot of a head rotation adds the sum of
+// its terms (a fixed list per slot, H::add_grads) to the partial row of the
+// sample's first tile, which the gradient reduction reads.
+template <typename H>
+__device__ __forceinline__ void head_finish_stream(const PassArgs& A, unsigned char* smem) {
+  constexpr int L = H::kL, NV = H::kNV, N = H::kN;
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.x;
+  Walk w;
+  w.tab = reinterpret_cast<const float2*>(A.tabs) + b * A.n_occ;  // exact (cos, sin) of heads
+  HeadRec* rec = reinterpret_cast<HeadRec*>(smem);
+  float4* fin = reinterpret_cast<float4*>(smem + N * L * 32);
+  float* vs = reinterpret_cast<float*>(smem + N * L * 32 + N * 16);
+  float* gs = vs + NV;  // [n][L]
+  const HeadPre<L> hp = H::head_pre(tid);
+  float2 fa, fb;
+  head_walk<L>(w, hp, rec, fin, N, fa, fb);
+  const int64_t row0 = b << A.ng;
+  for (int j = tid; j < NV; j += 64) {
+    float s = 0.f;
+    for (int g = 0; g < (1 << A.ng); ++g) s += A.vpart[(row0 + g) * NV + j];
+    vs[j] = s;
   }
+  for (int j = tid; j < N * L; j += 64) gs[j] = 0.f;
+  __syncthreads();
+  if (tid < N)
+    head_back<L>(w, rec, tid, make_float2(vs[4 * tid], vs[4 * tid + 1]),
+                 make_float2(vs[4 * tid + 2], vs[4 * tid + 3]),
+                 [&](int i, const HeadRec& r, float g) { gs[tid * L + i] = g * r.mul; });
+  __syncthreads();
+  H::add_grads(gs, A.gpart + row0 * A.n_slots, tid);
 }
 
 template <int WG, int R, typename FS, typename BS, typename HD = NoHead>
@@ -1892,12 +1985,16 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   const size_t sbase = (size_t)b << (A.k + A.ng);
   St<R> a, l;
   if (!BWD && (flags & PF_INIT)) {
+    if constexpr (Sched::kProductStart) {
+      Sched::template product_start<R>(a, w);  // the state after the heads
+    } else {
 #pragma unroll
-    for (int j = 0; j < NA; ++j) {
-      a.r[j] = 0.f;
-      a.i[j] = 0.f;
+      for (int j = 0; j < NA; ++j) {
+        a.r[j] = 0.f;
+        a.i[j] = 0.f;
+      }
+      if (tid == 0 && g == 0) a.r[0] = 1.f;
     }
-    if (tid == 0 && g == 0) a.r[0] = 1.f;
   } else {
     const float2* src = reinterpret_cast<const float2*>(A.psi_src) + sbase;
     load_tile<R>(a, src, base, off);
@@ -1929,6 +2026,10 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
       float2* dst = reinterpret_cast<float2*>(A.lam_dst) + sbase;
 #pragma unroll
       for (int j = 0; j < NA; ++j) dst[base ^ off[j]] = make_float2(l.r[j], l.i[j]);
+    }
+    if constexpr (Sched::kHeadPartials) {
+      // lambda where the heads end, contracted against the heads' states
+      if (flags & PF_LAST_ADJ) Sched::template head_partials<WG, R>(l, w, A.vpart + blk * Sched::kNV);
     }
     __syncthreads();
     float* gp = A.gpart + blk * A.n_slots;

@@ -60,10 +60,14 @@ struct Plan {
   // generated training step builds directly (and whose gradients it takes from
   // lambda contracted against the other qubits' states).
   std::vector<std::vector<Prim>> head;
+  // Streaming training step plan: prims leave out the heads' rotations (the
+  // first forward pass starts from the product state after them).
+  bool product_head = false;
   std::vector<int32_t> occ_src, occ_idx, occ_slot;
   std::vector<float> occ_cs;              // 2 per occurrence
   std::vector<float> occ_ma;              // 2 per occurrence: angle = mul * value + add
   bool affine = false;                    // some occurrence has (mul, add) != (1, 0)
+  double const_drift = 0.0;               // sum of the constants' cos^2 + sin^2 - 1 (planning)
   std::vector<uint32_t> fwd, bwd;         // instruction pairs
   std::vector<uint32_t> cols;             // exchange / tile I/O column tables
   std::vector<uint8_t> maps;              // logical -> phys tables (nq bytes each)
@@ -91,6 +95,9 @@ constexpr int kNumGateKinds = 32;  // VQC_RX .. VQC_CSWAP
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
                Plan& plan, std::string& msg, bool lane_gates, int tile_qubits = 0,
                int bwd_reg_bits = 0);
+// The streaming training step's plan without the heads' rotations (planner.cpp).
+// Returns 0, 1 when the circuit has no head rotation, or a VQC_ERR_* code.
+int build_step_plan(const Plan& full, Plan& step, std::string& msg);
 // OpenQASM front end (qasm.cpp).  Returns 0 or a VQC_ERR_* code with msg.
 int parse_qasm(const char* source, const char* input_names, std::vector<vqc_op>& ops,
                int& n_qubits, int& n_params, int& n_inputs, std::string& msg);
@@ -129,12 +136,14 @@ struct JitKernels {
   void* res_step = nullptr;           // forward, loss head and adjoint in one launch
   std::vector<void*> pass_fwd, pass_bwd;
   void* tables = nullptr;             // streaming: the per-sample table kernel, or none
+  void* head_finish = nullptr;        // streaming step with a product head: head gradients
 };
 constexpr int kTableThreads = 256;    // threads of the table kernel's workgroups
 struct JitUnit {
   std::string name, src;
 };
 std::vector<JitUnit> jit_units(const Plan& plan);
+bool stream_tables_fit(const Plan& plan);
 int jit_compile_only(const Plan& plan, std::string& log);
 // hiprtc compilation of one generated kernel (jit_compile.cpp)
 int compile_source(const std::string& src, std::vector<char>& code, std::string& log);

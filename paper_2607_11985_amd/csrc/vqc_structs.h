@@ -156,5 +156,8 @@ struct PassArgs {
   float* tabs;
   float* gsig;
   float* esig;
+  // training step with a product head: per tile of the last adjoint pass the
+  // partial sums of the 2-vectors v_q [B * 2^ng][NV] (NV = 4 n rounded up to 16)
+  float* vpart;
 };
 }  // namespace vqc

@@ -347,3 +347,35 @@ def test_tile_qubits_option():
         assert info["path"] == 2
         _lib.vqc_jit_check(h)
         _lib.vqc_destroy(h)
+
+
+@pytest.mark.parametrize("idx,heads", [(4, 42), (5, 64)])
+def test_streaming_step_plan(idx, heads):
+    """The streaming training step's own plan: it leaves out every qubit's head
+    (RY encoding and the first layer's rotations here), so that its passes run
+    the other rotations only; the inference forward keeps the whole circuit."""
+    w = W.make_config(idx, batch=2)
+    rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    assert rc == 0, _lib.vqc_last_error()
+    info = _lib.vqc_circuit_info(h)
+    assert info["path"] == 2
+    assert info["step_head_rotations"] == heads
+    assert 1 <= info["step_fwd_passes"] <= info["fwd_passes"]
+    assert info["step_bwd_passes"] == info["step_fwd_passes"]
+    _lib.vqc_jit_check(h)
+    _lib.vqc_destroy(h)
+
+
+def test_no_step_plan_without_heads_or_generated_kernels():
+    n = 14
+    ops, P, F = W.random_circuit(n, 5 * n, seed=77)
+    lead = [W.Op("CZ", (q, q + 1)) for q in range(0, n - 1, 2)]
+    for o, engine, want in ((ops, 0, True), (lead + ops, 0, False), (ops, 1, False)):
+        rc, h = host_compile(o, n, P, F, engine=engine)
+        assert rc == 0, _lib.vqc_last_error()
+        assert (_lib.vqc_circuit_info(h)["step_head_rotations"] > 0) == want
+        _lib.vqc_destroy(h)
+    w = W.make_config(2, batch=2)  # resident: the step kernel builds its heads itself
+    rc, h = host_compile(w.ops, w.n_qubits, w.n_params, w.n_inputs)
+    assert _lib.vqc_circuit_info(h)["step_head_rotations"] == 0
+    _lib.vqc_destroy(h)

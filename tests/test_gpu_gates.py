@@ -194,3 +194,35 @@ def test_cnot_on_every_qubit_pair(torch_mod, n):
         r = gpu_run(torch_mod, ops, n, P, F, params, inputs, cot, reg_bits=reg_bits)
         check_E(r["E"], Er)
         check_grads(r, dpr, dxr, cot)
+
+
+@pytest.mark.parametrize("n,path", [(8, "auto"), (14, "stream")])
+def test_many_constant_gates_keep_the_norm(torch_mod, n, path):
+    """Hundreds of fixed gates (H, S, T, SX, Toffolis), each followed by its
+    inverse, on a basis state: every <Z_q> is exactly +-1, and the GPU's is
+    +-(the state's norm squared).  The float (cos, sin) pairs of the gates'
+    angles are picked so that their norm errors cancel over the circuit; the
+    nearest floats of these angles all shrink the norm, by about 5e-8 per
+    rotation, which would put <Z> 1e-5 off after a few hundred."""
+    torch = torch_mod
+    rng = np.random.default_rng(27000 + n)
+    ops = [W.Op("RY", (q,), (("param", q),)) for q in range(n)]
+    inverse = {"H": "H", "S": "SDG", "SDG": "S", "T": "TDG", "TDG": "T", "SX": "SXDG",
+               "SXDG": "SX"}
+    kinds = sorted(inverse)
+    for _ in range(30 * n):
+        if rng.random() < 0.1:
+            a, b, c = (int(v) for v in rng.choice(n, size=3, replace=False))
+            ops += [W.Op("CCX", (a, b, c)), W.Op("CCX", (a, b, c))]
+        else:
+            k, q = kinds[int(rng.integers(len(kinds)))], int(rng.integers(n))
+            ops += [W.Op(k, (q,)), W.Op(inverse[k], (q,))]
+    P, F, B = n, 1, 2
+    params = np.zeros((B, P), dtype=np.float32)  # |0...0> and |1...1>
+    params[1] = np.float32(np.pi)
+    inputs = np.zeros((B, F), dtype=np.float32)
+    note(f"constant gates n={n} path={path} ops={len(ops)}")
+    r = gpu_run(torch, ops, n, P, F, params, inputs, None, path=path)
+    Er = oracle.forward(ops, n, params, inputs)
+    assert np.allclose(np.abs(Er), 1.0, atol=1e-9)
+    check_E(r["E"], Er)

@@ -31,9 +31,13 @@ def test_split_step_equals_separate_calls(torch_mod, n, B, loss, shared):
     torch = torch_mod
     from paper_2607_11985_amd.api import Circuit
     ops, P, F = W.random_circuit(n, 12 * n, seed=21000 + n + B)
+    # every qubit starts with an entangler: no head, so that the step runs the
+    # same passes as the separate calls (test_gpu_stream_head covers heads)
+    ops = [W.Op("CZ", (q, (q + 1) % n)) for q in range(0, n, 2)] + ops
     params, inputs = W.random_inputs(B, P, F, seed=21100 + n + B)
     y = np.random.default_rng(21200 + B).uniform(-1, 1, size=B).astype(np.float32)
     c = Circuit(ops, n, P, F, path="stream", shared_params=shared)
+    assert c.info()["step_head_rotations"] == 0
     note(f"split step n={n} B={B} loss={loss} shared={shared} tiles={c.info()['tile_qubits']}")
     p = torch.from_numpy(np.ascontiguousarray(params[0] if shared else params)).cuda()
     x = torch.from_numpy(inputs).cuda()
