@@ -1193,7 +1193,7 @@ std::string stream_head_partials(const Plan& p, int map_off, int R) {
 // The streaming training step's head gradient kernel (head_finish_stream): its
 // Head struct holds the head tables and, per gradient slot of a head rotation,
 // the list of its (qubit, step) terms.
-std::string head_finish_unit(const Plan& p) {
+std::string head_finish_unit(const Plan& p, const std::string& name) {
   std::ostringstream o;
   const int L = head_len(p), n = p.n, NV = head_nv(p);
   o << "#include \"vqc_device.h\"\nnamespace vqc {\nstruct Head {\n"
@@ -1222,7 +1222,8 @@ std::string head_finish_unit(const Plan& p) {
     << "  }\n}\n"
     << "};\n}  // namespace vqc\n";
   const size_t lds = (size_t)n * L * 32 + (size_t)n * 16 + (size_t)(NV + n * L) * 4;
-  o << "extern \"C\" __global__ void __launch_bounds__(64) vqc_sh(const vqc::PassArgs A) {\n"
+  o << "extern \"C\" __global__ void __launch_bounds__(64) " << name
+    << "(const vqc::PassArgs A) {\n"
     << "  __shared__ __align__(16) unsigned char smem[" << lds_size(lds) << "];\n"
     << "  vqc::head_finish_stream<vqc::Head>(A, smem);\n}\n";
   return o.str();
@@ -1279,7 +1280,7 @@ std::string step_unit(const Plan& p, const Frame& fr) {
 // LDS (the passes then compute their own).
 // With a product head the head rotations keep their exact (cos, sin) and
 // take no part in the frame.
-std::string table_unit(const Plan& p, const Frame& fr) {
+std::string table_unit(const Plan& p, const Frame& fr, const std::string& name = "vqc_st") {
   TanMode t;
   const int nocc = (int)p.occ_src.size();
   t.W = std::max(1, (nocc + 31) / 32);
@@ -1308,7 +1309,7 @@ std::string table_unit(const Plan& p, const Frame& fr) {
   emit_tables(o, p, t, fr, kTableThreads, true, false, head.empty() ? nullptr : &head);
   o << "};\n}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << kTableThreads
-    << ") vqc_st(const vqc::PassArgs A) {\n"
+    << ") " << name << "(const vqc::PassArgs A) {\n"
     << "  __shared__ __align__(16) unsigned char smem[" << t.end << "];\n"
     << "  vqc::table_body<" << kTableThreads << ", vqc::Sched>(A, smem);\n}\n";
   return o.str();
@@ -1320,38 +1321,41 @@ std::vector<JitUnit> jit_units(const Plan& p) {
   if (p.path == VQC_PATH_RESIDENT) {
     u.push_back({"vqc_rf", kernel_unit(p, fr, "vqc_rf", p.fwd.data(), (int)p.fwd.size() / 2,
                                        false, false, p.R, p.S, p.WG, p.lds_fwd, p.P + p.F, true,
-                                       p.end_off)});
+                                       p.end_off), 'r'});
     u.push_back({"vqc_rb", kernel_unit(p, fr, "vqc_rb", p.bwd.data(), (int)p.bwd.size() / 2,
                                        true, false, p.R, p.S, p.WG, p.lds_bwd, p.P + p.F, true,
-                                       p.end_off)});
-    u.push_back({"vqc_rs", step_unit(p, fr)});
+                                       p.end_off), 'b'});
+    u.push_back({"vqc_rs", step_unit(p, fr), 's'});
     return u;
   }
-  const std::string tables = table_unit(p, fr);
+  // the training step's plan with a product head: vqc_hf* / vqc_hb* / vqc_ht /
+  // vqc_hg, apart in traces from the whole circuit's vqc_sf* / vqc_sb* / vqc_st
+  const std::string pre = p.product_head ? "vqc_h" : "vqc_s";
+  const std::string tables = table_unit(p, fr, pre + "t");
   const bool load = !tables.empty();
   const bool ph = p.product_head && load;  // the heads' exact angles come from the tables
   for (size_t i = 0; i < p.fpass.size(); ++i) {
-    const std::string name = "vqc_sf" + std::to_string(i);
+    const std::string name = pre + "f" + std::to_string(i);
     const PassPlan& pp = p.fpass[i];
     const std::string head = ph && (pp.flags & PF_INIT)
                                  ? stream_product_start(p, pp.start_off, p.Rf) : std::string();
     u.push_back({name, kernel_unit(p, fr, name, p.fwd.data() + 2 * pp.ins_off, pp.n_ins, false,
                                    true, p.Rf, 1, 1 << (p.k - p.Rf), p.lds_fwd, pp.n_slots,
                                    (pp.flags & PF_ZPART) != 0, pp.end_off, load,
-                                   (int)(pp.flags & ~PF_INIT), head)});
+                                   (int)(pp.flags & ~PF_INIT), head), 'F'});
   }
   for (size_t i = 0; i < p.bpass.size(); ++i) {
-    const std::string name = "vqc_sb" + std::to_string(i);
+    const std::string name = pre + "b" + std::to_string(i);
     const PassPlan& pp = p.bpass[i];
     const std::string head = ph && (pp.flags & PF_LAST_ADJ)
                                  ? stream_head_partials(p, pp.end_off, p.Rb) : std::string();
     u.push_back({name, kernel_unit(p, fr, name, p.bwd.data() + 2 * pp.ins_off, pp.n_ins, true,
                                    true, p.Rb, 1, 1 << (p.k - p.Rb), p.lds_bwd, pp.n_slots,
                                    (pp.flags & PF_MAKE_LAMBDA) != 0, pp.start_off, load,
-                                   (int)(pp.flags & ~PF_INIT), head)});
+                                   (int)(pp.flags & ~PF_INIT), head), 'B'});
   }
-  if (load) u.push_back({"vqc_st", tables});
-  if (ph) u.push_back({"vqc_sh", head_finish_unit(p)});
+  if (load) u.push_back({pre + "t", tables, 'T'});
+  if (ph) u.push_back({"vqc_hg", head_finish_unit(p, "vqc_hg"), 'G'});
   return u;
 }
 
@@ -1576,14 +1580,16 @@ int jit_build(const Plan& p, int device, JitKernels& out, std::string& msg) {
   }
   out = JitKernels();
   for (size_t i = 0; i < units.size(); ++i) {
-    const std::string& nm = units[i].name;
-    if (nm == "vqc_rf") out.res_fwd = fns[i];
-    else if (nm == "vqc_rb") out.res_bwd = fns[i];
-    else if (nm == "vqc_rs") out.res_step = fns[i];
-    else if (nm == "vqc_st") out.tables = fns[i];
-    else if (nm == "vqc_sh") out.head_finish = fns[i];
-    else if (nm.compare(0, 6, "vqc_sf") == 0) out.pass_fwd.push_back(fns[i]);
-    else if (nm.compare(0, 6, "vqc_sb") == 0) out.pass_bwd.push_back(fns[i]);
+    switch (units[i].role) {
+      case 'r': out.res_fwd = fns[i]; break;
+      case 'b': out.res_bwd = fns[i]; break;
+      case 's': out.res_step = fns[i]; break;
+      case 'T': out.tables = fns[i]; break;
+      case 'G': out.head_finish = fns[i]; break;
+      case 'F': out.pass_fwd.push_back(fns[i]); break;
+      case 'B': out.pass_bwd.push_back(fns[i]); break;
+      default: break;
+    }
   }
   return VQC_OK;
 }

@@ -709,25 +709,46 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // adjoint starts from lambda = (sum_j g_j T^dag Z_j T) psi.  (The tangent
 // form's frame rows still propagate through the tail: they describe the final
 // state.)
+//
+// Diagonal gates (RZ, CZ) that commute with every gate kept after them are
+// dropped: moved to the end they act on a state whose every output is
+// diagonal in the computational basis (<Z>-strings and probabilities), so
+// neither the outputs nor any other gate's gradient change, and their own
+// gradients are zero (Im <psi| H |psi> = 0 for the diagonal Hermitian H the
+// adjoint pairs them with).  A diagonal gate commutes with diagonal gates and
+// CNOT controls; RX, RY and CNOT targets on its qubits block it.  One
+// backward scan decides both, each gate against the final form of the gates
+// after it (kept ones in place, folded ones at the end, dropped ones gone).
 void fold_trailing_entanglers(Plan& plan) {
+  // 0 keep, 1 tail (folded into the measurement), 2 dropped
   std::vector<char> tail(plan.prims.size(), 0);
-  uint32_t blocked = 0;
+  uint32_t blocked = 0;  // lines of a later kept gate (the fold rule)
+  uint32_t noncomm = 0;  // qubits of a later kept RX, RY or CNOT target (the drop rule)
   bool any = false;
   for (size_t i = plan.prims.size(); i-- > 0;) {
     const Prim& g = plan.prims[i];
     const uint32_t lines = lines_of(g);
-    if ((g.kind == P_CNOT || g.kind == P_CZ) && !(blocked & lines)) {
+    const bool diagonal = g.kind == P_RZ || g.kind == P_CZ;
+    if (diagonal && !(noncomm & lines)) {
+      tail[i] = 2;
+      any = true;
+    } else if (g.kind == P_CNOT && !(blocked & lines)) {
       tail[i] = 1;
       any = true;
     } else {
       blocked |= lines;
+      if (g.kind == P_RX || g.kind == P_RY) noncomm |= lines;
+      if (g.kind == P_CNOT) noncomm |= 1u << g.q1;
     }
   }
   if (!any) return;
   std::vector<Prim> body;
-  for (size_t i = 0; i < plan.prims.size(); ++i)
-    (tail[i] ? plan.tail : body).push_back(plan.prims[i]);
+  for (size_t i = 0; i < plan.prims.size(); ++i) {
+    if (tail[i] == 0) body.push_back(plan.prims[i]);
+    else if (tail[i] == 1) plan.tail.push_back(plan.prims[i]);
+  }
   plan.prims.swap(body);
+  if (plan.tail.empty()) return;
   plan.zmask.assign(plan.n, 0u);
   for (int j = 0; j < plan.n; ++j) {
     uint32_t m = 1u << j;

@@ -141,6 +141,9 @@ struct JitKernels {
 constexpr int kTableThreads = 256;    // threads of the table kernel's workgroups
 struct JitUnit {
   std::string name, src;
+  // what the kernel is: resident forward / adjoint / step ('r', 'b', 's'),
+  // streaming forward pass / adjoint pass / tables / head gradients ('F', 'B', 'T', 'G')
+  char role;
 };
 std::vector<JitUnit> jit_units(const Plan& plan);
 bool stream_tables_fit(const Plan& plan);

@@ -72,7 +72,9 @@ def test_configs_plan_on_host(idx):
     # forward and backward sweep each hold one instruction per primitive plus
     # exchanges, except the trailing entanglers (no rotation after them on their
     # qubits), which the measurement absorbs: here the last layer's CNOT ring / CZ
-    # chain
+    # chain; and except the diagonal gates that commute with every gate after
+    # them: here every qubit's last RZ (each layer ends in RZ before its
+    # entanglers)
     blocked, trailing = set(), 0
     for o in reversed(w.ops):
         if o.kind in ("CNOT", "CZ") and not blocked & set(o.wires):
@@ -80,7 +82,12 @@ def test_configs_plan_on_host(idx):
         else:
             blocked |= set(o.wires)
     assert trailing == (w.n_qubits - 1 if idx == 4 else w.n_qubits)
-    n_prims = sum(3 if o.kind == "ROT" else 1 for o in w.ops) - trailing
+    last = {}
+    for o in w.ops:
+        if o.kind not in ("CNOT", "CZ"):
+            last[o.wires[0]] = o.kind
+    assert all(k in ("RZ", "ROT") for k in last.values())
+    n_prims = sum(3 if o.kind == "ROT" else 1 for o in w.ops) - trailing - w.n_qubits
     assert info["fwd_instructions"] == n_prims + info["fwd_exchanges"]
     assert info["bwd_instructions"] == n_prims + info["bwd_exchanges"]
     assert _lib.vqc_workspace_bytes(h, 0, 1) == 0

@@ -163,13 +163,14 @@ def test_train_step_parity(torch_mod, n, loss, path, engine):
     torch.cuda.synchronize()
     E, dp, dx, g = (t.cpu().numpy() for t in (E, dp, dx, g))
     check_step(E, g, dp, dx, ops, n, params, inputs, y.astype(np.float64), loss, B)
-    # the separate calls give the same results (up to the compiler's rounding)
+    # the separate calls give the same results up to rounding (the step builds
+    # the state after the heads as a product instead of running their gates)
     E2, ws = c.forward(p, x, training=True)
     g2 = loss_grad(loss, E2, yt)
     dp2, dx2 = c.backward(p, x, g2, ws)
     torch.cuda.synchronize()
-    assert np.max(np.abs(E2.cpu().numpy() - E)) <= 1e-6
-    assert np.max(np.abs(g2.cpu().numpy() - g)) <= 1e-6
+    assert np.max(np.abs(E2.cpu().numpy() - E)) <= 2e-6
+    assert np.max(np.abs(g2.cpu().numpy() - g)) <= 2e-6
     check_grads({"dp": dp2.cpu().numpy(), "dx": dx2.cpu().numpy()}, dp, dx, g)
 
 

@@ -20,7 +20,6 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2607_11985_amd", "csrc")
-OUT = os.path.join(ROOT, "tests", "sanitize", "_build")
 SAN = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-fno-sanitize-recover=all",
        "-g", "-O1"]
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
@@ -39,12 +38,12 @@ def _env(extra):
 
 
 @pytest.fixture(scope="module")
-def harness():
+def harness(tmp_path_factory):
     from paper_2607_11985_amd.build import BUILD, write_embedded_headers
-    # a directory per process: parallel test workers must not overwrite an
+    # a directory of this test process's own (pytest's temporary directories,
+    # outside the repository): parallel test workers must not overwrite an
     # executable another one runs
-    out = os.path.join(OUT, str(os.getpid()))
-    os.makedirs(out, exist_ok=True)
+    out = str(tmp_path_factory.mktemp("sanitize"))
     os.makedirs(BUILD, exist_ok=True)
     srcs = [os.path.join(ROOT, "tests", "sanitize", "host_harness.cpp"),
             write_embedded_headers()] + \
@@ -98,10 +97,8 @@ print("oracle ok")
 """
 
 
-def test_oracle_under_sanitizers():
-    out = os.path.join(OUT, str(os.getpid()))
-    os.makedirs(out, exist_ok=True)
-    lib = os.path.join(out, "liboracle_san.so")
+def test_oracle_under_sanitizers(tmp_path):
+    lib = str(tmp_path / "liboracle_san.so")
     _run(["gcc", "-std=c99", "-fopenmp", "-fPIC", "-shared"] + SAN +
          ["-o", lib, os.path.join(ROOT, "oracle", "vqc_oracle.c"), "-lm"])
     asan = subprocess.run(["gcc", "-print-file-name=libasan.so"], capture_output=True,
