@@ -366,13 +366,23 @@ int on_two_streams(const vqc_circuit* c, int64_t batch, void* stream, F&& f) {
   return rc1;
 }
 
+// The training step's additions to its forward: the loss head (its cotangent
+// rows computed with the <Z> reduction) and the adjoint's gradient partials,
+// cleared by the table kernel.
+struct StepHead {
+  int32_t kind;
+  int64_t norm;
+  const float* target;
+  float* cot;
+};
+
 // Streaming forward: every pass (the first starts from |0...0> or reads psi0),
 // then the <Z> reduction into expvals; the last pass writes probs.  fd_slots > 0:
 // the batch is the central differences' shifted copies of slots fd_base ..
 int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
                    float* expvals, unsigned char* ws, void* stream, bool keep,
                    const void* psi0 = nullptr, float* probs = nullptr, int fd_base = 0,
-                   int fd_slots = 0, float fd_h = 0.f) {
+                   int fd_slots = 0, float fd_h = 0.f, const StepHead* step = nullptr) {
   const Plan& p = c->plan;
   const StreamLayout L = stream_layout(p, batch);
   int rc = 0;
@@ -396,7 +406,9 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     a.fd_h = fd_h;
     a.epart = reinterpret_cast<float*>(ws + L.epart);
     if (i == 0) {
-      rc = launch_tables(c, a, batch, stream);
+      vqc::PassArgs t = a;
+      if (step) t.gpart = reinterpret_cast<float*>(ws + L.gpart);
+      rc = launch_tables(c, t, batch, stream);
       if (rc) return hip_fail("table kernel launch", rc);
     }
     rc = c->engine == VQC_ENGINE_JIT
@@ -406,22 +418,30 @@ int stream_forward(const vqc_circuit* c, int64_t batch, const float* params, con
     if (rc) return hip_fail("forward pass launch", rc);
   }
   if (!expvals) return VQC_OK;
-  rc = vqc::launch_reduce_e(batch, p.ng, p.n, reinterpret_cast<const float*>(ws + L.epart),
-                            expvals, stream);
+  const float* epart = reinterpret_cast<const float*>(ws + L.epart);
+  rc = step ? vqc::launch_reduce_e_loss(batch, p.ng, p.n, epart, expvals, step->kind, step->norm,
+                                        step->target, step->cot, stream)
+            : vqc::launch_reduce_e(batch, p.ng, p.n, epart, expvals, stream);
   if (rc) return hip_fail("expectation reduction launch", rc);
   return VQC_OK;
 }
 
-// Streaming adjoint: clear the partials, every pass (the first reads the saved
-// psi_G and leaves it intact), then the reduction into dparams / dinputs.
+// Streaming adjoint: clear the partials (the table kernel does, when there is
+// one), every pass (the first reads the saved psi_G and leaves it intact), then
+// the reduction into dparams / dinputs (with a product head: the head
+// kernel's).  prepared: the training step's forward wrote this call's tables
+// and cleared the partials.
 int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, const float* inputs,
-                    const float* grad_out, unsigned char* ws, float* dp, float* dx, void* stream) {
+                    const float* grad_out, unsigned char* ws, float* dp, float* dx, void* stream,
+                    bool prepared = false) {
   const Plan& p = c->plan;
   const StreamLayout L = stream_layout(p, batch);
   float* gpart = reinterpret_cast<float*>(ws + L.gpart);
-  int rc = vqc::launch_fill_zero(gpart, (batch << p.ng) * (int64_t)(p.P + p.F), stream);
-  if (rc) return hip_fail("gradient partial clear", rc);
-  bool first = true;
+  int rc = 0;
+  if (!prepared && !c->jit.tables &&
+      (rc = vqc::launch_fill_zero(gpart, (batch << p.ng) * (int64_t)(p.P + p.F), stream)))
+    return hip_fail("gradient partial clear", rc);
+  bool first = !prepared;
   for (const vqc::PassPlan& pp : p.bpass) {
     vqc::PassArgs a = pass_args(c, pp, true, batch);
     const size_t j = &pp - p.bpass.data();
@@ -447,14 +467,16 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     first = false;
   }
   if (p.product_head) {
-    // the heads' gradients into the partials of each sample's first tile
+    // the heads' gradients, and every slot's sum over the tiles, into the rows
     vqc::PassArgs a = pass_args(c, p.bpass.back(), true, batch);
     a.gpart = gpart;
     a.vpart = reinterpret_cast<float*>(ws + L.vpart);
+    a.dparams = dp;
+    a.dinputs = dx;
     set_tables(a, ws, L);
     rc = c->jit.head_finish ? vqc::jit_launch(c->jit.head_finish, batch, 64, &a, sizeof(a), stream)
                             : (int)hipErrorInvalidDeviceFunction;
-    if (rc) return hip_fail("head gradient launch", rc);
+    return rc ? hip_fail("head gradient launch", rc) : VQC_OK;
   }
   rc = vqc::launch_reduce_grad(batch, p.ng, p.P + p.F, p.P, p.F, gpart, dp, dx, stream);
   if (rc) return hip_fail("gradient reduction launch", rc);
@@ -826,11 +848,13 @@ int stream_step(const vqc_circuit* c, int64_t batch, int64_t norm, const float* 
                 float* grad_out, float* dp, float* dx, unsigned char* ws, void* stream) {
   const Plan& p = c->plan;
   float* cot = grad_out ? grad_out : reinterpret_cast<float*>(ws + stream_layout(p, batch).cot);
-  int rc = stream_forward(c, batch, params, inputs, expvals, ws, stream, true);
+  const StepHead sh{loss_kind, norm, target, cot};
+  int rc = stream_forward(c, batch, params, inputs, expvals, ws, stream, true, nullptr, nullptr, 0,
+                          0, 0.f, &sh);
   if (rc) return rc;
-  rc = vqc::launch_loss_grad(loss_kind, batch, norm, p.n, expvals, target, cot, stream);
-  if (rc) return hip_fail("loss launch", rc);
-  return stream_backward(c, batch, params, inputs, cot, ws, dp, dx, stream);
+  // with a table kernel the forward's tables serve the adjoint, and it cleared the partials
+  return stream_backward(c, batch, params, inputs, cot, ws, dp, dx, stream,
+                         c->jit.tables != nullptr);
 }
 
 // The training step on a checked, large enough workspace, with the handle's

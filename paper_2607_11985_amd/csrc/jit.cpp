@@ -1196,8 +1196,9 @@ std::string stream_head_partials(const Plan& p, int map_off, int R) {
 std::string head_finish_unit(const Plan& p, const std::string& name) {
   std::ostringstream o;
   const int L = head_len(p), n = p.n, NV = head_nv(p);
+  const int NS = p.P + p.F;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\nstruct Head {\n"
-    << "static constexpr int kN = " << n << ", kNV = " << NV << ";\n";
+    << "static constexpr int kN = " << n << ", kNV = " << NV << ", kNS = " << NS << ";\n";
   emit_head_pre(o, p, "head_pre");
   std::map<int, std::vector<int>> terms;  // slot -> q * L + i
   for (int q = 0; q < n; ++q)
@@ -1211,17 +1212,17 @@ std::string head_finish_unit(const Plan& p, const std::string& name) {
     idx.insert(idx.end(), kv.second.begin(), kv.second.end());
     start.push_back((uint32_t)idx.size());
   }
-  o << "__device__ __forceinline__ static void add_grads(const float* gs, float* gp, int tid) {\n";
+  o << "__device__ __forceinline__ static void add_grads(const float* gs, float* hs, int tid) {\n";
   emit_array(o, "uint32_t", "kStart", start);
   emit_array(o, "uint32_t", "kIdx", idx);
   emit_array(o, "uint32_t", "kSlot", slot);
   o << "  for (int i = tid; i < " << slot.size() << "; i += 64) {\n"
     << "    float s = 0.f;\n"
     << "    for (uint32_t e = kStart[i]; e < kStart[i + 1]; ++e) s += gs[kIdx[e]];\n"
-    << "    gp[kSlot[i]] += s;\n"
+    << "    hs[kSlot[i]] = s;\n"
     << "  }\n}\n"
     << "};\n}  // namespace vqc\n";
-  const size_t lds = (size_t)n * L * 32 + (size_t)n * 16 + (size_t)(NV + n * L) * 4;
+  const size_t lds = (size_t)n * L * 32 + (size_t)n * 16 + (size_t)(NV + n * L + NS) * 4;
   o << "extern \"C\" __global__ void __launch_bounds__(64) " << name
     << "(const vqc::PassArgs A) {\n"
     << "  __shared__ __align__(16) unsigned char smem[" << lds_size(lds) << "];\n"

@@ -47,6 +47,31 @@ __global__ void reduce_e_kernel(int64_t B, int ng, int n, const float* __restric
   e[i] = v;
 }
 
+// The streaming training step's <Z> rows from the tiles' partials, then the
+// loss head's cotangent rows, in one launch: a block holds whole rows (256 / n
+// samples), which it passes to the loss head through LDS.
+__global__ void __launch_bounds__(256) reduce_e_loss_kernel(int64_t B, int ng, int n,
+                                                            const float* __restrict__ epart,
+                                                            float* __restrict__ e, int kind,
+                                                            int64_t norm,
+                                                            const float* __restrict__ y,
+                                                            float* __restrict__ g) {
+  __shared__ float rows[256];
+  const int spb = 256 / n;
+  const int t = threadIdx.x;
+  const int ls = t / n, q = t - ls * n;
+  const int64_t b = (int64_t)blockIdx.x * spb + ls;
+  const bool on = ls < spb && b < B;
+  if (on) {
+    float v = 0.f;
+    for (int gi = 0; gi < (1 << ng); ++gi) v += epart[((b << ng) + gi) * n + q];
+    e[b * n + q] = v;
+    rows[t] = v;
+  }
+  __syncthreads();
+  if (on) g[b * n + q] = loss_cot(kind, rows + ls * n, y ? y[b] : 0.f, n, q, norm);
+}
+
 __global__ void reduce_grad_kernel(int64_t B, int ng, int n_slots, int P, int F,
                                    const float* __restrict__ gpart, float* __restrict__ dparams,
                                    float* __restrict__ dinputs) {
@@ -228,6 +253,14 @@ int launch_stream_pass(const Plan& p, bool bwd, const PassArgs& a, int64_t block
 int launch_reduce_e(int64_t batch, int ng, int n, const float* epart, float* e, void* stream) {
   hipLaunchKernelGGL(reduce_e_kernel, dim3(grid_1d(batch * n, 256)), dim3(256), 0,
                      (hipStream_t)stream, batch, ng, n, epart, e);
+  return (int)hipGetLastError();
+}
+
+int launch_reduce_e_loss(int64_t batch, int ng, int n, const float* epart, float* e, int kind,
+                         int64_t norm, const float* y, float* g, void* stream) {
+  const int spb = 256 / n;
+  hipLaunchKernelGGL(reduce_e_loss_kernel, dim3((unsigned)((batch + spb - 1) / spb)), dim3(256), 0,
+                     (hipStream_t)stream, batch, ng, n, epart, e, kind, norm, y, g);
   return (int)hipGetLastError();
 }
 

@@ -999,6 +999,7 @@ int build_step_plan(const Plan& full, Plan& step, std::string& msg) {
       any = true;
     }
   if (!any || full.n > 64) return 1;  // one lane per qubit walks its head
+  if (full.P + full.F > kMaxStepSlots) return 1;  // the head kernel's LDS row of slots
   step = full;
   step.prims.clear();
   for (const Prim& g : full.prims)

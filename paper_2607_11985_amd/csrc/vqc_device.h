@@ -1759,16 +1759,17 @@ __device__ __forceinline__ void head_finish(const float (&v)[NV], const Walk& w,
                });
 }
 
-// The streaming training step's head gradients: one 64-thread workgroup per
-// sample, after its last adjoint pass.  v_q is the sum of the sample's tiles'
-// partials (in tile order); lane q walks qubit q's head forward (recording
-// the states) and back, writing each rotation's gradient times its chain-rule
-// factor to LDS; then each gradient slot of a head rotation adds the sum of
-// its terms (a fixed list per slot, H::add_grads) to the partial row of the
-// sample's first tile, which the gradient reduction reads.
+// The streaming training step's head gradients and gradient rows: one
+// 64-thread workgroup per sample, after its last adjoint pass.  v_q is the sum
+// of the sample's tiles' partials (in tile order); lane q walks qubit q's head
+// forward (recording the states) and back, writing each rotation's gradient
+// times its chain-rule factor to LDS; each gradient slot of a head rotation
+// sums its terms (a fixed list per slot, H::add_grads) into an LDS row; then
+// every slot's value is the sum of the tiles' partials (in tile order) plus
+// that row, written to dparams / dinputs.
 template <typename H>
 __device__ __forceinline__ void head_finish_stream(const PassArgs& A, unsigned char* smem) {
-  constexpr int L = H::kL, NV = H::kNV, N = H::kN;
+  constexpr int L = H::kL, NV = H::kNV, N = H::kN, NS = H::kNS;
   const int tid = threadIdx.x;
   const int64_t b = blockIdx.x;
   Walk w;
@@ -1776,7 +1777,8 @@ __device__ __forceinline__ void head_finish_stream(const PassArgs& A, unsigned c
   HeadRec* rec = reinterpret_cast<HeadRec*>(smem);
   float4* fin = reinterpret_cast<float4*>(smem + N * L * 32);
   float* vs = reinterpret_cast<float*>(smem + N * L * 32 + N * 16);
-  float* gs = vs + NV;  // [n][L]
+  float* gs = vs + NV;    // [n][L]
+  float* hs = gs + N * L;  // [NS]
   const HeadPre<L> hp = H::head_pre(tid);
   float2 fa, fb;
   head_walk<L>(w, hp, rec, fin, N, fa, fb);
@@ -1787,13 +1789,26 @@ __device__ __forceinline__ void head_finish_stream(const PassArgs& A, unsigned c
     vs[j] = s;
   }
   for (int j = tid; j < N * L; j += 64) gs[j] = 0.f;
+  for (int j = tid; j < NS; j += 64) hs[j] = 0.f;
   __syncthreads();
   if (tid < N)
     head_back<L>(w, rec, tid, make_float2(vs[4 * tid], vs[4 * tid + 1]),
                  make_float2(vs[4 * tid + 2], vs[4 * tid + 3]),
                  [&](int i, const HeadRec& r, float g) { gs[tid * L + i] = g * r.mul; });
   __syncthreads();
-  H::add_grads(gs, A.gpart + row0 * A.n_slots, tid);
+  H::add_grads(gs, hs, tid);
+  __syncthreads();
+  const float* gp = A.gpart + row0 * NS;
+  for (int s = tid; s < NS; s += 64) {
+    float v = 0.f;
+    for (int g = 0; g < (1 << A.ng); ++g) v += gp[g * NS + s];
+    v += hs[s];
+    if (s < A.P) {
+      if (A.dparams) A.dparams[b * A.P + s] = v;
+    } else if (A.dinputs) {
+      A.dinputs[b * A.F + (s - A.P)] = v;
+    }
+  }
 }
 
 template <int WG, int R, typename FS, typename BS, typename HD = NoHead>
@@ -1920,6 +1935,11 @@ __device__ __forceinline__ void table_body(const PassArgs& A, unsigned char* sme
     Gs[i] = gm[i];
   }
   for (int q = tid; q < A.n; q += WG) A.esig[b * A.n + q] = es[q];
+  if (A.gpart) {
+    // the training step's gradient partials of this sample, cleared for its adjoint
+    float* gp = A.gpart + (b << A.ng) * A.n_slots;
+    for (int i = tid; i < (A.n_slots << A.ng); i += WG) gp[i] = 0.f;
+  }
 }
 
 template <bool BWD, int R, int K, typename Sched>

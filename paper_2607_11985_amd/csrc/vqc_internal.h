@@ -95,6 +95,9 @@ constexpr int kNumGateKinds = 32;  // VQC_RX .. VQC_CSWAP
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
                Plan& plan, std::string& msg, bool lane_gates, int tile_qubits = 0,
                int bwd_reg_bits = 0);
+// Gradient slots (P + F) up to which the streaming training step runs a plan
+// without the heads (its head kernel holds a row of them in LDS).
+constexpr int kMaxStepSlots = 8192;
 // The streaming training step's plan without the heads' rotations (planner.cpp).
 // Returns 0, 1 when the circuit has no head rotation, or a VQC_ERR_* code.
 int build_step_plan(const Plan& full, Plan& step, std::string& msg);
@@ -110,6 +113,10 @@ int launch_resident_step(const Plan& plan, const TileArgs& a, int64_t blocks, vo
 int launch_stream_pass(const Plan& plan, bool bwd, const PassArgs& a, int64_t blocks,
                        void* stream);
 int launch_reduce_e(int64_t batch, int ng, int n, const float* epart, float* e, void* stream);
+// <Z> rows and the loss head's cotangent rows of `batch` rows of a batch of
+// `norm` samples in one launch (n <= 256)
+int launch_reduce_e_loss(int64_t batch, int ng, int n, const float* epart, float* e, int kind,
+                         int64_t norm, const float* y, float* g, void* stream);
 int launch_reduce_grad(int64_t batch, int ng, int n_slots, int P, int F, const float* gpart,
                        float* dparams, float* dinputs, void* stream);
 int launch_fill_zero(float* p, int64_t count, void* stream);

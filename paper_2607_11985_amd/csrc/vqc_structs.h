@@ -157,7 +157,11 @@ struct PassArgs {
   float* gsig;
   float* esig;
   // training step with a product head: per tile of the last adjoint pass the
-  // partial sums of the 2-vectors v_q [B * 2^ng][NV] (NV = 4 n rounded up to 16)
+  // partial sums of the 2-vectors v_q [B * 2^ng][NV] (NV = 4 n rounded up to 16),
+  // and the gradient rows the head kernel writes (dparams [B][P] or null,
+  // dinputs [B][F] or null)
   float* vpart;
+  float* dparams;
+  float* dinputs;
 };
 }  // namespace vqc

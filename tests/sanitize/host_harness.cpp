@@ -30,6 +30,10 @@ int launch_resident_backward(const Plan&, const TileArgs&, int64_t, void*) { no_
 int launch_resident_step(const Plan&, const TileArgs&, int64_t, void*) { no_device("step"); }
 int launch_stream_pass(const Plan&, bool, const PassArgs&, int64_t, void*) { no_device("pass"); }
 int launch_reduce_e(int64_t, int, int, const float*, float*, void*) { no_device("reduce_e"); }
+int launch_reduce_e_loss(int64_t, int, int, const float*, float*, int, int64_t, const float*,
+                         float*, void*) {
+  no_device("reduce_e_loss");
+}
 int launch_reduce_grad(int64_t, int, int, int, int, const float*, float*, float*, void*) {
   no_device("reduce_grad");
 }
