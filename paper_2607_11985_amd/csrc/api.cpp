@@ -474,7 +474,8 @@ int stream_backward(const vqc_circuit* c, int64_t batch, const float* params, co
     a.dparams = dp;
     a.dinputs = dx;
     set_tables(a, ws, L);
-    rc = c->jit.head_finish ? vqc::jit_launch(c->jit.head_finish, batch, 64, &a, sizeof(a), stream)
+    rc = c->jit.head_finish ? vqc::jit_launch(c->jit.head_finish, batch, vqc::kHeadThreads, &a,
+                                              sizeof(a), stream)
                             : (int)hipErrorInvalidDeviceFunction;
     return rc ? hip_fail("head gradient launch", rc) : VQC_OK;
   }

@@ -1212,21 +1212,22 @@ std::string head_finish_unit(const Plan& p, const std::string& name) {
     idx.insert(idx.end(), kv.second.begin(), kv.second.end());
     start.push_back((uint32_t)idx.size());
   }
-  o << "__device__ __forceinline__ static void add_grads(const float* gs, float* hs, int tid) {\n";
+  o << "__device__ __forceinline__ static void add_grads(const float* gs, float* hs, int tid, "
+       "int nt) {\n";
   emit_array(o, "uint32_t", "kStart", start);
   emit_array(o, "uint32_t", "kIdx", idx);
   emit_array(o, "uint32_t", "kSlot", slot);
-  o << "  for (int i = tid; i < " << slot.size() << "; i += 64) {\n"
+  o << "  for (int i = tid; i < " << slot.size() << "; i += nt) {\n"
     << "    float s = 0.f;\n"
     << "    for (uint32_t e = kStart[i]; e < kStart[i + 1]; ++e) s += gs[kIdx[e]];\n"
     << "    hs[kSlot[i]] = s;\n"
     << "  }\n}\n"
     << "};\n}  // namespace vqc\n";
   const size_t lds = (size_t)n * L * 32 + (size_t)n * 16 + (size_t)(NV + n * L + NS) * 4;
-  o << "extern \"C\" __global__ void __launch_bounds__(64) " << name
+  o << "extern \"C\" __global__ void __launch_bounds__(" << kHeadThreads << ") " << name
     << "(const vqc::PassArgs A) {\n"
     << "  __shared__ __align__(16) unsigned char smem[" << lds_size(lds) << "];\n"
-    << "  vqc::head_finish_stream<vqc::Head>(A, smem);\n}\n";
+    << "  vqc::head_finish_stream<" << kHeadThreads << ", vqc::Head>(A, smem);\n}\n";
   return o.str();
 }
 

@@ -1760,14 +1760,14 @@ __device__ __forceinline__ void head_finish(const float (&v)[NV], const Walk& w,
 }
 
 // The streaming training step's head gradients and gradient rows: one
-// 64-thread workgroup per sample, after its last adjoint pass.  v_q is the sum
+// workgroup of WG threads per sample, after its last adjoint pass.  v_q is the sum
 // of the sample's tiles' partials (in tile order); lane q walks qubit q's head
 // forward (recording the states) and back, writing each rotation's gradient
 // times its chain-rule factor to LDS; each gradient slot of a head rotation
 // sums its terms (a fixed list per slot, H::add_grads) into an LDS row; then
 // every slot's value is the sum of the tiles' partials (in tile order) plus
 // that row, written to dparams / dinputs.
-template <typename H>
+template <int WG, typename H>
 __device__ __forceinline__ void head_finish_stream(const PassArgs& A, unsigned char* smem) {
   constexpr int L = H::kL, NV = H::kNV, N = H::kN, NS = H::kNS;
   const int tid = threadIdx.x;
@@ -1783,23 +1783,23 @@ __device__ __forceinline__ void head_finish_stream(const PassArgs& A, unsigned c
   float2 fa, fb;
   head_walk<L>(w, hp, rec, fin, N, fa, fb);
   const int64_t row0 = b << A.ng;
-  for (int j = tid; j < NV; j += 64) {
+  for (int j = tid; j < NV; j += WG) {
     float s = 0.f;
     for (int g = 0; g < (1 << A.ng); ++g) s += A.vpart[(row0 + g) * NV + j];
     vs[j] = s;
   }
-  for (int j = tid; j < N * L; j += 64) gs[j] = 0.f;
-  for (int j = tid; j < NS; j += 64) hs[j] = 0.f;
+  for (int j = tid; j < N * L; j += WG) gs[j] = 0.f;
+  for (int j = tid; j < NS; j += WG) hs[j] = 0.f;
   __syncthreads();
   if (tid < N)
     head_back<L>(w, rec, tid, make_float2(vs[4 * tid], vs[4 * tid + 1]),
                  make_float2(vs[4 * tid + 2], vs[4 * tid + 3]),
                  [&](int i, const HeadRec& r, float g) { gs[tid * L + i] = g * r.mul; });
   __syncthreads();
-  H::add_grads(gs, hs, tid);
+  H::add_grads(gs, hs, tid, WG);
   __syncthreads();
   const float* gp = A.gpart + row0 * NS;
-  for (int s = tid; s < NS; s += 64) {
+  for (int s = tid; s < NS; s += WG) {
     float v = 0.f;
     for (int g = 0; g < (1 << A.ng); ++g) v += gp[g * NS + s];
     v += hs[s];

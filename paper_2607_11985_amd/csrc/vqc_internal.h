@@ -146,6 +146,9 @@ struct JitKernels {
   void* head_finish = nullptr;        // streaming step with a product head: head gradients
 };
 constexpr int kTableThreads = 256;    // threads of the table kernel's workgroups
+// threads of the streaming step's head kernel (one workgroup per sample: its
+// sums over the tiles of every gradient slot are spread over them)
+constexpr int kHeadThreads = 256;
 struct JitUnit {
   std::string name, src;
   // what the kernel is: resident forward / adjoint / step ('r', 'b', 's'),
