@@ -407,9 +407,11 @@ def measure(idx, args, torch, dev, want_cpu, cpu_budget):
     alu_frac, hbm_frac = alu / PEAK_FP32_TFLOPS, hbm / PEAK_HBM_GBS
     resident = info["path"] == 1
     if args.engine == "jit":
-        kname = "vqc_rs (one launch)" if resident else \
-            ("vqc_st, vqc_sf*, reduce_e, loss_grad, fill_zero, vqc_sb*, vqc_sh, reduce_grad (one "
-             "step: each batch half on its own stream)")
+        head = info["step_head_rotations"] > 0  # the step's own plan (product head)
+        kname = "vqc_rs (one launch)" if resident else (
+            ("vqc_ht, vqc_hf*, reduce_e_loss, vqc_hb*, vqc_hg" if head else
+             "vqc_st, vqc_sf*, reduce_e_loss, vqc_sb*, reduce_grad")
+            + " (one step: each batch half on its own stream)")
     else:
         kname = "resident_step_kernel" if resident else \
             "stream_kernel passes (one step: each batch half on its own stream)"

@@ -1198,7 +1198,8 @@ std::string head_finish_unit(const Plan& p, const std::string& name) {
   const int L = head_len(p), n = p.n, NV = head_nv(p);
   const int NS = p.P + p.F;
   o << "#include \"vqc_device.h\"\nnamespace vqc {\nstruct Head {\n"
-    << "static constexpr int kN = " << n << ", kNV = " << NV << ", kNS = " << NS << ";\n";
+    << "static constexpr int kN = " << n << ", kNV = " << NV << ", kNS = " << NS
+    << ", kNG = " << p.ng << ";\n";
   emit_head_pre(o, p, "head_pre");
   std::map<int, std::vector<int>> terms;  // slot -> q * L + i
   for (int q = 0; q < n; ++q)
@@ -1207,11 +1208,14 @@ std::string head_finish_unit(const Plan& p, const std::string& name) {
       if (s >= 0) terms[s].push_back(q * L + i);
     }
   std::vector<uint32_t> start{0}, idx, slot;
+  bool unique = true;  // no two head rotations share a gradient slot
   for (const auto& kv : terms) {
     slot.push_back((uint32_t)kv.first);
     idx.insert(idx.end(), kv.second.begin(), kv.second.end());
     start.push_back((uint32_t)idx.size());
+    unique = unique && kv.second.size() == 1;
   }
+  o << "static constexpr bool kUniqueSlots = " << (unique ? "true" : "false") << ";\n";
   o << "__device__ __forceinline__ static void add_grads(const float* gs, float* hs, int tid, "
        "int nt) {\n";
   emit_array(o, "uint32_t", "kStart", start);

@@ -43,6 +43,7 @@ __global__ void reduce_e_kernel(int64_t B, int ng, int n, const float* __restric
   const int64_t b = i / n;
   const int q = (int)(i - b * n);
   float v = 0.f;
+#pragma unroll 8  // loads in flight together; the sum keeps its order
   for (int g = 0; g < (1 << ng); ++g) v += epart[((b << ng) + g) * n + q];
   e[i] = v;
 }
@@ -64,6 +65,7 @@ __global__ void __launch_bounds__(256) reduce_e_loss_kernel(int64_t B, int ng, i
   const bool on = ls < spb && b < B;
   if (on) {
     float v = 0.f;
+#pragma unroll 8  // loads in flight together; the sum keeps its order
     for (int gi = 0; gi < (1 << ng); ++gi) v += epart[((b << ng) + gi) * n + q];
     e[b * n + q] = v;
     rows[t] = v;
@@ -80,6 +82,7 @@ __global__ void reduce_grad_kernel(int64_t B, int ng, int n_slots, int P, int F,
   const int64_t b = i / n_slots;
   const int s = (int)(i - b * n_slots);
   float v = 0.f;
+#pragma unroll 8  // loads in flight together; the sum keeps its order
   for (int g = 0; g < (1 << ng); ++g) v += gpart[((b << ng) + g) * n_slots + s];
   if (s < P) {
     if (dparams) dparams[b * P + s] = v;

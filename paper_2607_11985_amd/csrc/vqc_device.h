@@ -1760,49 +1760,73 @@ __device__ __forceinline__ void head_finish(const float (&v)[NV], const Walk& w,
 }
 
 // The streaming training step's head gradients and gradient rows: one
-// workgroup of WG threads per sample, after its last adjoint pass.  v_q is the sum
-// of the sample's tiles' partials (in tile order); lane q walks qubit q's head
-// forward (recording the states) and back, writing each rotation's gradient
-// times its chain-rule factor to LDS; each gradient slot of a head rotation
-// sums its terms (a fixed list per slot, H::add_grads) into an LDS row; then
-// every slot's value is the sum of the tiles' partials (in tile order) plus
-// that row, written to dparams / dinputs.
+// workgroup of WG threads per sample, after its last adjoint pass.  Every
+// slot's sum over the sample's tiles' partials (in tile order) is loaded
+// first, so that those loads overlap the rest.  v_q is the sum of the tiles'
+// head partials (in tile order); lane q walks qubit q's head forward
+// (recording the states) and back, and each rotation's gradient times its
+// chain-rule factor goes to an LDS row of slots: written in place when no two
+// head rotations share a slot, else summed per slot over a fixed list of
+// terms (H::add_grads).  Each slot's value is its tile sum plus that row,
+// written to dparams / dinputs.
 template <int WG, typename H>
 __device__ __forceinline__ void head_finish_stream(const PassArgs& A, unsigned char* smem) {
-  constexpr int L = H::kL, NV = H::kNV, N = H::kN, NS = H::kNS;
+  constexpr int L = H::kL, NV = H::kNV, N = H::kN, NS = H::kNS, T = 1 << H::kNG;
+  constexpr int PT = (NS + WG - 1) / WG;  // slots per thread
   const int tid = threadIdx.x;
   const int64_t b = blockIdx.x;
+  const int64_t row0 = b << H::kNG;
+  const float* gp = A.gpart + row0 * NS;
+  // a compile-time tile count: every load of a sum is in flight at once
+  float tsum[PT];
+#pragma unroll
+  for (int k = 0; k < PT; ++k) {
+    const int s = tid + k * WG;
+    float v = 0.f;
+    if (s < NS) {
+#pragma unroll
+      for (int g = 0; g < T; ++g) v += gp[g * NS + s];
+    }
+    tsum[k] = v;
+  }
   Walk w;
   w.tab = reinterpret_cast<const float2*>(A.tabs) + b * A.n_occ;  // exact (cos, sin) of heads
   HeadRec* rec = reinterpret_cast<HeadRec*>(smem);
   float4* fin = reinterpret_cast<float4*>(smem + N * L * 32);
   float* vs = reinterpret_cast<float*>(smem + N * L * 32 + N * 16);
-  float* gs = vs + NV;    // [n][L]
+  float* gs = vs + NV;     // [n][L]
   float* hs = gs + N * L;  // [NS]
   const HeadPre<L> hp = H::head_pre(tid);
   float2 fa, fb;
   head_walk<L>(w, hp, rec, fin, N, fa, fb);
-  const int64_t row0 = b << A.ng;
   for (int j = tid; j < NV; j += WG) {
     float s = 0.f;
-    for (int g = 0; g < (1 << A.ng); ++g) s += A.vpart[(row0 + g) * NV + j];
+#pragma unroll
+    for (int g = 0; g < T; ++g) s += A.vpart[(row0 + g) * NV + j];
     vs[j] = s;
   }
-  for (int j = tid; j < N * L; j += WG) gs[j] = 0.f;
   for (int j = tid; j < NS; j += WG) hs[j] = 0.f;
   __syncthreads();
   if (tid < N)
     head_back<L>(w, rec, tid, make_float2(vs[4 * tid], vs[4 * tid + 1]),
                  make_float2(vs[4 * tid + 2], vs[4 * tid + 3]),
-                 [&](int i, const HeadRec& r, float g) { gs[tid * L + i] = g * r.mul; });
+                 [&](int i, const HeadRec& r, float g) {
+                   if constexpr (H::kUniqueSlots) {
+                     if (r.slot1 > 0) hs[r.slot1 - 1] = g * r.mul;
+                   } else {
+                     gs[tid * L + i] = g * r.mul;
+                   }
+                 });
   __syncthreads();
-  H::add_grads(gs, hs, tid, WG);
-  __syncthreads();
-  const float* gp = A.gpart + row0 * NS;
-  for (int s = tid; s < NS; s += WG) {
-    float v = 0.f;
-    for (int g = 0; g < (1 << A.ng); ++g) v += gp[g * NS + s];
-    v += hs[s];
+  if constexpr (!H::kUniqueSlots) {
+    H::add_grads(gs, hs, tid, WG);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < PT; ++k) {
+    const int s = tid + k * WG;
+    if (s >= NS) break;
+    const float v = tsum[k] + hs[s];
     if (s < A.P) {
       if (A.dparams) A.dparams[b * A.P + s] = v;
     } else if (A.dinputs) {
