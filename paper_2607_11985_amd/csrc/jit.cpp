@@ -480,13 +480,41 @@ std::string occ_scale(const Plan& p, uint32_t occ) {
   return o.str();
 }
 
+// What a stream does with its swap frame at its end (vqc_device.h, "swap
+// frame"): resolve it (a reader of positions follows), leave it in w.fx for
+// the pass's stores, or drop it (nothing reads the state).
+enum FrameEnd { kFrameResolve, kFramePack, kFrameDrop };
+
 // Statements of one instruction stream for register width R.  With tangent
-// tables (tm.on) rotations use the tangent form and blocks are rescaled.
+// tables (tm.on) rotations use the tangent form and blocks are rescaled, and
+// CNOTs from a thread / tile bit onto a register bit go to the swap frame.
 void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, int n_ins, bool bwd,
                    int R, int k, int S, const GradMode& gm, const TanMode& tm,
-                   const std::vector<char>* skip = nullptr) {
+                   const std::vector<char>* skip = nullptr, FrameEnd fend = kFrameResolve) {
   const int t = k - R;
   const bool tan = tm.on;
+  // the swap frame: fs<r> (0 or 1 << 31 per thread) for register bit r; dirty:
+  // the bits whose frame may be set here (known while generating)
+  // (not in the kernels with gates on lane bits: there the lane swaps, which
+  // would have to resolve the frame first, follow most CNOTs)
+  const bool frames = tan && p.lanes == 0;
+  uint32_t dirty = 0;
+  if (frames) {
+    o << "  uint32_t";
+    for (int r = 0; r < R; ++r) o << (r ? ", " : " ") << "fs" << r << " = 0u";
+    o << ";\n";
+  }
+  // conditional swaps along the frame's bits in `bits` (one per state)
+  auto resolve = [&](uint32_t bits) {
+    bits &= dirty;
+    for (int r = 0; r < R; ++r) {
+      if (!((bits >> r) & 1u)) continue;
+      o << "  cnot_tr<R, " << r << ">(a, fs" << r << " != 0u);";
+      if (bwd) o << " cnot_tr<R, " << r << ">(l, fs" << r << " != 0u);";
+      o << " fs" << r << " = 0u;\n";
+    }
+    dirty &= ~bits;
+  };
   const int nrot = (int)(bwd ? tm.bocc.size() : tm.focc.size());
   int m = 0;  // rotation index in the stream
   // batched up to 8 amplitudes per thread, and with 16 in the streaming passes
@@ -557,6 +585,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         std::vector<std::pair<int, int>> swaps;
         if (lane_exchange(p, arg, k, R, t, swaps)) {
           // register bits swapped with lane bits: cross-lane moves, no LDS
+          resolve(dirty);
           o << "  { const uint32_t ln = opaque(__lane_id());\n";
           for (const auto& sw : swaps) {
             o << "    lane_swap<R, " << sw.first << ", " << sw.second << ">(a, ln);\n";
@@ -567,17 +596,38 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         }
         o << "  { static constexpr uint32_t col[] = {";
         for (int i = 0; i < 2 * k; ++i) o << (i ? "," : "") << hex(p.cols[arg + i]);
+        o << "};\n";
+        // the swap frame, folded into the write addresses
+        std::string fo = "0u";
+        if (dirty) {
+          o << "    const uint32_t fo = 0u";
+          for (int r = 0; r < R; ++r)
+            if ((dirty >> r) & 1u)
+              o << " ^ ((col[" << r << "] << 2) & (uint32_t)((int32_t)fs" << r << " >> 31))";
+          o << ";\n";
+          fo = "fo";
+        }
         if (bwd)
-          o << "};\n    exchange2<R>(a, l, w.xbuf, w.plane, col, " << k << ", " << t
-            << ", w.stid, w.sl);\n";
+          o << "    exchange2<R>(a, l, w.xbuf, w.plane, col, " << k << ", " << t
+            << ", w.stid, w.sl, " << fo << ");\n";
         else
-          o << "};\n    exchange<R>(a, w.xbuf, w.plane, col, " << k << ", " << t
-            << ", w.stid, w.sl);\n";
+          o << "    exchange<R>(a, w.xbuf, w.plane, col, " << k << ", " << t
+            << ", w.stid, w.sl, " << fo << ");\n";
+        for (int r = 0; r < R; ++r)
+          if ((dirty >> r) & 1u) o << "    fs" << r << " = 0u;\n";
+        dirty = 0;
         o << "  }\n";
         break;
       }
       case OP_CNOT: {
         const char* sts[2] = {"a", "l"};
+        if (frames && pb < R && pa >= R) {
+          // thread / tile control, register target: into the swap frame
+          o << "  fs" << pb << " ^= " << bit(pa) << " << 31;\n";
+          dirty |= 1u << pb;
+          break;
+        }
+        if (pb >= R && pa < R) resolve(1u << pa);  // a register control of a lane target
         for (int s = 0; s < (bwd ? 2 : 1); ++s) {
           if (pb >= R && pa >= R + 2 && pa < R + 6)  // lane target, bank / row control
             o << "  cnot_ll<R, " << pb - R << ", " << pa - R << ">(" << sts[s] << ");\n";
@@ -591,6 +641,11 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
           else
             o << "  cnot_tr<R, " << pb << ">(" << sts[s] << ", " << bit(pa) << ");\n";
         }
+        if (pa < R && pb < R && ((dirty >> pa) & 1u)) {
+          // F CNOT(c, t) = CNOT(c, t) F X_t: the control's frame spreads to the target
+          o << "  fs" << pb << " ^= fs" << pa << ";\n";
+          dirty |= 1u << pb;
+        }
         break;
       }
       case OP_CZ: {
@@ -602,6 +657,15 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         // per gate.
         int end = pc;
         while (end < n_ins && (ins[2 * end] & 31) == OP_CZ) ++end;
+        {
+          uint32_t regs = 0;
+          for (int q = pc; q < end; ++q) {
+            const int x = (ins[2 * q] >> 5) & 31, y = (ins[2 * q] >> 10) & 31;
+            if (x < R) regs |= 1u << x;
+            if (y < R) regs |= 1u << y;
+          }
+          resolve(regs);
+        }
         const int N = 1 << R;
         std::vector<int> cu(N, 0);
         std::vector<std::string> mr(R);
@@ -654,7 +718,12 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
             o << "  { const float2 tc = table_entry<" << arg % 64 << ">(T" << arg / 64 << "); ";
           else
             o << "  { const float2 tc = w.tab[" << arg << "]; ";
-          o << "const float t = tc.x; ";
+          // negated under the swap frame (RY, RZ on a frame bit)
+          const bool neg = reg && op != OP_RX && ((dirty >> pa) & 1u);
+          if (neg)
+            o << "const float t = flip_sign(tc.x, fs" << pa << "); ";
+          else
+            o << "const float t = tc.x; ";
           // RX / RY off the register bits sit on a lane bit (planner option)
           const std::string lane = std::to_string(pa - R);
           const std::string hi = pa >= R ? bit(pa) : "0u";
@@ -676,6 +745,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
               o << "float g = adj_rx_lane_t<R, " << lane << ">(a, l, t);";
             else
               o << "float g = adj_ry_lane_t<R, " << lane << ">(a, l, t, " << hi << ");";
+            if (neg) o << " g = flip_sign(g, fs" << pa << ");";
             // the states carry 1 / (the factors of the block before this gate)
             if (sreg)
               o << " g *= table_entry<" << arg % 64 << ">(G" << arg / 64 << ") * (bp * bp);";
@@ -749,6 +819,17 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
     }
   }
   if (batched) emit_flush(o, pend);
+  if (frames) {
+    if (fend == kFrameResolve) {
+      resolve(dirty);
+    } else if (fend == kFramePack) {
+      o << "  w.fx = 0u";
+      for (int r = 0; r < R; ++r)
+        if ((dirty >> r) & 1u) o << " | ((fs" << r << " >> 31) << " << r << ")";
+      o << ";\n";
+    }
+    for (int r = 0; r < R; ++r) o << "  (void)fs" << r << ";\n";
+  }
 }
 
 // The circuit's constants, compiled in (the interpreter reads them from the
@@ -835,7 +916,7 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
                        const GradMode& gm, const TanMode& tm, const Frame* tables, int map_off,
                        bool load = false, int fixed_flags = -1,
                        const std::vector<char>* skip = nullptr,
-                       const std::string& head = std::string()) {
+                       const std::string& head = std::string(), FrameEnd fend = kFrameResolve) {
   o << "struct " << name << " {\n";
   emit_constants(o, p, map_off);
   o << "static constexpr int kFixedFlags = " << fixed_flags << ";\n";
@@ -852,7 +933,7 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
     o << "  const uint32_t ln = (uint32_t)w.stid & " << gm.tm - 1 << "u;\n"
       << "  float ga[" << gm.nr << "];\n"
       << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) ga[j] = 0.f;\n";
-  emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm, tm, skip);
+  emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm, tm, skip, fend);
   if (regs)  // every (slot, group) accumulator is written by exactly one lane
     o << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) {\n"
       << "    const uint32_t slot = j * " << gm.tm << "u + ln;\n"
@@ -898,8 +979,17 @@ std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
   const int lanes = stream ? threads : 1 << (p.k - R);
   TanMode tm = tan_mode(p, bwd ? nullptr : ins, n_ins, bwd ? ins : nullptr, n_ins, S, esign, lds);
   tm.on = tm.on && tangent_wanted(S, R);
+  // the swap frame at the stream's end: a streaming pass's stores take it,
+  // unless its state is read in place after the sweep (<Z> and probabilities,
+  // the head partials); a resident forward resolves it for its epilogue
+  FrameEnd fend = bwd ? kFrameDrop : kFrameResolve;
+  if (stream) {
+    if (bwd) fend = (fixed_flags & PF_LAST_ADJ) ? (head.empty() ? kFrameDrop : kFrameResolve)
+                                                 : kFramePack;
+    else fend = (fixed_flags & PF_ZPART) ? kFrameResolve : kFramePack;
+  }
   emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr,
-                    map_off, load, fixed_flags, nullptr, head);
+                    map_off, load, fixed_flags, nullptr, head, fend);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << threads << ") " << occupancy(R)
     << name
@@ -1266,9 +1356,10 @@ std::string step_unit(const Plan& p, const Frame& fr) {
   }
   const std::vector<char>* skip = head.empty() ? nullptr : &head;
   emit_sched_struct(o, "SchedF", p, p.fwd.data(), nf, false, p.R, p.k, p.S, gm, tm, &fr,
-                    p.end_off, false, -1, skip);
+                    p.end_off, false, -1, skip, std::string(), kFrameResolve);
   emit_sched_struct(o, "SchedB", p, p.bwd.data(), nb, true, p.R, p.k, p.S, gm, tm, nullptr,
-                    p.end_off, false, -1, skip);
+                    p.end_off, false, -1, skip, std::string(),
+                    skip ? kFrameResolve : kFrameDrop);
   if (skip) emit_head(o, p, head_off);
   o << "}  // namespace vqc\n"
     << "extern \"C\" __global__ void __launch_bounds__(" << p.WG << ") " << occupancy(p.R)

@@ -920,23 +920,52 @@ __device__ __forceinline__ void exchange_at(St<R>& a, float* xbuf, uint32_t plan
   __syncthreads();
 }
 
+// fo: byte offset XORed into every write address, which resolves a swap frame
+// (register index u holds position u ^ f: its slot is that of u, XOR the
+// columns of f's bits)
 template <int R>
 __device__ __forceinline__ void exchange(St<R>& a, float* xbuf, uint32_t plane,
-                                         const uint32_t* col, int k, int t, int stid, int sl) {
+                                         const uint32_t* col, int k, int t, int stid, int sl,
+                                         uint32_t fo = 0u) {
   uint32_t bw, br;
   exchange_bases<R>(col, k, t, stid, sl, bw, br);
-  exchange_at<R>(a, xbuf, plane, col, k, bw, br);
+  exchange_at<R>(a, xbuf, plane, col, k, bw ^ fo, br);
 }
 
 // The same permutation of two states (the adjoint's psi and lambda), one after
 // the other through the buffer, with the slot bases formed once.
 template <int R>
 __device__ __forceinline__ void exchange2(St<R>& a, St<R>& l, float* xbuf, uint32_t plane,
-                                          const uint32_t* col, int k, int t, int stid, int sl) {
+                                          const uint32_t* col, int k, int t, int stid, int sl,
+                                          uint32_t fo = 0u) {
   uint32_t bw, br;
   exchange_bases<R>(col, k, t, stid, sl, bw, br);
-  exchange_at<R>(a, xbuf, plane, col, k, bw, br);
-  exchange_at<R>(l, xbuf, plane, col, k, bw, br);
+  exchange_at<R>(a, xbuf, plane, col, k, bw ^ fo, br);
+  exchange_at<R>(l, xbuf, plane, col, k, bw ^ fo, br);
+}
+
+// ------------------------------------------------------------ swap frame
+// In the generated kernels (tangent form) a CNOT whose control sits on a
+// thread / tile bit c and whose target sits on register bit r does not move
+// data: the thread records that its registers along bit r are swapped iff c
+// is set (a frame F = X_r^c, kept as a sign mask fs_r = c << 31), and the
+// state held is F times the true one.  A later gate G then runs as F G F:
+// RY and RZ on bit r with the angle negated (X RY X = RY(-theta), likewise
+// RZ), RX and everything on other bits unchanged, a register CNOT from r to
+// r' adds the frame X_r' (F CNOT = CNOT F X_r'); the adjoint's gradient of a
+// negated rotation is negated (Im <lambda| X P X |psi> = -Im <lambda|P|psi>
+// for P = Y, Z).  The frame is resolved where the positions matter: folded
+// into the write addresses of an LDS exchange or of a pass's stores (register
+// u goes to position u ^ f; the addresses are XOR-linear in u), or, before
+// anything else that reads positions, by one conditional swap per frame bit.
+
+// The XOR of the offsets of the frame's bits (off[2^b]: register bit b's column).
+template <int R>
+__device__ __forceinline__ uint32_t frame_offset(uint32_t fx, const uint32_t (&off)[1 << R]) {
+  uint32_t o = 0u;
+#pragma unroll
+  for (int b = 0; b < R; ++b) o ^= ((fx >> b) & 1u) ? off[1 << b] : 0u;
+  return o;
 }
 
 // ------------------------------------------------------- schedule runner
@@ -959,6 +988,9 @@ struct Walk {
   int k, t, S, G;
   int stid, sl, grp, width;
   uint32_t tb;        // tile bits above the register bits
+  // register bits (as a bit mask) whose swap frame a generated streaming pass
+  // left for the caller's stores (see swap frame below), 0 otherwise
+  mutable uint32_t fx;
   bool leader;
   bool never;         // false, but not provably so (see gate_boundary)
   unsigned char* smem;  // the workgroup's LDS (tables of the generated kernels)
@@ -1998,6 +2030,7 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.never = A.B < 0;
   w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
+  w.fx = 0u;
 
   if constexpr (Sched::kLoadTables) {
     // the sample's tables, written once per call by the table kernel
@@ -2055,9 +2088,9 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
 
   Sched::template run<R, BWD, true>(a, l, w, A.ins, A.n_ins);
 
-  // the stores, in the layout this pass writes
+  // the stores, in the layout this pass writes (with the swap frame run() left)
   io_offsets<R>(A.io_out, A.k, A.ng, tid, g, base, off);
-  base = opaque(base);
+  base = opaque(base ^ frame_offset<R>(w.fx, off));
   // the adjoint stores lambda only (its psi is the state the forward saved at
   // this pass's start), and nothing at all in its last pass
   if (!BWD) {
