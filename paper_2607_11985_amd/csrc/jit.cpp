@@ -481,9 +481,10 @@ std::string occ_scale(const Plan& p, uint32_t occ) {
 }
 
 // What a stream does with its swap frame at its end (vqc_device.h, "swap
-// frame"): resolve it (a reader of positions follows), leave it in w.fx for
-// the pass's stores, or drop it (nothing reads the state).
-enum FrameEnd { kFrameResolve, kFramePack, kFrameDrop };
+// frame"): resolve it (the epilogue or the stores read positions; a pass's
+// closing exchange has usually folded it already), or drop it (nothing reads
+// the state).
+enum FrameEnd { kFrameResolve, kFrameDrop };
 
 // Statements of one instruction stream for register width R.  With tangent
 // tables (tm.on) rotations use the tangent form and blocks are rescaled, and
@@ -820,14 +821,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   }
   if (batched) emit_flush(o, pend);
   if (frames) {
-    if (fend == kFrameResolve) {
-      resolve(dirty);
-    } else if (fend == kFramePack) {
-      o << "  w.fx = 0u";
-      for (int r = 0; r < R; ++r)
-        if ((dirty >> r) & 1u) o << " | ((fs" << r << " >> 31) << " << r << ")";
-      o << ";\n";
-    }
+    if (fend == kFrameResolve) resolve(dirty);
     for (int r = 0; r < R; ++r) o << "  (void)fs" << r << ";\n";
   }
 }
@@ -979,15 +973,11 @@ std::string kernel_unit(const Plan& p, const Frame& fr, const std::string& name,
   const int lanes = stream ? threads : 1 << (p.k - R);
   TanMode tm = tan_mode(p, bwd ? nullptr : ins, n_ins, bwd ? ins : nullptr, n_ins, S, esign, lds);
   tm.on = tm.on && tangent_wanted(S, R);
-  // the swap frame at the stream's end: a streaming pass's stores take it,
-  // unless its state is read in place after the sweep (<Z> and probabilities,
-  // the head partials); a resident forward resolves it for its epilogue
+  // the swap frame at the stream's end: resolved where the state is read or
+  // stored after the sweep, dropped by a resident adjoint and by the last
+  // streaming adjoint pass without a product head (nothing reads their states)
   FrameEnd fend = bwd ? kFrameDrop : kFrameResolve;
-  if (stream) {
-    if (bwd) fend = (fixed_flags & PF_LAST_ADJ) ? (head.empty() ? kFrameDrop : kFrameResolve)
-                                                 : kFramePack;
-    else fend = (fixed_flags & PF_ZPART) ? kFrameResolve : kFramePack;
-  }
+  if (stream && bwd && (!(fixed_flags & PF_LAST_ADJ) || !head.empty())) fend = kFrameResolve;
   emit_sched_struct(o, "Sched", p, ins, n_ins, bwd, R, p.k, S, grad_mode(lanes, n_slots), tm, &fr,
                     map_off, load, fixed_flags, nullptr, head, fend);
   o << "}  // namespace vqc\n"

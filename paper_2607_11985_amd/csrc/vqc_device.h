@@ -955,18 +955,10 @@ __device__ __forceinline__ void exchange2(St<R>& a, St<R>& l, float* xbuf, uint3
 // r' adds the frame X_r' (F CNOT = CNOT F X_r'); the adjoint's gradient of a
 // negated rotation is negated (Im <lambda| X P X |psi> = -Im <lambda|P|psi>
 // for P = Y, Z).  The frame is resolved where the positions matter: folded
-// into the write addresses of an LDS exchange or of a pass's stores (register
-// u goes to position u ^ f; the addresses are XOR-linear in u), or, before
-// anything else that reads positions, by one conditional swap per frame bit.
-
-// The XOR of the offsets of the frame's bits (off[2^b]: register bit b's column).
-template <int R>
-__device__ __forceinline__ uint32_t frame_offset(uint32_t fx, const uint32_t (&off)[1 << R]) {
-  uint32_t o = 0u;
-#pragma unroll
-  for (int b = 0; b < R; ++b) o ^= ((fx >> b) & 1u) ? off[1 << b] : 0u;
-  return o;
-}
+// into the write addresses of an LDS exchange (register u goes to position
+// u ^ f; the addresses are XOR-linear in u), or, before anything else that
+// reads positions (lane swaps, CZs, epilogues, stores), by one conditional
+// swap per frame bit.
 
 // ------------------------------------------------------- schedule runner
 
@@ -988,9 +980,6 @@ struct Walk {
   int k, t, S, G;
   int stid, sl, grp, width;
   uint32_t tb;        // tile bits above the register bits
-  // register bits (as a bit mask) whose swap frame a generated streaming pass
-  // left for the caller's stores (see swap frame below), 0 otherwise
-  mutable uint32_t fx;
   bool leader;
   bool never;         // false, but not provably so (see gate_boundary)
   unsigned char* smem;  // the workgroup's LDS (tables of the generated kernels)
@@ -2030,7 +2019,6 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   w.never = A.B < 0;
   w.smem = smem;
   w.tb = (uint32_t)tid | ((uint32_t)g << w.t);
-  w.fx = 0u;
 
   if constexpr (Sched::kLoadTables) {
     // the sample's tables, written once per call by the table kernel
@@ -2088,9 +2076,9 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
 
   Sched::template run<R, BWD, true>(a, l, w, A.ins, A.n_ins);
 
-  // the stores, in the layout this pass writes (with the swap frame run() left)
+  // the stores, in the layout this pass writes
   io_offsets<R>(A.io_out, A.k, A.ng, tid, g, base, off);
-  base = opaque(base ^ frame_offset<R>(w.fx, off));
+  base = opaque(base);
   // the adjoint stores lambda only (its psi is the state the forward saved at
   // this pass's start), and nothing at all in its last pass
   if (!BWD) {
