@@ -564,6 +564,22 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         o << "  const float G" << m << " = table_row(gmul, " << m << ", " << last << ");\n";
     }
   }
+  // The table entries of the next rotation are read one gate ahead (tangent
+  // form, tables in LDS): each gate is its own basic block (gate_boundary),
+  // so a read placed in the gate that uses it would leave the LDS latency
+  // exposed at every rotation.
+  std::vector<int> rots;
+  for (int pc = 0; pc < n_ins; ++pc) {
+    const int op = ins[2 * pc] & 31;
+    const int occ = (int)ins[2 * pc + 1];
+    if ((op == OP_RX || op == OP_RY || op == OP_RZ) && !(skip && (*skip)[occ])) rots.push_back(occ);
+  }
+  const bool ahead = tan && !sreg && !rots.empty();
+  size_t ri = 0;  // the next rotation's index in rots
+  if (ahead) {
+    o << "  float2 tcn = w.tab[" << rots[0] << "];\n";
+    if (bwd) o << "  float gmn = gmul[" << rots[0] << "];\n";
+  }
   // The sample's thread bits, computed once in the 4-amplitude kernels: their
   // few waves leave registers to spare, and each lane-bit gate then skips
   // recomputing its bit (and the sign mask formed from it) from an opaque
@@ -715,10 +731,19 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
         }
         const std::string at = std::to_string(arg) + " * " + std::to_string(S) + " + w.sl";
         if (tan) {
-          if (sreg)
+          if (sreg) {
             o << "  { const float2 tc = table_entry<" << arg % 64 << ">(T" << arg / 64 << "); ";
-          else
+          } else if (ahead) {
+            o << "  { const float2 tc = tcn; ";
+            if (bwd) o << "const float gm = gmn; ";
+            if (ri + 1 < rots.size()) {
+              o << "tcn = w.tab[" << rots[ri + 1] << "]; ";
+              if (bwd) o << "gmn = gmul[" << rots[ri + 1] << "]; ";
+            }
+            ++ri;
+          } else {
             o << "  { const float2 tc = w.tab[" << arg << "]; ";
+          }
           // negated under the swap frame (RY, RZ on a frame bit)
           const bool neg = reg && op != OP_RX && ((dirty >> pa) & 1u);
           if (neg)
@@ -750,6 +775,8 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
             // the states carry 1 / (the factors of the block before this gate)
             if (sreg)
               o << " g *= table_entry<" << arg % 64 << ">(G" << arg / 64 << ") * (bp * bp);";
+            else if (ahead)
+              o << " g *= gm * (bp * bp);";
             else
               o << " g *= gmul[" << arg << "] * (bp * bp);";
             o << occ_scale(p, arg);
