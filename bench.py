@@ -1,9 +1,10 @@
 """Throughput of the batched VQC hot path on one MI355X.
 
 One step = one pass of the whole hot path over one batch of synthetic input:
-forward (every gate, <Z>), the workload's loss-head cotangent, and the adjoint
-sweep (gradients for every parameter and input), on one HIP stream with the
-inputs resident in HBM.  A step is one vqc_train_step call (a single launch on
+forward (the circuit's gates, the state after every qubit's leading rotations
+built as a product, gates that change no output left out; <Z>), the
+workload's loss-head cotangent, and the adjoint sweep (gradients for every
+parameter and input), on one HIP stream with the inputs resident in HBM.  A step is one vqc_train_step call (a single launch on
 the resident path: the state never leaves the chip; the streaming passes
 otherwise); --separate times vqc_forward + vqc_loss_grad + vqc_backward.
 
@@ -338,7 +339,8 @@ def measure(idx, args, torch, dev, want_cpu, cpu_budget):
     for _ in range(max(Wm, 1)):
         fused(s)
     torch.cuda.synchronize()
-    # the fused step reproduces the separate calls (up to the compiler's rounding)
+    # the fused step reproduces the separate calls up to rounding (it builds the
+    # heads' state as a product where the separate calls run their gates)
     dev_max = max(float((t - r).abs().max()) if t.numel() else 0.0
                   for t, r in zip((E, g, dp, dx), ref))
     if dev_max > 1e-5:

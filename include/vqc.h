@@ -328,7 +328,12 @@ int vqc_loss_grad(int32_t kind, int64_t batch, int32_t n_qubits, const float *ex
  *   vqc_workspace_bytes(c, batch, 2) bytes, 256-byte aligned (on the resident
  *   path 0 bytes / NULL unless shared_params).
  * On the streaming path the batch halves run on two streams (see
- * vqc_workspace_bytes).  Results equal those of the three separate calls.  Errors: those of the
+ * vqc_workspace_bytes).  Results equal those of the three separate calls up
+ * to float rounding: with the generated kernels the step builds the state
+ * after every qubit's leading rotations (those before any entangler on it) as
+ * a product state and takes their gradients from lambda contracted against
+ * it, where the separate calls run them as gates (on the streaming path with
+ * a plan of its own, which vqc_circuit_info reports).  Errors: those of the
  * three calls.
  */
 int vqc_train_step(const vqc_circuit *c, int64_t batch, const float *params, const float *inputs,
