@@ -518,14 +518,15 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   };
   const int nrot = (int)(bwd ? tm.bocc.size() : tm.focc.size());
   int m = 0;  // rotation index in the stream
-  // batched up to 8 amplitudes per thread, and with 16 in the streaming passes
-  // (the pending partials fit beside psi and lambda: 109-120 VGPRs, four waves
-  // per SIMD; the 16-qubit adjoint 15 % fewer instructions, 1.93 -> 1.79 ms).
-  // The resident 16-amplitude kernels are left out: there the partials took
-  // the kernel from 108 to 147 VGPRs and one wave per SIMD, and the 12-qubit
-  // step ran 5 % slower.
-  const bool batched =
-      bwd && gm.regs && gm.tm == 64 && (R <= 3 || (R == 4 && p.path == VQC_PATH_STREAM));
+  // batched pending partials (a reduce-scatter per 16 slots instead of a DPP
+  // sum per rotation).  With 16 amplitudes per thread the pending registers
+  // sit beside psi and lambda: the streaming passes stay at 109-120 VGPRs, four
+  // waves per SIMD (16-qubit adjoint 15 % fewer instructions, 1.93 -> 1.79
+  // ms); the resident kernels go from four waves per SIMD to three (the
+  // 12-qubit backward 110 -> 150 VGPRs) or stay at three (the 12-qubit step,
+  // 168 VGPRs and the same spills) and still gain: step 0.879 -> 0.838 ms,
+  // backward 0.666 -> 0.654 ms.
+  const bool batched = bwd && gm.regs && gm.tm == 64 && R <= 4;
   Pending pend;
   if (batched)
     o << "  float pd0 = 0.f, pd1 = 0.f, pd2 = 0.f, pd3 = 0.f, pd4 = 0.f, pd5 = 0.f, pd6 = 0.f, "
