@@ -607,22 +607,12 @@ int vqc_compile(const vqc_op* ops, int32_t n_ops, int32_t n_qubits, int32_t n_pa
         4 * (p12.fpass.size() + p12.bpass.size()) <= 5 * n13)
       c->plan = std::move(p12);
   }
-  // The generated adjoint passes hold 16 amplitudes per thread by default (the
-  // batched gradient reduction fits there).  32 halve the workgroups per CU that
-  // hide each pass's loads and stores, and pay off only where they remove at
-  // least a fifth of the adjoint's exchanges and at least three per pass.
-  // Measured: the 14-qubit re-uploading workload (2 passes, 36 -> 27
-  // exchanges) 3 % faster; the 16-qubit ring (10-11 passes, 71 -> 61 and
-  // 62 -> 49 exchanges) 13-25 % slower.
-  if (engine == VQC_ENGINE_JIT && reg_bits == 0 && c->plan.path == VQC_PATH_STREAM) {
-    Plan p5;
-    std::string msg5;
-    if (vqc::build_plan(hops, n_qubits, n_params, n_inputs, path, 0, p5, msg5, true, c->plan.k,
-                        5) == 0 &&
-        5 * p5.bwd_exchanges <= 4 * c->plan.bwd_exchanges &&
-        c->plan.bwd_exchanges - p5.bwd_exchanges >= 3 * (int)c->plan.bpass.size())
-      c->plan = std::move(p5);
-  }
+  // The generated adjoint passes hold 16 amplitudes per thread (the batched
+  // gradient reduction fits there); reg_bits = 5 asks for 32.  32 halve the
+  // workgroups per CU that hide each pass's loads and stores.  Measured on one
+  // box: the 14-qubit re-uploading workload 11.58 ms per step at 32 (26
+  // exchanges) against 11.10 ms at 16 (33 exchanges); the 16-qubit ring was
+  // 13-25 % slower at 32.
   c->device = device;
   c->engine = engine;
   c->shared = shared;

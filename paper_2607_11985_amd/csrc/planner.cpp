@@ -795,8 +795,7 @@ void stream_lds(Plan& plan) {
 }
 
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
-               Plan& plan, std::string& msg, bool lane_gates, int tile_qubits,
-               int bwd_reg_bits) {
+               Plan& plan, std::string& msg, bool lane_gates, int tile_qubits) {
   if (n < 1 || n > kMaxQubits) {
     msg = "n_qubits must be in [1, " + std::to_string(kMaxQubits) + "]";
     return n < 1 ? VQC_ERR_INVALID_ARG : VQC_ERR_TOO_LARGE;
@@ -963,7 +962,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     plan.k = tile_qubits ? tile_qubits : lane_gates ? kMaxTileQubits - 1 : kMaxTileQubits;
     plan.ng = nq - plan.k;
     plan.Rf = reg_bits ? reg_bits : kStreamRegBitsFwd;
-    plan.Rb = reg_bits ? reg_bits : bwd_reg_bits ? bwd_reg_bits : kStreamRegBitsBwd;
+    plan.Rb = reg_bits ? reg_bits : kStreamRegBitsBwd;
     plan.t = plan.k - plan.Rf;       // the forward's geometry (informational)
     plan.WG = 1 << plan.t;
     plan.S = 1;

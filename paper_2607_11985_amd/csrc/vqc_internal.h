@@ -90,11 +90,9 @@ struct HostOp {
 constexpr int kNumGateKinds = 32;  // VQC_RX .. VQC_CSWAP
 // lane_gates: the schedule may put RX / RY / CNOT targets on lane bits (only
 // the generated kernels run such schedules).
-// tile_qubits: streaming tile size (0 = default).  bwd_reg_bits: register
-// bits of the streaming adjoint when reg_bits is 0 (0 = default).
+// tile_qubits: streaming tile size (0 = default).
 int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, int reg_bits,
-               Plan& plan, std::string& msg, bool lane_gates, int tile_qubits = 0,
-               int bwd_reg_bits = 0);
+               Plan& plan, std::string& msg, bool lane_gates, int tile_qubits = 0);
 // Gradient slots (P + F) up to which the streaming training step runs a plan
 // without the heads (its head kernel holds a row of them in LDS).
 constexpr int kMaxStepSlots = 8192;
