@@ -525,8 +525,11 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   // ms); the resident kernels go from four waves per SIMD to three (the
   // 12-qubit backward 110 -> 150 VGPRs) or stay at three (the 12-qubit step,
   // 168 VGPRs and the same spills) and still gain: step 0.879 -> 0.838 ms,
-  // backward 0.666 -> 0.654 ms.
-  const bool batched = bwd && gm.regs && gm.tm == 64 && R <= 4;
+  // backward 0.666 -> 0.654 ms.  Not in 1024-thread workgroups (a 14-qubit
+  // resident sample): those hold at most 128 VGPRs, and the pending registers
+  // spilled 1.1 KiB per thread there (569 k -> 444 k evals/s).
+  const bool batched = bwd && gm.regs && gm.tm == 64 && R <= 4 &&
+                       !(p.path == VQC_PATH_RESIDENT && (1 << (k - R)) > 512);
   Pending pend;
   if (batched)
     o << "  float pd0 = 0.f, pd1 = 0.f, pd2 = 0.f, pd3 = 0.f, pd4 = 0.f, pd5 = 0.f, pd6 = 0.f, "
