@@ -367,6 +367,18 @@ void push_io(const Mapping& m, const int* pos, int k, int R, std::vector<uint32_
   cols.insert(cols.end(), g.begin(), g.end());
 }
 
+// True if the n columns at cols[off] are distinct single bits: a tile's loads
+// and stores add a lane's address bits to a register's (streaming kernel).
+bool one_hot_columns(const std::vector<uint32_t>& cols, int off, int n) {
+  uint32_t seen = 0;
+  for (int i = 0; i < n; ++i) {
+    const uint32_t c = cols[off + i];
+    if (c == 0 || (c & (c - 1)) || (seen & c)) return false;
+    seen |= c;
+  }
+  return true;
+}
+
 // Plans the sweeps of the passes `groups` (one direction): each starts in the
 // tile I/O mapping of its input layout, runs its gates, and ends in the I/O
 // mapping of its output layout (no closing exchange when it stores nothing).
@@ -418,6 +430,11 @@ int plan_stream(Plan& plan, const std::vector<StreamGroup>& groups,
     push_io(io_in, ident, k, R, plan.cols);
     pp.io_lout_off = (int)plan.cols.size();
     push_io(m, ident, k, R, plan.cols, plan.pcol.empty() ? nullptr : plan.pcol.data());
+    if (!one_hot_columns(plan.cols, pp.io_off, nq) || !one_hot_columns(plan.cols, pp.io_out_off, nq) ||
+        !one_hot_columns(plan.cols, pp.io_lin_off, nq)) {
+      msg = "internal: tile address columns are not distinct bits";
+      return VQC_ERR_UNSUPPORTED;
+    }
     pp.slots_off = (int)plan.pslots.size();
     pp.n_slots = (int)slots.size();
     plan.pslots.insert(plan.pslots.end(), slots.begin(), slots.end());

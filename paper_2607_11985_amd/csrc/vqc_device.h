@@ -1941,13 +1941,42 @@ __device__ __forceinline__ void io_offsets(const uint32_t* io, int k, int ng, in
   for (int j = 0; j < (1 << R); ++j) off[j] = xor_cols<R>(j, c);
 }
 
+// A sample's state as a raw buffer (base: its first amplitude, `bytes` its
+// size; an access beyond it reads zero and stores nothing).  The load and
+// store columns are single address bits, distinct over the tile's ranks and
+// global bits, so a lane's bits (base) and a register's (off, uniform over the
+// workgroup) never overlap and their XOR is their sum: the lane's byte offset
+// is the access's vector offset and the register's its scalar offset, with no
+// address arithmetic per amplitude.
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t state_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ float2 amp_load(__amdgpu_buffer_rsrc_t r, uint32_t base_b, uint32_t off) {
+  const uint32_t so = (uint32_t)__builtin_amdgcn_readfirstlane((int)(off << 3));
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, base_b, so, 0);
+  return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
+}
+
+__device__ __forceinline__ void amp_store(__amdgpu_buffer_rsrc_t r, uint32_t base_b, uint32_t off,
+                                          float re, float im) {
+  const uint32_t so = (uint32_t)__builtin_amdgcn_readfirstlane((int)(off << 3));
+  u32x2 v;
+  v.x = __float_as_uint(re);
+  v.y = __float_as_uint(im);
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, base_b, so, 0);
+}
+
 // All loads are issued before the first split, so that they overlap.
 template <int R>
-__device__ __forceinline__ void load_tile(St<R>& a, const float2* src, uint32_t base,
+__device__ __forceinline__ void load_tile(St<R>& a, __amdgpu_buffer_rsrc_t src, uint32_t base,
                                           const uint32_t (&off)[1 << R]) {
+  const uint32_t base_b = base << 3;
   float2 v[1 << R];
 #pragma unroll
-  for (int j = 0; j < (1 << R); ++j) v[j] = src[base ^ off[j]];
+  for (int j = 0; j < (1 << R); ++j) v[j] = amp_load(src, base_b, off[j]);
 #pragma unroll
   for (int j = 0; j < (1 << R); ++j) split(v[j], a.r[j], a.i[j]);
 }
@@ -2048,6 +2077,12 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
   const bool logical_in = !BWD && !(flags & PF_INIT) && A.psi0_in;
   io_offsets<R>(logical_in ? A.io_lin : A.io, A.k, A.ng, tid, g, base, off);
   const size_t sbase = (size_t)b << (A.k + A.ng);
+  const uint32_t sbytes = 8u << (A.k + A.ng);
+  // the register columns of the layout this pass writes, read before the gate
+  // sequence (its barriers would make a later read a per-lane one)
+  uint32_t oc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) oc[r] = A.io_out[A.k - R + r];
   St<R> a, l;
   if (!BWD && (flags & PF_INIT)) {
     if constexpr (Sched::kProductStart) {
@@ -2061,16 +2096,16 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
       if (tid == 0 && g == 0) a.r[0] = 1.f;
     }
   } else {
-    const float2* src = reinterpret_cast<const float2*>(A.psi_src) + sbase;
-    load_tile<R>(a, src, base, off);
+    load_tile<R>(a, state_rsrc(reinterpret_cast<const float2*>(A.psi_src) + sbase, sbytes), base,
+                 off);
   }
   if (BWD) {
     if (flags & PF_MAKE_LAMBDA) {
       make_lambda<R, Sched>(l, a, A.grad_out + b * A.n, A.n, A.start_phys, A.zmask, w.tb, true,
                             Sched::esigns(w));
     } else {
-      const float2* src = reinterpret_cast<const float2*>(A.lam_src) + sbase;
-      load_tile<R>(l, src, base, off);
+      load_tile<R>(l, state_rsrc(reinterpret_cast<const float2*>(A.lam_src) + sbase, sbytes),
+                   base, off);
     }
   }
 
@@ -2078,19 +2113,21 @@ __device__ __forceinline__ void stream_body(const PassArgs& A, unsigned char* sm
 
   // the stores, in the layout this pass writes
   io_offsets<R>(A.io_out, A.k, A.ng, tid, g, base, off);
-  base = opaque(base);
+#pragma unroll
+  for (int j = 0; j < NA; ++j) off[j] = xor_cols<R>(j, oc);
+  const uint32_t base_b = opaque(base) << 3;
   // the adjoint stores lambda only (its psi is the state the forward saved at
   // this pass's start), and nothing at all in its last pass
   if (!BWD) {
-    float2* dst = reinterpret_cast<float2*>(A.psi_dst) + sbase;
+    const auto dst = state_rsrc(reinterpret_cast<float2*>(A.psi_dst) + sbase, sbytes);
 #pragma unroll
-    for (int j = 0; j < NA; ++j) dst[base ^ off[j]] = make_float2(a.r[j], a.i[j]);
+    for (int j = 0; j < NA; ++j) amp_store(dst, base_b, off[j], a.r[j], a.i[j]);
   }
   if (BWD) {
     if (!(flags & PF_LAST_ADJ)) {
-      float2* dst = reinterpret_cast<float2*>(A.lam_dst) + sbase;
+      const auto dst = state_rsrc(reinterpret_cast<float2*>(A.lam_dst) + sbase, sbytes);
 #pragma unroll
-      for (int j = 0; j < NA; ++j) dst[base ^ off[j]] = make_float2(l.r[j], l.i[j]);
+      for (int j = 0; j < NA; ++j) amp_store(dst, base_b, off[j], l.r[j], l.i[j]);
     }
     if constexpr (Sched::kHeadPartials) {
       // lambda where the heads end, contracted against the heads' states
