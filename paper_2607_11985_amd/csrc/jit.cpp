@@ -390,42 +390,65 @@ struct Pending {
   }
 };
 
+// Whether an adjoint stream batches its gradient partials (emit_flush): the
+// accumulator registers then hold slot 64 r + flush_slot(lane) in register r.
+bool batched_flush(const Plan& p, bool bwd, const GradMode& gm, int R, int k) {
+  return bwd && gm.regs && gm.tm == 64 && R <= 4 &&
+         !(p.path == VQC_PATH_RESIDENT && (1 << (k - R)) > 512);
+}
+
+// Reduce-scatter of the 16 pending partials over the wave's 64 lanes.
+// Position bit 3 pairs across lane bit 5 and bit 2 across lane bit 4, each
+// pair one permlane swap (the upper half's first operand trades with the lower
+// half's second) and one addition; bits 1 and 0 across lane bits 1 and 0, a
+// select pair and a DPP addition each; then a sum over lane bits 2 and 3 (two
+// DPP row rotations).  Lane L ends with the total of position
+// (L5 L4 L1 L0) and adds it to slot 64 r + s when s % 16 is that position and
+// s / 16 is (L3 L2): slot s of register r lives in lane
+// (s3 s2 s5 s4 s1 s0), the layout the accumulators are written out in.
 void emit_flush(std::ostringstream& o, Pending& pd) {
   if (pd.empty()) return;
-  static const int kSteps[4][2] = {{2, 0x141}, {0, 0xB1}, {1, 0x4E}, {3, 0x128}};
   o << "  { float v[16];\n";
   for (int j = 0; j < 16; ++j)
     o << "    v[" << j << "] = " << (pd.tag[j] >= 0 ? "pd" + std::to_string(j) : "0.f") << ";\n";
   o << "    const uint32_t lo = opaque(ln);\n";
-  int live = 16;  // values left, at indices 0..live-1 after compaction
-  std::vector<int> bits_left = {0, 1, 2, 3};
-  // value index -> position: keep a map from the remaining value-index bits
-  std::vector<int> order;  // value-index bits still present, low to high in position
-  order = {0, 1, 2, 3};
-  for (const auto& st : kSteps) {
-    const int b = st[0], ctrl = st[1];
-    // position bit of value-index bit b among the remaining bits
-    int pos = 0;
-    while (order[pos] != b) ++pos;
-    const int half = live / 2;
-    o << "    { const bool hb = (lo >> " << b << ") & 1u;\n";
+  // positions that may hold a partial, over the steps
+  uint32_t used = 0;
+  for (int j = 0; j < 16; ++j)
+    if (pd.tag[j] >= 0) used |= 1u << j;
+  auto swap_step = [&](int half, const char* fn) {
+    uint32_t next = 0;
     for (int q = 0; q < half; ++q) {
-      // positions with bit `pos` 0 / 1
-      const int lowmask = (1 << pos) - 1;
-      const int p0 = ((q & ~lowmask) << 1) | (q & lowmask);
-      const int p1 = p0 | (1 << pos);
-      o << "      const float k" << q << " = hb ? v[" << p1 << "] : v[" << p0 << "];\n"
-        << "      const float s" << q << " = hb ? v[" << p0 << "] : v[" << p1 << "];\n";
+      const bool a = (used >> q) & 1u, b = (used >> (q + half)) & 1u;
+      if (!a && !b) continue;
+      o << "    " << fn << "(v[" << q << "], v[" << q + half << "]); v[" << q << "] += v["
+        << q + half << "];\n";
+      next |= 1u << q;
     }
-    for (int q = 0; q < half; ++q)
-      o << "      v[" << q << "] = k" << q << " + dpp_f<" << ctrl << ">(s" << q << ");\n";
+    used = next;
+  };
+  swap_step(8, "swap_pair32");  // position bit 3 <-> lane bit 5
+  swap_step(4, "swap_pair16");  // position bit 2 <-> lane bit 4
+  // position bit 1 <-> lane bit 1, then bit 0 <-> lane bit 0 (quad_perm 2301, 1032)
+  static const int kDpp[2][3] = {{2, 1, 0x4E}, {1, 0, 0xB1}};
+  for (const auto& st : kDpp) {
+    const int half = st[0], lb = st[1], ctrl = st[2];
+    uint32_t next = 0;
+    o << "    { const bool hb = (lo >> " << lb << ") & 1u;\n";
+    for (int q = 0; q < half; ++q) {
+      const bool a = (used >> q) & 1u, b = (used >> (q + half)) & 1u;
+      if (!a && !b) continue;
+      o << "      const float k" << q << " = hb ? v[" << q + half << "] : v[" << q << "];\n"
+        << "      const float s" << q << " = hb ? v[" << q << "] : v[" << q + half << "];\n"
+        << "      v[" << q << "] = k" << q << " + dpp_f<" << ctrl << ">(s" << q << ");\n";
+      next |= 1u << q;
+    }
     o << "    }\n";
-    order.erase(order.begin() + pos);
-    live = half;
+    used = next;
   }
-  o << "    float tot = v[0] + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v[0]), 0x401F));\n"
-    << "    tot += __shfl_xor(tot, 32, 64);\n";
-  // lane L holds the total of value index L % 16 (identity map of bits)
+  // lane bits 2 and 3: row_ror 4, row_ror 8
+  o << "    float tot = v[0] + dpp_f<0x124>(v[0]);\n"
+    << "    tot += dpp_f<0x128>(tot);\n";
   std::map<int, std::pair<uint32_t, uint32_t>> byreg;  // register -> (position mask, row table)
   for (int j = 0; j < 16; ++j) {
     if (pd.tag[j] < 0) continue;
@@ -434,7 +457,7 @@ void emit_flush(std::ostringstream& o, Pending& pd) {
     e.first |= 1u << j;
     e.second |= (uint32_t)((slot % 64) >> 4) << (2 * j);
   }
-  o << "    const uint32_t j = lo & 15u, row = lo >> 4;\n";
+  o << "    const uint32_t j = (lo & 3u) | ((lo >> 2) & 12u), row = (lo >> 2) & 3u;\n";
   for (const auto& kv : byreg)
     o << "    ga[" << kv.first << "] += ((" << hex(kv.second.first) << " >> j) & 1u) && row == (("
       << hex(kv.second.second) << " >> (2u * j)) & 3u) ? tot : 0.f;\n";
@@ -528,8 +551,7 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   // backward 0.666 -> 0.654 ms.  Not in 1024-thread workgroups (a 14-qubit
   // resident sample): those hold at most 128 VGPRs, and the pending registers
   // spilled 1.1 KiB per thread there (569 k -> 444 k evals/s).
-  const bool batched = bwd && gm.regs && gm.tm == 64 && R <= 4 &&
-                       !(p.path == VQC_PATH_RESIDENT && (1 << (k - R)) > 512);
+  const bool batched = batched_flush(p, bwd, gm, R, k);
   Pending pend;
   if (batched)
     o << "  float pd0 = 0.f, pd1 = 0.f, pd2 = 0.f, pd3 = 0.f, pd4 = 0.f, pd5 = 0.f, pd6 = 0.f, "
@@ -961,7 +983,10 @@ void emit_sched_struct(std::ostringstream& o, const std::string& name, const Pla
   emit_schedule(o, p, ins, n_ins, bwd, R, k, S, gm, tm, skip, fend);
   if (regs)  // every (slot, group) accumulator is written by exactly one lane
     o << "#pragma unroll\n  for (int j = 0; j < " << gm.nr << "; ++j) {\n"
-      << "    const uint32_t slot = j * " << gm.tm << "u + ln;\n"
+      << "    const uint32_t slot = j * " << gm.tm << "u + "
+      << (batched_flush(p, bwd, gm, R, k) ? "((ln & 3u) | ((ln >> 2) & 12u) | ((ln << 2) & 48u))"
+                                          : "ln")
+      << ";\n"
       << "    if (slot < " << gm.ns << "u) w.acc[slot * w.G + w.grp] = ga[j];\n  }\n";
   o << "}\n"
     << "__device__ __forceinline__ static float lane_sum(float v, const Walk&) {\n"
