@@ -512,6 +512,59 @@ enum FrameEnd { kFrameResolve, kFrameDrop };
 // Statements of one instruction stream for register width R.  With tangent
 // tables (tm.on) rotations use the tangent form and blocks are rescaled, and
 // CNOTs from a thread / tile bit onto a register bit go to the swap frame.
+// Whether a rotation joins a run of RZs applied as one diagonal: an RZ whose
+// angle is not a constant.  A constant's float (cos, sin) pair is chosen so
+// that the norm errors of the circuit's constant gates cancel one by one;
+// in a product their rounding is the same every time the same gates come
+// round and would add up instead.
+bool fusable_rz(const Plan& p, uint32_t w0, uint32_t occ) {
+  return (w0 & 31) == OP_RZ && p.occ_src[occ] != kSrcConst;
+}
+
+// Orders each stretch of single-qubit rotations (no entangler or exchange
+// between them, so rotations on different bits commute) so that the fusable
+// RZs on different bits come together: every such RZ at the head of its
+// bit's sequence, then one other rotation from each bit, and again.  A Rot
+// layer (RZ RY RZ on every qubit) becomes a run of RZs, the RYs, and another
+// run of RZs.
+std::vector<uint32_t> cluster_diagonals(const Plan& p, const uint32_t* ins, int n_ins) {
+  std::vector<uint32_t> out(ins, ins + 2 * n_ins);
+  auto is_rot = [&](int i) {
+    const int op = ins[2 * i] & 31;
+    return op == OP_RX || op == OP_RY || op == OP_RZ;
+  };
+  auto is_rz = [&](int i) { return fusable_rz(p, ins[2 * i], ins[2 * i + 1]); };
+  for (int pc = 0; pc < n_ins;) {
+    if (!is_rot(pc)) {
+      ++pc;
+      continue;
+    }
+    int end = pc;
+    while (end < n_ins && is_rot(end)) ++end;
+    std::map<int, std::vector<int>> seq;  // physical bit -> its rotations, in order
+    for (int i = pc; i < end; ++i) seq[(ins[2 * i] >> 5) & 31].push_back(i);
+    std::map<int, size_t> head;
+    int w = pc;
+    auto put = [&](int i) {
+      out[2 * w] = ins[2 * i];
+      out[2 * w + 1] = ins[2 * i + 1];
+      ++w;
+    };
+    while (w < end) {
+      for (auto& kv : seq) {
+        size_t& h = head[kv.first];
+        while (h < kv.second.size() && is_rz(kv.second[h])) put(kv.second[h++]);
+      }
+      for (auto& kv : seq) {
+        size_t& h = head[kv.first];
+        if (h < kv.second.size() && !is_rz(kv.second[h])) put(kv.second[h++]);
+      }
+    }
+    pc = end;
+  }
+  return out;
+}
+
 void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, int n_ins, bool bwd,
                    int R, int k, int S, const GradMode& gm, const TanMode& tm,
                    const std::vector<char>* skip = nullptr, FrameEnd fend = kFrameResolve) {
@@ -522,6 +575,13 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   // (not in the kernels with gates on lane bits: there the lane swaps, which
   // would have to resolve the frame first, follow most CNOTs)
   const bool frames = tan && p.lanes == 0;
+  // runs of RZs on different bits become one diagonal (emit_rz_run below)
+  const bool fuse = frames && S == 1 && R >= 3;
+  std::vector<uint32_t> clustered;
+  if (fuse) {
+    clustered = cluster_diagonals(p, ins, n_ins);
+    ins = clustered.data();
+  }
   uint32_t dirty = 0;
   if (frames) {
     o << "  uint32_t";
@@ -618,6 +678,275 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   // a thread bit of the amplitude position (physical bit p >= R)
   auto bit = [&](int p) {
     return hbits ? "hb" + std::to_string(p - R) : "tile_bit<R>(w, " + std::to_string(p) + ")";
+  };
+  // A run of RZs (tangent form: amplitude x times 1 - i t z(x) per gate) is
+  // one diagonal D: the forward multiplies each amplitude by D once.  The
+  // adjoint takes every gradient of the run from Im(conj(lambda) psi), which
+  // no diagonal gate changes (the tangent form scales it by 1 / cos^2 per
+  // gate, which the block factor bp carries), then multiplies psi and lambda
+  // by the inverse diagonal once.  D is formed over the run's register bits
+  // but the highest (one product per value of the others) and applied in
+  // two halves, so that at most 8 complex values of it are live.
+  struct RzItem {
+    int occ, bit, slot;
+  };
+  auto fused_cheaper = [&](const std::vector<RzItem>& run) {
+    if (run.size() < 2) return false;
+    const int N = 1 << R;
+    int nt = 0, extra = 0;
+    uint32_t B = 0;
+    for (const auto& it : run) {
+      if (it.bit >= R) ++nt;
+      else {
+        if ((B >> it.bit) & 1u) ++extra;
+        B |= 1u << it.bit;
+      }
+    }
+    const int mb = __builtin_popcount(B);
+    int build = 2 * nt + 4 * extra;
+    for (int i = 1; i < mb; ++i) build += 4 << (i - 1);
+    if (mb) build += 4 << (mb - 1);
+    const int states = bwd ? 2 : 1;
+    const int fused = build + states * 4 * N + (bwd ? 3 * N + 3 * (int)run.size() : 0);
+    const int sep = (int)run.size() * (bwd ? 6 : 2) * N;
+    return 10 * fused < 9 * sep;
+  };
+  auto emit_rz_run = [&](const std::vector<RzItem>& run) {
+    const int N = 1 << R, L = (int)run.size();
+    const char* sg = bwd ? "" : "-";  // factor 1 + i sg x for z = +1
+    o << "  { // " << L << " RZs as one diagonal\n";
+    if (rots[ri] != run[0].occ) o << "#error rotation prefetch out of order\n";
+    for (int i = 0; i < L; ++i) {
+      if (i == 0) {
+        o << "    const float2 tc0 = tcn;";
+        if (bwd) o << " const float gm0 = gmn;";
+      } else {
+        o << "    const float2 tc" << i << " = w.tab[" << run[i].occ << "];";
+        if (bwd) o << " const float gm" << i << " = gmul[" << run[i].occ << "];";
+      }
+      o << "\n";
+    }
+    ri += L;
+    if (ri < rots.size()) {
+      o << "    tcn = w.tab[" << rots[ri] << "];";
+      if (bwd) o << " gmn = gmul[" << rots[ri] << "];";
+      o << "\n";
+    }
+    uint32_t B = 0;
+    int nt = 0;
+    for (int i = 0; i < L; ++i) {
+      const int b = run[i].bit;
+      const bool neg = b < R && ((dirty >> b) & 1u);
+      o << "    const float t" << i << " = "
+        << (neg ? "flip_sign(tc" + std::to_string(i) + ".x, fs" + std::to_string(b) + ")"
+                : "tc" + std::to_string(i) + ".x")
+        << ";\n";
+      if (b >= R) {
+        // t times the thread's z on its bit
+        o << "    const float z" << i << " = flip_sign(t" << i << ", " << bit(b) << " << 31);\n";
+        ++nt;
+      } else {
+        B |= 1u << b;
+      }
+    }
+    if (bwd) {
+      // the gradients, all from Im(conj(lambda) psi) at the run's output
+      for (int u = 0; u < N; ++u)
+        o << "    const float I" << u << " = fmaf(-l.i[" << u << "], a.r[" << u << "], l.r[" << u
+          << "] * a.i[" << u << "]);\n";
+      std::vector<std::string> P(N);
+      for (int u = 0; u < N; ++u) P[u] = "I" + std::to_string(u);
+      for (int j = 0; j < R; ++j) {
+        const int half = (int)P.size() / 2;
+        if ((B >> j) & 1u) {  // sum over z on register bit j
+          o << "    const float gb" << j << " = ";
+          for (int w2 = 0; w2 < half; ++w2)
+            o << (w2 ? " + " : "") << "(" << P[2 * w2] << " - " << P[2 * w2 + 1] << ")";
+          o << ";\n";
+        }
+        if (!nt && !(B >> (j + 1))) break;
+        std::vector<std::string> Q(half);
+        for (int w2 = 0; w2 < half; ++w2) {
+          Q[w2] = "P" + std::to_string(j) + "_" + std::to_string(w2);
+          o << "    const float " << Q[w2] << " = " << P[2 * w2] << " + " << P[2 * w2 + 1] << ";\n";
+        }
+        P.swap(Q);
+      }
+      o << "    const float bb = bp * bp;\n";
+      for (int i = 0; i < L; ++i) {
+        const int b = run[i].bit, slot = run[i].slot;
+        if (batched && slot >= 0) {
+          const int pos = slot & 15;
+          if (pend.tag[pos] >= 0 && pend.tag[pos] != slot) emit_flush(o, pend);
+        }
+        std::string g;
+        if (b >= R)
+          g = "flip_sign(" + P[0] + ", " + bit(b) + " << 31)";
+        else if ((dirty >> b) & 1u)
+          g = "flip_sign(gb" + std::to_string(b) + ", fs" + std::to_string(b) + ")";
+        else
+          g = "gb" + std::to_string(b);
+        o << "    { float g = " << g << "; g *= gm" << i << " * bb;" << occ_scale(p, run[i].occ);
+        if (slot < 0) {
+          o << " (void)g;";
+        } else if (batched) {
+          const int pos = slot & 15;
+          o << " pd" << pos << (pend.tag[pos] == slot ? " += g;" : " = g;")
+            << " asm volatile(\"\" : \"+v\"(pd" << pos << "));";
+          pend.tag[pos] = slot;
+        } else if (gm.regs) {
+          o << " const float gs = group_sum<" << gm.tm << ">(g); ga[" << slot / gm.tm
+            << "] += (opaque(ln) == " << slot % gm.tm << "u) ? gs : 0.f; asm volatile(\"\" : \"+v\"(ga["
+            << slot / gm.tm << "]));";
+        } else {
+          o << " { const float gs = group_sum<" << gm.tm << ">(g); if (w.leader) atomicAdd(&w.acc["
+            << slot << " * w.G + w.grp], gs); }";
+        }
+        o << " }\n";
+      }
+    }
+    for (int i = 0; i < L; ++i) o << "    bp *= tc" << i << ".y;\n";
+    // the thread part: the product of 1 + i sg z over the thread-bit RZs
+    bool haveT = false;
+    for (int i = 0; i < L; ++i) {
+      if (run[i].bit < R) continue;
+      const std::string x = std::string(sg) + "z" + std::to_string(i);
+      if (!haveT) {
+        o << "    float Tr = 1.f, Ti = " << x << ";\n";
+        haveT = true;
+      } else {
+        o << "    { const float x = " << x << ", nr = fmaf(-x, Ti, Tr); Ti = fmaf(x, Tr, Ti); Tr = nr; }\n";
+      }
+    }
+    // per register bit: the factor for z = +1 (that for z = -1 is its conjugate)
+    std::map<int, int> cnt;
+    for (int i = 0; i < L; ++i)
+      if (run[i].bit < R) ++cnt[run[i].bit];
+    std::map<int, bool> simple;
+    for (const auto& kv : cnt) {
+      const int b = kv.first;
+      simple[b] = kv.second == 1;
+      bool first = true;
+      for (int i = 0; i < L; ++i) {
+        if (run[i].bit != b) continue;
+        const std::string x = std::string(sg) + "t" + std::to_string(i);
+        if (simple[b]) {
+          o << "    const float s" << b << " = " << x << ";\n";
+        } else if (first) {
+          o << "    float F" << b << "r = 1.f, F" << b << "i = " << x << ";\n";
+        } else {
+          o << "    { const float x = " << x << ", nr = fmaf(-x, F" << b << "i, F" << b
+            << "r); F" << b << "i = fmaf(x, F" << b << "r, F" << b << "i); F" << b << "r = nr; }\n";
+        }
+        first = false;
+      }
+    }
+    // y = x times bit b's factor (conj: the z = -1 one); names of y's parts
+    auto times = [&](const std::string& xr, const std::string& xi, int b, bool conj,
+                     const std::string& yr, const std::string& yi) {
+      if (simple[b]) {
+        const std::string sb = "s" + std::to_string(b);
+        const std::string sp = conj ? "(-" + sb + ")" : sb;
+        o << "    const float " << yr << " = fmaf(-" << sp << ", " << xi << ", " << xr << "), " << yi
+          << " = fmaf(" << sp << ", " << xr << ", " << xi << ");\n";
+      } else {
+        const std::string fr = "F" + std::to_string(b) + "r", fi0 = "F" + std::to_string(b) + "i";
+        const std::string fi = conj ? "(-" + fi0 + ")" : fi0;
+        o << "    const float " << yr << " = fmaf(" << xr << ", " << fr << ", -(" << xi << " * " << fi
+          << ")), " << yi << " = fmaf(" << xr << ", " << fi << ", " << xi << " * " << fr << ");\n";
+      }
+    };
+    auto apply = [&](int u, const std::string& er, const std::string& ei) {
+      for (const char* st : {"a", "l"}) {
+        if (st[0] == 'l' && !bwd) break;
+        o << "    { const float xr = " << st << ".r[" << u << "], xi = " << st << ".i[" << u << "]; "
+          << st << ".r[" << u << "] = fmaf(xr, " << er << ", -(xi * " << ei << ")); " << st
+          << ".i[" << u << "] = fmaf(xr, " << ei << ", xi * " << er << "); }\n";
+      }
+    };
+    if (!B) {  // thread bits only: one factor for every amplitude
+      for (int u = 0; u < N; ++u) apply(u, "Tr", "Ti");
+    } else {
+      int top = 31 - __builtin_clz(B);
+      const uint32_t Bp = B & ~(1u << top);
+      // D over the bits of Bp: entry v (a subset of Bp) as Dr<v>, Di<v>
+      std::map<uint32_t, std::pair<std::string, std::string>> D;
+      if (haveT) D[0] = {"Tr", "Ti"};
+      for (int b = 0; b < R; ++b) {
+        if (!((Bp >> b) & 1u)) continue;
+        std::map<uint32_t, std::pair<std::string, std::string>> E;
+        if (D.empty()) {  // the first factor alone
+          const std::string n0 = "D" + std::to_string(1u << b);
+          if (simple[b]) {
+            o << "    const float D0r = 1.f, D0i = s" << b << ", " << n0 << "r = 1.f, " << n0
+              << "i = -s" << b << ";\n";
+          } else {
+            o << "    const float D0r = F" << b << "r, D0i = F" << b << "i, " << n0 << "r = F" << b
+              << "r, " << n0 << "i = -F" << b << "i;\n";
+          }
+          E[0] = {"D0r", "D0i"};
+          E[1u << b] = {n0 + "r", n0 + "i"};
+        } else {
+          for (const auto& kv : D) {
+            const uint32_t v = kv.first, v1 = v | (1u << b);
+            const std::string a0 = "D" + std::to_string(v) + "_" + std::to_string(b);
+            const std::string a1 = "D" + std::to_string(v1) + "_" + std::to_string(b);
+            times(kv.second.first, kv.second.second, b, false, a0 + "r", a0 + "i");
+            times(kv.second.first, kv.second.second, b, true, a1 + "r", a1 + "i");
+            E[v] = {a0 + "r", a0 + "i"};
+            E[v1] = {a1 + "r", a1 + "i"};
+          }
+        }
+        D.swap(E);
+      }
+      if (D.empty()) {  // the top bit's factor alone
+        if (simple[top]) {
+          const std::string sb = "s" + std::to_string(top);
+          for (int u = 0; u < N; ++u) {
+            if ((u >> top) & 1) continue;
+            for (const char* st : {"a", "l"}) {
+              if (st[0] == 'l' && !bwd) break;
+              for (int h = 0; h < 2; ++h) {
+                const int uu = u | (h << top);
+                const std::string sp = h ? "(-" + sb + ")" : sb;
+                o << "    { const float xr = " << st << ".r[" << uu << "], xi = " << st << ".i[" << uu
+                  << "]; " << st << ".r[" << uu << "] = fmaf(-" << sp << ", xi, xr); " << st << ".i["
+                  << uu << "] = fmaf(" << sp << ", xr, xi); }\n";
+              }
+            }
+          }
+        } else {
+          const std::string fr = "F" + std::to_string(top) + "r", fi = "F" + std::to_string(top) + "i";
+          for (int u = 0; u < N; ++u) {
+            if ((u >> top) & 1) continue;
+            apply(u, fr, fi);
+            apply(u | (1 << top), fr, "(-" + fi + ")");
+          }
+        }
+      } else {
+        for (const auto& kv : D) {
+          const uint32_t v = kv.first;
+          const std::string e0 = "E" + std::to_string(v) + "a", e1 = "E" + std::to_string(v) + "b";
+          times(kv.second.first, kv.second.second, top, false, e0 + "r", e0 + "i");
+          times(kv.second.first, kv.second.second, top, true, e1 + "r", e1 + "i");
+          for (int u = 0; u < N; ++u) {
+            if (((u >> top) & 1) || (uint32_t)(u & Bp) != v) continue;
+            apply(u, e0 + "r", e0 + "i");
+            apply(u | (1 << top), e1 + "r", e1 + "i");
+          }
+        }
+      }
+    }
+    bool resc = false;
+    for (int i = 0; i < L; ++i)
+      if ((m + i) % kBlock == kBlock - 1 || m + i == nrot - 1) resc = true;
+    m += L;
+    if (resc) {
+      o << "    rescale<R>(a, bp);";
+      if (bwd) o << " rescale<R>(l, bp);";
+      o << " bp = 1.f;\n";
+    }
+    o << "    gate_boundary(w);\n  }\n";
   };
   for (int pc = 0; pc < n_ins; ++pc) {
     const uint32_t w0 = ins[2 * pc], arg = ins[2 * pc + 1];
@@ -749,6 +1078,23 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       }
       default: {
         if (skip && (*skip)[arg]) break;  // a head rotation: run by the product start
+        if (fuse && fusable_rz(p, w0, arg)) {
+          std::vector<RzItem> run;
+          int end = pc;
+          for (; end < n_ins; ++end) {
+            const uint32_t we = ins[2 * end], occ = ins[2 * end + 1];
+            const int ope = we & 31;
+            if (ope != OP_RX && ope != OP_RY && ope != OP_RZ) break;
+            if (skip && (*skip)[occ]) continue;  // a head rotation: not run here
+            if (!fusable_rz(p, we, occ)) break;
+            run.push_back({(int)occ, (int)((ins[2 * end] >> 5) & 31), (int)(ins[2 * end] >> 16) - 1});
+          }
+          if (fused_cheaper(run)) {
+            emit_rz_run(run);
+            pc = end - 1;
+            break;
+          }
+        }
         const bool reg = pa < R;
         const char* kind = op == OP_RX ? "rx" : op == OP_RY ? "ry" : "rz";
         if (batched && slot >= 0) {  // the slot's position is taken by another slot
