@@ -806,137 +806,98 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
       }
     }
     for (int i = 0; i < L; ++i) o << "    bp *= tc" << i << ".y;\n";
-    // the thread part: the product of 1 + i sg z over the thread-bit RZs
+    // The diagonal in double precision (every entry rounded to float once:
+    // its rounding is shared by the amplitudes it multiplies, so a float
+    // product's error, about sqrt(L) ulp, would shift the norm coherently).
+    // The thread part: the product of 1 + i sg z over the thread-bit RZs.
     bool haveT = false;
     for (int i = 0; i < L; ++i) {
       if (run[i].bit < R) continue;
-      const std::string x = std::string(sg) + "z" + std::to_string(i);
+      const std::string x = std::string(sg) + "(double)z" + std::to_string(i);
       if (!haveT) {
-        o << "    float Tr = 1.f, Ti = " << x << ";\n";
+        o << "    double Tr = 1.0, Ti = " << x << ";\n";
         haveT = true;
       } else {
-        o << "    { const float x = " << x << ", nr = fmaf(-x, Ti, Tr); Ti = fmaf(x, Tr, Ti); Tr = nr; }\n";
+        o << "    { const double x = " << x << ", nr = fma(-x, Ti, Tr); Ti = fma(x, Tr, Ti); Tr = nr; }\n";
       }
     }
-    // per register bit: the factor for z = +1 (that for z = -1 is its conjugate)
+    // per register bit: the factor for z = +1, 1 + i s (one RZ) or F (a
+    // product); the factor for z = -1 is its conjugate
+    std::vector<int> bits;
     std::map<int, int> cnt;
     for (int i = 0; i < L; ++i)
-      if (run[i].bit < R) ++cnt[run[i].bit];
-    std::map<int, bool> simple;
-    for (const auto& kv : cnt) {
-      const int b = kv.first;
-      simple[b] = kv.second == 1;
+      if (run[i].bit < R && cnt[run[i].bit]++ == 0) bits.push_back(run[i].bit);
+    std::sort(bits.begin(), bits.end());
+    for (int b : bits) {
       bool first = true;
       for (int i = 0; i < L; ++i) {
         if (run[i].bit != b) continue;
-        const std::string x = std::string(sg) + "t" + std::to_string(i);
-        if (simple[b]) {
-          o << "    const float s" << b << " = " << x << ";\n";
-        } else if (first) {
-          o << "    float F" << b << "r = 1.f, F" << b << "i = " << x << ";\n";
-        } else {
-          o << "    { const float x = " << x << ", nr = fmaf(-x, F" << b << "i, F" << b
-            << "r); F" << b << "i = fmaf(x, F" << b << "r, F" << b << "i); F" << b << "r = nr; }\n";
-        }
+        const std::string x = std::string(sg) + "(double)t" + std::to_string(i);
+        if (cnt[b] == 1)
+          o << "    const double s" << b << " = " << x << ";\n";
+        else if (first)
+          o << "    double F" << b << "r = 1.0, F" << b << "i = " << x << ";\n";
+        else
+          o << "    { const double x = " << x << ", nr = fma(-x, F" << b << "i, F" << b << "r); F"
+            << b << "i = fma(x, F" << b << "r, F" << b << "i); F" << b << "r = nr; }\n";
         first = false;
       }
     }
-    // y = x times bit b's factor (conj: the z = -1 one); names of y's parts
-    auto times = [&](const std::string& xr, const std::string& xi, int b, bool conj,
-                     const std::string& yr, const std::string& yi) {
-      if (simple[b]) {
-        const std::string sb = "s" + std::to_string(b);
-        const std::string sp = conj ? "(-" + sb + ")" : sb;
-        o << "    const float " << yr << " = fmaf(-" << sp << ", " << xi << ", " << xr << "), " << yi
-          << " = fmaf(" << sp << ", " << xr << ", " << xi << ");\n";
+    // y = x times bit b's factor for bit value h
+    auto times = [&](const std::string& x, int b, int h, const std::string& y) {
+      if (cnt[b] == 1) {
+        const std::string sp = h ? "(-s" + std::to_string(b) + ")" : "s" + std::to_string(b);
+        o << "const double " << y << "r = fma(-" << sp << ", " << x << "i, " << x << "r), " << y
+          << "i = fma(" << sp << ", " << x << "r, " << x << "i);";
       } else {
-        const std::string fr = "F" + std::to_string(b) + "r", fi0 = "F" + std::to_string(b) + "i";
-        const std::string fi = conj ? "(-" + fi0 + ")" : fi0;
-        o << "    const float " << yr << " = fmaf(" << xr << ", " << fr << ", -(" << xi << " * " << fi
-          << ")), " << yi << " = fmaf(" << xr << ", " << fi << ", " << xi << " * " << fr << ");\n";
+        const std::string fr = "F" + std::to_string(b) + "r";
+        const std::string fi = h ? "(-F" + std::to_string(b) + "i)" : "F" + std::to_string(b) + "i";
+        o << "const double " << y << "r = fma(" << x << "r, " << fr << ", -(" << x << "i * " << fi
+          << ")), " << y << "i = fma(" << x << "r, " << fi << ", " << x << "i * " << fr << ");";
       }
     };
-    auto apply = [&](int u, const std::string& er, const std::string& ei) {
-      for (const char* st : {"a", "l"}) {
-        if (st[0] == 'l' && !bwd) break;
-        o << "    { const float xr = " << st << ".r[" << u << "], xi = " << st << ".i[" << u << "]; "
-          << st << ".r[" << u << "] = fmaf(xr, " << er << ", -(xi * " << ei << ")); " << st
-          << ".i[" << u << "] = fmaf(xr, " << ei << ", xi * " << er << "); }\n";
-      }
+    // the factor itself (the product's first factor when there is no thread part)
+    auto first_factor = [&](int b, int h, const std::string& y) {
+      if (cnt[b] == 1)
+        o << "const double " << y << "r = 1.0, " << y << "i = " << (h ? "-" : "") << "s" << b << ";";
+      else
+        o << "const double " << y << "r = F" << b << "r, " << y << "i = " << (h ? "-" : "") << "F" << b
+          << "i;";
     };
-    if (!B) {  // thread bits only: one factor for every amplitude
-      for (int u = 0; u < N; ++u) apply(u, "Tr", "Ti");
-    } else {
-      int top = 31 - __builtin_clz(B);
-      const uint32_t Bp = B & ~(1u << top);
-      // D over the bits of Bp: entry v (a subset of Bp) as Dr<v>, Di<v>
-      std::map<uint32_t, std::pair<std::string, std::string>> D;
-      if (haveT) D[0] = {"Tr", "Ti"};
-      for (int b = 0; b < R; ++b) {
-        if (!((Bp >> b) & 1u)) continue;
-        std::map<uint32_t, std::pair<std::string, std::string>> E;
-        if (D.empty()) {  // the first factor alone
-          const std::string n0 = "D" + std::to_string(1u << b);
-          if (simple[b]) {
-            o << "    const float D0r = 1.f, D0i = s" << b << ", " << n0 << "r = 1.f, " << n0
-              << "i = -s" << b << ";\n";
-          } else {
-            o << "    const float D0r = F" << b << "r, D0i = F" << b << "i, " << n0 << "r = F" << b
-              << "r, " << n0 << "i = -F" << b << "i;\n";
-          }
-          E[0] = {"D0r", "D0i"};
-          E[1u << b] = {n0 + "r", n0 + "i"};
-        } else {
-          for (const auto& kv : D) {
-            const uint32_t v = kv.first, v1 = v | (1u << b);
-            const std::string a0 = "D" + std::to_string(v) + "_" + std::to_string(b);
-            const std::string a1 = "D" + std::to_string(v1) + "_" + std::to_string(b);
-            times(kv.second.first, kv.second.second, b, false, a0 + "r", a0 + "i");
-            times(kv.second.first, kv.second.second, b, true, a1 + "r", a1 + "i");
-            E[v] = {a0 + "r", a0 + "i"};
-            E[v1] = {a1 + "r", a1 + "i"};
-          }
-        }
-        D.swap(E);
-      }
-      if (D.empty()) {  // the top bit's factor alone
-        if (simple[top]) {
-          const std::string sb = "s" + std::to_string(top);
-          for (int u = 0; u < N; ++u) {
-            if ((u >> top) & 1) continue;
-            for (const char* st : {"a", "l"}) {
-              if (st[0] == 'l' && !bwd) break;
-              for (int h = 0; h < 2; ++h) {
-                const int uu = u | (h << top);
-                const std::string sp = h ? "(-" + sb + ")" : sb;
-                o << "    { const float xr = " << st << ".r[" << uu << "], xi = " << st << ".i[" << uu
-                  << "]; " << st << ".r[" << uu << "] = fmaf(-" << sp << ", xi, xr); " << st << ".i["
-                  << uu << "] = fmaf(" << sp << ", xr, xi); }\n";
-              }
+    auto apply = [&](int u, const char* st) {
+      o << "      { const float xr = " << st << ".r[" << u << "], xi = " << st << ".i[" << u << "]; "
+        << st << ".r[" << u << "] = fmaf(xr, er, -(xi * ei)); " << st << ".i[" << u
+        << "] = fmaf(xr, ei, xi * er); }\n";
+    };
+    // depth-first over the register bits: one live product per level; at a
+    // leaf (a value of every bit) the entry goes to float and multiplies the
+    // amplitudes with those bits
+    std::function<void(size_t, uint32_t, const std::string&)> walk =
+        [&](size_t d, uint32_t val, const std::string& x) {
+          if (d == bits.size()) {
+            o << "    { const float er = (float)" << x << "r, ei = (float)" << x << "i;\n";
+            uint32_t Bm = 0;
+            for (int b : bits) Bm |= 1u << b;
+            for (int u = 0; u < N; ++u) {
+              if (((uint32_t)u & Bm) != val) continue;
+              apply(u, "a");
+              if (bwd) apply(u, "l");
             }
+            o << "    }\n";
+            return;
           }
-        } else {
-          const std::string fr = "F" + std::to_string(top) + "r", fi = "F" + std::to_string(top) + "i";
-          for (int u = 0; u < N; ++u) {
-            if ((u >> top) & 1) continue;
-            apply(u, fr, fi);
-            apply(u | (1 << top), fr, "(-" + fi + ")");
+          const int b = bits[d];
+          for (int h = 0; h < 2; ++h) {
+            const std::string y = "N" + std::to_string(d) + std::to_string(h);
+            o << "    { ";
+            if (x.empty()) first_factor(b, h, y);
+            else times(x, b, h, y);
+            o << "\n";
+            walk(d + 1, val | ((uint32_t)h << b), y);
+            o << "    }\n";
           }
-        }
-      } else {
-        for (const auto& kv : D) {
-          const uint32_t v = kv.first;
-          const std::string e0 = "E" + std::to_string(v) + "a", e1 = "E" + std::to_string(v) + "b";
-          times(kv.second.first, kv.second.second, top, false, e0 + "r", e0 + "i");
-          times(kv.second.first, kv.second.second, top, true, e1 + "r", e1 + "i");
-          for (int u = 0; u < N; ++u) {
-            if (((u >> top) & 1) || (uint32_t)(u & Bp) != v) continue;
-            apply(u, e0 + "r", e0 + "i");
-            apply(u | (1 << top), e1 + "r", e1 + "i");
-          }
-        }
-      }
-    }
+        };
+    walk(0, 0, haveT ? "T" : "");
     bool resc = false;
     for (int i = 0; i < L; ++i)
       if ((m + i) % kBlock == kBlock - 1 || m + i == nrot - 1) resc = true;

@@ -18,6 +18,7 @@
 #include <cmath>
 #include <cstring>
 #include <map>
+#include <set>
 
 #include "vqc.h"
 #include "vqc_internal.h"
@@ -118,6 +119,57 @@ int emit_exchange(const Mapping& a, const Mapping& b, int k, int R, std::vector<
 void emit(std::vector<uint32_t>& out, uint32_t op, int a, int b, int slot, uint32_t arg) {
   out.push_back(ins_word0(op, (uint32_t)a, (uint32_t)b, slot));
   out.push_back(arg);
+}
+
+// A list schedule of `seq` that holds back RZs with variable angles until no
+// other gate is ready, so that they come in runs over many qubits (the
+// generated kernels with 8 or more amplitudes per thread apply such a run as
+// one diagonal: a Rot layer becomes the RZs of every qubit, the RYs, then the
+// other RZs).  Each line keeps its order of gates; among ready gates the one
+// earlier in `seq` goes first, so the gates that need a register bit keep
+// their order.
+std::vector<Prim> lazy_diagonals(const std::vector<Prim>& seq, const Plan& plan) {
+  const int n = (int)seq.size();
+  std::vector<int> npred(n, 0);
+  std::vector<std::vector<int>> succ(n);
+  int last[kMaxQubits];
+  for (int q = 0; q < kMaxQubits; ++q) last[q] = -1;
+  for (int i = 0; i < n; ++i) {
+    const int lines[2] = {seq[i].q0, two_qubit(seq[i]) ? seq[i].q1 : -1};
+    for (int q : lines) {
+      if (q < 0) continue;
+      if (last[q] >= 0) {
+        succ[last[q]].push_back(i);
+        ++npred[i];
+      }
+      last[q] = i;
+    }
+  }
+  auto held = [&](int i) {
+    return seq[i].kind == P_RZ && seq[i].occ >= 0 && plan.occ_src[seq[i].occ] != VQC_SRC_CONST;
+  };
+  std::set<int> other, rz;
+  for (int i = 0; i < n; ++i)
+    if (!npred[i]) (held(i) ? rz : other).insert(i);
+  std::vector<Prim> out;
+  out.reserve(n);
+  auto take = [&](int i) {
+    out.push_back(seq[i]);
+    for (int s : succ[i])
+      if (--npred[s] == 0) (held(s) ? rz : other).insert(s);
+  };
+  while ((int)out.size() < n) {
+    if (!other.empty()) {
+      const int i = *other.begin();
+      other.erase(other.begin());
+      take(i);
+    } else {
+      const std::vector<int> run(rz.begin(), rz.end());
+      rz.clear();
+      for (int i : run) take(i);
+    }
+  }
+  return out;
 }
 
 // One register-level sweep over `seq` (already in execution order) starting
@@ -412,7 +464,8 @@ int plan_stream(Plan& plan, const std::vector<StreamGroup>& groups,
       slots.push_back(s);
       return id;
     };
-    int rc = plan_sweep(grp.prims, nq, k, R, m, out, plan.cols, exchanges, slot_of, msg);
+    const std::vector<Prim> seq = R >= 3 ? lazy_diagonals(grp.prims, plan) : grp.prims;
+    int rc = plan_sweep(seq, nq, k, R, m, out, plan.cols, exchanges, slot_of, msg);
     if (rc < 0) return rc;
     const bool stores = !(bwd && last);  // the adjoint's last pass ends at psi_0
     if (stores && !(m == io_out)) {
@@ -948,12 +1001,13 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     // Qubits on lane bits 4 and 5 still come to a register bit, by a permlane
     // swap (one instruction per two values).
     plan.lanes = (lane_gates && plan.R <= 2) ? std::min(plan.t, 4) : 0;
-    rc = plan_sweep(plan.prims, nq, plan.k, plan.R, m, plan.fwd, plan.cols, plan.fwd_exchanges,
-                    global_slot, msg, plan.lanes);
+    const bool lazy = plan.R >= 3 && plan.lanes == 0;
+    rc = plan_sweep(lazy ? lazy_diagonals(plan.prims, plan) : plan.prims, nq, plan.k, plan.R, m,
+                    plan.fwd, plan.cols, plan.fwd_exchanges, global_slot, msg, plan.lanes);
     if (rc < 0) return rc;
     plan.end_off = append_map(m, plan.maps);
-    rc = plan_sweep(rev, nq, plan.k, plan.R, m, plan.bwd, plan.cols, plan.bwd_exchanges,
-                    global_slot, msg, plan.lanes);
+    rc = plan_sweep(lazy ? lazy_diagonals(rev, plan) : rev, nq, plan.k, plan.R, m, plan.bwd,
+                    plan.cols, plan.bwd_exchanges, global_slot, msg, plan.lanes);
     if (rc < 0) return rc;
     plan.bwd_end_off = append_map(m, plan.maps);
     // LDS: exchange buffer | angle table [occ][S] | gradient accumulators [slot][G]

@@ -4,7 +4,8 @@ state after the heads, its last adjoint pass contracts lambda against the
 heads' states per tile, and a last kernel sums those partials over the tiles
 and walks each head back for its rotations' gradients.  Checked against the
 oracle, which runs every gate, and against the separate forward / backward
-calls (which run the heads as gates): heads of every kind and length, heads
+calls (which run the heads as gates; both sides against the oracle, and
+within half its E bar of each other): heads of every kind and length, heads
 that end after other qubits' entanglers, constant and affine angles,
 parameters shared between heads and later gates, shared parameters over the
 batch, circuits that are heads only, general gates, odd batches (two halves on
@@ -44,8 +45,17 @@ def run_and_check(torch, ops, n, P, F, B, loss, seed, shared=False, rows=None):
     g2 = loss_grad(loss, E2, yt)
     dp2, dx2 = c.backward(p, x, g2, ws)
     torch.cuda.synchronize()
-    assert np.max(np.abs(E2.cpu().numpy() - E)) <= 2e-6
-    assert np.max(np.abs(g2.cpu().numpy() - g)) <= 2e-6
+    if not shared:
+        r = list(range(B)) if rows is None else rows
+        Er = oracle.forward(ops, n, params[r], inputs[r])
+        note(f"E errors against the oracle: step {np.max(np.abs(E[r] - Er)):.2e}, separate calls "
+             f"{np.max(np.abs(E2.cpu().numpy()[r] - Er)):.2e}")
+        check_E(E2.cpu().numpy()[r], Er)
+    # two plans rounded independently (the step's has no head rotations, and
+    # its runs of RZs form differently): each is held to the oracle's bar
+    # above, and they agree within half of it
+    assert np.max(np.abs(E2.cpu().numpy() - E)) <= 5e-6
+    assert np.max(np.abs(g2.cpu().numpy() - g)) <= 5e-6
     if shared:
         # one parameter vector: against the oracle's gradient summed over the batch
         rows_p = np.repeat(params[:1], B, axis=0)
