@@ -575,8 +575,9 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   // (not in the kernels with gates on lane bits: there the lane swaps, which
   // would have to resolve the frame first, follow most CNOTs)
   const bool frames = tan && p.lanes == 0;
-  // runs of RZs on different bits become one diagonal (emit_rz_run below)
-  const bool fuse = frames && S == 1 && R >= 3;
+  // runs of RZs on different bits become one diagonal (emit_rz_run below;
+  // one sample per workgroup, tangent form)
+  const bool fuse = tan && S == 1 && R >= 2;
   std::vector<uint32_t> clustered;
   if (fuse) {
     clustered = cluster_diagonals(p, ins, n_ins);
@@ -715,22 +716,31 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
     const int N = 1 << R, L = (int)run.size();
     const char* sg = bwd ? "" : "-";  // factor 1 + i sg x for z = +1
     o << "  { // " << L << " RZs as one diagonal\n";
-    if (rots[ri] != run[0].occ) o << "#error rotation prefetch out of order\n";
-    for (int i = 0; i < L; ++i) {
-      if (i == 0) {
-        o << "    const float2 tc0 = tcn;";
-        if (bwd) o << " const float gm0 = gmn;";
-      } else {
-        o << "    const float2 tc" << i << " = w.tab[" << run[i].occ << "];";
-        if (bwd) o << " const float gm" << i << " = gmul[" << run[i].occ << "];";
+    if (S == 1 && R <= 2) {  // the tables in registers (table_row)
+      for (int i = 0; i < L; ++i) {
+        const int occ = run[i].occ;
+        o << "    const float2 tc" << i << " = table_entry<" << occ % 64 << ">(T" << occ / 64 << ");";
+        if (bwd) o << " const float gm" << i << " = table_entry<" << occ % 64 << ">(G" << occ / 64 << ");";
+        o << "\n";
       }
-      o << "\n";
-    }
-    ri += L;
-    if (ri < rots.size()) {
-      o << "    tcn = w.tab[" << rots[ri] << "];";
-      if (bwd) o << " gmn = gmul[" << rots[ri] << "];";
-      o << "\n";
+    } else {  // in LDS, the run's first entries read ahead
+      if (rots[ri] != run[0].occ) o << "#error rotation prefetch out of order\n";
+      for (int i = 0; i < L; ++i) {
+        if (i == 0) {
+          o << "    const float2 tc0 = tcn;";
+          if (bwd) o << " const float gm0 = gmn;";
+        } else {
+          o << "    const float2 tc" << i << " = w.tab[" << run[i].occ << "];";
+          if (bwd) o << " const float gm" << i << " = gmul[" << run[i].occ << "];";
+        }
+        o << "\n";
+      }
+      ri += L;
+      if (ri < rots.size()) {
+        o << "    tcn = w.tab[" << rots[ri] << "];";
+        if (bwd) o << " gmn = gmul[" << rots[ri] << "];";
+        o << "\n";
+      }
     }
     uint32_t B = 0;
     int nt = 0;

@@ -1001,7 +1001,7 @@ int build_plan(const std::vector<HostOp>& ops, int n, int P, int F, int path, in
     // Qubits on lane bits 4 and 5 still come to a register bit, by a permlane
     // swap (one instruction per two values).
     plan.lanes = (lane_gates && plan.R <= 2) ? std::min(plan.t, 4) : 0;
-    const bool lazy = plan.R >= 3 && plan.lanes == 0;
+    const bool lazy = plan.R >= 2;
     rc = plan_sweep(lazy ? lazy_diagonals(plan.prims, plan) : plan.prims, nq, plan.k, plan.R, m,
                     plan.fwd, plan.cols, plan.fwd_exchanges, global_slot, msg, plan.lanes);
     if (rc < 0) return rc;
