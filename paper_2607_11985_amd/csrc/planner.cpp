@@ -122,7 +122,8 @@ void emit(std::vector<uint32_t>& out, uint32_t op, int a, int b, int slot, uint3
 }
 
 // A list schedule of `seq` that holds back RZs with variable angles until no
-// other gate is ready, so that they come in runs over many qubits (the
+// other gate is ready, then emits every ready one and those they make ready,
+// so that they come in runs over many qubits (the
 // generated kernels with 8 or more amplitudes per thread apply such a run as
 // one diagonal: a Rot layer becomes the RZs of every qubit, the RYs, then the
 // other RZs).  Each line keeps its order of gates; among ready gates the one
@@ -163,10 +164,12 @@ std::vector<Prim> lazy_diagonals(const std::vector<Prim>& seq, const Plan& plan)
       const int i = *other.begin();
       other.erase(other.begin());
       take(i);
-    } else {
-      const std::vector<int> run(rz.begin(), rz.end());
-      rz.clear();
-      for (int i : run) take(i);
+    } else {  // every ready RZ, and those they make ready (a qubit's next RZ)
+      while (!rz.empty()) {
+        const int i = *rz.begin();
+        rz.erase(rz.begin());
+        take(i);
+      }
     }
   }
   return out;
