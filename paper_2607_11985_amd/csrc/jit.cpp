@@ -685,9 +685,12 @@ void emit_schedule(std::ostringstream& o, const Plan& p, const uint32_t* ins, in
   // adjoint takes every gradient of the run from Im(conj(lambda) psi), which
   // no diagonal gate changes (the tangent form scales it by 1 / cos^2 per
   // gate, which the block factor bp carries), then multiplies psi and lambda
-  // by the inverse diagonal once.  D is formed over the run's register bits
-  // but the highest (one product per value of the others) and applied in
-  // two halves, so that at most 8 complex values of it are live.
+  // by the inverse diagonal once.  D's entries (one per value of the run's
+  // register bits, times the thread-bit factor) are formed in double,
+  // depth first over those bits so that one product per level is live, and
+  // each goes to float once.  A run is fused when an instruction count of
+  // both ways says so, with a tenth of margin for the fused code's
+  // registers.
   struct RzItem {
     int occ, bit, slot;
   };
